@@ -1,0 +1,577 @@
+/*
+ * ssref.c -- plain CPU oracle for the fused LLM sampling pipeline.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the tests, the smoke check and the CPU-baseline leg of
+ * the benchmark do.  It shares no code, header, table or constant with the
+ * HIP implementation.
+ *
+ * What it computes (SonicSampler, arXiv 2607.20475):
+ *   - the logit-processing prologue in the paper's order (Alg. 8 "Stage 1",
+ *     prologue steps; equations of Appendix C.1): grammar bit-mask,
+ *     multiplicative repetition penalty, frequency and presence penalties,
+ *     logit bias.  Each step is one IEEE float32 operation per element, as a
+ *     float32 kernel computes it (build with -ffp-contract=off);
+ *   - a full sort of the valid tokens (value descending, index ascending:
+ *     the paper's index-complement packing in Section 3.4 makes the lower
+ *     index win ties);
+ *   - truncation in Alg. 11 order (top-k, then top-p on the top-k-renormalised
+ *     distribution, then min-p in the logit domain, eq. "min_p_trick",
+ *     Appendix C.2), temperature entering only the probabilities;
+ *   - categorical selection by inverse CDF over the kept prefix, with a
+ *     uniform from Philox4x32-10 keyed by (seed, request, position);
+ *   - speculative verification (Section 3.1 "Speculative Verification",
+ *     Appendix C.4): accept when u*q(d) <= p(d), else resample from
+ *     normalize(max(0, p - q)); a bonus token after full acceptance.
+ *
+ * Probabilities, sums and every decision taken on them are in double
+ * precision.  Readings of points the paper leaves open are listed in the
+ * design notes; the ones that change results are repeated where they apply.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* Per-request indicator bits: the paper's bit-level encoding table (Section 3.5). */
+enum {
+  R_GRAMMAR = 0x001, R_REP = 0x002, R_FREQ = 0x004, R_PRES = 0x008,
+  R_BIAS = 0x010, R_TEMP = 0x020, R_GREEDY = 0x040, R_TOPK = 0x080,
+  R_TOPP = 0x100, R_MINP = 0x200
+};
+/* Per-row result flags. */
+enum { RF_EMPTY = 1, RF_KCAP = 8 };
+
+/* ------------------------------------------------------------------------- */
+/* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11), written from its        */
+/* published definition: 10 rounds of two 32x32->64 multiplies with a Weyl    */
+/* key schedule.                                                              */
+/* ------------------------------------------------------------------------- */
+void ssref_philox4x32_10(const uint32_t ctr_in[4], const uint32_t key_in[2], uint32_t out[4]) {
+  uint32_t c0 = ctr_in[0], c1 = ctr_in[1], c2 = ctr_in[2], c3 = ctr_in[3];
+  uint32_t k0 = key_in[0], k1 = key_in[1];
+  for (int round = 0; round < 10; ++round) {
+    uint64_t p0 = (uint64_t)0xD2511F53u * (uint64_t)c0;
+    uint64_t p1 = (uint64_t)0xCD9E8D57u * (uint64_t)c2;
+    uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    uint32_t n0 = hi1 ^ c1 ^ k0;
+    uint32_t n1 = lo1;
+    uint32_t n2 = hi0 ^ c3 ^ k1;
+    uint32_t n3 = lo0;
+    c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* Uniform in (0,1) for (seed, request, position); `word` 0 drives token draws,
+ * word 1 the acceptance test.  u = (w + 1/2) * 2^-32, exact in double. */
+double ssref_uniform(uint64_t seed, uint32_t request, int64_t position, int word) {
+  uint32_t ctr[4] = {request, (uint32_t)((uint64_t)position & 0xFFFFFFFFu),
+                     (uint32_t)((uint64_t)position >> 32), 0u};
+  uint32_t key[2] = {(uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32)};
+  uint32_t o[4];
+  ssref_philox4x32_10(ctr, key, o);
+  return ((double)o[word & 3] + 0.5) * (1.0 / 4294967296.0);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Logit load: bf16 widens exactly to float32.  NaN -> -inf, -0 -> +0.         */
+/* ------------------------------------------------------------------------- */
+static float load_logit(const void *x, int dtype, int64_t i) {
+  float v;
+  if (dtype == 1) {
+    uint32_t u = ((uint32_t)((const uint16_t *)x)[i]) << 16;
+    memcpy(&v, &u, 4);
+  } else {
+    v = ((const float *)x)[i];
+  }
+  if (isnan(v)) return -INFINITY;
+  if (v == 0.0f) return 0.0f;
+  return v;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Prologue for one row (Alg. 8 prologue order; Appendix C.1 equations).       */
+/*   hist/nhist  : decoded token ids so far (multiplicity = count c_i)         */
+/*   extra/nextra: further decoded ids (accepted drafts during verification)   */
+/*   bias        : (id, value) entries, summed per id in list order            */
+/*   mask_row    : allow bits, bit (i & 31) of word (i >> 5); NULL = no mask    */
+/* ------------------------------------------------------------------------- */
+void ssref_process_row(const void *x, int dtype, int V, uint32_t mode,
+                       float rep, float freq, float pres,
+                       const int32_t *hist, int nhist, const int32_t *extra, int nextra,
+                       const int32_t *bias_ids, const float *bias_vals, int nbias,
+                       const uint32_t *mask_row, float *y) {
+  for (int i = 0; i < V; ++i) y[i] = load_logit(x, dtype, i);
+
+  /* Grammar bit-masking: x_i <- -inf where m_i = 0. */
+  if ((mode & R_GRAMMAR) && mask_row) {
+    for (int i = 0; i < V; ++i)
+      if (((mask_row[i >> 5] >> (i & 31)) & 1u) == 0u) y[i] = -INFINITY;
+  }
+
+  /* Repetition penalties: c_i = occurrences of i in the decoded sequence. */
+  if (mode & (R_REP | R_FREQ | R_PRES)) {
+    int32_t *c = (int32_t *)calloc((size_t)V, sizeof(int32_t));
+    for (int h = 0; h < nhist; ++h)
+      if (hist[h] >= 0 && hist[h] < V) c[hist[h]]++;
+    for (int h = 0; h < nextra; ++h)
+      if (extra[h] >= 0 && extra[h] < V) c[extra[h]]++;
+    for (int i = 0; i < V; ++i) {
+      if (c[i] == 0) continue;
+      float v = y[i];
+      if (mode & R_REP) v = (v > 0.0f) ? v / rep : v * rep;   /* multiplicative */
+      if (mode & R_FREQ) { float t = freq * (float)c[i]; v = v - t; }  /* - beta*c_i */
+      if (mode & R_PRES) v = v - pres;                         /* - gamma*1[c_i>0] */
+      y[i] = v;
+    }
+    free(c);
+  }
+
+  /* Logit bias: x_i <- x_i + b_i, b_i the float32 sum of the row's entries for i. */
+  if ((mode & R_BIAS) && nbias > 0) {
+    float *b = (float *)calloc((size_t)V, sizeof(float));
+    unsigned char *has = (unsigned char *)calloc((size_t)V, 1);
+    for (int e = 0; e < nbias; ++e) {
+      int id = bias_ids[e];
+      if (id < 0 || id >= V) continue;
+      b[id] = b[id] + bias_vals[e];
+      has[id] = 1;
+    }
+    for (int i = 0; i < V; ++i)
+      if (has[i]) y[i] = y[i] + b[i];
+    free(b);
+    free(has);
+  }
+}
+
+/* ------------------------------------------------------------------------- */
+/* Canonical order: valid tokens (y > -inf) by value descending, then index    */
+/* ascending.  A full sort; the comparator is a total order.                   */
+/* ------------------------------------------------------------------------- */
+typedef struct { float y; int32_t i; } vi_t;
+
+static int cmp_vi(const void *a, const void *b) {
+  const vi_t *p = (const vi_t *)a, *q = (const vi_t *)b;
+  if (p->y > q->y) return -1;
+  if (p->y < q->y) return 1;
+  return (p->i < q->i) ? -1 : (p->i > q->i);
+}
+
+int ssref_order(const float *y, int V, int32_t *order) {
+  vi_t *a = (vi_t *)malloc(sizeof(vi_t) * (size_t)(V > 0 ? V : 1));
+  int n = 0;
+  for (int i = 0; i < V; ++i)
+    if (y[i] > -INFINITY) { a[n].y = y[i]; a[n].i = i; ++n; }
+  qsort(a, (size_t)n, sizeof(vi_t), cmp_vi);
+  for (int r = 0; r < n; ++r) order[r] = a[r].i;
+  free(a);
+  return n;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Truncated distribution of one row (Alg. 11 epilogue order).                 */
+/* ------------------------------------------------------------------------- */
+typedef struct {
+  int greedy;      /* 1: greedy row (argmax, no distribution)              */
+  int n_valid;     /* tokens with y > -inf                                 */
+  int n_k, n_p, n_m, n_s;
+  double M, tau, Z_k, Z_s;
+  double margin_p; /* relative distance of the top-p comparisons to p*Z_k  */
+  double margin_m; /* distance of the min-p comparisons to ln(theta)       */
+  int flags;
+} dist_t;
+
+static double weight_of(double yr, double M, double tau) {
+  if (yr == M) return 1.0;               /* also covers y = M = +inf */
+  return exp((yr - M) / tau);
+}
+
+/* Fills w[0..n_s) (unnormalised weights in canonical order) and `d`. */
+static void row_distribution(const float *y, const int32_t *order, int n_valid, uint32_t mode,
+                             float temperature, int32_t top_k, float top_p, float min_p,
+                             int k_cap, double *w, dist_t *d) {
+  memset(d, 0, sizeof(*d));
+  d->n_valid = n_valid;
+  d->margin_p = INFINITY;
+  d->margin_m = INFINITY;
+  if (n_valid == 0) { d->flags |= RF_EMPTY; return; }
+  d->greedy = (mode & R_GREEDY) || ((mode & R_TEMP) && temperature <= 0.0f);
+  d->M = (double)y[order[0]];
+  if (d->greedy) { d->n_k = d->n_p = d->n_m = d->n_s = 1; d->Z_k = d->Z_s = 1.0; w[0] = 1.0; return; }
+  d->tau = (mode & R_TEMP) ? (double)temperature : 1.0;
+
+  /* Top-k: the k highest logits.  Bounded by the candidate capacity k_cap
+   * (the paper's bounded candidate set, Section 3.3). */
+  int64_t k_req = ((mode & R_TOPK) && top_k >= 1) ? (int64_t)top_k : INT64_MAX;
+  int64_t nk = k_req;
+  if (nk > k_cap) nk = k_cap;
+  if (nk > n_valid) nk = n_valid;
+  if ((k_req < n_valid ? k_req : n_valid) > k_cap) d->flags |= RF_KCAP;
+  d->n_k = (int)nk;
+
+  double Zk = 0.0;
+  for (int r = 0; r < d->n_k; ++r) {
+    w[r] = weight_of((double)y[order[r]], d->M, d->tau);
+    Zk += w[r];
+  }
+  d->Z_k = Zk;
+
+  /* Top-p on the top-k renormalised distribution: keep rank r while the mass
+   * strictly before it is below p (minimal prefix with mass >= p). */
+  d->n_p = d->n_k;
+  if ((mode & R_TOPP) && top_p < 1.0f) {
+    double thr = (double)top_p * Zk;
+    double excl = 0.0;
+    int cnt = 0;
+    for (int r = 0; r < d->n_k; ++r) {
+      double m = fabs(excl - thr) / Zk;
+      if (m < d->margin_p) d->margin_p = m;
+      if (excl < thr) cnt = r + 1; else break;
+      excl += w[r];
+    }
+    if (cnt < 1) cnt = 1;
+    d->n_p = cnt;
+  }
+
+  /* Min-p in the logit domain: keep r when (y_r - M)/tau >= ln(theta);
+   * rank 0 is always kept. */
+  d->n_m = d->n_k;
+  if ((mode & R_MINP) && min_p > 0.0f) {
+    double lt = log((double)min_p);
+    int cnt = 1;
+    for (int r = 1; r < d->n_k; ++r) {
+      double yr = (double)y[order[r]];
+      double l = (yr == d->M) ? 0.0 : (yr - d->M) / d->tau;
+      double m = fabs(l - lt);
+      if (m < d->margin_m) d->margin_m = m;
+      if (l >= lt) cnt = r + 1; else break;
+    }
+    d->n_m = cnt;
+  }
+
+  int ns = d->n_k;
+  if (d->n_p < ns) ns = d->n_p;
+  if (d->n_m < ns) ns = d->n_m;
+  d->n_s = ns;
+  double Zs = 0.0;
+  for (int r = 0; r < ns; ++r) Zs += w[r];
+  d->Z_s = Zs;
+}
+
+/* Inverse CDF over weights w[0..n): first r with sum_{s<=r} w_s > u*Z. */
+static int draw_index(const double *w, int n, double Z, double u, double *margin) {
+  double target = u * Z;
+  double cum = 0.0, prev = 0.0;
+  int pick = n - 1;
+  for (int r = 0; r < n; ++r) {
+    prev = cum;
+    cum += w[r];
+    if (cum > target) { pick = r; break; }
+  }
+  if (margin) {
+    double m = fabs(cum - target);
+    if (pick > 0 && fabs(prev - target) < m) m = fabs(prev - target);
+    *margin = (Z > 0.0) ? m / Z : 0.0;
+  }
+  return pick;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Parameter bundle (NULL arrays disable the matching mode bits).              */
+/* ------------------------------------------------------------------------- */
+typedef struct {
+  int B, V;
+  const uint32_t *mode;
+  const float *temperature, *top_p, *min_p, *rep, *freq, *pres;
+  const int32_t *top_k;
+  const int32_t *hist_off, *hist_ids;
+  const int32_t *bias_off, *bias_ids;
+  const float *bias_vals;
+  const uint32_t *bitmask;
+  int64_t mask_ld;
+  const uint64_t *seed;
+  const int64_t *position;
+  int k_cap;
+} ssref_params;
+
+static uint32_t effective_mode(const ssref_params *p, int b) {
+  uint32_t m = p->mode ? p->mode[b] : 0u;
+  if (!p->temperature) m &= ~(uint32_t)R_TEMP;
+  if (!p->top_k) m &= ~(uint32_t)R_TOPK;
+  if (!p->top_p) m &= ~(uint32_t)R_TOPP;
+  if (!p->min_p) m &= ~(uint32_t)R_MINP;
+  if (!p->rep) m &= ~(uint32_t)R_REP;
+  if (!p->freq) m &= ~(uint32_t)R_FREQ;
+  if (!p->pres) m &= ~(uint32_t)R_PRES;
+  if (!p->hist_off || !p->hist_ids) m &= ~(uint32_t)(R_REP | R_FREQ | R_PRES);
+  if (!p->bias_off || !p->bias_ids || !p->bias_vals) m &= ~(uint32_t)R_BIAS;
+  if (!p->bitmask) m &= ~(uint32_t)R_GRAMMAR;
+  return m;
+}
+
+static float pf(const float *a, int b, float dflt) { return a ? a[b] : dflt; }
+
+static void process_one(const void *x, int dtype, int64_t row_off, const ssref_params *p, int b,
+                        const int32_t *extra, int nextra, int64_t mask_row, float *y) {
+  uint32_t mode = effective_mode(p, b);
+  const int32_t *hist = NULL; int nh = 0;
+  if (mode & (R_REP | R_FREQ | R_PRES)) { hist = p->hist_ids + p->hist_off[b]; nh = p->hist_off[b + 1] - p->hist_off[b]; }
+  const int32_t *bid = NULL; const float *bval = NULL; int nb = 0;
+  if (mode & R_BIAS) { bid = p->bias_ids + p->bias_off[b]; bval = p->bias_vals + p->bias_off[b]; nb = p->bias_off[b + 1] - p->bias_off[b]; }
+  const uint32_t *mrow = (mode & R_GRAMMAR) ? p->bitmask + mask_row * p->mask_ld : NULL;
+  const void *xr = (dtype == 1) ? (const void *)((const uint16_t *)x + row_off)
+                                : (const void *)((const float *)x + row_off);
+  ssref_process_row(xr, dtype, p->V, mode, pf(p->rep, b, 1.0f), pf(p->freq, b, 0.0f),
+                    pf(p->pres, b, 0.0f), hist, nh, extra, nextra, bid, bval, nb, mrow, y);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Batched entry points (OpenMP over rows; rows are independent).              */
+/* ------------------------------------------------------------------------- */
+
+/* Singular-mode sampling.  margin[b]: smallest relative distance of any
+ * data-dependent comparison (draw, top-p, min-p) to its boundary. */
+int ssref_sample(const void *x, int dtype, int64_t ld, const ssref_params *p,
+                 int32_t *out_token, float *out_logprob, int32_t *flags,
+                 double *margin, int32_t *n_kept, int nthreads) {
+  int B = p->B, V = p->V;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+#endif
+  for (int b = 0; b < B; ++b) {
+    float *y = (float *)malloc(sizeof(float) * (size_t)V);
+    int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)V);
+    double *w = (double *)malloc(sizeof(double) * (size_t)(p->k_cap > 0 ? p->k_cap : 1) + 8);
+    process_one(x, dtype, (int64_t)b * ld, p, b, NULL, 0, b, y);
+    int nv = ssref_order(y, V, order);
+    uint32_t mode = effective_mode(p, b);
+    dist_t d;
+    row_distribution(y, order, nv, mode, pf(p->temperature, b, 1.0f), p->top_k ? p->top_k[b] : 0,
+                     pf(p->top_p, b, 1.0f), pf(p->min_p, b, 0.0f), p->k_cap, w, &d);
+    double mg = INFINITY;
+    int tok = -1;
+    float lp = 0.0f;
+    if (nv > 0) {
+      if (d.greedy) {
+        tok = order[0];
+      } else {
+        double u = ssref_uniform(p->seed[b], (uint32_t)b, p->position[b], 0);
+        double md;
+        int r = draw_index(w, d.n_s, d.Z_s, u, &md);
+        tok = order[r];
+        lp = (float)log(w[r] / d.Z_s);
+        mg = md;
+        if (d.margin_p < mg) mg = d.margin_p;
+        if (d.margin_m < mg) mg = d.margin_m;
+      }
+    }
+    out_token[b] = tok;
+    if (out_logprob) out_logprob[b] = lp;
+    if (flags) flags[b] = d.flags;
+    if (margin) margin[b] = mg;
+    if (n_kept) n_kept[b] = d.n_s;
+    free(y); free(order); free(w);
+  }
+  return 0;
+}
+
+/* Materialised processed logits y [B,V] (float32, pre-temperature) and the
+ * final truncated distribution P [B,V] (double; zero outside the kept set,
+ * one-hot at the argmax for greedy rows). */
+int ssref_process_logits(const void *x, int dtype, int64_t ld, const ssref_params *p,
+                         float *out_y, double *out_p, int32_t *flags, int nthreads) {
+  int B = p->B, V = p->V;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+#endif
+  for (int b = 0; b < B; ++b) {
+    float *y = out_y ? out_y + (int64_t)b * V : (float *)malloc(sizeof(float) * (size_t)V);
+    int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)V);
+    double *w = (double *)malloc(sizeof(double) * (size_t)(p->k_cap > 0 ? p->k_cap : 1) + 8);
+    process_one(x, dtype, (int64_t)b * ld, p, b, NULL, 0, b, y);
+    int nv = ssref_order(y, V, order);
+    dist_t d;
+    row_distribution(y, order, nv, effective_mode(p, b), pf(p->temperature, b, 1.0f),
+                     p->top_k ? p->top_k[b] : 0, pf(p->top_p, b, 1.0f), pf(p->min_p, b, 0.0f),
+                     p->k_cap, w, &d);
+    if (out_p) {
+      double *P = out_p + (int64_t)b * V;
+      for (int i = 0; i < V; ++i) P[i] = 0.0;
+      if (nv > 0) {
+        if (d.greedy) P[order[0]] = 1.0;
+        else for (int r = 0; r < d.n_s; ++r) P[order[r]] = w[r] / d.Z_s;
+      }
+    }
+    if (flags) flags[b] = d.flags;
+    if (!out_y) free(y);
+    free(order); free(w);
+  }
+  return 0;
+}
+
+/* Standalone top-k on raw values (no prologue): the first min(k_b, k_max,
+ * n_valid) entries of the canonical order, padded with (-inf, -1).
+ * k == NULL means k_b = k_max for every row; k_b <= 0 selects nothing. */
+int ssref_topk(const void *x, int dtype, int B, int V, int64_t ld, const int32_t *k, int k_max,
+               float *out_val, int32_t *out_idx, int nthreads) {
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+#endif
+  for (int b = 0; b < B; ++b) {
+    float *y = (float *)malloc(sizeof(float) * (size_t)V);
+    int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)V);
+    const void *xr = (dtype == 1) ? (const void *)((const uint16_t *)x + (int64_t)b * ld)
+                                  : (const void *)((const float *)x + (int64_t)b * ld);
+    for (int i = 0; i < V; ++i) y[i] = load_logit(xr, dtype, i);
+    int nv = ssref_order(y, V, order);
+    int kb = k ? k[b] : k_max;
+    if (kb < 0) kb = 0;
+    if (kb > k_max) kb = k_max;
+    if (kb > nv) kb = nv;
+    for (int r = 0; r < k_max; ++r) {
+      out_val[(int64_t)b * k_max + r] = (r < kb) ? y[order[r]] : -INFINITY;
+      out_idx[(int64_t)b * k_max + r] = (r < kb) ? order[r] : -1;
+    }
+    free(y); free(order);
+  }
+  return 0;
+}
+
+/* Multistep speculative verification over target rows [B, L+1, V].
+ * Row l (0-based) is the target distribution for draft position l+1; its
+ * penalty history is the request history plus accepted drafts d_1..d_l.
+ * Draft ids outside [0, V) end the draft (q = 0 there: the position then
+ * samples from the target distribution).  Outputs out_tokens [B, L+1]
+ * (-1 padded) and n_acc [B]. */
+int ssref_verify(const void *x, int dtype, int64_t ld_row, const float *draft_probs,
+                 int64_t ld_q, const int32_t *draft_tokens, int L, const ssref_params *p,
+                 int32_t *out_tokens, int32_t *n_acc, int32_t *flags, double *margin, int nthreads) {
+  int B = p->B, V = p->V;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+#endif
+  for (int b = 0; b < B; ++b) {
+    float *y = (float *)malloc(sizeof(float) * (size_t)V);
+    int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)V);
+    int cap = p->k_cap > 0 ? p->k_cap : 1;
+    double *w = (double *)malloc(sizeof(double) * (size_t)cap + 8);
+    double *res = (double *)malloc(sizeof(double) * (size_t)cap + 8);
+    const int32_t *d = draft_tokens + (int64_t)b * L;
+    uint32_t mode = effective_mode(p, b);
+    int fl = 0;
+    double mg = INFINITY;
+    int acc = 0;
+    for (int l = 0; l <= L; ++l) out_tokens[(int64_t)b * (L + 1) + l] = -1;
+
+    for (int l = 1; l <= L + 1; ++l) {
+      int64_t row = (int64_t)b * (L + 1) + (l - 1);
+      process_one(x, dtype, row * ld_row, p, b, d, l - 1, row, y);
+      int nv = ssref_order(y, V, order);
+      dist_t ds;
+      row_distribution(y, order, nv, mode, pf(p->temperature, b, 1.0f), p->top_k ? p->top_k[b] : 0,
+                       pf(p->top_p, b, 1.0f), pf(p->min_p, b, 0.0f), p->k_cap, w, &ds);
+      if (!ds.greedy) {
+        if (ds.margin_p < mg) mg = ds.margin_p;
+        if (ds.margin_m < mg) mg = ds.margin_m;
+      }
+      int64_t pos = p->position[b] + (l - 1);
+      int has_draft = (l <= L) && d[l - 1] >= 0 && d[l - 1] < V;
+      int emit = -1;
+      int accepted = 0;
+      if (nv == 0) {
+        fl |= RF_EMPTY;
+      } else if (ds.greedy) {
+        if (has_draft && d[l - 1] == order[0]) accepted = 1;
+        else emit = order[0];
+      } else if (!has_draft) {
+        double md;
+        int r = draw_index(w, ds.n_s, ds.Z_s, ssref_uniform(p->seed[b], (uint32_t)b, pos, 0), &md);
+        if (md < mg) mg = md;
+        emit = order[r];
+      } else {
+        int dl = d[l - 1];
+        double Pd = 0.0;
+        for (int r = 0; r < ds.n_s; ++r)
+          if (order[r] == dl) { Pd = w[r] / ds.Z_s; break; }
+        double qd = (double)draft_probs[(int64_t)b * L * ld_q + (int64_t)(l - 1) * ld_q + dl];
+        double a = ssref_uniform(p->seed[b], (uint32_t)b, pos, 1);
+        double lhs = a * qd;
+        if (Pd > 0.0) {
+          double den = (Pd > qd) ? Pd : qd;
+          double m = fabs(lhs - Pd) / den;
+          if (m < mg) mg = m;
+        }
+        if (Pd > 0.0 && lhs <= Pd) {
+          accepted = 1;
+        } else {
+          /* residual max(0, P - q) over the kept set, in canonical order */
+          double R = 0.0;
+          for (int r = 0; r < ds.n_s; ++r) {
+            double P = w[r] / ds.Z_s;
+            double qv = (double)draft_probs[(int64_t)b * L * ld_q + (int64_t)(l - 1) * ld_q + order[r]];
+            double v = P - qv;
+            res[r] = v > 0.0 ? v : 0.0;
+            R += res[r];
+          }
+          double u = ssref_uniform(p->seed[b], (uint32_t)b, pos, 0);
+          double md;
+          int r;
+          if (R > 0.0) r = draw_index(res, ds.n_s, R, u, &md);
+          else r = draw_index(w, ds.n_s, ds.Z_s, u, &md);
+          if (md < mg) mg = md;
+          emit = order[r];
+        }
+      }
+      if (accepted) {
+        out_tokens[(int64_t)b * (L + 1) + (l - 1)] = d[l - 1];
+        acc = l;
+        continue;
+      }
+      out_tokens[(int64_t)b * (L + 1) + (l - 1)] = emit;
+      break;
+    }
+    if (acc > L) acc = L;
+    n_acc[b] = acc;
+    if (flags) flags[b] = fl;
+    if (margin) margin[b] = mg;
+    free(y); free(order); free(w); free(res);
+  }
+  return 0;
+}
+
+/* One row's truncated distribution, for pin tests: fills order[0..n_valid),
+ * P[0..n_s) (normalised, canonical order) and the counts/normalisers. */
+int ssref_row_distribution(const float *y, int V, uint32_t mode, float temperature, int32_t top_k,
+                           float top_p, float min_p, int k_cap, int32_t *order, double *P,
+                           int32_t *counts /* n_valid,n_k,n_p,n_m,n_s,greedy,flags */,
+                           double *sums /* M, tau, Z_k, Z_s, margin_p, margin_m */) {
+  int nv = ssref_order(y, V, order);
+  double *w = (double *)malloc(sizeof(double) * (size_t)(k_cap > 0 ? k_cap : 1) + 8);
+  dist_t d;
+  row_distribution(y, order, nv, mode, temperature, top_k, top_p, min_p, k_cap, w, &d);
+  for (int r = 0; r < d.n_s; ++r) P[r] = w[r] / d.Z_s;
+  counts[0] = d.n_valid; counts[1] = d.n_k; counts[2] = d.n_p; counts[3] = d.n_m;
+  counts[4] = d.n_s; counts[5] = d.greedy; counts[6] = d.flags;
+  sums[0] = d.M; sums[1] = d.tau; sums[2] = d.Z_k; sums[3] = d.Z_s;
+  sums[4] = d.margin_p; sums[5] = d.margin_m;
+  free(w);
+  return nv;
+}
+
+/* Inverse-CDF draw over given weights (exposed for pin tests). */
+int ssref_draw(const double *w, int n, double u) {
+  double Z = 0.0;
+  for (int r = 0; r < n; ++r) Z += w[r];
+  return draw_index(w, n, Z, u, NULL);
+}

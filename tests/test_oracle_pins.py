@@ -1,0 +1,408 @@
+"""Pins for the CPU oracle against facts fixed outside it.
+
+Each test checks the oracle against something it does not compute itself:
+published Philox vectors, hand-computed prologue values from the paper's
+equations, library routines (lexsort, argmax, softmax) on cases that reduce
+to them, invariants of the truncation rules, and chi-square tests of the
+sampling and verification distributions.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+from scipy import special, stats
+
+import oracle
+from gen import workloads as W
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _load(name):
+    with open(os.path.join(GOLD, name)) as f:
+        return json.load(f)
+
+
+def _num(v):
+    if isinstance(v, str):
+        return {"-inf": -np.inf, "inf": np.inf, "nan": np.nan, "-0.0": -0.0}[v]
+    return v
+
+
+# --------------------------------------------------------------------------
+# Philox4x32-10 and the uniform mapping
+# --------------------------------------------------------------------------
+def test_philox_published_vectors():
+    for v in _load("philox_kat.json")["vectors"]:
+        out = oracle.philox4x32_10([int(c, 16) for c in v["ctr"]], [int(k, 16) for k in v["key"]])
+        assert out == [int(o, 16) for o in v["out"]]
+
+
+def test_uniform_layout_uses_counter_request_position():
+    # seed 0, request 0, position 0 is the all-zero counter/key vector
+    v0 = _load("philox_kat.json")["vectors"][0]
+    for word in range(4):
+        u = oracle.uniform(0, 0, 0, word)
+        assert u == (int(v0["out"][word], 16) + 0.5) / 2.0**32
+    us = [oracle.uniform(1234, r, p, w) for r in range(8) for p in range(8) for w in range(2)]
+    assert all(0.0 < u < 1.0 for u in us)
+    assert len(set(us)) == len(us)
+
+
+# --------------------------------------------------------------------------
+# Prologue: hand-computed values from the paper's equations
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("case", _load("prologue_cases.json")["cases"], ids=lambda c: c["name"])
+def test_prologue_golden(case):
+    if "x_arange" in case:
+        x = np.arange(case["x_arange"], dtype=np.float32)
+    else:
+        x = np.array([_num(v) for v in case["x"]], np.float32)
+    y = oracle.process_row(
+        x, "f32", case["mode"], rep=case.get("rep", 1.0), freq=case.get("freq", 0.0),
+        pres=case.get("pres", 0.0), hist=case.get("hist", []), bias_ids=case.get("bias_ids", []),
+        bias_vals=case.get("bias_vals", []),
+        mask_row=None if "mask" not in case else np.array(case["mask"], np.uint32))
+    if "y_allowed" in case:
+        allowed = set(case["y_allowed"])
+        for i, v in enumerate(y):
+            assert (v == x[i]) if i in allowed else (v == -np.inf)
+        return
+    want = np.array([_num(v) for v in case["y"]], np.float32)
+    assert np.array_equal(y.view(np.uint32), want.view(np.uint32)), (y, want)
+
+
+def test_prologue_bf16_widening_is_exact():
+    rng = np.random.default_rng(0)
+    f = rng.normal(0, 3, 4096).astype(np.float32)
+    h = W.bf16_bits_from_f32(f)
+    y = oracle.process_row(h, "bf16", 0)
+    assert np.array_equal(y, W.f32_from_bf16_bits(h))
+
+
+# --------------------------------------------------------------------------
+# Ordering and top-k: brute force against numpy's lexsort
+# --------------------------------------------------------------------------
+def _lexsort_topk(y, k):
+    valid = np.nonzero(y > -np.inf)[0]
+    o = valid[np.lexsort((valid, -y[valid].astype(np.float64)))]
+    return o[:k]
+
+
+@pytest.mark.parametrize("kind", ["normal", "ties", "zeros", "bf16_flat", "masked"])
+def test_topk_matches_lexsort(kind):
+    rng = np.random.default_rng(11)
+    B, V, km = 6, 3000, 300
+    if kind == "normal":
+        x = rng.normal(0, 2, (B, V)).astype(np.float32)
+    elif kind == "ties":
+        x = rng.integers(-20, 20, (B, V)).astype(np.float32) / 4
+    elif kind == "zeros":
+        x = np.zeros((B, V), np.float32)
+    elif kind == "bf16_flat":
+        # U(128.6, 128.7) rounds to 129.0 in bf16: an all-ties row (paper, Section 4.4)
+        x = W.f32_from_bf16_bits(W.bf16_bits_from_f32(rng.uniform(128.6, 128.7, (B, V)).astype(np.float32)))
+        assert np.all(x == 129.0)
+    else:
+        x = rng.normal(0, 1, (B, V)).astype(np.float32)
+        x[:, ::3] = -np.inf
+        x[:, 1::7] = np.nan
+    k = np.array([1, 7, 50, 300, 0, 299], np.int32)
+    inp = W.custom_rows(x, W.F32, k_max=km, top_k=k)
+    val, idx = oracle.topk(inp)
+    for b in range(B):
+        yb = np.where(np.isnan(x[b]), -np.inf, x[b])
+        want = _lexsort_topk(yb, min(int(k[b]), km))
+        n = len(want)
+        assert np.array_equal(idx[b, :n], want)
+        assert np.array_equal(val[b, :n], yb[want])
+        assert np.all(idx[b, n:] == -1) and np.all(val[b, n:] == -np.inf)
+
+
+def test_topk_negative_zero_ties_positive_zero():
+    x = np.array([[np.nan, -0.0, 0.0, 1.0]], np.float32)
+    val, idx = oracle.topk(W.custom_rows(x, W.F32, k_max=4, top_k=[4]))
+    assert list(idx[0]) == [3, 1, 2, -1]
+    assert np.array_equal(val[0, :3], np.array([1.0, 0.0, 0.0], np.float32))
+    assert not np.signbit(val[0, 1])
+
+
+# --------------------------------------------------------------------------
+# Greedy = first argmax of the processed logits
+# --------------------------------------------------------------------------
+def test_greedy_is_first_argmax():
+    inp = W.config1(B=8)
+    inp["mode"][:] = W.MODE_GREEDY | W.MODE_REP | W.MODE_FREQ | W.MODE_PRES | W.MODE_BIAS
+    out = oracle.sample(inp)
+    y = oracle.process_logits(inp)["y"]
+    for b in range(inp["B"]):
+        assert out["token"][b] == int(np.argmax(y[b]))
+    # temperature 0 with the TEMP bit also means greedy
+    inp2 = W.config0()
+    o2 = oracle.sample(inp2)
+    assert o2["token"][0] == int(np.argmax(inp2["x"][0]))
+
+
+def test_greedy_ties_take_lowest_index():
+    x = np.zeros((1, 64), np.float32)
+    x[0, [5, 9, 40]] = 3.0
+    o = oracle.sample(W.custom_rows(x, W.F32, mode=[W.MODE_GREEDY]))
+    assert o["token"][0] == 5
+
+
+def test_empty_row_returns_minus_one():
+    x = np.ones((1, 64), np.float32)
+    inp = W.custom_rows(x, W.F32, mode=[W.MODE_GRAMMAR | W.MODE_TEMP], bitmask=np.zeros((1, 2), np.uint32))
+    o = oracle.sample(inp)
+    assert o["token"][0] == -1 and (o["flags"][0] & 1)
+
+
+# --------------------------------------------------------------------------
+# Truncation rules against softmax (scipy) on cases that reduce to it
+# --------------------------------------------------------------------------
+def _softmax_sorted(y, tau):
+    o = np.lexsort((np.arange(y.size), -y.astype(np.float64)))
+    p = special.softmax(y[o].astype(np.float64) / tau)
+    return o, p
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_top_p_is_minimal_prefix_with_mass_p(seed):
+    rng = np.random.default_rng(100 + seed)
+    V = 500
+    y = rng.normal(0, 2, V).astype(np.float32)
+    tau = float(rng.uniform(0.5, 1.5))
+    p = float(rng.uniform(0.3, 0.99))
+    d = oracle.row_distribution(y, W.MODE_TEMP | W.MODE_TOPP, temperature=tau, top_p=p, k_cap=V)
+    o, sp = _softmax_sorted(y, np.float32(tau))
+    assert np.array_equal(d["order"], o)
+    cum = np.cumsum(sp)
+    n = d["n_p"]
+    assert cum[n - 1] >= p - 1e-12          # kept mass reaches p
+    assert n == 1 or cum[n - 2] < p + 1e-12  # one fewer does not
+    assert np.allclose(d["P"], sp[:n] / sp[:n].sum(), rtol=1e-12, atol=0)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_min_p_keeps_tokens_with_p_at_least_theta_pmax(seed):
+    rng = np.random.default_rng(200 + seed)
+    V = 400
+    y = rng.normal(0, 2, V).astype(np.float32)
+    tau = float(rng.uniform(0.5, 1.5))
+    theta = float(rng.uniform(0.01, 0.5))
+    d = oracle.row_distribution(y, W.MODE_TEMP | W.MODE_MINP, temperature=tau, min_p=theta, k_cap=V)
+    o, sp = _softmax_sorted(y, np.float32(tau))
+    keep = sp >= np.float32(theta) * sp[0]
+    assert d["margin_m"] > 1e-9
+    assert d["n_m"] == int(keep.sum())
+    assert np.all(keep[: d["n_m"]])
+
+
+def test_top_k_then_top_p_renormalises_within_top_k():
+    # three tokens with softmax masses 0.5, 0.3, 0.2 (tau=1); top-k=2 renormalises
+    # to 0.625/0.375, so top-p=0.6 keeps one token; without top-k it keeps two.
+    y = np.log(np.array([0.5, 0.3, 0.2])).astype(np.float32)
+    d1 = oracle.row_distribution(y, W.MODE_TOPK | W.MODE_TOPP, top_k=2, top_p=0.6, k_cap=3)
+    d2 = oracle.row_distribution(y, W.MODE_TOPP, top_p=0.6, k_cap=3)
+    assert d1["n_s"] == 1 and d2["n_s"] == 2
+
+
+def test_temperature_two_token_closed_form():
+    for a, b, tau in [(1.0, 0.0, 1.0), (2.0, -1.0, 0.5), (0.25, 0.0, 2.0)]:
+        y = np.array([a, b], np.float32)
+        d = oracle.row_distribution(y, W.MODE_TEMP, temperature=tau, k_cap=2)
+        p0 = 1.0 / (1.0 + math.exp(-(a - b) / tau))
+        assert abs(d["P"][0] - p0) < 1e-15 and abs(d["P"][1] - (1 - p0)) < 1e-15
+
+
+def test_probability_ratio_identity():
+    rng = np.random.default_rng(5)
+    y = rng.normal(0, 1, 64).astype(np.float32)
+    d = oracle.row_distribution(y, W.MODE_TEMP, temperature=0.7, k_cap=64)
+    ys = y[d["order"]].astype(np.float64)
+    r = d["P"][1:] / d["P"][0]
+    assert np.allclose(r, np.exp((ys[1:] - ys[0]) / np.float64(np.float32(0.7))), rtol=1e-13)
+
+
+def test_k_cap_bounds_rows_without_top_k():
+    y = np.random.default_rng(3).normal(0, 1, 100).astype(np.float32)
+    d = oracle.row_distribution(y, W.MODE_TEMP, k_cap=10)
+    assert d["n_k"] == 10 and d["n_s"] == 10 and (d["flags"] & 8)
+    d2 = oracle.row_distribution(y, W.MODE_TEMP | W.MODE_TOPK, top_k=5, k_cap=10)
+    assert d2["n_k"] == 5 and not (d2["flags"] & 8)
+
+
+# --------------------------------------------------------------------------
+# Draw
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("case", _load("draw_cases.json")["cases"])
+def test_draw_golden(case):
+    assert oracle.draw(case["w"], case["u"]) == case["pick"]
+
+
+def _chi2_ok(counts, probs, alpha=1e-4):
+    n = counts.sum()
+    exp = probs * n
+    keep = exp > 5
+    lump_c = counts[~keep].sum()
+    lump_e = exp[~keep].sum()
+    c = np.append(counts[keep], lump_c) if lump_e > 0 else counts[keep]
+    e = np.append(exp[keep], lump_e) if lump_e > 0 else exp[keep]
+    stat, pv = stats.chisquare(c, e * c.sum() / e.sum())
+    return pv > alpha, pv
+
+
+def test_sampling_distribution_chi_square():
+    V, B = 12, 40000
+    y = np.random.default_rng(7).normal(0, 1, V).astype(np.float32)
+    x = np.tile(y, (B, 1))
+    inp = W.custom_rows(x, W.F32, k_max=V,
+                        mode=np.full(B, W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP),
+                        temperature=np.full(B, 0.8), top_k=np.full(B, 9), top_p=np.full(B, 0.95),
+                        position=np.arange(B))
+    tok = oracle.sample(inp)["token"]
+    d = oracle.row_distribution(y, W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP, temperature=0.8,
+                                top_k=9, top_p=0.95, k_cap=V)
+    probs = np.zeros(V)
+    probs[d["order"][: d["n_s"]]] = d["P"]
+    # kept set equals the softmax top-p rule on the renormalised top-9
+    o, sp = _softmax_sorted(y, np.float32(0.8))
+    sp9 = sp[:9] / sp[:9].sum()
+    n = int(np.searchsorted(np.cumsum(sp9), 0.95) + 1)
+    assert d["n_s"] == n
+    counts = np.bincount(tok, minlength=V).astype(np.float64)
+    assert counts[probs == 0].sum() == 0
+    ok, pv = _chi2_ok(counts[probs > 0], probs[probs > 0])
+    assert ok, pv
+
+
+# --------------------------------------------------------------------------
+# Speculative verification
+# --------------------------------------------------------------------------
+def _verify_inputs(x_rows, q, d, mode, L, **params):
+    """x_rows [B, L+1, V] float32, q [B, L, V], d [B, L]."""
+    B = x_rows.shape[0]
+    inp = W.custom_rows(x_rows.reshape(B * (L + 1), -1), W.F32, k_max=x_rows.shape[-1], mode=mode, **params)
+    inp["x"] = x_rows
+    inp["B"] = B
+    for k in ("mode", "temperature", "top_k", "top_p", "min_p", "rep", "freq", "pres", "seed", "position"):
+        if inp[k] is not None and inp[k].shape[0] != B:
+            inp[k] = inp[k][:B]
+    inp["hist_offsets"] = inp["hist_offsets"][: B + 1] if inp["hist_offsets"].shape[0] > B + 1 else inp["hist_offsets"]
+    inp["bias_offsets"] = inp["bias_offsets"][: B + 1] if inp["bias_offsets"].shape[0] > B + 1 else inp["bias_offsets"]
+    inp["L"] = L
+    inp["draft_probs"] = q.astype(np.float32)
+    inp["draft_tokens"] = d.astype(np.int32)
+    return inp
+
+
+def test_verify_first_token_follows_target_chi_square():
+    V, B, L = 8, 40000, 1
+    rng = np.random.default_rng(21)
+    t = rng.normal(0, 1, V).astype(np.float32)
+    qv = special.softmax(rng.normal(0, 1, V)).astype(np.float32)
+    d = rng.choice(V, size=(B, L), p=qv / qv.sum())
+    x = np.tile(t, (B, L + 1, 1))
+    q = np.tile(qv, (B, L, 1))
+    inp = _verify_inputs(x, q, d, np.full(B, W.MODE_TEMP), L, temperature=np.full(B, 0.9),
+                         position=np.arange(B) * 7)
+    out = oracle.verify(inp)
+    first = out["tokens"][:, 0]
+    assert np.all(first >= 0)
+    p = special.softmax(t.astype(np.float64) / np.float32(0.9))
+    ok, pv = _chi2_ok(np.bincount(first, minlength=V).astype(float), p)
+    assert ok, pv
+    # acceptance rate of one draft equals sum_x min(p(x), q(x)) (Leviathan et al.)
+    acc = float(np.mean(out["n_acc"] == 1))
+    want = float(np.minimum(p, qv.astype(np.float64)).sum())
+    assert abs(acc - want) < 4 * math.sqrt(want * (1 - want) / B)
+
+
+def test_verify_second_token_uses_accepted_draft_history():
+    # With a repetition penalty the target for position 2 depends on token 1;
+    # conditioned on token 1, token 2 must follow that penalised target.
+    V, B, L = 6, 60000, 2
+    rng = np.random.default_rng(33)
+    t = rng.normal(0, 0.7, V).astype(np.float32)
+    qv = special.softmax(rng.normal(0, 0.5, V)).astype(np.float32)
+    d = rng.choice(V, size=(B, L), p=qv / qv.sum())
+    x = np.tile(t, (B, L + 1, 1))
+    q = np.tile(qv, (B, L, 1))
+    mode = W.MODE_TEMP | W.MODE_REP | W.MODE_PRES
+    inp = _verify_inputs(x, q, d, np.full(B, mode), L, temperature=np.full(B, 1.0),
+                         rep=np.full(B, 3.0), pres=np.full(B, 1.0), position=np.arange(B) * 5,
+                         hist_offsets=np.zeros(B + 1, np.int32))
+    out = oracle.verify(inp)
+    tok = out["tokens"]
+    two = tok[:, 1] >= 0
+    assert two.sum() > 5000
+    for t1 in range(V):
+        sel = two & (tok[:, 0] == t1)
+        if sel.sum() < 500:
+            continue
+        ypen = oracle.process_row(t, "f32", mode, rep=3.0, pres=1.0, hist=[t1])
+        p2 = special.softmax(ypen.astype(np.float64))
+        ok, pv = _chi2_ok(np.bincount(tok[sel, 1], minlength=V).astype(float), p2)
+        assert ok, (t1, pv)
+
+
+def test_verify_special_cases():
+    V, L, B = 16, 3, 64
+    rng = np.random.default_rng(4)
+    t = rng.normal(0, 1, V).astype(np.float32)
+    x = np.tile(t, (B, L + 1, 1))
+    p = special.softmax(t.astype(np.float64))
+    # q equal to the target: every draft is accepted, bonus appended
+    d = rng.choice(V, size=(B, L), p=p)
+    inp = _verify_inputs(x, np.tile(p.astype(np.float32), (B, L, 1)), d, np.full(B, W.MODE_TEMP), L,
+                         position=np.arange(B))
+    o = oracle.verify(inp)
+    # float32 rounding of q can exceed P by an ulp; acceptance is then u*q <= P almost surely
+    assert np.mean(o["n_acc"] == L) > 0.95
+    # draft outside the target's top-k: P(d) = 0, always rejected
+    order = np.argsort(-t, kind="stable")
+    d0 = np.tile(order[-1], (B, L))
+    inp = _verify_inputs(x, np.tile(p.astype(np.float32), (B, L, 1)), d0,
+                         np.full(B, W.MODE_TEMP | W.MODE_TOPK), L, top_k=np.full(B, 4), position=np.arange(B))
+    o = oracle.verify(inp)
+    assert np.all(o["n_acc"] == 0) and np.all(np.isin(o["tokens"][:, 0], order[:4]))
+    assert np.all(o["tokens"][:, 1:] == -1)
+    # greedy: accept iff the draft is the argmax; correction is the argmax
+    am = int(np.argmax(t))
+    d1 = np.full((B, L), am)
+    d1[::2, 1] = order[1]
+    inp = _verify_inputs(x, np.tile(p.astype(np.float32), (B, L, 1)), d1, np.full(B, W.MODE_GREEDY), L)
+    o = oracle.verify(inp)
+    assert np.all(o["n_acc"][1::2] == L) and np.all(o["tokens"][1::2, L] == am)
+    assert np.all(o["n_acc"][::2] == 1) and np.all(o["tokens"][::2, :2] == am)
+    # a negative draft id ends the draft: that position samples from the target
+    d2 = np.full((B, L), -1)
+    inp = _verify_inputs(x, np.tile(p.astype(np.float32), (B, L, 1)), d2, np.full(B, W.MODE_GREEDY), L)
+    o = oracle.verify(inp)
+    assert np.all(o["n_acc"] == 0) and np.all(o["tokens"][:, 0] == am)
+
+
+def test_process_logits_distribution_sums_to_one():
+    inp = W.config0()
+    out = oracle.process_logits(inp)
+    P = out["P"]
+    assert np.all(np.abs(P.sum(axis=1) - 1.0) < 1e-12)
+    assert P[0, np.argmax(inp["x"][0])] == 1.0  # temperature 0: one-hot
+    for b in range(1, 4):
+        assert np.count_nonzero(P[b]) <= 50
+
+
+@pytest.mark.parametrize("case", _load("truncation_cases.json")["cases"], ids=lambda c: c["name"])
+def test_truncation_golden(case):
+    if "y_from_probs" in case:
+        y = np.log(np.array(case["y_from_probs"], np.float64)).astype(np.float32)
+    else:
+        y = np.array(case["y"], np.float32)
+    d = oracle.row_distribution(y, case["mode"], temperature=case.get("temperature", 1.0),
+                                top_k=case.get("top_k", 0), top_p=case.get("top_p", 1.0),
+                                min_p=case.get("min_p", 0.0), k_cap=y.size)
+    assert d["n_s"] == case["n_s"]
+    if "order" in case:
+        assert list(d["order"][: d["n_s"]]) == case["order"]
