@@ -213,7 +213,7 @@ static void row_distribution(const float *y, const int32_t *order, int n_valid, 
   int64_t nk = k_req;
   if (nk > k_cap) nk = k_cap;
   if (nk > n_valid) nk = n_valid;
-  if ((k_req < n_valid ? k_req : n_valid) > k_cap) d->flags |= RF_KCAP;
+  if (k_req > k_cap) d->flags |= RF_KCAP;  /* request wants more than the bound */
   d->n_k = (int)nk;
 
   double Zk = 0.0;
@@ -481,6 +481,7 @@ int ssref_verify(const void *x, int dtype, int64_t ld_row, const float *draft_pr
       dist_t ds;
       row_distribution(y, order, nv, mode, pf(p->temperature, b, 1.0f), p->top_k ? p->top_k[b] : 0,
                        pf(p->top_p, b, 1.0f), pf(p->min_p, b, 0.0f), p->k_cap, w, &ds);
+      fl |= ds.flags;
       if (!ds.greedy) {
         if (ds.margin_p < mg) mg = ds.margin_p;
         if (ds.margin_m < mg) mg = ds.margin_m;
@@ -490,7 +491,7 @@ int ssref_verify(const void *x, int dtype, int64_t ld_row, const float *draft_pr
       int emit = -1;
       int accepted = 0;
       if (nv == 0) {
-        fl |= RF_EMPTY;
+        /* empty target row: rejected, no correction token */
       } else if (ds.greedy) {
         if (has_draft && d[l - 1] == order[0]) accepted = 1;
         else emit = order[0];

@@ -1,0 +1,206 @@
+// ss_device.hpp -- device primitives for the gfx950 sampler kernels.
+//
+// Order-preserving keys, Philox4x32-10, wave64 / workgroup reductions and
+// scans, and an LDS bitonic sort.  Workgroups are kBlock = 256 threads
+// (four 64-lane wavefronts).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ss {
+
+constexpr int kBlock = 256;
+constexpr int kWaves = kBlock / 64;
+
+// ---------------------------------------------------------------------------
+// Order-preserving 32-bit key of a float32 bit pattern.
+//   positives  u  -> u + 2^31          (+0 -> 0x80000000)
+//   negatives  u  -> 2^32 - u          (-0 -> 0x80000000: ties with +0)
+// so key order is value order and -0 == +0.  -inf maps to kKeyNegInf,
+// negative NaNs below it; positive NaNs (above +inf) are folded to 0.
+// Keys <= kKeyNegInf are "invalid" (never selected).  The lexicographic
+// encoding of the paper's Section 3.4 is the 16-bit analogue of this map.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kKeyNegInf = 0x00800000u;
+constexpr uint32_t kKeyPosInf = 0xFF800000u;
+constexpr uint32_t kKeyFloor = kKeyNegInf + 1u;  // smallest valid key
+
+__device__ __forceinline__ uint32_t key_of_bits(uint32_t u) {
+  const uint32_t s = (uint32_t)((int32_t)u >> 31);
+  const uint32_t k = (u ^ s) + (s ? 1u : 0x80000000u);
+  return k > kKeyPosInf ? 0u : k;
+}
+
+__device__ __forceinline__ uint32_t key_of_float(float f) { return key_of_bits(__float_as_uint(f)); }
+
+__device__ __forceinline__ float float_of_key(uint32_t k) {
+  const uint32_t u = (k >= 0x80000000u) ? (k - 0x80000000u) : (0u - k);
+  return __uint_as_float(u);
+}
+
+// canonical value of a logit: NaN -> -inf, -0 -> +0
+__device__ __forceinline__ float canon(float v) {
+  if (v != v) return -__builtin_inff();
+  return v == 0.0f ? 0.0f : v;
+}
+
+// Composite rank key: larger = earlier in canonical order (value desc, index asc).
+__device__ __forceinline__ uint64_t comp_of(uint32_t key, uint32_t idx) {
+  return ((uint64_t)key << 32) | (uint64_t)(~idx);
+}
+__device__ __forceinline__ uint32_t comp_key(uint64_t c) { return (uint32_t)(c >> 32); }
+__device__ __forceinline__ uint32_t comp_idx(uint64_t c) { return ~(uint32_t)c; }
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon et al., SC'11), counter (request, pos lo, pos hi, 0),
+// key (seed lo, seed hi).  Word 0 drives token draws, word 1 acceptance.
+// ---------------------------------------------------------------------------
+__device__ inline uint4 philox4x32_10(uint4 c, uint2 k) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
+    c = make_uint4(hi1 ^ c.y ^ k.x, lo1, hi0 ^ c.w ^ k.y, lo0);
+    k.x += 0x9E3779B9u;
+    k.y += 0xBB67AE85u;
+  }
+  return c;
+}
+
+__device__ inline double uniform01(uint64_t seed, uint32_t request, int64_t position, int word) {
+  const uint64_t p = (uint64_t)position;
+  const uint4 o = philox4x32_10(make_uint4(request, (uint32_t)p, (uint32_t)(p >> 32), 0u),
+                                make_uint2((uint32_t)seed, (uint32_t)(seed >> 32)));
+  const uint32_t w = word == 0 ? o.x : (word == 1 ? o.y : (word == 2 ? o.z : o.w));
+  return ((double)w + 0.5) * (1.0 / 4294967296.0);
+}
+
+// weight of a kept token: exp((y - M)/tau), exactly 1 at the maximum
+__device__ inline double weight_of(double y, double M, double tau) {
+  return (y == M) ? 1.0 : exp((y - M) / tau);
+}
+
+// ---------------------------------------------------------------------------
+// wave64 / workgroup helpers
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int lane() { return (int)__lane_id(); }
+__device__ __forceinline__ int wave() { return (int)(threadIdx.x >> 6); }
+
+template <typename T>
+__device__ __forceinline__ T wave_max(T v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    T w = __shfl_xor(v, o, 64);
+    v = w > v ? w : v;
+  }
+  return v;
+}
+template <typename T>
+__device__ __forceinline__ T wave_min(T v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    T w = __shfl_xor(v, o, 64);
+    v = w < v ? w : v;
+  }
+  return v;
+}
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+template <typename T>
+__device__ __forceinline__ T wave_incl_scan(T v) {
+  const int l = lane();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    T w = __shfl_up(v, o, 64);
+    if (l >= o) v += w;
+  }
+  return v;
+}
+
+// Workgroup reductions through a small LDS scratch of kWaves entries.
+// Every call ends with a barrier so the scratch can be reused at once.
+template <typename T>
+__device__ inline T block_max(T v, T* scratch) {
+  v = wave_max(v);
+  if (lane() == 0) scratch[wave()] = v;
+  __syncthreads();
+  T r = scratch[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) r = scratch[w] > r ? scratch[w] : r;
+  __syncthreads();
+  return r;
+}
+template <typename T>
+__device__ inline T block_min(T v, T* scratch) {
+  v = wave_min(v);
+  if (lane() == 0) scratch[wave()] = v;
+  __syncthreads();
+  T r = scratch[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) r = scratch[w] < r ? scratch[w] : r;
+  __syncthreads();
+  return r;
+}
+// Deterministic sum: fixed shuffle tree, then waves in order.
+template <typename T>
+__device__ inline T block_sum(T v, T* scratch) {
+  v = wave_sum(v);
+  if (lane() == 0) scratch[wave()] = v;
+  __syncthreads();
+  T r = scratch[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) r += scratch[w];
+  __syncthreads();
+  return r;
+}
+// Exclusive scan over threads in thread order; returns this thread's offset,
+// writes the workgroup total.
+template <typename T>
+__device__ inline T block_excl_scan(T v, T* scratch, T& total) {
+  const T inc = wave_incl_scan(v);
+  if (lane() == 63) scratch[wave()] = inc;
+  __syncthreads();
+  T off = T(0), tot = T(0);
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const T s = scratch[w];
+    if (w < wave()) off += s;
+    tot += s;
+  }
+  __syncthreads();
+  total = tot;
+  return off + inc - v;
+}
+
+// ---------------------------------------------------------------------------
+// LDS bitonic sort, descending, of n (power of two) 64-bit keys.
+// ---------------------------------------------------------------------------
+__device__ inline void lds_sort_desc(uint64_t* a, int n) {
+  for (int k = 2; k <= n; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int p = threadIdx.x; p < (n >> 1); p += kBlock) {
+        const int i = ((p & ~(j - 1)) << 1) | (p & (j - 1));
+        const int m = i + j;
+        const uint64_t x = a[i], y = a[m];
+        const bool desc = (i & k) == 0;
+        if (desc ? (x < y) : (x > y)) {
+          a[i] = y;
+          a[m] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+__host__ __device__ inline int next_pow2(int v) {
+  int p = 1;
+  while (p < v) p <<= 1;
+  return p;
+}
+
+}  // namespace ss

@@ -1,0 +1,1603 @@
+// ss_kernel.hip -- fused LLM sampling pipeline for MI355X (gfx950).
+//
+// One launch per call (plus one materialising pass for ss_process_logits).
+// Grid: rows x T workgroups, T = ceil(V / kTile).  Each workgroup streams one
+// kTile-element slice of one logit row exactly once and
+//   1. applies the logit-processing prologue (paper Appendix C.1, Alg. 8
+//      order): grammar allow bits, repetition / frequency / presence penalties
+//      and sparse logit bias -- penalties and bias touch only the ids in the
+//      request's history / bias lists, so they are computed once per distinct
+//      id by an "owner" thread and the bulk of the tile pays nothing for them;
+//   2. turns every element into an order-preserving 32-bit key;
+//   3. reduces the tile maximum (greedy rows stop here);
+//   4. for truncating rows, derives an emission threshold from the maxima of
+//      groups of 4 elements (the q-th largest group maximum bounds the tile's
+//      q-th largest element from below) and writes the elements at or above
+//      it to a small per-tile candidate region -- a bounded candidate set, as
+//      in the paper's two-stage scheme (Section 3.2), but with a row-level
+//      quota instead of a fixed per-tile k;
+//   5. takes a ticket; the last workgroup of the row merges: it checks that
+//      the candidates provably contain the row's top-k (at least k of them lie
+//      above the largest tile threshold), selects the exact top-k by radix
+//      select in registers, and runs the truncation / selection epilogue
+//      (Alg. 11 order) in double precision.  If the check fails (skewed or
+//      heavily tied rows) it recomputes the exact top-k by streaming the row
+//      again -- a slow but always-correct path, flagged SS_FLAG_FALLBACK.
+// No host synchronisation, fixed grid, self-resetting counters: every call
+// can be captured in a HIP graph.
+#include <hip/hip_runtime.h>
+#include <limits.h>
+#include <stdint.h>
+
+#include "ss.h"
+#include "ss_device.hpp"
+
+namespace ss {
+
+constexpr int kTile = 8192;
+constexpr int kPT = kTile / kBlock;  // element slots per thread (32)
+constexpr int kGPT = 8;              // group maxima per thread
+constexpr int kGS = kPT / kGPT;      // slots per group (4)
+constexpr int kG = kGPT * kBlock;    // groups per tile (2048)
+constexpr int kHCap = 1024;          // in-tile history entries held in LDS
+constexpr int kBCap = 128;           // in-tile bias entries held in LDS
+constexpr int kRPT = 32;             // merge candidates per thread (registers)
+constexpr int kMaxT = (SS_MAX_V + kTile - 1) / kTile;
+constexpr int kEPT = SS_MAX_K / kBlock;  // selected entries per thread in the epilogue
+constexpr uint32_t kNotOwner = 0xFFFFFFFFu;
+constexpr uint32_t kNoEmit = 0xFFFFFFFFu;  // emits nothing (above every valid key)
+
+enum { OP_TOPK = SS_OP_TOPK, OP_SAMPLE = SS_OP_SAMPLE, OP_VERIFY = SS_OP_VERIFY, OP_PROCESS = SS_OP_PROCESS };
+enum { KIND_EMPTY = 0, KIND_GREEDY = 1, KIND_DIST = 2 };
+
+struct RowSummary {
+  uint64_t thr;  // composite key of the last kept rank
+  double Z;      // sum of kept weights
+  float M;       // row maximum
+  float tau;
+  int32_t argmax;
+  int32_t kind;
+};
+struct RowResult {
+  int32_t accept;
+  int32_t emit;
+  int32_t flags;
+  int32_t pad;
+};
+
+struct KArgs {
+  const void* x;
+  int64_t ld;
+  int op, B, rows, V, T, L, k_cap, cap, k_out, vec_ok;
+  uint32_t feat;
+  const uint32_t* mode;
+  const float* temperature;
+  const int32_t* top_k;
+  const float* top_p;
+  const float* min_p;
+  const float* rep;
+  const float* freq;
+  const float* pres;
+  const int32_t* hist_off;
+  const int32_t* hist_ids;
+  const int32_t* bias_off;
+  const int32_t* bias_ids;
+  const float* bias_vals;
+  const uint32_t* bitmask;
+  int64_t mask_ld;
+  const uint64_t* seed;
+  const int64_t* position;
+  const float* draft_probs;
+  int64_t ld_q;
+  const int32_t* draft_tokens;
+  int32_t* out_token;
+  float* out_logprob;
+  int32_t* out_idx;
+  float* out_prob;
+  int32_t* flags;
+  float* out_val;
+  int32_t* out_tokens;
+  int32_t* out_nacc;
+  float* out_logits;
+  float* out_probs;
+  uint32_t* ticket;
+  uint32_t* req_ticket;
+  uint4* rec;
+  uint2* cand;
+  RowResult* res;
+  RowSummary* summ;
+};
+
+struct Smem {
+  uint64_t red64[kWaves];
+  double redd[kWaves];
+  double bcd[4];
+  uint32_t bm[kBlock];  // per-thread bits of patched slots
+  uint32_t hlK[kHCap];  // owner key per history entry (kNotOwner otherwise)
+  uint32_t blK[kBCap];
+  int32_t bl_pos[kBCap];
+  float bl_val[kBCap];
+  uint32_t hist[256];
+  uint32_t mhist[256];
+  uint32_t prefix[kMaxT + 1];
+  uint32_t wc[kWaves];
+  uint32_t red32[kWaves];
+  uint32_t cnt[4];
+  uint32_t bc[8];
+  uint16_t hl[kHCap];
+  uint16_t bl_l[kBCap];
+};
+constexpr int kSmemFixed = (int)((sizeof(Smem) + 15) & ~(size_t)15);
+
+// ---------------------------------------------------------------------------
+// Element layout: thread t, slot j (0..31) holds chunk i = j / VW, element
+// e = j % VW of vector v = i * kBlock + t, i.e. local index (v * VW + e).
+// A chunk is one 16-byte load (8 bf16 or 4 float32).
+// ---------------------------------------------------------------------------
+template <int DT>
+struct DTT;
+template <>
+struct DTT<SS_F32> {
+  static constexpr int VW = 4, NV = 8, ES = 4;
+};
+template <>
+struct DTT<SS_BF16> {
+  static constexpr int VW = 8, NV = 4, ES = 2;
+};
+
+template <int DT>
+__device__ __forceinline__ int local_of_slot(int t, int j) {
+  constexpr int VW = DTT<DT>::VW;
+  return ((j / VW) * kBlock + t) * VW + (j % VW);
+}
+
+__device__ __forceinline__ uint32_t comp4(const uint4& v, int c) {
+  return c == 0 ? v.x : (c == 1 ? v.y : (c == 2 ? v.z : v.w));
+}
+
+// float32 bit pattern of slot j
+template <int DT>
+__device__ __forceinline__ uint32_t slot_bits(const uint4 (&r)[DTT<DT>::NV], int j) {
+  if constexpr (DT == SS_F32) {
+    return comp4(r[j >> 2], j & 3);
+  } else {
+    const uint32_t w = comp4(r[j >> 3], (j & 7) >> 1);
+    return (j & 1) ? (w & 0xFFFF0000u) : (w << 16);
+  }
+}
+
+// raw element load from global memory (scalar), as float32 bits
+template <int DT>
+__device__ __forceinline__ uint32_t load_elem_bits(const unsigned char* xrow, int64_t i) {
+  if constexpr (DT == SS_F32) {
+    return reinterpret_cast<const uint32_t*>(xrow)[i];
+  } else {
+    return ((uint32_t)reinterpret_cast<const uint16_t*>(xrow)[i]) << 16;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Per-row context
+// ---------------------------------------------------------------------------
+struct Ctx {
+  int row, req, ell;
+  uint32_t mode;
+  const unsigned char* xrow;
+  const int32_t* hist;
+  int nhist;
+  const int32_t* extra;
+  int nextra;
+  const int32_t* bias_ids;
+  const float* bias_vals;
+  int nbias;
+  const uint32_t* mask;
+  float rep, freq, pres;
+  bool greedy;
+  bool kcap;
+  int k_eff;
+};
+
+template <int DT>
+__device__ Ctx make_ctx(const KArgs& a, int row) {
+  Ctx c;
+  c.row = row;
+  if (a.op == OP_VERIFY) {
+    c.req = row / (a.L + 1);
+    c.ell = row % (a.L + 1);
+  } else {
+    c.req = row;
+    c.ell = 0;
+  }
+  const int b = c.req;
+  const uint32_t m = (a.op == OP_TOPK ? SS_TOPK : (a.mode ? a.mode[b] : 0u)) & a.feat;
+  c.mode = m;
+  c.xrow = reinterpret_cast<const unsigned char*>(a.x) + (size_t)row * (size_t)a.ld * DTT<DT>::ES;
+  c.hist = nullptr;
+  c.nhist = 0;
+  c.extra = nullptr;
+  c.nextra = 0;
+  if (m & (SS_REP | SS_FREQ | SS_PRES)) {
+    c.hist = a.hist_ids + a.hist_off[b];
+    c.nhist = a.hist_off[b + 1] - a.hist_off[b];
+    if (a.op == OP_VERIFY && a.draft_tokens) {
+      c.extra = a.draft_tokens + (size_t)b * a.L;
+      c.nextra = c.ell;
+    }
+  }
+  c.bias_ids = nullptr;
+  c.bias_vals = nullptr;
+  c.nbias = 0;
+  if (m & SS_BIAS) {
+    c.bias_ids = a.bias_ids + a.bias_off[b];
+    c.bias_vals = a.bias_vals + a.bias_off[b];
+    c.nbias = a.bias_off[b + 1] - a.bias_off[b];
+  }
+  c.mask = (m & SS_GRAMMAR) ? a.bitmask + (size_t)row * (size_t)a.mask_ld : nullptr;
+  c.rep = (m & SS_REP) ? a.rep[b] : 1.0f;
+  c.freq = (m & SS_FREQ) ? a.freq[b] : 0.0f;
+  c.pres = (m & SS_PRES) ? a.pres[b] : 0.0f;
+  c.kcap = false;
+  if (a.op == OP_TOPK) {
+    c.greedy = false;
+    int k = a.top_k ? a.top_k[b] : a.k_cap;
+    c.k_eff = k < 0 ? 0 : (k > a.k_cap ? a.k_cap : k);
+  } else {
+    c.greedy = (m & SS_GREEDY) || ((m & SS_TEMP) && a.temperature[b] <= 0.0f);
+    const int64_t kreq = ((m & SS_TOPK) && a.top_k[b] >= 1) ? (int64_t)a.top_k[b] : (int64_t)INT_MAX;
+    c.k_eff = kreq < a.k_cap ? (int)kreq : a.k_cap;
+    c.kcap = !c.greedy && kreq > a.k_cap;
+  }
+  return c;
+}
+
+__host__ __device__ inline int quota(int k, int T) {
+  if (T <= 1) return k;
+  const int kt = (k + T - 1) / T;
+  int s = 0;
+  while (s * s < kt) ++s;
+  const int q = kt + 4 * s + 8;
+  return q < k ? q : k;
+}
+
+__host__ __device__ inline int tile_cap(int kcap, int T) {
+  const int q = quota(kcap, T);
+  if (2 * q > kG) return kTile;
+  const int c = 2 * q + 64;
+  return c < kTile ? c : kTile;
+}
+
+// ---------------------------------------------------------------------------
+// Prologue for one patched id (local index l): count c, ordered bias sum,
+// penalties in Appendix C.1 order, each one float32 operation.
+// ---------------------------------------------------------------------------
+template <int DT>
+__device__ uint32_t patched_key(const Ctx& c, int lo, int l, int count, bool has_bias, float bsum) {
+  const int64_t g = (int64_t)lo + l;
+  float v = canon(__uint_as_float(load_elem_bits<DT>(c.xrow, g)));
+  if (c.mask) {
+    const uint32_t w = c.mask[g >> 5];
+    if (((w >> (g & 31)) & 1u) == 0u) return 0u;
+  }
+  if (count > 0) {
+    if (c.mode & SS_REP) v = (v > 0.0f) ? v / c.rep : v * c.rep;
+    if (c.mode & SS_FREQ) {
+      const float t = c.freq * (float)count;
+      v = v - t;
+    }
+    if (c.mode & SS_PRES) v = v - c.pres;
+  }
+  if (has_bias) v = v + bsum;
+  return key_of_float(v);
+}
+
+template <int DT>
+__device__ __forceinline__ void set_patch_bit(Smem& S, int l) {
+  constexpr int VW = DTT<DT>::VW;
+  const int v = l / VW, e = l % VW;
+  const int t = v % kBlock, i = v / kBlock;
+  atomicOr(&S.bm[t], 1u << (i * VW + e));
+}
+
+// Loads one tile and produces keys.  Slots whose id carries a penalty or bias
+// come out as 0 (excluded) and their true keys are held by owner entries in
+// LDS (S.hlK / S.blK, indexed like S.hl / S.bl_l), unless the in-tile lists
+// overflow LDS, in which case the slots are fixed in place.  Returns the
+// number of owner entries to scan (n_hl in *hl_n_out).
+template <int DT>
+__device__ int load_tile(const KArgs& a, const Ctx& c, int lo, Smem& S, uint32_t (&key)[kPT],
+                         int* hl_n_out) {
+  constexpr int VW = DTT<DT>::VW, NV = DTT<DT>::NV, ES = DTT<DT>::ES;
+  const int tid = threadIdx.x;
+  const int V = a.V;
+  const int n_tile = min(kTile, V - lo);
+  uint4 raw[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int l0 = (i * kBlock + tid) * VW;
+    if (a.vec_ok && l0 + VW <= n_tile) {
+      raw[i] = *reinterpret_cast<const uint4*>(c.xrow + ((size_t)lo + l0) * ES);
+    } else {
+      uint32_t w[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) w[q] = 0xFFFFFFFFu;  // negative NaN: invalid
+#pragma unroll
+      for (int e = 0; e < VW; ++e) {
+        const int l = l0 + e;
+        if (l < n_tile) {
+          if constexpr (DT == SS_F32) {
+            w[e] = reinterpret_cast<const uint32_t*>(c.xrow)[lo + l];
+          } else {
+            const uint32_t h = reinterpret_cast<const uint16_t*>(c.xrow)[lo + l];
+            const int q = e >> 1;
+            w[q] = (e & 1) ? ((w[q] & 0x0000FFFFu) | (h << 16)) : ((w[q] & 0xFFFF0000u) | h);
+          }
+        }
+      }
+      raw[i] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  }
+
+  // grammar allow bits, one bit per slot
+  uint32_t allow = 0xFFFFFFFFu;
+  if (c.mask) {
+    allow = 0u;
+    const int W = (V + 31) >> 5;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int g0 = lo + (i * kBlock + tid) * VW;
+      const int wi = g0 >> 5;
+      const uint32_t word = (wi < W) ? c.mask[wi] : 0u;
+      allow |= ((word >> (g0 & 31)) & ((1u << VW) - 1u)) << (i * VW);
+    }
+  }
+
+  // patch lists (history / drafts / bias ids inside this tile)
+  const bool do_hist = (c.mode & (SS_REP | SS_FREQ | SS_PRES)) && (c.nhist + c.nextra) > 0;
+  const bool do_bias = (c.mode & SS_BIAS) && c.nbias > 0;
+  int hl_n = 0, bl_n = 0;
+  bool overflow = false;
+  uint32_t pbits = 0u;
+  if (do_hist || do_bias) {
+    S.bm[tid] = 0u;
+    if (tid == 0) {
+      S.cnt[0] = 0u;
+      S.cnt[1] = 0u;
+    }
+    __syncthreads();
+    if (do_hist) {
+      const int n = c.nhist + c.nextra;
+      for (int h = tid; h < n; h += kBlock) {
+        const int id = h < c.nhist ? c.hist[h] : c.extra[h - c.nhist];
+        const int rel = id - lo;
+        if (id >= 0 && id < V && rel >= 0 && rel < n_tile) {
+          const uint32_t p = atomicAdd(&S.cnt[0], 1u);
+          if (p < (uint32_t)kHCap) S.hl[p] = (uint16_t)rel;
+          set_patch_bit<DT>(S, rel);
+        }
+      }
+    }
+    if (do_bias) {
+      for (int e = tid; e < c.nbias; e += kBlock) {
+        const int id = c.bias_ids[e];
+        const int rel = id - lo;
+        if (id >= 0 && id < V && rel >= 0 && rel < n_tile) {
+          const uint32_t p = atomicAdd(&S.cnt[1], 1u);
+          if (p < (uint32_t)kBCap) {
+            S.bl_l[p] = (uint16_t)rel;
+            S.bl_pos[p] = e;
+            S.bl_val[p] = c.bias_vals[e];
+          }
+          set_patch_bit<DT>(S, rel);
+        }
+      }
+    }
+    __syncthreads();
+    hl_n = (int)S.cnt[0];
+    bl_n = (int)S.cnt[1];
+    overflow = hl_n > kHCap || bl_n > kBCap;
+    pbits = S.bm[tid];
+    if (!overflow) {
+      // owners: the first list entry of each distinct id computes its key
+      for (int n = tid; n < hl_n + bl_n; n += kBlock) {
+        uint32_t K = kNotOwner;
+        int l, cntv = 0;
+        bool owner = true;
+        if (n < hl_n) {
+          l = S.hl[n];
+          for (int m = 0; m < hl_n; ++m) {
+            if (S.hl[m] == l) {
+              ++cntv;
+              if (m < n) owner = false;
+            }
+          }
+        } else {
+          const int nb = n - hl_n;
+          l = S.bl_l[nb];
+          for (int m = 0; m < hl_n && owner; ++m)
+            if (S.hl[m] == l) owner = false;
+          for (int m = 0; m < nb && owner; ++m)
+            if (S.bl_l[m] == l) owner = false;
+        }
+        if (owner) {
+          float bsum = 0.0f;
+          bool hb = false;
+          if (do_bias) {
+            int last = -1;
+            for (;;) {  // entries of this id in list order
+              int best = INT_MAX, bi = -1;
+              for (int m = 0; m < bl_n; ++m)
+                if (S.bl_l[m] == l && S.bl_pos[m] > last && S.bl_pos[m] < best) {
+                  best = S.bl_pos[m];
+                  bi = m;
+                }
+              if (bi < 0) break;
+              bsum = bsum + S.bl_val[bi];
+              hb = true;
+              last = best;
+            }
+          }
+          K = patched_key<DT>(c, lo, l, cntv, hb, bsum);
+        }
+        if (n < hl_n)
+          S.hlK[n] = K;
+        else
+          S.blK[n - hl_n] = K;
+      }
+      allow &= ~pbits;
+    }
+  }
+
+  const bool use_allow = (c.mask != nullptr) || ((do_hist || do_bias) && !overflow);
+  if (use_allow) {
+#pragma unroll
+    for (int j = 0; j < kPT; ++j) {
+      const uint32_t k = key_of_bits(slot_bits<DT>(raw, j));
+      key[j] = ((allow >> j) & 1u) ? k : 0u;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kPT; ++j) key[j] = key_of_bits(slot_bits<DT>(raw, j));
+  }
+
+  if ((do_hist || do_bias) && overflow) {
+    // LDS lists overflowed: patch this thread's slots in place, scanning the
+    // request's lists in global memory (slow, rare, exact).
+#pragma unroll
+    for (int j = 0; j < kPT; ++j) {
+      if ((pbits >> j) & 1u) {
+        const int l = local_of_slot<DT>(tid, j);
+        const int id = lo + l;
+        int cntv = 0;
+        if (do_hist) {
+          for (int h = 0; h < c.nhist; ++h) cntv += (c.hist[h] == id);
+          for (int h = 0; h < c.nextra; ++h) cntv += (c.extra[h] == id);
+        }
+        float bsum = 0.0f;
+        bool hb = false;
+        if (do_bias) {
+          for (int e = 0; e < c.nbias; ++e)
+            if (c.bias_ids[e] == id) {
+              bsum = bsum + c.bias_vals[e];
+              hb = true;
+            }
+        }
+        key[j] = patched_key<DT>(c, lo, l, cntv, hb, bsum);
+      }
+    }
+    hl_n = 0;
+    bl_n = 0;
+  }
+  *hl_n_out = hl_n;
+  return (do_hist || do_bias) && !overflow ? hl_n + bl_n : 0;
+}
+
+__device__ __forceinline__ int owner_local(const Smem& S, int n, int hl_n) {
+  return n < hl_n ? (int)S.hl[n] : (int)S.bl_l[n - hl_n];
+}
+__device__ __forceinline__ uint32_t owner_key(const Smem& S, int n, int hl_n) {
+  return n < hl_n ? S.hlK[n] : S.blK[n - hl_n];
+}
+
+// ---------------------------------------------------------------------------
+// Radix digit search on a 256-bin histogram in S (wave 0).
+// Descending: find d with above(d) < want <= above(d) + h[d], above(d) =
+// elements in bins > d.  Ascending: the same with bins < d.
+// Writes (d, count before d, h[d]) to bc[0..2]; d = 256 if total < want.
+// ---------------------------------------------------------------------------
+__device__ inline void radix_digit(const uint32_t* h, uint32_t want, bool descending, uint32_t* bc) {
+  if (threadIdx.x < 64) {
+    const int l = lane();
+    uint32_t cb[4];
+    uint32_t s = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int bin = descending ? (255 - 4 * l - u) : (4 * l + u);
+      cb[u] = h[bin];
+      s += cb[u];
+    }
+    const uint32_t inc = wave_incl_scan(s);
+    const uint32_t total = __shfl(inc, 63, 64);
+    uint32_t run = inc - s;
+    if (l == 0) {
+      bc[0] = 256u;
+      bc[1] = total;
+      bc[2] = 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int bin = descending ? (255 - 4 * l - u) : (4 * l + u);
+      if (run < want && run + cb[u] >= want) {
+        bc[0] = (uint32_t)bin;
+        bc[1] = run;
+        bc[2] = cb[u];
+      }
+      run += cb[u];
+    }
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// Stream phase helpers
+// ---------------------------------------------------------------------------
+
+// q-th largest of the per-thread group maxima, resolved to the top 16 key
+// bits.  The result t satisfies #{group maxima >= t} >= q whenever q valid
+// maxima exist; otherwise kKeyFloor.
+__device__ uint32_t group_threshold(const uint32_t (&gm)[kGPT], int q, Smem& S) {
+  const int tid = threadIdx.x;
+  S.hist[tid] = 0u;
+  __syncthreads();
+#pragma unroll
+  for (int g = 0; g < kGPT; ++g) atomicAdd(&S.hist[gm[g] >> 24], 1u);
+  __syncthreads();
+  radix_digit(S.hist, (uint32_t)q, true, S.bc);
+  const uint32_t d1 = S.bc[0];
+  const uint32_t q1 = (uint32_t)q - S.bc[1];
+  __syncthreads();
+  if (d1 >= 256u) return kKeyFloor;
+  S.hist[tid] = 0u;
+  __syncthreads();
+#pragma unroll
+  for (int g = 0; g < kGPT; ++g)
+    if ((gm[g] >> 24) == d1) atomicAdd(&S.hist[(gm[g] >> 16) & 255u], 1u);
+  __syncthreads();
+  radix_digit(S.hist, q1, true, S.bc);
+  const uint32_t d2 = S.bc[0];
+  __syncthreads();
+  const uint32_t t = (d1 << 24) | ((d2 & 255u) << 16);
+  return t < kKeyFloor ? kKeyFloor : t;
+}
+
+// ---------------------------------------------------------------------------
+// Generic exact selection: the `want` largest composites (key desc, index
+// asc) among the elements a visitor produces.  The visitor is called once per
+// radix pass by every thread: visit(f) calls f(key, idx) for this thread's
+// elements (keys < kKeyFloor must be skipped by f's filter below).  Returns
+// the boundary (tk, ti): an element is selected iff key > tk or
+// (key == tk and idx <= ti).
+// ---------------------------------------------------------------------------
+template <typename Visit>
+__device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, Smem& S, uint32_t* tk_out, uint32_t* ti_out) {
+  const int tid = threadIdx.x;
+  uint32_t prefix = 0u;
+  uint32_t tk = 0u, ti = 0xFFFFFFFFu;
+  bool done = false;
+  for (int b = 3; b >= 0 && !done; --b) {
+    const int sh = 8 * b;
+    S.mhist[tid] = 0u;
+    __syncthreads();
+    visit([&](uint32_t k, uint32_t) {
+      if (k >= kKeyFloor && (b == 3 || (k >> (sh + 8)) == prefix)) atomicAdd(&S.mhist[(k >> sh) & 255u], 1u);
+    });
+    __syncthreads();
+    radix_digit(S.mhist, want, true, S.bc);
+    const uint32_t d = S.bc[0], above = S.bc[1], hd = S.bc[2];
+    __syncthreads();
+    prefix = (prefix << 8) | (d & 255u);
+    want -= above;
+    if (hd == want) {
+      tk = prefix << sh;  // every key with this prefix is selected
+      ti = 0xFFFFFFFFu;
+      done = true;
+    } else if (b == 0) {
+      tk = prefix;
+    }
+  }
+  if (!done) {
+    // ties at key tk: the `want` lowest indices
+    uint32_t ip = 0u;
+    for (int b = 2; b >= 0; --b) {  // indices < 2^24
+      const int sh = 8 * b;
+      S.mhist[tid] = 0u;
+      __syncthreads();
+      visit([&](uint32_t k, uint32_t i) {
+        if (k == tk && (b == 2 || (i >> (sh + 8)) == ip)) atomicAdd(&S.mhist[(i >> sh) & 255u], 1u);
+      });
+      __syncthreads();
+      radix_digit(S.mhist, want, false, S.bc);
+      const uint32_t d = S.bc[0], below = S.bc[1], hd = S.bc[2];
+      __syncthreads();
+      ip = (ip << 8) | (d & 255u);
+      want -= below;
+      if (hd == want) {
+        ti = (ip << sh) | ((1u << sh) - 1u);
+        break;
+      }
+      if (b == 0) ti = ip;
+    }
+  }
+  *tk_out = tk;
+  *ti_out = ti;
+}
+
+__device__ __forceinline__ bool selected(uint32_t k, uint32_t i, uint32_t tk, uint32_t ti) {
+  return k >= kKeyFloor && (k > tk || (k == tk && i <= ti));
+}
+
+// ---------------------------------------------------------------------------
+// Fallback: exact top-`want` of the whole row by streaming it again through
+// this workgroup.  Fills sel[0..n) (unordered) and returns n; *n_valid gets
+// the number of valid elements in the row.
+// ---------------------------------------------------------------------------
+// Kept out of line: it is the rare path and carries most of the register
+// pressure, which must not leak into the fast path's allocation.
+template <int DT>
+__device__ __attribute__((noinline)) int fallback_select(const KArgs& a, const Ctx& c, int want, Smem& S, uint64_t* sel, int* n_valid) {
+  const int tid = threadIdx.x;
+  const int T = a.T;
+  // pass 0: count valid elements
+  uint32_t nv_local = 0;
+  for (int j = 0; j < T; ++j) {
+    uint32_t key[kPT];
+    int hl_n;
+    const int no = load_tile<DT>(a, c, j * kTile, S, key, &hl_n);
+#pragma unroll
+    for (int s = 0; s < kPT; ++s) nv_local += key[s] >= kKeyFloor;
+    for (int n = tid; n < no; n += kBlock) {
+      const uint32_t K = owner_key(S, n, hl_n);
+      nv_local += (K != kNotOwner && K >= kKeyFloor);
+    }
+    __syncthreads();
+  }
+  const int nv = (int)block_sum(nv_local, S.red32);
+  *n_valid = nv;
+  if (want > nv) want = nv;
+  if (want <= 0) return 0;
+  auto visit_row = [&](auto&& f) {
+    for (int j = 0; j < T; ++j) {
+      uint32_t key[kPT];
+      int hl_n;
+      const int lo = j * kTile;
+      const int no = load_tile<DT>(a, c, lo, S, key, &hl_n);
+#pragma unroll
+      for (int s = 0; s < kPT; ++s) f(key[s], (uint32_t)(lo + local_of_slot<DT>(tid, s)));
+      for (int n = tid; n < no; n += kBlock) {
+        const uint32_t K = owner_key(S, n, hl_n);
+        if (K != kNotOwner) f(K, (uint32_t)(lo + owner_local(S, n, hl_n)));
+      }
+      __syncthreads();
+    }
+  };
+  uint32_t tk, ti;
+  radix_select(visit_row, (uint32_t)want, S, &tk, &ti);
+  // collect in row order
+  uint32_t base = 0;
+  for (int j = 0; j < T; ++j) {
+    uint32_t key[kPT];
+    int hl_n;
+    const int lo = j * kTile;
+    const int no = load_tile<DT>(a, c, lo, S, key, &hl_n);
+    uint32_t cntl = 0;
+#pragma unroll
+    for (int s = 0; s < kPT; ++s) cntl += selected(key[s], lo + local_of_slot<DT>(tid, s), tk, ti);
+    for (int n = tid; n < no; n += kBlock) {
+      const uint32_t K = owner_key(S, n, hl_n);
+      cntl += (K != kNotOwner) && selected(K, lo + owner_local(S, n, hl_n), tk, ti);
+    }
+    uint32_t tot;
+    uint32_t off = base + block_excl_scan(cntl, S.red32, tot);
+#pragma unroll
+    for (int s = 0; s < kPT; ++s) {
+      const uint32_t i = lo + local_of_slot<DT>(tid, s);
+      if (selected(key[s], i, tk, ti)) sel[off++] = comp_of(key[s], i);
+    }
+    for (int n = tid; n < no; n += kBlock) {
+      const uint32_t K = owner_key(S, n, hl_n);
+      const uint32_t i = lo + owner_local(S, n, hl_n);
+      if (K != kNotOwner && selected(K, i, tk, ti)) sel[off++] = comp_of(K, i);
+    }
+    base += tot;
+    __syncthreads();
+  }
+  return (int)base;
+}
+
+// ---------------------------------------------------------------------------
+// Epilogue on the exact top-k set sel[0..n_sel): min-p filter, sort of the
+// survivors, prefix sums, top-p cut, draw.  Returns the kept count n_S and
+// leaves the sorted kept prefix in sel.  Weights/prefixes of this thread's
+// chunk are returned for the caller's further use (verification).
+// ---------------------------------------------------------------------------
+struct Dist {
+  int n_s;
+  double Z_s;
+  double M, tau;
+  int chunk0, chunk_n;  // this thread's rows [chunk0, chunk0 + chunk_n) of sel
+  double w[kEPT];       // weights of the chunk
+  double incl[kEPT];    // inclusive prefix sums
+};
+
+__device__ __forceinline__ void build_dist(const KArgs& a, const Ctx& c, uint64_t Mcomp, int n_sel, Smem& S, uint64_t* sel,
+                           Dist& D) {
+  const int tid = threadIdx.x;
+  const int b = c.req;
+  const double M = (double)float_of_key(comp_key(Mcomp));
+  const double tau = (c.mode & SS_TEMP) ? (double)a.temperature[b] : 1.0;
+  D.M = M;
+  D.tau = tau;
+  const bool minp = (c.mode & SS_MINP) && a.min_p[b] > 0.0f;
+  const bool topp = (c.mode & SS_TOPP) && a.top_p[b] < 1.0f;
+  const double lt = minp ? log((double)a.min_p[b]) : 0.0;
+
+  // Z_k over the top-k set; min-p survivors
+  uint64_t e[kEPT];
+  double zl = 0.0;
+  uint32_t nm_local = 0;
+  uint32_t keep = 0;
+#pragma unroll
+  for (int m = 0; m < kEPT; ++m) {
+    const int r = tid + m * kBlock;
+    e[m] = 0;
+    if (r < n_sel) {
+      e[m] = sel[r];
+      const double y = (double)float_of_key(comp_key(e[m]));
+      zl += weight_of(y, M, tau);
+      bool kp = true;
+      if (minp && e[m] != Mcomp) {
+        const double l = (y == M) ? 0.0 : (y - M) / tau;
+        kp = l >= lt;
+      }
+      if (kp) {
+        keep |= 1u << m;
+        ++nm_local;
+      }
+    }
+  }
+  const double Zk = block_sum(zl, S.redd);
+  uint32_t n_m;
+  uint32_t off = block_excl_scan(nm_local, S.red32, n_m);  // ends with a barrier: sel reads done
+#pragma unroll
+  for (int m = 0; m < kEPT; ++m)
+    if ((keep >> m) & 1u) sel[off++] = e[m];
+  const int N = next_pow2((int)n_m);
+  for (int r = (int)n_m + tid; r < N; r += kBlock) sel[r] = 0ull;
+  __syncthreads();
+  lds_sort_desc(sel, N);
+
+  // prefix sums over the sorted min-p prefix, chunked per thread
+  const int cs = ((int)n_m + kBlock - 1) / kBlock;
+  D.chunk0 = tid * cs;
+  D.chunk_n = max(0, min(cs, (int)n_m - D.chunk0));
+  double loc = 0.0;
+  double excl_loc[kEPT];
+#pragma unroll
+  for (int m = 0; m < kEPT; ++m) {
+    D.w[m] = 0.0;
+    excl_loc[m] = 0.0;
+    if (m < D.chunk_n) {
+      const double y = (double)float_of_key(comp_key(sel[D.chunk0 + m]));
+      D.w[m] = weight_of(y, M, tau);
+      excl_loc[m] = loc;
+      loc += D.w[m];
+      D.incl[m] = loc;
+    }
+  }
+  double tot;
+  const double base = block_excl_scan(loc, S.redd, tot);
+  uint32_t np_local = 0;
+  const double thr = topp ? (double)a.top_p[b] * Zk : 0.0;
+#pragma unroll
+  for (int m = 0; m < kEPT; ++m) {
+    if (m < D.chunk_n) {
+      D.incl[m] += base;
+      if (topp && base + excl_loc[m] < thr) ++np_local;
+    }
+  }
+  int n_s = (int)n_m;
+  if (topp) {
+    int np = (int)block_sum(np_local, S.red32);
+    if (np < 1) np = 1;
+    if (np < n_s) n_s = np;
+  }
+  D.n_s = n_s;
+  // Z_S = inclusive prefix at rank n_s - 1
+  const int last = n_s - 1;
+  if (last >= D.chunk0 && last < D.chunk0 + D.chunk_n) {
+#pragma unroll
+    for (int m = 0; m < kEPT; ++m)
+      if (D.chunk0 + m == last) S.bcd[0] = D.incl[m];
+  }
+  __syncthreads();
+  D.Z_s = S.bcd[0];
+  __syncthreads();
+}
+
+// inverse CDF over the kept prefix: first rank with inclusive sum > u * Z_S
+__device__ __forceinline__ int draw_rank(const Dist& D, double u, Smem& S) {
+  const double target = u * D.Z_s;
+  uint32_t r = 0xFFFFFFFFu;
+#pragma unroll
+  for (int m = 0; m < kEPT; ++m) {
+    const int rr = D.chunk0 + m;
+    if (m < D.chunk_n && rr < D.n_s && D.incl[m] > target && (uint32_t)rr < r) r = (uint32_t)rr;
+  }
+  r = block_min(r, S.red32);
+  return r == 0xFFFFFFFFu ? D.n_s - 1 : (int)r;
+}
+
+// weight of sorted rank r (any thread may ask; broadcast through LDS)
+__device__ __forceinline__ double rank_weight(const Dist& D, int r, Smem& S) {
+  if (r >= D.chunk0 && r < D.chunk0 + D.chunk_n) {
+#pragma unroll
+    for (int m = 0; m < kEPT; ++m)
+      if (D.chunk0 + m == r) S.bcd[1] = D.w[m];
+  }
+  __syncthreads();
+  const double w = S.bcd[1];
+  __syncthreads();
+  return w;
+}
+
+// ---------------------------------------------------------------------------
+// Exact top-`want` set of a row from its tile candidates (fast path) or by
+// streaming the row again (fallback).  Writes sel[0..n) unordered.
+// ---------------------------------------------------------------------------
+template <int DT>
+__device__ __forceinline__ int select_exact(const KArgs& a, const Ctx& c, Smem& S, uint64_t* sel, int want,
+                                            uint32_t tmax, uint32_t ovf, uint32_t n_total, int* flags) {
+  const int tid = threadIdx.x;
+  const int T = a.T, row = c.row;
+  bool fast = ovf == 0u && n_total <= (uint32_t)(kRPT * kBlock);
+  uint32_t ck[kRPT], ci[kRPT];
+  uint32_t cl = 0;
+  if (fast) {
+    int jt = 0;
+#pragma unroll
+    for (int m = 0; m < kRPT; ++m) {
+      const uint32_t f = tid + m * kBlock;
+      ck[m] = 0u;
+      ci[m] = 0u;
+      if (f < n_total) {
+        while (f >= S.prefix[jt + 1]) ++jt;
+        const uint2 e = a.cand[((size_t)row * T + jt) * a.cap + (f - S.prefix[jt])];
+        if (e.x >= tmax) {
+          ck[m] = e.x;
+          ci[m] = e.y;
+          ++cl;
+        }
+      }
+    }
+  }
+  const uint32_t C = fast ? block_sum(cl, S.red32) : 0u;
+  if (fast) {
+    if (tmax == kKeyFloor) {  // every tile emitted all of its valid elements
+      if ((int)C < want) want = (int)C;
+    } else if ((int)C < want) {
+      fast = false;  // candidates do not provably contain the top-k
+    }
+  }
+  if (!fast) {
+    int nv;
+    *flags |= SS_FLAG_FALLBACK;
+    return fallback_select<DT>(a, c, want, S, sel, &nv);
+  }
+  if (want <= 0) return 0;
+  auto visit_regs = [&](auto&& f) {
+#pragma unroll
+    for (int m = 0; m < kRPT; ++m) f(ck[m], ci[m]);
+  };
+  uint32_t tk, ti;
+  radix_select(visit_regs, (uint32_t)want, S, &tk, &ti);
+  uint32_t cntl = 0;
+#pragma unroll
+  for (int m = 0; m < kRPT; ++m) cntl += selected(ck[m], ci[m], tk, ti);
+  uint32_t tot;
+  uint32_t off = block_excl_scan(cntl, S.red32, tot);
+#pragma unroll
+  for (int m = 0; m < kRPT; ++m)
+    if (selected(ck[m], ci[m], tk, ti)) sel[off++] = comp_of(ck[m], ci[m]);
+  return (int)tot;
+}
+
+// ---------------------------------------------------------------------------
+// Row merge: one workgroup per row.
+// ---------------------------------------------------------------------------
+template <int DT, int OP>
+__device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S, uint64_t* sel) {
+  const int tid = threadIdx.x;
+  const int T = a.T, row = c.row, b = c.req;
+  // tile records
+  uint4 r4 = make_uint4(0u, 0u, kNoEmit, 0u);
+  if (tid < T) r4 = a.rec[(size_t)row * T + tid];
+  const uint64_t tcomp = (tid < T && r4.x >= kKeyFloor) ? comp_of(r4.x, r4.y) : 0ull;
+  const uint64_t Mcomp = block_max(tcomp, S.red64);
+  const uint32_t tmax = block_max(tid < T ? r4.z : 0u, S.red32);
+  const uint32_t ovf = block_max((tid < T && r4.w > (uint32_t)a.cap) ? 1u : 0u, S.red32);
+  const uint32_t nj = (tid < T) ? min(r4.w, (uint32_t)a.cap) : 0u;
+  uint32_t n_total;
+  const uint32_t pre = block_excl_scan(nj, S.red32, n_total);
+  if (tid < T) S.prefix[tid] = pre;
+  if (tid == 0) S.prefix[T] = n_total;
+  __syncthreads();
+
+  int flags = c.kcap ? SS_FLAG_KCAP : 0;
+  const bool empty = Mcomp == 0ull;
+  const int argmax = empty ? -1 : (int)comp_idx(Mcomp);
+  if (empty) flags = SS_FLAG_EMPTY;
+
+  if constexpr (OP == OP_TOPK) {
+    int n_sel = 0;
+    if (!empty && c.k_eff > 0) {
+      n_sel = select_exact<DT>(a, c, S, sel, c.k_eff, tmax, ovf, n_total, &flags);
+      const int N = next_pow2(n_sel);
+      for (int r = n_sel + tid; r < N; r += kBlock) sel[r] = 0ull;
+      __syncthreads();
+      lds_sort_desc(sel, N);
+    }
+    for (int r = tid; r < a.k_cap; r += kBlock) {
+      const size_t o = (size_t)b * a.k_cap + r;
+      if (r < n_sel) {
+        a.out_val[o] = float_of_key(comp_key(sel[r]));
+        a.out_idx[o] = (int32_t)comp_idx(sel[r]);
+      } else {
+        a.out_val[o] = -__builtin_inff();
+        a.out_idx[o] = -1;
+      }
+    }
+    if (a.flags && tid == 0) a.flags[b] = flags & SS_FLAG_FALLBACK;
+    return;
+  } else {
+    int token = -1;
+    float logprob = 0.0f;
+    int accept = 0;
+    const int64_t pos = a.position ? a.position[b] + c.ell : (int64_t)c.ell;
+    const uint64_t seed = a.seed ? a.seed[b] : 0ull;
+    bool has_draft = false;
+    int dtok = -1;
+    if constexpr (OP == OP_VERIFY) {
+      if (c.ell < a.L) {
+        dtok = a.draft_tokens[(size_t)b * a.L + c.ell];
+        has_draft = dtok >= 0 && dtok < a.V;
+      }
+    }
+
+    if (!empty && c.greedy) {
+      token = argmax;
+      if constexpr (OP == OP_VERIFY) accept = has_draft && dtok == argmax;
+      if constexpr (OP == OP_PROCESS) {
+        if (tid == 0) {
+          RowSummary s;
+          s.thr = Mcomp;
+          s.Z = 1.0;
+          s.M = float_of_key(comp_key(Mcomp));
+          s.tau = 1.0f;
+          s.argmax = argmax;
+          s.kind = KIND_GREEDY;
+          a.summ[row] = s;
+        }
+      }
+      if constexpr (OP == OP_SAMPLE) {
+        if (a.out_idx) {
+          for (int r = tid; r < a.k_out; r += kBlock) {
+            a.out_idx[(size_t)b * a.k_out + r] = r == 0 ? argmax : -1;
+            a.out_prob[(size_t)b * a.k_out + r] = r == 0 ? 1.0f : 0.0f;
+          }
+        }
+      }
+    } else if (!empty) {
+      const int n_sel = select_exact<DT>(a, c, S, sel, c.k_eff, tmax, ovf, n_total, &flags);
+      __syncthreads();
+      Dist D;
+      build_dist(a, c, Mcomp, n_sel, S, sel, D);
+      const double u0 = uniform01(seed, (uint32_t)b, pos, 0);
+      if constexpr (OP == OP_PROCESS) {
+        if (tid == 0) {
+          RowSummary s;
+          s.thr = sel[D.n_s - 1];
+          s.Z = D.Z_s;
+          s.M = (float)D.M;
+          s.tau = (float)D.tau;
+          s.argmax = argmax;
+          s.kind = KIND_DIST;
+          a.summ[row] = s;
+        }
+      } else {
+        if (OP == OP_SAMPLE || !has_draft) {
+          const int r = draw_rank(D, u0, S);
+          token = (int)comp_idx(sel[r]);
+          const double w = rank_weight(D, r, S);
+          logprob = (float)log(w / D.Z_s);
+          if constexpr (OP == OP_SAMPLE) {
+            if (a.out_idx) {
+              for (int rr = tid; rr < a.k_out; rr += kBlock)
+                a.out_idx[(size_t)b * a.k_out + rr] = rr < D.n_s ? (int32_t)comp_idx(sel[rr]) : -1;
+#pragma unroll
+              for (int m = 0; m < kEPT; ++m) {
+                const int rr = D.chunk0 + m;
+                if (m < D.chunk_n && rr < D.n_s && rr < a.k_out)
+                  a.out_prob[(size_t)b * a.k_out + rr] = (float)(D.w[m] / D.Z_s);
+              }
+              for (int rr = D.n_s + tid; rr < a.k_out; rr += kBlock) a.out_prob[(size_t)b * a.k_out + rr] = 0.0f;
+              if (D.n_s > a.k_out) flags |= SS_FLAG_OUT_TRUNC;
+            }
+          }
+        } else {
+          // verification of draft token dtok against this row's distribution
+          const float* qrow = a.draft_probs + ((size_t)b * a.L + c.ell) * (size_t)a.ld_q;
+          double pd_local = 0.0;
+#pragma unroll
+          for (int m = 0; m < kEPT; ++m) {
+            const int rr = D.chunk0 + m;
+            if (m < D.chunk_n && rr < D.n_s && (int)comp_idx(sel[rr]) == dtok) pd_local = D.w[m] / D.Z_s;
+          }
+          const double Pd = block_max(pd_local, S.redd);
+          const double qd = (double)qrow[dtok];
+          const double u1 = uniform01(seed, (uint32_t)b, pos, 1);
+          accept = (Pd > 0.0 && u1 * qd <= Pd) ? 1 : 0;
+          if (!accept) {
+            // residual max(0, P - q) over the kept prefix, canonical order
+            double rw[kEPT];
+            double loc = 0.0;
+#pragma unroll
+            for (int m = 0; m < kEPT; ++m) {
+              rw[m] = 0.0;
+              const int rr = D.chunk0 + m;
+              if (m < D.chunk_n && rr < D.n_s) {
+                const double P = D.w[m] / D.Z_s;
+                const double v = P - (double)qrow[comp_idx(sel[rr])];
+                loc += v > 0.0 ? v : 0.0;
+                rw[m] = loc;  // local inclusive prefix
+              }
+            }
+            double Rtot;
+            const double base = block_excl_scan(loc, S.redd, Rtot);
+            int r;
+            if (Rtot > 0.0) {
+              const double target = u0 * Rtot;
+              uint32_t rr_min = 0xFFFFFFFFu;
+#pragma unroll
+              for (int m = 0; m < kEPT; ++m) {
+                const int rr = D.chunk0 + m;
+                if (m < D.chunk_n && rr < D.n_s && base + rw[m] > target && (uint32_t)rr < rr_min) rr_min = rr;
+              }
+              rr_min = block_min(rr_min, S.red32);
+              r = rr_min == 0xFFFFFFFFu ? D.n_s - 1 : (int)rr_min;
+            } else {
+              r = draw_rank(D, u0, S);
+            }
+            token = (int)comp_idx(sel[r]);
+          }
+        }
+      }
+    }
+
+    if constexpr (OP == OP_PROCESS) {
+      if (empty && tid == 0) {
+        RowSummary s;
+        s.thr = 0;
+        s.Z = 1.0;
+        s.M = 0.0f;
+        s.tau = 1.0f;
+        s.argmax = -1;
+        s.kind = KIND_EMPTY;
+        a.summ[row] = s;
+      }
+      if (a.flags && tid == 0) a.flags[b] = flags;
+      return;
+    } else if constexpr (OP == OP_SAMPLE) {
+      if (tid == 0) {
+        a.out_token[b] = token;
+        if (a.out_logprob) a.out_logprob[b] = logprob;
+        if (a.flags) a.flags[b] = flags;
+      }
+      if (empty && a.out_idx) {
+        for (int r = tid; r < a.k_out; r += kBlock) {
+          a.out_idx[(size_t)b * a.k_out + r] = -1;
+          a.out_prob[(size_t)b * a.k_out + r] = 0.0f;
+        }
+      }
+      return;
+    } else {
+      // publish this row's decision; the request's last row assembles
+      if (tid == 0) {
+        RowResult rr;
+        rr.accept = accept;
+        rr.emit = token;
+        rr.flags = flags;
+        rr.pad = 0;
+        a.res[row] = rr;
+      }
+      __threadfence();
+      __syncthreads();
+      if (tid == 0) {
+        const uint32_t tk = atomicAdd(&a.req_ticket[b], 1u);
+        S.bc[3] = (tk == (uint32_t)a.L) ? 1u : 0u;
+      }
+      __syncthreads();
+      if (S.bc[3] == 0u) return;
+      __threadfence();
+      if (tid == 0) {
+        a.req_ticket[b] = 0u;
+        const int L = a.L;
+        int n = 0;
+        int fl = 0;
+        int32_t* out = a.out_tokens + (size_t)b * (L + 1);
+        for (int l = 0; l <= L; ++l) out[l] = -1;
+        for (int l = 0; l <= L; ++l) {
+          const RowResult rr = a.res[(size_t)b * (L + 1) + l];
+          fl |= rr.flags;
+          if (l < L && rr.accept) {
+            out[l] = a.draft_tokens[(size_t)b * L + l];
+            ++n;
+            continue;
+          }
+          out[l] = rr.emit;
+          break;
+        }
+        a.out_nacc[b] = n;
+        if (a.flags) a.flags[b] = fl;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// The fused kernel
+// ---------------------------------------------------------------------------
+template <int DT>
+__global__ __launch_bounds__(kBlock) void ss_stream_kernel(KArgs a) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  Smem& S = *reinterpret_cast<Smem*>(smem_raw);
+  const int tid = threadIdx.x;
+  const int row = blockIdx.x / a.T;
+  const int tile = blockIdx.x - row * a.T;
+  const int lo = tile * kTile;
+  const Ctx c = make_ctx<DT>(a, row);
+
+  uint32_t key[kPT];
+  int hl_n;
+  const int n_own = load_tile<DT>(a, c, lo, S, key, &hl_n);
+
+  // group maxima and thread maximum
+  uint32_t gm[kGPT];
+#pragma unroll
+  for (int g = 0; g < kGPT; ++g) {
+    uint32_t m = key[g * kGS];
+#pragma unroll
+    for (int s = 1; s < kGS; ++s) m = max(m, key[g * kGS + s]);
+    gm[g] = m;
+  }
+  uint32_t tmax = gm[0];
+#pragma unroll
+  for (int g = 1; g < kGPT; ++g) tmax = max(tmax, gm[g]);
+  uint32_t omax = 0u;
+  for (int n = tid; n < n_own; n += kBlock) {
+    const uint32_t K = owner_key(S, n, hl_n);
+    if (K != kNotOwner) omax = max(omax, K);
+  }
+  const uint32_t Mt = block_max(max(tmax, omax), S.red32);
+  // lowest index holding the maximum
+  uint32_t aidx = 0xFFFFFFFFu;
+  if (Mt >= kKeyFloor) {
+    if (tmax == Mt) {
+#pragma unroll
+      for (int j = kPT - 1; j >= 0; --j)
+        if (key[j] == Mt) aidx = (uint32_t)(lo + local_of_slot<DT>(tid, j));
+    }
+    for (int n = tid; n < n_own; n += kBlock) {
+      const uint32_t K = owner_key(S, n, hl_n);
+      if (K != kNotOwner && K == Mt) aidx = min(aidx, (uint32_t)(lo + owner_local(S, n, hl_n)));
+    }
+  }
+  aidx = block_min(aidx, S.red32);
+
+  // candidate emission for truncating rows
+  uint32_t t = kNoEmit;
+  uint32_t n_emit = 0;
+  if (!c.greedy && c.k_eff > 0 && Mt < kKeyFloor) {
+    t = kKeyFloor;  // no valid element: everything valid (nothing) is emitted
+  } else if (!c.greedy && c.k_eff > 0) {
+    const int q = quota(c.k_eff, a.T);
+    t = (2 * q > kG) ? kKeyFloor : group_threshold(gm, q, S);
+    uint2* region = a.cand + ((size_t)row * a.T + tile) * a.cap;
+    // count (per wave, ballot)
+    uint32_t wcount = 0;
+#pragma unroll
+    for (int j = 0; j < kPT; ++j) wcount += (uint32_t)__popcll(__ballot(key[j] >= t));
+    if (lane() == 0) S.wc[wave()] = wcount;
+    uint32_t ocnt = 0;
+    for (int n = tid; n < n_own; n += kBlock) {
+      const uint32_t K = owner_key(S, n, hl_n);
+      ocnt += (K != kNotOwner && K >= t);
+    }
+    uint32_t otot;
+    const uint32_t ooff = block_excl_scan(ocnt, S.red32, otot);  // barrier also publishes S.wc
+    uint32_t base = 0, regtot = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      if (w < wave()) base += S.wc[w];
+      regtot += S.wc[w];
+    }
+    const uint32_t cap = (uint32_t)a.cap;
+#pragma unroll
+    for (int j = 0; j < kPT; ++j) {
+      const bool s = key[j] >= t;
+      const uint64_t m = __ballot(s);
+      if (m) {
+        if (s) {
+          const uint32_t p = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                               __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+          if (p < cap) region[p] = make_uint2(key[j], (uint32_t)(lo + local_of_slot<DT>(tid, j)));
+        }
+        base += (uint32_t)__popcll(m);
+      }
+    }
+    uint32_t p = regtot + ooff;
+    for (int n = tid; n < n_own; n += kBlock) {
+      const uint32_t K = owner_key(S, n, hl_n);
+      if (K != kNotOwner && K >= t) {
+        if (p < cap) region[p] = make_uint2(K, (uint32_t)(lo + owner_local(S, n, hl_n)));
+        ++p;
+      }
+    }
+    n_emit = regtot + otot;
+  }
+  if (tid == 0) a.rec[(size_t)row * a.T + tile] = make_uint4(Mt, aidx, t, n_emit);
+}
+
+// One workgroup per row: merge the tile records and candidates of the row.
+template <int DT, int OP>
+__global__ __launch_bounds__(kBlock) void ss_merge_kernel(KArgs a) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  Smem& S = *reinterpret_cast<Smem*>(smem_raw);
+  uint64_t* sel = reinterpret_cast<uint64_t*>(smem_raw + kSmemFixed);
+  const Ctx c = make_ctx<DT>(a, blockIdx.x);
+  merge_row<DT, OP>(a, c, S, sel);
+}
+
+// ---------------------------------------------------------------------------
+// Materialising pass of ss_process_logits: processed logits and final
+// probabilities for every element, from the per-row summary.
+// ---------------------------------------------------------------------------
+template <int DT>
+__global__ __launch_bounds__(kBlock) void ss_materialize_kernel(KArgs a) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  Smem& S = *reinterpret_cast<Smem*>(smem_raw);
+  const int tid = threadIdx.x;
+  const int row = blockIdx.x / a.T;
+  const int tile = blockIdx.x - row * a.T;
+  const int lo = tile * kTile;
+  const Ctx c = make_ctx<DT>(a, row);
+  uint32_t key[kPT];
+  int hl_n;
+  const int n_own = load_tile<DT>(a, c, lo, S, key, &hl_n);
+  const RowSummary s = a.summ[row];
+  const size_t ob = (size_t)row * (size_t)a.V;
+  auto prob_of = [&](uint32_t k, uint32_t i) -> float {
+    if (s.kind == KIND_EMPTY || k < kKeyFloor) return 0.0f;
+    if (s.kind == KIND_GREEDY) return (int)i == s.argmax ? 1.0f : 0.0f;
+    if (comp_of(k, i) < s.thr) return 0.0f;
+    return (float)(weight_of((double)float_of_key(k), (double)s.M, (double)s.tau) / s.Z);
+  };
+  auto logit_of = [&](uint32_t k) -> float { return k >= kKeyFloor ? float_of_key(k) : -__builtin_inff(); };
+#pragma unroll
+  for (int j = 0; j < kPT; ++j) {
+    const int l = local_of_slot<DT>(tid, j);
+    if (lo + l < a.V) {
+      const uint32_t i = (uint32_t)(lo + l);
+      if (a.out_logits) a.out_logits[ob + i] = logit_of(key[j]);
+      if (a.out_probs) a.out_probs[ob + i] = prob_of(key[j], i);
+    }
+  }
+  __threadfence();
+  __syncthreads();
+  for (int n = tid; n < n_own; n += kBlock) {
+    const uint32_t K = owner_key(S, n, hl_n);
+    if (K == kNotOwner) continue;
+    const uint32_t i = (uint32_t)(lo + owner_local(S, n, hl_n));
+    if (a.out_logits) a.out_logits[ob + i] = logit_of(K);
+    if (a.out_probs) a.out_probs[ob + i] = prob_of(K, i);
+  }
+}
+
+__global__ void ss_zero_kernel(uint32_t* p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+// ---------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------
+struct Layout {
+  int T, cap, rows;
+  size_t off_ticket, off_req, off_rec, off_cand, off_res, total;
+  int smem;
+};
+
+static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+static bool make_layout(int op, int B, int V, int L, int k_max, Layout* lay) {
+  if (B <= 0 || V <= 0 || V > SS_MAX_V || k_max < 1 || k_max > SS_MAX_K) return false;
+  if (op == OP_VERIFY && (L < 1 || L > SS_MAX_L)) return false;
+  if (op < OP_TOPK || op > OP_PROCESS) return false;
+  const int rows = op == OP_VERIFY ? B * (L + 1) : B;
+  const int T = (V + kTile - 1) / kTile;
+  const int cap = tile_cap(k_max, T);
+  size_t o = 0;
+  lay->off_ticket = o;
+  o = align256(o + (size_t)rows * 4);
+  lay->off_req = o;
+  o = align256(o + (size_t)B * 4);
+  const size_t zero_end = o;
+  (void)zero_end;
+  lay->off_rec = o;
+  o = align256(o + (size_t)rows * T * 16);
+  lay->off_cand = o;
+  o = align256(o + (size_t)rows * T * cap * 8);
+  lay->off_res = o;
+  const size_t res_bytes = op == OP_VERIFY ? sizeof(RowResult) : (op == OP_PROCESS ? sizeof(RowSummary) : 0);
+  o = align256(o + (size_t)rows * res_bytes);
+  lay->total = o;
+  lay->T = T;
+  lay->cap = cap;
+  lay->rows = rows;
+  lay->smem = kSmemFixed + 8 * next_pow2(k_max);
+  return true;
+}
+
+static uint32_t feature_mask(const ss_params* p) {
+  uint32_t f = SS_GREEDY | SS_GRAMMAR | SS_REP | SS_FREQ | SS_PRES | SS_BIAS | SS_TEMP | SS_TOPK | SS_TOPP | SS_MINP;
+  if (!p->temperature) f &= ~SS_TEMP;
+  if (!p->top_k) f &= ~SS_TOPK;
+  if (!p->top_p) f &= ~SS_TOPP;
+  if (!p->min_p) f &= ~SS_MINP;
+  if (!p->rep_penalty) f &= ~SS_REP;
+  if (!p->freq_penalty) f &= ~SS_FREQ;
+  if (!p->pres_penalty) f &= ~SS_PRES;
+  if (!p->hist_offsets || !p->hist_ids) f &= ~(SS_REP | SS_FREQ | SS_PRES);
+  if (!p->bias_offsets || !p->bias_ids || !p->bias_vals) f &= ~SS_BIAS;
+  if (!p->bitmask) f &= ~SS_GRAMMAR;
+  return f;
+}
+
+static void fill_params(KArgs& k, const ss_params* p) {
+  k.mode = p->mode;
+  k.temperature = p->temperature;
+  k.top_k = p->top_k;
+  k.top_p = p->top_p;
+  k.min_p = p->min_p;
+  k.rep = p->rep_penalty;
+  k.freq = p->freq_penalty;
+  k.pres = p->pres_penalty;
+  k.hist_off = p->hist_offsets;
+  k.hist_ids = p->hist_ids;
+  k.bias_off = p->bias_offsets;
+  k.bias_ids = p->bias_ids;
+  k.bias_vals = p->bias_vals;
+  k.bitmask = p->bitmask;
+  k.mask_ld = p->bitmask_ld;
+  k.seed = p->seed;
+  k.position = p->position;
+  k.feat = feature_mask(p);
+}
+
+static int esize(int dtype) { return dtype == SS_BF16 ? 2 : 4; }
+
+template <int DT>
+static void launch_merge(const KArgs& k, dim3 grid, dim3 block, int smem, hipStream_t st) {
+  switch (k.op) {
+    case OP_TOPK:
+      hipLaunchKernelGGL((ss_merge_kernel<DT, OP_TOPK>), grid, block, smem, st, k);
+      break;
+    case OP_SAMPLE:
+      hipLaunchKernelGGL((ss_merge_kernel<DT, OP_SAMPLE>), grid, block, smem, st, k);
+      break;
+    case OP_VERIFY:
+      hipLaunchKernelGGL((ss_merge_kernel<DT, OP_VERIFY>), grid, block, smem, st, k);
+      break;
+    default:
+      hipLaunchKernelGGL((ss_merge_kernel<DT, OP_PROCESS>), grid, block, smem, st, k);
+      break;
+  }
+}
+
+static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStream_t st, bool materialize) {
+  unsigned char* w = reinterpret_cast<unsigned char*>(ws);
+  k.T = lay.T;
+  k.cap = lay.cap;
+  k.ticket = reinterpret_cast<uint32_t*>(w + lay.off_ticket);
+  k.req_ticket = reinterpret_cast<uint32_t*>(w + lay.off_req);
+  k.rec = reinterpret_cast<uint4*>(w + lay.off_rec);
+  k.cand = reinterpret_cast<uint2*>(w + lay.off_cand);
+  k.res = reinterpret_cast<RowResult*>(w + lay.off_res);
+  k.summ = reinterpret_cast<RowSummary*>(w + lay.off_res);
+  const dim3 grid((unsigned)(lay.rows * lay.T)), rgrid((unsigned)lay.rows), block(kBlock);
+  if (dtype == SS_BF16) {
+    hipLaunchKernelGGL(ss_stream_kernel<SS_BF16>, grid, block, kSmemFixed, st, k);
+    launch_merge<SS_BF16>(k, rgrid, block, lay.smem, st);
+    if (materialize) hipLaunchKernelGGL(ss_materialize_kernel<SS_BF16>, grid, block, kSmemFixed, st, k);
+  } else {
+    hipLaunchKernelGGL(ss_stream_kernel<SS_F32>, grid, block, kSmemFixed, st, k);
+    launch_merge<SS_F32>(k, rgrid, block, lay.smem, st);
+    if (materialize) hipLaunchKernelGGL(ss_materialize_kernel<SS_F32>, grid, block, kSmemFixed, st, k);
+  }
+  return hipGetLastError() == hipSuccess ? SS_OK : SS_ERR_HIP;
+}
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+static bool params_ok(const ss_params* p, int B, int V, int rows) {
+  if (!p || p->B != B || p->V != V || !p->mode) return false;
+  if (p->bitmask && p->bitmask_ld < (int64_t)((V + 31) / 32)) return false;
+  (void)rows;
+  return true;
+}
+
+}  // namespace ss
+
+using namespace ss;
+
+extern "C" {
+
+size_t ss_workspace_bytes(int op, int B, int V, int L, int k_max, int dtype) {
+  if (dtype != SS_F32 && dtype != SS_BF16) return 0;
+  Layout lay;
+  if (!make_layout(op, B, V, L, k_max, &lay)) return 0;
+  return lay.total;
+}
+
+ss_status ss_workspace_init(void* ws, size_t ws_bytes, void* stream) {
+  if (!ws || (ws_bytes & 3u) || !aligned16(ws)) return SS_ERR_INVALID_ARG;
+  const size_t n = ws_bytes / 4;
+  if (n == 0) return SS_OK;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(ss_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
+                     reinterpret_cast<uint32_t*>(ws), n);
+  return hipGetLastError() == hipSuccess ? SS_OK : SS_ERR_HIP;
+}
+
+ss_status ss_topk(const void* x, int dtype, int B, int V, int64_t ld, const int32_t* k, int k_max,
+                  float* out_val, int32_t* out_idx, int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+  if (!x || !out_val || !out_idx || !ws || (dtype != SS_F32 && dtype != SS_BF16) || ld < V) return SS_ERR_INVALID_ARG;
+  Layout lay;
+  if (!make_layout(OP_TOPK, B, V, 0, k_max, &lay)) return SS_ERR_INVALID_ARG;
+  if (ws_bytes < lay.total || !aligned16(ws)) return SS_ERR_WORKSPACE;
+  KArgs a = {};
+  a.x = x;
+  a.ld = ld;
+  a.op = OP_TOPK;
+  a.B = B;
+  a.rows = B;
+  a.V = V;
+  a.L = 0;
+  a.k_cap = k_max;
+  a.k_out = 0;
+  a.vec_ok = aligned16(x) && ((ld * esize(dtype)) % 16 == 0);
+  a.feat = SS_TOPK;
+  a.top_k = k;
+  a.out_val = out_val;
+  a.out_idx = out_idx;
+  a.flags = flags;
+  return launch(a, dtype, lay, ws, (hipStream_t)stream, false);
+}
+
+ss_status ss_sample(const void* logits, int dtype, int64_t ld, const ss_params* p, int k_max, int32_t* out_token,
+                    float* out_logprob, int32_t* out_idx, float* out_prob, int k_out, int32_t* flags, void* ws,
+                    size_t ws_bytes, void* stream) {
+  if (!logits || !p || !out_token || !ws || (dtype != SS_F32 && dtype != SS_BF16)) return SS_ERR_INVALID_ARG;
+  if (k_out < 0 || (k_out > 0 && (!out_idx || !out_prob))) return SS_ERR_INVALID_ARG;
+  const int B = p->B, V = p->V;
+  if (ld < V || !params_ok(p, B, V, B)) return SS_ERR_INVALID_ARG;
+  Layout lay;
+  if (!make_layout(OP_SAMPLE, B, V, 0, k_max, &lay)) return SS_ERR_INVALID_ARG;
+  if (ws_bytes < lay.total || !aligned16(ws)) return SS_ERR_WORKSPACE;
+  KArgs a = {};
+  a.x = logits;
+  a.ld = ld;
+  a.op = OP_SAMPLE;
+  a.B = B;
+  a.rows = B;
+  a.V = V;
+  a.L = 0;
+  a.k_cap = k_max;
+  a.k_out = k_out;
+  a.vec_ok = aligned16(logits) && ((ld * esize(dtype)) % 16 == 0);
+  fill_params(a, p);
+  a.out_token = out_token;
+  a.out_logprob = out_logprob;
+  a.out_idx = k_out > 0 ? out_idx : nullptr;
+  a.out_prob = k_out > 0 ? out_prob : nullptr;
+  a.flags = flags;
+  return launch(a, dtype, lay, ws, (hipStream_t)stream, false);
+}
+
+ss_status ss_verify(const void* target_logits, int dtype, int64_t ld_row, const float* draft_probs, int64_t ld_q,
+                    const int32_t* draft_tokens, int L, const ss_params* p, int k_max, int32_t* out_tokens,
+                    int32_t* out_num_accepted, int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+  if (!target_logits || !p || !draft_probs || !draft_tokens || !out_tokens || !out_num_accepted || !ws)
+    return SS_ERR_INVALID_ARG;
+  if (dtype != SS_F32 && dtype != SS_BF16) return SS_ERR_INVALID_ARG;
+  const int B = p->B, V = p->V;
+  if (ld_row < V || ld_q < V || !params_ok(p, B, V, B * (L + 1))) return SS_ERR_INVALID_ARG;
+  if (!p->seed || !p->position) return SS_ERR_INVALID_ARG;
+  Layout lay;
+  if (!make_layout(OP_VERIFY, B, V, L, k_max, &lay)) return SS_ERR_INVALID_ARG;
+  if (ws_bytes < lay.total || !aligned16(ws)) return SS_ERR_WORKSPACE;
+  KArgs a = {};
+  a.x = target_logits;
+  a.ld = ld_row;
+  a.op = OP_VERIFY;
+  a.B = B;
+  a.rows = B * (L + 1);
+  a.V = V;
+  a.L = L;
+  a.k_cap = k_max;
+  a.k_out = 0;
+  a.vec_ok = aligned16(target_logits) && ((ld_row * esize(dtype)) % 16 == 0);
+  fill_params(a, p);
+  a.draft_probs = draft_probs;
+  a.ld_q = ld_q;
+  a.draft_tokens = draft_tokens;
+  a.out_tokens = out_tokens;
+  a.out_nacc = out_num_accepted;
+  a.flags = flags;
+  return launch(a, dtype, lay, ws, (hipStream_t)stream, false);
+}
+
+ss_status ss_process_logits(const void* logits, int dtype, int64_t ld, const ss_params* p, int k_max,
+                            float* out_logits, float* out_probs, int32_t* flags, void* ws, size_t ws_bytes,
+                            void* stream) {
+  if (!logits || !p || !ws || (dtype != SS_F32 && dtype != SS_BF16)) return SS_ERR_INVALID_ARG;
+  const int B = p->B, V = p->V;
+  if (ld < V || !params_ok(p, B, V, B)) return SS_ERR_INVALID_ARG;
+  Layout lay;
+  if (!make_layout(OP_PROCESS, B, V, 0, k_max, &lay)) return SS_ERR_INVALID_ARG;
+  if (ws_bytes < lay.total || !aligned16(ws)) return SS_ERR_WORKSPACE;
+  KArgs a = {};
+  a.x = logits;
+  a.ld = ld;
+  a.op = OP_PROCESS;
+  a.B = B;
+  a.rows = B;
+  a.V = V;
+  a.L = 0;
+  a.k_cap = k_max;
+  a.k_out = 0;
+  a.vec_ok = aligned16(logits) && ((ld * esize(dtype)) % 16 == 0);
+  fill_params(a, p);
+  a.out_logits = out_logits;
+  a.out_probs = out_probs;
+  a.flags = flags;
+  return launch(a, dtype, lay, ws, (hipStream_t)stream, true);
+}
+
+const char* ss_status_string(ss_status s) {
+  switch (s) {
+    case SS_OK:
+      return "ok";
+    case SS_ERR_INVALID_ARG:
+      return "invalid argument";
+    case SS_ERR_UNSUPPORTED:
+      return "unsupported";
+    case SS_ERR_WORKSPACE:
+      return "workspace too small or misaligned";
+    case SS_ERR_HIP:
+      return "HIP launch error";
+    default:
+      return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,372 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bars: top-k values/indices, greedy ids, processed logits and verification ids
+are bit-exact; probabilities and log-probabilities agree to 1e-5 relative;
+sampled ids are exact except where the oracle reports a data-dependent
+comparison within 1e-6 of its boundary (counted and printed).
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gen import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+EMPTY, FALLBACK, OUT_TRUNC, KCAP = 1, 2, 4, 8
+NEAR = 1e-6
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def ssb():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_20475_amd import binding
+    binding.lib()
+    return binding
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def run_sample(ssb, inp, k_out=0):
+    x = ssb.logits_tensor(inp)
+    prm = ssb.Params.from_arrays(inp)
+    out = ssb.sample(x, prm, inp["k_max"], k_out=k_out)
+    torch.cuda.synchronize()
+    return [_np(o) for o in out]
+
+
+def check_sample(inp, tok, lp, fl, label):
+    ref = oracle.sample(inp)
+    mism = tok != ref["token"]
+    near = mism & (ref["margin"] < NEAR)
+    bad = np.nonzero(mism & ~near)[0]
+    assert bad.size == 0, (label, bad[:10], tok[bad[:10]], ref["token"][bad[:10]], ref["margin"][bad[:10]])
+    same = ~mism
+    np.testing.assert_allclose(lp[same], ref["logprob"][same], rtol=1e-5, atol=1e-6)
+    assert np.array_equal(fl & (EMPTY | KCAP), ref["flags"] & (EMPTY | KCAP)), label
+    say(f"[{label}] rows={tok.size} near-boundary={int(near.sum())} fallback={int(((fl & FALLBACK) > 0).sum())}")
+    return ref
+
+
+# --------------------------------------------------------------------------
+# Standalone top-k
+# --------------------------------------------------------------------------
+def check_topk(ssb, inp, label):
+    x = ssb.logits_tensor(inp)
+    k = torch.from_numpy(inp["top_k"].astype(np.int32)).cuda() if inp.get("top_k") is not None else None
+    fl = torch.zeros(inp["B"], dtype=torch.int32, device="cuda")
+    say(f"[{label}] topk B={inp['B']} V={inp['V']} k_max={inp['k_max']} dtype={inp['dtype']}")
+    val, idx = ssb.topk(x, k, inp["k_max"], flags=fl)
+    torch.cuda.synchronize()
+    rv, ri = oracle.topk(inp)
+    gv, gi = _np(val), _np(idx)
+    bad = np.nonzero(~(gi == ri).all(axis=1))[0]
+    assert bad.size == 0, (label, bad[:5])
+    assert np.array_equal(gv.view(np.uint32), rv.view(np.uint32)), label
+    say(f"[{label}] ok, fallback rows={int((_np(fl) & FALLBACK > 0).sum())}")
+
+
+def test_topk_config2_full(ssb):
+    check_topk(ssb, W.config2(), "cfg2")
+
+
+@pytest.mark.parametrize("kind", ["zeros", "bf16_flat", "ties", "nan_inf", "sorted", "small_v", "odd_v"])
+def test_topk_edge_cases(ssb, kind):
+    rng = np.random.default_rng(5)
+    B, V, km, dt = 8, 40000, 600, W.F32
+    if kind == "zeros":
+        x = np.zeros((B, V), np.float32)
+    elif kind == "bf16_flat":
+        x = W.bf16_bits_from_f32(rng.uniform(128.6, 128.7, (B, V)).astype(np.float32))
+        dt = W.BF16
+    elif kind == "ties":
+        x = (rng.integers(-8, 8, (B, V)) / 4).astype(np.float32)
+    elif kind == "nan_inf":
+        x = rng.normal(0, 1, (B, V)).astype(np.float32)
+        x[:, ::5] = np.nan
+        x[:, 1::7] = -np.inf
+        x[:, 2::11] = -0.0
+        x[1] = -np.inf
+        x[2, :] = np.nan
+        x[2, 17] = 3.0
+    elif kind == "sorted":
+        x = np.sort(rng.normal(0, 1, (B, V)).astype(np.float32), axis=1)[:, ::-1].copy()
+    elif kind == "small_v":
+        V = 100
+        x = rng.normal(0, 1, (B, V)).astype(np.float32)
+        km = 64
+    else:
+        V = 40001
+        x = W.bf16_bits_from_f32(rng.normal(0, 2, (B, V)).astype(np.float32))
+        dt = W.BF16
+    k = np.array([1, 2, 50, km, 0, km - 1, 600, 7][:B], np.int32)
+    k = np.minimum(k, km)
+    inp = W.custom_rows(x, dt, k_max=km, top_k=k)
+    check_topk(ssb, inp, f"topk-{kind}")
+
+
+def test_topk_large_k_small_vocab(ssb):
+    rng = np.random.default_rng(9)
+    x = rng.normal(0, 1, (3, 20000)).astype(np.float32)
+    inp = W.custom_rows(x, W.F32, k_max=4096, top_k=np.array([4096, 4095, 3000], np.int32))
+    check_topk(ssb, inp, "topk-k4096-V20000")
+
+
+# --------------------------------------------------------------------------
+# Fused sampling
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["cfg0", "cfg1", "cfg3"])
+def test_sample_configs(ssb, name):
+    inp = W.make_config(name)
+    say(f"[{name}] sample B={inp['B']} V={inp['V']} dtype={inp['dtype']}")
+    tok, lp, fl = run_sample(ssb, inp)
+    check_sample(inp, tok, lp, fl, name)
+
+
+def test_sample_kept_distribution_outputs(ssb):
+    inp = W.config1(B=16)
+    say("[cfg1-B16] sample with k_out=64")
+    tok, lp, fl, idx, prob = run_sample(ssb, inp, k_out=64)
+    check_sample(inp, tok, lp, fl, "cfg1-kout")
+    ref = oracle.process_logits(inp)
+    for b in range(inp["B"]):
+        P = ref["P"][b]
+        n = int(np.count_nonzero(P))
+        o = np.lexsort((np.arange(P.size), -P))[:n]
+        m = min(n, 64)
+        if (inp["mode"][b] & W.MODE_GREEDY) == 0:
+            assert np.array_equal(np.sort(idx[b, :m]), np.sort(o[:m])), b
+        np.testing.assert_allclose(prob[b, :m], P[idx[b, :m]], rtol=1e-5, atol=1e-30)
+        assert np.all(idx[b, m:] == -1)
+
+
+def _edge_inputs(kind):
+    rng = np.random.default_rng(77)
+    B = 8
+    stoch = W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP | W.MODE_MINP
+    if kind == "zeros":
+        V = 30000
+        x = np.zeros((B, V), np.float32)
+        return W.custom_rows(x, W.F32, k_max=256, mode=np.full(B, stoch), top_k=np.full(B, 200),
+                             top_p=np.full(B, 0.9), min_p=np.full(B, 0.0), position=np.arange(B))
+    if kind == "bf16_flat":
+        V = 65536
+        x = W.bf16_bits_from_f32(rng.uniform(128.6, 128.7, (B, V)).astype(np.float32))
+        return W.custom_rows(x, W.BF16, k_max=128, mode=np.full(B, stoch), top_k=np.full(B, 128),
+                             top_p=np.full(B, 0.5), position=np.arange(B))
+    if kind == "ragged_odd":
+        V = 50001
+        x = W.bf16_bits_from_f32(rng.normal(0, 2, (B, V)).astype(np.float32))
+        return W.custom_rows(x, W.BF16, k_max=300, mode=np.full(B, stoch), top_k=np.arange(1, B + 1) * 37,
+                             top_p=np.full(B, 0.97), min_p=np.full(B, 0.001), temperature=np.full(B, 1.1),
+                             position=np.arange(B) + 5)
+    if kind == "small_v":
+        V = 70
+        x = rng.normal(0, 1, (B, V)).astype(np.float32)
+        return W.custom_rows(x, W.F32, k_max=64, mode=np.full(B, stoch), top_k=np.array([1, 5, 64, 0, 70, 3, 2, 9]),
+                             top_p=np.full(B, 0.99), position=np.arange(B))
+    if kind == "nan_empty":
+        V = 20000
+        x = rng.normal(0, 1, (B, V)).astype(np.float32)
+        x[0] = np.nan
+        x[1] = -np.inf
+        x[2, ::2] = np.nan
+        x[3, 1::3] = -np.inf
+        x[4, :] = -0.0
+        return W.custom_rows(x, W.F32, k_max=64, mode=np.full(B, stoch), top_k=np.full(B, 40),
+                             position=np.arange(B))
+    if kind == "no_topk":
+        V = 40000
+        x = rng.normal(0, 3, (B, V)).astype(np.float32)
+        return W.custom_rows(x, W.F32, k_max=512, mode=np.full(B, W.MODE_TEMP | W.MODE_TOPP),
+                             temperature=np.full(B, 0.8), top_p=np.full(B, 0.999), position=np.arange(B))
+    if kind == "grammar_few":
+        V = 65536
+        x = rng.normal(0, 2, (B, V)).astype(np.float32)
+        mask = np.zeros((B, V // 32), np.uint32)
+        for b in range(B):
+            ids = rng.choice(V, 10 + b, replace=False)
+            for i in ids:
+                mask[b, i >> 5] |= np.uint32(1 << (int(i) & 31))
+        mask[7] = 0
+        return W.custom_rows(x, W.F32, k_max=256, mode=np.full(B, stoch | W.MODE_GRAMMAR), top_k=np.full(B, 100),
+                             bitmask=mask, position=np.arange(B))
+    if kind == "long_history":
+        V = 65536
+        x = W.bf16_bits_from_f32(rng.normal(0, 2, (B, V)).astype(np.float32))
+        hist = [np.concatenate([rng.integers(0, 5000, 3000), rng.integers(0, V, 500)]).astype(np.int32) for _ in range(B)]
+        off = np.zeros(B + 1, np.int32)
+        off[1:] = np.cumsum([len(h) for h in hist])
+        bias_ids = [np.array([3, 3, 9, 70000, -1, 3], np.int32) for _ in range(B)]
+        bias_vals = [np.array([0.5, 0.25, -1.0, 9.0, 9.0, 0.125], np.float32) for _ in range(B)]
+        boff = np.zeros(B + 1, np.int32)
+        boff[1:] = np.cumsum([len(h) for h in bias_ids])
+        m = stoch | W.MODE_REP | W.MODE_FREQ | W.MODE_PRES | W.MODE_BIAS
+        mode = np.full(B, m)
+        mode[::2] = W.MODE_GREEDY | W.MODE_REP | W.MODE_FREQ | W.MODE_PRES | W.MODE_BIAS
+        return W.custom_rows(x, W.BF16, k_max=256, mode=mode, top_k=np.full(B, 200), top_p=np.full(B, 0.95),
+                             rep=np.full(B, 1.2), freq=np.full(B, 0.1), pres=np.full(B, 0.3),
+                             hist_offsets=off, hist_ids=np.concatenate(hist), bias_offsets=boff,
+                             bias_ids=np.concatenate(bias_ids), bias_vals=np.concatenate(bias_vals),
+                             position=np.arange(B))
+    if kind == "greedy_ties":
+        V = 30000
+        x = np.zeros((B, V), np.float32)
+        for b in range(B):
+            x[b, rng.choice(V, 5, replace=False)] = 4.0
+        return W.custom_rows(x, W.F32, k_max=64, mode=np.full(B, W.MODE_GREEDY))
+    raise KeyError(kind)
+
+
+@pytest.mark.parametrize("kind", ["zeros", "bf16_flat", "ragged_odd", "small_v", "nan_empty", "no_topk",
+                                  "grammar_few", "long_history", "greedy_ties"])
+def test_sample_edge_cases(ssb, kind):
+    inp = _edge_inputs(kind)
+    say(f"[{kind}] sample B={inp['B']} V={inp['V']}")
+    tok, lp, fl = run_sample(ssb, inp)
+    check_sample(inp, tok, lp, fl, kind)
+
+
+# --------------------------------------------------------------------------
+# Materialised pipeline
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["cfg0", "cfg1", "long_history", "nan_empty", "grammar_few"])
+def test_process_logits(ssb, name):
+    inp = W.make_config(name) if name.startswith("cfg") else _edge_inputs(name)
+    if name == "cfg1":
+        inp = W.config1(B=16)
+    say(f"[{name}] process B={inp['B']} V={inp['V']}")
+    x = ssb.logits_tensor(inp)
+    prm = ssb.Params.from_arrays(inp)
+    y, P, fl = ssb.process_logits(x, prm, inp["k_max"])
+    torch.cuda.synchronize()
+    y, P = _np(y), _np(P)
+    ref = oracle.process_logits(inp)
+    smp = oracle.sample(inp)
+    assert np.array_equal(y.view(np.uint32), ref["y"].view(np.uint32)), name
+    rows = smp["margin"] >= NEAR
+    err = np.abs(P[rows].astype(np.float64) - ref["P"][rows])
+    assert np.all(err <= 1e-5 * ref["P"][rows] + 1e-38), (name, err.max())
+    say(f"[{name}] ok, near-boundary rows skipped for P: {int((~rows).sum())}")
+
+
+# --------------------------------------------------------------------------
+# Verification
+# --------------------------------------------------------------------------
+def run_verify(ssb, inp):
+    x = ssb.logits_tensor(inp)
+    q = torch.from_numpy(np.ascontiguousarray(inp["draft_probs"], np.float32)).cuda()
+    d = torch.from_numpy(np.ascontiguousarray(inp["draft_tokens"], np.int32)).cuda()
+    prm = ssb.Params.from_arrays(inp)
+    out, nacc, fl = ssb.verify(x, q, d, prm, inp["k_max"])
+    torch.cuda.synchronize()
+    return _np(out), _np(nacc), _np(fl)
+
+
+def check_verify(inp, out, nacc, fl, label):
+    ref = oracle.verify(inp)
+    mism = ~(out == ref["tokens"]).all(axis=1) | (nacc != ref["n_acc"])
+    near = mism & (ref["margin"] < NEAR)
+    bad = np.nonzero(mism & ~near)[0]
+    assert bad.size == 0, (label, bad[:5], out[bad[:5]], ref["tokens"][bad[:5]])
+    assert np.array_equal(fl & (EMPTY | KCAP), ref["flags"] & (EMPTY | KCAP)), label
+    say(f"[{label}] requests={nacc.size} mean accepted={nacc.mean():.2f} near-boundary={int(near.sum())}")
+
+
+def test_verify_config4(ssb):
+    inp = W.config4()
+    say("[cfg4] verify B=64 L=4 V=131072")
+    out, nacc, fl = run_verify(ssb, inp)
+    check_verify(inp, out, nacc, fl, "cfg4")
+
+
+def test_verify_edge_cases(ssb):
+    rng = np.random.default_rng(41)
+    B, L, V = 12, 3, 5000
+    t = rng.normal(0, 1.5, (B, L + 1, V)).astype(np.float32)
+    q = rng.dirichlet(np.ones(V) * 0.3, size=(B, L)).astype(np.float32)
+    d = np.stack([[rng.choice(V, p=q[b, l] / q[b, l].sum()) for l in range(L)] for b in range(B)]).astype(np.int32)
+    d[1, 1] = -1          # end of draft
+    d[2, 0] = V + 5       # out-of-range draft
+    mode = np.full(B, W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP | W.MODE_REP | W.MODE_PRES)
+    mode[3] = W.MODE_GREEDY
+    mode[4] = W.MODE_GREEDY | W.MODE_REP
+    d[3, :] = np.argmax(t[3, 0])
+    hist = [rng.integers(0, V, 50).astype(np.int32) for _ in range(B)]
+    off = np.zeros(B + 1, np.int32)
+    off[1:] = np.cumsum([len(h) for h in hist])
+    inp = W.custom_rows(t.reshape(B * (L + 1), V), W.F32, k_max=256, mode=mode,
+                        temperature=np.full(B * (L + 1), 0.9), top_k=np.full(B * (L + 1), 100),
+                        top_p=np.full(B * (L + 1), 0.95), rep=np.full(B * (L + 1), 1.5),
+                        pres=np.full(B * (L + 1), 0.5), position=np.arange(B * (L + 1)) * 3)
+    for k in ("mode", "temperature", "top_k", "top_p", "min_p", "rep", "freq", "pres", "seed", "position"):
+        inp[k] = inp[k][:B]
+    inp["mode"] = mode.astype(np.uint32)
+    inp["hist_offsets"], inp["hist_ids"] = off, np.concatenate(hist)
+    inp["bias_offsets"] = np.zeros(B + 1, np.int32)
+    inp.update(x=t, B=B, L=L, draft_probs=q, draft_tokens=d)
+    say("[verify-edge] B=12 L=3 V=5000")
+    out, nacc, fl = run_verify(ssb, inp)
+    check_verify(inp, out, nacc, fl, "verify-edge")
+
+
+# --------------------------------------------------------------------------
+# Graph capture and determinism
+# --------------------------------------------------------------------------
+def test_graph_replay_matches_eager(ssb):
+    inp = W.config1()
+    x = ssb.logits_tensor(inp)
+    prm = ssb.Params.from_arrays(inp)
+    ws = ssb.workspace(ssb.OP_SAMPLE, inp["B"], inp["V"], 0, inp["k_max"], ssb.BF16)
+    tok = torch.empty(inp["B"], dtype=torch.int32, device="cuda")
+    lp = torch.empty(inp["B"], dtype=torch.float32, device="cuda")
+    fl = torch.empty(inp["B"], dtype=torch.int32, device="cuda")
+    say("[graph] eager reference")
+    ssb.sample(x, prm, inp["k_max"], out_token=tok, out_logprob=lp, flags=fl, ws=ws)
+    torch.cuda.synchronize()
+    ref = (_np(tok).copy(), _np(lp).copy())
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        ssb.sample(x, prm, inp["k_max"], out_token=tok, out_logprob=lp, flags=fl, ws=ws)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    say("[graph] capture")
+    with torch.cuda.graph(g):
+        ssb.sample(x, prm, inp["k_max"], out_token=tok, out_logprob=lp, flags=fl, ws=ws)
+    for rep in range(3):
+        tok.fill_(-7)
+        say(f"[graph] replay {rep}")
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(_np(tok), ref[0]) and np.array_equal(_np(lp), ref[1]), rep
+        # eager work between replays
+        ssb.sample(x, prm, inp["k_max"], ws=ws)
+        torch.cuda.synchronize()
+    # new step: the graph reads positions from device memory
+    prm.position.add_(1)
+    g.replay()
+    torch.cuda.synchronize()
+    inp2 = dict(inp)
+    inp2["position"] = inp["position"] + 1
+    check_sample(inp2, _np(tok), _np(lp), _np(fl), "graph-pos+1")
+
+
+def test_repeat_calls_are_bitwise_identical(ssb):
+    inp = W.config3(B=32)
+    say("[determinism] cfg3 B=32 x3")
+    outs = [run_sample(ssb, inp) for _ in range(3)]
+    for o in outs[1:]:
+        assert all(np.array_equal(a, b) for a, b in zip(outs[0], o))
