@@ -1,0 +1,288 @@
+"""Benchmark of the fused sampling hot path on one MI355X.
+
+Default workload: the heterogeneous singular batch -- B=64 requests,
+V=131072 bf16 logits, half greedy, half stochastic with per-request
+temperature / top-k / top-p / min-p, repetition / frequency / presence
+penalties over a 512-token history and a 16-entry sparse logit bias.
+One step = one ss_sample call (streaming kernel + merge kernel) on one batch.
+
+Timing: the K steps are captured in HIP graphs over R rotated logit buffers
+(R x 16.8 MB > 2 x the 256 MB Infinity Cache, so every step reads HBM) and
+replayed between two events after warm-up; value = rows / s over the timed
+region.  The streaming kernel's own duration is measured separately with two
+HIP events recorded around it (ss_set_kernel_events) over eager calls on the
+same stream; its algorithmic bytes (logits + history/bias lists + per-request
+params) over that duration give the roofline fraction against 8 TB/s.
+
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("µs per batch + rows/sec for fused sample/verify at V=2^17; "
+          "achieved HBM GB/s vs peak")
+HBM_PEAK_GBS = 8000.0
+MALL_BYTES = 256 << 20
+
+
+def _params_bytes(inp):
+    n = 0
+    for k in ("mode", "temperature", "top_k", "top_p", "min_p", "rep", "freq", "pres", "seed", "position",
+              "hist_offsets", "hist_ids", "bias_offsets", "bias_ids", "bias_vals", "bitmask"):
+        a = inp.get(k)
+        if a is not None:
+            n += np.asarray(a).nbytes
+    return n
+
+
+def algorithmic_bytes(inp, out_bytes_per_row=12):
+    """Bytes one pass must move: logits once, sparse lists, params, outputs."""
+    logits = np.asarray(inp["x"]).nbytes
+    return logits, logits + _params_bytes(inp) + out_bytes_per_row * inp["B"]
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for p in ("paper_2607_20475_amd/csrc/ss_kernel.hip", "paper_2607_20475_amd/csrc/ss_device.hpp"):
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload, n_launch_units):
+    """HBM traffic per launch from committed rocprofv3 counter summaries, or None
+    when the kernel source changed since the counters were taken."""
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as f:
+        d = json.load(f)
+    e = d.get(workload)
+    if not e or e.get("kernel_hash") != kernel_source_hash():
+        return None
+    return e.get("bytes_per_launch")
+
+
+def cpu_baseline(inp, reps):
+    import oracle
+    nthreads = os.cpu_count() or 1
+    omp = os.environ.get("OMP_NUM_THREADS")
+    if omp and omp.isdigit():
+        nthreads = min(nthreads, int(omp))
+    oracle.sample(inp, nthreads=nthreads)  # load + warm
+    t0 = time.perf_counter()
+    for r in range(reps):
+        inp2 = dict(inp)
+        inp2["position"] = inp["position"] + r
+        oracle.sample(inp2, nthreads=nthreads)
+    dt = time.perf_counter() - t0
+    rows = reps * inp["B"]
+    return dict(value=rows / dt, unit="rows/s", cores=nthreads, kind="oracle",
+                sample=f"{reps} batches x {inp['B']} rows of the same workload (positions varied), "
+                       f"{dt:.2f} s wall on {nthreads} threads")
+
+
+def bench_sample(args, torch, ssb, W):
+    inp = W.config1()
+    B, V, kmax = inp["B"], inp["V"], inp["k_max"]
+    dev = "cuda"
+    x0 = ssb.logits_tensor(inp, dev)
+    buf_bytes = x0.numel() * x0.element_size()
+    R = max(2, -(-2 * MALL_BYTES // buf_bytes))
+    xs = [x0] + [x0.clone() for _ in range(R - 1)]
+    prm = ssb.Params.from_arrays(inp, dev)
+    ws = ssb.workspace(ssb.OP_SAMPLE, B, V, 0, kmax, ssb.BF16, dev)
+    tok = torch.empty(B, dtype=torch.int32, device=dev)
+    lp = torch.empty(B, dtype=torch.float32, device=dev)
+    fl = torch.empty(B, dtype=torch.int32, device=dev)
+
+    def step(i):
+        ssb.sample(xs[i % R], prm, kmax, out_token=tok, out_logprob=lp, flags=fl, ws=ws)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # graphs of G steps cycling through the buffers
+    G = min(R, args.steps)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for i in range(G):
+            step(i)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g_full = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_full):
+        for i in range(G):
+            step(i)
+    rem = args.steps % G
+    g_rem = None
+    if rem:
+        g_rem = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_rem):
+            for i in range(rem):
+                step(i)
+    n_full = args.steps // G
+    for _ in range(2):
+        g_full.replay()
+    torch.cuda.synchronize()
+
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(n_full):
+        g_full.replay()
+    if g_rem is not None:
+        g_rem.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    ms_per_step = ms / args.steps
+
+    # streaming-kernel duration via events around it (eager calls, same stream)
+    kb = torch.cuda.Event(enable_timing=True)
+    ka = torch.cuda.Event(enable_timing=True)
+    kb.record()
+    ka.record()
+    torch.cuda.synchronize()
+    ssb.set_kernel_events(kb, ka)
+    n_k = min(args.steps, 400)
+    tot = 0.0
+    try:
+        for i in range(n_k):
+            step(i)
+            ka.synchronize()
+            tot += kb.elapsed_time(ka)
+    finally:
+        ssb.set_kernel_events(None, None)
+    kernel_us = 1000.0 * tot / n_k
+    torch.cuda.synchronize()
+    return inp, ms_per_step, kernel_us, R, fl
+
+
+def bench_verify(args, torch, ssb, W):
+    inp = W.config4()
+    B, L, V, kmax = inp["B"], inp["L"], inp["V"], inp["k_max"]
+    dev = "cuda"
+    x0 = ssb.logits_tensor(inp, dev)
+    q = torch.from_numpy(np.ascontiguousarray(inp["draft_probs"])).to(dev)
+    d = torch.from_numpy(np.ascontiguousarray(inp["draft_tokens"])).to(dev)
+    R = max(2, -(-2 * MALL_BYTES // (x0.numel() * x0.element_size())))
+    xs = [x0] + [x0.clone() for _ in range(R - 1)]
+    prm = ssb.Params.from_arrays(inp, dev)
+    ws = ssb.workspace(ssb.OP_VERIFY, B, V, L, kmax, ssb.BF16, dev)
+    out = torch.empty(B, L + 1, dtype=torch.int32, device=dev)
+    na = torch.empty(B, dtype=torch.int32, device=dev)
+    fl = torch.empty(B, dtype=torch.int32, device=dev)
+
+    def step(i):
+        ssb.verify(xs[i % R], q, d, prm, kmax, out_tokens=out, out_nacc=na, flags=fl, ws=ws)
+
+    for i in range(max(4, args.warmup // 4)):
+        step(i)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for i in range(R):
+            step(i)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(R):
+            step(i)
+    g.replay()
+    torch.cuda.synchronize()
+    reps = max(1, args.steps // (4 * R))
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    us = 1000.0 * e0.elapsed_time(e1) / (reps * R)
+    logits = x0.numel() * x0.element_size()
+    gathers = B * L * (kmax + 1) * 4  # upper bound of q gathered on the kept sets
+    alg = logits + _params_bytes(inp) + d.numel() * 4 + B * (L + 2) * 4 + gathers
+    return dict(workload="multistep verification B=64 L=4 V=131072 bf16 target, fp32 draft",
+                us_per_batch=us, requests_per_s=B / (us * 1e-6), rows_per_s=B * (L + 1) / (us * 1e-6),
+                alg_bytes=alg, GBps=alg / (us * 1e-6) / 1e9, steps=reps * R)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1024)
+    ap.add_argument("--warmup", type=int, default=32)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--no-verify", action="store_true", help="skip the secondary verification measurement")
+    ap.add_argument("--cpu-reps", type=int, default=8)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on one GPU only; --gpus must be 1 "
+              "(rows are independent, so a multi-GPU run would shard the batch with no communication)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from gen import workloads as W
+    from paper_2607_20475_amd import binding as ssb
+    ssb.lib()
+
+    inp, ms_per_step, kernel_us, R, fl = bench_sample(args, torch, ssb, W)
+    B = inp["B"]
+    logits_b, path_b = algorithmic_bytes(inp)
+    stream_b = logits_b + _params_bytes(inp)
+    us = ms_per_step * 1000.0
+    achieved = stream_b / (kernel_us * 1e-6) / 1e9
+    fallback_rows = int(((fl.cpu().numpy() & ssb.FLAG_FALLBACK) > 0).sum())
+    traffic = load_traffic("cfg1_sample", 1)
+
+    res = {
+        "metric": METRIC,
+        "value": B / (ms_per_step * 1e-3),
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "heterogeneous singular batch: fused sample B=64 V=131072 bf16, "
+                               "mixed greedy/stochastic, penalties, history 512, sparse bias 16",
+                   "B": B, "V": inp["V"], "k_max": inp["k_max"], "rotated_buffers": R},
+        "us_per_batch": us,
+        "path_GBps": path_b / (us * 1e-6) / 1e9,
+        "path_alg_bytes": path_b,
+        "fallback_rows": fallback_rows,
+        "roofline": {"bound": "hbm", "kernel": "ss_stream_kernel<bf16>", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic, "alg_bytes_per_launch": stream_b, "kernel_us": kernel_us},
+    }
+    if not args.no_verify:
+        res["verify"] = bench_verify(args, torch, ssb, W)
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_reps)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -192,6 +192,15 @@ ss_status ss_process_logits(const void *logits, int dtype, int64_t ld, const ss_
                             float *out_logits, float *out_probs, int32_t *flags, void *ws,
                             size_t ws_bytes, void *stream);
 
+/*
+ * Profiling hook.  When both handles are non-NULL hipEvent_t values, every
+ * later call records `before` on its stream immediately before its streaming
+ * (prologue + candidate) kernel and `after` immediately after it, so
+ * hipEventElapsedTime gives that kernel's duration.  NULL, NULL disables it.
+ * Process-wide, not thread-safe, and not meant for use under graph capture.
+ */
+ss_status ss_set_kernel_events(void *before, void *after);
+
 const char *ss_status_string(ss_status s);
 
 #ifdef __cplusplus

@@ -65,6 +65,8 @@ def lib():
                                 vp, vp, sz, vp]
         L.ss_process_logits.restype = i32
         L.ss_process_logits.argtypes = [vp, C.c_int, i64, C.POINTER(_Params), C.c_int, vp, vp, vp, vp, sz, vp]
+        L.ss_set_kernel_events.restype = i32
+        L.ss_set_kernel_events.argtypes = [vp, vp]
         L.ss_status_string.restype = C.c_char_p
         L.ss_status_string.argtypes = [i32]
         _lib = L
@@ -237,6 +239,14 @@ def process_logits(logits, params, k_max, out_logits=None, out_probs=None, flags
     _check(lib().ss_process_logits(_ptr(logits), dt, logits.stride(0), C.byref(p), k_max, _ptr(out_logits),
                                    _ptr(out_probs), _ptr(flags), _ptr(ws), ws.numel(), _stream()))
     return out_logits, out_probs, flags
+
+
+def set_kernel_events(before=None, after=None):
+    """Profiling hook: record two torch.cuda.Event around every later call's
+    streaming kernel (None, None disables)."""
+    hb = None if before is None else C.c_void_p(before.cuda_event)
+    ha = None if after is None else C.c_void_p(after.cuda_event)
+    _check(lib().ss_set_kernel_events(hb, ha))
 
 
 def logits_tensor(d, device="cuda"):

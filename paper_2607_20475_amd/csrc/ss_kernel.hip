@@ -1394,6 +1394,9 @@ static void fill_params(KArgs& k, const ss_params* p) {
 
 static int esize(int dtype) { return dtype == SS_BF16 ? 2 : 4; }
 
+// profiling hook (ss_set_kernel_events)
+static hipEvent_t g_ev_before = nullptr, g_ev_after = nullptr;
+
 template <int DT>
 static void launch_merge(const KArgs& k, dim3 grid, dim3 block, int smem, hipStream_t st) {
   switch (k.op) {
@@ -1423,12 +1426,16 @@ static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStr
   k.res = reinterpret_cast<RowResult*>(w + lay.off_res);
   k.summ = reinterpret_cast<RowSummary*>(w + lay.off_res);
   const dim3 grid((unsigned)(lay.rows * lay.T)), rgrid((unsigned)lay.rows), block(kBlock);
-  if (dtype == SS_BF16) {
+  if (g_ev_before) (void)hipEventRecord(g_ev_before, st);
+  if (dtype == SS_BF16)
     hipLaunchKernelGGL(ss_stream_kernel<SS_BF16>, grid, block, kSmemFixed, st, k);
+  else
+    hipLaunchKernelGGL(ss_stream_kernel<SS_F32>, grid, block, kSmemFixed, st, k);
+  if (g_ev_after) (void)hipEventRecord(g_ev_after, st);
+  if (dtype == SS_BF16) {
     launch_merge<SS_BF16>(k, rgrid, block, lay.smem, st);
     if (materialize) hipLaunchKernelGGL(ss_materialize_kernel<SS_BF16>, grid, block, kSmemFixed, st, k);
   } else {
-    hipLaunchKernelGGL(ss_stream_kernel<SS_F32>, grid, block, kSmemFixed, st, k);
     launch_merge<SS_F32>(k, rgrid, block, lay.smem, st);
     if (materialize) hipLaunchKernelGGL(ss_materialize_kernel<SS_F32>, grid, block, kSmemFixed, st, k);
   }
@@ -1581,6 +1588,13 @@ ss_status ss_process_logits(const void* logits, int dtype, int64_t ld, const ss_
   a.out_probs = out_probs;
   a.flags = flags;
   return launch(a, dtype, lay, ws, (hipStream_t)stream, true);
+}
+
+ss_status ss_set_kernel_events(void* before, void* after) {
+  if ((before == nullptr) != (after == nullptr)) return SS_ERR_INVALID_ARG;
+  g_ev_before = reinterpret_cast<hipEvent_t>(before);
+  g_ev_after = reinterpret_cast<hipEvent_t>(after);
+  return SS_OK;
 }
 
 const char* ss_status_string(ss_status s) {
