@@ -83,6 +83,15 @@ __device__ inline double weight_of(double y, double M, double tau) {
 // ---------------------------------------------------------------------------
 // wave64 / workgroup helpers
 // ---------------------------------------------------------------------------
+
+// Workgroup barrier that orders LDS only: global loads still in flight stay
+// in flight (a full __syncthreads() fence is used only where global memory
+// written by other threads must be ordered).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 __device__ __forceinline__ int lane() { return (int)__lane_id(); }
 __device__ __forceinline__ int wave() { return (int)(threadIdx.x >> 6); }
 
@@ -127,22 +136,22 @@ template <typename T>
 __device__ inline T block_max(T v, T* scratch) {
   v = wave_max(v);
   if (lane() == 0) scratch[wave()] = v;
-  __syncthreads();
+  lds_barrier();
   T r = scratch[0];
 #pragma unroll
   for (int w = 1; w < kWaves; ++w) r = scratch[w] > r ? scratch[w] : r;
-  __syncthreads();
+  lds_barrier();
   return r;
 }
 template <typename T>
 __device__ inline T block_min(T v, T* scratch) {
   v = wave_min(v);
   if (lane() == 0) scratch[wave()] = v;
-  __syncthreads();
+  lds_barrier();
   T r = scratch[0];
 #pragma unroll
   for (int w = 1; w < kWaves; ++w) r = scratch[w] < r ? scratch[w] : r;
-  __syncthreads();
+  lds_barrier();
   return r;
 }
 // Deterministic sum: fixed shuffle tree, then waves in order.
@@ -150,11 +159,11 @@ template <typename T>
 __device__ inline T block_sum(T v, T* scratch) {
   v = wave_sum(v);
   if (lane() == 0) scratch[wave()] = v;
-  __syncthreads();
+  lds_barrier();
   T r = scratch[0];
 #pragma unroll
   for (int w = 1; w < kWaves; ++w) r += scratch[w];
-  __syncthreads();
+  lds_barrier();
   return r;
 }
 // Exclusive scan over threads in thread order; returns this thread's offset,
@@ -163,7 +172,7 @@ template <typename T>
 __device__ inline T block_excl_scan(T v, T* scratch, T& total) {
   const T inc = wave_incl_scan(v);
   if (lane() == 63) scratch[wave()] = inc;
-  __syncthreads();
+  lds_barrier();
   T off = T(0), tot = T(0);
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) {
@@ -171,7 +180,7 @@ __device__ inline T block_excl_scan(T v, T* scratch, T& total) {
     if (w < wave()) off += s;
     tot += s;
   }
-  __syncthreads();
+  lds_barrier();
   total = tot;
   return off + inc - v;
 }
@@ -192,7 +201,7 @@ __device__ inline void lds_sort_desc(uint64_t* a, int n) {
           a[m] = x;
         }
       }
-      __syncthreads();
+      lds_barrier();
     }
   }
 }

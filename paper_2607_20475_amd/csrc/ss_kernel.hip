@@ -41,11 +41,15 @@ constexpr int kGS = kPT / kGPT;      // slots per group (4)
 constexpr int kG = kGPT * kBlock;    // groups per tile (2048)
 constexpr int kHCap = 1024;          // in-tile history entries held in LDS
 constexpr int kBCap = 128;           // in-tile bias entries held in LDS
+constexpr int kPCap = 128;           // patched slots per wavefront held in LDS
+constexpr int kIdsPT = 2;            // history ids each thread loads up front
 constexpr int kRPT = 32;             // merge candidates per thread (registers)
 constexpr int kMaxT = (SS_MAX_V + kTile - 1) / kTile;
 constexpr int kEPT = SS_MAX_K / kBlock;  // selected entries per thread in the epilogue
-constexpr uint32_t kNotOwner = 0xFFFFFFFFu;
+constexpr int kHCopies = 8;              // privatised histogram copies (lane & 7)
+constexpr int kHStride = 257;            // padded so copies of one bin sit in different banks
 constexpr uint32_t kNoEmit = 0xFFFFFFFFu;  // emits nothing (above every valid key)
+constexpr double kFix = 1125899906842624.0;  // 2^50: fixed-point scale of weight sums
 
 enum { OP_TOPK = SS_OP_TOPK, OP_SAMPLE = SS_OP_SAMPLE, OP_VERIFY = SS_OP_VERIFY, OP_PROCESS = SS_OP_PROCESS };
 enum { KIND_EMPTY = 0, KIND_GREEDY = 1, KIND_DIST = 2 };
@@ -112,20 +116,19 @@ struct Smem {
   uint64_t red64[kWaves];
   double redd[kWaves];
   double bcd[4];
-  uint32_t bm[kBlock];  // per-thread bits of patched slots
-  uint32_t hlK[kHCap];  // owner key per history entry (kNotOwner otherwise)
-  uint32_t blK[kBCap];
+  uint2 pw[kWaves][kPCap];  // per-wave patched slots: (lane | slot<<6 | bias<<11 | count<<12, bias sum)
+  uint32_t bm[kBlock];      // per-thread bits of patched slots
   int32_t bl_pos[kBCap];
   float bl_val[kBCap];
-  uint32_t hist[256];
-  uint32_t mhist[256];
+  uint32_t hist[kHCopies * kHStride];
   uint32_t prefix[kMaxT + 1];
-  uint32_t wc[kWaves];
+  uint32_t pw_n[kWaves];
   uint32_t red32[kWaves];
   uint32_t cnt[4];
   uint32_t bc[8];
   uint16_t hl[kHCap];
   uint16_t bl_l[kBCap];
+  uint8_t low[256];  // radix select: bin holds keys with non-zero low bits
 };
 constexpr int kSmemFixed = (int)((sizeof(Smem) + 15) & ~(size_t)15);
 
@@ -198,7 +201,7 @@ struct Ctx {
 };
 
 template <int DT>
-__device__ Ctx make_ctx(const KArgs& a, int row) {
+__device__ __forceinline__ Ctx make_ctx(const KArgs& a, int row) {
   Ctx c;
   c.row = row;
   if (a.op == OP_VERIFY) {
@@ -267,50 +270,127 @@ __host__ __device__ inline int tile_cap(int kcap, int T) {
 }
 
 // ---------------------------------------------------------------------------
-// Prologue for one patched id (local index l): count c, ordered bias sum,
-// penalties in Appendix C.1 order, each one float32 operation.
+// Prologue of one element in Appendix C.1 order, each step one float32 op:
+// repetition penalty, frequency and presence penalties (count > 0), then the
+// logit bias.  Grammar masking is applied by the caller.
 // ---------------------------------------------------------------------------
-template <int DT>
-__device__ uint32_t patched_key(const Ctx& c, int lo, int l, int count, bool has_bias, float bsum) {
-  const int64_t g = (int64_t)lo + l;
-  float v = canon(__uint_as_float(load_elem_bits<DT>(c.xrow, g)));
-  if (c.mask) {
-    const uint32_t w = c.mask[g >> 5];
-    if (((w >> (g & 31)) & 1u) == 0u) return 0u;
-  }
+__device__ __forceinline__ uint32_t penalised_key(uint32_t bits, uint32_t mode, float rep, float freq, float pres,
+                                                  int count, bool has_bias, float bsum) {
+  float v = canon(__uint_as_float(bits));
   if (count > 0) {
-    if (c.mode & SS_REP) v = (v > 0.0f) ? v / c.rep : v * c.rep;
-    if (c.mode & SS_FREQ) {
-      const float t = c.freq * (float)count;
+    if (mode & SS_REP) v = (v > 0.0f) ? v / rep : v * rep;
+    if (mode & SS_FREQ) {
+      const float t = freq * (float)count;
       v = v - t;
     }
-    if (c.mode & SS_PRES) v = v - c.pres;
+    if (mode & SS_PRES) v = v - pres;
   }
   if (has_bias) v = v + bsum;
   return key_of_float(v);
 }
 
 template <int DT>
-__device__ __forceinline__ void set_patch_bit(Smem& S, int l) {
+__device__ __forceinline__ void slot_of_local(int l, int* t, int* j) {
   constexpr int VW = DTT<DT>::VW;
   const int v = l / VW, e = l % VW;
-  const int t = v % kBlock, i = v / kBlock;
-  atomicOr(&S.bm[t], 1u << (i * VW + e));
+  *t = v % kBlock;
+  *j = (v / kBlock) * VW + e;
 }
 
-// Loads one tile and produces keys.  Slots whose id carries a penalty or bias
-// come out as 0 (excluded) and their true keys are held by owner entries in
-// LDS (S.hlK / S.blK, indexed like S.hl / S.bl_l), unless the in-tile lists
-// overflow LDS, in which case the slots are fixed in place.  Returns the
-// number of owner entries to scan (n_hl in *hl_n_out).
 template <int DT>
-__device__ int load_tile(const KArgs& a, const Ctx& c, int lo, Smem& S, uint32_t (&key)[kPT],
-                         int* hl_n_out) {
+__device__ __forceinline__ void set_patch_bit(Smem& S, int l) {
+  int t, j;
+  slot_of_local<DT>(l, &t, &j);
+  atomicOr(&S.bm[t], 1u << j);
+}
+
+// float32 bits of raw slot j for a wave-uniform j: the chunk registers are
+// viewed as one vector so the uniform index becomes register-relative moves.
+typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x32 __attribute__((ext_vector_type(32)));
+template <int DT>
+__device__ __forceinline__ uint32_t slot_bits_uniform(const uint4 (&r)[DTT<DT>::NV], int j) {
+  if constexpr (DT == SS_F32) {
+    u32x32 v;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      v[4 * q + 0] = r[q].x;
+      v[4 * q + 1] = r[q].y;
+      v[4 * q + 2] = r[q].z;
+      v[4 * q + 3] = r[q].w;
+    }
+    return v[j];
+  } else {
+    u32x16 v;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      v[4 * q + 0] = r[q].x;
+      v[4 * q + 1] = r[q].y;
+      v[4 * q + 2] = r[q].z;
+      v[4 * q + 3] = r[q].w;
+    }
+    const uint32_t w = v[j >> 1];
+    return (j & 1) ? (w & 0xFFFF0000u) : (w << 16);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Loads one tile and produces the processed keys of this thread's 32 slots
+// (0 = invalid: masked, NaN, beyond V).  The request's history / bias ids are
+// fetched before the tile so that building the in-tile patch lists overlaps
+// the tile's own loads; one owner per distinct id computes its occurrence
+// count and ordered bias sum from LDS, and the thread holding that element
+// applies the penalties to its registers.  Long lists that overflow LDS fall
+// back to per-slot scans of the global lists (rare, exact).
+// ---------------------------------------------------------------------------
+template <int DT, bool FULL>
+__device__ __forceinline__ void load_tile(const KArgs& a, const Ctx& c, int lo, Smem& S, uint32_t (&key)[kPT]) {
   constexpr int VW = DTT<DT>::VW, NV = DTT<DT>::NV, ES = DTT<DT>::ES;
   const int tid = threadIdx.x;
   const int V = a.V;
   const int n_tile = min(kTile, V - lo);
+  const bool do_hist = (c.mode & (SS_REP | SS_FREQ | SS_PRES)) && (c.nhist + c.nextra) > 0;
+  const bool do_bias = (c.mode & SS_BIAS) && c.nbias > 0;
+  const bool patch = do_hist || do_bias;
+  const int nh = c.nhist + c.nextra;
+
+  // 1. request lists and grammar words first, as a fixed sequence of loads
+  //    (disabled entries read a dummy in-bounds address), so that waiting for
+  //    them never has to drain the tile loads issued after them.
+  const int32_t* dummy = reinterpret_cast<const int32_t*>(c.xrow);
+  int hid[kIdsPT];
+#pragma unroll
+  for (int u = 0; u < kIdsPT; ++u) {
+    const int h = tid + u * kBlock;
+    const bool ok = do_hist && h < nh;
+    const int32_t* src = !ok ? dummy : (h < c.nhist ? c.hist + h : c.extra + (h - c.nhist));
+    hid[u] = *src;
+    if (!ok) hid[u] = -1;
+  }
+  const bool bok = do_bias && tid < c.nbias;
+  int bid = *(bok ? c.bias_ids + tid : dummy);
+  float bval = *(bok ? c.bias_vals + tid : reinterpret_cast<const float*>(dummy));
+  if (!bok) bid = -1;
+  uint32_t mw[NV];
+  {
+    const int W = (V + 31) >> 5;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int wi = (lo + (i * kBlock + tid) * VW) >> 5;
+      const bool ok = c.mask != nullptr && wi < W;
+      mw[i] = *(ok ? c.mask + wi : reinterpret_cast<const uint32_t*>(dummy));
+      if (!ok) mw[i] = 0u;
+    }
+  }
+
+  // 2. the tile
   uint4 raw[NV];
+  if constexpr (FULL) {
+    // full, aligned tile: all 16-byte loads in flight together
+    const uint4* src = reinterpret_cast<const uint4*>(c.xrow + (size_t)lo * ES);
+#pragma unroll
+    for (int i = 0; i < NV; ++i) raw[i] = src[i * kBlock + tid];
+  } else {
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const int l0 = (i * kBlock + tid) * VW;
@@ -336,70 +416,45 @@ __device__ int load_tile(const KArgs& a, const Ctx& c, int lo, Smem& S, uint32_t
       raw[i] = make_uint4(w[0], w[1], w[2], w[3]);
     }
   }
-
-  // grammar allow bits, one bit per slot
-  uint32_t allow = 0xFFFFFFFFu;
-  if (c.mask) {
-    allow = 0u;
-    const int W = (V + 31) >> 5;
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int g0 = lo + (i * kBlock + tid) * VW;
-      const int wi = g0 >> 5;
-      const uint32_t word = (wi < W) ? c.mask[wi] : 0u;
-      allow |= ((word >> (g0 & 31)) & ((1u << VW) - 1u)) << (i * VW);
-    }
   }
-
-  // patch lists (history / drafts / bias ids inside this tile)
-  const bool do_hist = (c.mode & (SS_REP | SS_FREQ | SS_PRES)) && (c.nhist + c.nextra) > 0;
-  const bool do_bias = (c.mode & SS_BIAS) && c.nbias > 0;
-  int hl_n = 0, bl_n = 0;
+  // 3. in-tile patch lists and owners (LDS only; overlaps the tile loads)
   bool overflow = false;
-  uint32_t pbits = 0u;
-  if (do_hist || do_bias) {
+  if (patch) {
     S.bm[tid] = 0u;
-    if (tid == 0) {
-      S.cnt[0] = 0u;
-      S.cnt[1] = 0u;
-    }
-    __syncthreads();
-    if (do_hist) {
-      const int n = c.nhist + c.nextra;
-      for (int h = tid; h < n; h += kBlock) {
-        const int id = h < c.nhist ? c.hist[h] : c.extra[h - c.nhist];
-        const int rel = id - lo;
-        if (id >= 0 && id < V && rel >= 0 && rel < n_tile) {
-          const uint32_t p = atomicAdd(&S.cnt[0], 1u);
-          if (p < (uint32_t)kHCap) S.hl[p] = (uint16_t)rel;
-          set_patch_bit<DT>(S, rel);
-        }
+    if (tid < 4) S.cnt[tid] = 0u;
+    if (tid < kWaves) S.pw_n[tid] = 0u;
+    lds_barrier();
+    auto add_hist = [&](int id) {
+      const int rel = id - lo;
+      if (id >= 0 && id < V && rel >= 0 && rel < n_tile) {
+        const uint32_t p = atomicAdd(&S.cnt[0], 1u);
+        if (p < (uint32_t)kHCap) S.hl[p] = (uint16_t)rel;
+        set_patch_bit<DT>(S, rel);
       }
-    }
-    if (do_bias) {
-      for (int e = tid; e < c.nbias; e += kBlock) {
-        const int id = c.bias_ids[e];
-        const int rel = id - lo;
-        if (id >= 0 && id < V && rel >= 0 && rel < n_tile) {
-          const uint32_t p = atomicAdd(&S.cnt[1], 1u);
-          if (p < (uint32_t)kBCap) {
-            S.bl_l[p] = (uint16_t)rel;
-            S.bl_pos[p] = e;
-            S.bl_val[p] = c.bias_vals[e];
-          }
-          set_patch_bit<DT>(S, rel);
+    };
+#pragma unroll
+    for (int u = 0; u < kIdsPT; ++u) add_hist(hid[u]);
+    for (int h = tid + kIdsPT * kBlock; h < nh; h += kBlock)  // long histories
+      add_hist(h < c.nhist ? c.hist[h] : c.extra[h - c.nhist]);
+    auto add_bias = [&](int e, int id, float val) {
+      const int rel = id - lo;
+      if (id >= 0 && id < V && rel >= 0 && rel < n_tile) {
+        const uint32_t p = atomicAdd(&S.cnt[1], 1u);
+        if (p < (uint32_t)kBCap) {
+          S.bl_l[p] = (uint16_t)rel;
+          S.bl_pos[p] = e;
+          S.bl_val[p] = val;
         }
+        set_patch_bit<DT>(S, rel);
       }
-    }
-    __syncthreads();
-    hl_n = (int)S.cnt[0];
-    bl_n = (int)S.cnt[1];
+    };
+    if (do_bias && tid < c.nbias) add_bias(tid, bid, bval);
+    for (int e = tid + kBlock; e < c.nbias; e += kBlock) add_bias(e, c.bias_ids[e], c.bias_vals[e]);
+    lds_barrier();
+    const int hl_n = (int)S.cnt[0], bl_n = (int)S.cnt[1];
     overflow = hl_n > kHCap || bl_n > kBCap;
-    pbits = S.bm[tid];
     if (!overflow) {
-      // owners: the first list entry of each distinct id computes its key
       for (int n = tid; n < hl_n + bl_n; n += kBlock) {
-        uint32_t K = kNotOwner;
         int l, cntv = 0;
         bool owner = true;
         if (n < hl_n) {
@@ -418,55 +473,85 @@ __device__ int load_tile(const KArgs& a, const Ctx& c, int lo, Smem& S, uint32_t
           for (int m = 0; m < nb && owner; ++m)
             if (S.bl_l[m] == l) owner = false;
         }
-        if (owner) {
-          float bsum = 0.0f;
-          bool hb = false;
-          if (do_bias) {
-            int last = -1;
-            for (;;) {  // entries of this id in list order
-              int best = INT_MAX, bi = -1;
-              for (int m = 0; m < bl_n; ++m)
-                if (S.bl_l[m] == l && S.bl_pos[m] > last && S.bl_pos[m] < best) {
-                  best = S.bl_pos[m];
-                  bi = m;
-                }
-              if (bi < 0) break;
-              bsum = bsum + S.bl_val[bi];
-              hb = true;
-              last = best;
-            }
+        if (!owner) continue;
+        float bsum = 0.0f;
+        bool hb = false;
+        if (do_bias) {
+          int last = -1;
+          for (;;) {  // this id's entries in list order
+            int best = INT_MAX, bi = -1;
+            for (int m = 0; m < bl_n; ++m)
+              if (S.bl_l[m] == l && S.bl_pos[m] > last && S.bl_pos[m] < best) {
+                best = S.bl_pos[m];
+                bi = m;
+              }
+            if (bi < 0) break;
+            bsum = bsum + S.bl_val[bi];
+            hb = true;
+            last = best;
           }
-          K = patched_key<DT>(c, lo, l, cntv, hb, bsum);
         }
-        if (n < hl_n)
-          S.hlK[n] = K;
-        else
-          S.blK[n - hl_n] = K;
+        int t, j;
+        slot_of_local<DT>(l, &t, &j);
+        const int w = t >> 6;
+        const uint32_t p = atomicAdd(&S.pw_n[w], 1u);
+        if (p < (uint32_t)kPCap)
+          S.pw[w][p] = make_uint2((uint32_t)(t & 63) | ((uint32_t)j << 6) | ((hb ? 1u : 0u) << 11) |
+                                      ((uint32_t)min(cntv, (1 << 20) - 1) << 12),
+                                  __float_as_uint(bsum));
       }
-      allow &= ~pbits;
+      lds_barrier();
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) overflow = overflow || S.pw_n[w] > (uint32_t)kPCap;
     }
   }
 
-  const bool use_allow = (c.mask != nullptr) || ((do_hist || do_bias) && !overflow);
-  if (use_allow) {
+  // 4. keys (grammar allow bits first: one per slot); the keys live in one
+  //    vector so a patched slot can be written with a wave-uniform index
+  uint32_t allow = 0xFFFFFFFFu;
+  if (c.mask) {
+    allow = 0u;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int g0 = lo + (i * kBlock + tid) * VW;
+      allow |= ((mw[i] >> (g0 & 31)) & ((1u << VW) - 1u)) << (i * VW);
+    }
+  }
+  u32x32 kv;
+  if (c.mask) {
 #pragma unroll
     for (int j = 0; j < kPT; ++j) {
       const uint32_t k = key_of_bits(slot_bits<DT>(raw, j));
-      key[j] = ((allow >> j) & 1u) ? k : 0u;
+      kv[j] = ((allow >> j) & 1u) ? k : 0u;
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < kPT; ++j) key[j] = key_of_bits(slot_bits<DT>(raw, j));
+    for (int j = 0; j < kPT; ++j) kv[j] = key_of_bits(slot_bits<DT>(raw, j));
   }
 
-  if ((do_hist || do_bias) && overflow) {
-    // LDS lists overflowed: patch this thread's slots in place, scanning the
-    // request's lists in global memory (slow, rare, exact).
+  // 5. penalties / bias: the holder of each patched slot rewrites its key
+  if (patch && !overflow) {
+    const int w = wave();
+    const int n = (int)S.pw_n[w];
+    for (int e = 0; e < n; ++e) {
+      const uint2 ent = S.pw[w][e];
+      const uint32_t hdr = __builtin_amdgcn_readfirstlane(ent.x);
+      const int slot = (int)((hdr >> 6) & 31u);
+      const uint32_t bits = slot_bits_uniform<DT>(raw, slot);
+      if (lane() == (int)(hdr & 63u) && ((allow >> slot) & 1u)) {
+        kv[slot] = penalised_key(bits, c.mode, c.rep, c.freq, c.pres, (int)(hdr >> 12), ((hdr >> 11) & 1u) != 0u,
+                                 __uint_as_float(__builtin_amdgcn_readfirstlane(ent.y)));
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kPT; ++j) key[j] = kv[j];
+  if (patch && overflow) {
+    const uint32_t pbits = S.bm[tid];
 #pragma unroll
     for (int j = 0; j < kPT; ++j) {
       if ((pbits >> j) & 1u) {
-        const int l = local_of_slot<DT>(tid, j);
-        const int id = lo + l;
+        const int id = lo + local_of_slot<DT>(tid, j);
         int cntv = 0;
         if (do_hist) {
           for (int h = 0; h < c.nhist; ++h) cntv += (c.hist[h] == id);
@@ -481,29 +566,30 @@ __device__ int load_tile(const KArgs& a, const Ctx& c, int lo, Smem& S, uint32_t
               hb = true;
             }
         }
-        key[j] = patched_key<DT>(c, lo, l, cntv, hb, bsum);
+        if ((allow >> j) & 1u)
+          key[j] = penalised_key(slot_bits<DT>(raw, j), c.mode, c.rep, c.freq, c.pres, cntv, hb, bsum);
       }
     }
-    hl_n = 0;
-    bl_n = 0;
   }
-  *hl_n_out = hl_n;
-  return (do_hist || do_bias) && !overflow ? hl_n + bl_n : 0;
+  if (patch) lds_barrier();  // LDS lists may be rebuilt by the caller's next tile
 }
 
-__device__ __forceinline__ int owner_local(const Smem& S, int n, int hl_n) {
-  return n < hl_n ? (int)S.hl[n] : (int)S.bl_l[n - hl_n];
-}
-__device__ __forceinline__ uint32_t owner_key(const Smem& S, int n, int hl_n) {
-  return n < hl_n ? S.hlK[n] : S.blK[n - hl_n];
-}
+// A tile takes the straight-line path when it is complete and 16-byte aligned.
+__device__ __forceinline__ bool tile_full(const KArgs& a, int lo) { return a.vec_ok && a.V - lo >= kTile; }
 
 // ---------------------------------------------------------------------------
-// Radix digit search on a 256-bin histogram in S (wave 0).
-// Descending: find d with above(d) < want <= above(d) + h[d], above(d) =
-// elements in bins > d.  Ascending: the same with bins < d.
-// Writes (d, count before d, h[d]) to bc[0..2]; d = 256 if total < want.
+// Radix digit search on a privatised 256-bin histogram (kHCopies copies,
+// stride kHStride), done by wave 0.  Descending: find d with
+// above(d) < want <= above(d) + h[d], above(d) = count in bins > d;
+// ascending: the same with bins < d.  Writes (d, count before d, h[d]) to
+// bc[0..2]; d = 256 if the total is below `want`.
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ void hist_clear(uint32_t* h) {
+  for (int i = threadIdx.x; i < kHCopies * kHStride; i += kBlock) h[i] = 0u;
+}
+__device__ __forceinline__ void hist_add(uint32_t* h, uint32_t bin) {
+  atomicAdd(&h[(lane() & (kHCopies - 1)) * kHStride + bin], 1u);
+}
 __device__ inline void radix_digit(const uint32_t* h, uint32_t want, bool descending, uint32_t* bc) {
   if (threadIdx.x < 64) {
     const int l = lane();
@@ -512,8 +598,11 @@ __device__ inline void radix_digit(const uint32_t* h, uint32_t want, bool descen
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int bin = descending ? (255 - 4 * l - u) : (4 * l + u);
-      cb[u] = h[bin];
-      s += cb[u];
+      uint32_t v = 0;
+#pragma unroll
+      for (int cp = 0; cp < kHCopies; ++cp) v += h[cp * kHStride + bin];
+      cb[u] = v;
+      s += v;
     }
     const uint32_t inc = wave_incl_scan(s);
     const uint32_t total = __shfl(inc, 63, 64);
@@ -534,66 +623,66 @@ __device__ inline void radix_digit(const uint32_t* h, uint32_t want, bool descen
       run += cb[u];
     }
   }
-  __syncthreads();
+  lds_barrier();
 }
 
-// ---------------------------------------------------------------------------
-// Stream phase helpers
-// ---------------------------------------------------------------------------
-
 // q-th largest of the per-thread group maxima, resolved to the top 16 key
-// bits.  The result t satisfies #{group maxima >= t} >= q whenever q valid
-// maxima exist; otherwise kKeyFloor.
+// bits: #{group maxima >= t} >= q whenever q valid maxima exist; kKeyFloor
+// otherwise.
 __device__ uint32_t group_threshold(const uint32_t (&gm)[kGPT], int q, Smem& S) {
-  const int tid = threadIdx.x;
-  S.hist[tid] = 0u;
-  __syncthreads();
+  hist_clear(S.hist);
+  lds_barrier();
 #pragma unroll
-  for (int g = 0; g < kGPT; ++g) atomicAdd(&S.hist[gm[g] >> 24], 1u);
-  __syncthreads();
+  for (int g = 0; g < kGPT; ++g) hist_add(S.hist, gm[g] >> 24);
+  lds_barrier();
   radix_digit(S.hist, (uint32_t)q, true, S.bc);
   const uint32_t d1 = S.bc[0];
   const uint32_t q1 = (uint32_t)q - S.bc[1];
-  __syncthreads();
+  lds_barrier();
   if (d1 >= 256u) return kKeyFloor;
-  S.hist[tid] = 0u;
-  __syncthreads();
+  hist_clear(S.hist);
+  lds_barrier();
 #pragma unroll
   for (int g = 0; g < kGPT; ++g)
-    if ((gm[g] >> 24) == d1) atomicAdd(&S.hist[(gm[g] >> 16) & 255u], 1u);
-  __syncthreads();
+    if ((gm[g] >> 24) == d1) hist_add(S.hist, (gm[g] >> 16) & 255u);
+  lds_barrier();
   radix_digit(S.hist, q1, true, S.bc);
   const uint32_t d2 = S.bc[0];
-  __syncthreads();
+  lds_barrier();
   const uint32_t t = (d1 << 24) | ((d2 & 255u) << 16);
   return t < kKeyFloor ? kKeyFloor : t;
 }
 
 // ---------------------------------------------------------------------------
 // Generic exact selection: the `want` largest composites (key desc, index
-// asc) among the elements a visitor produces.  The visitor is called once per
-// radix pass by every thread: visit(f) calls f(key, idx) for this thread's
-// elements (keys < kKeyFloor must be skipped by f's filter below).  Returns
-// the boundary (tk, ti): an element is selected iff key > tk or
+// asc) among the elements a visitor produces.  visit(f) calls f(key, idx) for
+// this thread's elements; every thread calls it the same number of times.
+// Returns the boundary (tk, ti): an element is selected iff key > tk or
 // (key == tk and idx <= ti).
 // ---------------------------------------------------------------------------
 template <typename Visit>
-__device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, Smem& S, uint32_t* tk_out, uint32_t* ti_out) {
+__device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, Smem& S, uint32_t* tk_out,
+                                             uint32_t* ti_out) {
   const int tid = threadIdx.x;
   uint32_t prefix = 0u;
   uint32_t tk = 0u, ti = 0xFFFFFFFFu;
   bool done = false;
   for (int b = 3; b >= 0 && !done; --b) {
     const int sh = 8 * b;
-    S.mhist[tid] = 0u;
-    __syncthreads();
+    hist_clear(S.hist);
+    if (b == 2) S.low[tid] = 0;
+    lds_barrier();
     visit([&](uint32_t k, uint32_t) {
-      if (k >= kKeyFloor && (b == 3 || (k >> (sh + 8)) == prefix)) atomicAdd(&S.mhist[(k >> sh) & 255u], 1u);
+      if (k >= kKeyFloor && (b == 3 || (k >> (sh + 8)) == prefix)) {
+        hist_add(S.hist, (k >> sh) & 255u);
+        if (b == 2 && (k & 0xFFFFu) != 0u) S.low[(k >> 16) & 255u] = 1;
+      }
     });
-    __syncthreads();
-    radix_digit(S.mhist, want, true, S.bc);
+    lds_barrier();
+    radix_digit(S.hist, want, true, S.bc);
     const uint32_t d = S.bc[0], above = S.bc[1], hd = S.bc[2];
-    __syncthreads();
+    const bool low_zero = (b == 2) && S.low[d & 255u] == 0;
+    lds_barrier();
     prefix = (prefix << 8) | (d & 255u);
     want -= above;
     if (hd == want) {
@@ -602,6 +691,9 @@ __device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, Smem&
       done = true;
     } else if (b == 0) {
       tk = prefix;
+    } else if (low_zero) {
+      tk = prefix << 16;  // the boundary keys are all equal: resolve ties by index
+      break;
     }
   }
   if (!done) {
@@ -609,15 +701,15 @@ __device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, Smem&
     uint32_t ip = 0u;
     for (int b = 2; b >= 0; --b) {  // indices < 2^24
       const int sh = 8 * b;
-      S.mhist[tid] = 0u;
-      __syncthreads();
+      hist_clear(S.hist);
+      lds_barrier();
       visit([&](uint32_t k, uint32_t i) {
-        if (k == tk && (b == 2 || (i >> (sh + 8)) == ip)) atomicAdd(&S.mhist[(i >> sh) & 255u], 1u);
+        if (k == tk && (b == 2 || (i >> (sh + 8)) == ip)) hist_add(S.hist, (i >> sh) & 255u);
       });
-      __syncthreads();
-      radix_digit(S.mhist, want, false, S.bc);
+      lds_barrier();
+      radix_digit(S.hist, want, false, S.bc);
       const uint32_t d = S.bc[0], below = S.bc[1], hd = S.bc[2];
-      __syncthreads();
+      lds_barrier();
       ip = (ip << 8) | (d & 255u);
       want -= below;
       if (hd == want) {
@@ -637,28 +729,25 @@ __device__ __forceinline__ bool selected(uint32_t k, uint32_t i, uint32_t tk, ui
 
 // ---------------------------------------------------------------------------
 // Fallback: exact top-`want` of the whole row by streaming it again through
-// this workgroup.  Fills sel[0..n) (unordered) and returns n; *n_valid gets
-// the number of valid elements in the row.
+// this workgroup.  Fills sel[0..n) (row order) and returns n; *n_valid gets
+// the number of valid elements in the row.  Kept out of line: it is the rare
+// path and carries most of the register pressure, which must not leak into
+// the fast path's allocation.
 // ---------------------------------------------------------------------------
-// Kept out of line: it is the rare path and carries most of the register
-// pressure, which must not leak into the fast path's allocation.
 template <int DT>
-__device__ __attribute__((noinline)) int fallback_select(const KArgs& a, const Ctx& c, int want, Smem& S, uint64_t* sel, int* n_valid) {
+__device__ __attribute__((noinline)) int fallback_select(const KArgs& a, const Ctx& c, int want, Smem& S,
+                                                         uint64_t* sel, int* n_valid) {
   const int tid = threadIdx.x;
   const int T = a.T;
-  // pass 0: count valid elements
   uint32_t nv_local = 0;
   for (int j = 0; j < T; ++j) {
     uint32_t key[kPT];
-    int hl_n;
-    const int no = load_tile<DT>(a, c, j * kTile, S, key, &hl_n);
+    if (tile_full(a, j * kTile))
+      load_tile<DT, true>(a, c, j * kTile, S, key);
+    else
+      load_tile<DT, false>(a, c, j * kTile, S, key);
 #pragma unroll
     for (int s = 0; s < kPT; ++s) nv_local += key[s] >= kKeyFloor;
-    for (int n = tid; n < no; n += kBlock) {
-      const uint32_t K = owner_key(S, n, hl_n);
-      nv_local += (K != kNotOwner && K >= kKeyFloor);
-    }
-    __syncthreads();
   }
   const int nv = (int)block_sum(nv_local, S.red32);
   *n_valid = nv;
@@ -667,34 +756,28 @@ __device__ __attribute__((noinline)) int fallback_select(const KArgs& a, const C
   auto visit_row = [&](auto&& f) {
     for (int j = 0; j < T; ++j) {
       uint32_t key[kPT];
-      int hl_n;
       const int lo = j * kTile;
-      const int no = load_tile<DT>(a, c, lo, S, key, &hl_n);
+      if (tile_full(a, lo))
+        load_tile<DT, true>(a, c, lo, S, key);
+      else
+        load_tile<DT, false>(a, c, lo, S, key);
 #pragma unroll
       for (int s = 0; s < kPT; ++s) f(key[s], (uint32_t)(lo + local_of_slot<DT>(tid, s)));
-      for (int n = tid; n < no; n += kBlock) {
-        const uint32_t K = owner_key(S, n, hl_n);
-        if (K != kNotOwner) f(K, (uint32_t)(lo + owner_local(S, n, hl_n)));
-      }
-      __syncthreads();
     }
   };
   uint32_t tk, ti;
   radix_select(visit_row, (uint32_t)want, S, &tk, &ti);
-  // collect in row order
   uint32_t base = 0;
   for (int j = 0; j < T; ++j) {
     uint32_t key[kPT];
-    int hl_n;
     const int lo = j * kTile;
-    const int no = load_tile<DT>(a, c, lo, S, key, &hl_n);
+    if (tile_full(a, lo))
+      load_tile<DT, true>(a, c, lo, S, key);
+    else
+      load_tile<DT, false>(a, c, lo, S, key);
     uint32_t cntl = 0;
 #pragma unroll
     for (int s = 0; s < kPT; ++s) cntl += selected(key[s], lo + local_of_slot<DT>(tid, s), tk, ti);
-    for (int n = tid; n < no; n += kBlock) {
-      const uint32_t K = owner_key(S, n, hl_n);
-      cntl += (K != kNotOwner) && selected(K, lo + owner_local(S, n, hl_n), tk, ti);
-    }
     uint32_t tot;
     uint32_t off = base + block_excl_scan(cntl, S.red32, tot);
 #pragma unroll
@@ -702,22 +785,18 @@ __device__ __attribute__((noinline)) int fallback_select(const KArgs& a, const C
       const uint32_t i = lo + local_of_slot<DT>(tid, s);
       if (selected(key[s], i, tk, ti)) sel[off++] = comp_of(key[s], i);
     }
-    for (int n = tid; n < no; n += kBlock) {
-      const uint32_t K = owner_key(S, n, hl_n);
-      const uint32_t i = lo + owner_local(S, n, hl_n);
-      if (K != kNotOwner && selected(K, i, tk, ti)) sel[off++] = comp_of(K, i);
-    }
+
     base += tot;
-    __syncthreads();
   }
   return (int)base;
 }
 
 // ---------------------------------------------------------------------------
 // Epilogue on the exact top-k set sel[0..n_sel): min-p filter, sort of the
-// survivors, prefix sums, top-p cut, draw.  Returns the kept count n_S and
-// leaves the sorted kept prefix in sel.  Weights/prefixes of this thread's
-// chunk are returned for the caller's further use (verification).
+// survivors, prefix sums, top-p cut (Alg. 11 order).  Leaves the sorted kept
+// prefix in sel; each thread keeps the weights / inclusive sums of its chunk.
+// Z_k is summed in 2^-50 fixed point so that it does not depend on the order
+// in which candidates arrived.
 // ---------------------------------------------------------------------------
 struct Dist {
   int n_s;
@@ -728,8 +807,8 @@ struct Dist {
   double incl[kEPT];    // inclusive prefix sums
 };
 
-__device__ __forceinline__ void build_dist(const KArgs& a, const Ctx& c, uint64_t Mcomp, int n_sel, Smem& S, uint64_t* sel,
-                           Dist& D) {
+__device__ __forceinline__ void build_dist(const KArgs& a, const Ctx& c, uint64_t Mcomp, int n_sel, Smem& S,
+                                           uint64_t* sel, Dist& D) {
   const int tid = threadIdx.x;
   const int b = c.req;
   const double M = (double)float_of_key(comp_key(Mcomp));
@@ -740,9 +819,8 @@ __device__ __forceinline__ void build_dist(const KArgs& a, const Ctx& c, uint64_
   const bool topp = (c.mode & SS_TOPP) && a.top_p[b] < 1.0f;
   const double lt = minp ? log((double)a.min_p[b]) : 0.0;
 
-  // Z_k over the top-k set; min-p survivors
   uint64_t e[kEPT];
-  double zl = 0.0;
+  uint64_t zl = 0;
   uint32_t nm_local = 0;
   uint32_t keep = 0;
 #pragma unroll
@@ -752,7 +830,7 @@ __device__ __forceinline__ void build_dist(const KArgs& a, const Ctx& c, uint64_
     if (r < n_sel) {
       e[m] = sel[r];
       const double y = (double)float_of_key(comp_key(e[m]));
-      zl += weight_of(y, M, tau);
+      if (topp) zl += (uint64_t)__double2ll_rn(weight_of(y, M, tau) * kFix);
       bool kp = true;
       if (minp && e[m] != Mcomp) {
         const double l = (y == M) ? 0.0 : (y - M) / tau;
@@ -764,7 +842,7 @@ __device__ __forceinline__ void build_dist(const KArgs& a, const Ctx& c, uint64_
       }
     }
   }
-  const double Zk = block_sum(zl, S.redd);
+  const double Zk = topp ? (double)block_sum(zl, S.red64) / kFix : 0.0;
   uint32_t n_m;
   uint32_t off = block_excl_scan(nm_local, S.red32, n_m);  // ends with a barrier: sel reads done
 #pragma unroll
@@ -772,7 +850,7 @@ __device__ __forceinline__ void build_dist(const KArgs& a, const Ctx& c, uint64_
     if ((keep >> m) & 1u) sel[off++] = e[m];
   const int N = next_pow2((int)n_m);
   for (int r = (int)n_m + tid; r < N; r += kBlock) sel[r] = 0ull;
-  __syncthreads();
+  lds_barrier();
   lds_sort_desc(sel, N);
 
   // prefix sums over the sorted min-p prefix, chunked per thread
@@ -818,9 +896,9 @@ __device__ __forceinline__ void build_dist(const KArgs& a, const Ctx& c, uint64_
     for (int m = 0; m < kEPT; ++m)
       if (D.chunk0 + m == last) S.bcd[0] = D.incl[m];
   }
-  __syncthreads();
+  lds_barrier();
   D.Z_s = S.bcd[0];
-  __syncthreads();
+  lds_barrier();
 }
 
 // inverse CDF over the kept prefix: first rank with inclusive sum > u * Z_S
@@ -836,16 +914,16 @@ __device__ __forceinline__ int draw_rank(const Dist& D, double u, Smem& S) {
   return r == 0xFFFFFFFFu ? D.n_s - 1 : (int)r;
 }
 
-// weight of sorted rank r (any thread may ask; broadcast through LDS)
+// weight of sorted rank r (broadcast through LDS)
 __device__ __forceinline__ double rank_weight(const Dist& D, int r, Smem& S) {
   if (r >= D.chunk0 && r < D.chunk0 + D.chunk_n) {
 #pragma unroll
     for (int m = 0; m < kEPT; ++m)
       if (D.chunk0 + m == r) S.bcd[1] = D.w[m];
   }
-  __syncthreads();
+  lds_barrier();
   const double w = S.bcd[1];
-  __syncthreads();
+  lds_barrier();
   return w;
 }
 
@@ -862,14 +940,20 @@ __device__ __forceinline__ int select_exact(const KArgs& a, const Ctx& c, Smem& 
   uint32_t ck[kRPT], ci[kRPT];
   uint32_t cl = 0;
   if (fast) {
-    int jt = 0;
+    // flattened candidate f -> (tile, offset) by binary search of the prefix
+    int lgT = 0;
+    while ((1 << lgT) < T) ++lgT;
 #pragma unroll
     for (int m = 0; m < kRPT; ++m) {
       const uint32_t f = tid + m * kBlock;
       ck[m] = 0u;
       ci[m] = 0u;
       if (f < n_total) {
-        while (f >= S.prefix[jt + 1]) ++jt;
+        int jt = 0;
+        for (int s2 = lgT - 1; s2 >= 0; --s2) {
+          const int probe = jt + (1 << s2);
+          if (probe < T && S.prefix[probe] <= f) jt = probe;
+        }
         const uint2 e = a.cand[((size_t)row * T + jt) * a.cap + (f - S.prefix[jt])];
         if (e.x >= tmax) {
           ck[m] = e.x;
@@ -929,7 +1013,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S,
   const uint32_t pre = block_excl_scan(nj, S.red32, n_total);
   if (tid < T) S.prefix[tid] = pre;
   if (tid == 0) S.prefix[T] = n_total;
-  __syncthreads();
+  lds_barrier();
 
   int flags = c.kcap ? SS_FLAG_KCAP : 0;
   const bool empty = Mcomp == 0ull;
@@ -942,7 +1026,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S,
       n_sel = select_exact<DT>(a, c, S, sel, c.k_eff, tmax, ovf, n_total, &flags);
       const int N = next_pow2(n_sel);
       for (int r = n_sel + tid; r < N; r += kBlock) sel[r] = 0ull;
-      __syncthreads();
+      lds_barrier();
       lds_sort_desc(sel, N);
     }
     for (int r = tid; r < a.k_cap; r += kBlock) {
@@ -997,7 +1081,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S,
       }
     } else if (!empty) {
       const int n_sel = select_exact<DT>(a, c, S, sel, c.k_eff, tmax, ovf, n_total, &flags);
-      __syncthreads();
+      lds_barrier();
       Dist D;
       build_dist(a, c, Mcomp, n_sel, S, sel, D);
       const double u0 = uniform01(seed, (uint32_t)b, pos, 0);
@@ -1153,21 +1237,16 @@ __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S,
 }
 
 // ---------------------------------------------------------------------------
-// The fused kernel
+// Streaming kernel: one workgroup per (row, tile).  Tile maximum and argmax
+// for every row; for truncating rows, candidate emission above a per-tile
+// threshold (the q-th largest of 2048 group maxima, q = quota(k, T)).
 // ---------------------------------------------------------------------------
-template <int DT>
-__global__ __launch_bounds__(kBlock) void ss_stream_kernel(KArgs a) {
-  extern __shared__ __align__(16) unsigned char smem_raw[];
-  Smem& S = *reinterpret_cast<Smem*>(smem_raw);
+template <int DT, bool FULL>
+__device__ __forceinline__ void stream_tile(const KArgs& a, const Ctx& c, Smem& S, int row, int tile) {
   const int tid = threadIdx.x;
-  const int row = blockIdx.x / a.T;
-  const int tile = blockIdx.x - row * a.T;
   const int lo = tile * kTile;
-  const Ctx c = make_ctx<DT>(a, row);
-
   uint32_t key[kPT];
-  int hl_n;
-  const int n_own = load_tile<DT>(a, c, lo, S, key, &hl_n);
+  load_tile<DT, FULL>(a, c, lo, S, key);
 
   // group maxima and thread maximum
   uint32_t gm[kGPT];
@@ -1178,82 +1257,77 @@ __global__ __launch_bounds__(kBlock) void ss_stream_kernel(KArgs a) {
     for (int s = 1; s < kGS; ++s) m = max(m, key[g * kGS + s]);
     gm[g] = m;
   }
+
   uint32_t tmax = gm[0];
 #pragma unroll
   for (int g = 1; g < kGPT; ++g) tmax = max(tmax, gm[g]);
-  uint32_t omax = 0u;
-  for (int n = tid; n < n_own; n += kBlock) {
-    const uint32_t K = owner_key(S, n, hl_n);
-    if (K != kNotOwner) omax = max(omax, K);
-  }
-  const uint32_t Mt = block_max(max(tmax, omax), S.red32);
+  const uint32_t Mt = block_max(tmax, S.red32);
   // lowest index holding the maximum
   uint32_t aidx = 0xFFFFFFFFu;
-  if (Mt >= kKeyFloor) {
-    if (tmax == Mt) {
+  if (Mt >= kKeyFloor && tmax == Mt) {
 #pragma unroll
-      for (int j = kPT - 1; j >= 0; --j)
-        if (key[j] == Mt) aidx = (uint32_t)(lo + local_of_slot<DT>(tid, j));
-    }
-    for (int n = tid; n < n_own; n += kBlock) {
-      const uint32_t K = owner_key(S, n, hl_n);
-      if (K != kNotOwner && K == Mt) aidx = min(aidx, (uint32_t)(lo + owner_local(S, n, hl_n)));
-    }
+    for (int j = kPT - 1; j >= 0; --j)
+      if (key[j] == Mt) aidx = (uint32_t)(lo + local_of_slot<DT>(tid, j));
+
   }
   aidx = block_min(aidx, S.red32);
 
-  // candidate emission for truncating rows
   uint32_t t = kNoEmit;
   uint32_t n_emit = 0;
-  if (!c.greedy && c.k_eff > 0 && Mt < kKeyFloor) {
-    t = kKeyFloor;  // no valid element: everything valid (nothing) is emitted
-  } else if (!c.greedy && c.k_eff > 0) {
-    const int q = quota(c.k_eff, a.T);
-    t = (2 * q > kG) ? kKeyFloor : group_threshold(gm, q, S);
-    uint2* region = a.cand + ((size_t)row * a.T + tile) * a.cap;
-    // count (per wave, ballot)
-    uint32_t wcount = 0;
+  if (!c.greedy && c.k_eff > 0) {
+    if (Mt < kKeyFloor) {
+      t = kKeyFloor;  // nothing valid here: everything valid (nothing) is emitted
+    } else {
+      const int q = quota(c.k_eff, a.T);
+      if (tid == 0) S.bc[5] = 0u;
+      if (2 * q > kG) {
+        t = kKeyFloor;
+        lds_barrier();
+      } else {
+        t = group_threshold(gm, q, S);  // starts with a barrier
+      }
+      uint2* region = a.cand + ((size_t)row * a.T + tile) * a.cap;
+      uint32_t wcount = 0;
 #pragma unroll
-    for (int j = 0; j < kPT; ++j) wcount += (uint32_t)__popcll(__ballot(key[j] >= t));
-    if (lane() == 0) S.wc[wave()] = wcount;
-    uint32_t ocnt = 0;
-    for (int n = tid; n < n_own; n += kBlock) {
-      const uint32_t K = owner_key(S, n, hl_n);
-      ocnt += (K != kNotOwner && K >= t);
-    }
-    uint32_t otot;
-    const uint32_t ooff = block_excl_scan(ocnt, S.red32, otot);  // barrier also publishes S.wc
-    uint32_t base = 0, regtot = 0;
+      for (int j = 0; j < kPT; ++j) wcount += (uint32_t)__popcll(__ballot(key[j] >= t));
+
+      uint32_t base = 0;
+      if (lane() == 0) base = atomicAdd(&S.bc[5], wcount);
+      base = __builtin_amdgcn_readfirstlane(base);
+      const uint32_t cap = (uint32_t)a.cap;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      if (w < wave()) base += S.wc[w];
-      regtot += S.wc[w];
-    }
-    const uint32_t cap = (uint32_t)a.cap;
-#pragma unroll
-    for (int j = 0; j < kPT; ++j) {
-      const bool s = key[j] >= t;
-      const uint64_t m = __ballot(s);
-      if (m) {
-        if (s) {
-          const uint32_t p = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                               __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-          if (p < cap) region[p] = make_uint2(key[j], (uint32_t)(lo + local_of_slot<DT>(tid, j)));
+      for (int j = 0; j < kPT; ++j) {
+        const bool s = key[j] >= t;
+        const uint64_t m = __ballot(s);
+        if (m) {
+          if (s) {
+            const uint32_t p = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+            if (p < cap) region[p] = make_uint2(key[j], (uint32_t)(lo + local_of_slot<DT>(tid, j)));
+          }
+          base += (uint32_t)__popcll(m);
         }
-        base += (uint32_t)__popcll(m);
       }
+
+      lds_barrier();
+      n_emit = S.bc[5];
     }
-    uint32_t p = regtot + ooff;
-    for (int n = tid; n < n_own; n += kBlock) {
-      const uint32_t K = owner_key(S, n, hl_n);
-      if (K != kNotOwner && K >= t) {
-        if (p < cap) region[p] = make_uint2(K, (uint32_t)(lo + owner_local(S, n, hl_n)));
-        ++p;
-      }
-    }
-    n_emit = regtot + otot;
   }
   if (tid == 0) a.rec[(size_t)row * a.T + tile] = make_uint4(Mt, aidx, t, n_emit);
+}
+
+template <int DT>
+__global__ __launch_bounds__(kBlock) void ss_stream_kernel(KArgs a) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  Smem& S = *reinterpret_cast<Smem*>(smem_raw);
+  const int row = blockIdx.x / a.T;
+  const int tile = blockIdx.x - row * a.T;
+  const Ctx c = make_ctx<DT>(a, row);
+  // two straight-line copies: the full-tile path keeps every load in flight
+  if (tile_full(a, tile * kTile))
+    stream_tile<DT, true>(a, c, S, row, tile);
+  else
+    stream_tile<DT, false>(a, c, S, row, tile);
 }
 
 // One workgroup per row: merge the tile records and candidates of the row.
@@ -1280,34 +1354,28 @@ __global__ __launch_bounds__(kBlock) void ss_materialize_kernel(KArgs a) {
   const int lo = tile * kTile;
   const Ctx c = make_ctx<DT>(a, row);
   uint32_t key[kPT];
-  int hl_n;
-  const int n_own = load_tile<DT>(a, c, lo, S, key, &hl_n);
+  if (tile_full(a, lo))
+    load_tile<DT, true>(a, c, lo, S, key);
+  else
+    load_tile<DT, false>(a, c, lo, S, key);
   const RowSummary s = a.summ[row];
   const size_t ob = (size_t)row * (size_t)a.V;
-  auto prob_of = [&](uint32_t k, uint32_t i) -> float {
-    if (s.kind == KIND_EMPTY || k < kKeyFloor) return 0.0f;
-    if (s.kind == KIND_GREEDY) return (int)i == s.argmax ? 1.0f : 0.0f;
-    if (comp_of(k, i) < s.thr) return 0.0f;
-    return (float)(weight_of((double)float_of_key(k), (double)s.M, (double)s.tau) / s.Z);
+  auto emit = [&](uint32_t k, uint32_t i) {
+    if (a.out_logits) a.out_logits[ob + i] = k >= kKeyFloor ? float_of_key(k) : -__builtin_inff();
+    if (a.out_probs) {
+      float p = 0.0f;
+      if (s.kind == KIND_GREEDY) {
+        p = (int)i == s.argmax ? 1.0f : 0.0f;
+      } else if (s.kind == KIND_DIST && k >= kKeyFloor && comp_of(k, i) >= s.thr) {
+        p = (float)(weight_of((double)float_of_key(k), (double)s.M, (double)s.tau) / s.Z);
+      }
+      a.out_probs[ob + i] = p;
+    }
   };
-  auto logit_of = [&](uint32_t k) -> float { return k >= kKeyFloor ? float_of_key(k) : -__builtin_inff(); };
 #pragma unroll
   for (int j = 0; j < kPT; ++j) {
     const int l = local_of_slot<DT>(tid, j);
-    if (lo + l < a.V) {
-      const uint32_t i = (uint32_t)(lo + l);
-      if (a.out_logits) a.out_logits[ob + i] = logit_of(key[j]);
-      if (a.out_probs) a.out_probs[ob + i] = prob_of(key[j], i);
-    }
-  }
-  __threadfence();
-  __syncthreads();
-  for (int n = tid; n < n_own; n += kBlock) {
-    const uint32_t K = owner_key(S, n, hl_n);
-    if (K == kNotOwner) continue;
-    const uint32_t i = (uint32_t)(lo + owner_local(S, n, hl_n));
-    if (a.out_logits) a.out_logits[ob + i] = logit_of(K);
-    if (a.out_probs) a.out_probs[ob + i] = prob_of(K, i);
+    if (lo + l < a.V) emit(key[j], (uint32_t)(lo + l));
   }
 }
 

@@ -220,6 +220,26 @@ def _edge_inputs(kind):
                              hist_offsets=off, hist_ids=np.concatenate(hist), bias_offsets=boff,
                              bias_ids=np.concatenate(bias_ids), bias_vals=np.concatenate(bias_vals),
                              position=np.arange(B))
+    if kind == "dense_patch":
+        # consecutive penalised / biased ids: one thread holds several patched slots
+        V = 40000
+        x = W.bf16_bits_from_f32(rng.normal(0, 2, (B, V)).astype(np.float32))
+        hist = [np.concatenate([np.arange(96, 112), np.arange(9000, 9040), rng.integers(0, V, 64)]).astype(np.int32)
+                for _ in range(B)]
+        off = np.zeros(B + 1, np.int32)
+        off[1:] = np.cumsum([len(h) for h in hist])
+        bids = [np.arange(200, 216, dtype=np.int32) for _ in range(B)]
+        bvals = [np.full(16, 3.0, np.float32) for _ in range(B)]
+        boff = np.zeros(B + 1, np.int32)
+        boff[1:] = np.cumsum([len(h) for h in bids])
+        m = stoch | W.MODE_REP | W.MODE_FREQ | W.MODE_PRES | W.MODE_BIAS
+        mode = np.full(B, m)
+        mode[::2] = W.MODE_GREEDY | W.MODE_REP | W.MODE_FREQ | W.MODE_PRES | W.MODE_BIAS
+        return W.custom_rows(x, W.BF16, k_max=128, mode=mode, top_k=np.full(B, 100), top_p=np.full(B, 0.99),
+                             rep=np.full(B, 1.2), freq=np.full(B, 0.1), pres=np.full(B, 0.3),
+                             hist_offsets=off, hist_ids=np.concatenate(hist), bias_offsets=boff,
+                             bias_ids=np.concatenate(bids), bias_vals=np.concatenate(bvals),
+                             position=np.arange(B))
     if kind == "greedy_ties":
         V = 30000
         x = np.zeros((B, V), np.float32)
@@ -230,7 +250,7 @@ def _edge_inputs(kind):
 
 
 @pytest.mark.parametrize("kind", ["zeros", "bf16_flat", "ragged_odd", "small_v", "nan_empty", "no_topk",
-                                  "grammar_few", "long_history", "greedy_ties"])
+                                  "grammar_few", "long_history", "dense_patch", "greedy_ties"])
 def test_sample_edge_cases(ssb, kind):
     inp = _edge_inputs(kind)
     say(f"[{kind}] sample B={inp['B']} V={inp['V']}")
@@ -241,7 +261,7 @@ def test_sample_edge_cases(ssb, kind):
 # --------------------------------------------------------------------------
 # Materialised pipeline
 # --------------------------------------------------------------------------
-@pytest.mark.parametrize("name", ["cfg0", "cfg1", "long_history", "nan_empty", "grammar_few"])
+@pytest.mark.parametrize("name", ["cfg0", "cfg1", "long_history", "dense_patch", "nan_empty", "grammar_few"])
 def test_process_logits(ssb, name):
     inp = W.make_config(name) if name.startswith("cfg") else _edge_inputs(name)
     if name == "cfg1":
