@@ -27,6 +27,7 @@
 // can be captured in a HIP graph.
 #include <hip/hip_runtime.h>
 #include <limits.h>
+#include <stddef.h>
 #include <stdint.h>
 
 #include "ss.h"
@@ -38,15 +39,18 @@ constexpr int kTile = 8192;
 constexpr int kPT = kTile / kBlock;  // element slots per thread (32)
 constexpr int kGPT = 8;              // group maxima per thread
 constexpr int kGS = kPT / kGPT;      // slots per group (4)
-constexpr int kG = kGPT * kBlock;    // groups per tile (2048)
+constexpr int kUnits = kWaves;       // emission units per tile: one per wavefront
+constexpr int kUnitElems = kTile / kUnits;  // elements per unit (2048)
+constexpr int kUnitGroups = kGPT * 64;      // group maxima per unit (512)
 constexpr int kHCap = 1024;          // in-tile history entries held in LDS
 constexpr int kBCap = 128;           // in-tile bias entries held in LDS
 constexpr int kPCap = 128;           // patched slots per wavefront held in LDS
 constexpr int kIdsPT = 2;            // history ids each thread loads up front
 constexpr int kRPT = 32;             // merge candidates per thread (registers)
 constexpr int kMaxT = (SS_MAX_V + kTile - 1) / kTile;
+constexpr int kMaxU = kMaxT * kUnits;  // emission units per row
 constexpr int kEPT = SS_MAX_K / kBlock;  // selected entries per thread in the epilogue
-constexpr int kHCopies = 8;              // privatised histogram copies (lane & 7)
+constexpr int kHCopies = 4;              // privatised histogram copies (lane & 3)
 constexpr int kHStride = 257;            // padded so copies of one bin sit in different banks
 constexpr uint32_t kNoEmit = 0xFFFFFFFFu;  // emits nothing (above every valid key)
 constexpr double kFix = 1125899906842624.0;  // 2^50: fixed-point scale of weight sums
@@ -120,16 +124,19 @@ struct Smem {
   uint32_t bm[kBlock];      // per-thread bits of patched slots
   int32_t bl_pos[kBCap];
   float bl_val[kBCap];
-  uint32_t hist[kHCopies * kHStride];
-  uint32_t prefix[kMaxT + 1];
+  uint32_t prefix[kMaxU + 1];
   uint32_t pw_n[kWaves];
   uint32_t red32[kWaves];
   uint32_t cnt[4];
   uint32_t bc[8];
-  uint16_t hl[kHCap];
+  uint16_t hl[kHCap];  // distinct history ids of the tile (local index)
   uint16_t bl_l[kBCap];
-  uint8_t low[256];  // radix select: bin holds keys with non-zero low bits
+  uint8_t low[256];             // radix select: bin holds keys with non-zero low bits
+  uint32_t cnt8[kTile / 4];     // packed 8-bit occurrence counts per local index
+  // merge only from here
+  uint32_t hist[2][kHCopies * kHStride];  // double-buffered privatised radix histograms
 };
+constexpr int kSmemStream = (int)((offsetof(Smem, hist) + 15) & ~(size_t)15);
 constexpr int kSmemFixed = (int)((sizeof(Smem) + 15) & ~(size_t)15);
 
 // ---------------------------------------------------------------------------
@@ -153,6 +160,13 @@ __device__ __forceinline__ int local_of_slot(int t, int j) {
   constexpr int VW = DTT<DT>::VW;
   return ((j / VW) * kBlock + t) * VW + (j % VW);
 }
+
+// key without the positive-NaN fold; callers fold when the maximum exceeds +inf
+__device__ __forceinline__ uint32_t key_raw(uint32_t u) {
+  const uint32_t s = (uint32_t)((int32_t)u >> 31);
+  return (u ^ s) + (s ? 1u : 0x80000000u);
+}
+__device__ __forceinline__ uint32_t fold_nan(uint32_t k) { return k > kKeyPosInf ? 0u : k; }
 
 __device__ __forceinline__ uint32_t comp4(const uint4& v, int c) {
   return c == 0 ? v.x : (c == 1 ? v.y : (c == 2 ? v.z : v.w));
@@ -253,20 +267,25 @@ __device__ __forceinline__ Ctx make_ctx(const KArgs& a, int row) {
   return c;
 }
 
-__host__ __device__ inline int quota(int k, int T) {
-  if (T <= 1) return k;
-  const int kt = (k + T - 1) / T;
+// Candidate quota of one emission unit when a row's top-k is spread over U
+// units: the unit emits at least its q largest elements (by its threshold),
+// with q well above the unit's expected share k/U, so that the largest unit
+// threshold lies below the row's k-th value except with tiny probability.
+__host__ __device__ inline int quota(int k, int U) {
+  if (U <= 1) return k;
+  const int kt = (k + U - 1) / U;
   int s = 0;
   while (s * s < kt) ++s;
-  const int q = kt + 4 * s + 8;
+  const int q = kt + 5 * s + 6;
   return q < k ? q : k;
 }
 
-__host__ __device__ inline int tile_cap(int kcap, int T) {
-  const int q = quota(kcap, T);
-  if (2 * q > kG) return kTile;
-  const int c = 2 * q + 64;
-  return c < kTile ? c : kTile;
+// capacity of one unit's candidate region
+__host__ __device__ inline int unit_cap(int kcap, int U) {
+  const int q = quota(kcap, U);
+  if (2 * q > kUnitGroups) return kUnitElems;
+  const int c = 2 * q + 32;
+  return c < kUnitElems ? c : kUnitElems;
 }
 
 // ---------------------------------------------------------------------------
@@ -417,19 +436,30 @@ __device__ __forceinline__ void load_tile(const KArgs& a, const Ctx& c, int lo, 
     }
   }
   }
-  // 3. in-tile patch lists and owners (LDS only; overlaps the tile loads)
+  // 3. in-tile patch lists and owners (LDS only; overlaps the tile loads).
+  //    Occurrences are counted in a packed 8-bit table; the entry whose
+  //    increment finds zero owns the id and records it once.  A count that
+  //    would pass 255 sends the tile to the exact slow path.
   bool overflow = false;
   if (patch) {
     S.bm[tid] = 0u;
     if (tid < 4) S.cnt[tid] = 0u;
     if (tid < kWaves) S.pw_n[tid] = 0u;
+#pragma unroll
+    for (int q = 0; q < kTile / 4 / kBlock / 4; ++q)
+      reinterpret_cast<uint4*>(S.cnt8)[q * kBlock + tid] = make_uint4(0u, 0u, 0u, 0u);
     lds_barrier();
     auto add_hist = [&](int id) {
       const int rel = id - lo;
       if (id >= 0 && id < V && rel >= 0 && rel < n_tile) {
-        const uint32_t p = atomicAdd(&S.cnt[0], 1u);
-        if (p < (uint32_t)kHCap) S.hl[p] = (uint16_t)rel;
-        set_patch_bit<DT>(S, rel);
+        const uint32_t sh = (uint32_t)(rel & 3) * 8u;
+        const uint32_t old = (atomicAdd(&S.cnt8[rel >> 2], 1u << sh) >> sh) & 0xFFu;
+        if (old == 0xFFu) S.cnt[2] = 1u;  // saturated
+        if (old == 0u) {
+          const uint32_t p = atomicAdd(&S.cnt[0], 1u);
+          if (p < (uint32_t)kHCap) S.hl[p] = (uint16_t)rel;
+          set_patch_bit<DT>(S, rel);
+        }
       }
     };
 #pragma unroll
@@ -452,28 +482,23 @@ __device__ __forceinline__ void load_tile(const KArgs& a, const Ctx& c, int lo, 
     for (int e = tid + kBlock; e < c.nbias; e += kBlock) add_bias(e, c.bias_ids[e], c.bias_vals[e]);
     lds_barrier();
     const int hl_n = (int)S.cnt[0], bl_n = (int)S.cnt[1];
-    overflow = hl_n > kHCap || bl_n > kBCap;
+    overflow = hl_n > kHCap || bl_n > kBCap || S.cnt[2] != 0u;
     if (!overflow) {
       for (int n = tid; n < hl_n + bl_n; n += kBlock) {
-        int l, cntv = 0;
+        int l;
         bool owner = true;
         if (n < hl_n) {
           l = S.hl[n];
-          for (int m = 0; m < hl_n; ++m) {
-            if (S.hl[m] == l) {
-              ++cntv;
-              if (m < n) owner = false;
-            }
-          }
         } else {
           const int nb = n - hl_n;
           l = S.bl_l[nb];
-          for (int m = 0; m < hl_n && owner; ++m)
-            if (S.hl[m] == l) owner = false;
+          // ids with a history count are owned by their history entry
+          owner = ((S.cnt8[l >> 2] >> ((l & 3) * 8)) & 0xFFu) == 0u;
           for (int m = 0; m < nb && owner; ++m)
             if (S.bl_l[m] == l) owner = false;
         }
         if (!owner) continue;
+        const int cntv = (int)((S.cnt8[l >> 2] >> ((l & 3) * 8)) & 0xFFu);
         float bsum = 0.0f;
         bool hb = false;
         if (do_bias) {
@@ -497,7 +522,7 @@ __device__ __forceinline__ void load_tile(const KArgs& a, const Ctx& c, int lo, 
         const uint32_t p = atomicAdd(&S.pw_n[w], 1u);
         if (p < (uint32_t)kPCap)
           S.pw[w][p] = make_uint2((uint32_t)(t & 63) | ((uint32_t)j << 6) | ((hb ? 1u : 0u) << 11) |
-                                      ((uint32_t)min(cntv, (1 << 20) - 1) << 12),
+                                      ((uint32_t)cntv << 12),
                                   __float_as_uint(bsum));
       }
       lds_barrier();
@@ -521,12 +546,12 @@ __device__ __forceinline__ void load_tile(const KArgs& a, const Ctx& c, int lo, 
   if (c.mask) {
 #pragma unroll
     for (int j = 0; j < kPT; ++j) {
-      const uint32_t k = key_of_bits(slot_bits<DT>(raw, j));
+      const uint32_t k = key_raw(slot_bits<DT>(raw, j));
       kv[j] = ((allow >> j) & 1u) ? k : 0u;
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < kPT; ++j) kv[j] = key_of_bits(slot_bits<DT>(raw, j));
+    for (int j = 0; j < kPT; ++j) kv[j] = key_raw(slot_bits<DT>(raw, j));
   }
 
   // 5. penalties / bias: the holder of each patched slot rewrites its key
@@ -626,33 +651,6 @@ __device__ inline void radix_digit(const uint32_t* h, uint32_t want, bool descen
   lds_barrier();
 }
 
-// q-th largest of the per-thread group maxima, resolved to the top 16 key
-// bits: #{group maxima >= t} >= q whenever q valid maxima exist; kKeyFloor
-// otherwise.
-__device__ uint32_t group_threshold(const uint32_t (&gm)[kGPT], int q, Smem& S) {
-  hist_clear(S.hist);
-  lds_barrier();
-#pragma unroll
-  for (int g = 0; g < kGPT; ++g) hist_add(S.hist, gm[g] >> 24);
-  lds_barrier();
-  radix_digit(S.hist, (uint32_t)q, true, S.bc);
-  const uint32_t d1 = S.bc[0];
-  const uint32_t q1 = (uint32_t)q - S.bc[1];
-  lds_barrier();
-  if (d1 >= 256u) return kKeyFloor;
-  hist_clear(S.hist);
-  lds_barrier();
-#pragma unroll
-  for (int g = 0; g < kGPT; ++g)
-    if ((gm[g] >> 24) == d1) hist_add(S.hist, (gm[g] >> 16) & 255u);
-  lds_barrier();
-  radix_digit(S.hist, q1, true, S.bc);
-  const uint32_t d2 = S.bc[0];
-  lds_barrier();
-  const uint32_t t = (d1 << 24) | ((d2 & 255u) << 16);
-  return t < kKeyFloor ? kKeyFloor : t;
-}
-
 // ---------------------------------------------------------------------------
 // Generic exact selection: the `want` largest composites (key desc, index
 // asc) among the elements a visitor produces.  visit(f) calls f(key, idx) for
@@ -663,26 +661,29 @@ __device__ uint32_t group_threshold(const uint32_t (&gm)[kGPT], int q, Smem& S) 
 template <typename Visit>
 __device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, Smem& S, uint32_t* tk_out,
                                              uint32_t* ti_out) {
+  // Requires S.hist[0] zeroed and published.  The two histogram buffers
+  // alternate: the next pass's buffer is cleared during the current pass.
   const int tid = threadIdx.x;
+  int cur = 0;
   uint32_t prefix = 0u;
   uint32_t tk = 0u, ti = 0xFFFFFFFFu;
   bool done = false;
   for (int b = 3; b >= 0 && !done; --b) {
     const int sh = 8 * b;
-    hist_clear(S.hist);
-    if (b == 2) S.low[tid] = 0;
-    lds_barrier();
+    uint32_t* h = S.hist[cur];
     visit([&](uint32_t k, uint32_t) {
       if (k >= kKeyFloor && (b == 3 || (k >> (sh + 8)) == prefix)) {
-        hist_add(S.hist, (k >> sh) & 255u);
+        hist_add(h, (k >> sh) & 255u);
         if (b == 2 && (k & 0xFFFFu) != 0u) S.low[(k >> 16) & 255u] = 1;
       }
     });
+    hist_clear(S.hist[cur ^ 1]);
+    if (b == 3) S.low[tid] = 0;
     lds_barrier();
-    radix_digit(S.hist, want, true, S.bc);
+    radix_digit(h, want, true, S.bc);
     const uint32_t d = S.bc[0], above = S.bc[1], hd = S.bc[2];
     const bool low_zero = (b == 2) && S.low[d & 255u] == 0;
-    lds_barrier();
+    cur ^= 1;
     prefix = (prefix << 8) | (d & 255u);
     want -= above;
     if (hd == want) {
@@ -701,15 +702,15 @@ __device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, Smem&
     uint32_t ip = 0u;
     for (int b = 2; b >= 0; --b) {  // indices < 2^24
       const int sh = 8 * b;
-      hist_clear(S.hist);
-      lds_barrier();
+      uint32_t* h = S.hist[cur];
       visit([&](uint32_t k, uint32_t i) {
-        if (k == tk && (b == 2 || (i >> (sh + 8)) == ip)) hist_add(S.hist, (i >> sh) & 255u);
+        if (k == tk && (b == 2 || (i >> (sh + 8)) == ip)) hist_add(h, (i >> sh) & 255u);
       });
+      hist_clear(S.hist[cur ^ 1]);
       lds_barrier();
-      radix_digit(S.hist, want, false, S.bc);
+      radix_digit(h, want, false, S.bc);
       const uint32_t d = S.bc[0], below = S.bc[1], hd = S.bc[2];
-      lds_barrier();
+      cur ^= 1;
       ip = (ip << 8) | (d & 255u);
       want -= below;
       if (hd == want) {
@@ -747,7 +748,7 @@ __device__ __attribute__((noinline)) int fallback_select(const KArgs& a, const C
     else
       load_tile<DT, false>(a, c, j * kTile, S, key);
 #pragma unroll
-    for (int s = 0; s < kPT; ++s) nv_local += key[s] >= kKeyFloor;
+    for (int s = 0; s < kPT; ++s) nv_local += fold_nan(key[s]) >= kKeyFloor;
   }
   const int nv = (int)block_sum(nv_local, S.red32);
   *n_valid = nv;
@@ -762,9 +763,11 @@ __device__ __attribute__((noinline)) int fallback_select(const KArgs& a, const C
       else
         load_tile<DT, false>(a, c, lo, S, key);
 #pragma unroll
-      for (int s = 0; s < kPT; ++s) f(key[s], (uint32_t)(lo + local_of_slot<DT>(tid, s)));
+      for (int s = 0; s < kPT; ++s) f(fold_nan(key[s]), (uint32_t)(lo + local_of_slot<DT>(tid, s)));
     }
   };
+  hist_clear(S.hist[0]);
+  lds_barrier();
   uint32_t tk, ti;
   radix_select(visit_row, (uint32_t)want, S, &tk, &ti);
   uint32_t base = 0;
@@ -775,6 +778,8 @@ __device__ __attribute__((noinline)) int fallback_select(const KArgs& a, const C
       load_tile<DT, true>(a, c, lo, S, key);
     else
       load_tile<DT, false>(a, c, lo, S, key);
+#pragma unroll
+    for (int s = 0; s < kPT; ++s) key[s] = fold_nan(key[s]);
     uint32_t cntl = 0;
 #pragma unroll
     for (int s = 0; s < kPT; ++s) cntl += selected(key[s], lo + local_of_slot<DT>(tid, s), tk, ti);
@@ -935,32 +940,31 @@ template <int DT>
 __device__ __forceinline__ int select_exact(const KArgs& a, const Ctx& c, Smem& S, uint64_t* sel, int want,
                                             uint32_t tmax, uint32_t ovf, uint32_t n_total, int* flags) {
   const int tid = threadIdx.x;
-  const int T = a.T, row = c.row;
+  const int row = c.row;
+  const int U = a.T * kUnits;
   bool fast = ovf == 0u && n_total <= (uint32_t)(kRPT * kBlock);
   uint32_t ck[kRPT], ci[kRPT];
   uint32_t cl = 0;
   if (fast) {
-    // flattened candidate f -> (tile, offset) by binary search of the prefix
-    int lgT = 0;
-    while ((1 << lgT) < T) ++lgT;
+    // flattened candidate f -> (unit, offset) by binary search of the prefix;
+    // every load is issued (clamped index) so they are all in flight at once
+    int lgU = 0;
+    while ((1 << lgU) < U) ++lgU;
 #pragma unroll
     for (int m = 0; m < kRPT; ++m) {
-      const uint32_t f = tid + m * kBlock;
-      ck[m] = 0u;
-      ci[m] = 0u;
-      if (f < n_total) {
-        int jt = 0;
-        for (int s2 = lgT - 1; s2 >= 0; --s2) {
-          const int probe = jt + (1 << s2);
-          if (probe < T && S.prefix[probe] <= f) jt = probe;
-        }
-        const uint2 e = a.cand[((size_t)row * T + jt) * a.cap + (f - S.prefix[jt])];
-        if (e.x >= tmax) {
-          ck[m] = e.x;
-          ci[m] = e.y;
-          ++cl;
-        }
+      const uint32_t f0 = tid + m * kBlock;
+      const bool ok = f0 < n_total;
+      const uint32_t f = ok ? f0 : 0u;
+      int ju = 0;
+      for (int s2 = lgU - 1; s2 >= 0; --s2) {
+        const int probe = ju + (1 << s2);
+        if (probe < U && S.prefix[probe] <= f) ju = probe;
       }
+      const uint2 e = a.cand[((size_t)row * U + ju) * a.cap + (f - S.prefix[ju])];
+      const bool keep = ok && e.x >= tmax;
+      ck[m] = keep ? e.x : 0u;
+      ci[m] = keep ? e.y : 0u;
+      cl += keep ? 1u : 0u;
     }
   }
   const uint32_t C = fast ? block_sum(cl, S.red32) : 0u;
@@ -1000,19 +1004,31 @@ __device__ __forceinline__ int select_exact(const KArgs& a, const Ctx& c, Smem& 
 template <int DT, int OP>
 __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S, uint64_t* sel) {
   const int tid = threadIdx.x;
-  const int T = a.T, row = c.row, b = c.req;
-  // tile records
-  uint4 r4 = make_uint4(0u, 0u, kNoEmit, 0u);
-  if (tid < T) r4 = a.rec[(size_t)row * T + tid];
-  const uint64_t tcomp = (tid < T && r4.x >= kKeyFloor) ? comp_of(r4.x, r4.y) : 0ull;
+  const int row = c.row, b = c.req;
+  // unit records (two consecutive units per thread)
+  const int U = a.T * kUnits;
+  uint64_t tcomp = 0ull;
+  uint32_t tthr = 0u, tovf = 0u, nl[2] = {0u, 0u};
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int u = 2 * tid + h;
+    if (u < U) {
+      const uint4 r4 = a.rec[(size_t)row * U + u];
+      if (r4.x >= kKeyFloor) tcomp = max(tcomp, comp_of(r4.x, r4.y));
+      tthr = max(tthr, r4.z);
+      tovf |= r4.w > (uint32_t)a.cap ? 1u : 0u;
+      nl[h] = min(r4.w, (uint32_t)a.cap);
+    }
+  }
   const uint64_t Mcomp = block_max(tcomp, S.red64);
-  const uint32_t tmax = block_max(tid < T ? r4.z : 0u, S.red32);
-  const uint32_t ovf = block_max((tid < T && r4.w > (uint32_t)a.cap) ? 1u : 0u, S.red32);
-  const uint32_t nj = (tid < T) ? min(r4.w, (uint32_t)a.cap) : 0u;
+  const uint32_t tmax = block_max(tthr, S.red32);
+  const uint32_t ovf = block_max(tovf, S.red32);
   uint32_t n_total;
-  const uint32_t pre = block_excl_scan(nj, S.red32, n_total);
-  if (tid < T) S.prefix[tid] = pre;
-  if (tid == 0) S.prefix[T] = n_total;
+  const uint32_t pre = block_excl_scan(nl[0] + nl[1], S.red32, n_total);
+  if (2 * tid < U) S.prefix[2 * tid] = pre;
+  if (2 * tid + 1 < U) S.prefix[2 * tid + 1] = pre + nl[0];
+  if (tid == 0) S.prefix[U] = n_total;
+  hist_clear(S.hist[0]);
   lds_barrier();
 
   int flags = c.kcap ? SS_FLAG_KCAP : 0;
@@ -1241,6 +1257,25 @@ __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S,
 // for every row; for truncating rows, candidate emission above a per-tile
 // threshold (the q-th largest of 2048 group maxima, q = quota(k, T)).
 // ---------------------------------------------------------------------------
+// Largest 16-bit key prefix t with at least q of the wave's values >= t
+// (binary search on the threshold; counts come from ballots, no LDS).
+template <int N>
+__device__ __forceinline__ uint32_t wave_threshold(const uint32_t (&v)[N], uint32_t q) {
+  uint32_t prefix = 0u;
+#pragma unroll 1
+  for (int b = 31; b >= 16; --b) {
+    const uint32_t cand = prefix | (1u << b);
+    uint32_t cnt = 0u;
+#pragma unroll
+    for (int i = 0; i < N; ++i) cnt += (uint32_t)__popcll(__ballot(v[i] >= cand));
+    if (cnt >= q) prefix = cand;
+  }
+  return prefix < kKeyFloor ? kKeyFloor : prefix;
+}
+
+// One tile of the streaming kernel.  After the loads everything is local to
+// a wavefront: each wavefront is an emission unit with its own maximum,
+// threshold and candidate region, so the tail needs no workgroup barrier.
 template <int DT, bool FULL>
 __device__ __forceinline__ void stream_tile(const KArgs& a, const Ctx& c, Smem& S, int row, int tile) {
   const int tid = threadIdx.x;
@@ -1248,72 +1283,73 @@ __device__ __forceinline__ void stream_tile(const KArgs& a, const Ctx& c, Smem& 
   uint32_t key[kPT];
   load_tile<DT, FULL>(a, c, lo, S, key);
 
-  // group maxima and thread maximum
   uint32_t gm[kGPT];
+  auto group_maxima = [&]() {
 #pragma unroll
-  for (int g = 0; g < kGPT; ++g) {
-    uint32_t m = key[g * kGS];
+    for (int g = 0; g < kGPT; ++g) {
+      uint32_t m = key[g * kGS];
 #pragma unroll
-    for (int s = 1; s < kGS; ++s) m = max(m, key[g * kGS + s]);
-    gm[g] = m;
-  }
-
+      for (int s = 1; s < kGS; ++s) m = max(m, key[g * kGS + s]);
+      gm[g] = m;
+    }
+  };
+  group_maxima();
   uint32_t tmax = gm[0];
 #pragma unroll
   for (int g = 1; g < kGPT; ++g) tmax = max(tmax, gm[g]);
-  const uint32_t Mt = block_max(tmax, S.red32);
-  // lowest index holding the maximum
+  if (__ballot(tmax > kKeyPosInf)) {  // a positive NaN in this wavefront: fold it to invalid
+#pragma unroll
+    for (int j = 0; j < kPT; ++j) key[j] = fold_nan(key[j]);
+    group_maxima();
+    tmax = gm[0];
+#pragma unroll
+    for (int g = 1; g < kGPT; ++g) tmax = max(tmax, gm[g]);
+  }
+  // wavefront maximum and the lowest index holding it
+  const uint32_t wm = wave_max(tmax);
   uint32_t aidx = 0xFFFFFFFFu;
-  if (Mt >= kKeyFloor && tmax == Mt) {
+  if (wm >= kKeyFloor && tmax == wm) {
 #pragma unroll
     for (int j = kPT - 1; j >= 0; --j)
-      if (key[j] == Mt) aidx = (uint32_t)(lo + local_of_slot<DT>(tid, j));
-
+      if (key[j] == wm) aidx = (uint32_t)(lo + local_of_slot<DT>(tid, j));
   }
-  aidx = block_min(aidx, S.red32);
+  aidx = wave_min(aidx);
 
+  const int w = wave();
+  const int unit = (row * a.T + tile) * kUnits + w;
   uint32_t t = kNoEmit;
-  uint32_t n_emit = 0;
+  uint32_t n = 0u;
   if (!c.greedy && c.k_eff > 0) {
-    if (Mt < kKeyFloor) {
+    if (wm < kKeyFloor) {
       t = kKeyFloor;  // nothing valid here: everything valid (nothing) is emitted
     } else {
-      const int q = quota(c.k_eff, a.T);
-      if (tid == 0) S.bc[5] = 0u;
-      if (2 * q > kG) {
+      const int q = quota(c.k_eff, a.T * kUnits);
+      if (2 * q > kUnitGroups) {
         t = kKeyFloor;
-        lds_barrier();
+      } else if (q <= 16) {
+        const uint32_t v1[1] = {tmax};
+        t = wave_threshold(v1, (uint32_t)q);
       } else {
-        t = group_threshold(gm, q, S);  // starts with a barrier
+        t = wave_threshold(gm, (uint32_t)q);
       }
-      uint2* region = a.cand + ((size_t)row * a.T + tile) * a.cap;
-      uint32_t wcount = 0;
-#pragma unroll
-      for (int j = 0; j < kPT; ++j) wcount += (uint32_t)__popcll(__ballot(key[j] >= t));
-
-      uint32_t base = 0;
-      if (lane() == 0) base = atomicAdd(&S.bc[5], wcount);
-      base = __builtin_amdgcn_readfirstlane(base);
+      uint2* region = a.cand + (size_t)unit * a.cap;
       const uint32_t cap = (uint32_t)a.cap;
 #pragma unroll
       for (int j = 0; j < kPT; ++j) {
-        const bool s = key[j] >= t;
-        const uint64_t m = __ballot(s);
+        const bool sel = key[j] >= t;
+        const uint64_t m = __ballot(sel);
         if (m) {
-          if (s) {
-            const uint32_t p = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+          if (sel) {
+            const uint32_t p = n + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
             if (p < cap) region[p] = make_uint2(key[j], (uint32_t)(lo + local_of_slot<DT>(tid, j)));
           }
-          base += (uint32_t)__popcll(m);
+          n += (uint32_t)__popcll(m);
         }
       }
-
-      lds_barrier();
-      n_emit = S.bc[5];
     }
   }
-  if (tid == 0) a.rec[(size_t)row * a.T + tile] = make_uint4(Mt, aidx, t, n_emit);
+  if (lane() == 0) a.rec[unit] = make_uint4(wm, aidx, t, n);
 }
 
 template <int DT>
@@ -1358,6 +1394,8 @@ __global__ __launch_bounds__(kBlock) void ss_materialize_kernel(KArgs a) {
     load_tile<DT, true>(a, c, lo, S, key);
   else
     load_tile<DT, false>(a, c, lo, S, key);
+#pragma unroll
+  for (int j = 0; j < kPT; ++j) key[j] = fold_nan(key[j]);
   const RowSummary s = a.summ[row];
   const size_t ob = (size_t)row * (size_t)a.V;
   auto emit = [&](uint32_t k, uint32_t i) {
@@ -1401,7 +1439,7 @@ static bool make_layout(int op, int B, int V, int L, int k_max, Layout* lay) {
   if (op < OP_TOPK || op > OP_PROCESS) return false;
   const int rows = op == OP_VERIFY ? B * (L + 1) : B;
   const int T = (V + kTile - 1) / kTile;
-  const int cap = tile_cap(k_max, T);
+  const int cap = unit_cap(k_max, T * kUnits);
   size_t o = 0;
   lay->off_ticket = o;
   o = align256(o + (size_t)rows * 4);
@@ -1410,9 +1448,9 @@ static bool make_layout(int op, int B, int V, int L, int k_max, Layout* lay) {
   const size_t zero_end = o;
   (void)zero_end;
   lay->off_rec = o;
-  o = align256(o + (size_t)rows * T * 16);
+  o = align256(o + (size_t)rows * T * kUnits * 16);
   lay->off_cand = o;
-  o = align256(o + (size_t)rows * T * cap * 8);
+  o = align256(o + (size_t)rows * T * kUnits * cap * 8);
   lay->off_res = o;
   const size_t res_bytes = op == OP_VERIFY ? sizeof(RowResult) : (op == OP_PROCESS ? sizeof(RowSummary) : 0);
   o = align256(o + (size_t)rows * res_bytes);
@@ -1496,16 +1534,16 @@ static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStr
   const dim3 grid((unsigned)(lay.rows * lay.T)), rgrid((unsigned)lay.rows), block(kBlock);
   if (g_ev_before) (void)hipEventRecord(g_ev_before, st);
   if (dtype == SS_BF16)
-    hipLaunchKernelGGL(ss_stream_kernel<SS_BF16>, grid, block, kSmemFixed, st, k);
+    hipLaunchKernelGGL(ss_stream_kernel<SS_BF16>, grid, block, kSmemStream, st, k);
   else
-    hipLaunchKernelGGL(ss_stream_kernel<SS_F32>, grid, block, kSmemFixed, st, k);
+    hipLaunchKernelGGL(ss_stream_kernel<SS_F32>, grid, block, kSmemStream, st, k);
   if (g_ev_after) (void)hipEventRecord(g_ev_after, st);
   if (dtype == SS_BF16) {
     launch_merge<SS_BF16>(k, rgrid, block, lay.smem, st);
-    if (materialize) hipLaunchKernelGGL(ss_materialize_kernel<SS_BF16>, grid, block, kSmemFixed, st, k);
+    if (materialize) hipLaunchKernelGGL(ss_materialize_kernel<SS_BF16>, grid, block, kSmemStream, st, k);
   } else {
     launch_merge<SS_F32>(k, rgrid, block, lay.smem, st);
-    if (materialize) hipLaunchKernelGGL(ss_materialize_kernel<SS_F32>, grid, block, kSmemFixed, st, k);
+    if (materialize) hipLaunchKernelGGL(ss_materialize_kernel<SS_F32>, grid, block, kSmemStream, st, k);
   }
   return hipGetLastError() == hipSuccess ? SS_OK : SS_ERR_HIP;
 }
