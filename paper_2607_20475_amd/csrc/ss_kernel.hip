@@ -116,6 +116,27 @@ struct KArgs {
   RowSummary* summ;
 };
 
+// ---------------------------------------------------------------------------
+// Per-row context
+// ---------------------------------------------------------------------------
+struct Ctx {
+  int row, req, ell;
+  uint32_t mode;
+  const unsigned char* xrow;
+  const int32_t* hist;
+  int nhist;
+  const int32_t* extra;
+  int nextra;
+  const int32_t* bias_ids;
+  const float* bias_vals;
+  int nbias;
+  const uint32_t* mask;
+  float rep, freq, pres;
+  bool greedy;
+  bool kcap;
+  int k_eff;
+};
+
 struct Smem {
   uint64_t red64[kWaves];
   double redd[kWaves];
@@ -131,13 +152,18 @@ struct Smem {
   uint32_t bc[8];
   uint16_t hl[kHCap];  // distinct history ids of the tile (local index)
   uint16_t bl_l[kBCap];
-  uint8_t low[256];             // radix select: bin holds keys with non-zero low bits
   uint32_t cnt8[kTile / 4];     // packed 8-bit occurrence counts per local index
   // merge only from here
   uint32_t hist[2][kHCopies * kHStride];  // double-buffered privatised radix histograms
+  uint32_t low[2][64];  // per bin (bytes): some key in the bin has non-zero bits below the digit
+  KArgs fa;              // kernel arguments and row context handed to the fallback
+  Ctx fc;
 };
 constexpr int kSmemStream = (int)((offsetof(Smem, hist) + 15) & ~(size_t)15);
 constexpr int kSmemFixed = (int)((sizeof(Smem) + 15) & ~(size_t)15);
+// merge dynamic LDS: [Smem][candidates: kRPT * kBlock uint2][sel: next_pow2(k_max) uint64]
+constexpr int kCandBytes = 8 * kRPT * kBlock;
+constexpr int kSelOff = kSmemFixed + kCandBytes;
 
 // ---------------------------------------------------------------------------
 // Element layout: thread t, slot j (0..31) holds chunk i = j / VW, element
@@ -193,26 +219,6 @@ __device__ __forceinline__ uint32_t load_elem_bits(const unsigned char* xrow, in
   }
 }
 
-// ---------------------------------------------------------------------------
-// Per-row context
-// ---------------------------------------------------------------------------
-struct Ctx {
-  int row, req, ell;
-  uint32_t mode;
-  const unsigned char* xrow;
-  const int32_t* hist;
-  int nhist;
-  const int32_t* extra;
-  int nextra;
-  const int32_t* bias_ids;
-  const float* bias_vals;
-  int nbias;
-  const uint32_t* mask;
-  float rep, freq, pres;
-  bool greedy;
-  bool kcap;
-  int k_eff;
-};
 
 template <int DT>
 __device__ __forceinline__ Ctx make_ctx(const KArgs& a, int row) {
@@ -603,29 +609,37 @@ __device__ __forceinline__ void load_tile(const KArgs& a, const Ctx& c, int lo, 
 __device__ __forceinline__ bool tile_full(const KArgs& a, int lo) { return a.vec_ok && a.V - lo >= kTile; }
 
 // ---------------------------------------------------------------------------
-// Radix digit search on a privatised 256-bin histogram (kHCopies copies,
-// stride kHStride), done by wave 0.  Descending: find d with
-// above(d) < want <= above(d) + h[d], above(d) = count in bins > d;
-// ascending: the same with bins < d.  Writes (d, count before d, h[d]) to
-// bc[0..2]; d = 256 if the total is below `want`.
+// Radix selection in the merge.  Histograms are privatised (kHCopies copies,
+// stride kHStride) and double-buffered: the buffer of the next pass is
+// cleared while the current one fills, so one barrier separates passes.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void hist_clear(uint32_t* h) {
-  for (int i = threadIdx.x; i < kHCopies * kHStride; i += kBlock) h[i] = 0u;
+__device__ __forceinline__ void radix_clear(Smem& S, int buf) {
+  for (int i = threadIdx.x; i < kHCopies * kHStride; i += kBlock) S.hist[buf][i] = 0u;
+  if (threadIdx.x < 64) S.low[buf][threadIdx.x] = 0u;
 }
 __device__ __forceinline__ void hist_add(uint32_t* h, uint32_t bin) {
   atomicAdd(&h[(lane() & (kHCopies - 1)) * kHStride + bin], 1u);
 }
-__device__ inline void radix_digit(const uint32_t* h, uint32_t want, bool descending, uint32_t* bc) {
+
+// Digit search by wave 0 over nb <= 256 bins.  Descending: find d with
+// above(d) < want <= above(d) + h[d], above(d) = count in the bins above d;
+// ascending: the same with the bins below d.  Writes (d, count before d, h[d],
+// low flag of d) to bc[0..3]; d = nb if the total is below `want`.
+__device__ inline void radix_digit(const uint32_t* h, const uint32_t* low, int nb, uint32_t want, bool descending,
+                                   uint32_t* bc) {
   if (threadIdx.x < 64) {
     const int l = lane();
     uint32_t cb[4];
     uint32_t s = 0;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int bin = descending ? (255 - 4 * l - u) : (4 * l + u);
+      const int r = 4 * l + u;
+      const int bin = descending ? (nb - 1 - r) : r;
       uint32_t v = 0;
+      if (r < nb) {
 #pragma unroll
-      for (int cp = 0; cp < kHCopies; ++cp) v += h[cp * kHStride + bin];
+        for (int cp = 0; cp < kHCopies; ++cp) v += h[cp * kHStride + bin];
+      }
       cb[u] = v;
       s += v;
     }
@@ -633,17 +647,20 @@ __device__ inline void radix_digit(const uint32_t* h, uint32_t want, bool descen
     const uint32_t total = __shfl(inc, 63, 64);
     uint32_t run = inc - s;
     if (l == 0) {
-      bc[0] = 256u;
+      bc[0] = (uint32_t)nb;
       bc[1] = total;
       bc[2] = 0u;
+      bc[3] = 1u;
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int bin = descending ? (255 - 4 * l - u) : (4 * l + u);
-      if (run < want && run + cb[u] >= want) {
+      const int r = 4 * l + u;
+      const int bin = descending ? (nb - 1 - r) : r;
+      if (r < nb && run < want && run + cb[u] >= want) {
         bc[0] = (uint32_t)bin;
         bc[1] = run;
         bc[2] = cb[u];
+        bc[3] = low ? (low[bin >> 2] >> (8 * (bin & 3))) & 255u : 1u;
       }
       run += cb[u];
     }
@@ -652,72 +669,90 @@ __device__ inline void radix_digit(const uint32_t* h, uint32_t want, bool descen
 }
 
 // ---------------------------------------------------------------------------
-// Generic exact selection: the `want` largest composites (key desc, index
-// asc) among the elements a visitor produces.  visit(f) calls f(key, idx) for
+// Exact selection of the `want` largest composites (key desc, index asc)
+// among the valid keys a visitor produces.  visit(f) calls f(key, idx) for
 // this thread's elements; every thread calls it the same number of times.
-// Returns the boundary (tk, ti): an element is selected iff key > tk or
-// (key == tk and idx <= ti).
+// Every valid visited key lies in [lo_key, hi_key]: the bits above the
+// highest bit in which the two bounds differ are common to all of them, so
+// the 8-bit digit passes start just below those bits.  A pass whose chosen
+// bin holds only keys with zero bits below the digit fixes the boundary key
+// at once (bf16 logits leave the low 16 bits zero).  Ties at the boundary key
+// take the lowest indices (indices < V).  Returns (tk, ti): an element is
+// selected iff key > tk or (key == tk and idx <= ti).  Requires radix buffer
+// 0 cleared and published.
 // ---------------------------------------------------------------------------
 template <typename Visit>
-__device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, Smem& S, uint32_t* tk_out,
-                                             uint32_t* ti_out) {
-  // Requires S.hist[0] zeroed and published.  The two histogram buffers
-  // alternate: the next pass's buffer is cleared during the current pass.
-  const int tid = threadIdx.x;
+__device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint32_t lo_key, uint32_t hi_key, int V,
+                                             Smem& S, uint32_t* tk_out, uint32_t* ti_out) {
   int cur = 0;
-  uint32_t prefix = 0u;
-  uint32_t tk = 0u, ti = 0xFFFFFFFFu;
-  bool done = false;
-  for (int b = 3; b >= 0 && !done; --b) {
-    const int sh = 8 * b;
+  int sh = 32 - __clz(lo_key ^ hi_key);  // bits [0, sh) vary among the keys
+  uint32_t prefix = sh >= 32 ? 0u : (hi_key >> sh);
+  uint32_t tk = hi_key, ti = 0xFFFFFFFFu;
+  bool ties = true;
+  while (sh > 0) {
+    const int w = sh < 8 ? sh : 8;
+    sh -= w;
+    const int hs = sh + w;
+    const uint32_t dm = (1u << w) - 1u;
+    const uint32_t lm = (1u << sh) - 1u;
     uint32_t* h = S.hist[cur];
+    uint8_t* lowb = reinterpret_cast<uint8_t*>(S.low[cur]);
     visit([&](uint32_t k, uint32_t) {
-      if (k >= kKeyFloor && (b == 3 || (k >> (sh + 8)) == prefix)) {
-        hist_add(h, (k >> sh) & 255u);
-        if (b == 2 && (k & 0xFFFFu) != 0u) S.low[(k >> 16) & 255u] = 1;
+      if (k >= kKeyFloor && (hs >= 32 || (k >> hs) == prefix)) {
+        const uint32_t d = (k >> sh) & dm;
+        hist_add(h, d);
+        if (k & lm) lowb[d] = 1;
       }
     });
-    hist_clear(S.hist[cur ^ 1]);
-    if (b == 3) S.low[tid] = 0;
+    radix_clear(S, cur ^ 1);
     lds_barrier();
-    radix_digit(h, want, true, S.bc);
-    const uint32_t d = S.bc[0], above = S.bc[1], hd = S.bc[2];
-    const bool low_zero = (b == 2) && S.low[d & 255u] == 0;
+    radix_digit(h, S.low[cur], (int)dm + 1, want, true, S.bc);
+    const uint32_t d = S.bc[0], above = S.bc[1], hd = S.bc[2], lowd = S.bc[3];
     cur ^= 1;
-    prefix = (prefix << 8) | (d & 255u);
-    want -= above;
-    if (hd == want) {
-      tk = prefix << sh;  // every key with this prefix is selected
+    if (d > dm) {  // fewer valid keys than `want`: all are selected
+      tk = kKeyNegInf;
       ti = 0xFFFFFFFFu;
-      done = true;
-    } else if (b == 0) {
-      tk = prefix;
-    } else if (low_zero) {
-      tk = prefix << 16;  // the boundary keys are all equal: resolve ties by index
+      ties = false;
+      break;
+    }
+    prefix = (prefix << w) | d;
+    want -= above;
+    if (hd == want) {  // every key with this prefix is selected
+      tk = prefix << sh;
+      ti = 0xFFFFFFFFu;
+      ties = false;
+      break;
+    }
+    if (sh == 0 || lowd == 0u) {  // the boundary keys all equal prefix << sh
+      tk = prefix << sh;
       break;
     }
   }
-  if (!done) {
+  if (ties) {
     // ties at key tk: the `want` lowest indices
+    int ib = 32 - __clz((uint32_t)(V > 1 ? V - 1 : 1));
     uint32_t ip = 0u;
-    for (int b = 2; b >= 0; --b) {  // indices < 2^24
-      const int sh = 8 * b;
+    while (ib > 0) {
+      const int w = ib < 8 ? ib : 8;
+      ib -= w;
+      const int hs = ib + w;
+      const uint32_t dm = (1u << w) - 1u;
       uint32_t* h = S.hist[cur];
       visit([&](uint32_t k, uint32_t i) {
-        if (k == tk && (b == 2 || (i >> (sh + 8)) == ip)) hist_add(h, (i >> sh) & 255u);
+        if (k == tk && (i >> hs) == ip) hist_add(h, (i >> ib) & dm);
       });
-      hist_clear(S.hist[cur ^ 1]);
+      radix_clear(S, cur ^ 1);
       lds_barrier();
-      radix_digit(h, want, false, S.bc);
+      radix_digit(h, nullptr, (int)dm + 1, want, false, S.bc);
       const uint32_t d = S.bc[0], below = S.bc[1], hd = S.bc[2];
       cur ^= 1;
-      ip = (ip << 8) | (d & 255u);
+      ip = (ip << w) | (d & dm);
       want -= below;
       if (hd == want) {
-        ti = (ip << sh) | ((1u << sh) - 1u);
+        ti = (ip << ib) | ((1u << ib) - 1u);
         break;
       }
-      if (b == 0) ti = ip;
+      if (ib == 0) ti = ip;
     }
   }
   *tk_out = tk;
@@ -730,14 +765,19 @@ __device__ __forceinline__ bool selected(uint32_t k, uint32_t i, uint32_t tk, ui
 
 // ---------------------------------------------------------------------------
 // Fallback: exact top-`want` of the whole row by streaming it again through
-// this workgroup.  Fills sel[0..n) (row order) and returns n; *n_valid gets
-// the number of valid elements in the row.  Kept out of line: it is the rare
-// path and carries most of the register pressure, which must not leak into
-// the fast path's allocation.
+// this workgroup.  Fills sel[0..n) (row order) and returns n.  The kernel
+// arguments and row context come through LDS (S.fa, S.fc, written by the
+// caller): the function is kept out of line so that its register pressure
+// does not leak into the fast path, and handing it the by-value kernel
+// argument itself would make every merge copy that argument to scratch.
 // ---------------------------------------------------------------------------
 template <int DT>
-__device__ __attribute__((noinline)) int fallback_select(const KArgs& a, const Ctx& c, int want, Smem& S,
-                                                         uint64_t* sel, int* n_valid) {
+__device__ __attribute__((noinline)) int fallback_select(int want) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  Smem& S = *reinterpret_cast<Smem*>(smem_raw);
+  uint64_t* sel = reinterpret_cast<uint64_t*>(smem_raw + kSelOff);
+  const KArgs& a = S.fa;
+  const Ctx& c = S.fc;
   const int tid = threadIdx.x;
   const int T = a.T;
   uint32_t nv_local = 0;
@@ -751,7 +791,6 @@ __device__ __attribute__((noinline)) int fallback_select(const KArgs& a, const C
     for (int s = 0; s < kPT; ++s) nv_local += fold_nan(key[s]) >= kKeyFloor;
   }
   const int nv = (int)block_sum(nv_local, S.red32);
-  *n_valid = nv;
   if (want > nv) want = nv;
   if (want <= 0) return 0;
   auto visit_row = [&](auto&& f) {
@@ -766,10 +805,10 @@ __device__ __attribute__((noinline)) int fallback_select(const KArgs& a, const C
       for (int s = 0; s < kPT; ++s) f(fold_nan(key[s]), (uint32_t)(lo + local_of_slot<DT>(tid, s)));
     }
   };
-  hist_clear(S.hist[0]);
+  radix_clear(S, 0);
   lds_barrier();
   uint32_t tk, ti;
-  radix_select(visit_row, (uint32_t)want, S, &tk, &ti);
+  radix_select(visit_row, (uint32_t)want, kKeyFloor, 0xFFFFFFFFu, a.V, S, &tk, &ti);
   uint32_t base = 0;
   for (int j = 0; j < T; ++j) {
     uint32_t key[kPT];
@@ -790,10 +829,17 @@ __device__ __attribute__((noinline)) int fallback_select(const KArgs& a, const C
       const uint32_t i = lo + local_of_slot<DT>(tid, s);
       if (selected(key[s], i, tk, ti)) sel[off++] = comp_of(key[s], i);
     }
-
     base += tot;
   }
   return (int)base;
+}
+
+// sort sel[0..n) descending (canonical order), padding to a power of two
+__device__ __forceinline__ void sort_selected(uint64_t* sel, int n) {
+  const int N = next_pow2(n);
+  for (int r = n + (int)threadIdx.x; r < N; r += kBlock) sel[r] = 0ull;
+  lds_barrier();
+  lds_sort_desc(sel, N);
 }
 
 // ---------------------------------------------------------------------------
@@ -933,68 +979,102 @@ __device__ __forceinline__ double rank_weight(const Dist& D, int r, Smem& S) {
 }
 
 // ---------------------------------------------------------------------------
-// Exact top-`want` set of a row from its tile candidates (fast path) or by
+// Exact top-`want` set of a row from its unit candidates (fast path) or by
 // streaming the row again (fallback).  Writes sel[0..n) unordered.
 // ---------------------------------------------------------------------------
 template <int DT>
 __device__ __forceinline__ int select_exact(const KArgs& a, const Ctx& c, Smem& S, uint64_t* sel, int want,
-                                            uint32_t tmax, uint32_t ovf, uint32_t n_total, int* flags) {
+                                            uint32_t tmax, uint32_t hi_key, uint32_t ovf, uint32_t n_total,
+                                            int* flags) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  uint2* cnd = reinterpret_cast<uint2*>(smem_raw + kSmemFixed);  // kRPT * kBlock staged candidates
   const int tid = threadIdx.x;
-  const int row = c.row;
   const int U = a.T * kUnits;
   bool fast = ovf == 0u && n_total <= (uint32_t)(kRPT * kBlock);
-  uint32_t ck[kRPT], ci[kRPT];
   uint32_t cl = 0;
   if (fast) {
-    // flattened candidate f -> (unit, offset) by binary search of the prefix;
-    // every load is issued (clamped index) so they are all in flight at once
-    int lgU = 0;
-    while ((1 << lgU) < U) ++lgU;
+    // candidate f = tid + m * kBlock of the row's unit-major sequence lies in
+    // the unit u with prefix[u] <= f < prefix[u + 1]; the binary searches of
+    // a thread's slots run in lockstep so that their LDS reads, and then the
+    // candidate loads, are in flight together.  Slots at or beyond n_total
+    // (and candidates below tmax) are staged as invalid (key 0).
+    const int lgU = U > 1 ? 32 - __clz((uint32_t)(U - 1)) : 0;
+    const uint2* rc = a.cand + (size_t)c.row * U * a.cap;
+    constexpr int kG = 32;  // slots per batch
 #pragma unroll
-    for (int m = 0; m < kRPT; ++m) {
-      const uint32_t f0 = tid + m * kBlock;
-      const bool ok = f0 < n_total;
-      const uint32_t f = ok ? f0 : 0u;
-      int ju = 0;
-      for (int s2 = lgU - 1; s2 >= 0; --s2) {
-        const int probe = ju + (1 << s2);
-        if (probe < U && S.prefix[probe] <= f) ju = probe;
+    for (int g = 0; g < kRPT; g += kG) {
+      uint32_t ju[kG], pv[kG];
+#pragma unroll
+      for (int m = 0; m < kG; ++m) {
+        ju[m] = 0u;
+        pv[m] = 0u;
       }
-      const uint2 e = a.cand[((size_t)row * U + ju) * a.cap + (f - S.prefix[ju])];
-      const bool keep = ok && e.x >= tmax;
-      ck[m] = keep ? e.x : 0u;
-      ci[m] = keep ? e.y : 0u;
-      cl += keep ? 1u : 0u;
+      for (int s2 = lgU - 1; s2 >= 0; --s2) {
+        uint32_t pp[kG];
+#pragma unroll
+        for (int m = 0; m < kG; ++m) pp[m] = S.prefix[min(ju[m] + (1u << s2), (uint32_t)U)];
+#pragma unroll
+        for (int m = 0; m < kG; ++m) {
+          const uint32_t f0 = (uint32_t)(tid + (g + m) * kBlock);
+          const uint32_t f = f0 < n_total ? f0 : 0u;
+          if (pp[m] <= f) {
+            ju[m] = min(ju[m] + (1u << s2), (uint32_t)U);
+            pv[m] = pp[m];
+          }
+        }
+      }
+      uint2 e[kG];
+#pragma unroll
+      for (int m = 0; m < kG; ++m) {
+        const uint32_t f0 = (uint32_t)(tid + (g + m) * kBlock);
+        const uint32_t f = f0 < n_total ? f0 : 0u;
+        e[m] = rc[(size_t)min(ju[m], (uint32_t)(U - 1)) * a.cap + (f - pv[m])];
+      }
+#pragma unroll
+      for (int m = 0; m < kG; ++m) {
+        const bool keep = (uint32_t)(tid + (g + m) * kBlock) < n_total && e[m].x >= tmax;
+        cnd[tid + (g + m) * kBlock] = keep ? e[m] : make_uint2(0u, 0u);
+        cl += keep ? 1u : 0u;
+      }
     }
   }
-  const uint32_t C = fast ? block_sum(cl, S.red32) : 0u;
+  const uint32_t C = fast ? block_sum(cl, S.red32) : 0u;  // its barriers publish cnd
   if (fast) {
-    if (tmax == kKeyFloor) {  // every tile emitted all of its valid elements
+    if (tmax == kKeyFloor) {  // every unit emitted all of its valid elements
       if ((int)C < want) want = (int)C;
     } else if ((int)C < want) {
       fast = false;  // candidates do not provably contain the top-k
     }
   }
   if (!fast) {
-    int nv;
     *flags |= SS_FLAG_FALLBACK;
-    return fallback_select<DT>(a, c, want, S, sel, &nv);
+    if (tid == 0) S.fc = c;  // S.fa was written at kernel entry
+    lds_barrier();
+    return fallback_select<DT>(want);
   }
   if (want <= 0) return 0;
-  auto visit_regs = [&](auto&& f) {
+  auto visit_lds = [&](auto&& f) {
 #pragma unroll
-    for (int m = 0; m < kRPT; ++m) f(ck[m], ci[m]);
+    for (int m = 0; m < kRPT; ++m) {
+      const uint2 v = cnd[tid + m * kBlock];
+      f(v.x, v.y);
+    }
   };
   uint32_t tk, ti;
-  radix_select(visit_regs, (uint32_t)want, S, &tk, &ti);
+  radix_select(visit_lds, (uint32_t)want, tmax, hi_key, a.V, S, &tk, &ti);
   uint32_t cntl = 0;
 #pragma unroll
-  for (int m = 0; m < kRPT; ++m) cntl += selected(ck[m], ci[m], tk, ti);
+  for (int m = 0; m < kRPT; ++m) {
+    const uint2 v = cnd[tid + m * kBlock];
+    cntl += selected(v.x, v.y, tk, ti);
+  }
   uint32_t tot;
   uint32_t off = block_excl_scan(cntl, S.red32, tot);
 #pragma unroll
-  for (int m = 0; m < kRPT; ++m)
-    if (selected(ck[m], ci[m], tk, ti)) sel[off++] = comp_of(ck[m], ci[m]);
+  for (int m = 0; m < kRPT; ++m) {
+    const uint2 v = cnd[tid + m * kBlock];
+    if (selected(v.x, v.y, tk, ti)) sel[off++] = comp_of(v.x, v.y);
+  }
   return (int)tot;
 }
 
@@ -1028,7 +1108,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S,
   if (2 * tid < U) S.prefix[2 * tid] = pre;
   if (2 * tid + 1 < U) S.prefix[2 * tid + 1] = pre + nl[0];
   if (tid == 0) S.prefix[U] = n_total;
-  hist_clear(S.hist[0]);
+  radix_clear(S, 0);
   lds_barrier();
 
   int flags = c.kcap ? SS_FLAG_KCAP : 0;
@@ -1039,11 +1119,8 @@ __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S,
   if constexpr (OP == OP_TOPK) {
     int n_sel = 0;
     if (!empty && c.k_eff > 0) {
-      n_sel = select_exact<DT>(a, c, S, sel, c.k_eff, tmax, ovf, n_total, &flags);
-      const int N = next_pow2(n_sel);
-      for (int r = n_sel + tid; r < N; r += kBlock) sel[r] = 0ull;
-      lds_barrier();
-      lds_sort_desc(sel, N);
+      n_sel = select_exact<DT>(a, c, S, sel, c.k_eff, tmax, comp_key(Mcomp), ovf, n_total, &flags);
+      sort_selected(sel, n_sel);
     }
     for (int r = tid; r < a.k_cap; r += kBlock) {
       const size_t o = (size_t)b * a.k_cap + r;
@@ -1096,7 +1173,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S,
         }
       }
     } else if (!empty) {
-      const int n_sel = select_exact<DT>(a, c, S, sel, c.k_eff, tmax, ovf, n_total, &flags);
+      const int n_sel = select_exact<DT>(a, c, S, sel, c.k_eff, tmax, comp_key(Mcomp), ovf, n_total, &flags);
       lds_barrier();
       Dist D;
       build_dist(a, c, Mcomp, n_sel, S, sel, D);
@@ -1371,7 +1448,8 @@ template <int DT, int OP>
 __global__ __launch_bounds__(kBlock) void ss_merge_kernel(KArgs a) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Smem& S = *reinterpret_cast<Smem*>(smem_raw);
-  uint64_t* sel = reinterpret_cast<uint64_t*>(smem_raw + kSmemFixed);
+  uint64_t* sel = reinterpret_cast<uint64_t*>(smem_raw + kSelOff);
+  if (threadIdx.x == 0) S.fa = a;  // for the out-of-line fallback
   const Ctx c = make_ctx<DT>(a, blockIdx.x);
   merge_row<DT, OP>(a, c, S, sel);
 }
@@ -1458,7 +1536,7 @@ static bool make_layout(int op, int B, int V, int L, int k_max, Layout* lay) {
   lay->T = T;
   lay->cap = cap;
   lay->rows = rows;
-  lay->smem = kSmemFixed + 8 * next_pow2(k_max);
+  lay->smem = kSelOff + 8 * next_pow2(k_max);
   return true;
 }
 
