@@ -617,8 +617,11 @@ __device__ __forceinline__ void radix_clear(Smem& S, int buf) {
   for (int i = threadIdx.x; i < kHCopies * kHStride; i += kBlock) S.hist[buf][i] = 0u;
   if (threadIdx.x < 64) S.low[buf][threadIdx.x] = 0u;
 }
-__device__ __forceinline__ void hist_add(uint32_t* h, uint32_t bin) {
-  atomicAdd(&h[(lane() & (kHCopies - 1)) * kHStride + bin], 1u);
+__device__ __forceinline__ void hist_add(uint32_t* h, uint32_t bin, bool pred) {
+  if (pred) atomicAdd(&h[(lane() & (kHCopies - 1)) * kHStride + bin], 1u);
+}
+__device__ __forceinline__ void low_mark(uint32_t* low, uint32_t bin, bool pred) {
+  if (pred) reinterpret_cast<uint8_t*>(low)[bin] = 1;
 }
 
 // Digit search by wave 0 over nb <= 256 bins.  Descending: find d with
@@ -670,25 +673,45 @@ __device__ inline void radix_digit(const uint32_t* h, const uint32_t* low, int n
 
 // ---------------------------------------------------------------------------
 // Exact selection of the `want` largest composites (key desc, index asc)
-// among the valid keys a visitor produces.  visit(f) calls f(key, idx) for
-// this thread's elements; every thread calls it the same number of times.
+// among the n_valid valid keys a visitor produces.  visit(f) calls f(key, idx)
+// for this thread's elements; every thread calls it the same number of times.
 // Every valid visited key lies in [lo_key, hi_key]: the bits above the
 // highest bit in which the two bounds differ are common to all of them, so
-// the 8-bit digit passes start just below those bits.  A pass whose chosen
-// bin holds only keys with zero bits below the digit fixes the boundary key
-// at once (bf16 logits leave the low 16 bits zero).  Ties at the boundary key
-// take the lowest indices (indices < V).  Returns (tk, ti): an element is
-// selected iff key > tk or (key == tk and idx <= ti).  Requires radix buffer
-// 0 cleared and published.
+// the 8-bit digit passes start just below those bits (first_window).  A pass
+// whose chosen bin holds only keys with zero bits below the digit fixes the
+// boundary key at once (bf16 logits leave the low 16 bits zero).  Ties at the
+// boundary key take the lowest indices (indices < V): by direct ranking when
+// there are at most kBlock of them, else by index digit passes.  With
+// first_built the caller has already filled radix buffer 0 with the first
+// key pass; otherwise buffer 0 must be cleared and published.  Returns
+// (tk, ti): an element is selected iff key > tk or (key == tk and idx <= ti).
 // ---------------------------------------------------------------------------
+struct Window {
+  int sh;       // shift of the first digit
+  uint32_t dm;  // digit mask of the first pass
+};
+__device__ __forceinline__ Window first_window(uint32_t lo_key, uint32_t hi_key) {
+  const int sh = 32 - __clz(lo_key ^ hi_key);
+  const int w = sh < 8 ? sh : 8;
+  return Window{sh - w, (1u << w) - 1u};
+}
+
 template <typename Visit>
-__device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint32_t lo_key, uint32_t hi_key, int V,
-                                             Smem& S, uint32_t* tk_out, uint32_t* ti_out) {
+__device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint32_t n_valid, uint32_t lo_key,
+                                             uint32_t hi_key, int V, bool first_built, Smem& S, uint32_t* tk_out,
+                                             uint32_t* ti_out) {
   int cur = 0;
   int sh = 32 - __clz(lo_key ^ hi_key);  // bits [0, sh) vary among the keys
   uint32_t prefix = sh >= 32 ? 0u : (hi_key >> sh);
   uint32_t tk = hi_key, ti = 0xFFFFFFFFu;
+  uint32_t n_tie = n_valid;
   bool ties = true;
+  bool skip_visit = first_built;
+  if (want >= n_valid) {  // everything valid is selected
+    tk = kKeyNegInf;
+    ties = false;
+    sh = 0;
+  }
   while (sh > 0) {
     const int w = sh < 8 ? sh : 8;
     sh -= w;
@@ -696,17 +719,19 @@ __device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint3
     const uint32_t dm = (1u << w) - 1u;
     const uint32_t lm = (1u << sh) - 1u;
     uint32_t* h = S.hist[cur];
-    uint8_t* lowb = reinterpret_cast<uint8_t*>(S.low[cur]);
-    visit([&](uint32_t k, uint32_t) {
-      if (k >= kKeyFloor && (hs >= 32 || (k >> hs) == prefix)) {
+    uint32_t* lw = S.low[cur];
+    if (!skip_visit) {
+      visit([&](uint32_t k, uint32_t) {
+        const bool part = k >= kKeyFloor && (hs >= 32 || (k >> hs) == prefix);
         const uint32_t d = (k >> sh) & dm;
-        hist_add(h, d);
-        if (k & lm) lowb[d] = 1;
-      }
-    });
+        hist_add(h, d, part);
+        low_mark(lw, d, part && (k & lm) != 0u);
+      });
+    }
+    skip_visit = false;
     radix_clear(S, cur ^ 1);
     lds_barrier();
-    radix_digit(h, S.low[cur], (int)dm + 1, want, true, S.bc);
+    radix_digit(h, lw, (int)dm + 1, want, true, S.bc);
     const uint32_t d = S.bc[0], above = S.bc[1], hd = S.bc[2], lowd = S.bc[3];
     cur ^= 1;
     if (d > dm) {  // fewer valid keys than `want`: all are selected
@@ -725,11 +750,35 @@ __device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint3
     }
     if (sh == 0 || lowd == 0u) {  // the boundary keys all equal prefix << sh
       tk = prefix << sh;
+      n_tie = hd;
       break;
     }
   }
-  if (ties) {
-    // ties at key tk: the `want` lowest indices
+  if (ties && n_tie <= (uint32_t)kBlock) {
+    // few ties: list their indices, rank each against the others
+    uint32_t cnt = 0;
+    visit([&](uint32_t k, uint32_t) { cnt += k == tk ? 1u : 0u; });
+    uint32_t tot;
+    uint32_t off = block_excl_scan(cnt, S.red32, tot);
+    uint32_t* tl = S.hist[cur];  // free: cleared for a next pass that does not come
+    visit([&](uint32_t k, uint32_t i) {
+      if (k == tk) tl[off++] = i;
+    });
+    lds_barrier();
+    if (threadIdx.x < tot) {
+      const uint32_t my = tl[threadIdx.x];
+      uint32_t r = 0;
+      for (uint32_t j = 0; j < tot; ++j) r += tl[j] < my ? 1u : 0u;
+      if (r == want - 1u) S.bc[4] = my;
+    }
+    lds_barrier();
+    ti = S.bc[4];
+  } else if (ties) {
+    // many ties: the `want` lowest indices by index digit passes
+    if (skip_visit) {  // no key pass ran: buffer 0 still holds the caller's histogram
+      radix_clear(S, cur);
+      lds_barrier();
+    }
     int ib = 32 - __clz((uint32_t)(V > 1 ? V - 1 : 1));
     uint32_t ip = 0u;
     while (ib > 0) {
@@ -738,9 +787,7 @@ __device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint3
       const int hs = ib + w;
       const uint32_t dm = (1u << w) - 1u;
       uint32_t* h = S.hist[cur];
-      visit([&](uint32_t k, uint32_t i) {
-        if (k == tk && (i >> hs) == ip) hist_add(h, (i >> ib) & dm);
-      });
+      visit([&](uint32_t k, uint32_t i) { hist_add(h, (i >> ib) & dm, k == tk && (i >> hs) == ip); });
       radix_clear(S, cur ^ 1);
       lds_barrier();
       radix_digit(h, nullptr, (int)dm + 1, want, false, S.bc);
@@ -808,7 +855,7 @@ __device__ __attribute__((noinline)) int fallback_select(int want) {
   radix_clear(S, 0);
   lds_barrier();
   uint32_t tk, ti;
-  radix_select(visit_row, (uint32_t)want, kKeyFloor, 0xFFFFFFFFu, a.V, S, &tk, &ti);
+  radix_select(visit_row, (uint32_t)want, (uint32_t)nv, kKeyFloor, 0xFFFFFFFFu, a.V, false, S, &tk, &ti);
   uint32_t base = 0;
   for (int j = 0; j < T; ++j) {
     uint32_t key[kPT];
@@ -987,59 +1034,61 @@ __device__ __forceinline__ int select_exact(const KArgs& a, const Ctx& c, Smem& 
                                             uint32_t tmax, uint32_t hi_key, uint32_t ovf, uint32_t n_total,
                                             int* flags) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
-  uint2* cnd = reinterpret_cast<uint2*>(smem_raw + kSmemFixed);  // kRPT * kBlock staged candidates
+  uint2* cnd = reinterpret_cast<uint2*>(smem_raw + kSmemFixed);  // kRPT * kBlock staging slots
   const int tid = threadIdx.x;
   const int U = a.T * kUnits;
+  const uint32_t cap = (uint32_t)a.cap;
   bool fast = ovf == 0u && n_total <= (uint32_t)(kRPT * kBlock);
-  uint32_t cl = 0;
+  // every kept candidate lies in [tmax, hi_key]: the first radix pass is
+  // taken while the candidates arrive
+  const Window fw = first_window(tmax, hi_key);
+  uint32_t cl = 0, keepm = 0;
+  uint2 e[kRPT];
   if (fast) {
-    // candidate f = tid + m * kBlock of the row's unit-major sequence lies in
-    // the unit u with prefix[u] <= f < prefix[u + 1]; the binary searches of
-    // a thread's slots run in lockstep so that their LDS reads, and then the
-    // candidate loads, are in flight together.  Slots at or beyond n_total
-    // (and candidates below tmax) are staged as invalid (key 0).
-    const int lgU = U > 1 ? 32 - __clz((uint32_t)(U - 1)) : 0;
-    const uint2* rc = a.cand + (size_t)c.row * U * a.cap;
-    constexpr int kG = 32;  // slots per batch
-#pragma unroll
-    for (int g = 0; g < kRPT; g += kG) {
-      uint32_t ju[kG], pv[kG];
-#pragma unroll
-      for (int m = 0; m < kG; ++m) {
-        ju[m] = 0u;
-        pv[m] = 0u;
+    // 1. table: slot f of the row's unit-major candidate sequence -> offset
+    //    of that candidate in the row's region (kept in cnd[f].x); each
+    //    wavefront fills the slots of a range of units
+    {
+      const int G = U >= kBlock ? 1 : kBlock / U;  // threads per unit
+      for (int u = tid / G; u < U; u += kBlock / G) {
+        const uint32_t p = S.prefix[u];
+        const uint32_t n = S.prefix[u + 1] - p;
+        for (uint32_t j = (uint32_t)(tid % G); j < n; j += (uint32_t)G) cnd[p + j].x = (uint32_t)u * cap + j;
       }
-      for (int s2 = lgU - 1; s2 >= 0; --s2) {
-        uint32_t pp[kG];
+      // the first radix pass below records no low-bit flags: mark every bin
+      if (tid < 64) S.low[0][tid] = 0x01010101u;
+    }
+    lds_barrier();
+    // 2. gather: every load in flight at once; slots past n_total load the
+    //    region's first entry and are dropped
+    const uint2* rc = a.cand + (size_t)c.row * U * cap;
+    uint32_t gi[kRPT];
 #pragma unroll
-        for (int m = 0; m < kG; ++m) pp[m] = S.prefix[min(ju[m] + (1u << s2), (uint32_t)U)];
+    for (int m = 0; m < kRPT; ++m) {
+      const uint32_t f = (uint32_t)(tid + m * kBlock);
+      gi[m] = f < n_total ? cnd[f].x : 0u;
+    }
 #pragma unroll
-        for (int m = 0; m < kG; ++m) {
-          const uint32_t f0 = (uint32_t)(tid + (g + m) * kBlock);
-          const uint32_t f = f0 < n_total ? f0 : 0u;
-          if (pp[m] <= f) {
-            ju[m] = min(ju[m] + (1u << s2), (uint32_t)U);
-            pv[m] = pp[m];
-          }
-        }
-      }
-      uint2 e[kG];
+    for (int m = 0; m < kRPT; ++m) e[m] = rc[gi[m]];
+    // 3. keep flags, count, first radix pass
+    uint32_t* h = S.hist[0];
 #pragma unroll
-      for (int m = 0; m < kG; ++m) {
-        const uint32_t f0 = (uint32_t)(tid + (g + m) * kBlock);
-        const uint32_t f = f0 < n_total ? f0 : 0u;
-        e[m] = rc[(size_t)min(ju[m], (uint32_t)(U - 1)) * a.cap + (f - pv[m])];
-      }
-#pragma unroll
-      for (int m = 0; m < kG; ++m) {
-        const bool keep = (uint32_t)(tid + (g + m) * kBlock) < n_total && e[m].x >= tmax;
-        cnd[tid + (g + m) * kBlock] = keep ? e[m] : make_uint2(0u, 0u);
-        cl += keep ? 1u : 0u;
-      }
+    for (int m = 0; m < kRPT; ++m) {
+      const bool keep = (uint32_t)(tid + m * kBlock) < n_total && e[m].x >= tmax;
+      keepm |= keep ? (1u << m) : 0u;
+      cl += keep ? 1u : 0u;
+      hist_add(h, (e[m].x >> fw.sh) & fw.dm, keep);
     }
   }
-  const uint32_t C = fast ? block_sum(cl, S.red32) : 0u;  // its barriers publish cnd
+  // 4. compaction of the kept candidates to cnd[0, C): the scan's barriers
+  //    also order every table read above before the writes below
+  uint32_t C = 0;
+  const uint32_t off0 = block_excl_scan(cl, S.red32, C);
   if (fast) {
+    uint32_t off = off0;
+#pragma unroll
+    for (int m = 0; m < kRPT; ++m)
+      if ((keepm >> m) & 1u) cnd[off++] = e[m];
     if (tmax == kKeyFloor) {  // every unit emitted all of its valid elements
       if ((int)C < want) want = (int)C;
     } else if ((int)C < want) {
@@ -1052,29 +1101,29 @@ __device__ __forceinline__ int select_exact(const KArgs& a, const Ctx& c, Smem& 
     lds_barrier();
     return fallback_select<DT>(want);
   }
+  // rows of kBlock compacted slots, padded with invalid entries to a multiple of 4
+  const int nrow = (((int)C + kBlock - 1) / kBlock + 3) & ~3;
+  for (int i = (int)C + tid; i < nrow * kBlock; i += kBlock) cnd[i] = make_uint2(0u, 0u);
+  lds_barrier();
   if (want <= 0) return 0;
-  auto visit_lds = [&](auto&& f) {
+  auto visit_cnd = [&](auto&& f) {
+    for (int r0 = 0; r0 < nrow; r0 += 4) {
+      uint2 v[4];
 #pragma unroll
-    for (int m = 0; m < kRPT; ++m) {
-      const uint2 v = cnd[tid + m * kBlock];
-      f(v.x, v.y);
+      for (int i = 0; i < 4; ++i) v[i] = cnd[tid + (r0 + i) * kBlock];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) f(v[i].x, v[i].y);
     }
   };
   uint32_t tk, ti;
-  radix_select(visit_lds, (uint32_t)want, tmax, hi_key, a.V, S, &tk, &ti);
+  radix_select(visit_cnd, (uint32_t)want, C, tmax, hi_key, a.V, true, S, &tk, &ti);
   uint32_t cntl = 0;
-#pragma unroll
-  for (int m = 0; m < kRPT; ++m) {
-    const uint2 v = cnd[tid + m * kBlock];
-    cntl += selected(v.x, v.y, tk, ti);
-  }
+  visit_cnd([&](uint32_t k, uint32_t i) { cntl += selected(k, i, tk, ti) ? 1u : 0u; });
   uint32_t tot;
   uint32_t off = block_excl_scan(cntl, S.red32, tot);
-#pragma unroll
-  for (int m = 0; m < kRPT; ++m) {
-    const uint2 v = cnd[tid + m * kBlock];
-    if (selected(v.x, v.y, tk, ti)) sel[off++] = comp_of(v.x, v.y);
-  }
+  visit_cnd([&](uint32_t k, uint32_t i) {
+    if (selected(k, i, tk, ti)) sel[off++] = comp_of(k, i);
+  });
   return (int)tot;
 }
 
