@@ -206,6 +206,39 @@ __device__ inline void lds_sort_desc(uint64_t* a, int n) {
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// wave64 helpers built on DPP row operations and ballots (no LDS traffic).
+// Every lane of the wavefront must be active.
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+// maximum over the wavefront, returned in a scalar register
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  v = max(v, dpp_mov<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = max(v, dpp_mov<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = max(v, dpp_mov<0x141>(v));  // row_half_mirror
+  v = max(v, dpp_mov<0x140>(v));  // row_mirror: every lane holds its row's maximum
+  const uint32_t r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+  const uint32_t r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+  return max(max(r0, r1), max(r2, r3));
+}
+// exclusive prefix over lanes of small per-lane counts c < 32 (bit planes
+// counted with mbcnt); `total` receives the wavefront sum
+__device__ __forceinline__ uint32_t wave_excl_small(uint32_t c, uint32_t& total) {
+  uint32_t off = 0u, tot = 0u;
+#pragma unroll
+  for (int b = 0; b < 5; ++b) {
+    const uint64_t m = __ballot((c >> b) & 1u);
+    off += __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u)) << b;
+    tot += (uint32_t)__popcll(m) << b;
+  }
+  total = tot;
+  return off;
+}
+
 __host__ __device__ inline int next_pow2(int v) {
   int p = 1;
   while (p < v) p <<= 1;

@@ -1,30 +1,41 @@
 // ss_kernel.hip -- fused LLM sampling pipeline for MI355X (gfx950).
 //
-// One launch per call (plus one materialising pass for ss_process_logits).
-// Grid: rows x T workgroups, T = ceil(V / kTile).  Each workgroup streams one
-// kTile-element slice of one logit row exactly once and
-//   1. applies the logit-processing prologue (paper Appendix C.1, Alg. 8
-//      order): grammar allow bits, repetition / frequency / presence penalties
-//      and sparse logit bias -- penalties and bias touch only the ids in the
-//      request's history / bias lists, so they are computed once per distinct
-//      id by an "owner" thread and the bulk of the tile pays nothing for them;
-//   2. turns every element into an order-preserving 32-bit key;
-//   3. reduces the tile maximum (greedy rows stop here);
-//   4. for truncating rows, derives an emission threshold from the maxima of
-//      groups of 4 elements (the q-th largest group maximum bounds the tile's
-//      q-th largest element from below) and writes the elements at or above
-//      it to a small per-tile candidate region -- a bounded candidate set, as
-//      in the paper's two-stage scheme (Section 3.2), but with a row-level
-//      quota instead of a fixed per-tile k;
-//   5. takes a ticket; the last workgroup of the row merges: it checks that
-//      the candidates provably contain the row's top-k (at least k of them lie
-//      above the largest tile threshold), selects the exact top-k by radix
-//      select in registers, and runs the truncation / selection epilogue
-//      (Alg. 11 order) in double precision.  If the check fails (skewed or
-//      heavily tied rows) it recomputes the exact top-k by streaming the row
-//      again -- a slow but always-correct path, flagged SS_FLAG_FALLBACK.
-// No host synchronisation, fixed grid, self-resetting counters: every call
-// can be captured in a HIP graph.
+// Two launches per call (plus a verification assembly or a materialising
+// pass for ss_verify / ss_process_logits); the grids depend only on the
+// shapes, nothing synchronises with the host, so every call can be captured
+// in a HIP graph.
+//
+// Streaming kernel.  Every wavefront owns one "unit": 2048 consecutive logits
+// of one row (16-byte loads, 32 elements per lane, read exactly once).  It
+// turns them into order-preserving keys (grammar allow bits applied, NaN ->
+// invalid), finds a unit threshold t -- the largest 16-bit key prefix such
+// that at least q group maxima of the unit reach it, q being the unit's share
+// of the row's top-k plus a statistical margin -- and writes every group of
+// consecutive elements whose maximum reaches t to the unit's candidate region.
+// This is the paper's bounded candidate set of the two-stage scheme (Section
+// 3.2), chosen per unit by ballots instead of a per-tile sort.  Nothing here
+// depends on the request's penalty history or logit bias: those touch at most
+// a few hundred ids per row and are applied in the merge, so the streaming
+// pass has no barrier, no LDS and no per-row list traffic.
+//
+// Merge kernel, one workgroup per row:
+//   1. builds a hash table of the row's penalised / biased ids (LDS; a
+//      generation-tagged table in the workspace when the lists hold more
+//      distinct ids than LDS does) with occurrence counts and ordered bias
+//      sums, gathers their raw logits and applies the Appendix C.1 prologue
+//      (repetition, frequency, presence penalty, bias; Alg. 8 order);
+//   2. gathers the candidate groups, drops the raw copies of patched ids and
+//      keeps the elements at or above the largest unit threshold tmax, plus
+//      the patched final values at or above it.  If at least k of them reach
+//      tmax they provably contain the row's exact top-k; otherwise (candidate
+//      overflow, skewed or heavily tied rows, patched top tokens) an exact
+//      slow path re-reads the units that could hide a top-k element;
+//   3. selects the exact top-k (radix select, ties -> lower index) and runs
+//      the Alg. 11 epilogue: temperature weights, min-p, top-p and the token
+//      draw.  Top-p and the draw are "first element in canonical order whose
+//      running mass crosses a target" searches, done as radix descents with
+//      2^-50 fixed-point mass histograms, so no sort is needed unless the
+//      caller asks for the kept list in order.
 #include <hip/hip_runtime.h>
 #include <limits.h>
 #include <stddef.h>
@@ -35,33 +46,27 @@
 
 namespace ss {
 
-constexpr int kTile = 8192;
-constexpr int kPT = kTile / kBlock;  // element slots per thread (32)
-constexpr int kGPT = 8;              // group maxima per thread
-constexpr int kGS = kPT / kGPT;      // slots per group (4)
-constexpr int kUnits = kWaves;       // emission units per tile: one per wavefront
-constexpr int kUnitElems = kTile / kUnits;  // elements per unit (2048)
-constexpr int kUnitGroups = kGPT * 64;      // group maxima per unit (512)
-constexpr int kHCap = 1024;          // in-tile history entries held in LDS
-constexpr int kBCap = 128;           // in-tile bias entries held in LDS
-constexpr int kPCap = 128;           // patched slots per wavefront held in LDS
-constexpr int kIdsPT = 2;            // history ids each thread loads up front
-constexpr int kRPT = 32;             // merge candidates per thread (registers)
-constexpr int kMaxT = (SS_MAX_V + kTile - 1) / kTile;
-constexpr int kMaxU = kMaxT * kUnits;  // emission units per row
-constexpr int kEPT = SS_MAX_K / kBlock;  // selected entries per thread in the epilogue
-constexpr int kHCopies = 4;              // privatised histogram copies (lane & 3)
-constexpr int kHStride = 257;            // padded so copies of one bin sit in different banks
-constexpr uint32_t kNoEmit = 0xFFFFFFFFu;  // emits nothing (above every valid key)
-constexpr double kFix = 1125899906842624.0;  // 2^50: fixed-point scale of weight sums
+constexpr int kUE = 2048;                    // elements per unit (one wavefront)
+constexpr int kMaxU = SS_MAX_V / kUE;        // units per row at most (512)
+constexpr int kH = 1024;                     // patch hash slots
+constexpr int kProbe = 64;                   // longest probe sequence before giving up
+constexpr int kGH = 16384;                   // per-row patch table in global memory (LDS table overflow)
+constexpr int kGProbe = 1024;
+constexpr uint32_t kLinear = 0xFFFFFFFFu;    // patched-list count meaning "look the lists up"
+constexpr int kHCopies = 2;                  // privatised radix histograms
+constexpr int kHStride = 257;
+constexpr int kTS = SS_MAX_K / kBlock;       // selected elements per thread (16)
+constexpr int kGB = 8;                       // candidate groups loaded per thread per batch
+constexpr uint32_t kNoEmit = 0xFFFFFFFFu;    // threshold of a unit that emits nothing
+constexpr double kFix = 1125899906842624.0;  // 2^50: fixed-point scale of probability mass
 
 enum { OP_TOPK = SS_OP_TOPK, OP_SAMPLE = SS_OP_SAMPLE, OP_VERIFY = SS_OP_VERIFY, OP_PROCESS = SS_OP_PROCESS };
 enum { KIND_EMPTY = 0, KIND_GREEDY = 1, KIND_DIST = 2 };
 
 struct RowSummary {
-  uint64_t thr;  // composite key of the last kept rank
+  uint64_t thr;  // composite key of the last kept element
   double Z;      // sum of kept weights
-  float M;       // row maximum
+  float M;       // row maximum (processed logit)
   float tau;
   int32_t argmax;
   int32_t kind;
@@ -76,7 +81,7 @@ struct RowResult {
 struct KArgs {
   const void* x;
   int64_t ld;
-  int op, B, rows, V, T, L, k_cap, cap, k_out, vec_ok;
+  int op, B, rows, V, U, L, k_cap, cap, pcap, k_out, vec_ok;
   uint32_t feat;
   const uint32_t* mode;
   const float* temperature;
@@ -108,13 +113,75 @@ struct KArgs {
   int32_t* out_nacc;
   float* out_logits;
   float* out_probs;
-  uint32_t* ticket;
-  uint32_t* req_ticket;
   uint4* rec;
-  uint2* cand;
+  uint4* cand;
   RowResult* res;
   RowSummary* summ;
+  uint2* patched;      // process: per row kGH (id, final key) pairs
+  uint64_t* gtag;      // per row kGH slots: (generation << 32) | (id + 1)
+  uint32_t* gcnt;      // occurrence count | has-bias bit 31
+  uint32_t* gfin;      // final key
+  uint32_t* ggen;      // per row generation counter
+  uint32_t* npatched;  // process: per row count
 };
+
+// ---------------------------------------------------------------------------
+// Element layout: lane l, slot s (0..31) holds element (s / VW * 64 + l) * VW
+// + s % VW of its unit; a chunk of VW consecutive elements is one 16-byte load.
+// Emission groups are GE consecutive elements (two key dwords).
+// ---------------------------------------------------------------------------
+template <int DT>
+struct DTT;
+template <>
+struct DTT<SS_F32> {
+  static constexpr int VW = 4, NLD = 8, ES = 4, GPL = 16, GE = 2;
+};
+template <>
+struct DTT<SS_BF16> {
+  static constexpr int VW = 8, NLD = 4, ES = 2, GPL = 8, GE = 4;
+};
+
+__host__ __device__ inline int groups_per_unit(int dt) { return dt == SS_BF16 ? 512 : 1024; }
+
+// key without the positive-NaN fold; callers fold when the maximum exceeds +inf
+__device__ __forceinline__ uint32_t key_raw(uint32_t u) {
+  const uint32_t s = (uint32_t)((int32_t)u >> 31);
+  return (u ^ s) + (s ? 1u : 0x80000000u);
+}
+__device__ __forceinline__ uint32_t fold_nan(uint32_t k) { return k > kKeyPosInf ? 0u : k; }
+
+typedef unsigned short us2 __attribute__((ext_vector_type(2)));
+typedef short ss2 __attribute__((ext_vector_type(2)));
+// two packed bfloat16 -> two packed 16-bit keys (the upper halves of their
+// float32 keys: bf16 keys have zero low halves)
+__device__ __forceinline__ uint32_t key2_bf16(uint32_t d) {
+  const ss2 v = __builtin_bit_cast(ss2, d);
+  const uint32_t s = __builtin_bit_cast(uint32_t, (ss2)(v >> (ss2){15, 15}));
+  const uint32_t c = (s & 0x80018001u) ^ 0x80008000u;
+  const us2 r = __builtin_bit_cast(us2, d ^ s) + __builtin_bit_cast(us2, c);
+  return __builtin_bit_cast(uint32_t, r);
+}
+__device__ __forceinline__ uint32_t pkmax16(uint32_t a, uint32_t b) {
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(us2, a), __builtin_bit_cast(us2, b)));
+}
+__device__ __forceinline__ uint32_t hmax16(uint32_t d) { return max(d & 0xFFFFu, d >> 16); }
+// positive bf16 NaN keys (above +inf = 0xFF80) -> 0 in both halves
+__device__ __forceinline__ uint32_t fold_nan2(uint32_t d) {
+  uint32_t lo = d & 0xFFFFu, hi = d >> 16;
+  lo = lo > 0xFF80u ? 0u : lo;
+  hi = hi > 0xFF80u ? 0u : hi;
+  return lo | (hi << 16);
+}
+
+// float32 bit pattern of element i of a row (scalar access, any alignment)
+template <int DT>
+__device__ __forceinline__ uint32_t load_elem_bits(const unsigned char* xrow, int64_t i) {
+  if constexpr (DT == SS_F32) {
+    return reinterpret_cast<const uint32_t*>(xrow)[i];
+  } else {
+    return ((uint32_t)reinterpret_cast<const uint16_t*>(xrow)[i]) << 16;
+  }
+}
 
 // ---------------------------------------------------------------------------
 // Per-row context
@@ -136,89 +203,6 @@ struct Ctx {
   bool kcap;
   int k_eff;
 };
-
-struct Smem {
-  uint64_t red64[kWaves];
-  double redd[kWaves];
-  double bcd[4];
-  uint2 pw[kWaves][kPCap];  // per-wave patched slots: (lane | slot<<6 | bias<<11 | count<<12, bias sum)
-  uint32_t bm[kBlock];      // per-thread bits of patched slots
-  int32_t bl_pos[kBCap];
-  float bl_val[kBCap];
-  uint32_t prefix[kMaxU + 1];
-  uint32_t pw_n[kWaves];
-  uint32_t red32[kWaves];
-  uint32_t cnt[4];
-  uint32_t bc[8];
-  uint16_t hl[kHCap];  // distinct history ids of the tile (local index)
-  uint16_t bl_l[kBCap];
-  uint32_t cnt8[kTile / 4];     // packed 8-bit occurrence counts per local index
-  // merge only from here
-  uint32_t hist[2][kHCopies * kHStride];  // double-buffered privatised radix histograms
-  uint32_t low[2][64];  // per bin (bytes): some key in the bin has non-zero bits below the digit
-  KArgs fa;              // kernel arguments and row context handed to the fallback
-  Ctx fc;
-};
-constexpr int kSmemStream = (int)((offsetof(Smem, hist) + 15) & ~(size_t)15);
-constexpr int kSmemFixed = (int)((sizeof(Smem) + 15) & ~(size_t)15);
-// merge dynamic LDS: [Smem][candidates: kRPT * kBlock uint2][sel: next_pow2(k_max) uint64]
-constexpr int kCandBytes = 8 * kRPT * kBlock;
-constexpr int kSelOff = kSmemFixed + kCandBytes;
-
-// ---------------------------------------------------------------------------
-// Element layout: thread t, slot j (0..31) holds chunk i = j / VW, element
-// e = j % VW of vector v = i * kBlock + t, i.e. local index (v * VW + e).
-// A chunk is one 16-byte load (8 bf16 or 4 float32).
-// ---------------------------------------------------------------------------
-template <int DT>
-struct DTT;
-template <>
-struct DTT<SS_F32> {
-  static constexpr int VW = 4, NV = 8, ES = 4;
-};
-template <>
-struct DTT<SS_BF16> {
-  static constexpr int VW = 8, NV = 4, ES = 2;
-};
-
-template <int DT>
-__device__ __forceinline__ int local_of_slot(int t, int j) {
-  constexpr int VW = DTT<DT>::VW;
-  return ((j / VW) * kBlock + t) * VW + (j % VW);
-}
-
-// key without the positive-NaN fold; callers fold when the maximum exceeds +inf
-__device__ __forceinline__ uint32_t key_raw(uint32_t u) {
-  const uint32_t s = (uint32_t)((int32_t)u >> 31);
-  return (u ^ s) + (s ? 1u : 0x80000000u);
-}
-__device__ __forceinline__ uint32_t fold_nan(uint32_t k) { return k > kKeyPosInf ? 0u : k; }
-
-__device__ __forceinline__ uint32_t comp4(const uint4& v, int c) {
-  return c == 0 ? v.x : (c == 1 ? v.y : (c == 2 ? v.z : v.w));
-}
-
-// float32 bit pattern of slot j
-template <int DT>
-__device__ __forceinline__ uint32_t slot_bits(const uint4 (&r)[DTT<DT>::NV], int j) {
-  if constexpr (DT == SS_F32) {
-    return comp4(r[j >> 2], j & 3);
-  } else {
-    const uint32_t w = comp4(r[j >> 3], (j & 7) >> 1);
-    return (j & 1) ? (w & 0xFFFF0000u) : (w << 16);
-  }
-}
-
-// raw element load from global memory (scalar), as float32 bits
-template <int DT>
-__device__ __forceinline__ uint32_t load_elem_bits(const unsigned char* xrow, int64_t i) {
-  if constexpr (DT == SS_F32) {
-    return reinterpret_cast<const uint32_t*>(xrow)[i];
-  } else {
-    return ((uint32_t)reinterpret_cast<const uint16_t*>(xrow)[i]) << 16;
-  }
-}
-
 
 template <int DT>
 __device__ __forceinline__ Ctx make_ctx(const KArgs& a, int row) {
@@ -269,16 +253,17 @@ __device__ __forceinline__ Ctx make_ctx(const KArgs& a, int row) {
     const int64_t kreq = ((m & SS_TOPK) && a.top_k[b] >= 1) ? (int64_t)a.top_k[b] : (int64_t)INT_MAX;
     c.k_eff = kreq < a.k_cap ? (int)kreq : a.k_cap;
     c.kcap = !c.greedy && kreq > a.k_cap;
+    if (c.greedy) c.k_eff = 1;
   }
   return c;
 }
 
-// Candidate quota of one emission unit when a row's top-k is spread over U
-// units: the unit emits at least its q largest elements (by its threshold),
-// with q well above the unit's expected share k/U, so that the largest unit
-// threshold lies below the row's k-th value except with tiny probability.
+// Candidate quota of one unit when a row's top-k is spread over U units: the
+// unit keeps at least its q largest elements, q well above the expected share
+// k/U (five standard deviations plus six), so that the largest unit threshold
+// lies below the row's k-th value except with negligible probability.
 __host__ __device__ inline int quota(int k, int U) {
-  if (U <= 1) return k;
+  if (U <= 1 || k <= 1) return k;
   const int kt = (k + U - 1) / U;
   int s = 0;
   while (s * s < kt) ++s;
@@ -286,18 +271,27 @@ __host__ __device__ inline int quota(int k, int U) {
   return q < k ? q : k;
 }
 
-// capacity of one unit's candidate region
-__host__ __device__ inline int unit_cap(int kcap, int U) {
-  const int q = quota(kcap, U);
-  if (2 * q > kUnitGroups) return kUnitElems;
-  const int c = 2 * q + 32;
-  return c < kUnitElems ? c : kUnitElems;
+// threshold groups per lane for quota q (groups of 32/G elements); 0 when the
+// quota is too large for a group threshold and the unit emits all it has
+__host__ __device__ inline int thr_groups(int q, int gpl) {
+  for (int G = 1; G <= gpl; G <<= 1)
+    if (64 * G >= 4 * q) return G;
+  return 0;
+}
+
+// capacity (groups) of one unit's candidate region
+__host__ __device__ inline int unit_cap(int k_cap, int U, int dt) {
+  const int gpu = groups_per_unit(dt);
+  const int q = quota(k_cap, U);
+  if (thr_groups(q, dt == SS_BF16 ? 8 : 16) == 0) return gpu;
+  const int c = 2 * q + 64;
+  return c < gpu ? c : gpu;
 }
 
 // ---------------------------------------------------------------------------
-// Prologue of one element in Appendix C.1 order, each step one float32 op:
-// repetition penalty, frequency and presence penalties (count > 0), then the
-// logit bias.  Grammar masking is applied by the caller.
+// Prologue of one patched element in Appendix C.1 order, each step one
+// float32 op: repetition penalty, frequency and presence penalties (count >
+// 0), then the logit bias.  Grammar masking is applied by the caller.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t penalised_key(uint32_t bits, uint32_t mode, float rep, float freq, float pres,
                                                   int count, bool has_bias, float bsum) {
@@ -314,306 +308,358 @@ __device__ __forceinline__ uint32_t penalised_key(uint32_t bits, uint32_t mode, 
   return key_of_float(v);
 }
 
-template <int DT>
-__device__ __forceinline__ void slot_of_local(int l, int* t, int* j) {
-  constexpr int VW = DTT<DT>::VW;
-  const int v = l / VW, e = l % VW;
-  *t = v % kBlock;
-  *j = (v / kBlock) * VW + e;
+// ===========================================================================
+// Streaming phase: one unit per wavefront
+// ===========================================================================
+template <int NW>
+__device__ __forceinline__ uint32_t thr_search(const uint32_t (&gm)[NW], uint32_t q, int shift) {
+  // largest 16-bit prefix p with at least q of the wavefront's values >= p << shift
+  uint32_t prefix = 0u;
+#pragma unroll 1
+  for (int b = 15; b >= 0; --b) {
+    const uint32_t cand = (prefix | (1u << b)) << shift;
+    uint32_t cnt = 0u;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) cnt += (uint32_t)__popcll(__ballot(gm[i] >= cand));
+    if (cnt >= q) prefix |= 1u << b;
+  }
+  return prefix << shift;
 }
 
-template <int DT>
-__device__ __forceinline__ void set_patch_bit(Smem& S, int l) {
-  int t, j;
-  slot_of_local<DT>(l, &t, &j);
-  atomicOr(&S.bm[t], 1u << j);
+// threshold over G groups per lane of the 32 keys held as bf16 pairs
+template <int G>
+__device__ __forceinline__ uint32_t thr_bf16(const uint32_t (&kd)[16], uint32_t q) {
+  constexpr int D = 16 / G;
+  uint32_t gm[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    uint32_t m = kd[g * D];
+#pragma unroll
+    for (int j = 1; j < D; ++j) m = pkmax16(m, kd[g * D + j]);
+    gm[g] = hmax16(m);
+  }
+  return thr_search<G>(gm, q, 0);
+}
+template <int G>
+__device__ __forceinline__ uint32_t thr_f32(const uint32_t (&kk)[32], uint32_t q) {
+  constexpr int D = 32 / G;
+  uint32_t gm[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    uint32_t m = kk[g * D];
+#pragma unroll
+    for (int j = 1; j < D; ++j) m = max(m, kk[g * D + j]);
+    gm[g] = m;
+  }
+  return thr_search<G>(gm, q, 16);
 }
 
-// float32 bits of raw slot j for a wave-uniform j: the chunk registers are
-// viewed as one vector so the uniform index becomes register-relative moves.
-typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x32 __attribute__((ext_vector_type(32)));
+// Streams unit `gu` (wave-uniform) and writes its record and candidate groups.
 template <int DT>
-__device__ __forceinline__ uint32_t slot_bits_uniform(const uint4 (&r)[DTT<DT>::NV], int j) {
-  if constexpr (DT == SS_F32) {
-    u32x32 v;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      v[4 * q + 0] = r[q].x;
-      v[4 * q + 1] = r[q].y;
-      v[4 * q + 2] = r[q].z;
-      v[4 * q + 3] = r[q].w;
-    }
-    return v[j];
-  } else {
-    u32x16 v;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      v[4 * q + 0] = r[q].x;
-      v[4 * q + 1] = r[q].y;
-      v[4 * q + 2] = r[q].z;
-      v[4 * q + 3] = r[q].w;
-    }
-    const uint32_t w = v[j >> 1];
-    return (j & 1) ? (w & 0xFFFF0000u) : (w << 16);
-  }
-}
+__device__ __forceinline__ void scan_unit(const KArgs& a, int gu) {
+  constexpr int VW = DTT<DT>::VW, NLD = DTT<DT>::NLD, ES = DTT<DT>::ES, GPL = DTT<DT>::GPL;
+  const int ln = lane();
+  const int row = gu / a.U;
+  const int u = gu - row * a.U;
+  const int lo = u * kUE;
+  const int n = min(kUE, a.V - lo);
+  const int b = a.op == OP_VERIFY ? row / (a.L + 1) : row;
+  const uint32_t mode = (a.op == OP_TOPK ? SS_TOPK : (a.mode ? a.mode[b] : 0u)) & a.feat;
+  const uint32_t* mask = (mode & SS_GRAMMAR) ? a.bitmask + (size_t)row * (size_t)a.mask_ld : nullptr;
+  const unsigned char* xrow = reinterpret_cast<const unsigned char*>(a.x) + (size_t)row * (size_t)a.ld * ES;
 
-// ---------------------------------------------------------------------------
-// Loads one tile and produces the processed keys of this thread's 32 slots
-// (0 = invalid: masked, NaN, beyond V).  The request's history / bias ids are
-// fetched before the tile so that building the in-tile patch lists overlaps
-// the tile's own loads; one owner per distinct id computes its occurrence
-// count and ordered bias sum from LDS, and the thread holding that element
-// applies the penalties to its registers.  Long lists that overflow LDS fall
-// back to per-slot scans of the global lists (rare, exact).
-// ---------------------------------------------------------------------------
-template <int DT, bool FULL>
-__device__ __forceinline__ void load_tile(const KArgs& a, const Ctx& c, int lo, Smem& S, uint32_t (&key)[kPT]) {
-  constexpr int VW = DTT<DT>::VW, NV = DTT<DT>::NV, ES = DTT<DT>::ES;
-  const int tid = threadIdx.x;
-  const int V = a.V;
-  const int n_tile = min(kTile, V - lo);
-  const bool do_hist = (c.mode & (SS_REP | SS_FREQ | SS_PRES)) && (c.nhist + c.nextra) > 0;
-  const bool do_bias = (c.mode & SS_BIAS) && c.nbias > 0;
-  const bool patch = do_hist || do_bias;
-  const int nh = c.nhist + c.nextra;
-
-  // 1. request lists and grammar words first, as a fixed sequence of loads
-  //    (disabled entries read a dummy in-bounds address), so that waiting for
-  //    them never has to drain the tile loads issued after them.
-  const int32_t* dummy = reinterpret_cast<const int32_t*>(c.xrow);
-  int hid[kIdsPT];
+  // 1. loads: the unit's chunks, then the grammar words that cover them
+  uint4 r[NLD];
+  if (a.vec_ok && n == kUE) {
+    const uint4* src = reinterpret_cast<const uint4*>(xrow + (size_t)lo * ES);
 #pragma unroll
-  for (int u = 0; u < kIdsPT; ++u) {
-    const int h = tid + u * kBlock;
-    const bool ok = do_hist && h < nh;
-    const int32_t* src = !ok ? dummy : (h < c.nhist ? c.hist + h : c.extra + (h - c.nhist));
-    hid[u] = *src;
-    if (!ok) hid[u] = -1;
-  }
-  const bool bok = do_bias && tid < c.nbias;
-  int bid = *(bok ? c.bias_ids + tid : dummy);
-  float bval = *(bok ? c.bias_vals + tid : reinterpret_cast<const float*>(dummy));
-  if (!bok) bid = -1;
-  uint32_t mw[NV];
-  {
-    const int W = (V + 31) >> 5;
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int wi = (lo + (i * kBlock + tid) * VW) >> 5;
-      const bool ok = c.mask != nullptr && wi < W;
-      mw[i] = *(ok ? c.mask + wi : reinterpret_cast<const uint32_t*>(dummy));
-      if (!ok) mw[i] = 0u;
-    }
-  }
-
-  // 2. the tile
-  uint4 raw[NV];
-  if constexpr (FULL) {
-    // full, aligned tile: all 16-byte loads in flight together
-    const uint4* src = reinterpret_cast<const uint4*>(c.xrow + (size_t)lo * ES);
-#pragma unroll
-    for (int i = 0; i < NV; ++i) raw[i] = src[i * kBlock + tid];
+    for (int i = 0; i < NLD; ++i) r[i] = src[i * 64 + ln];
   } else {
 #pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const int l0 = (i * kBlock + tid) * VW;
-    if (a.vec_ok && l0 + VW <= n_tile) {
-      raw[i] = *reinterpret_cast<const uint4*>(c.xrow + ((size_t)lo + l0) * ES);
-    } else {
-      uint32_t w[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) w[q] = 0xFFFFFFFFu;  // negative NaN: invalid
+    for (int i = 0; i < NLD; ++i) {
+      const int l0 = (i * 64 + ln) * VW;
+      uint32_t w[4] = {0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};  // negative NaN: invalid
 #pragma unroll
       for (int e = 0; e < VW; ++e) {
-        const int l = l0 + e;
-        if (l < n_tile) {
+        if (l0 + e < n) {
           if constexpr (DT == SS_F32) {
-            w[e] = reinterpret_cast<const uint32_t*>(c.xrow)[lo + l];
+            w[e] = reinterpret_cast<const uint32_t*>(xrow)[lo + l0 + e];
           } else {
-            const uint32_t h = reinterpret_cast<const uint16_t*>(c.xrow)[lo + l];
+            const uint32_t h = reinterpret_cast<const uint16_t*>(xrow)[lo + l0 + e];
             const int q = e >> 1;
             w[q] = (e & 1) ? ((w[q] & 0x0000FFFFu) | (h << 16)) : ((w[q] & 0xFFFF0000u) | h);
           }
         }
       }
-      raw[i] = make_uint4(w[0], w[1], w[2], w[3]);
+      r[i] = make_uint4(w[0], w[1], w[2], w[3]);
     }
   }
-  }
-  // 3. in-tile patch lists and owners (LDS only; overlaps the tile loads).
-  //    Occurrences are counted in a packed 8-bit table; the entry whose
-  //    increment finds zero owns the id and records it once.  A count that
-  //    would pass 255 sends the tile to the exact slow path.
-  bool overflow = false;
-  if (patch) {
-    S.bm[tid] = 0u;
-    if (tid < 4) S.cnt[tid] = 0u;
-    if (tid < kWaves) S.pw_n[tid] = 0u;
+  uint32_t mw[NLD];
+  if (mask) {
+    const int W = (a.V + 31) >> 5;
 #pragma unroll
-    for (int q = 0; q < kTile / 4 / kBlock / 4; ++q)
-      reinterpret_cast<uint4*>(S.cnt8)[q * kBlock + tid] = make_uint4(0u, 0u, 0u, 0u);
-    lds_barrier();
-    auto add_hist = [&](int id) {
-      const int rel = id - lo;
-      if (id >= 0 && id < V && rel >= 0 && rel < n_tile) {
-        const uint32_t sh = (uint32_t)(rel & 3) * 8u;
-        const uint32_t old = (atomicAdd(&S.cnt8[rel >> 2], 1u << sh) >> sh) & 0xFFu;
-        if (old == 0xFFu) S.cnt[2] = 1u;  // saturated
-        if (old == 0u) {
-          const uint32_t p = atomicAdd(&S.cnt[0], 1u);
-          if (p < (uint32_t)kHCap) S.hl[p] = (uint16_t)rel;
-          set_patch_bit<DT>(S, rel);
-        }
-      }
-    };
-#pragma unroll
-    for (int u = 0; u < kIdsPT; ++u) add_hist(hid[u]);
-    for (int h = tid + kIdsPT * kBlock; h < nh; h += kBlock)  // long histories
-      add_hist(h < c.nhist ? c.hist[h] : c.extra[h - c.nhist]);
-    auto add_bias = [&](int e, int id, float val) {
-      const int rel = id - lo;
-      if (id >= 0 && id < V && rel >= 0 && rel < n_tile) {
-        const uint32_t p = atomicAdd(&S.cnt[1], 1u);
-        if (p < (uint32_t)kBCap) {
-          S.bl_l[p] = (uint16_t)rel;
-          S.bl_pos[p] = e;
-          S.bl_val[p] = val;
-        }
-        set_patch_bit<DT>(S, rel);
-      }
-    };
-    if (do_bias && tid < c.nbias) add_bias(tid, bid, bval);
-    for (int e = tid + kBlock; e < c.nbias; e += kBlock) add_bias(e, c.bias_ids[e], c.bias_vals[e]);
-    lds_barrier();
-    const int hl_n = (int)S.cnt[0], bl_n = (int)S.cnt[1];
-    overflow = hl_n > kHCap || bl_n > kBCap || S.cnt[2] != 0u;
-    if (!overflow) {
-      for (int n = tid; n < hl_n + bl_n; n += kBlock) {
-        int l;
-        bool owner = true;
-        if (n < hl_n) {
-          l = S.hl[n];
-        } else {
-          const int nb = n - hl_n;
-          l = S.bl_l[nb];
-          // ids with a history count are owned by their history entry
-          owner = ((S.cnt8[l >> 2] >> ((l & 3) * 8)) & 0xFFu) == 0u;
-          for (int m = 0; m < nb && owner; ++m)
-            if (S.bl_l[m] == l) owner = false;
-        }
-        if (!owner) continue;
-        const int cntv = (int)((S.cnt8[l >> 2] >> ((l & 3) * 8)) & 0xFFu);
-        float bsum = 0.0f;
-        bool hb = false;
-        if (do_bias) {
-          int last = -1;
-          for (;;) {  // this id's entries in list order
-            int best = INT_MAX, bi = -1;
-            for (int m = 0; m < bl_n; ++m)
-              if (S.bl_l[m] == l && S.bl_pos[m] > last && S.bl_pos[m] < best) {
-                best = S.bl_pos[m];
-                bi = m;
-              }
-            if (bi < 0) break;
-            bsum = bsum + S.bl_val[bi];
-            hb = true;
-            last = best;
-          }
-        }
-        int t, j;
-        slot_of_local<DT>(l, &t, &j);
-        const int w = t >> 6;
-        const uint32_t p = atomicAdd(&S.pw_n[w], 1u);
-        if (p < (uint32_t)kPCap)
-          S.pw[w][p] = make_uint2((uint32_t)(t & 63) | ((uint32_t)j << 6) | ((hb ? 1u : 0u) << 11) |
-                                      ((uint32_t)cntv << 12),
-                                  __float_as_uint(bsum));
-      }
-      lds_barrier();
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) overflow = overflow || S.pw_n[w] > (uint32_t)kPCap;
+    for (int i = 0; i < NLD; ++i) {
+      const int wi = (lo + (i * 64 + ln) * VW) >> 5;
+      mw[i] = wi < W ? mask[wi] : 0u;
     }
   }
 
-  // 4. keys (grammar allow bits first: one per slot); the keys live in one
-  //    vector so a patched slot can be written with a wave-uniform index
-  uint32_t allow = 0xFFFFFFFFu;
-  if (c.mask) {
-    allow = 0u;
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int g0 = lo + (i * kBlock + tid) * VW;
-      allow |= ((mw[i] >> (g0 & 31)) & ((1u << VW) - 1u)) << (i * VW);
-    }
-  }
-  u32x32 kv;
-  if (c.mask) {
-#pragma unroll
-    for (int j = 0; j < kPT; ++j) {
-      const uint32_t k = key_raw(slot_bits<DT>(raw, j));
-      kv[j] = ((allow >> j) & 1u) ? k : 0u;
-    }
+  // 2. row parameters (scalar), read while the chunks are in flight
+  int k_eff;
+  if (a.op == OP_TOPK) {
+    const int k = a.top_k ? a.top_k[b] : a.k_cap;
+    k_eff = k < 0 ? 0 : min(k, a.k_cap);
   } else {
-#pragma unroll
-    for (int j = 0; j < kPT; ++j) kv[j] = key_raw(slot_bits<DT>(raw, j));
+    const bool greedy = (mode & SS_GREEDY) || ((mode & SS_TEMP) && a.temperature[b] <= 0.0f);
+    k_eff = greedy ? 1 : (((mode & SS_TOPK) && a.top_k[b] >= 1) ? min(a.top_k[b], a.k_cap) : a.k_cap);
   }
 
-  // 5. penalties / bias: the holder of each patched slot rewrites its key
-  if (patch && !overflow) {
-    const int w = wave();
-    const int n = (int)S.pw_n[w];
-    for (int e = 0; e < n; ++e) {
-      const uint2 ent = S.pw[w][e];
-      const uint32_t hdr = __builtin_amdgcn_readfirstlane(ent.x);
-      const int slot = (int)((hdr >> 6) & 31u);
-      const uint32_t bits = slot_bits_uniform<DT>(raw, slot);
-      if (lane() == (int)(hdr & 63u) && ((allow >> slot) & 1u)) {
-        kv[slot] = penalised_key(bits, c.mode, c.rep, c.freq, c.pres, (int)(hdr >> 12), ((hdr >> 11) & 1u) != 0u,
-                                 __uint_as_float(__builtin_amdgcn_readfirstlane(ent.y)));
+  // 3. keys, unit maximum, threshold, emission
+  uint4* region = a.cand + (size_t)gu * (size_t)a.cap;
+  const uint32_t cap = (uint32_t)a.cap;
+  uint32_t t, wm, total;
+  if constexpr (DT == SS_BF16) {
+    uint32_t kd[16];
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      kd[4 * i + 0] = key2_bf16(r[i].x);
+      kd[4 * i + 1] = key2_bf16(r[i].y);
+      kd[4 * i + 2] = key2_bf16(r[i].z);
+      kd[4 * i + 3] = key2_bf16(r[i].w);
+    }
+    if (mask) {
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        const uint32_t bits = mw[i] >> (((i * 64 + ln) * 8) & 31);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const uint32_t b2 = bits >> (2 * w);
+          const uint32_t m = ((b2 & 1u) ? 0x0000FFFFu : 0u) | ((b2 & 2u) ? 0xFFFF0000u : 0u);
+          kd[4 * i + w] &= m;
+        }
+      }
+    }
+    uint32_t lm = kd[0];
+#pragma unroll
+    for (int j = 1; j < 16; ++j) lm = pkmax16(lm, kd[j]);
+    uint32_t wm16 = wave_max_u32(hmax16(lm));
+    if (wm16 > 0xFF80u) {  // a positive NaN in this unit: fold it to invalid
+#pragma unroll
+      for (int j = 0; j < 16; ++j) kd[j] = fold_nan2(kd[j]);
+      lm = kd[0];
+#pragma unroll
+      for (int j = 1; j < 16; ++j) lm = pkmax16(lm, kd[j]);
+      wm16 = wave_max_u32(hmax16(lm));
+    }
+    uint32_t t16;
+    if (k_eff <= 0) {
+      t16 = 0x10000u;  // above every key: nothing emitted
+    } else if (wm16 < 0x0081u) {
+      t16 = 0x0081u;  // nothing valid
+    } else {
+      const uint32_t q = (uint32_t)quota(k_eff, a.U);
+      const int G = thr_groups((int)q, GPL);
+      if (q <= 1) t16 = wm16;
+      else if (G == 1) t16 = thr_bf16<1>(kd, q);
+      else if (G == 2) t16 = thr_bf16<2>(kd, q);
+      else if (G == 4) t16 = thr_bf16<4>(kd, q);
+      else if (G == 8) t16 = thr_bf16<8>(kd, q);
+      else t16 = 0x0081u;
+      t16 = max(t16, 0x0081u);
+    }
+    uint32_t gmask = 0u;
+#pragma unroll
+    for (int g = 0; g < 8; ++g) gmask |= (hmax16(pkmax16(kd[2 * g], kd[2 * g + 1])) >= t16) ? (1u << g) : 0u;
+    const uint32_t off = wave_excl_small((uint32_t)__popc(gmask), total);
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      if ((gmask >> g) & 1u) {
+        const uint32_t p = off + (uint32_t)__popc(gmask & ((1u << g) - 1u));
+        const uint32_t idx0 = (uint32_t)(lo + ((g >> 1) * 64 + ln) * 8 + (g & 1) * 4);
+        if (p < cap) region[p] = make_uint4(idx0, kd[2 * g], kd[2 * g + 1], 0u);
+      }
+    }
+    t = t16 >= 0x10000u ? kNoEmit : (t16 << 16);
+    wm = wm16 << 16;
+  } else {
+    uint32_t kk[32];
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      kk[4 * i + 0] = key_raw(r[i].x);
+      kk[4 * i + 1] = key_raw(r[i].y);
+      kk[4 * i + 2] = key_raw(r[i].z);
+      kk[4 * i + 3] = key_raw(r[i].w);
+    }
+    if (mask) {
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        const uint32_t bits = mw[i] >> (((i * 64 + ln) * 4) & 31);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) kk[4 * i + w] = ((bits >> w) & 1u) ? kk[4 * i + w] : 0u;
+      }
+    }
+    uint32_t lm = kk[0];
+#pragma unroll
+    for (int j = 1; j < 32; ++j) lm = max(lm, kk[j]);
+    wm = wave_max_u32(lm);
+    if (wm > kKeyPosInf) {
+#pragma unroll
+      for (int j = 0; j < 32; ++j) kk[j] = fold_nan(kk[j]);
+      lm = kk[0];
+#pragma unroll
+      for (int j = 1; j < 32; ++j) lm = max(lm, kk[j]);
+      wm = wave_max_u32(lm);
+    }
+    if (k_eff <= 0) {
+      t = kNoEmit;
+    } else if (wm < kKeyFloor) {
+      t = kKeyFloor;
+    } else {
+      const uint32_t q = (uint32_t)quota(k_eff, a.U);
+      const int G = thr_groups((int)q, GPL);
+      if (q <= 1) t = wm;
+      else if (G == 1) t = thr_f32<1>(kk, q);
+      else if (G == 2) t = thr_f32<2>(kk, q);
+      else if (G == 4) t = thr_f32<4>(kk, q);
+      else if (G == 8) t = thr_f32<8>(kk, q);
+      else if (G == 16) t = thr_f32<16>(kk, q);
+      else t = kKeyFloor;
+      t = max(t, kKeyFloor);
+    }
+    uint32_t gmask = 0u;
+    if (t != kNoEmit) {
+#pragma unroll
+      for (int g = 0; g < 16; ++g) gmask |= (max(kk[2 * g], kk[2 * g + 1]) >= t) ? (1u << g) : 0u;
+    }
+    const uint32_t off = wave_excl_small((uint32_t)__popc(gmask), total);
+#pragma unroll
+    for (int g = 0; g < 16; ++g) {
+      if ((gmask >> g) & 1u) {
+        const uint32_t p = off + (uint32_t)__popc(gmask & ((1u << g) - 1u));
+        const uint32_t idx0 = (uint32_t)(lo + ((g >> 1) * 64 + ln) * 4 + (g & 1) * 2);
+        if (p < cap) region[p] = make_uint4(idx0, kk[2 * g], kk[2 * g + 1], 0u);
       }
     }
   }
-#pragma unroll
-  for (int j = 0; j < kPT; ++j) key[j] = kv[j];
-  if (patch && overflow) {
-    const uint32_t pbits = S.bm[tid];
-#pragma unroll
-    for (int j = 0; j < kPT; ++j) {
-      if ((pbits >> j) & 1u) {
-        const int id = lo + local_of_slot<DT>(tid, j);
-        int cntv = 0;
-        if (do_hist) {
-          for (int h = 0; h < c.nhist; ++h) cntv += (c.hist[h] == id);
-          for (int h = 0; h < c.nextra; ++h) cntv += (c.extra[h] == id);
-        }
-        float bsum = 0.0f;
-        bool hb = false;
-        if (do_bias) {
-          for (int e = 0; e < c.nbias; ++e)
-            if (c.bias_ids[e] == id) {
-              bsum = bsum + c.bias_vals[e];
-              hb = true;
-            }
-        }
-        if ((allow >> j) & 1u)
-          key[j] = penalised_key(slot_bits<DT>(raw, j), c.mode, c.rep, c.freq, c.pres, cntv, hb, bsum);
-      }
-    }
-  }
-  if (patch) lds_barrier();  // LDS lists may be rebuilt by the caller's next tile
+  if (ln == 0) a.rec[gu] = make_uint4(t, total, wm, 0u);
 }
 
-// A tile takes the straight-line path when it is complete and 16-byte aligned.
-__device__ __forceinline__ bool tile_full(const KArgs& a, int lo) { return a.vec_ok && a.V - lo >= kTile; }
+// ===========================================================================
+// Merge phase
+// ===========================================================================
+struct MSmem {
+  uint64_t r64[kWaves];
+  double rd[kWaves];
+  uint32_t r32[kWaves];
+  uint32_t bc[8];
+  uint64_t bc64[4];
+  double bcd[4];
+  int32_t closed[kWaves];
+  uint32_t flagsw;  // bit 0: hash overflow
+  int32_t hk[kH];   // patched id (or -1)
+  uint32_t hc[kH];  // occurrence count | has-bias bit 31
+  uint32_t hf[kH];  // final key
+  uint32_t uoff[kMaxU + 1];
+  uint32_t rmask[kMaxU / 32];  // units re-read by the slow path
+  uint32_t hist[2][kHCopies * kHStride];
+  uint32_t low[2][64];
+  uint64_t mhist[256];
+};
+constexpr int kSmemFixed = (int)((sizeof(MSmem) + 15) & ~(size_t)15);
+
+__device__ __forceinline__ uint32_t hslot(int id) { return ((uint32_t)id * 2654435761u) >> 22; }  // 10 bits
+static_assert(kH == 1024, "hslot assumes 1024 slots");
+
+__device__ __forceinline__ int hfind(const MSmem& S, int id) {
+  uint32_t s = hslot(id);
+  for (int p = 0; p < kProbe; ++p) {
+    const int k = S.hk[s];
+    if (k == id) return (int)s;
+    if (k < 0) return -1;
+    s = (s + 1) & (kH - 1);
+  }
+  return -1;
+}
+
 
 // ---------------------------------------------------------------------------
-// Radix selection in the merge.  Histograms are privatised (kHCopies copies,
-// stride kHStride) and double-buffered: the buffer of the next pass is
-// cleared while the current one fills, so one barrier separates passes.
+// Patch table of a row in global memory, used when the row's history and
+// bias lists hold more distinct ids than the LDS table: open addressing over
+// kGH slots tagged with a per-call generation, so stale slots of earlier
+// calls count as empty and the table never needs clearing.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void radix_clear(Smem& S, int buf) {
+struct PatchG {
+  uint64_t* tag;
+  uint32_t* cnt;
+  uint32_t* fin;
+  uint32_t gen;
+};
+__device__ __forceinline__ uint32_t ghslot(int id) { return ((uint32_t)id * 2654435761u) >> 18; }  // 14 bits
+static_assert(kGH == 16384, "ghslot assumes 16384 slots");
+
+__device__ __forceinline__ int gfind(const PatchG& g, int id) {
+  const uint64_t want = ((uint64_t)g.gen << 32) | (uint32_t)(id + 1);
+  uint32_t s = ghslot(id);
+  for (int p = 0; p < kGProbe; ++p) {
+    const uint64_t t = __hip_atomic_load(&g.tag[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (t == want) return (int)s;
+    if ((uint32_t)(t >> 32) != g.gen) return -1;
+    s = (s + 1) & (kGH - 1);
+  }
+  return -1;
+}
+// claims a slot for id (the claiming thread zeroes its count); -1 when full
+__device__ __forceinline__ int gclaim(const PatchG& g, int id) {
+  const uint64_t want = ((uint64_t)g.gen << 32) | (uint32_t)(id + 1);
+  uint32_t s = ghslot(id);
+  for (int p = 0; p < kGProbe; ++p) {
+    uint64_t t = __hip_atomic_load(&g.tag[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (;;) {
+      if (t == want) return (int)s;
+      if ((uint32_t)(t >> 32) == g.gen) break;  // another id of this call
+      const uint64_t old = atomicCAS((unsigned long long*)&g.tag[s], (unsigned long long)t, (unsigned long long)want);
+      if (old == t) {
+        g.cnt[s] = 0u;
+        return (int)s;
+      }
+      t = old;
+    }
+    s = (s + 1) & (kGH - 1);
+  }
+  return -1;
+}
+
+// linear lookups in the row's lists (last resort, any list length)
+__device__ __forceinline__ bool lin_info(const Ctx& c, int id, int* count, bool* hb, float* bsum) {
+  int n = 0;
+  for (int h = 0; h < c.nhist; ++h) n += c.hist[h] == id;
+  for (int h = 0; h < c.nextra; ++h) n += c.extra[h] == id;
+  float bs = 0.0f;
+  bool has = false;
+  for (int e = 0; e < c.nbias; ++e)
+    if (c.bias_ids[e] == id) {
+      bs = bs + c.bias_vals[e];
+      has = true;
+    }
+  *count = n;
+  *hb = has;
+  *bsum = bs;
+  return n > 0 || has;
+}
+// entry e of the concatenated list (history, drafts, bias ids)
+__device__ __forceinline__ int lin_entry(const Ctx& c, int e) {
+  if (e < c.nhist) return c.hist[e];
+  e -= c.nhist;
+  if (e < c.nextra) return c.extra[e];
+  return c.bias_ids[e - c.nextra];
+}
+
+// ---------------------------------------------------------------------------
+// Radix selection (count based).  Histograms are privatised (kHCopies copies)
+// and double-buffered: the buffer of the next pass is cleared while the
+// current one fills, so one barrier separates passes.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void radix_clear(MSmem& S, int buf) {
   for (int i = threadIdx.x; i < kHCopies * kHStride; i += kBlock) S.hist[buf][i] = 0u;
   if (threadIdx.x < 64) S.low[buf][threadIdx.x] = 0u;
 }
@@ -625,9 +671,9 @@ __device__ __forceinline__ void low_mark(uint32_t* low, uint32_t bin, bool pred)
 }
 
 // Digit search by wave 0 over nb <= 256 bins.  Descending: find d with
-// above(d) < want <= above(d) + h[d], above(d) = count in the bins above d;
-// ascending: the same with the bins below d.  Writes (d, count before d, h[d],
-// low flag of d) to bc[0..3]; d = nb if the total is below `want`.
+// above(d) < want <= above(d) + h[d]; ascending: the same with the bins
+// below d.  Writes (d, count before d, h[d], low flag of d) to bc[0..3]; d =
+// nb if the total is below `want`.
 __device__ inline void radix_digit(const uint32_t* h, const uint32_t* low, int nb, uint32_t want, bool descending,
                                    uint32_t* bc) {
   if (threadIdx.x < 64) {
@@ -671,42 +717,25 @@ __device__ inline void radix_digit(const uint32_t* h, const uint32_t* low, int n
   lds_barrier();
 }
 
-// ---------------------------------------------------------------------------
 // Exact selection of the `want` largest composites (key desc, index asc)
 // among the n_valid valid keys a visitor produces.  visit(f) calls f(key, idx)
-// for this thread's elements; every thread calls it the same number of times.
-// Every valid visited key lies in [lo_key, hi_key]: the bits above the
-// highest bit in which the two bounds differ are common to all of them, so
-// the 8-bit digit passes start just below those bits (first_window).  A pass
-// whose chosen bin holds only keys with zero bits below the digit fixes the
-// boundary key at once (bf16 logits leave the low 16 bits zero).  Ties at the
-// boundary key take the lowest indices (indices < V): by direct ranking when
-// there are at most kBlock of them, else by index digit passes.  With
-// first_built the caller has already filled radix buffer 0 with the first
-// key pass; otherwise buffer 0 must be cleared and published.  Returns
-// (tk, ti): an element is selected iff key > tk or (key == tk and idx <= ti).
-// ---------------------------------------------------------------------------
-struct Window {
-  int sh;       // shift of the first digit
-  uint32_t dm;  // digit mask of the first pass
-};
-__device__ __forceinline__ Window first_window(uint32_t lo_key, uint32_t hi_key) {
-  const int sh = 32 - __clz(lo_key ^ hi_key);
-  const int w = sh < 8 ? sh : 8;
-  return Window{sh - w, (1u << w) - 1u};
-}
-
+// for this thread's elements.  Every valid visited key lies in [lo_key,
+// hi_key]: the digit passes start just below the bits the two bounds share.
+// A pass whose chosen bin holds only keys with zero bits below the digit fixes
+// the boundary key at once (bf16 keys leave the low 16 bits zero).  Ties at
+// the boundary key take the lowest indices (indices < V).  Returns (tk, ti):
+// an element is selected iff key > tk or (key == tk and idx <= ti).
 template <typename Visit>
-__device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint32_t n_valid, uint32_t lo_key,
-                                             uint32_t hi_key, int V, bool first_built, Smem& S, uint32_t* tk_out,
-                                             uint32_t* ti_out) {
+__device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint32_t n_valid, uint32_t lo_key, uint32_t hi_key,
+                             int V, MSmem& S, uint32_t* tk_out, uint32_t* ti_out) {
   int cur = 0;
   int sh = 32 - __clz(lo_key ^ hi_key);  // bits [0, sh) vary among the keys
   uint32_t prefix = sh >= 32 ? 0u : (hi_key >> sh);
   uint32_t tk = hi_key, ti = 0xFFFFFFFFu;
   uint32_t n_tie = n_valid;
   bool ties = true;
-  bool skip_visit = first_built;
+  radix_clear(S, 0);
+  lds_barrier();
   if (want >= n_valid) {  // everything valid is selected
     tk = kKeyNegInf;
     ties = false;
@@ -720,15 +749,12 @@ __device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint3
     const uint32_t lm = (1u << sh) - 1u;
     uint32_t* h = S.hist[cur];
     uint32_t* lw = S.low[cur];
-    if (!skip_visit) {
-      visit([&](uint32_t k, uint32_t) {
-        const bool part = k >= kKeyFloor && (hs >= 32 || (k >> hs) == prefix);
-        const uint32_t d = (k >> sh) & dm;
-        hist_add(h, d, part);
-        low_mark(lw, d, part && (k & lm) != 0u);
-      });
-    }
-    skip_visit = false;
+    visit([&](uint32_t k, uint32_t) {
+      const bool part = k >= kKeyFloor && (hs >= 32 || (k >> hs) == prefix);
+      const uint32_t d = (k >> sh) & dm;
+      hist_add(h, d, part);
+      low_mark(lw, d, part && (k & lm) != 0u);
+    });
     radix_clear(S, cur ^ 1);
     lds_barrier();
     radix_digit(h, lw, (int)dm + 1, want, true, S.bc);
@@ -759,7 +785,7 @@ __device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint3
     uint32_t cnt = 0;
     visit([&](uint32_t k, uint32_t) { cnt += k == tk ? 1u : 0u; });
     uint32_t tot;
-    uint32_t off = block_excl_scan(cnt, S.red32, tot);
+    uint32_t off = block_excl_scan(cnt, S.r32, tot);
     uint32_t* tl = S.hist[cur];  // free: cleared for a next pass that does not come
     visit([&](uint32_t k, uint32_t i) {
       if (k == tk) tl[off++] = i;
@@ -773,12 +799,9 @@ __device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint3
     }
     lds_barrier();
     ti = S.bc[4];
+    lds_barrier();
   } else if (ties) {
     // many ties: the `want` lowest indices by index digit passes
-    if (skip_visit) {  // no key pass ran: buffer 0 still holds the caller's histogram
-      radix_clear(S, cur);
-      lds_barrier();
-    }
     int ib = 32 - __clz((uint32_t)(V > 1 ? V - 1 : 1));
     uint32_t ip = 0u;
     while (ib > 0) {
@@ -811,366 +834,702 @@ __device__ __forceinline__ bool selected(uint32_t k, uint32_t i, uint32_t tk, ui
 }
 
 // ---------------------------------------------------------------------------
-// Fallback: exact top-`want` of the whole row by streaming it again through
-// this workgroup.  Fills sel[0..n) (row order) and returns n.  The kernel
-// arguments and row context come through LDS (S.fa, S.fc, written by the
-// caller): the function is kept out of line so that its register pressure
-// does not leak into the fast path, and handing it the by-value kernel
-// argument itself would make every merge copy that argument to scratch.
+// Weighted crossing search over a set held in LDS (T[0..nT), slots tid + 256 m
+// with fixed-point weights Wl[i], membership bit m of `inset`): the first
+// element in canonical order (key descending, index ascending) whose
+// inclusive running mass is >= X (strict: > X).  Radix descent with mass
+// histograms, first on the key digits (bins descending), then, inside the
+// group of equal keys, on the index digits (bins ascending).  Returns the
+// composite key, or 0 when the whole set's mass does not reach X.
+// ---------------------------------------------------------------------------
+// wave 0: first non-empty bin, in scan order, whose running mass crosses X;
+// writes (bin, mass before it, its count) to bc[0], bc64[0], bc[2] and its
+// low-bits flag to bc[3]; bc[0] = ~0 if none
+__device__ __forceinline__ void mass_digit(MSmem& S, int nb, double X, bool strict, bool descending) {
+  if (threadIdx.x < 64) {
+    const int l = lane();
+    uint64_t mb[4];
+    uint32_t cb[4];
+    uint64_t ms = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = 4 * l + q;
+      const int bin = descending ? nb - 1 - r : r;
+      mb[q] = 0;
+      cb[q] = 0;
+      if (r < nb) {
+        mb[q] = S.mhist[bin];
+#pragma unroll
+        for (int cp = 0; cp < kHCopies; ++cp) cb[q] += S.hist[0][cp * kHStride + bin];
+      }
+      ms += mb[q];
+    }
+    const uint64_t inc = wave_incl_scan(ms);
+    uint64_t run = inc - ms;
+    // the condition is monotone over non-empty bins: the lowest lane with a
+    // hit holds the first one
+    int hq = -1;
+    uint64_t hrun = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = 4 * l + q;
+      const uint64_t nr = run + mb[q];
+      const bool hit = r < nb && cb[q] > 0u && (strict ? ((double)nr > X) : ((double)nr >= X));
+      if (hit && hq < 0) {
+        hq = q;
+        hrun = run;
+      }
+      run = nr;
+    }
+    const uint64_t hm = __ballot(hq >= 0);
+    if (hm == 0ull) {
+      if (l == 0) S.bc[0] = 0xFFFFFFFFu;
+    } else if (l == (int)__builtin_ctzll(hm)) {
+      const int bin = descending ? nb - 1 - (4 * l + hq) : 4 * l + hq;
+      S.bc[0] = (uint32_t)bin;
+      S.bc64[0] = hrun;
+      S.bc[2] = cb[hq];
+      S.bc[3] = (S.low[0][bin >> 2] >> (8 * (bin & 3))) & 255u;
+    }
+  }
+  lds_barrier();
+}
+
+__device__ __forceinline__ uint64_t cross_find(MSmem& S, const uint2* T, const uint64_t* Wl, int nT, uint32_t inset, double X,
+                                            bool strict, uint32_t lo_key, uint32_t hi_key, int V) {
+  const int tid = threadIdx.x;
+  const int M = (nT + kBlock - 1) / kBlock;
+  // phase 0: key digits; phase 1: index digits among keys equal to tk
+  int sh = 32 - __clz(lo_key ^ hi_key);
+  uint32_t prefix = sh >= 32 ? 0u : (hi_key >> sh);
+  uint32_t tk = hi_key;
+  int phase = sh > 0 ? 0 : 1;
+  int ib = 32 - __clz((uint32_t)(V > 1 ? V - 1 : 1));
+  uint32_t ip = 0u;
+  uint32_t cnt_last = 0xFFFFFFFFu;
+  if (phase == 1) {
+    // one key value in the whole set: does its mass reach X at all?
+    uint64_t ml = 0;
+    for (int m = 0; m < M; ++m) {
+      const int i = tid + m * kBlock;
+      if (i < nT && ((inset >> m) & 1u)) ml += Wl[i];
+    }
+    const uint64_t mt = block_sum(ml, S.r64);
+    if (!(strict ? (double)mt > X : (double)mt >= X)) return 0ull;
+  }
+  for (;;) {
+    int w, hs, csh;
+    if (phase == 0) {
+      w = sh < 8 ? sh : 8;
+      sh -= w;
+      hs = sh + w;
+      csh = sh;
+    } else {
+      if (ib <= 0 || cnt_last == 1u) break;
+      w = ib < 8 ? ib : 8;
+      ib -= w;
+      hs = ib + w;
+      csh = ib;
+    }
+    const uint32_t dm = (1u << w) - 1u;
+    const uint32_t lm = (1u << csh) - 1u;
+    for (int i = tid; i < 256; i += kBlock) S.mhist[i] = 0ull;
+    for (int i = tid; i < kHCopies * kHStride; i += kBlock) S.hist[0][i] = 0u;
+    if (tid < 64) S.low[0][tid] = 0u;
+    lds_barrier();
+    for (int m = 0; m < M; ++m) {
+      const int i = tid + m * kBlock;
+      if (i < nT && ((inset >> m) & 1u)) {
+        const uint2 e = T[i];
+        bool part;
+        uint32_t d;
+        if (phase == 0) {
+          part = hs >= 32 || (e.x >> hs) == prefix;
+          d = (e.x >> csh) & dm;
+        } else {
+          part = e.x == tk && (hs >= 32 || (e.y >> hs) == ip);
+          d = (e.y >> csh) & dm;
+        }
+        if (part) {
+          atomicAdd(&S.mhist[d], Wl[i]);
+          hist_add(S.hist[0], d, true);
+          low_mark(S.low[0], d, phase == 0 && (e.x & lm) != 0u);
+        }
+      }
+    }
+    lds_barrier();
+    mass_digit(S, (int)dm + 1, X, strict, phase == 0);
+    const uint32_t d = S.bc[0];
+    const uint64_t before = S.bc64[0];
+    const uint32_t cnt = S.bc[2], lowd = S.bc[3];
+    lds_barrier();
+    if (d == 0xFFFFFFFFu) return 0ull;  // the set's mass does not reach X
+    X -= (double)before;
+    cnt_last = cnt;
+    if (phase == 0) {
+      prefix = (prefix << w) | d;
+      if (sh == 0 || lowd == 0u) {  // every key in the bin equals prefix << sh
+        tk = prefix << sh;
+        phase = 1;
+      } else if (cnt == 1u) {  // a single element: resolved below
+        tk = 0u;
+        break;
+      }
+    } else {
+      ip = (ip << w) | d;
+    }
+  }
+  // the element: the only one matching the resolved prefixes
+  for (int m = 0; m < M; ++m) {
+    const int i = tid + m * kBlock;
+    if (i < nT && ((inset >> m) & 1u)) {
+      const uint2 e = T[i];
+      bool match;
+      if (phase == 0) match = (e.x >> sh) == prefix;
+      else match = e.x == tk && (ib >= 32 || (e.y >> ib) == ip);
+      if (match) {
+        S.bc[5] = e.x;
+        S.bc[6] = e.y;
+      }
+    }
+  }
+  lds_barrier();
+  const uint64_t r = comp_of(S.bc[5], S.bc[6]);
+  lds_barrier();
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// Candidate visitor.  Visits the row's candidate elements from global memory:
+// the groups of every unit not marked for re-reading (unit offsets in
+// S.uoff, flattened over 256 threads, located by binary search), every
+// element of the marked units (re-read from the logits with the grammar mask
+// applied), and the patched final values.  Raw copies of patched ids are
+// skipped.  f(key, idx) receives only valid keys.
 // ---------------------------------------------------------------------------
 template <int DT>
-__device__ __attribute__((noinline)) int fallback_select(int want) {
-  extern __shared__ __align__(16) unsigned char smem_raw[];
-  Smem& S = *reinterpret_cast<Smem*>(smem_raw);
-  uint64_t* sel = reinterpret_cast<uint64_t*>(smem_raw + kSelOff);
-  const KArgs& a = S.fa;
-  const Ctx& c = S.fc;
-  const int tid = threadIdx.x;
-  const int T = a.T;
-  uint32_t nv_local = 0;
-  for (int j = 0; j < T; ++j) {
-    uint32_t key[kPT];
-    if (tile_full(a, j * kTile))
-      load_tile<DT, true>(a, c, j * kTile, S, key);
-    else
-      load_tile<DT, false>(a, c, j * kTile, S, key);
-#pragma unroll
-    for (int s = 0; s < kPT; ++s) nv_local += fold_nan(key[s]) >= kKeyFloor;
+__device__ __forceinline__ int unit_of_group(const MSmem& S, int U, uint32_t f) {
+  int lo = 0, hi = U - 1;  // largest u with uoff[u] <= f
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (S.uoff[mid] <= f) lo = mid;
+    else hi = mid - 1;
   }
-  const int nv = (int)block_sum(nv_local, S.red32);
-  if (want > nv) want = nv;
-  if (want <= 0) return 0;
-  auto visit_row = [&](auto&& f) {
-    for (int j = 0; j < T; ++j) {
-      uint32_t key[kPT];
-      const int lo = j * kTile;
-      if (tile_full(a, lo))
-        load_tile<DT, true>(a, c, lo, S, key);
-      else
-        load_tile<DT, false>(a, c, lo, S, key);
+  return lo;
+}
+
+// final key of a patched id found by a linear lookup in the row's lists
+template <int DT>
+__device__ __forceinline__ uint32_t lin_final(const KArgs& a, const Ctx& c, int id) {
+  int cn;
+  bool hb;
+  float bs;
+  lin_info(c, id, &cn, &hb, &bs);
+  const int Wm = (a.V + 31) >> 5;
+  const bool allowed = !c.mask || ((((id >> 5) < Wm ? c.mask[id >> 5] : 0u) >> (id & 31)) & 1u);
+  if (!allowed) return 0u;
+  return fold_nan(penalised_key(load_elem_bits<DT>(c.xrow, id), c.mode, c.rep, c.freq, c.pres, cn, hb, bs));
+}
+
+// patch modes: 0 none, 1 LDS table, 2 global table, 3 linear lookups
+template <int DT>
+__device__ __forceinline__ bool is_patched(const Ctx& c, const MSmem& S, int pmode, const PatchG& g, int id) {
+  if (pmode == 0) return false;
+  if (pmode == 1) return hfind(S, id) >= 0;
+  if (pmode == 2) return gfind(g, id) >= 0;
+  int cn;
+  bool hb;
+  float bs;
+  return lin_info(c, id, &cn, &hb, &bs);
+}
+
+template <int DT, typename F>
+__device__ __forceinline__ void visit_candidates(const KArgs& a, const Ctx& c, const MSmem& S, uint32_t NG, int nre,
+                                                 int pmode, const PatchG& pg, F&& f) {
+  constexpr int GE = DTT<DT>::GE, VW = DTT<DT>::VW;
+  const int tid = threadIdx.x;
+  const int U = a.U;
+  const uint4* rc = a.cand + (size_t)c.row * U * a.cap;
+  // 1. groups of the units that are not re-read
+  for (uint32_t f0 = 0; f0 < NG; f0 += kBlock * kGB) {
+    uint4 g[kGB];
+    bool ok[kGB];
 #pragma unroll
-      for (int s = 0; s < kPT; ++s) f(fold_nan(key[s]), (uint32_t)(lo + local_of_slot<DT>(tid, s)));
+    for (int m = 0; m < kGB; ++m) {
+      const uint32_t fi = f0 + (uint32_t)(tid + m * kBlock);
+      ok[m] = false;
+      g[m] = make_uint4(0u, 0u, 0u, 0u);
+      if (fi < NG) {
+        const int u = unit_of_group<DT>(S, U, fi);
+        if (!((S.rmask[u >> 5] >> (u & 31)) & 1u)) {
+          ok[m] = true;
+          g[m] = rc[(size_t)u * a.cap + (fi - S.uoff[u])];
+        }
+      }
     }
-  };
-  radix_clear(S, 0);
-  lds_barrier();
-  uint32_t tk, ti;
-  radix_select(visit_row, (uint32_t)want, (uint32_t)nv, kKeyFloor, 0xFFFFFFFFu, a.V, false, S, &tk, &ti);
-  uint32_t base = 0;
-  for (int j = 0; j < T; ++j) {
-    uint32_t key[kPT];
-    const int lo = j * kTile;
-    if (tile_full(a, lo))
-      load_tile<DT, true>(a, c, lo, S, key);
-    else
-      load_tile<DT, false>(a, c, lo, S, key);
 #pragma unroll
-    for (int s = 0; s < kPT; ++s) key[s] = fold_nan(key[s]);
-    uint32_t cntl = 0;
+    for (int m = 0; m < kGB; ++m) {
+      if (!ok[m]) continue;
 #pragma unroll
-    for (int s = 0; s < kPT; ++s) cntl += selected(key[s], lo + local_of_slot<DT>(tid, s), tk, ti);
+      for (int e = 0; e < GE; ++e) {
+        uint32_t k;
+        if constexpr (DT == SS_BF16) k = (((e < 2 ? g[m].y : g[m].z) >> (16 * (e & 1))) & 0xFFFFu) << 16;
+        else k = e ? g[m].z : g[m].y;
+        const uint32_t i = g[m].x + (uint32_t)e;
+        if (k >= kKeyFloor && !is_patched<DT>(c, S, pmode, pg, (int)i)) f(k, i);
+      }
+    }
+  }
+  // 2. every element of the re-read units
+  if (nre > 0) {
+    const int W = (a.V + 31) >> 5;
+    for (int u = 0; u < U; ++u) {
+      if (!((S.rmask[u >> 5] >> (u & 31)) & 1u)) continue;
+      const int lo = u * kUE;
+      for (int l0 = tid * VW; l0 < kUE; l0 += kBlock * VW) {
+        uint32_t mwd = 0xFFFFFFFFu;
+        if (c.mask) {
+          const int wi = (lo + l0) >> 5;
+          mwd = wi < W ? (c.mask[wi] >> ((lo + l0) & 31)) : 0u;
+        }
+        for (int e = 0; e < VW; ++e) {
+          const int i = lo + l0 + e;
+          if (i >= a.V) break;
+          uint32_t k = fold_nan(key_raw(load_elem_bits<DT>(c.xrow, i)));
+          if (!((mwd >> e) & 1u)) k = 0u;
+          if (k >= kKeyFloor && !is_patched<DT>(c, S, pmode, pg, i)) f(k, (uint32_t)i);
+        }
+      }
+    }
+  }
+  // 3. patched final values
+  if (pmode == 1) {
+    for (int s = tid; s < kH; s += kBlock) {
+      const int id = S.hk[s];
+      if (id >= 0 && S.hf[s] >= kKeyFloor) f(S.hf[s], (uint32_t)id);
+    }
+  } else if (pmode == 2) {
+    for (int s = tid; s < kGH; s += kBlock) {
+      const uint64_t t = pg.tag[s];
+      if ((uint32_t)(t >> 32) == pg.gen && pg.fin[s] >= kKeyFloor) f(pg.fin[s], (uint32_t)t - 1u);
+    }
+  } else if (pmode == 3) {
+    const int ne = c.nhist + c.nextra + c.nbias;
+    for (int e = tid; e < ne; e += kBlock) {
+      const int id = lin_entry(c, e);
+      if (id < 0 || id >= a.V) continue;
+      bool first = true;
+      for (int e2 = 0; e2 < e && first; ++e2) first = lin_entry(c, e2) != id;
+      if (!first) continue;
+      const uint32_t k = lin_final<DT>(a, c, id);
+      if (k >= kKeyFloor) f(k, (uint32_t)id);
+    }
+  }
+}
+
+
+// Fast-path pool: every candidate element at or above tmax (raw copies of
+// patched ids dropped) plus the patched final values at or above it, in a
+// deterministic order (batches of kGB groups per thread, block-scan offsets).
+// Returns the element count (elements beyond a.pcap are counted, not stored).
+template <int DT>
+__device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MSmem& S, uint32_t NG, bool patch, uint32_t tmax,
+                                uint2* pool, uint32_t& pmax_out) {
+  constexpr int GE = DTT<DT>::GE;
+  const int tid = threadIdx.x;
+  const int U = a.U;
+  const uint4* rc = a.cand + (size_t)c.row * U * a.cap;
+  const uint32_t pcap = (uint32_t)a.pcap;
+  uint32_t base = 0u, pmax = 0u;
+  for (uint32_t f0 = 0; f0 < NG; f0 += kBlock * kGB) {
+    uint4 g[kGB];
+#pragma unroll
+    for (int m = 0; m < kGB; ++m) {
+      const uint32_t fi = f0 + (uint32_t)(tid + m * kBlock);
+      g[m] = make_uint4(0u, 0u, 0u, 0u);
+      if (fi < NG) {
+        const int u = unit_of_group<DT>(S, U, fi);
+        g[m] = rc[(size_t)u * a.cap + (fi - S.uoff[u])];
+      }
+    }
+    uint32_t keep = 0u, cnt = 0u;
+#pragma unroll
+    for (int m = 0; m < kGB; ++m) {
+#pragma unroll
+      for (int e = 0; e < GE; ++e) {
+        uint32_t k;
+        if constexpr (DT == SS_BF16) k = (((e < 2 ? g[m].y : g[m].z) >> (16 * (e & 1))) & 0xFFFFu) << 16;
+        else k = e ? g[m].z : g[m].y;
+        const uint32_t i = g[m].x + (uint32_t)e;
+        if (k >= tmax && k >= kKeyFloor && !(patch && hfind(S, (int)i) >= 0)) {
+          keep |= 1u << (m * GE + e);
+          ++cnt;
+          pmax = max(pmax, k);
+        }
+      }
+    }
     uint32_t tot;
-    uint32_t off = base + block_excl_scan(cntl, S.red32, tot);
+    uint32_t off = base + block_excl_scan(cnt, S.r32, tot);
 #pragma unroll
-    for (int s = 0; s < kPT; ++s) {
-      const uint32_t i = lo + local_of_slot<DT>(tid, s);
-      if (selected(key[s], i, tk, ti)) sel[off++] = comp_of(key[s], i);
+    for (int m = 0; m < kGB; ++m) {
+#pragma unroll
+      for (int e = 0; e < GE; ++e) {
+        if ((keep >> (m * GE + e)) & 1u) {
+          uint32_t k;
+          if constexpr (DT == SS_BF16) k = (((e < 2 ? g[m].y : g[m].z) >> (16 * (e & 1))) & 0xFFFFu) << 16;
+          else k = e ? g[m].z : g[m].y;
+          if (off < pcap) pool[off] = make_uint2(k, g[m].x + (uint32_t)e);
+          ++off;
+        }
+      }
     }
     base += tot;
   }
-  return (int)base;
+  if (patch) {
+    uint32_t cnt = 0u;
+    for (int s = tid; s < kH; s += kBlock) {
+      const uint32_t k = S.hf[s];
+      if (S.hk[s] >= 0 && k >= tmax && k >= kKeyFloor) {
+        ++cnt;
+        pmax = max(pmax, k);
+      }
+    }
+    uint32_t tot;
+    uint32_t off = base + block_excl_scan(cnt, S.r32, tot);
+    for (int s = tid; s < kH; s += kBlock) {
+      const uint32_t k = S.hf[s];
+      if (S.hk[s] >= 0 && k >= tmax && k >= kKeyFloor) {
+        if (off < pcap) pool[off] = make_uint2(k, (uint32_t)S.hk[s]);
+        ++off;
+      }
+    }
+    base += tot;
+  }
+  pmax_out = block_max(pmax, S.r32);  // its barriers publish the pool
+  return base;
 }
 
-// sort sel[0..n) descending (canonical order), padding to a power of two
-__device__ __forceinline__ void sort_selected(uint64_t* sel, int n) {
-  const int N = next_pow2(n);
-  for (int r = n + (int)threadIdx.x; r < N; r += kBlock) sel[r] = 0ull;
-  lds_barrier();
-  lds_sort_desc(sel, N);
-}
 
-// ---------------------------------------------------------------------------
-// Epilogue on the exact top-k set sel[0..n_sel): min-p filter, sort of the
-// survivors, prefix sums, top-p cut (Alg. 11 order).  Leaves the sorted kept
-// prefix in sel; each thread keeps the weights / inclusive sums of its chunk.
-// Z_k is summed in 2^-50 fixed point so that it does not depend on the order
-// in which candidates arrived.
-// ---------------------------------------------------------------------------
-struct Dist {
-  int n_s;
-  double Z_s;
-  double M, tau;
-  int chunk0, chunk_n;  // this thread's rows [chunk0, chunk0 + chunk_n) of sel
-  double w[kEPT];       // weights of the chunk
-  double incl[kEPT];    // inclusive prefix sums
-};
-
-__device__ __forceinline__ void build_dist(const KArgs& a, const Ctx& c, uint64_t Mcomp, int n_sel, Smem& S,
-                                           uint64_t* sel, Dist& D) {
+// In-place stable compaction of pool[0, n) to the elements satisfying
+// pred, in rounds of 4 * kBlock: a round writes only below its own first
+// unread index, so no element is overwritten before it is read.
+template <typename Pred>
+__device__ __forceinline__ uint32_t compact_pool(MSmem& S, uint2* pool, int n, Pred&& pred) {
   const int tid = threadIdx.x;
-  const int b = c.req;
-  const double M = (double)float_of_key(comp_key(Mcomp));
-  const double tau = (c.mode & SS_TEMP) ? (double)a.temperature[b] : 1.0;
-  D.M = M;
-  D.tau = tau;
-  const bool minp = (c.mode & SS_MINP) && a.min_p[b] > 0.0f;
-  const bool topp = (c.mode & SS_TOPP) && a.top_p[b] < 1.0f;
-  const double lt = minp ? log((double)a.min_p[b]) : 0.0;
-
-  uint64_t e[kEPT];
-  uint64_t zl = 0;
-  uint32_t nm_local = 0;
-  uint32_t keep = 0;
+  uint32_t base = 0u;
+  for (int r0 = 0; r0 < n; r0 += 4 * kBlock) {
+    uint2 e[4];
+    uint32_t sel = 0u, cnt = 0u;
 #pragma unroll
-  for (int m = 0; m < kEPT; ++m) {
-    const int r = tid + m * kBlock;
-    e[m] = 0;
-    if (r < n_sel) {
-      e[m] = sel[r];
-      const double y = (double)float_of_key(comp_key(e[m]));
-      if (topp) zl += (uint64_t)__double2ll_rn(weight_of(y, M, tau) * kFix);
-      bool kp = true;
-      if (minp && e[m] != Mcomp) {
-        const double l = (y == M) ? 0.0 : (y - M) / tau;
-        kp = l >= lt;
-      }
-      if (kp) {
-        keep |= 1u << m;
-        ++nm_local;
+    for (int m = 0; m < 4; ++m) {
+      const int i = r0 + tid * 4 + m;
+      e[m] = i < n ? pool[i] : make_uint2(0u, 0u);
+      if (i < n && pred(e[m])) {
+        sel |= 1u << m;
+        ++cnt;
       }
     }
-  }
-  const double Zk = topp ? (double)block_sum(zl, S.red64) / kFix : 0.0;
-  uint32_t n_m;
-  uint32_t off = block_excl_scan(nm_local, S.red32, n_m);  // ends with a barrier: sel reads done
+    uint32_t tot;
+    uint32_t off = base + block_excl_scan(cnt, S.r32, tot);  // its barriers end this round's reads
 #pragma unroll
-  for (int m = 0; m < kEPT; ++m)
-    if ((keep >> m) & 1u) sel[off++] = e[m];
-  const int N = next_pow2((int)n_m);
-  for (int r = (int)n_m + tid; r < N; r += kBlock) sel[r] = 0ull;
-  lds_barrier();
-  lds_sort_desc(sel, N);
-
-  // prefix sums over the sorted min-p prefix, chunked per thread
-  const int cs = ((int)n_m + kBlock - 1) / kBlock;
-  D.chunk0 = tid * cs;
-  D.chunk_n = max(0, min(cs, (int)n_m - D.chunk0));
-  double loc = 0.0;
-  double excl_loc[kEPT];
-#pragma unroll
-  for (int m = 0; m < kEPT; ++m) {
-    D.w[m] = 0.0;
-    excl_loc[m] = 0.0;
-    if (m < D.chunk_n) {
-      const double y = (double)float_of_key(comp_key(sel[D.chunk0 + m]));
-      D.w[m] = weight_of(y, M, tau);
-      excl_loc[m] = loc;
-      loc += D.w[m];
-      D.incl[m] = loc;
-    }
+    for (int m = 0; m < 4; ++m)
+      if ((sel >> m) & 1u) pool[off++] = e[m];
+    base += tot;
+    lds_barrier();
   }
-  double tot;
-  const double base = block_excl_scan(loc, S.redd, tot);
-  uint32_t np_local = 0;
-  const double thr = topp ? (double)a.top_p[b] * Zk : 0.0;
-#pragma unroll
-  for (int m = 0; m < kEPT; ++m) {
-    if (m < D.chunk_n) {
-      D.incl[m] += base;
-      if (topp && base + excl_loc[m] < thr) ++np_local;
-    }
-  }
-  int n_s = (int)n_m;
-  if (topp) {
-    int np = (int)block_sum(np_local, S.red32);
-    if (np < 1) np = 1;
-    if (np < n_s) n_s = np;
-  }
-  D.n_s = n_s;
-  // Z_S = inclusive prefix at rank n_s - 1
-  const int last = n_s - 1;
-  if (last >= D.chunk0 && last < D.chunk0 + D.chunk_n) {
-#pragma unroll
-    for (int m = 0; m < kEPT; ++m)
-      if (D.chunk0 + m == last) S.bcd[0] = D.incl[m];
-  }
-  lds_barrier();
-  D.Z_s = S.bcd[0];
-  lds_barrier();
+  return base;
 }
 
-// inverse CDF over the kept prefix: first rank with inclusive sum > u * Z_S
-__device__ __forceinline__ int draw_rank(const Dist& D, double u, Smem& S) {
-  const double target = u * D.Z_s;
-  uint32_t r = 0xFFFFFFFFu;
-#pragma unroll
-  for (int m = 0; m < kEPT; ++m) {
-    const int rr = D.chunk0 + m;
-    if (m < D.chunk_n && rr < D.n_s && D.incl[m] > target && (uint32_t)rr < r) r = (uint32_t)rr;
-  }
-  r = block_min(r, S.red32);
-  return r == 0xFFFFFFFFu ? D.n_s - 1 : (int)r;
-}
-
-// weight of sorted rank r (broadcast through LDS)
-__device__ __forceinline__ double rank_weight(const Dist& D, int r, Smem& S) {
-  if (r >= D.chunk0 && r < D.chunk0 + D.chunk_n) {
-#pragma unroll
-    for (int m = 0; m < kEPT; ++m)
-      if (D.chunk0 + m == r) S.bcd[1] = D.w[m];
-  }
-  lds_barrier();
-  const double w = S.bcd[1];
-  lds_barrier();
-  return w;
-}
 
 // ---------------------------------------------------------------------------
-// Exact top-`want` set of a row from its unit candidates (fast path) or by
-// streaming the row again (fallback).  Writes sel[0..n) unordered.
+// Exact slow path of the merge (candidate overflow, patch-table overflow,
+// skewed or heavily tied rows, patched top tokens): v0 = the want-th largest
+// element among those the units emitted; every unit whose threshold lies
+// above v0 (or whose candidate list overflowed) may hide a top-k element and
+// is re-read whole; the exact top-k of the result is written to pool[0, n).
+// Kept out of line: it is rare, and one copy per element type serves every
+// operation.
 // ---------------------------------------------------------------------------
 template <int DT>
-__device__ __forceinline__ int select_exact(const KArgs& a, const Ctx& c, Smem& S, uint64_t* sel, int want,
-                                            uint32_t tmax, uint32_t hi_key, uint32_t ovf, uint32_t n_total,
-                                            int* flags) {
-  extern __shared__ __align__(16) unsigned char smem_raw[];
-  uint2* cnd = reinterpret_cast<uint2*>(smem_raw + kSmemFixed);  // kRPT * kBlock staging slots
+__device__ __noinline__ int slow_select(const KArgs& a, const Ctx& c, MSmem& S, uint2* pool, uint32_t NG, int pmode,
+                                        const PatchG& pg, int want, uint32_t* tk_out, uint32_t* ti_out) {
   const int tid = threadIdx.x;
-  const int U = a.T * kUnits;
-  const uint32_t cap = (uint32_t)a.cap;
-  bool fast = ovf == 0u && n_total <= (uint32_t)(kRPT * kBlock);
-  // every kept candidate lies in [tmax, hi_key]: the first radix pass is
-  // taken while the candidates arrive
-  const Window fw = first_window(tmax, hi_key);
-  uint32_t cl = 0, keepm = 0;
-  uint2 e[kRPT];
-  if (fast) {
-    // 1. table: slot f of the row's unit-major candidate sequence -> offset
-    //    of that candidate in the row's region (kept in cnd[f].x); each
-    //    wavefront fills the slots of a range of units
-    {
-      const int G = U >= kBlock ? 1 : kBlock / U;  // threads per unit
-      for (int u = tid / G; u < U; u += kBlock / G) {
-        const uint32_t p = S.prefix[u];
-        const uint32_t n = S.prefix[u + 1] - p;
-        for (uint32_t j = (uint32_t)(tid % G); j < n; j += (uint32_t)G) cnd[p + j].x = (uint32_t)u * cap + j;
-      }
-      // the first radix pass below records no low-bit flags: mark every bin
-      if (tid < 64) S.low[0][tid] = 0x01010101u;
-    }
-    lds_barrier();
-    // 2. gather: every load in flight at once; slots past n_total load the
-    //    region's first entry and are dropped
-    const uint2* rc = a.cand + (size_t)c.row * U * cap;
-    uint32_t gi[kRPT];
-#pragma unroll
-    for (int m = 0; m < kRPT; ++m) {
-      const uint32_t f = (uint32_t)(tid + m * kBlock);
-      gi[m] = f < n_total ? cnd[f].x : 0u;
-    }
-#pragma unroll
-    for (int m = 0; m < kRPT; ++m) e[m] = rc[gi[m]];
-    // 3. keep flags, count, first radix pass
-    uint32_t* h = S.hist[0];
-#pragma unroll
-    for (int m = 0; m < kRPT; ++m) {
-      const bool keep = (uint32_t)(tid + m * kBlock) < n_total && e[m].x >= tmax;
-      keepm |= keep ? (1u << m) : 0u;
-      cl += keep ? 1u : 0u;
-      hist_add(h, (e[m].x >> fw.sh) & fw.dm, keep);
-    }
+  const int U = a.U;
+  const int row = c.row;
+  uint32_t tk = 0u, ti = 0u;
+  int nT = 0;
+  uint32_t nv = 0u;
+  visit_candidates<DT>(a, c, S, NG, 0, pmode, pg, [&](uint32_t, uint32_t) { ++nv; });
+  nv = block_sum(nv, S.r32);
+  uint32_t v0 = kKeyFloor;
+  if (nv >= (uint32_t)want) {
+    uint32_t t0, i0;
+    radix_select([&](auto&& f) { visit_candidates<DT>(a, c, S, NG, 0, pmode, pg, f); }, (uint32_t)want, nv,
+                 kKeyFloor, 0xFFFFFFFFu, a.V, S, &t0, &i0);
+    v0 = t0;
   }
-  // 4. compaction of the kept candidates to cnd[0, C): the scan's barriers
-  //    also order every table read above before the writes below
-  uint32_t C = 0;
-  const uint32_t off0 = block_excl_scan(cl, S.red32, C);
-  if (fast) {
-    uint32_t off = off0;
-#pragma unroll
-    for (int m = 0; m < kRPT; ++m)
-      if ((keepm >> m) & 1u) cnd[off++] = e[m];
-    if (tmax == kKeyFloor) {  // every unit emitted all of its valid elements
-      if ((int)C < want) want = (int)C;
-    } else if ((int)C < want) {
-      fast = false;  // candidates do not provably contain the top-k
-    }
+  int nre = 0;
+  for (int u = tid; u < U; u += kBlock) {
+    const uint32_t tu = a.rec[(size_t)row * U + u].x;
+    if (tu != kNoEmit && tu > v0) atomicOr(&S.rmask[u >> 5], 1u << (u & 31));
   }
-  if (!fast) {
-    *flags |= SS_FLAG_FALLBACK;
-    if (tid == 0) S.fc = c;  // S.fa was written at kernel entry
-    lds_barrier();
-    return fallback_select<DT>(want);
-  }
-  // rows of kBlock compacted slots, padded with invalid entries to a multiple of 4
-  const int nrow = (((int)C + kBlock - 1) / kBlock + 3) & ~3;
-  for (int i = (int)C + tid; i < nrow * kBlock; i += kBlock) cnd[i] = make_uint2(0u, 0u);
   lds_barrier();
-  if (want <= 0) return 0;
-  auto visit_cnd = [&](auto&& f) {
-    for (int r0 = 0; r0 < nrow; r0 += 4) {
-      uint2 v[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = cnd[tid + (r0 + i) * kBlock];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) f(v[i].x, v[i].y);
-    }
-  };
-  uint32_t tk, ti;
-  radix_select(visit_cnd, (uint32_t)want, C, tmax, hi_key, a.V, true, S, &tk, &ti);
-  uint32_t cntl = 0;
-  visit_cnd([&](uint32_t k, uint32_t i) { cntl += selected(k, i, tk, ti) ? 1u : 0u; });
-  uint32_t tot;
-  uint32_t off = block_excl_scan(cntl, S.red32, tot);
-  visit_cnd([&](uint32_t k, uint32_t i) {
-    if (selected(k, i, tk, ti)) sel[off++] = comp_of(k, i);
-  });
-  return (int)tot;
+  for (int w = 0; w < kMaxU / 32; ++w) nre += __popc(S.rmask[w]);
+  // a unit that overflowed has only part of its groups: re-read it whole
+  uint32_t nx = 0u;
+  visit_candidates<DT>(a, c, S, NG, nre, pmode, pg, [&](uint32_t, uint32_t) { ++nx; });
+  nx = block_sum(nx, S.r32);
+  if (want > (int)nx) want = (int)nx;
+  if (want > 0) {
+    radix_select([&](auto&& f) { visit_candidates<DT>(a, c, S, NG, nre, pmode, pg, f); }, (uint32_t)want, nx,
+                 kKeyFloor, 0xFFFFFFFFu, a.V, S, &tk, &ti);
+    uint32_t cl = 0u;
+    visit_candidates<DT>(a, c, S, NG, nre, pmode, pg, [&](uint32_t k, uint32_t i) { cl += selected(k, i, tk, ti); });
+    uint32_t tot;
+    uint32_t off = block_excl_scan(cl, S.r32, tot);
+    visit_candidates<DT>(a, c, S, NG, nre, pmode, pg, [&](uint32_t k, uint32_t i) {
+      if (selected(k, i, tk, ti)) pool[off++] = make_uint2(k, i);
+    });
+    nT = (int)tot;
+  }
+  *tk_out = tk;
+  *ti_out = ti;
+  return nT;
 }
 
 // ---------------------------------------------------------------------------
-// Row merge: one workgroup per row.
+// Row merge: the whole workgroup, after the row's last unit was written.
 // ---------------------------------------------------------------------------
 template <int DT, int OP>
-__device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S, uint64_t* sel) {
+__device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uint2* pool) {
+  constexpr int GE = DTT<DT>::GE;
   const int tid = threadIdx.x;
-  const int row = c.row, b = c.req;
-  // unit records (two consecutive units per thread)
-  const int U = a.T * kUnits;
-  uint64_t tcomp = 0ull;
-  uint32_t tthr = 0u, tovf = 0u, nl[2] = {0u, 0u};
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int u = 2 * tid + h;
+  const Ctx c = make_ctx<DT>(a, row);
+  const int b = c.req;
+  const int U = a.U;
+  const uint32_t cap = (uint32_t)a.cap;
+
+  // 1. unit records: largest threshold, row maximum, candidate offsets
+  uint32_t hi = 0u, tmax = 0u, ovf = 0u;
+  uint32_t NG = 0u;
+  for (int h = 0; h * kBlock < U; ++h) {
+    const int u = tid + h * kBlock;
+    uint32_t cnt = 0u;
     if (u < U) {
       const uint4 r4 = a.rec[(size_t)row * U + u];
-      if (r4.x >= kKeyFloor) tcomp = max(tcomp, comp_of(r4.x, r4.y));
-      tthr = max(tthr, r4.z);
-      tovf |= r4.w > (uint32_t)a.cap ? 1u : 0u;
-      nl[h] = min(r4.w, (uint32_t)a.cap);
+      hi = max(hi, r4.z);
+      if (r4.x != kNoEmit) tmax = max(tmax, r4.x);
+      if (r4.y > cap) {  // partial candidate list: the unit is re-read by the slow path
+        ovf = 1u;
+        atomicOr(&S.rmask[u >> 5], 1u << (u & 31));
+      }
+      cnt = min(r4.y, cap);
     }
+    uint32_t tot;
+    const uint32_t off = block_excl_scan(cnt, S.r32, tot);
+    if (u < U) S.uoff[u] = NG + off;
+    NG += tot;
   }
-  const uint64_t Mcomp = block_max(tcomp, S.red64);
-  const uint32_t tmax = block_max(tthr, S.red32);
-  const uint32_t ovf = block_max(tovf, S.red32);
-  uint32_t n_total;
-  const uint32_t pre = block_excl_scan(nl[0] + nl[1], S.red32, n_total);
-  if (2 * tid < U) S.prefix[2 * tid] = pre;
-  if (2 * tid + 1 < U) S.prefix[2 * tid + 1] = pre + nl[0];
-  if (tid == 0) S.prefix[U] = n_total;
-  radix_clear(S, 0);
-  lds_barrier();
+  if (tid == 0) S.uoff[U] = NG;
+  if (tid == 0) S.flagsw = 0u;
+  hi = block_max(hi, S.r32);
+  tmax = block_max(tmax, S.r32);
+  ovf = block_max(ovf, S.r32);
 
   int flags = c.kcap ? SS_FLAG_KCAP : 0;
-  const bool empty = Mcomp == 0ull;
-  const int argmax = empty ? -1 : (int)comp_idx(Mcomp);
+  const bool empty = hi < kKeyFloor;
+  int want = c.k_eff;
+
+  // 2. patched ids: counts, ordered bias sums, final keys
+  const bool patch = !empty && want > 0 && (c.nhist + c.nextra + c.nbias) > 0;
+  int pmode = 0;
+  PatchG pg;
+  pg.tag = a.gtag + (size_t)row * kGH;
+  pg.cnt = a.gcnt + (size_t)row * kGH;
+  pg.fin = a.gfin + (size_t)row * kGH;
+  pg.gen = 0u;
+  const int Wm = (a.V + 31) >> 5;
+  if (patch) {
+    for (int s = tid; s < kH; s += kBlock) {
+      S.hk[s] = -1;
+      S.hc[s] = 0u;
+    }
+    lds_barrier();
+    auto ins = [&](int id, uint32_t addc, uint32_t orb) {
+      if (id < 0 || id >= a.V) return;
+      uint32_t s = hslot(id);
+      for (int p = 0; p < kProbe; ++p) {
+        const int old = atomicCAS(&S.hk[s], -1, id);
+        if (old == -1 || old == id) {
+          if (addc) atomicAdd(&S.hc[s], addc);
+          if (orb) atomicOr(&S.hc[s], orb);
+          return;
+        }
+        s = (s + 1) & (kH - 1);
+      }
+      S.flagsw = 1u;
+    };
+    for (int h0 = 0; h0 < c.nhist; h0 += 4 * kBlock) {
+      int id[4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const int h = h0 + tid + m * kBlock;
+        id[m] = h < c.nhist ? c.hist[h] : -1;
+      }
+#pragma unroll
+      for (int m = 0; m < 4; ++m) ins(id[m], 1u, 0u);
+    }
+    for (int h = tid; h < c.nextra; h += kBlock) ins(c.extra[h], 1u, 0u);
+    for (int e = tid; e < c.nbias; e += kBlock) ins(c.bias_ids[e], 0u, 0x80000000u);
+    __syncthreads();
+    if (S.flagsw == 0u) {
+      pmode = 1;
+#pragma unroll 1
+      for (int s0 = 0; s0 < kH; s0 += 4 * kBlock) {
+        int id[4];
+        uint32_t bits[4], mw[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          id[m] = S.hk[s0 + tid + m * kBlock];
+          bits[m] = 0u;
+          mw[m] = 0xFFFFFFFFu;
+          if (id[m] >= 0) {
+            bits[m] = load_elem_bits<DT>(c.xrow, id[m]);
+            if (c.mask) mw[m] = (id[m] >> 5) < Wm ? c.mask[id[m] >> 5] : 0u;
+          }
+        }
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const int s = s0 + tid + m * kBlock;
+          if (id[m] < 0) continue;
+          const uint32_t hcv = S.hc[s];
+          const bool hb = (hcv >> 31) != 0u;
+          float bsum = 0.0f;
+          if (hb) {
+            for (int e = 0; e < c.nbias; ++e)
+              if (c.bias_ids[e] == id[m]) bsum = bsum + c.bias_vals[e];
+          }
+          uint32_t k = 0u;
+          if ((mw[m] >> (id[m] & 31)) & 1u)
+            k = fold_nan(penalised_key(bits[m], c.mode, c.rep, c.freq, c.pres, (int)(hcv & 0x7FFFFFFFu), hb, bsum));
+          S.hf[s] = k;
+        }
+      }
+      lds_barrier();
+    } else {
+      // more distinct ids than the LDS table holds: the row's table in global memory
+      if (tid == 0) {
+        uint32_t gnew = a.ggen[row] + 1u;
+        if (gnew == 0u) gnew = 1u;
+        a.ggen[row] = gnew;
+        S.bc[7] = gnew;
+      }
+      lds_barrier();
+      pg.gen = S.bc[7];
+      lds_barrier();
+      const int ne = c.nhist + c.nextra + c.nbias;
+      bool full = false;
+      for (int e = tid; e < ne; e += kBlock) {
+        const int id = lin_entry(c, e);
+        if (id >= 0 && id < a.V && gclaim(pg, id) < 0) full = true;
+      }
+      if (full) S.flagsw = 3u;
+      __threadfence();
+      __syncthreads();
+      if (S.flagsw == 3u) {
+        pmode = 3;
+      } else {
+        pmode = 2;
+        for (int e = tid; e < ne; e += kBlock) {
+          const int id = lin_entry(c, e);
+          if (id < 0 || id >= a.V) continue;
+          const int sl = gfind(pg, id);
+          if (e < c.nhist + c.nextra) atomicAdd(&pg.cnt[sl], 1u);
+          else atomicOr(&pg.cnt[sl], 0x80000000u);
+        }
+        __threadfence();
+        __syncthreads();
+        for (int sl = tid; sl < kGH; sl += kBlock) {
+          const uint64_t t = pg.tag[sl];
+          if ((uint32_t)(t >> 32) != pg.gen) continue;
+          const int id = (int)((uint32_t)t - 1u);
+          const uint32_t hcv = pg.cnt[sl];
+          const bool hb = (hcv >> 31) != 0u;
+          float bsum = 0.0f;
+          if (hb) {
+            for (int e = 0; e < c.nbias; ++e)
+              if (c.bias_ids[e] == id) bsum = bsum + c.bias_vals[e];
+          }
+          const bool allowed = !c.mask || ((((id >> 5) < Wm ? c.mask[id >> 5] : 0u) >> (id & 31)) & 1u);
+          pg.fin[sl] = allowed ? fold_nan(penalised_key(load_elem_bits<DT>(c.xrow, id), c.mode, c.rep, c.freq,
+                                                        c.pres, (int)(hcv & 0x7FFFFFFFu), hb, bsum))
+                               : 0u;
+        }
+        __threadfence();
+        __syncthreads();
+      }
+      ovf = 1u;  // the fast path uses the LDS table only
+    }
+  }
+
+  // 3. candidate pool: elements >= tmax (fast path)
+  int nT = 0;
+  uint32_t tk = 0u, ti = 0u;
+  bool slow = ovf != 0u;
+  uint32_t plo = tmax, phi = hi;
+  if (!empty && want > 0) {
+    uint32_t C = 0u;
+    if (!slow) {
+      uint32_t pmax = 0u;
+      C = gather_pool<DT>(a, c, S, NG, pmode == 1, tmax, pool, pmax);
+      if ((int)C > a.pcap || (int)C < want) {
+        slow = true;
+      } else {
+        phi = pmax;
+      }
+    }
+    if (!slow) {
+      auto visit_pool = [&](auto&& f) {
+        for (int i = tid; i < (int)C; i += kBlock) f(pool[i].x, pool[i].y);
+      };
+      radix_select(visit_pool, (uint32_t)want, C, plo, phi, a.V, S, &tk, &ti);
+      nT = (int)compact_pool(S, pool, (int)C, [&](uint2 e) { return selected(e.x, e.y, tk, ti); });
+    } else {
+      flags |= SS_FLAG_FALLBACK;
+      nT = slow_select<DT>(a, c, S, pool, NG, pmode, pg, want, &tk, &ti);
+    }
+  }
+  lds_barrier();
+  if (tid < kMaxU / 32) S.rmask[tid] = 0u;  // clean for the next merge of this workgroup
+  const bool none = empty || nT == 0;
+  if (!empty && nT == 0 && want > 0) flags |= SS_FLAG_EMPTY;  // every token masked or penalised to -inf
+
+  // 4. row maximum (canonical first element) of the selection
+  uint64_t mc = 0ull;
+  uint32_t kmin = 0xFFFFFFFFu;
+  for (int i = tid; i < nT; i += kBlock) {
+    mc = max(mc, comp_of(pool[i].x, pool[i].y));
+    kmin = min(kmin, pool[i].x);
+  }
+  const uint64_t Mcomp = block_max(mc, S.r64);
+  kmin = block_min(kmin, S.r32);
+  const int argmax = none ? -1 : (int)comp_idx(Mcomp);
   if (empty) flags = SS_FLAG_EMPTY;
+  if (none) flags |= SS_FLAG_EMPTY;
 
   if constexpr (OP == OP_TOPK) {
-    int n_sel = 0;
-    if (!empty && c.k_eff > 0) {
-      n_sel = select_exact<DT>(a, c, S, sel, c.k_eff, tmax, comp_key(Mcomp), ovf, n_total, &flags);
-      sort_selected(sel, n_sel);
+    const int n_sel = nT;
+    if (n_sel > 0) {
+      uint64_t* sel = reinterpret_cast<uint64_t*>(pool);
+      const int N = next_pow2(n_sel);
+      for (int i = tid; i < N; i += kBlock) {  // each slot converted by its own thread
+        const uint64_t cm = i < n_sel ? comp_of(pool[i].x, pool[i].y) : 0ull;
+        sel[i] = cm;
+      }
+      lds_barrier();
+      lds_sort_desc(sel, N);
     }
+    const uint64_t* sel = reinterpret_cast<const uint64_t*>(pool);
     for (int r = tid; r < a.k_cap; r += kBlock) {
       const size_t o = (size_t)b * a.k_cap + r;
       if (r < n_sel) {
@@ -1197,8 +1556,30 @@ __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S,
         has_draft = dtok >= 0 && dtok < a.V;
       }
     }
-
-    if (!empty && c.greedy) {
+    if (OP == OP_PROCESS && a.patched && tid == 0) a.npatched[row] = 0u;
+    if (OP == OP_PROCESS && pmode == 1) {
+      // (id, final key) list for the materialising pass
+      uint32_t cnt = 0u;
+      for (int s = tid; s < kH; s += kBlock) cnt += S.hk[s] >= 0 ? 1u : 0u;
+      uint32_t tot;
+      uint32_t off = block_excl_scan(cnt, S.r32, tot);
+      for (int s = tid; s < kH; s += kBlock)
+        if (S.hk[s] >= 0) a.patched[(size_t)row * kGH + off++] = make_uint2((uint32_t)S.hk[s], S.hf[s]);
+      if (tid == 0) a.npatched[row] = tot;
+    } else if (OP == OP_PROCESS && pmode == 2) {
+      uint32_t cnt = 0u;
+      for (int s = tid; s < kGH; s += kBlock) cnt += (uint32_t)(pg.tag[s] >> 32) == pg.gen ? 1u : 0u;
+      uint32_t tot;
+      uint32_t off = block_excl_scan(cnt, S.r32, tot);
+      for (int s = tid; s < kGH; s += kBlock) {
+        const uint64_t t = pg.tag[s];
+        if ((uint32_t)(t >> 32) == pg.gen) a.patched[(size_t)row * kGH + off++] = make_uint2((uint32_t)t - 1u, pg.fin[s]);
+      }
+      if (tid == 0) a.npatched[row] = tot;
+    } else if (OP == OP_PROCESS && pmode == 3) {
+      if (tid == 0) a.npatched[row] = kLinear;
+    }
+    if (!none && c.greedy) {
       token = argmax;
       if constexpr (OP == OP_VERIFY) accept = has_draft && dtok == argmax;
       if constexpr (OP == OP_PROCESS) {
@@ -1221,95 +1602,157 @@ __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S,
           }
         }
       }
-    } else if (!empty) {
-      const int n_sel = select_exact<DT>(a, c, S, sel, c.k_eff, tmax, comp_key(Mcomp), ovf, n_total, &flags);
-      lds_barrier();
-      Dist D;
-      build_dist(a, c, Mcomp, n_sel, S, sel, D);
+    } else if (!none) {
+      // ---- truncation and selection epilogue (Alg. 11 order) on T = pool[0, nT)
+      const double M = (double)float_of_key(comp_key(Mcomp));
+      const double tau = (c.mode & SS_TEMP) ? (double)a.temperature[b] : 1.0;
+      const bool minp = (c.mode & SS_MINP) && a.min_p[b] > 0.0f;
+      const bool topp = (c.mode & SS_TOPP) && a.top_p[b] < 1.0f;
+      const double lt = minp ? log((double)a.min_p[b]) : 0.0;
+      // weights of T in 2^-50 fixed point, stored behind T in the pool region
+      uint64_t* Wl = reinterpret_cast<uint64_t*>(pool) + a.pcap / 2;
+      const int MT = (nT + kBlock - 1) / kBlock;
+      uint32_t inT = 0u, keepm = 0u;
+      uint64_t zl = 0ull;
+      for (int m = 0; m < MT; ++m) {
+        const int i = tid + m * kBlock;
+        if (i < nT) {
+          const uint2 e = pool[i];
+          const double y = (double)float_of_key(e.x);
+          const uint64_t w = (uint64_t)__double2ll_rn(weight_of(y, M, tau) * kFix);
+          Wl[i] = w;
+          zl += w;
+          inT |= 1u << m;
+          bool kp = true;
+          if (minp && comp_of(e.x, e.y) != Mcomp) {
+            const double l = (y == M) ? 0.0 : (y - M) / tau;
+            kp = l >= lt;
+          }
+          if (kp) keepm |= 1u << m;
+        }
+      }
+      const uint64_t Zk = block_sum(zl, S.r64);  // its barriers publish Wl
+      // top-p boundary: first element whose running mass reaches p * Z_k
+      uint64_t ep = 0ull;
+      if (topp)
+        ep = cross_find(S, pool, Wl, nT, inT, (double)a.top_p[b] * (double)Zk, false, kmin, comp_key(Mcomp), a.V);
+      // kept set S = T, min-p survivors, canonical prefix up to ep
+      uint32_t inS = 0u;
+      uint64_t zs = 0ull, lastc = ~0ull;
+      uint32_t ns = 0u;
+      uint32_t smin = 0xFFFFFFFFu;
+      for (int m = 0; m < MT; ++m) {
+        const int i = tid + m * kBlock;
+        if ((keepm >> m) & 1u) {
+          const uint64_t cm = comp_of(pool[i].x, pool[i].y);
+          if (ep == 0ull || cm >= ep) {
+            inS |= 1u << m;
+            zs += Wl[i];
+            ++ns;
+            lastc = min(lastc, cm);
+            smin = min(smin, pool[i].x);
+          }
+        }
+      }
+      const uint64_t Zs = block_sum(zs, S.r64);
+      const uint32_t n_s = block_sum(ns, S.r32);
+      const uint64_t last = block_min(lastc, S.r64);
+      smin = block_min(smin, S.r32);
+      const double Zsd = (double)Zs / kFix;
       const double u0 = uniform01(seed, (uint32_t)b, pos, 0);
+      auto draw = [&](double total) -> uint64_t {
+        const uint64_t e = cross_find(S, pool, Wl, nT, inS, u0 * total, true, smin, comp_key(Mcomp), a.V);
+        return e == 0ull ? last : e;
+      };
       if constexpr (OP == OP_PROCESS) {
         if (tid == 0) {
           RowSummary s;
-          s.thr = sel[D.n_s - 1];
-          s.Z = D.Z_s;
-          s.M = (float)D.M;
-          s.tau = (float)D.tau;
+          s.thr = last;
+          s.Z = Zsd;
+          s.M = (float)M;
+          s.tau = (float)tau;
           s.argmax = argmax;
           s.kind = KIND_DIST;
           a.summ[row] = s;
         }
       } else {
         if (OP == OP_SAMPLE || !has_draft) {
-          const int r = draw_rank(D, u0, S);
-          token = (int)comp_idx(sel[r]);
-          const double w = rank_weight(D, r, S);
-          logprob = (float)log(w / D.Z_s);
+          const uint64_t e = draw((double)Zs);
+          token = (int)comp_idx(e);
+          const double w = weight_of((double)float_of_key(comp_key(e)), M, tau);
+          logprob = (float)log(w / Zsd);
           if constexpr (OP == OP_SAMPLE) {
             if (a.out_idx) {
-              for (int rr = tid; rr < a.k_out; rr += kBlock)
-                a.out_idx[(size_t)b * a.k_out + rr] = rr < D.n_s ? (int32_t)comp_idx(sel[rr]) : -1;
-#pragma unroll
-              for (int m = 0; m < kEPT; ++m) {
-                const int rr = D.chunk0 + m;
-                if (m < D.chunk_n && rr < D.n_s && rr < a.k_out)
-                  a.out_prob[(size_t)b * a.k_out + rr] = (float)(D.w[m] / D.Z_s);
+              // kept list in canonical order: compact S to the front, sort
+              uint64_t* srt = reinterpret_cast<uint64_t*>(pool);
+              for (int m = 0; m < MT; ++m) {
+                const int i = tid + m * kBlock;
+                if (i < nT && !((inS >> m) & 1u)) pool[i] = make_uint2(0u, 0u);
               }
-              for (int rr = D.n_s + tid; rr < a.k_out; rr += kBlock) a.out_prob[(size_t)b * a.k_out + rr] = 0.0f;
-              if (D.n_s > a.k_out) flags |= SS_FLAG_OUT_TRUNC;
+              lds_barrier();
+              const uint32_t tot = compact_pool(S, pool, nT, [](uint2 e2) { return e2.x != 0u; });
+              const int N = next_pow2((int)tot);
+              for (int i = tid; i < N; i += kBlock) {
+                const uint64_t cm = i < (int)tot ? comp_of(pool[i].x, pool[i].y) : 0ull;
+                srt[i] = cm;
+              }
+              lds_barrier();
+              lds_sort_desc(srt, N);
+              for (int rr = tid; rr < a.k_out; rr += kBlock) {
+                if (rr < (int)n_s) {
+                  const uint64_t cc = srt[rr];
+                  a.out_idx[(size_t)b * a.k_out + rr] = (int32_t)comp_idx(cc);
+                  a.out_prob[(size_t)b * a.k_out + rr] =
+                      (float)(weight_of((double)float_of_key(comp_key(cc)), M, tau) / Zsd);
+                } else {
+                  a.out_idx[(size_t)b * a.k_out + rr] = -1;
+                  a.out_prob[(size_t)b * a.k_out + rr] = 0.0f;
+                }
+              }
+              if ((int)n_s > a.k_out) flags |= SS_FLAG_OUT_TRUNC;
             }
           }
         } else {
           // verification of draft token dtok against this row's distribution
           const float* qrow = a.draft_probs + ((size_t)b * a.L + c.ell) * (size_t)a.ld_q;
           double pd_local = 0.0;
-#pragma unroll
-          for (int m = 0; m < kEPT; ++m) {
-            const int rr = D.chunk0 + m;
-            if (m < D.chunk_n && rr < D.n_s && (int)comp_idx(sel[rr]) == dtok) pd_local = D.w[m] / D.Z_s;
+          for (int m = 0; m < MT; ++m) {
+            const int i = tid + m * kBlock;
+            if (((inS >> m) & 1u) && (int)pool[i].y == dtok)
+              pd_local = weight_of((double)float_of_key(pool[i].x), M, tau) / Zsd;
           }
-          const double Pd = block_max(pd_local, S.redd);
+          const double Pd = block_max(pd_local, S.rd);
           const double qd = (double)qrow[dtok];
           const double u1 = uniform01(seed, (uint32_t)b, pos, 1);
           accept = (Pd > 0.0 && u1 * qd <= Pd) ? 1 : 0;
           if (!accept) {
-            // residual max(0, P - q) over the kept prefix, canonical order
-            double rw[kEPT];
-            double loc = 0.0;
-#pragma unroll
-            for (int m = 0; m < kEPT; ++m) {
-              rw[m] = 0.0;
-              const int rr = D.chunk0 + m;
-              if (m < D.chunk_n && rr < D.n_s) {
-                const double P = D.w[m] / D.Z_s;
-                const double v = P - (double)qrow[comp_idx(sel[rr])];
-                loc += v > 0.0 ? v : 0.0;
-                rw[m] = loc;  // local inclusive prefix
-              }
-            }
-            double Rtot;
-            const double base = block_excl_scan(loc, S.redd, Rtot);
-            int r;
-            if (Rtot > 0.0) {
-              const double target = u0 * Rtot;
-              uint32_t rr_min = 0xFFFFFFFFu;
-#pragma unroll
-              for (int m = 0; m < kEPT; ++m) {
-                const int rr = D.chunk0 + m;
-                if (m < D.chunk_n && rr < D.n_s && base + rw[m] > target && (uint32_t)rr < rr_min) rr_min = rr;
-              }
-              rr_min = block_min(rr_min, S.red32);
-              r = rr_min == 0xFFFFFFFFu ? D.n_s - 1 : (int)rr_min;
+            // residual max(0, P - q) over the kept set, canonical order
+            auto resid = [&](int i) -> uint64_t {
+              const double P = weight_of((double)float_of_key(pool[i].x), M, tau) / Zsd;
+              const double v = P - (double)qrow[pool[i].y];
+              return v > 0.0 ? (uint64_t)__double2ll_rn(v * kFix) : 0ull;
+            };
+            uint64_t rl = 0ull;
+            for (int m = 0; m < MT; ++m)
+              if ((inS >> m) & 1u) rl += resid(tid + m * kBlock);
+            const uint64_t Rt = block_sum(rl, S.r64);
+            uint64_t e;
+            if (Rt > 0ull) {
+              for (int m = 0; m < MT; ++m)
+                if ((inS >> m) & 1u) Wl[tid + m * kBlock] = resid(tid + m * kBlock);
+              lds_barrier();
+              e = draw((double)Rt);
             } else {
-              r = draw_rank(D, u0, S);
+              e = draw((double)Zs);
             }
-            token = (int)comp_idx(sel[r]);
+            token = (int)comp_idx(e);
           }
         }
       }
     }
 
     if constexpr (OP == OP_PROCESS) {
-      if (empty && tid == 0) {
+      if (none && tid == 0) {
         RowSummary s;
         s.thr = 0;
         s.Z = 1.0;
@@ -1327,7 +1770,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S,
         if (a.out_logprob) a.out_logprob[b] = logprob;
         if (a.flags) a.flags[b] = flags;
       }
-      if (empty && a.out_idx) {
+      if (none && a.out_idx) {
         for (int r = tid; r < a.k_out; r += kBlock) {
           a.out_idx[(size_t)b * a.k_out + r] = -1;
           a.out_prob[(size_t)b * a.k_out + r] = 0.0f;
@@ -1335,7 +1778,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S,
       }
       return;
     } else {
-      // publish this row's decision; the request's last row assembles
+      // publish this row's decision; the assembly kernel combines a request's rows
       if (tid == 0) {
         RowResult rr;
         rr.accept = accept;
@@ -1344,187 +1787,84 @@ __device__ __forceinline__ void merge_row(const KArgs& a, const Ctx& c, Smem& S,
         rr.pad = 0;
         a.res[row] = rr;
       }
-      __threadfence();
-      __syncthreads();
-      if (tid == 0) {
-        const uint32_t tk = atomicAdd(&a.req_ticket[b], 1u);
-        S.bc[3] = (tk == (uint32_t)a.L) ? 1u : 0u;
-      }
-      __syncthreads();
-      if (S.bc[3] == 0u) return;
-      __threadfence();
-      if (tid == 0) {
-        a.req_ticket[b] = 0u;
-        const int L = a.L;
-        int n = 0;
-        int fl = 0;
-        int32_t* out = a.out_tokens + (size_t)b * (L + 1);
-        for (int l = 0; l <= L; ++l) out[l] = -1;
-        for (int l = 0; l <= L; ++l) {
-          const RowResult rr = a.res[(size_t)b * (L + 1) + l];
-          fl |= rr.flags;
-          if (l < L && rr.accept) {
-            out[l] = a.draft_tokens[(size_t)b * L + l];
-            ++n;
-            continue;
-          }
-          out[l] = rr.emit;
-          break;
-        }
-        a.out_nacc[b] = n;
-        if (a.flags) a.flags[b] = fl;
-      }
     }
   }
 }
 
-// ---------------------------------------------------------------------------
-// Streaming kernel: one workgroup per (row, tile).  Tile maximum and argmax
-// for every row; for truncating rows, candidate emission above a per-tile
-// threshold (the q-th largest of 2048 group maxima, q = quota(k, T)).
-// ---------------------------------------------------------------------------
-// Largest 16-bit key prefix t with at least q of the wave's values >= t
-// (binary search on the threshold; counts come from ballots, no LDS).
-template <int N>
-__device__ __forceinline__ uint32_t wave_threshold(const uint32_t (&v)[N], uint32_t q) {
-  uint32_t prefix = 0u;
-#pragma unroll 1
-  for (int b = 31; b >= 16; --b) {
-    const uint32_t cand = prefix | (1u << b);
-    uint32_t cnt = 0u;
-#pragma unroll
-    for (int i = 0; i < N; ++i) cnt += (uint32_t)__popcll(__ballot(v[i] >= cand));
-    if (cnt >= q) prefix = cand;
-  }
-  return prefix < kKeyFloor ? kKeyFloor : prefix;
-}
-
-// One tile of the streaming kernel.  After the loads everything is local to
-// a wavefront: each wavefront is an emission unit with its own maximum,
-// threshold and candidate region, so the tail needs no workgroup barrier.
-template <int DT, bool FULL>
-__device__ __forceinline__ void stream_tile(const KArgs& a, const Ctx& c, Smem& S, int row, int tile) {
-  const int tid = threadIdx.x;
-  const int lo = tile * kTile;
-  uint32_t key[kPT];
-  load_tile<DT, FULL>(a, c, lo, S, key);
-
-  uint32_t gm[kGPT];
-  auto group_maxima = [&]() {
-#pragma unroll
-    for (int g = 0; g < kGPT; ++g) {
-      uint32_t m = key[g * kGS];
-#pragma unroll
-      for (int s = 1; s < kGS; ++s) m = max(m, key[g * kGS + s]);
-      gm[g] = m;
-    }
-  };
-  group_maxima();
-  uint32_t tmax = gm[0];
-#pragma unroll
-  for (int g = 1; g < kGPT; ++g) tmax = max(tmax, gm[g]);
-  if (__ballot(tmax > kKeyPosInf)) {  // a positive NaN in this wavefront: fold it to invalid
-#pragma unroll
-    for (int j = 0; j < kPT; ++j) key[j] = fold_nan(key[j]);
-    group_maxima();
-    tmax = gm[0];
-#pragma unroll
-    for (int g = 1; g < kGPT; ++g) tmax = max(tmax, gm[g]);
-  }
-  // wavefront maximum and the lowest index holding it
-  const uint32_t wm = wave_max(tmax);
-  uint32_t aidx = 0xFFFFFFFFu;
-  if (wm >= kKeyFloor && tmax == wm) {
-#pragma unroll
-    for (int j = kPT - 1; j >= 0; --j)
-      if (key[j] == wm) aidx = (uint32_t)(lo + local_of_slot<DT>(tid, j));
-  }
-  aidx = wave_min(aidx);
-
-  const int w = wave();
-  const int unit = (row * a.T + tile) * kUnits + w;
-  uint32_t t = kNoEmit;
-  uint32_t n = 0u;
-  if (!c.greedy && c.k_eff > 0) {
-    if (wm < kKeyFloor) {
-      t = kKeyFloor;  // nothing valid here: everything valid (nothing) is emitted
-    } else {
-      const int q = quota(c.k_eff, a.T * kUnits);
-      if (2 * q > kUnitGroups) {
-        t = kKeyFloor;
-      } else if (q <= 16) {
-        const uint32_t v1[1] = {tmax};
-        t = wave_threshold(v1, (uint32_t)q);
-      } else {
-        t = wave_threshold(gm, (uint32_t)q);
-      }
-      uint2* region = a.cand + (size_t)unit * a.cap;
-      const uint32_t cap = (uint32_t)a.cap;
-#pragma unroll
-      for (int j = 0; j < kPT; ++j) {
-        const bool sel = key[j] >= t;
-        const uint64_t m = __ballot(sel);
-        if (m) {
-          if (sel) {
-            const uint32_t p = n + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-            if (p < cap) region[p] = make_uint2(key[j], (uint32_t)(lo + local_of_slot<DT>(tid, j)));
-          }
-          n += (uint32_t)__popcll(m);
-        }
-      }
-    }
-  }
-  if (lane() == 0) a.rec[unit] = make_uint4(wm, aidx, t, n);
-}
-
+// ===========================================================================
+// Kernels
+// ===========================================================================
+// Streaming kernel: one unit per wavefront, no LDS, no barrier.  Workgroups
+// are remapped so that consecutive units (one row) share an XCD and its L2.
 template <int DT>
 __global__ __launch_bounds__(kBlock) void ss_stream_kernel(KArgs a) {
-  extern __shared__ __align__(16) unsigned char smem_raw[];
-  Smem& S = *reinterpret_cast<Smem*>(smem_raw);
-  const int row = blockIdx.x / a.T;
-  const int tile = blockIdx.x - row * a.T;
-  const Ctx c = make_ctx<DT>(a, row);
-  // two straight-line copies: the full-tile path keeps every load in flight
-  if (tile_full(a, tile * kTile))
-    stream_tile<DT, true>(a, c, S, row, tile);
-  else
-    stream_tile<DT, false>(a, c, S, row, tile);
+  int bid = blockIdx.x;
+  const int nb = gridDim.x;
+  if (bid < (nb & ~7)) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
+  const int gu = __builtin_amdgcn_readfirstlane(bid * kWaves + wave());
+  if (gu < a.rows * a.U) scan_unit<DT>(a, gu);
 }
 
-// One workgroup per row: merge the tile records and candidates of the row.
+// Merge kernel: one workgroup per row (the launch boundary orders the
+// streaming kernel's records and candidates before it).
 template <int DT, int OP>
 __global__ __launch_bounds__(kBlock) void ss_merge_kernel(KArgs a) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
-  Smem& S = *reinterpret_cast<Smem*>(smem_raw);
-  uint64_t* sel = reinterpret_cast<uint64_t*>(smem_raw + kSelOff);
-  if (threadIdx.x == 0) S.fa = a;  // for the out-of-line fallback
-  const Ctx c = make_ctx<DT>(a, blockIdx.x);
-  merge_row<DT, OP>(a, c, S, sel);
+  MSmem& S = *reinterpret_cast<MSmem*>(smem_raw);
+  uint2* pool = reinterpret_cast<uint2*>(smem_raw + kSmemFixed);
+  if (threadIdx.x < kMaxU / 32) S.rmask[threadIdx.x] = 0u;
+  __syncthreads();
+  merge_row<DT, OP>(a, blockIdx.x, S, pool);
+}
+
+// Verification assembly: per request, the accepted drafts, then the first
+// row's correction (or the bonus token), then -1.
+__global__ __launch_bounds__(kBlock) void ss_assemble_kernel(KArgs a) {
+  const int b = blockIdx.x * kBlock + threadIdx.x;
+  if (b >= a.B) return;
+  const int L = a.L;
+  int n = 0;
+  int fl = 0;
+  int32_t* out = a.out_tokens + (size_t)b * (L + 1);
+  int l = 0;
+  for (; l <= L; ++l) {
+    const RowResult rr = a.res[(size_t)b * (L + 1) + l];
+    fl |= rr.flags;
+    if (l < L && rr.accept) {
+      out[l] = a.draft_tokens[(size_t)b * L + l];
+      ++n;
+      continue;
+    }
+    out[l] = rr.emit;
+    ++l;
+    break;
+  }
+  for (; l <= L; ++l) out[l] = -1;
+  a.out_nacc[b] = n;
+  if (a.flags) a.flags[b] = fl;
 }
 
 // ---------------------------------------------------------------------------
 // Materialising pass of ss_process_logits: processed logits and final
-// probabilities for every element, from the per-row summary.
+// probabilities for every element, from the per-row summary; patched ids take
+// their final values from the merge's list.
 // ---------------------------------------------------------------------------
 template <int DT>
 __global__ __launch_bounds__(kBlock) void ss_materialize_kernel(KArgs a) {
-  extern __shared__ __align__(16) unsigned char smem_raw[];
-  Smem& S = *reinterpret_cast<Smem*>(smem_raw);
+  constexpr int TILE = 4096;
   const int tid = threadIdx.x;
-  const int row = blockIdx.x / a.T;
-  const int tile = blockIdx.x - row * a.T;
-  const int lo = tile * kTile;
-  const Ctx c = make_ctx<DT>(a, row);
-  uint32_t key[kPT];
-  if (tile_full(a, lo))
-    load_tile<DT, true>(a, c, lo, S, key);
-  else
-    load_tile<DT, false>(a, c, lo, S, key);
-#pragma unroll
-  for (int j = 0; j < kPT; ++j) key[j] = fold_nan(key[j]);
+  const int T = (a.V + TILE - 1) / TILE;
+  const int row = blockIdx.x / T;
+  const int tile = blockIdx.x - row * T;
+  const int lo = tile * TILE;
+  const int hi = min(a.V, lo + TILE);
+  const int b = row;
+  const uint32_t mode = (a.mode ? a.mode[b] : 0u) & a.feat;
+  const uint32_t* mask = (mode & SS_GRAMMAR) ? a.bitmask + (size_t)row * (size_t)a.mask_ld : nullptr;
+  const unsigned char* xrow = reinterpret_cast<const unsigned char*>(a.x) + (size_t)row * (size_t)a.ld * DTT<DT>::ES;
   const RowSummary s = a.summ[row];
   const size_t ob = (size_t)row * (size_t)a.V;
+  const int Wm = (a.V + 31) >> 5;
   auto emit = [&](uint32_t k, uint32_t i) {
     if (a.out_logits) a.out_logits[ob + i] = k >= kKeyFloor ? float_of_key(k) : -__builtin_inff();
     if (a.out_probs) {
@@ -1537,10 +1877,31 @@ __global__ __launch_bounds__(kBlock) void ss_materialize_kernel(KArgs a) {
       a.out_probs[ob + i] = p;
     }
   };
-#pragma unroll
-  for (int j = 0; j < kPT; ++j) {
-    const int l = local_of_slot<DT>(tid, j);
-    if (lo + l < a.V) emit(key[j], (uint32_t)(lo + l));
+  // final keys of the patched ids of this tile, staged in LDS (kNone elsewhere)
+  constexpr uint32_t kNone = 0xFFFFFFFFu;
+  __shared__ uint32_t pv[TILE];
+  for (int l = tid; l < TILE; l += kBlock) pv[l] = kNone;
+  __syncthreads();
+  const uint32_t np = a.npatched ? a.npatched[row] : 0u;
+  const uint2* pl = a.patched + (size_t)row * kGH;
+  for (uint32_t j = tid; np != kLinear && j < np; j += kBlock) {
+    const uint2 e = pl[j];
+    if ((int)e.x >= lo && (int)e.x < hi) pv[e.x - lo] = e.y;
+  }
+  __syncthreads();
+  for (int i = lo + tid; i < hi; i += kBlock) {
+    uint32_t k = fold_nan(key_raw(load_elem_bits<DT>(xrow, i)));
+    if (mask && !((((i >> 5) < Wm ? mask[i >> 5] : 0u) >> (i & 31)) & 1u)) k = 0u;
+    const uint32_t pk = pv[i - lo];
+    if (pk != kNone) k = pk;
+    if (np == kLinear) {  // very long lists: look every id up
+      const Ctx c = make_ctx<DT>(a, row);
+      int cn;
+      bool hb;
+      float bs;
+      if (lin_info(c, i, &cn, &hb, &bs) && k != 0u) k = lin_final<DT>(a, c, i);
+    }
+    emit(k, (uint32_t)i);
   }
 }
 
@@ -1553,39 +1914,54 @@ __global__ void ss_zero_kernel(uint32_t* p, size_t n) {
 // Host side
 // ---------------------------------------------------------------------------
 struct Layout {
-  int T, cap, rows;
-  size_t off_ticket, off_req, off_rec, off_cand, off_res, total;
-  int smem;
+  int U, cap, pcap, rows, smem;
+  size_t off_rec, off_cand, off_res, off_patch, off_npatch, off_gtag, off_gcnt, off_gfin,
+      off_ggen, total;
 };
 
 static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
-static bool make_layout(int op, int B, int V, int L, int k_max, Layout* lay) {
+static bool make_layout(int op, int B, int V, int L, int k_max, int dtype, Layout* lay) {
   if (B <= 0 || V <= 0 || V > SS_MAX_V || k_max < 1 || k_max > SS_MAX_K) return false;
   if (op == OP_VERIFY && (L < 1 || L > SS_MAX_L)) return false;
   if (op < OP_TOPK || op > OP_PROCESS) return false;
   const int rows = op == OP_VERIFY ? B * (L + 1) : B;
-  const int T = (V + kTile - 1) / kTile;
-  const int cap = unit_cap(k_max, T * kUnits);
+  const int U = (V + kUE - 1) / kUE;
+  const int cap = unit_cap(k_max, U, dtype);
+  // pool entries: candidates; after selection T in the front half and, for
+  // the sampling ops, its fixed-point weights in the back half
+  int pcap = 2 * k_max + 128;
+  if (pcap < 1024) pcap = 1024;
+  if (op == OP_TOPK && pcap > SS_MAX_K) pcap = SS_MAX_K > next_pow2(k_max) ? SS_MAX_K : next_pow2(k_max);
+  if (pcap < next_pow2(k_max)) pcap = next_pow2(k_max);
+  pcap = (pcap + 255) & ~255;
   size_t o = 0;
-  lay->off_ticket = o;
-  o = align256(o + (size_t)rows * 4);
-  lay->off_req = o;
-  o = align256(o + (size_t)B * 4);
-  const size_t zero_end = o;
-  (void)zero_end;
   lay->off_rec = o;
-  o = align256(o + (size_t)rows * T * kUnits * 16);
+  o = align256(o + (size_t)rows * U * 16);
   lay->off_cand = o;
-  o = align256(o + (size_t)rows * T * kUnits * cap * 8);
+  o = align256(o + (size_t)rows * U * cap * 16);
   lay->off_res = o;
   const size_t res_bytes = op == OP_VERIFY ? sizeof(RowResult) : (op == OP_PROCESS ? sizeof(RowSummary) : 0);
   o = align256(o + (size_t)rows * res_bytes);
+  lay->off_patch = o;
+  if (op == OP_PROCESS) o = align256(o + (size_t)rows * kGH * 8);
+  lay->off_npatch = o;
+  if (op == OP_PROCESS) o = align256(o + (size_t)rows * 4);
+  const size_t ghr = op == OP_TOPK ? 0 : (size_t)rows;  // top-k applies no penalties
+  lay->off_ggen = o;
+  o = align256(o + ghr * 4);
+  lay->off_gtag = o;
+  o = align256(o + ghr * kGH * 8);
+  lay->off_gcnt = o;
+  o = align256(o + ghr * kGH * 4);
+  lay->off_gfin = o;
+  o = align256(o + ghr * kGH * 4);
   lay->total = o;
-  lay->T = T;
+  lay->U = U;
   lay->cap = cap;
+  lay->pcap = pcap;
   lay->rows = rows;
-  lay->smem = kSelOff + 8 * next_pow2(k_max);
+  lay->smem = kSmemFixed + 8 * pcap;
   return true;
 }
 
@@ -1648,39 +2024,78 @@ static void launch_merge(const KArgs& k, dim3 grid, dim3 block, int smem, hipStr
   }
 }
 
+static bool smem_configured[2][4];
+
+template <int DT, int OP>
+static bool set_smem(int bytes) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&ss_merge_kernel<DT, OP>),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess;
+}
+
 static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStream_t st, bool materialize) {
   unsigned char* w = reinterpret_cast<unsigned char*>(ws);
-  k.T = lay.T;
+  k.U = lay.U;
   k.cap = lay.cap;
-  k.ticket = reinterpret_cast<uint32_t*>(w + lay.off_ticket);
-  k.req_ticket = reinterpret_cast<uint32_t*>(w + lay.off_req);
+  k.pcap = lay.pcap;
   k.rec = reinterpret_cast<uint4*>(w + lay.off_rec);
-  k.cand = reinterpret_cast<uint2*>(w + lay.off_cand);
+  k.cand = reinterpret_cast<uint4*>(w + lay.off_cand);
   k.res = reinterpret_cast<RowResult*>(w + lay.off_res);
   k.summ = reinterpret_cast<RowSummary*>(w + lay.off_res);
-  const dim3 grid((unsigned)(lay.rows * lay.T)), rgrid((unsigned)lay.rows), block(kBlock);
+  k.patched = k.op == OP_PROCESS ? reinterpret_cast<uint2*>(w + lay.off_patch) : nullptr;
+  k.npatched = k.op == OP_PROCESS ? reinterpret_cast<uint32_t*>(w + lay.off_npatch) : nullptr;
+  k.gtag = reinterpret_cast<uint64_t*>(w + lay.off_gtag);
+  k.gcnt = reinterpret_cast<uint32_t*>(w + lay.off_gcnt);
+  k.gfin = reinterpret_cast<uint32_t*>(w + lay.off_gfin);
+  k.ggen = reinterpret_cast<uint32_t*>(w + lay.off_ggen);
+  const int di = dtype == SS_BF16 ? 1 : 0;
+  if (!smem_configured[di][k.op]) {
+    // the largest dynamic LDS any call can ask for
+    const int maxb = kSmemFixed + 8 * (2 * SS_MAX_K + 512);
+    bool ok;
+    if (dtype == SS_BF16) {
+      ok = k.op == OP_TOPK ? set_smem<SS_BF16, OP_TOPK>(maxb)
+           : k.op == OP_SAMPLE ? set_smem<SS_BF16, OP_SAMPLE>(maxb)
+           : k.op == OP_VERIFY ? set_smem<SS_BF16, OP_VERIFY>(maxb)
+                               : set_smem<SS_BF16, OP_PROCESS>(maxb);
+    } else {
+      ok = k.op == OP_TOPK ? set_smem<SS_F32, OP_TOPK>(maxb)
+           : k.op == OP_SAMPLE ? set_smem<SS_F32, OP_SAMPLE>(maxb)
+           : k.op == OP_VERIFY ? set_smem<SS_F32, OP_VERIFY>(maxb)
+                               : set_smem<SS_F32, OP_PROCESS>(maxb);
+    }
+    if (!ok) return SS_ERR_HIP;
+    smem_configured[di][k.op] = true;
+  }
+  const int nunits = lay.rows * lay.U;
+  const dim3 grid((unsigned)((nunits + kWaves - 1) / kWaves)), rgrid((unsigned)lay.rows), block(kBlock);
   if (g_ev_before) (void)hipEventRecord(g_ev_before, st);
   if (dtype == SS_BF16)
-    hipLaunchKernelGGL(ss_stream_kernel<SS_BF16>, grid, block, kSmemStream, st, k);
+    hipLaunchKernelGGL(ss_stream_kernel<SS_BF16>, grid, block, 0, st, k);
   else
-    hipLaunchKernelGGL(ss_stream_kernel<SS_F32>, grid, block, kSmemStream, st, k);
+    hipLaunchKernelGGL(ss_stream_kernel<SS_F32>, grid, block, 0, st, k);
   if (g_ev_after) (void)hipEventRecord(g_ev_after, st);
-  if (dtype == SS_BF16) {
+  if (dtype == SS_BF16)
     launch_merge<SS_BF16>(k, rgrid, block, lay.smem, st);
-    if (materialize) hipLaunchKernelGGL(ss_materialize_kernel<SS_BF16>, grid, block, kSmemStream, st, k);
-  } else {
+  else
     launch_merge<SS_F32>(k, rgrid, block, lay.smem, st);
-    if (materialize) hipLaunchKernelGGL(ss_materialize_kernel<SS_F32>, grid, block, kSmemStream, st, k);
+  if (k.op == OP_VERIFY)
+    hipLaunchKernelGGL(ss_assemble_kernel, dim3((unsigned)((k.B + kBlock - 1) / kBlock)), block, 0, st, k);
+  if (materialize) {
+    const int T = (k.V + 4095) / 4096;
+    const dim3 mgrid((unsigned)(lay.rows * T));
+    if (dtype == SS_BF16)
+      hipLaunchKernelGGL(ss_materialize_kernel<SS_BF16>, mgrid, block, 0, st, k);
+    else
+      hipLaunchKernelGGL(ss_materialize_kernel<SS_F32>, mgrid, block, 0, st, k);
   }
   return hipGetLastError() == hipSuccess ? SS_OK : SS_ERR_HIP;
 }
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-static bool params_ok(const ss_params* p, int B, int V, int rows) {
+static bool params_ok(const ss_params* p, int B, int V) {
   if (!p || p->B != B || p->V != V || !p->mode) return false;
   if (p->bitmask && p->bitmask_ld < (int64_t)((V + 31) / 32)) return false;
-  (void)rows;
   return true;
 }
 
@@ -1693,7 +2108,7 @@ extern "C" {
 size_t ss_workspace_bytes(int op, int B, int V, int L, int k_max, int dtype) {
   if (dtype != SS_F32 && dtype != SS_BF16) return 0;
   Layout lay;
-  if (!make_layout(op, B, V, L, k_max, &lay)) return 0;
+  if (!make_layout(op, B, V, L, k_max, dtype, &lay)) return 0;
   return lay.total;
 }
 
@@ -1708,11 +2123,11 @@ ss_status ss_workspace_init(void* ws, size_t ws_bytes, void* stream) {
   return hipGetLastError() == hipSuccess ? SS_OK : SS_ERR_HIP;
 }
 
-ss_status ss_topk(const void* x, int dtype, int B, int V, int64_t ld, const int32_t* k, int k_max,
-                  float* out_val, int32_t* out_idx, int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+ss_status ss_topk(const void* x, int dtype, int B, int V, int64_t ld, const int32_t* k, int k_max, float* out_val,
+                  int32_t* out_idx, int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
   if (!x || !out_val || !out_idx || !ws || (dtype != SS_F32 && dtype != SS_BF16) || ld < V) return SS_ERR_INVALID_ARG;
   Layout lay;
-  if (!make_layout(OP_TOPK, B, V, 0, k_max, &lay)) return SS_ERR_INVALID_ARG;
+  if (!make_layout(OP_TOPK, B, V, 0, k_max, dtype, &lay)) return SS_ERR_INVALID_ARG;
   if (ws_bytes < lay.total || !aligned16(ws)) return SS_ERR_WORKSPACE;
   KArgs a = {};
   a.x = x;
@@ -1739,9 +2154,9 @@ ss_status ss_sample(const void* logits, int dtype, int64_t ld, const ss_params* 
   if (!logits || !p || !out_token || !ws || (dtype != SS_F32 && dtype != SS_BF16)) return SS_ERR_INVALID_ARG;
   if (k_out < 0 || (k_out > 0 && (!out_idx || !out_prob))) return SS_ERR_INVALID_ARG;
   const int B = p->B, V = p->V;
-  if (ld < V || !params_ok(p, B, V, B)) return SS_ERR_INVALID_ARG;
+  if (ld < V || !params_ok(p, B, V)) return SS_ERR_INVALID_ARG;
   Layout lay;
-  if (!make_layout(OP_SAMPLE, B, V, 0, k_max, &lay)) return SS_ERR_INVALID_ARG;
+  if (!make_layout(OP_SAMPLE, B, V, 0, k_max, dtype, &lay)) return SS_ERR_INVALID_ARG;
   if (ws_bytes < lay.total || !aligned16(ws)) return SS_ERR_WORKSPACE;
   KArgs a = {};
   a.x = logits;
@@ -1770,10 +2185,10 @@ ss_status ss_verify(const void* target_logits, int dtype, int64_t ld_row, const 
     return SS_ERR_INVALID_ARG;
   if (dtype != SS_F32 && dtype != SS_BF16) return SS_ERR_INVALID_ARG;
   const int B = p->B, V = p->V;
-  if (ld_row < V || ld_q < V || !params_ok(p, B, V, B * (L + 1))) return SS_ERR_INVALID_ARG;
+  if (ld_row < V || ld_q < V || !params_ok(p, B, V)) return SS_ERR_INVALID_ARG;
   if (!p->seed || !p->position) return SS_ERR_INVALID_ARG;
   Layout lay;
-  if (!make_layout(OP_VERIFY, B, V, L, k_max, &lay)) return SS_ERR_INVALID_ARG;
+  if (!make_layout(OP_VERIFY, B, V, L, k_max, dtype, &lay)) return SS_ERR_INVALID_ARG;
   if (ws_bytes < lay.total || !aligned16(ws)) return SS_ERR_WORKSPACE;
   KArgs a = {};
   a.x = target_logits;
@@ -1801,9 +2216,9 @@ ss_status ss_process_logits(const void* logits, int dtype, int64_t ld, const ss_
                             void* stream) {
   if (!logits || !p || !ws || (dtype != SS_F32 && dtype != SS_BF16)) return SS_ERR_INVALID_ARG;
   const int B = p->B, V = p->V;
-  if (ld < V || !params_ok(p, B, V, B)) return SS_ERR_INVALID_ARG;
+  if (ld < V || !params_ok(p, B, V)) return SS_ERR_INVALID_ARG;
   Layout lay;
-  if (!make_layout(OP_PROCESS, B, V, 0, k_max, &lay)) return SS_ERR_INVALID_ARG;
+  if (!make_layout(OP_PROCESS, B, V, 0, k_max, dtype, &lay)) return SS_ERR_INVALID_ARG;
   if (ws_bytes < lay.total || !aligned16(ws)) return SS_ERR_WORKSPACE;
   KArgs a = {};
   a.x = logits;
