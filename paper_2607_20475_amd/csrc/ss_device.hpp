@@ -95,38 +95,76 @@ __device__ __forceinline__ void lds_barrier() {
 __device__ __forceinline__ int lane() { return (int)__lane_id(); }
 __device__ __forceinline__ int wave() { return (int)(threadIdx.x >> 6); }
 
+// ---------------------------------------------------------------------------
+// Cross-lane primitives on DPP row operations (no LDS round trip).  Every
+// lane of the wavefront must be active.  64-bit values move as two halves.
+// ---------------------------------------------------------------------------
+template <int CTRL, int ROWM = 0xF, int BANKM = 0xF, bool BC = false>
+__device__ __forceinline__ uint32_t dpp32(uint32_t old, uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROWM, BANKM, BC);
+}
+template <int CTRL, int ROWM = 0xF, int BANKM = 0xF, bool BC = false>
+__device__ __forceinline__ uint64_t dpp64(uint64_t old, uint64_t v) {
+  const uint32_t lo = dpp32<CTRL, ROWM, BANKM, BC>((uint32_t)old, (uint32_t)v);
+  const uint32_t hi = dpp32<CTRL, ROWM, BANKM, BC>((uint32_t)(old >> 32), (uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+template <typename T, int CTRL, int ROWM = 0xF, int BANKM = 0xF, bool BC = false>
+__device__ __forceinline__ T dppT(T old, T v) {
+  if constexpr (sizeof(T) == 8) {
+    return __builtin_bit_cast(T, dpp64<CTRL, ROWM, BANKM, BC>(__builtin_bit_cast(uint64_t, old),
+                                                               __builtin_bit_cast(uint64_t, v)));
+  } else {
+    return __builtin_bit_cast(T, dpp32<CTRL, ROWM, BANKM, BC>(__builtin_bit_cast(uint32_t, old),
+                                                               __builtin_bit_cast(uint32_t, v)));
+  }
+}
+template <typename T>
+__device__ __forceinline__ T readlane_T(T v, int l) {
+  if constexpr (sizeof(T) == 8) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)u, l), hi = __builtin_amdgcn_readlane((uint32_t)(u >> 32), l);
+    return __builtin_bit_cast(T, ((uint64_t)hi << 32) | lo);
+  } else {
+    return __builtin_bit_cast(T, (uint32_t)__builtin_amdgcn_readlane(__builtin_bit_cast(uint32_t, v), l));
+  }
+}
+// every lane ends with the reduction over its 16-lane row
+template <typename T, typename Op>
+__device__ __forceinline__ T row_reduce(T v, Op op) {
+  v = op(v, dppT<T, 0xB1>(v, v));   // quad_perm [1,0,3,2]
+  v = op(v, dppT<T, 0x4E>(v, v));   // quad_perm [2,3,0,1]
+  v = op(v, dppT<T, 0x141>(v, v));  // row_half_mirror
+  v = op(v, dppT<T, 0x140>(v, v));  // row_mirror
+  return v;
+}
+template <typename T, typename Op>
+__device__ __forceinline__ T wave_reduce(T v, Op op) {
+  v = row_reduce(v, op);
+  return op(op(readlane_T(v, 0), readlane_T(v, 16)), op(readlane_T(v, 32), readlane_T(v, 48)));
+}
 template <typename T>
 __device__ __forceinline__ T wave_max(T v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    T w = __shfl_xor(v, o, 64);
-    v = w > v ? w : v;
-  }
-  return v;
+  return wave_reduce(v, [](T x, T y) { return x > y ? x : y; });
 }
 template <typename T>
 __device__ __forceinline__ T wave_min(T v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    T w = __shfl_xor(v, o, 64);
-    v = w < v ? w : v;
-  }
-  return v;
+  return wave_reduce(v, [](T x, T y) { return x < y ? x : y; });
 }
 template <typename T>
 __device__ __forceinline__ T wave_sum(T v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  return wave_reduce(v, [](T x, T y) { return x + y; });
 }
+// inclusive prefix sum over the 64 lanes: Hillis-Steele inside each row,
+// then the row totals carried across rows
 template <typename T>
 __device__ __forceinline__ T wave_incl_scan(T v) {
-  const int l = lane();
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    T w = __shfl_up(v, o, 64);
-    if (l >= o) v += w;
-  }
+  v += dppT<T, 0x111, 0xF, 0xF, true>(T(0), v);  // row_shr:1, zero fill
+  v += dppT<T, 0x112, 0xF, 0xF, true>(T(0), v);  // row_shr:2
+  v += dppT<T, 0x114, 0xF, 0xF, true>(T(0), v);  // row_shr:4
+  v += dppT<T, 0x118, 0xF, 0xF, true>(T(0), v);  // row_shr:8
+  v += dppT<T, 0x142, 0xA, 0xF, false>(T(0), v);  // row_bcast:15 into rows 1, 3
+  v += dppT<T, 0x143, 0xC, 0xF, false>(T(0), v);  // row_bcast:31 into rows 2, 3
   return v;
 }
 

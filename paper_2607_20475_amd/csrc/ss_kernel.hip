@@ -48,7 +48,7 @@ namespace ss {
 
 constexpr int kUE = 2048;                    // elements per unit (one wavefront)
 constexpr int kMaxU = SS_MAX_V / kUE;        // units per row at most (512)
-constexpr int kH = 1024;                     // patch hash slots
+constexpr int kH = 2048;                     // patch hash slots (LDS)
 constexpr int kProbe = 64;                   // longest probe sequence before giving up
 constexpr int kGH = 16384;                   // per-row patch table in global memory (LDS table overflow)
 constexpr int kGProbe = 1024;
@@ -56,7 +56,8 @@ constexpr uint32_t kLinear = 0xFFFFFFFFu;    // patched-list count meaning "look
 constexpr int kHCopies = 2;                  // privatised radix histograms
 constexpr int kHStride = 257;
 constexpr int kTS = SS_MAX_K / kBlock;       // selected elements per thread (16)
-constexpr int kGB = 8;                       // candidate groups loaded per thread per batch
+constexpr int kGT = 4096;                    // gather table entries (LDS)
+constexpr int kGS = 2048;                    // candidate groups staged in LDS per batch
 constexpr uint32_t kNoEmit = 0xFFFFFFFFu;    // threshold of a unit that emits nothing
 constexpr double kFix = 1125899906842624.0;  // 2^50: fixed-point scale of probability mass
 
@@ -199,6 +200,10 @@ struct Ctx {
   int nbias;
   const uint32_t* mask;
   float rep, freq, pres;
+  float tau, top_p, min_p;  // sampling parameters (tau 1 when the TEMP bit is off)
+  uint64_t seed;
+  int64_t pos;              // Philox position of this row
+  int dtok;                 // verification: draft token of this row (-1: none)
   bool greedy;
   bool kcap;
   int k_eff;
@@ -243,13 +248,20 @@ __device__ __forceinline__ Ctx make_ctx(const KArgs& a, int row) {
   c.rep = (m & SS_REP) ? a.rep[b] : 1.0f;
   c.freq = (m & SS_FREQ) ? a.freq[b] : 0.0f;
   c.pres = (m & SS_PRES) ? a.pres[b] : 0.0f;
+  c.tau = (m & SS_TEMP) ? a.temperature[b] : 1.0f;
+  c.top_p = (m & SS_TOPP) ? a.top_p[b] : 1.0f;
+  c.min_p = (m & SS_MINP) ? a.min_p[b] : 0.0f;
+  c.seed = a.seed ? a.seed[b] : 0ull;
+  c.pos = (a.position ? a.position[b] : 0) + c.ell;
+  c.dtok = -1;
+  if (a.op == OP_VERIFY && c.ell < a.L) c.dtok = a.draft_tokens[(size_t)b * a.L + c.ell];
   c.kcap = false;
   if (a.op == OP_TOPK) {
     c.greedy = false;
     int k = a.top_k ? a.top_k[b] : a.k_cap;
     c.k_eff = k < 0 ? 0 : (k > a.k_cap ? a.k_cap : k);
   } else {
-    c.greedy = (m & SS_GREEDY) || ((m & SS_TEMP) && a.temperature[b] <= 0.0f);
+    c.greedy = (m & SS_GREEDY) || ((m & SS_TEMP) && c.tau <= 0.0f);
     const int64_t kreq = ((m & SS_TOPK) && a.top_k[b] >= 1) ? (int64_t)a.top_k[b] : (int64_t)INT_MAX;
     c.k_eff = kreq < a.k_cap ? (int)kreq : a.k_cap;
     c.kcap = !c.greedy && kreq > a.k_cap;
@@ -556,20 +568,33 @@ struct MSmem {
   double bcd[4];
   int32_t closed[kWaves];
   uint32_t flagsw;  // bit 0: hash overflow
+  uint32_t pbits[512];  // filter: bit hbit(id) set for every patched id
   int32_t hk[kH];   // patched id (or -1)
   uint32_t hc[kH];  // occurrence count | has-bias bit 31
   uint32_t hf[kH];  // final key
+  uint16_t claim[kH];  // slots claimed by distinct ids, in claim order
+  uint32_t nclaim;
+  uint32_t gtab[kGT];  // candidate slot -> group offset in the row's regions
+  uint4 stg[kGS];      // candidate groups of the current batch
   uint32_t uoff[kMaxU + 1];
   uint32_t rmask[kMaxU / 32];  // units re-read by the slow path
-  uint32_t hist[2][kHCopies * kHStride];
+  alignas(16) uint32_t hist[2][(kHCopies * kHStride + 3) & ~3];  // rows 16-byte aligned (tie lists are read as uint4)
   uint32_t low[2][64];
   uint64_t mhist[256];
 };
 constexpr int kSmemFixed = (int)((sizeof(MSmem) + 15) & ~(size_t)15);
+// the largest merge footprint (sampling ops at k_max = SS_MAX_K) fits gfx950's 160 KiB of LDS
+static_assert(kSmemFixed + 8 * (2 * SS_MAX_K + 512) <= 160 * 1024, "merge LDS too large");
 
-__device__ __forceinline__ uint32_t hslot(int id) { return ((uint32_t)id * 2654435761u) >> 22; }  // 10 bits
-static_assert(kH == 1024, "hslot assumes 1024 slots");
+__device__ __forceinline__ uint32_t hslot(int id) { return ((uint32_t)id * 2654435761u) >> 21; }  // 11 bits
+static_assert(kH == 2048, "hslot assumes 2048 slots");
 
+__device__ __forceinline__ uint32_t hbit(int id) { return ((uint32_t)id * 0x9E3779B1u) >> 18; }  // 14 bits
+// false only when id is certainly not patched (one LDS read)
+__device__ __forceinline__ bool maybe_patched(const MSmem& S, int id) {
+  const uint32_t h = hbit(id);
+  return (S.pbits[h >> 5] >> (h & 31)) & 1u;
+}
 __device__ __forceinline__ int hfind(const MSmem& S, int id) {
   uint32_t s = hslot(id);
   for (int p = 0; p < kProbe; ++p) {
@@ -693,7 +718,7 @@ __device__ inline void radix_digit(const uint32_t* h, const uint32_t* low, int n
       s += v;
     }
     const uint32_t inc = wave_incl_scan(s);
-    const uint32_t total = __shfl(inc, 63, 64);
+    const uint32_t total = readlane_T(inc, 63);
     uint32_t run = inc - s;
     if (l == 0) {
       bc[0] = (uint32_t)nb;
@@ -794,7 +819,12 @@ __device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint3
     if (threadIdx.x < tot) {
       const uint32_t my = tl[threadIdx.x];
       uint32_t r = 0;
-      for (uint32_t j = 0; j < tot; ++j) r += tl[j] < my ? 1u : 0u;
+      const uint32_t tot4 = tot & ~3u;
+      for (uint32_t j = 0; j < tot4; j += 4) {  // four entries per LDS read
+        const uint4 q = *reinterpret_cast<const uint4*>(&tl[j]);
+        r += (q.x < my ? 1u : 0u) + (q.y < my ? 1u : 0u) + (q.z < my ? 1u : 0u) + (q.w < my ? 1u : 0u);
+      }
+      for (uint32_t j = tot4; j < tot; ++j) r += tl[j] < my ? 1u : 0u;
       if (r == want - 1u) S.bc[4] = my;
     }
     lds_barrier();
@@ -999,25 +1029,6 @@ __device__ __forceinline__ uint64_t cross_find(MSmem& S, const uint2* T, const u
   return r;
 }
 
-// ---------------------------------------------------------------------------
-// Candidate visitor.  Visits the row's candidate elements from global memory:
-// the groups of every unit not marked for re-reading (unit offsets in
-// S.uoff, flattened over 256 threads, located by binary search), every
-// element of the marked units (re-read from the logits with the grammar mask
-// applied), and the patched final values.  Raw copies of patched ids are
-// skipped.  f(key, idx) receives only valid keys.
-// ---------------------------------------------------------------------------
-template <int DT>
-__device__ __forceinline__ int unit_of_group(const MSmem& S, int U, uint32_t f) {
-  int lo = 0, hi = U - 1;  // largest u with uoff[u] <= f
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (S.uoff[mid] <= f) lo = mid;
-    else hi = mid - 1;
-  }
-  return lo;
-}
-
 // final key of a patched id found by a linear lookup in the row's lists
 template <int DT>
 __device__ __forceinline__ uint32_t lin_final(const KArgs& a, const Ctx& c, int id) {
@@ -1035,7 +1046,7 @@ __device__ __forceinline__ uint32_t lin_final(const KArgs& a, const Ctx& c, int 
 template <int DT>
 __device__ __forceinline__ bool is_patched(const Ctx& c, const MSmem& S, int pmode, const PatchG& g, int id) {
   if (pmode == 0) return false;
-  if (pmode == 1) return hfind(S, id) >= 0;
+  if (pmode == 1) return maybe_patched(S, id) && hfind(S, id) >= 0;
   if (pmode == 2) return gfind(g, id) >= 0;
   int cn;
   bool hb;
@@ -1043,19 +1054,84 @@ __device__ __forceinline__ bool is_patched(const Ctx& c, const MSmem& S, int pmo
   return lin_info(c, id, &cn, &hb, &bs);
 }
 
-template <int DT, typename F>
-__device__ __forceinline__ void visit_candidates(const KArgs& a, const Ctx& c, const MSmem& S, uint32_t NG, int nre,
-                                                 int pmode, const PatchG& pg, F&& f) {
+// ---------------------------------------------------------------------------
+// Exact slow path of the merge (candidate overflow, patch-table overflow,
+// skewed or heavily tied rows, patched top tokens).  It visits the row's
+// candidate elements from global memory: the groups of every unit not marked
+// for re-reading (located by binary search on the unit offsets), every
+// element of the marked units (re-read from the logits, grammar mask
+// applied) and the patched final values; raw copies of patched ids are
+// skipped.  Each visit applies one element-wise operation selected by an op
+// code, so a single out-of-line copy per element type serves every pass.
+// ---------------------------------------------------------------------------
+template <int DT>
+__device__ __forceinline__ int unit_of_group(const MSmem& S, int U, uint32_t f) {
+  int lo = 0, hi = U - 1;  // largest u with uoff[u] <= f
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (S.uoff[mid] <= f) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+enum { VOP_COUNT = 0, VOP_HKEY, VOP_COUNT_EQ, VOP_LIST_EQ, VOP_HIDX, VOP_COUNT_SEL, VOP_COLLECT };
+struct VOp {
+  int op;
+  uint32_t prefix, dm, lm, tk, ti, ip;
+  int sh, hs, ib;
+  uint32_t* hist;
+  uint32_t* low;
+  uint32_t* tl;
+  uint2* pool;
+};
+
+__device__ __forceinline__ void vop_apply(const VOp& o, uint32_t k, uint32_t i, uint32_t& acc, uint32_t& off) {
+  switch (o.op) {
+    case VOP_COUNT:
+      ++acc;
+      break;
+    case VOP_HKEY: {
+      const bool part = o.hs >= 32 || (k >> o.hs) == o.prefix;
+      const uint32_t d = (k >> o.sh) & o.dm;
+      hist_add(o.hist, d, part);
+      low_mark(o.low, d, part && (k & o.lm) != 0u);
+      break;
+    }
+    case VOP_COUNT_EQ:
+      acc += k == o.tk ? 1u : 0u;
+      break;
+    case VOP_LIST_EQ:
+      if (k == o.tk) o.tl[off++] = i;
+      break;
+    case VOP_HIDX:
+      hist_add(o.hist, (i >> o.ib) & o.dm, k == o.tk && (i >> o.hs) == o.ip);
+      break;
+    case VOP_COUNT_SEL:
+      acc += selected(k, i, o.tk, o.ti) ? 1u : 0u;
+      break;
+    default:  // VOP_COLLECT
+      if (selected(k, i, o.tk, o.ti)) o.pool[off++] = make_uint2(k, i);
+      break;
+  }
+}
+
+// visits every candidate element once; returns the op's per-thread count,
+// advances *off for the list-writing ops
+template <int DT>
+__device__ __forceinline__ uint32_t slow_visit(const KArgs& a, const Ctx& c, const MSmem& S, uint32_t NG, int nre,
+                                            int pmode, const PatchG& pg, const VOp& o, uint32_t* offp) {
   constexpr int GE = DTT<DT>::GE, VW = DTT<DT>::VW;
   const int tid = threadIdx.x;
   const int U = a.U;
   const uint4* rc = a.cand + (size_t)c.row * U * a.cap;
+  uint32_t acc = 0u, off = offp ? *offp : 0u;
   // 1. groups of the units that are not re-read
-  for (uint32_t f0 = 0; f0 < NG; f0 += kBlock * kGB) {
-    uint4 g[kGB];
-    bool ok[kGB];
+  for (uint32_t f0 = 0; f0 < NG; f0 += kBlock * 4) {
+    uint4 g[4];
+    bool ok[4];
 #pragma unroll
-    for (int m = 0; m < kGB; ++m) {
+    for (int m = 0; m < 4; ++m) {
       const uint32_t fi = f0 + (uint32_t)(tid + m * kBlock);
       ok[m] = false;
       g[m] = make_uint4(0u, 0u, 0u, 0u);
@@ -1068,7 +1144,7 @@ __device__ __forceinline__ void visit_candidates(const KArgs& a, const Ctx& c, c
       }
     }
 #pragma unroll
-    for (int m = 0; m < kGB; ++m) {
+    for (int m = 0; m < 4; ++m) {
       if (!ok[m]) continue;
 #pragma unroll
       for (int e = 0; e < GE; ++e) {
@@ -1076,7 +1152,7 @@ __device__ __forceinline__ void visit_candidates(const KArgs& a, const Ctx& c, c
         if constexpr (DT == SS_BF16) k = (((e < 2 ? g[m].y : g[m].z) >> (16 * (e & 1))) & 0xFFFFu) << 16;
         else k = e ? g[m].z : g[m].y;
         const uint32_t i = g[m].x + (uint32_t)e;
-        if (k >= kKeyFloor && !is_patched<DT>(c, S, pmode, pg, (int)i)) f(k, i);
+        if (k >= kKeyFloor && !is_patched<DT>(c, S, pmode, pg, (int)i)) vop_apply(o, k, i, acc, off);
       }
     }
   }
@@ -1097,21 +1173,22 @@ __device__ __forceinline__ void visit_candidates(const KArgs& a, const Ctx& c, c
           if (i >= a.V) break;
           uint32_t k = fold_nan(key_raw(load_elem_bits<DT>(c.xrow, i)));
           if (!((mwd >> e) & 1u)) k = 0u;
-          if (k >= kKeyFloor && !is_patched<DT>(c, S, pmode, pg, i)) f(k, (uint32_t)i);
+          if (k >= kKeyFloor && !is_patched<DT>(c, S, pmode, pg, i)) vop_apply(o, k, (uint32_t)i, acc, off);
         }
       }
     }
   }
   // 3. patched final values
   if (pmode == 1) {
-    for (int s = tid; s < kH; s += kBlock) {
-      const int id = S.hk[s];
-      if (id >= 0 && S.hf[s] >= kKeyFloor) f(S.hf[s], (uint32_t)id);
+    const uint32_t ncl = S.nclaim;
+    for (uint32_t j = tid; j < ncl; j += kBlock) {
+      const uint32_t sl = S.claim[j];
+      if (S.hf[sl] >= kKeyFloor) vop_apply(o, S.hf[sl], (uint32_t)S.hk[sl], acc, off);
     }
   } else if (pmode == 2) {
     for (int s = tid; s < kGH; s += kBlock) {
       const uint64_t t = pg.tag[s];
-      if ((uint32_t)(t >> 32) == pg.gen && pg.fin[s] >= kKeyFloor) f(pg.fin[s], (uint32_t)t - 1u);
+      if ((uint32_t)(t >> 32) == pg.gen && pg.fin[s] >= kKeyFloor) vop_apply(o, pg.fin[s], (uint32_t)t - 1u, acc, off);
     }
   } else if (pmode == 3) {
     const int ne = c.nhist + c.nextra + c.nbias;
@@ -1122,94 +1199,289 @@ __device__ __forceinline__ void visit_candidates(const KArgs& a, const Ctx& c, c
       for (int e2 = 0; e2 < e && first; ++e2) first = lin_entry(c, e2) != id;
       if (!first) continue;
       const uint32_t k = lin_final<DT>(a, c, id);
-      if (k >= kKeyFloor) f(k, (uint32_t)id);
+      if (k >= kKeyFloor) vop_apply(o, k, (uint32_t)id, acc, off);
     }
   }
+  if (offp) *offp = off;
+  return acc;
 }
 
+// Exact selection of the `want` largest composites (key desc, index asc)
+// among the n_valid valid candidate elements, by the same digit passes as
+// radix_select, each pass one slow_visit.
+template <int DT>
+__device__ __forceinline__ void slow_radix(const KArgs& a, const Ctx& c, MSmem& S, uint32_t NG, int nre, int pmode,
+                                        const PatchG& pg, uint32_t want, uint32_t n_valid, uint32_t* tk_out,
+                                        uint32_t* ti_out) {
+  VOp o = {};
+  int cur = 0;
+  int sh = 32;
+  uint32_t prefix = 0u;
+  uint32_t tk = 0xFFFFFFFFu, ti = 0xFFFFFFFFu;
+  uint32_t n_tie = n_valid;
+  bool ties = true;
+  radix_clear(S, 0);
+  lds_barrier();
+  if (want >= n_valid) {
+    tk = kKeyNegInf;
+    ties = false;
+    sh = 0;
+  }
+  while (sh > 0) {
+    const int w = sh < 8 ? sh : 8;
+    sh -= w;
+    o.op = VOP_HKEY;
+    o.sh = sh;
+    o.hs = sh + w;
+    o.dm = (1u << w) - 1u;
+    o.lm = (1u << sh) - 1u;
+    o.prefix = prefix;
+    o.hist = S.hist[cur];
+    o.low = S.low[cur];
+    slow_visit<DT>(a, c, S, NG, nre, pmode, pg, o, nullptr);
+    radix_clear(S, cur ^ 1);
+    lds_barrier();
+    radix_digit(S.hist[cur], S.low[cur], (int)o.dm + 1, want, true, S.bc);
+    const uint32_t d = S.bc[0], above = S.bc[1], hd = S.bc[2], lowd = S.bc[3];
+    cur ^= 1;
+    if (d > o.dm) {
+      tk = kKeyNegInf;
+      ti = 0xFFFFFFFFu;
+      ties = false;
+      break;
+    }
+    prefix = (prefix << w) | d;
+    want -= above;
+    if (hd == want) {
+      tk = prefix << sh;
+      ti = 0xFFFFFFFFu;
+      ties = false;
+      break;
+    }
+    if (sh == 0 || lowd == 0u) {
+      tk = prefix << sh;
+      n_tie = hd;
+      break;
+    }
+  }
+  if (ties && n_tie <= (uint32_t)kBlock) {
+    o.op = VOP_COUNT_EQ;
+    o.tk = tk;
+    const uint32_t cnt = slow_visit<DT>(a, c, S, NG, nre, pmode, pg, o, nullptr);
+    uint32_t tot;
+    uint32_t off = block_excl_scan(cnt, S.r32, tot);
+    o.op = VOP_LIST_EQ;
+    o.tl = S.hist[cur];
+    slow_visit<DT>(a, c, S, NG, nre, pmode, pg, o, &off);
+    lds_barrier();
+    if (threadIdx.x < tot) {
+      const uint32_t my = o.tl[threadIdx.x];
+      uint32_t r = 0;
+      const uint32_t tot4 = tot & ~3u;
+      for (uint32_t j = 0; j < tot4; j += 4) {  // four entries per LDS read
+        const uint4 q = *reinterpret_cast<const uint4*>(&o.tl[j]);
+        r += (q.x < my ? 1u : 0u) + (q.y < my ? 1u : 0u) + (q.z < my ? 1u : 0u) + (q.w < my ? 1u : 0u);
+      }
+      for (uint32_t j = tot4; j < tot; ++j) r += o.tl[j] < my ? 1u : 0u;
+      if (r == want - 1u) S.bc[4] = my;
+    }
+    lds_barrier();
+    ti = S.bc[4];
+    lds_barrier();
+  } else if (ties) {
+    int ib = 32 - __clz((uint32_t)(a.V > 1 ? a.V - 1 : 1));
+    uint32_t ip = 0u;
+    while (ib > 0) {
+      const int w = ib < 8 ? ib : 8;
+      ib -= w;
+      o.op = VOP_HIDX;
+      o.tk = tk;
+      o.ib = ib;
+      o.hs = ib + w;
+      o.dm = (1u << w) - 1u;
+      o.ip = ip;
+      o.hist = S.hist[cur];
+      slow_visit<DT>(a, c, S, NG, nre, pmode, pg, o, nullptr);
+      radix_clear(S, cur ^ 1);
+      lds_barrier();
+      radix_digit(S.hist[cur], nullptr, (int)o.dm + 1, want, false, S.bc);
+      const uint32_t d = S.bc[0], below = S.bc[1], hd = S.bc[2];
+      cur ^= 1;
+      ip = (ip << w) | (d & o.dm);
+      want -= below;
+      if (hd == want) {
+        ti = (ip << ib) | ((1u << ib) - 1u);
+        break;
+      }
+      if (ib == 0) ti = ip;
+    }
+  }
+  *tk_out = tk;
+  *ti_out = ti;
+}
 
+// v0 = the want-th largest element among those the units emitted; every
+// unit whose threshold lies above v0 (or whose candidate list overflowed)
+// may hide a top-k element and is re-read whole; the exact top-k of the
+// result is written to pool[0, n).
+template <int DT>
+__device__ __forceinline__ int slow_select(const KArgs& a, const Ctx& c, MSmem& S, uint2* pool, uint32_t NG, int pmode,
+                                        const PatchG& pg, int want, uint32_t* tk_out, uint32_t* ti_out) {
+  const int tid = threadIdx.x;
+  const int U = a.U;
+  const int row = c.row;
+  uint32_t tk = 0u, ti = 0u;
+  int nT = 0;
+  VOp o = {};
+  o.op = VOP_COUNT;
+  uint32_t nv = slow_visit<DT>(a, c, S, NG, 0, pmode, pg, o, nullptr);
+  nv = block_sum(nv, S.r32);
+  uint32_t v0 = kKeyFloor;
+  if (nv >= (uint32_t)want) {
+    uint32_t i0;
+    slow_radix<DT>(a, c, S, NG, 0, pmode, pg, (uint32_t)want, nv, &v0, &i0);
+  }
+  for (int u = tid; u < U; u += kBlock) {
+    const uint32_t tu = a.rec[(size_t)row * U + u].x;
+    if (tu != kNoEmit && tu > v0) atomicOr(&S.rmask[u >> 5], 1u << (u & 31));
+  }
+  lds_barrier();
+  int nre = 0;
+  for (int w = 0; w < kMaxU / 32; ++w) nre += __popc(S.rmask[w]);
+  o.op = VOP_COUNT;
+  uint32_t nx = slow_visit<DT>(a, c, S, NG, nre, pmode, pg, o, nullptr);
+  nx = block_sum(nx, S.r32);
+  if (want > (int)nx) want = (int)nx;
+  if (want > 0) {
+    slow_radix<DT>(a, c, S, NG, nre, pmode, pg, (uint32_t)want, nx, &tk, &ti);
+    o.op = VOP_COUNT_SEL;
+    o.tk = tk;
+    o.ti = ti;
+    const uint32_t cl = slow_visit<DT>(a, c, S, NG, nre, pmode, pg, o, nullptr);
+    uint32_t tot;
+    uint32_t off = block_excl_scan(cl, S.r32, tot);
+    o.op = VOP_COLLECT;
+    o.pool = pool;
+    slow_visit<DT>(a, c, S, NG, nre, pmode, pg, o, &off);
+    nT = (int)tot;
+    lds_barrier();
+  }
+  *tk_out = tk;
+  *ti_out = ti;
+  return nT;
+}
+
+// ---------------------------------------------------------------------------
 // Fast-path pool: every candidate element at or above tmax (raw copies of
 // patched ids dropped) plus the patched final values at or above it, in a
-// deterministic order (batches of kGB groups per thread, block-scan offsets).
+// deterministic order (batches staged in LDS, block-scan offsets).
 // Returns the element count (elements beyond a.pcap are counted, not stored).
 template <int DT>
-__device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MSmem& S, uint32_t NG, bool patch, uint32_t tmax,
-                                uint2* pool, uint32_t& pmax_out) {
+__device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MSmem& S, uint32_t NG, bool patch,
+                                                uint32_t tmax, uint2* pool, uint32_t& nvalid_out) {
   constexpr int GE = DTT<DT>::GE;
   const int tid = threadIdx.x;
   const int U = a.U;
   const uint4* rc = a.cand + (size_t)c.row * U * a.cap;
   const uint32_t pcap = (uint32_t)a.pcap;
-  uint32_t base = 0u, pmax = 0u;
-  for (uint32_t f0 = 0; f0 < NG; f0 += kBlock * kGB) {
-    uint4 g[kGB];
-#pragma unroll
-    for (int m = 0; m < kGB; ++m) {
-      const uint32_t fi = f0 + (uint32_t)(tid + m * kBlock);
-      g[m] = make_uint4(0u, 0u, 0u, 0u);
-      if (fi < NG) {
-        const int u = unit_of_group<DT>(S, U, fi);
-        g[m] = rc[(size_t)u * a.cap + (fi - S.uoff[u])];
+  // patched final values at or above tmax go first
+  uint32_t base = 0u;
+  if (patch) {
+    uint32_t cnt = 0u;
+    const uint32_t ncl = S.nclaim;
+    for (uint32_t j = tid; j < ncl; j += kBlock) {
+      const uint32_t k = S.hf[S.claim[j]];
+      cnt += (k >= tmax && k >= kKeyFloor) ? 1u : 0u;
+    }
+    uint32_t tot;
+    uint32_t off = block_excl_scan(cnt, S.r32, tot);
+    for (uint32_t j = tid; j < ncl; j += kBlock) {
+      const uint32_t sl = S.claim[j];
+      const uint32_t k = S.hf[sl];
+      if (k >= tmax && k >= kKeyFloor) {
+        if (off < pcap) pool[off] = make_uint2(k, (uint32_t)S.hk[sl]);
+        ++off;
       }
     }
-    uint32_t keep = 0u, cnt = 0u;
+    base = tot;
+  }
+  // slot -> offset table, TPU threads per unit
+  const bool table = NG <= (uint32_t)kGT;
+  if (table) {
+    const int TPU = U >= kBlock ? 1 : kBlock / U;
+    for (int x = tid; x < U * TPU; x += kBlock) {
+      const int u = x / TPU, sub = x - u * TPU;
+      const uint32_t o = S.uoff[u], n = S.uoff[u + 1] - o;
+      for (uint32_t j = (uint32_t)sub; j < n; j += (uint32_t)TPU) S.gtab[o + j] = (uint32_t)u * a.cap + j;
+    }
+    lds_barrier();
+  }
+  auto key_of = [](const uint4& gq, int e) -> uint32_t {
+    if constexpr (DT == SS_BF16) return (((e < 2 ? gq.y : gq.z) >> (16 * (e & 1))) & 0xFFFFu) << 16;
+    else return e ? gq.z : gq.y;
+  };
+  uint32_t ninv = 0u;
+  constexpr int kPer = kGS / kBlock;
+  for (uint32_t f0 = 0; f0 < NG; f0 += (uint32_t)kGS) {
+    const uint32_t nb = min((uint32_t)kGS, NG - f0);
+    // offsets, then every load of the batch in flight, then staged in LDS
+    uint32_t go[kPer];
 #pragma unroll
-    for (int m = 0; m < kGB; ++m) {
+    for (int m = 0; m < kPer; ++m) {
+      const uint32_t q = (uint32_t)(tid + m * kBlock);
+      go[m] = 0xFFFFFFFFu;
+      if (q < nb) {
+        if (table) {
+          go[m] = S.gtab[f0 + q];
+        } else {
+          const int u = unit_of_group<DT>(S, U, f0 + q);
+          go[m] = (uint32_t)u * a.cap + (f0 + q - S.uoff[u]);
+        }
+      }
+    }
+    uint4 g[kPer];
+#pragma unroll
+    for (int m = 0; m < kPer; ++m) g[m] = rc[go[m] == 0xFFFFFFFFu ? 0u : go[m]];
+#pragma unroll
+    for (int m = 0; m < kPer; ++m)
+      if (go[m] != 0xFFFFFFFFu) S.stg[tid + m * kBlock] = g[m];
+    lds_barrier();
+    uint32_t cnt = 0u;
+    for (uint32_t q = (uint32_t)tid; q < nb; q += kBlock) {
+      const uint4 gq = S.stg[q];
 #pragma unroll
       for (int e = 0; e < GE; ++e) {
-        uint32_t k;
-        if constexpr (DT == SS_BF16) k = (((e < 2 ? g[m].y : g[m].z) >> (16 * (e & 1))) & 0xFFFFu) << 16;
-        else k = e ? g[m].z : g[m].y;
-        const uint32_t i = g[m].x + (uint32_t)e;
-        if (k >= tmax && k >= kKeyFloor && !(patch && hfind(S, (int)i) >= 0)) {
-          keep |= 1u << (m * GE + e);
-          ++cnt;
-          pmax = max(pmax, k);
-        }
+        const uint32_t k = key_of(gq, e);
+        cnt += (k >= tmax && k >= kKeyFloor) ? 1u : 0u;
       }
     }
     uint32_t tot;
     uint32_t off = base + block_excl_scan(cnt, S.r32, tot);
-#pragma unroll
-    for (int m = 0; m < kGB; ++m) {
+    for (uint32_t q = (uint32_t)tid; q < nb; q += kBlock) {
+      const uint4 gq = S.stg[q];
 #pragma unroll
       for (int e = 0; e < GE; ++e) {
-        if ((keep >> (m * GE + e)) & 1u) {
-          uint32_t k;
-          if constexpr (DT == SS_BF16) k = (((e < 2 ? g[m].y : g[m].z) >> (16 * (e & 1))) & 0xFFFFu) << 16;
-          else k = e ? g[m].z : g[m].y;
-          if (off < pcap) pool[off] = make_uint2(k, g[m].x + (uint32_t)e);
+        uint32_t k = key_of(gq, e);
+        if (k >= tmax && k >= kKeyFloor) {
+          const uint32_t id = gq.x + (uint32_t)e;
+          // raw copy of a patched id: kept invalid (its final value is above)
+          if (patch && maybe_patched(S, (int)id) && hfind(S, (int)id) >= 0) {
+            k = 0u;
+            ++ninv;
+          }
+          if (off < pcap) pool[off] = make_uint2(k, id);
           ++off;
         }
       }
     }
     base += tot;
+    lds_barrier();  // the staging area is refilled by the next batch
   }
-  if (patch) {
-    uint32_t cnt = 0u;
-    for (int s = tid; s < kH; s += kBlock) {
-      const uint32_t k = S.hf[s];
-      if (S.hk[s] >= 0 && k >= tmax && k >= kKeyFloor) {
-        ++cnt;
-        pmax = max(pmax, k);
-      }
-    }
-    uint32_t tot;
-    uint32_t off = base + block_excl_scan(cnt, S.r32, tot);
-    for (int s = tid; s < kH; s += kBlock) {
-      const uint32_t k = S.hf[s];
-      if (S.hk[s] >= 0 && k >= tmax && k >= kKeyFloor) {
-        if (off < pcap) pool[off] = make_uint2(k, (uint32_t)S.hk[s]);
-        ++off;
-      }
-    }
-    base += tot;
-  }
-  pmax_out = block_max(pmax, S.r32);  // its barriers publish the pool
+  nvalid_out = base - (patch ? block_sum(ninv, S.r32) : 0u);
   return base;
 }
 
-
+// ---------------------------------------------------------------------------
 // In-place stable compaction of pool[0, n) to the elements satisfying
 // pred, in rounds of 4 * kBlock: a round writes only below its own first
 // unread index, so no element is overwritten before it is read.
@@ -1242,62 +1514,6 @@ __device__ __forceinline__ uint32_t compact_pool(MSmem& S, uint2* pool, int n, P
 
 
 // ---------------------------------------------------------------------------
-// Exact slow path of the merge (candidate overflow, patch-table overflow,
-// skewed or heavily tied rows, patched top tokens): v0 = the want-th largest
-// element among those the units emitted; every unit whose threshold lies
-// above v0 (or whose candidate list overflowed) may hide a top-k element and
-// is re-read whole; the exact top-k of the result is written to pool[0, n).
-// Kept out of line: it is rare, and one copy per element type serves every
-// operation.
-// ---------------------------------------------------------------------------
-template <int DT>
-__device__ __noinline__ int slow_select(const KArgs& a, const Ctx& c, MSmem& S, uint2* pool, uint32_t NG, int pmode,
-                                        const PatchG& pg, int want, uint32_t* tk_out, uint32_t* ti_out) {
-  const int tid = threadIdx.x;
-  const int U = a.U;
-  const int row = c.row;
-  uint32_t tk = 0u, ti = 0u;
-  int nT = 0;
-  uint32_t nv = 0u;
-  visit_candidates<DT>(a, c, S, NG, 0, pmode, pg, [&](uint32_t, uint32_t) { ++nv; });
-  nv = block_sum(nv, S.r32);
-  uint32_t v0 = kKeyFloor;
-  if (nv >= (uint32_t)want) {
-    uint32_t t0, i0;
-    radix_select([&](auto&& f) { visit_candidates<DT>(a, c, S, NG, 0, pmode, pg, f); }, (uint32_t)want, nv,
-                 kKeyFloor, 0xFFFFFFFFu, a.V, S, &t0, &i0);
-    v0 = t0;
-  }
-  int nre = 0;
-  for (int u = tid; u < U; u += kBlock) {
-    const uint32_t tu = a.rec[(size_t)row * U + u].x;
-    if (tu != kNoEmit && tu > v0) atomicOr(&S.rmask[u >> 5], 1u << (u & 31));
-  }
-  lds_barrier();
-  for (int w = 0; w < kMaxU / 32; ++w) nre += __popc(S.rmask[w]);
-  // a unit that overflowed has only part of its groups: re-read it whole
-  uint32_t nx = 0u;
-  visit_candidates<DT>(a, c, S, NG, nre, pmode, pg, [&](uint32_t, uint32_t) { ++nx; });
-  nx = block_sum(nx, S.r32);
-  if (want > (int)nx) want = (int)nx;
-  if (want > 0) {
-    radix_select([&](auto&& f) { visit_candidates<DT>(a, c, S, NG, nre, pmode, pg, f); }, (uint32_t)want, nx,
-                 kKeyFloor, 0xFFFFFFFFu, a.V, S, &tk, &ti);
-    uint32_t cl = 0u;
-    visit_candidates<DT>(a, c, S, NG, nre, pmode, pg, [&](uint32_t k, uint32_t i) { cl += selected(k, i, tk, ti); });
-    uint32_t tot;
-    uint32_t off = block_excl_scan(cl, S.r32, tot);
-    visit_candidates<DT>(a, c, S, NG, nre, pmode, pg, [&](uint32_t k, uint32_t i) {
-      if (selected(k, i, tk, ti)) pool[off++] = make_uint2(k, i);
-    });
-    nT = (int)tot;
-  }
-  *tk_out = tk;
-  *ti_out = ti;
-  return nT;
-}
-
-// ---------------------------------------------------------------------------
 // Row merge: the whole workgroup, after the row's last unit was written.
 // ---------------------------------------------------------------------------
 template <int DT, int OP>
@@ -1309,6 +1525,15 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   const int U = a.U;
   const uint32_t cap = (uint32_t)a.cap;
 
+  // history ids (first 4 * kBlock) are loaded up front, next to the records
+  int hid0[4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const int h = tid + m * kBlock;
+    hid0[m] = h < c.nhist ? c.hist[h] : -1;
+  }
+  const int bid0 = tid < c.nbias ? c.bias_ids[tid] : -1;
+  const float bval0 = tid < c.nbias ? c.bias_vals[tid] : 0.0f;
   // 1. unit records: largest threshold, row maximum, candidate offsets
   uint32_t hi = 0u, tmax = 0u, ovf = 0u;
   uint32_t NG = 0u;
@@ -1349,48 +1574,58 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   pg.fin = a.gfin + (size_t)row * kGH;
   pg.gen = 0u;
   const int Wm = (a.V + 31) >> 5;
+  uint32_t hfmax = 0u;  // largest patched final key (LDS mode)
   if (patch) {
-    for (int s = tid; s < kH; s += kBlock) {
-      S.hk[s] = -1;
-      S.hc[s] = 0u;
+    for (int s = tid; s < kH / 4; s += kBlock) {
+      reinterpret_cast<int4*>(S.hk)[s] = make_int4(-1, -1, -1, -1);
+      reinterpret_cast<uint4*>(S.hc)[s] = make_uint4(0u, 0u, 0u, 0u);
     }
+    for (int s = tid; s < 512 / 4; s += kBlock) reinterpret_cast<uint4*>(S.pbits)[s] = make_uint4(0u, 0u, 0u, 0u);
+    if (tid == 0) S.nclaim = 0u;
     lds_barrier();
-    auto ins = [&](int id, uint32_t addc, uint32_t orb) {
+    // bias entries record their value in hf[] (the final key is written
+    // later); a second entry for the same id sets the "duplicate" bit and the
+    // finals then sum that id's entries in list order
+    auto ins = [&](int id, uint32_t addc, bool bias, float bval) {
       if (id < 0 || id >= a.V) return;
+      const uint32_t hb2 = hbit(id);
+      atomicOr(&S.pbits[hb2 >> 5], 1u << (hb2 & 31));
       uint32_t s = hslot(id);
       for (int p = 0; p < kProbe; ++p) {
         const int old = atomicCAS(&S.hk[s], -1, id);
         if (old == -1 || old == id) {
+          if (old == -1) S.claim[atomicAdd(&S.nclaim, 1u)] = (uint16_t)s;
           if (addc) atomicAdd(&S.hc[s], addc);
-          if (orb) atomicOr(&S.hc[s], orb);
+          if (bias) {
+            const uint32_t prev = atomicOr(&S.hc[s], 0x80000000u);
+            if (prev & 0x80000000u) atomicOr(&S.hc[s], 0x40000000u);
+            else S.hf[s] = __float_as_uint(bval);
+          }
           return;
         }
         s = (s + 1) & (kH - 1);
       }
       S.flagsw = 1u;
     };
-    for (int h0 = 0; h0 < c.nhist; h0 += 4 * kBlock) {
-      int id[4];
 #pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const int h = h0 + tid + m * kBlock;
-        id[m] = h < c.nhist ? c.hist[h] : -1;
-      }
-#pragma unroll
-      for (int m = 0; m < 4; ++m) ins(id[m], 1u, 0u);
-    }
-    for (int h = tid; h < c.nextra; h += kBlock) ins(c.extra[h], 1u, 0u);
-    for (int e = tid; e < c.nbias; e += kBlock) ins(c.bias_ids[e], 0u, 0x80000000u);
+    for (int m = 0; m < 4; ++m) ins(hid0[m], 1u, false, 0.0f);
+    for (int h = tid + 4 * kBlock; h < c.nhist; h += kBlock) ins(c.hist[h], 1u, false, 0.0f);  // long histories
+    for (int h = tid; h < c.nextra; h += kBlock) ins(c.extra[h], 1u, false, 0.0f);
+    ins(bid0, 0u, true, bval0);
+    for (int e = tid + kBlock; e < c.nbias; e += kBlock) ins(c.bias_ids[e], 0u, true, c.bias_vals[e]);
     __syncthreads();
     if (S.flagsw == 0u) {
       pmode = 1;
+      const uint32_t ncl = S.nclaim;
 #pragma unroll 1
-      for (int s0 = 0; s0 < kH; s0 += 4 * kBlock) {
-        int id[4];
+      for (uint32_t j0 = 0; j0 < ncl; j0 += 4 * kBlock) {
+        int id[4], sl[4];
         uint32_t bits[4], mw[4];
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
-          id[m] = S.hk[s0 + tid + m * kBlock];
+          const uint32_t j = j0 + tid + m * kBlock;
+          sl[m] = j < ncl ? (int)S.claim[j] : -1;
+          id[m] = sl[m] >= 0 ? S.hk[sl[m]] : -1;
           bits[m] = 0u;
           mw[m] = 0xFFFFFFFFu;
           if (id[m] >= 0) {
@@ -1400,22 +1635,27 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
         }
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
-          const int s = s0 + tid + m * kBlock;
           if (id[m] < 0) continue;
+          const int s = sl[m];
           const uint32_t hcv = S.hc[s];
           const bool hb = (hcv >> 31) != 0u;
           float bsum = 0.0f;
           if (hb) {
-            for (int e = 0; e < c.nbias; ++e)
-              if (c.bias_ids[e] == id[m]) bsum = bsum + c.bias_vals[e];
+            if (hcv & 0x40000000u) {  // duplicate bias ids: list order
+              for (int e = 0; e < c.nbias; ++e)
+                if (c.bias_ids[e] == id[m]) bsum = bsum + c.bias_vals[e];
+            } else {
+              bsum = 0.0f + __uint_as_float(S.hf[s]);
+            }
           }
           uint32_t k = 0u;
           if ((mw[m] >> (id[m] & 31)) & 1u)
-            k = fold_nan(penalised_key(bits[m], c.mode, c.rep, c.freq, c.pres, (int)(hcv & 0x7FFFFFFFu), hb, bsum));
+            k = fold_nan(penalised_key(bits[m], c.mode, c.rep, c.freq, c.pres, (int)(hcv & 0x3FFFFFFFu), hb, bsum));
           S.hf[s] = k;
+          hfmax = max(hfmax, k);
         }
       }
-      lds_barrier();
+      hfmax = block_max(hfmax, S.r32);
     } else {
       // more distinct ids than the LDS table holds: the row's table in global memory
       if (tid == 0) {
@@ -1479,20 +1719,25 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   uint32_t plo = tmax, phi = hi;
   if (!empty && want > 0) {
     uint32_t C = 0u;
+    uint32_t Cv = 0u;  // valid pool elements (C less the invalidated raw copies)
     if (!slow) {
-      uint32_t pmax = 0u;
-      C = gather_pool<DT>(a, c, S, NG, pmode == 1, tmax, pool, pmax);
-      if ((int)C > a.pcap || (int)C < want) {
-        slow = true;
-      } else {
-        phi = pmax;
-      }
+      C = gather_pool<DT>(a, c, S, NG, pmode == 1, tmax, pool, Cv);
+      if ((int)C > a.pcap || (int)Cv < want) slow = true;
+      phi = max(hi, hfmax);  // every pool key lies in [tmax, phi]
     }
-    if (!slow) {
+    if (!slow && want == 1) {  // greedy: the pool maximum
+      uint64_t mc = 0ull;
+      for (int i = tid; i < (int)C; i += kBlock)
+        if (pool[i].x >= kKeyFloor) mc = max(mc, comp_of(pool[i].x, pool[i].y));
+      mc = block_max(mc, S.r64);
+      if (tid == 0) pool[0] = make_uint2(comp_key(mc), comp_idx(mc));
+      lds_barrier();
+      nT = 1;
+    } else if (!slow) {
       auto visit_pool = [&](auto&& f) {
         for (int i = tid; i < (int)C; i += kBlock) f(pool[i].x, pool[i].y);
       };
-      radix_select(visit_pool, (uint32_t)want, C, plo, phi, a.V, S, &tk, &ti);
+      radix_select(visit_pool, (uint32_t)want, Cv, plo, phi, a.V, S, &tk, &ti);
       nT = (int)compact_pool(S, pool, (int)C, [&](uint2 e) { return selected(e.x, e.y, tk, ti); });
     } else {
       flags |= SS_FLAG_FALLBACK;
@@ -1546,26 +1791,25 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
     int token = -1;
     float logprob = 0.0f;
     int accept = 0;
-    const int64_t pos = a.position ? a.position[b] + c.ell : (int64_t)c.ell;
-    const uint64_t seed = a.seed ? a.seed[b] : 0ull;
+    const int64_t pos = c.pos;
+    const uint64_t seed = c.seed;
     bool has_draft = false;
     int dtok = -1;
     if constexpr (OP == OP_VERIFY) {
       if (c.ell < a.L) {
-        dtok = a.draft_tokens[(size_t)b * a.L + c.ell];
+        dtok = c.dtok;
         has_draft = dtok >= 0 && dtok < a.V;
       }
     }
     if (OP == OP_PROCESS && a.patched && tid == 0) a.npatched[row] = 0u;
     if (OP == OP_PROCESS && pmode == 1) {
       // (id, final key) list for the materialising pass
-      uint32_t cnt = 0u;
-      for (int s = tid; s < kH; s += kBlock) cnt += S.hk[s] >= 0 ? 1u : 0u;
-      uint32_t tot;
-      uint32_t off = block_excl_scan(cnt, S.r32, tot);
-      for (int s = tid; s < kH; s += kBlock)
-        if (S.hk[s] >= 0) a.patched[(size_t)row * kGH + off++] = make_uint2((uint32_t)S.hk[s], S.hf[s]);
-      if (tid == 0) a.npatched[row] = tot;
+      const uint32_t ncl = S.nclaim;
+      for (uint32_t j = tid; j < ncl; j += kBlock) {
+        const uint32_t sl = S.claim[j];
+        a.patched[(size_t)row * kGH + j] = make_uint2((uint32_t)S.hk[sl], S.hf[sl]);
+      }
+      if (tid == 0) a.npatched[row] = ncl;
     } else if (OP == OP_PROCESS && pmode == 2) {
       uint32_t cnt = 0u;
       for (int s = tid; s < kGH; s += kBlock) cnt += (uint32_t)(pg.tag[s] >> 32) == pg.gen ? 1u : 0u;
@@ -1605,10 +1849,10 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
     } else if (!none) {
       // ---- truncation and selection epilogue (Alg. 11 order) on T = pool[0, nT)
       const double M = (double)float_of_key(comp_key(Mcomp));
-      const double tau = (c.mode & SS_TEMP) ? (double)a.temperature[b] : 1.0;
-      const bool minp = (c.mode & SS_MINP) && a.min_p[b] > 0.0f;
-      const bool topp = (c.mode & SS_TOPP) && a.top_p[b] < 1.0f;
-      const double lt = minp ? log((double)a.min_p[b]) : 0.0;
+      const double tau = (double)c.tau;
+      const bool minp = (c.mode & SS_MINP) && c.min_p > 0.0f;
+      const bool topp = (c.mode & SS_TOPP) && c.top_p < 1.0f;
+      const double lt = minp ? log((double)c.min_p) : 0.0;
       // weights of T in 2^-50 fixed point, stored behind T in the pool region
       uint64_t* Wl = reinterpret_cast<uint64_t*>(pool) + a.pcap / 2;
       const int MT = (nT + kBlock - 1) / kBlock;
@@ -1635,7 +1879,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
       // top-p boundary: first element whose running mass reaches p * Z_k
       uint64_t ep = 0ull;
       if (topp)
-        ep = cross_find(S, pool, Wl, nT, inT, (double)a.top_p[b] * (double)Zk, false, kmin, comp_key(Mcomp), a.V);
+        ep = cross_find(S, pool, Wl, nT, inT, (double)c.top_p * (double)Zk, false, kmin, comp_key(Mcomp), a.V);
       // kept set S = T, min-p survivors, canonical prefix up to ep
       uint32_t inS = 0u;
       uint64_t zs = 0ull, lastc = ~0ull;
@@ -1814,7 +2058,13 @@ __global__ __launch_bounds__(kBlock) void ss_merge_kernel(KArgs a) {
   uint2* pool = reinterpret_cast<uint2*>(smem_raw + kSmemFixed);
   if (threadIdx.x < kMaxU / 32) S.rmask[threadIdx.x] = 0u;
   __syncthreads();
-  merge_row<DT, OP>(a, blockIdx.x, S, pool);
+  // The streaming kernel placed row r's units on XCD floor(8 r / rows) when
+  // its grid splits evenly over the 8 XCDs; the same remap here runs the
+  // row's merge on that XCD, whose L2 still holds the row's candidates.
+  int row = blockIdx.x;
+  const int nunits = a.rows * a.U;
+  if ((a.rows & 7) == 0 && (nunits & 31) == 0) row = (row & 7) * (a.rows >> 3) + (row >> 3);
+  merge_row<DT, OP>(a, row, S, pool);
 }
 
 // Verification assembly: per request, the accepted drafts, then the first
