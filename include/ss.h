@@ -193,13 +193,16 @@ ss_status ss_process_logits(const void *logits, int dtype, int64_t ld, const ss_
                             size_t ws_bytes, void *stream);
 
 /*
- * Profiling hook.  When both handles are non-NULL hipEvent_t values, every
- * later call records `before` on its stream immediately before its streaming
- * (prologue + candidate) kernel and `after` immediately after it, so
- * hipEventElapsedTime gives that kernel's duration.  NULL, NULL disables it.
+ * Profiling hook.  When all three handles are non-NULL hipEvent_t values, every
+ * later call records `before_stream` on its stream immediately before its
+ * streaming kernel, `before_merge` between the streaming kernel and the row
+ * merge kernel, and `after_merge` immediately after the merge kernel, so
+ * hipEventElapsedTime of consecutive pairs gives each kernel's duration.
+ * Three NULLs disable it; a mix of NULL and non-NULL is SS_ERR_INVALID_ARG.
+ * The handles stay owned by the caller and must outlive their use.
  * Process-wide, not thread-safe, and not meant for use under graph capture.
  */
-ss_status ss_set_kernel_events(void *before, void *after);
+ss_status ss_set_kernel_events(void *before_stream, void *before_merge, void *after_merge);
 
 const char *ss_status_string(ss_status s);
 

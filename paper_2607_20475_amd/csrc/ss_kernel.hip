@@ -2254,7 +2254,7 @@ static void fill_params(KArgs& k, const ss_params* p) {
 static int esize(int dtype) { return dtype == SS_BF16 ? 2 : 4; }
 
 // profiling hook (ss_set_kernel_events)
-static hipEvent_t g_ev_before = nullptr, g_ev_after = nullptr;
+static hipEvent_t g_ev[3] = {nullptr, nullptr, nullptr};
 
 template <int DT>
 static void launch_merge(const KArgs& k, dim3 grid, dim3 block, int smem, hipStream_t st) {
@@ -2318,16 +2318,17 @@ static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStr
   }
   const int nunits = lay.rows * lay.U;
   const dim3 grid((unsigned)((nunits + kWaves - 1) / kWaves)), rgrid((unsigned)lay.rows), block(kBlock);
-  if (g_ev_before) (void)hipEventRecord(g_ev_before, st);
+  if (g_ev[0]) (void)hipEventRecord(g_ev[0], st);
   if (dtype == SS_BF16)
     hipLaunchKernelGGL(ss_stream_kernel<SS_BF16>, grid, block, 0, st, k);
   else
     hipLaunchKernelGGL(ss_stream_kernel<SS_F32>, grid, block, 0, st, k);
-  if (g_ev_after) (void)hipEventRecord(g_ev_after, st);
+  if (g_ev[0]) (void)hipEventRecord(g_ev[1], st);
   if (dtype == SS_BF16)
     launch_merge<SS_BF16>(k, rgrid, block, lay.smem, st);
   else
     launch_merge<SS_F32>(k, rgrid, block, lay.smem, st);
+  if (g_ev[0]) (void)hipEventRecord(g_ev[2], st);
   if (k.op == OP_VERIFY)
     hipLaunchKernelGGL(ss_assemble_kernel, dim3((unsigned)((k.B + kBlock - 1) / kBlock)), block, 0, st, k);
   if (materialize) {
@@ -2488,10 +2489,12 @@ ss_status ss_process_logits(const void* logits, int dtype, int64_t ld, const ss_
   return launch(a, dtype, lay, ws, (hipStream_t)stream, true);
 }
 
-ss_status ss_set_kernel_events(void* before, void* after) {
-  if ((before == nullptr) != (after == nullptr)) return SS_ERR_INVALID_ARG;
-  g_ev_before = reinterpret_cast<hipEvent_t>(before);
-  g_ev_after = reinterpret_cast<hipEvent_t>(after);
+ss_status ss_set_kernel_events(void* before_stream, void* before_merge, void* after_merge) {
+  const bool on = before_stream && before_merge && after_merge;
+  if (!on && (before_stream || before_merge || after_merge)) return SS_ERR_INVALID_ARG;
+  g_ev[0] = reinterpret_cast<hipEvent_t>(before_stream);
+  g_ev[1] = reinterpret_cast<hipEvent_t>(before_merge);
+  g_ev[2] = reinterpret_cast<hipEvent_t>(after_merge);
   return SS_OK;
 }
 
