@@ -46,6 +46,8 @@
 
 namespace ss {
 
+constexpr int kPBLog = 18;                  // patched-id bitmap: 2^18 bits
+constexpr int kPB = 1 << kPBLog;
 constexpr int kUE = 2048;                    // elements per unit (one wavefront)
 constexpr int kMaxU = SS_MAX_V / kUE;        // units per row at most (512)
 constexpr int kH = 2048;                     // patch hash slots (LDS)
@@ -206,6 +208,7 @@ struct Ctx {
   int dtok;                 // verification: draft token of this row (-1: none)
   bool greedy;
   bool kcap;
+  bool pexact;              // the patched-id bitmap is exact (V <= kPB)
   int k_eff;
 };
 
@@ -256,6 +259,7 @@ __device__ __forceinline__ Ctx make_ctx(const KArgs& a, int row) {
   c.dtok = -1;
   if (a.op == OP_VERIFY && c.ell < a.L) c.dtok = a.draft_tokens[(size_t)b * a.L + c.ell];
   c.kcap = false;
+  c.pexact = a.V <= kPB;
   if (a.op == OP_TOPK) {
     c.greedy = false;
     int k = a.top_k ? a.top_k[b] : a.k_cap;
@@ -568,14 +572,13 @@ struct MSmem {
   double bcd[4];
   int32_t closed[kWaves];
   uint32_t flagsw;  // bit 0: hash overflow
-  uint32_t pbits[512];  // filter: bit hbit(id) set for every patched id
+  uint32_t pbits[kPB / 32];  // bit pbit(id) set for every patched id
   int32_t hk[kH];   // patched id (or -1)
   uint32_t hc[kH];  // occurrence count | has-bias bit 31
   uint32_t hf[kH];  // final key
   uint16_t claim[kH];  // slots claimed by distinct ids, in claim order
   uint32_t nclaim;
   uint32_t gtab[kGT];  // candidate slot -> group offset in the row's regions
-  uint4 stg[kGS];      // candidate groups of the current batch
   uint32_t uoff[kMaxU + 1];
   uint32_t rmask[kMaxU / 32];  // units re-read by the slow path
   alignas(16) uint32_t hist[2][(kHCopies * kHStride + 3) & ~3];  // rows 16-byte aligned (tie lists are read as uint4)
@@ -589,10 +592,14 @@ static_assert(kSmemFixed + 8 * (2 * SS_MAX_K + 512) <= 160 * 1024, "merge LDS to
 __device__ __forceinline__ uint32_t hslot(int id) { return ((uint32_t)id * 2654435761u) >> 21; }  // 11 bits
 static_assert(kH == 2048, "hslot assumes 2048 slots");
 
-__device__ __forceinline__ uint32_t hbit(int id) { return ((uint32_t)id * 0x9E3779B1u) >> 18; }  // 14 bits
+// Patched-id bitmap position: the id itself when V <= kPB (the bitmap is then
+// exact), else an 18-bit hash (a set bit then needs a table lookup).
+__device__ __forceinline__ uint32_t pbit(int id, bool exact) {
+  return exact ? (uint32_t)id : (((uint32_t)id * 0x9E3779B1u) >> (32 - kPBLog));
+}
 // false only when id is certainly not patched (one LDS read)
-__device__ __forceinline__ bool maybe_patched(const MSmem& S, int id) {
-  const uint32_t h = hbit(id);
+__device__ __forceinline__ bool maybe_patched(const MSmem& S, int id, bool exact) {
+  const uint32_t h = pbit(id, exact);
   return (S.pbits[h >> 5] >> (h & 31)) & 1u;
 }
 __device__ __forceinline__ int hfind(const MSmem& S, int id) {
@@ -604,6 +611,9 @@ __device__ __forceinline__ int hfind(const MSmem& S, int id) {
     s = (s + 1) & (kH - 1);
   }
   return -1;
+}
+__device__ __forceinline__ bool lds_patched(const MSmem& S, int id, bool exact) {
+  return maybe_patched(S, id, exact) && (exact || hfind(S, id) >= 0);
 }
 
 
@@ -1046,7 +1056,7 @@ __device__ __forceinline__ uint32_t lin_final(const KArgs& a, const Ctx& c, int 
 template <int DT>
 __device__ __forceinline__ bool is_patched(const Ctx& c, const MSmem& S, int pmode, const PatchG& g, int id) {
   if (pmode == 0) return false;
-  if (pmode == 1) return maybe_patched(S, id) && hfind(S, id) >= 0;
+  if (pmode == 1) return lds_patched(S, id, c.pexact);
   if (pmode == 2) return gfind(g, id) >= 0;
   int cn;
   bool hb;
@@ -1374,7 +1384,8 @@ __device__ __forceinline__ int slow_select(const KArgs& a, const Ctx& c, MSmem& 
 // ---------------------------------------------------------------------------
 // Fast-path pool: every candidate element at or above tmax (raw copies of
 // patched ids dropped) plus the patched final values at or above it, in a
-// deterministic order (batches staged in LDS, block-scan offsets).
+// deterministic order (batches of groups held in registers, block-scan
+// offsets).
 // Returns the element count (elements beyond a.pcap are counted, not stored).
 template <int DT>
 __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MSmem& S, uint32_t NG, bool patch,
@@ -1420,11 +1431,15 @@ __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MS
     if constexpr (DT == SS_BF16) return (((e < 2 ? gq.y : gq.z) >> (16 * (e & 1))) & 0xFFFFu) << 16;
     else return e ? gq.z : gq.y;
   };
-  uint32_t ninv = 0u;
+  // Groups start at multiples of GE, so a group's ids share one bitmap word.
+  const bool exact = a.V <= kPB;
+  const uint32_t pwmax = (uint32_t)((a.V + 31) >> 5) - 1u;
   constexpr int kPer = kGS / kBlock;
+  static_assert(kPer * GE <= 32, "selection mask is 32 bits");
   for (uint32_t f0 = 0; f0 < NG; f0 += (uint32_t)kGS) {
     const uint32_t nb = min((uint32_t)kGS, NG - f0);
-    // offsets, then every load of the batch in flight, then staged in LDS
+    // offsets, then every load of the batch in flight; each thread keeps its
+    // groups in registers
     uint32_t go[kPer];
 #pragma unroll
     for (int m = 0; m < kPer; ++m) {
@@ -1442,42 +1457,42 @@ __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MS
     uint4 g[kPer];
 #pragma unroll
     for (int m = 0; m < kPer; ++m) g[m] = rc[go[m] == 0xFFFFFFFFu ? 0u : go[m]];
+    // patched-id bitmap words (all reads issued before any is used)
+    uint32_t pw[kPer];
 #pragma unroll
-    for (int m = 0; m < kPer; ++m)
-      if (go[m] != 0xFFFFFFFFu) S.stg[tid + m * kBlock] = g[m];
-    lds_barrier();
-    uint32_t cnt = 0u;
-    for (uint32_t q = (uint32_t)tid; q < nb; q += kBlock) {
-      const uint4 gq = S.stg[q];
+    for (int m = 0; m < kPer; ++m) {
+      pw[m] = 0u;
+      if (patch && exact) pw[m] = S.pbits[go[m] == 0xFFFFFFFFu ? 0u : min(g[m].x >> 5, pwmax)];
+    }
+    // selection: key >= tmax, valid, and not the raw copy of a patched id
+    // (its final value is in the pool already when it is >= tmax)
+    uint32_t sel = 0u;
+#pragma unroll
+    for (int m = 0; m < kPer; ++m) {
 #pragma unroll
       for (int e = 0; e < GE; ++e) {
-        const uint32_t k = key_of(gq, e);
-        cnt += (k >= tmax && k >= kKeyFloor) ? 1u : 0u;
+        const uint32_t k = key_of(g[m], e);
+        const uint32_t id = g[m].x + (uint32_t)e;
+        bool v = go[m] != 0xFFFFFFFFu && k >= tmax && k >= kKeyFloor;
+        if (patch) v = v && !(exact ? ((pw[m] >> (id & 31u)) & 1u) != 0u : lds_patched(S, (int)id, false));
+        sel |= (v ? 1u : 0u) << (m * GE + e);
       }
     }
     uint32_t tot;
-    uint32_t off = base + block_excl_scan(cnt, S.r32, tot);
-    for (uint32_t q = (uint32_t)tid; q < nb; q += kBlock) {
-      const uint4 gq = S.stg[q];
+    uint32_t off = base + block_excl_scan((uint32_t)__builtin_popcount(sel), S.r32, tot);
+#pragma unroll
+    for (int m = 0; m < kPer; ++m) {
 #pragma unroll
       for (int e = 0; e < GE; ++e) {
-        uint32_t k = key_of(gq, e);
-        if (k >= tmax && k >= kKeyFloor) {
-          const uint32_t id = gq.x + (uint32_t)e;
-          // raw copy of a patched id: kept invalid (its final value is above)
-          if (patch && maybe_patched(S, (int)id) && hfind(S, (int)id) >= 0) {
-            k = 0u;
-            ++ninv;
-          }
-          if (off < pcap) pool[off] = make_uint2(k, id);
+        if ((sel >> (m * GE + e)) & 1u) {
+          if (off < pcap) pool[off] = make_uint2(key_of(g[m], e), g[m].x + (uint32_t)e);
           ++off;
         }
       }
     }
     base += tot;
-    lds_barrier();  // the staging area is refilled by the next batch
   }
-  nvalid_out = base - (patch ? block_sum(ninv, S.r32) : 0u);
+  nvalid_out = base;
   return base;
 }
 
@@ -1580,7 +1595,9 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
       reinterpret_cast<int4*>(S.hk)[s] = make_int4(-1, -1, -1, -1);
       reinterpret_cast<uint4*>(S.hc)[s] = make_uint4(0u, 0u, 0u, 0u);
     }
-    for (int s = tid; s < 512 / 4; s += kBlock) reinterpret_cast<uint4*>(S.pbits)[s] = make_uint4(0u, 0u, 0u, 0u);
+    const bool exact = a.V <= kPB;
+    const int pwords = exact ? (a.V + 31) >> 5 : kPB / 32;
+    for (int s = tid; s < (pwords + 3) >> 2; s += kBlock) reinterpret_cast<uint4*>(S.pbits)[s] = make_uint4(0u, 0u, 0u, 0u);
     if (tid == 0) S.nclaim = 0u;
     lds_barrier();
     // bias entries record their value in hf[] (the final key is written
@@ -1588,7 +1605,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
     // finals then sum that id's entries in list order
     auto ins = [&](int id, uint32_t addc, bool bias, float bval) {
       if (id < 0 || id >= a.V) return;
-      const uint32_t hb2 = hbit(id);
+      const uint32_t hb2 = pbit(id, exact);
       atomicOr(&S.pbits[hb2 >> 5], 1u << (hb2 & 31));
       uint32_t s = hslot(id);
       for (int p = 0; p < kProbe; ++p) {
@@ -1628,10 +1645,11 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
           id[m] = sl[m] >= 0 ? S.hk[sl[m]] : -1;
           bits[m] = 0u;
           mw[m] = 0xFFFFFFFFu;
-          if (id[m] >= 0) {
-            bits[m] = load_elem_bits<DT>(c.xrow, id[m]);
-            if (c.mask) mw[m] = (id[m] >> 5) < Wm ? c.mask[id[m] >> 5] : 0u;
-          }
+          // unconditional loads (element 0 stands in for an empty slot), so
+          // that all of them are in flight together
+          const int ld_id = id[m] >= 0 ? id[m] : 0;
+          bits[m] = load_elem_bits<DT>(c.xrow, ld_id);
+          if (c.mask) mw[m] = (ld_id >> 5) < Wm ? c.mask[ld_id >> 5] : 0u;
         }
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
