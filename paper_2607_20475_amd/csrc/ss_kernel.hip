@@ -586,7 +586,8 @@ struct MSmem {
   uint64_t mhist[256];
 };
 constexpr int kSmemFixed = (int)((sizeof(MSmem) + 15) & ~(size_t)15);
-// the largest merge footprint (sampling ops at k_max = SS_MAX_K) fits gfx950's 160 KiB of LDS
+// the largest merge footprint (sampling ops at k_max = SS_MAX_K: pcap + kBlock
+// <= 2 SS_MAX_K + 512 entries) fits gfx950's 160 KiB of LDS
 static_assert(kSmemFixed + 8 * (2 * SS_MAX_K + 512) <= 160 * 1024, "merge LDS too large");
 
 __device__ __forceinline__ uint32_t hslot(int id) { return ((uint32_t)id * 2654435761u) >> 21; }  // 11 bits
@@ -1382,6 +1383,54 @@ __device__ __forceinline__ int slow_select(const KArgs& a, const Ctx& c, MSmem& 
 }
 
 // ---------------------------------------------------------------------------
+// One batch of candidate groups held in registers: kGS groups, kGPer per
+// thread (slot tid + kBlock m), with their group offsets (~0u: no group).
+constexpr int kGPer = kGS / kBlock;
+struct GBatch {
+  uint32_t go[kGPer];
+  uint4 g[kGPer];
+};
+
+// Slot -> group offset table of the row's candidate regions (TPU threads per
+// unit), when the row's groups fit it.
+__device__ __forceinline__ void gather_table(const KArgs& a, MSmem& S, int U, uint32_t NG) {
+  if (NG > (uint32_t)kGT) return;
+  const int tid = threadIdx.x;
+  const int TPU = U >= kBlock ? 1 : kBlock / U;
+  for (int x = tid; x < U * TPU; x += kBlock) {
+    const int u = x / TPU, sub = x - u * TPU;
+    const uint32_t o = S.uoff[u], n = S.uoff[u + 1] - o;
+    for (uint32_t j = (uint32_t)sub; j < n; j += (uint32_t)TPU) S.gtab[o + j] = (uint32_t)u * a.cap + j;
+  }
+  lds_barrier();
+}
+
+// Issues the loads of the batch starting at group f0 (every load in flight,
+// nothing waits for them here).
+template <int DT>
+__device__ __forceinline__ void gather_issue(const KArgs& a, const MSmem& S, int row, int U, uint32_t NG, uint32_t f0,
+                                             GBatch& gb) {
+  const int tid = threadIdx.x;
+  const uint4* rc = a.cand + (size_t)row * U * a.cap;
+  const uint32_t nb = f0 < NG ? min((uint32_t)kGS, NG - f0) : 0u;
+  const bool table = NG <= (uint32_t)kGT;
+#pragma unroll
+  for (int m = 0; m < kGPer; ++m) {
+    const uint32_t q = (uint32_t)(tid + m * kBlock);
+    gb.go[m] = 0xFFFFFFFFu;
+    if (q < nb) {
+      if (table) {
+        gb.go[m] = S.gtab[f0 + q];
+      } else {
+        const int u = unit_of_group<DT>(S, U, f0 + q);
+        gb.go[m] = (uint32_t)u * a.cap + (f0 + q - S.uoff[u]);
+      }
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < kGPer; ++m) gb.g[m] = rc[gb.go[m] == 0xFFFFFFFFu ? 0u : gb.go[m]];
+}
+
 // Fast-path pool: every candidate element at or above tmax (raw copies of
 // patched ids dropped) plus the patched final values at or above it, in a
 // deterministic order (batches of groups held in registers, block-scan
@@ -1393,8 +1442,11 @@ __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MS
   constexpr int GE = DTT<DT>::GE;
   const int tid = threadIdx.x;
   const int U = a.U;
-  const uint4* rc = a.cand + (size_t)c.row * U * a.cap;
   const uint32_t pcap = (uint32_t)a.pcap;
+  // the first batch's loads are in flight during the patched-finals pass
+  gather_table(a, S, U, NG);
+  GBatch cur;
+  gather_issue<DT>(a, S, c.row, U, NG, 0u, cur);
   // patched final values at or above tmax go first
   uint32_t base = 0u;
   if (patch) {
@@ -1416,17 +1468,6 @@ __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MS
     }
     base = tot;
   }
-  // slot -> offset table, TPU threads per unit
-  const bool table = NG <= (uint32_t)kGT;
-  if (table) {
-    const int TPU = U >= kBlock ? 1 : kBlock / U;
-    for (int x = tid; x < U * TPU; x += kBlock) {
-      const int u = x / TPU, sub = x - u * TPU;
-      const uint32_t o = S.uoff[u], n = S.uoff[u + 1] - o;
-      for (uint32_t j = (uint32_t)sub; j < n; j += (uint32_t)TPU) S.gtab[o + j] = (uint32_t)u * a.cap + j;
-    }
-    lds_barrier();
-  }
   auto key_of = [](const uint4& gq, int e) -> uint32_t {
     if constexpr (DT == SS_BF16) return (((e < 2 ? gq.y : gq.z) >> (16 * (e & 1))) & 0xFFFFu) << 16;
     else return e ? gq.z : gq.y;
@@ -1434,29 +1475,14 @@ __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MS
   // Groups start at multiples of GE, so a group's ids share one bitmap word.
   const bool exact = a.V <= kPB;
   const uint32_t pwmax = (uint32_t)((a.V + 31) >> 5) - 1u;
-  constexpr int kPer = kGS / kBlock;
+  constexpr int kPer = kGPer;
   static_assert(kPer * GE <= 32, "selection mask is 32 bits");
+  // batch f0 is processed while the loads of batch f0 + kGS are in flight
   for (uint32_t f0 = 0; f0 < NG; f0 += (uint32_t)kGS) {
-    const uint32_t nb = min((uint32_t)kGS, NG - f0);
-    // offsets, then every load of the batch in flight; each thread keeps its
-    // groups in registers
-    uint32_t go[kPer];
-#pragma unroll
-    for (int m = 0; m < kPer; ++m) {
-      const uint32_t q = (uint32_t)(tid + m * kBlock);
-      go[m] = 0xFFFFFFFFu;
-      if (q < nb) {
-        if (table) {
-          go[m] = S.gtab[f0 + q];
-        } else {
-          const int u = unit_of_group<DT>(S, U, f0 + q);
-          go[m] = (uint32_t)u * a.cap + (f0 + q - S.uoff[u]);
-        }
-      }
-    }
-    uint4 g[kPer];
-#pragma unroll
-    for (int m = 0; m < kPer; ++m) g[m] = rc[go[m] == 0xFFFFFFFFu ? 0u : go[m]];
+    GBatch nxt;
+    if (f0 + (uint32_t)kGS < NG) gather_issue<DT>(a, S, c.row, U, NG, f0 + (uint32_t)kGS, nxt);
+    const uint32_t(&go)[kPer] = cur.go;
+    const uint4(&g)[kPer] = cur.g;
     // patched-id bitmap words (all reads issued before any is used)
     uint32_t pw[kPer];
 #pragma unroll
@@ -1469,28 +1495,45 @@ __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MS
     uint32_t sel = 0u;
 #pragma unroll
     for (int m = 0; m < kPer; ++m) {
+      const bool gv = go[m] != 0xFFFFFFFFu;
 #pragma unroll
       for (int e = 0; e < GE; ++e) {
         const uint32_t k = key_of(g[m], e);
-        const uint32_t id = g[m].x + (uint32_t)e;
-        bool v = go[m] != 0xFFFFFFFFu && k >= tmax && k >= kKeyFloor;
-        if (patch) v = v && !(exact ? ((pw[m] >> (id & 31u)) & 1u) != 0u : lds_patched(S, (int)id, false));
-        sel |= (v ? 1u : 0u) << (m * GE + e);
+        sel |= ((gv && k >= tmax && k >= kKeyFloor) ? 1u : 0u) << (m * GE + e);
+      }
+    }
+    if (patch) {
+      if (exact) {
+#pragma unroll
+        for (int m = 0; m < kPer; ++m) sel &= ~(((pw[m] >> (g[m].x & 31u)) & ((1u << GE) - 1u)) << (m * GE));
+      } else {
+#pragma unroll
+        for (int m = 0; m < kPer; ++m) {
+          const uint32_t bm = (sel >> (m * GE)) & ((1u << GE) - 1u);
+          if (bm != 0u) {
+#pragma unroll 1
+            for (int e = 0; e < GE; ++e)
+              if (((bm >> e) & 1u) && lds_patched(S, (int)(g[m].x + (uint32_t)e), false)) sel &= ~(1u << (m * GE + e));
+          }
+        }
       }
     }
     uint32_t tot;
-    uint32_t off = base + block_excl_scan((uint32_t)__builtin_popcount(sel), S.r32, tot);
+    uint32_t pos = base + block_excl_scan((uint32_t)__builtin_popcount(sel), S.r32, tot);
+    // every element is written: a selected one to the next pool slot, the
+    // others (and those beyond pcap) to this thread's dump slot past the pool
+    const uint32_t dump = pcap + (uint32_t)tid;
 #pragma unroll
     for (int m = 0; m < kPer; ++m) {
 #pragma unroll
       for (int e = 0; e < GE; ++e) {
-        if ((sel >> (m * GE + e)) & 1u) {
-          if (off < pcap) pool[off] = make_uint2(key_of(g[m], e), g[m].x + (uint32_t)e);
-          ++off;
-        }
+        const uint32_t bit = (sel >> (m * GE + e)) & 1u;
+        pool[(bit != 0u && pos < pcap) ? pos : dump] = make_uint2(key_of(g[m], e), g[m].x + (uint32_t)e);
+        pos += bit;
       }
     }
     base += tot;
+    cur = nxt;
   }
   nvalid_out = base;
   return base;
@@ -2229,7 +2272,7 @@ static bool make_layout(int op, int B, int V, int L, int k_max, int dtype, Layou
   lay->cap = cap;
   lay->pcap = pcap;
   lay->rows = rows;
-  lay->smem = kSmemFixed + 8 * pcap;
+  lay->smem = kSmemFixed + 8 * (pcap + kBlock);  // pool plus one dump slot per thread
   return true;
 }
 
