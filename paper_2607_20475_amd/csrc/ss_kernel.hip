@@ -56,7 +56,9 @@ constexpr int kGH = 16384;                   // per-row patch table in global me
 constexpr int kGProbe = 1024;
 constexpr uint32_t kLinear = 0xFFFFFFFFu;    // patched-list count meaning "look the lists up"
 constexpr int kHCopies = 2;                  // privatised radix histograms
-constexpr int kHStride = 257;
+constexpr int kRB = 9;                       // widest radix digit (bits)
+constexpr int kRBins = 1 << kRB;
+constexpr int kHStride = kRBins + 1;
 constexpr int kTS = SS_MAX_K / kBlock;       // selected elements per thread (16)
 constexpr int kGT = 4096;                    // gather table entries (LDS)
 constexpr int kGS = 2048;                    // candidate groups staged in LDS per batch
@@ -572,19 +574,28 @@ struct MSmem {
   double bcd[4];
   int32_t closed[kWaves];
   uint32_t flagsw;  // bit 0: hash overflow
+  uint64_t x64[2][kWaves];  // scratch of the fused reductions
+  uint32_t x32[3][kWaves];
   uint32_t pbits[kPB / 32];  // bit pbit(id) set for every patched id
   int32_t hk[kH];   // patched id (or -1)
   uint32_t hc[kH];  // occurrence count | has-bias bit 31
   uint32_t hf[kH];  // final key
   uint16_t claim[kH];  // slots claimed by distinct ids, in claim order
   uint32_t nclaim;
-  uint32_t gtab[kGT];  // candidate slot -> group offset in the row's regions
+  union {
+    uint32_t gtab[kGT];  // candidate slot -> group offset in the row's regions (gather)
+    struct {             // radix histograms (selection and the epilogue, after the gather)
+      alignas(16) uint32_t hist[2][(kHCopies * kHStride + 3) & ~3];  // rows 16-byte aligned (tie lists are read as uint4)
+      uint32_t low[2][kRBins / 4];
+      uint64_t mhist[kRBins];
+    };
+  };
   uint32_t uoff[kMaxU + 1];
   uint32_t rmask[kMaxU / 32];  // units re-read by the slow path
-  alignas(16) uint32_t hist[2][(kHCopies * kHStride + 3) & ~3];  // rows 16-byte aligned (tie lists are read as uint4)
-  uint32_t low[2][64];
-  uint64_t mhist[256];
 };
+static_assert(sizeof(uint32_t) * 2 * ((kHCopies * kHStride + 3) & ~3) + 4 * 2 * (kRBins / 4) + 8 * kRBins <=
+                  sizeof(uint32_t) * kGT,
+              "radix histograms share the gather table's space");
 constexpr int kSmemFixed = (int)((sizeof(MSmem) + 15) & ~(size_t)15);
 // the largest merge footprint (sampling ops at k_max = SS_MAX_K: pcap + kBlock
 // <= 2 SS_MAX_K + 512 entries) fits gfx950's 160 KiB of LDS
@@ -592,6 +603,67 @@ static_assert(kSmemFixed + 8 * (2 * SS_MAX_K + 512) <= 160 * 1024, "merge LDS to
 
 __device__ __forceinline__ uint32_t hslot(int id) { return ((uint32_t)id * 2654435761u) >> 21; }  // 11 bits
 static_assert(kH == 2048, "hslot assumes 2048 slots");
+
+// Several workgroup reductions sharing one pair of barriers.
+__device__ __forceinline__ void block_max3(uint32_t& x, uint32_t& y, uint32_t& z, MSmem& S) {
+  x = wave_max(x);
+  y = wave_max(y);
+  z = wave_max(z);
+  if (lane() == 0) {
+    S.x32[0][wave()] = x;
+    S.x32[1][wave()] = y;
+    S.x32[2][wave()] = z;
+  }
+  lds_barrier();
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    x = max(x, S.x32[0][w]);
+    y = max(y, S.x32[1][w]);
+    z = max(z, S.x32[2][w]);
+  }
+  lds_barrier();
+}
+// (max of a 64-bit value, min of a 32-bit value)
+__device__ __forceinline__ void block_max_min(uint64_t& x, uint32_t& y, MSmem& S) {
+  x = wave_max(x);
+  y = wave_min(y);
+  if (lane() == 0) {
+    S.x64[0][wave()] = x;
+    S.x32[0][wave()] = y;
+  }
+  lds_barrier();
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    x = S.x64[0][w] > x ? S.x64[0][w] : x;
+    y = min(y, S.x32[0][w]);
+  }
+  lds_barrier();
+}
+// (sum, min) of 64-bit values and (sum, min) of 32-bit values; the sums are
+// integer, so exact in any order
+__device__ __forceinline__ void block_sum_min2(uint64_t& s64, uint64_t& m64, uint32_t& s32, uint32_t& m32, MSmem& S) {
+  s64 = wave_sum(s64);
+  m64 = wave_min(m64);
+  s32 = wave_sum(s32);
+  m32 = wave_min(m32);
+  if (lane() == 0) {
+    S.x64[0][wave()] = s64;
+    S.x64[1][wave()] = m64;
+    S.x32[0][wave()] = s32;
+    S.x32[1][wave()] = m32;
+  }
+  lds_barrier();
+  s64 = 0ull;
+  s32 = 0u;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    s64 += S.x64[0][w];
+    m64 = S.x64[1][w] < m64 ? S.x64[1][w] : m64;
+    s32 += S.x32[0][w];
+    m32 = min(m32, S.x32[1][w]);
+  }
+  lds_barrier();
+}
 
 // Patched-id bitmap position: the id itself when V <= kPB (the bitmap is then
 // exact), else an 18-bit hash (a set bit then needs a table lookup).
@@ -697,7 +769,7 @@ __device__ __forceinline__ int lin_entry(const Ctx& c, int e) {
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void radix_clear(MSmem& S, int buf) {
   for (int i = threadIdx.x; i < kHCopies * kHStride; i += kBlock) S.hist[buf][i] = 0u;
-  if (threadIdx.x < 64) S.low[buf][threadIdx.x] = 0u;
+  if (threadIdx.x < kRBins / 4) S.low[buf][threadIdx.x] = 0u;
 }
 __device__ __forceinline__ void hist_add(uint32_t* h, uint32_t bin, bool pred) {
   if (pred) atomicAdd(&h[(lane() & (kHCopies - 1)) * kHStride + bin], 1u);
@@ -706,19 +778,20 @@ __device__ __forceinline__ void low_mark(uint32_t* low, uint32_t bin, bool pred)
   if (pred) reinterpret_cast<uint8_t*>(low)[bin] = 1;
 }
 
-// Digit search by wave 0 over nb <= 256 bins.  Descending: find d with
+// Digit search by wave 0 over nb <= kRBins bins.  Descending: find d with
 // above(d) < want <= above(d) + h[d]; ascending: the same with the bins
 // below d.  Writes (d, count before d, h[d], low flag of d) to bc[0..3]; d =
 // nb if the total is below `want`.
-__device__ inline void radix_digit(const uint32_t* h, const uint32_t* low, int nb, uint32_t want, bool descending,
-                                   uint32_t* bc) {
+template <int BPL>
+__device__ inline void radix_digit_n(const uint32_t* h, const uint32_t* low, int nb, uint32_t want, bool descending,
+                                     uint32_t* bc) {
   if (threadIdx.x < 64) {
     const int l = lane();
-    uint32_t cb[4];
+    uint32_t cb[BPL];
     uint32_t s = 0;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int r = 4 * l + u;
+    for (int u = 0; u < BPL; ++u) {
+      const int r = BPL * l + u;
       const int bin = descending ? (nb - 1 - r) : r;
       uint32_t v = 0;
       if (r < nb) {
@@ -738,8 +811,8 @@ __device__ inline void radix_digit(const uint32_t* h, const uint32_t* low, int n
       bc[3] = 1u;
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int r = 4 * l + u;
+    for (int u = 0; u < BPL; ++u) {
+      const int r = BPL * l + u;
       const int bin = descending ? (nb - 1 - r) : r;
       if (r < nb && run < want && run + cb[u] >= want) {
         bc[0] = (uint32_t)bin;
@@ -751,6 +824,13 @@ __device__ inline void radix_digit(const uint32_t* h, const uint32_t* low, int n
     }
   }
   lds_barrier();
+}
+__device__ __forceinline__ void radix_digit(const uint32_t* h, const uint32_t* low, int nb, uint32_t want,
+                                            bool descending, uint32_t* bc) {
+  if (nb <= 256)
+    radix_digit_n<4>(h, low, nb, want, descending, bc);
+  else
+    radix_digit_n<kRBins / 64>(h, low, nb, want, descending, bc);
 }
 
 // Exact selection of the `want` largest composites (key desc, index asc)
@@ -778,7 +858,7 @@ __device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint3
     sh = 0;
   }
   while (sh > 0) {
-    const int w = sh < 8 ? sh : 8;
+    const int w = sh < kRB ? sh : kRB;
     sh -= w;
     const int hs = sh + w;
     const uint32_t dm = (1u << w) - 1u;
@@ -846,7 +926,7 @@ __device__ __forceinline__ void radix_select(Visit&& visit, uint32_t want, uint3
     int ib = 32 - __clz((uint32_t)(V > 1 ? V - 1 : 1));
     uint32_t ip = 0u;
     while (ib > 0) {
-      const int w = ib < 8 ? ib : 8;
+      const int w = ib < kRB ? ib : kRB;
       ib -= w;
       const int hs = ib + w;
       const uint32_t dm = (1u << w) - 1u;
@@ -889,12 +969,13 @@ __device__ __forceinline__ bool selected(uint32_t k, uint32_t i, uint32_t tk, ui
 __device__ __forceinline__ void mass_digit(MSmem& S, int nb, double X, bool strict, bool descending) {
   if (threadIdx.x < 64) {
     const int l = lane();
-    uint64_t mb[4];
-    uint32_t cb[4];
+    constexpr int BPL = 4;  // nb <= 256
+    uint64_t mb[BPL];
+    uint32_t cb[BPL];
     uint64_t ms = 0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int r = 4 * l + q;
+    for (int q = 0; q < BPL; ++q) {
+      const int r = BPL * l + q;
       const int bin = descending ? nb - 1 - r : r;
       mb[q] = 0;
       cb[q] = 0;
@@ -912,8 +993,8 @@ __device__ __forceinline__ void mass_digit(MSmem& S, int nb, double X, bool stri
     int hq = -1;
     uint64_t hrun = 0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int r = 4 * l + q;
+    for (int q = 0; q < BPL; ++q) {
+      const int r = BPL * l + q;
       const uint64_t nr = run + mb[q];
       const bool hit = r < nb && cb[q] > 0u && (strict ? ((double)nr > X) : ((double)nr >= X));
       if (hit && hq < 0) {
@@ -926,7 +1007,7 @@ __device__ __forceinline__ void mass_digit(MSmem& S, int nb, double X, bool stri
     if (hm == 0ull) {
       if (l == 0) S.bc[0] = 0xFFFFFFFFu;
     } else if (l == (int)__builtin_ctzll(hm)) {
-      const int bin = descending ? nb - 1 - (4 * l + hq) : 4 * l + hq;
+      const int bin = descending ? nb - 1 - (BPL * l + hq) : BPL * l + hq;
       S.bc[0] = (uint32_t)bin;
       S.bc64[0] = hrun;
       S.bc[2] = cb[hq];
@@ -974,14 +1055,29 @@ __device__ __forceinline__ uint64_t cross_find(MSmem& S, const uint2* T, const u
     }
     const uint32_t dm = (1u << w) - 1u;
     const uint32_t lm = (1u << csh) - 1u;
-    for (int i = tid; i < 256; i += kBlock) S.mhist[i] = 0ull;
-    for (int i = tid; i < kHCopies * kHStride; i += kBlock) S.hist[0][i] = 0u;
+    for (int i = tid; i <= (int)dm; i += kBlock) {
+      S.mhist[i] = 0ull;
+#pragma unroll
+      for (int cp = 0; cp < kHCopies; ++cp) S.hist[0][cp * kHStride + i] = 0u;
+    }
     if (tid < 64) S.low[0][tid] = 0u;
     lds_barrier();
-    for (int m = 0; m < M; ++m) {
+    for (int m0 = 0; m0 < M; m0 += 4) {
+      // four entries and their weights loaded before any is used
+      uint2 ev[4];
+      uint64_t wv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = tid + (m0 + u) * kBlock;
+        ev[u] = T[i < nT ? i : 0];
+        wv[u] = Wl[i < nT ? i : 0];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+      const int m = m0 + u;
       const int i = tid + m * kBlock;
-      if (i < nT && ((inset >> m) & 1u)) {
-        const uint2 e = T[i];
+      if (m < M && i < nT && ((inset >> m) & 1u)) {
+        const uint2 e = ev[u];
         bool part;
         uint32_t d;
         if (phase == 0) {
@@ -992,10 +1088,11 @@ __device__ __forceinline__ uint64_t cross_find(MSmem& S, const uint2* T, const u
           d = (e.y >> csh) & dm;
         }
         if (part) {
-          atomicAdd(&S.mhist[d], Wl[i]);
+          atomicAdd(&S.mhist[d], wv[u]);
           hist_add(S.hist[0], d, true);
           low_mark(S.low[0], d, phase == 0 && (e.x & lm) != 0u);
         }
+      }
       }
     }
     lds_barrier();
@@ -1592,6 +1689,18 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   }
   const int bid0 = tid < c.nbias ? c.bias_ids[tid] : -1;
   const float bval0 = tid < c.nbias ? c.bias_vals[tid] : 0.0f;
+  // the patch tables are cleared while the records load (the barriers of
+  // the record scan order the clearing before the inserts)
+  const bool pexact = a.V <= kPB;
+  if ((c.nhist + c.nextra + c.nbias) > 0) {
+    for (int s = tid; s < kH / 4; s += kBlock) {
+      reinterpret_cast<int4*>(S.hk)[s] = make_int4(-1, -1, -1, -1);
+      reinterpret_cast<uint4*>(S.hc)[s] = make_uint4(0u, 0u, 0u, 0u);
+    }
+    const int pwords = pexact ? (a.V + 31) >> 5 : kPB / 32;
+    for (int s = tid; s < (pwords + 3) >> 2; s += kBlock) reinterpret_cast<uint4*>(S.pbits)[s] = make_uint4(0u, 0u, 0u, 0u);
+    if (tid == 0) S.nclaim = 0u;
+  }
   // 1. unit records: largest threshold, row maximum, candidate offsets
   uint32_t hi = 0u, tmax = 0u, ovf = 0u;
   uint32_t NG = 0u;
@@ -1615,9 +1724,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   }
   if (tid == 0) S.uoff[U] = NG;
   if (tid == 0) S.flagsw = 0u;
-  hi = block_max(hi, S.r32);
-  tmax = block_max(tmax, S.r32);
-  ovf = block_max(ovf, S.r32);
+  block_max3(hi, tmax, ovf, S);
 
   int flags = c.kcap ? SS_FLAG_KCAP : 0;
   const bool empty = hi < kKeyFloor;
@@ -1634,15 +1741,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   const int Wm = (a.V + 31) >> 5;
   uint32_t hfmax = 0u;  // largest patched final key (LDS mode)
   if (patch) {
-    for (int s = tid; s < kH / 4; s += kBlock) {
-      reinterpret_cast<int4*>(S.hk)[s] = make_int4(-1, -1, -1, -1);
-      reinterpret_cast<uint4*>(S.hc)[s] = make_uint4(0u, 0u, 0u, 0u);
-    }
-    const bool exact = a.V <= kPB;
-    const int pwords = exact ? (a.V + 31) >> 5 : kPB / 32;
-    for (int s = tid; s < (pwords + 3) >> 2; s += kBlock) reinterpret_cast<uint4*>(S.pbits)[s] = make_uint4(0u, 0u, 0u, 0u);
-    if (tid == 0) S.nclaim = 0u;
-    lds_barrier();
+    const bool exact = pexact;
     // bias entries record their value in hf[] (the final key is written
     // later); a second entry for the same id sets the "duplicate" bit and the
     // finals then sum that id's entries in list order
@@ -1795,8 +1894,16 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
       lds_barrier();
       nT = 1;
     } else if (!slow) {
+      // four pool entries per thread are loaded before any is used
       auto visit_pool = [&](auto&& f) {
-        for (int i = tid; i < (int)C; i += kBlock) f(pool[i].x, pool[i].y);
+        for (int i0 = tid; i0 < (int)C; i0 += 4 * kBlock) {
+          uint2 e[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) e[u] = pool[i0 + u * kBlock < (int)C ? i0 + u * kBlock : 0];
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (i0 + u * kBlock < (int)C) f(e[u].x, e[u].y);
+        }
       };
       radix_select(visit_pool, (uint32_t)want, Cv, plo, phi, a.V, S, &tk, &ti);
       nT = (int)compact_pool(S, pool, (int)C, [&](uint2 e) { return selected(e.x, e.y, tk, ti); });
@@ -1817,8 +1924,8 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
     mc = max(mc, comp_of(pool[i].x, pool[i].y));
     kmin = min(kmin, pool[i].x);
   }
-  const uint64_t Mcomp = block_max(mc, S.r64);
-  kmin = block_min(kmin, S.r32);
+  block_max_min(mc, kmin, S);
+  const uint64_t Mcomp = mc;
   const int argmax = none ? -1 : (int)comp_idx(Mcomp);
   if (empty) flags = SS_FLAG_EMPTY;
   if (none) flags |= SS_FLAG_EMPTY;
@@ -1959,10 +2066,10 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
           }
         }
       }
-      const uint64_t Zs = block_sum(zs, S.r64);
-      const uint32_t n_s = block_sum(ns, S.r32);
-      const uint64_t last = block_min(lastc, S.r64);
-      smin = block_min(smin, S.r32);
+      block_sum_min2(zs, lastc, ns, smin, S);
+      const uint64_t Zs = zs;
+      const uint32_t n_s = ns;
+      const uint64_t last = lastc;
       const double Zsd = (double)Zs / kFix;
       const double u0 = uniform01(seed, (uint32_t)b, pos, 0);
       auto draw = [&](double total) -> uint64_t {
