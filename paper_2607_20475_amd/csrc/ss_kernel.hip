@@ -332,14 +332,32 @@ __device__ __forceinline__ uint32_t penalised_key(uint32_t bits, uint32_t mode, 
 template <int NW>
 __device__ __forceinline__ uint32_t thr_search(const uint32_t (&gm)[NW], uint32_t q, int shift) {
   // largest 16-bit prefix p with at least q of the wavefront's values >= p << shift
-  uint32_t prefix = 0u;
+  // (or, once exactly q values lie at or above it, that shorter prefix).  The
+  // caller guarantees q <= 64 NW, so p lies between the wavefront's smallest
+  // and largest prefix: the search starts at their highest differing bit.
+  uint32_t lmin = gm[0], lmax = gm[0];
+#pragma unroll
+  for (int i = 1; i < NW; ++i) {
+    lmin = min(lmin, gm[i]);
+    lmax = max(lmax, gm[i]);
+  }
+  const uint32_t vmin = wave_min(lmin) >> shift, vmax = wave_max_u32(lmax) >> shift;
+  const uint32_t diff = vmin ^ vmax;
+  if (diff == 0u) return vmin << shift;
+  const int hb = 31 - __clz(diff);
+  uint32_t prefix = vmax & ~((2u << hb) - 1u);
 #pragma unroll 1
-  for (int b = 15; b >= 0; --b) {
+  for (int b = hb; b >= 0; --b) {
     const uint32_t cand = (prefix | (1u << b)) << shift;
     uint32_t cnt = 0u;
 #pragma unroll
     for (int i = 0; i < NW; ++i) cnt += (uint32_t)__popcll(__ballot(gm[i] >= cand));
-    if (cnt >= q) prefix |= 1u << b;
+    if (cnt >= q) {
+      prefix |= 1u << b;
+      // exactly q values at or above the prefix: the lower bits cannot drop
+      // any of them, and a lower threshold is still a valid one
+      if (cnt == q) break;
+    }
   }
   return prefix << shift;
 }
