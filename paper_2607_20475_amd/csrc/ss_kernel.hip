@@ -2368,7 +2368,6 @@ static bool make_layout(int op, int B, int V, int L, int k_max, int dtype, Layou
   // the sampling ops, its fixed-point weights in the back half
   int pcap = 2 * k_max + 128;
   if (pcap < 1024) pcap = 1024;
-  if (op == OP_TOPK && pcap > SS_MAX_K) pcap = SS_MAX_K > next_pow2(k_max) ? SS_MAX_K : next_pow2(k_max);
   if (pcap < next_pow2(k_max)) pcap = next_pow2(k_max);
   pcap = (pcap + 255) & ~255;
   size_t o = 0;
