@@ -79,6 +79,13 @@ __device__ inline double uniform01(uint64_t seed, uint32_t request, int64_t posi
 __device__ inline double weight_of(double y, double M, double tau) {
   return (y == M) ? 1.0 : exp((y - M) / tau);
 }
+// The same weight with the exponent (y - M) / tau formed in double and the
+// exponential taken in float (about one ulp): relative error near 1e-7, far
+// inside the 1e-5 relative agreement the probabilities are held to, at a
+// fraction of the cost of a double exponential.
+__device__ inline double weight_fast(double y, double M, double inv_tau) {
+  return (y == M) ? 1.0 : (double)expf((float)((y - M) * inv_tau));
+}
 
 // ---------------------------------------------------------------------------
 // wave64 / workgroup helpers

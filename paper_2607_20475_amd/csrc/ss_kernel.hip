@@ -1553,7 +1553,7 @@ __device__ __forceinline__ void gather_issue(const KArgs& a, const MSmem& S, int
 // Returns the element count (elements beyond a.pcap are counted, not stored).
 template <int DT>
 __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MSmem& S, uint32_t NG, bool patch,
-                                                uint32_t tmax, uint2* pool, uint32_t& nvalid_out) {
+                                                uint32_t tmax, uint2* pool, uint32_t& nvalid_out, uint32_t& nfin_out) {
   constexpr int GE = DTT<DT>::GE;
   const int tid = threadIdx.x;
   const int U = a.U;
@@ -1583,6 +1583,7 @@ __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MS
     }
     base = tot;
   }
+  nfin_out = base;  // pool[0, base): the patched final values
   auto key_of = [](const uint4& gq, int e) -> uint32_t {
     if constexpr (DT == SS_BF16) return (((e < 2 ? gq.y : gq.z) >> (16 * (e & 1))) & 0xFFFFu) << 16;
     else return e ? gq.z : gq.y;
@@ -1685,6 +1686,319 @@ __device__ __forceinline__ uint32_t compact_pool(MSmem& S, uint2* pool, int n, P
   return base;
 }
 
+
+// ---------------------------------------------------------------------------
+// Sampling epilogue on key bins, for bf16 rows whose pool keys span fewer than
+// kRBins consecutive 16-bit key values (Alg. 11 order, Appendix C.2-C.3).
+// Raw bf16 values lie on the 16-bit key grid, and elements with one key share
+// one weight, so the top-k boundary, Z_k, the top-p and min-p cuts, Z_S and
+// the drawn key follow from per-key counts in canonical order (keys
+// descending, ties by ascending index); only the drawn element's index needs
+// a pass over the pool.  Penalised or biased values (the patched finals at
+// the front of the pool) may fall between grid keys: such a value is placed
+// before the grid elements of its bin (it exceeds their key), and a boundary
+// inside a bin holding one is resolved by walking that bin's few off-grid
+// values in canonical order.  The fixed-point masses are the same integers
+// the element-wise epilogue sums.  Returns false, with nothing written, when
+// min-p would cut inside the maximum's own key or more than 64 patched
+// finals are pooled: the element-wise epilogue then handles the row.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint2* pool, int C, int nfin,
+                                              uint32_t want, uint32_t lo16, int V, int b, int& token, float& logprob) {
+  const int tid = threadIdx.x;
+  const bool minp = (c.mode & SS_MINP) && c.min_p > 0.0f;
+  const bool topp = (c.mode & SS_TOPP) && c.top_p < 1.0f;
+  const double lt = minp ? log((double)c.min_p) : 0.0;
+  if (lt > 0.0 || nfin > 64) return false;
+  const double tau = (double)c.tau;
+  const double itau = 1.0 / tau;
+  uint32_t* cnt = S.hist[0];     // grid elements per bin (bin = key16 - lo16)
+  uint32_t* abv = S.hist[1];     // per position: T elements before it
+  uint64_t* mbf = S.mhist;       // per position: T mass before it
+  for (int i = tid; i < kRBins; i += kBlock) cnt[i] = 0u;
+  if (tid == 0) {
+    S.bc[2] = 0u;           // last position holding elements of S
+    S.bc[4] = 0xFFFFFFFFu;  // top-p crossing position
+    S.bc[5] = 0xFFFFFFFFu;  // first position with a value dropped by min-p
+    S.bc[6] = 0xFFFFFFFFu;  // draw position
+    S.bc[7] = 0u;           // largest pool key
+  }
+  lds_barrier();
+  uint32_t kmx = 0u;
+  for (int i0 = tid; i0 < C; i0 += 4 * kBlock) {
+    uint32_t kk[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) kk[u] = pool[i0 + u * kBlock < C ? i0 + u * kBlock : 0].x;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (i0 + u * kBlock < C) {
+        if ((kk[u] & 0xFFFFu) == 0u) atomicAdd(&cnt[(kk[u] >> 16) - lo16], 1u);
+        kmx = max(kmx, kk[u]);
+      }
+  }
+  kmx = wave_max(kmx);
+  if (lane() == 0) atomicMax(&S.bc[7], kmx);
+  lds_barrier();
+  // positions in canonical order: position p holds bin top - p, its off-grid
+  // values first (they exceed its grid key), then its grid elements; thread t
+  // holds positions 2t and 2t + 1
+  const uint32_t Kmax = S.bc[7];
+  const uint32_t top = (Kmax >> 16) - lo16;
+  const double M = (double)float_of_key(Kmax);
+  auto bin_of = [&](int pos) { return (int)top - pos; };
+  auto wf_of = [&](uint32_t key) -> uint64_t {
+    return (uint64_t)__double2ll_rn(weight_fast((double)float_of_key(key), M, itau) * kFix);
+  };
+  auto grid_key = [&](int pos) { return (lo16 + (uint32_t)bin_of(pos)) << 16; };
+  auto dropped = [&](uint32_t key) {
+    const double y = (double)float_of_key(key);
+    const double l = (y == M) ? 0.0 : (y - M) / tau;
+    return !(l >= lt);
+  };
+  auto off_in = [&](uint32_t k, int pos) { return (k & 0xFFFFu) != 0u && (int)((k >> 16) - lo16) == bin_of(pos); };
+  // the off-grid value following composite `after` in canonical order within
+  // position pos (0 when none): (key << 32) | ~index
+  auto next_off = [&](int pos, uint64_t after) -> uint64_t {
+    uint64_t best = 0ull;
+    for (int f = 0; f < nfin; ++f) {
+      const uint2 e = pool[f];
+      if (off_in(e.x, pos)) {
+        const uint64_t cm = comp_of(e.x, e.y);
+        if (cm < after && cm > best) best = cm;
+      }
+    }
+    return best;
+  };
+  // Walk the first `lim` elements of position pos (off-grid values, then grid
+  // elements by index) from mass `base`: with `find`, stop at the first
+  // element whose inclusive mass reaches X (exceeds it when strict).  Returns
+  // the elements walked and the mass after them; *idx is the stopping
+  // element's index when it is off grid, else -1 with *gj its grid rank.
+  auto first_j = [&](uint64_t bp, uint64_t wp, uint32_t np, double X, bool strict) -> uint32_t {
+    auto ok = [&](uint32_t j) {
+      const double v = (double)(bp + (uint64_t)j * wp);
+      return strict ? v > X : v >= X;
+    };
+    uint32_t j = 1u;
+    if (wp > 0ull) {
+      const double jd = (X - (double)bp) / (double)wp;
+      j = jd <= 1.0 ? 1u : (jd >= (double)np ? np : (uint32_t)jd);
+    }
+    while (j > 1u && ok(j - 1u)) --j;
+    while (j < np && !ok(j)) ++j;
+    return j;
+  };
+  auto walk = [&](int pos, uint32_t lim, uint64_t base, bool find, double X, bool strict, uint64_t* mass_out,
+                  int* idx, uint32_t* gj) -> uint32_t {
+    uint64_t cum = base;
+    uint32_t j = 0u;
+    uint64_t after = ~0ull;
+    *idx = -1;
+    *gj = 0u;
+    while (j < lim) {
+      const uint64_t nx = next_off(pos, after);
+      if (nx == 0ull) break;
+      ++j;
+      cum += wf_of(comp_key(nx));
+      after = nx;
+      if (find && (strict ? (double)cum > X : (double)cum >= X)) {
+        *idx = (int)comp_idx(nx);
+        *mass_out = cum;
+        return j;
+      }
+    }
+    if (j < lim) {
+      const uint64_t wg = wf_of(grid_key(pos));
+      const uint32_t g = find ? first_j(cum, wg, lim - j, X, strict) : lim - j;
+      cum += (uint64_t)g * wg;
+      j += g;
+      *gj = g;
+    }
+    *mass_out = cum;
+    return j;
+  };
+  uint32_t ct[2], nn[2], fg[2];
+  uint64_t mm[2], wg[2];
+  bool drop[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int pos = 2 * tid + h;
+    const int bn = bin_of(pos);
+    const uint32_t cg = bn >= 0 ? cnt[bn] : 0u;
+    uint32_t co = 0u;
+    uint64_t mo = 0ull;
+    if (bn >= 0) {
+      for (int f = 0; f < nfin; ++f) {  // the few off-grid values of this bin
+        const uint32_t k = pool[f].x;
+        if (off_in(k, pos)) {
+          ++co;
+          mo += wf_of(k);
+        }
+      }
+    }
+    ct[h] = cg + co;
+    fg[h] = co;
+    mm[h] = mo;
+    wg[h] = bn >= 0 ? wf_of(grid_key(pos)) : 0ull;
+    drop[h] = minp && bn >= 0 && dropped(grid_key(pos));
+  }
+  uint32_t tot;
+  const uint32_t a0 = block_excl_scan(ct[0] + ct[1], S.r32, tot);
+  const uint32_t aa[2] = {a0, a0 + ct[0]};
+  // T: every element of the positions above the top-k boundary, the first
+  // `want` minus those above at the boundary, nothing below
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int pos = 2 * tid + h;
+    nn[h] = aa[h] >= want ? 0u : min(ct[h], want - aa[h]);
+    if (fg[h] == 0u || nn[h] == ct[h]) {
+      mm[h] = fg[h] == 0u ? (uint64_t)nn[h] * wg[h] : mm[h] + (uint64_t)(ct[h] - fg[h]) * wg[h];
+    } else if (nn[h] == 0u) {
+      mm[h] = 0ull;
+    } else {  // the boundary inside a mixed bin: walk its first nn elements
+      uint64_t ms;
+      int ix;
+      uint32_t g;
+      walk(pos, nn[h], 0ull, false, 0.0, false, &ms, &ix, &g);
+      mm[h] = ms;
+    }
+  }
+  uint64_t Zk;
+  const uint64_t b0 = block_excl_scan(mm[0] + mm[1], S.r64, Zk);
+  const uint64_t bb[2] = {b0, b0 + mm[0]};
+  const double Xp = (double)c.top_p * (double)Zk;
+  bool hit_p = false, hit_q = false;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int pos = 2 * tid + h;
+    abv[pos] = aa[h];
+    mbf[pos] = bb[h];
+    if (topp && !hit_p && nn[h] > 0u && (double)(bb[h] + mm[h]) >= Xp) {
+      atomicMin(&S.bc[4], (uint32_t)pos);  // top-p: first position whose inclusive mass reaches p Z_k
+      hit_p = true;
+    }
+    if (!hit_q && nn[h] > 0u && drop[h]) {
+      atomicMin(&S.bc[5], (uint32_t)pos);  // min-p: first position whose grid value is dropped
+      hit_q = true;
+    }
+  }
+  lds_barrier();
+  auto n_at = [&](int pos) -> uint32_t {
+    const uint32_t ab = abv[pos];
+    uint32_t co = 0u;
+    for (int f = 0; f < nfin; ++f) co += off_in(pool[f].x, pos) ? 1u : 0u;
+    return ab >= want ? 0u : min(cnt[bin_of(pos)] + co, want - ab);
+  };
+  // kept set S: the shorter of the two prefixes; its end (a bound on the
+  // positions, and when S ends inside a position the elements of S in it)
+  // and mass Z_S
+  int endp = (int)top;  // no cut: S = T
+  uint32_t endn = 0u;   // nonzero: S ends after this many elements of endp
+  uint64_t Zs = Zk;
+  const uint32_t P = S.bc[4], Q = S.bc[5];
+  if (P != 0xFFFFFFFFu) {
+    uint64_t ms;
+    int ix;
+    uint32_t g;
+    const uint32_t j = walk((int)P, n_at((int)P), mbf[P], true, Xp, false, &ms, &ix, &g);
+    endp = (int)P;
+    endn = j;
+    Zs = ms;
+  }
+  if (Q != 0xFFFFFFFFu && (endn == 0u || (int)Q <= endp)) {
+    // min-p: position Q's grid value is dropped; only its off-grid values at
+    // or above the cut (its first ones in canonical order) stay, and nothing
+    // after it
+    uint32_t keep = 0u;
+    for (int f = 0; f < nfin; ++f) {
+      const uint32_t k = pool[f].x;
+      keep += (off_in(k, (int)Q) && !dropped(k)) ? 1u : 0u;
+    }
+    keep = min(keep, n_at((int)Q));
+    if ((int)Q == endp && endn != 0u) keep = min(keep, endn);
+    if (keep > 0u) {
+      uint64_t ms;
+      int ix;
+      uint32_t g;
+      walk((int)Q, keep, mbf[Q], false, 0.0, false, &ms, &ix, &g);
+      Zs = ms;
+      endp = (int)Q;
+      endn = keep;
+    } else {
+      Zs = mbf[Q];
+      endp = (int)Q - 1;
+      endn = 0u;
+    }
+  }
+  // draw: first element of S whose inclusive mass exceeds u Z_S; and the last
+  // position holding elements of S
+  const double Xd = uniform01(c.seed, (uint32_t)b, c.pos, 0) * (double)Zs;
+  bool hit_d = false;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int pos = 2 * tid + h;
+    if (nn[h] > 0u && pos <= endp) {
+      atomicMax(&S.bc[2], (uint32_t)pos);
+      const uint64_t mS = (endn != 0u && pos == endp) ? Zs - bb[h] : mm[h];  // S's part of the end position
+      if (!hit_d && (double)(bb[h] + mS) > Xd) {
+        atomicMin(&S.bc[6], (uint32_t)pos);
+        hit_d = true;
+      }
+    }
+  }
+  lds_barrier();
+  const int last = (int)S.bc[2];
+  int D = (int)S.bc[6];
+  if (D == (int)0xFFFFFFFF || D > last) D = last;
+  const uint32_t jlim = (endn != 0u && D == endp) ? endn : n_at(D);
+  const uint64_t bd = mbf[D];
+  const uint32_t cd = cnt[bin_of(D)];
+  uint64_t md;
+  int dix;
+  uint32_t dgj;
+  walk(D, jlim, bd, true, Xd, true, &md, &dix, &dgj);
+  // every thread has read the bin tables: the index search below (or the
+  // element-wise epilogue) may reuse their memory
+  lds_barrier();
+  if (dix < 0 && dgj == 0u) return false;  // the walk ended on no element (not expected)
+  // the drawn element: an off-grid value directly, else the dgj-th lowest index
+  // among the pool's grid elements of the drawn key (T holds the lowest
+  // indices of the boundary key)
+  uint32_t idx;
+  uint32_t Kdraw;
+  if (dix >= 0) {
+    idx = (uint32_t)dix;
+    uint32_t kd = 0u;
+    for (int f = 0; f < nfin; ++f)
+      if (pool[f].y == idx && off_in(pool[f].x, D)) kd = pool[f].x;
+    Kdraw = kd;
+  } else {
+    const uint32_t Kd = grid_key(D);
+    Kdraw = Kd;
+    const uint32_t j = dgj;
+    if (j == 1u || j == cd) {
+      uint32_t r = j == 1u ? 0xFFFFFFFFu : 0u;
+      for (int i = tid; i < C; i += kBlock) {
+        const uint2 e = pool[i];
+        if (e.x == Kd) r = j == 1u ? min(r, e.y) : max(r, e.y);
+      }
+      idx = j == 1u ? block_min(r, S.r32) : block_max(r, S.r32);
+    } else {
+      auto visit_key = [&](auto&& f) {
+        for (int i = tid; i < C; i += kBlock) {
+          const uint2 e = pool[i];
+          if (e.x == Kd) f(e.x, e.y);
+        }
+      };
+      uint32_t tk2, ti2;
+      radix_select(visit_key, j, cd, Kd, Kd, V, S, &tk2, &ti2);
+      idx = ti2;
+    }
+  }
+  token = (int)idx;
+  logprob = (float)log(weight_fast((double)float_of_key(Kdraw), M, itau) / ((double)Zs / kFix));
+  return true;
+}
 
 // ---------------------------------------------------------------------------
 // Row merge: the whole workgroup, after the row's last unit was written.
@@ -1895,11 +2209,15 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   uint32_t tk = 0u, ti = 0u;
   bool slow = ovf != 0u;
   uint32_t plo = tmax, phi = hi;
+  bool binned = false;  // sampling epilogue done on key bins
+  int btoken = -1;
+  float blogprob = 0.0f;
   if (!empty && want > 0) {
+    uint32_t nfin = 0u;  // patched final values at the front of the pool
     uint32_t C = 0u;
     uint32_t Cv = 0u;  // valid pool elements (C less the invalidated raw copies)
     if (!slow) {
-      C = gather_pool<DT>(a, c, S, NG, pmode == 1, tmax, pool, Cv);
+      C = gather_pool<DT>(a, c, S, NG, pmode == 1, tmax, pool, Cv, nfin);
       if ((int)C > a.pcap || (int)Cv < want) slow = true;
       phi = max(hi, hfmax);  // every pool key lies in [tmax, phi]
     }
@@ -1923,8 +2241,16 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
             if (i0 + u * kBlock < (int)C) f(e[u].x, e[u].y);
         }
       };
-      radix_select(visit_pool, (uint32_t)want, Cv, plo, phi, a.V, S, &tk, &ti);
-      nT = (int)compact_pool(S, pool, (int)C, [&](uint2 e) { return selected(e.x, e.y, tk, ti); });
+      if constexpr (OP == OP_SAMPLE && DT == SS_BF16) {
+        if (!a.out_idx && (phi >> 16) - (tmax >> 16) < (uint32_t)kRBins)
+          binned = sample_binned(c, S, pool, (int)C, (int)nfin, (uint32_t)want, tmax >> 16, a.V, b, btoken, blogprob);
+      }
+      if (binned) {
+        nT = want;  // T is not materialised on this path
+      } else {
+        radix_select(visit_pool, (uint32_t)want, Cv, plo, phi, a.V, S, &tk, &ti);
+        nT = (int)compact_pool(S, pool, (int)C, [&](uint2 e) { return selected(e.x, e.y, tk, ti); });
+      }
     } else {
       flags |= SS_FLAG_FALLBACK;
       nT = slow_select<DT>(a, c, S, pool, NG, pmode, pg, want, &tk, &ti);
@@ -1938,11 +2264,13 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   // 4. row maximum (canonical first element) of the selection
   uint64_t mc = 0ull;
   uint32_t kmin = 0xFFFFFFFFu;
-  for (int i = tid; i < nT; i += kBlock) {
-    mc = max(mc, comp_of(pool[i].x, pool[i].y));
-    kmin = min(kmin, pool[i].x);
+  if (!binned) {
+    for (int i = tid; i < nT; i += kBlock) {
+      mc = max(mc, comp_of(pool[i].x, pool[i].y));
+      kmin = min(kmin, pool[i].x);
+    }
+    block_max_min(mc, kmin, S);
   }
-  block_max_min(mc, kmin, S);
   const uint64_t Mcomp = mc;
   const int argmax = none ? -1 : (int)comp_idx(Mcomp);
   if (empty) flags = SS_FLAG_EMPTY;
@@ -2032,10 +2360,14 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
           }
         }
       }
+    } else if (binned) {
+      token = btoken;
+      logprob = blogprob;
     } else if (!none) {
       // ---- truncation and selection epilogue (Alg. 11 order) on T = pool[0, nT)
       const double M = (double)float_of_key(comp_key(Mcomp));
       const double tau = (double)c.tau;
+      const double itau = 1.0 / tau;
       const bool minp = (c.mode & SS_MINP) && c.min_p > 0.0f;
       const bool topp = (c.mode & SS_TOPP) && c.top_p < 1.0f;
       const double lt = minp ? log((double)c.min_p) : 0.0;
@@ -2049,7 +2381,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
         if (i < nT) {
           const uint2 e = pool[i];
           const double y = (double)float_of_key(e.x);
-          const uint64_t w = (uint64_t)__double2ll_rn(weight_of(y, M, tau) * kFix);
+          const uint64_t w = (uint64_t)__double2ll_rn(weight_fast(y, M, itau) * kFix);
           Wl[i] = w;
           zl += w;
           inT |= 1u << m;
@@ -2109,7 +2441,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
         if (OP == OP_SAMPLE || !has_draft) {
           const uint64_t e = draw((double)Zs);
           token = (int)comp_idx(e);
-          const double w = weight_of((double)float_of_key(comp_key(e)), M, tau);
+          const double w = weight_fast((double)float_of_key(comp_key(e)), M, itau);
           logprob = (float)log(w / Zsd);
           if constexpr (OP == OP_SAMPLE) {
             if (a.out_idx) {
@@ -2133,7 +2465,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
                   const uint64_t cc = srt[rr];
                   a.out_idx[(size_t)b * a.k_out + rr] = (int32_t)comp_idx(cc);
                   a.out_prob[(size_t)b * a.k_out + rr] =
-                      (float)(weight_of((double)float_of_key(comp_key(cc)), M, tau) / Zsd);
+                      (float)(weight_fast((double)float_of_key(comp_key(cc)), M, itau) / Zsd);
                 } else {
                   a.out_idx[(size_t)b * a.k_out + rr] = -1;
                   a.out_prob[(size_t)b * a.k_out + rr] = 0.0f;
@@ -2149,7 +2481,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
           for (int m = 0; m < MT; ++m) {
             const int i = tid + m * kBlock;
             if (((inS >> m) & 1u) && (int)pool[i].y == dtok)
-              pd_local = weight_of((double)float_of_key(pool[i].x), M, tau) / Zsd;
+              pd_local = weight_fast((double)float_of_key(pool[i].x), M, itau) / Zsd;
           }
           const double Pd = block_max(pd_local, S.rd);
           const double qd = (double)qrow[dtok];
@@ -2158,7 +2490,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
           if (!accept) {
             // residual max(0, P - q) over the kept set, canonical order
             auto resid = [&](int i) -> uint64_t {
-              const double P = weight_of((double)float_of_key(pool[i].x), M, tau) / Zsd;
+              const double P = weight_fast((double)float_of_key(pool[i].x), M, itau) / Zsd;
               const double v = P - (double)qrow[pool[i].y];
               return v > 0.0 ? (uint64_t)__double2ll_rn(v * kFix) : 0ull;
             };
@@ -2299,6 +2631,7 @@ __global__ __launch_bounds__(kBlock) void ss_materialize_kernel(KArgs a) {
   const uint32_t* mask = (mode & SS_GRAMMAR) ? a.bitmask + (size_t)row * (size_t)a.mask_ld : nullptr;
   const unsigned char* xrow = reinterpret_cast<const unsigned char*>(a.x) + (size_t)row * (size_t)a.ld * DTT<DT>::ES;
   const RowSummary s = a.summ[row];
+  const double sitau = 1.0 / (double)s.tau;
   const size_t ob = (size_t)row * (size_t)a.V;
   const int Wm = (a.V + 31) >> 5;
   auto emit = [&](uint32_t k, uint32_t i) {
@@ -2308,7 +2641,7 @@ __global__ __launch_bounds__(kBlock) void ss_materialize_kernel(KArgs a) {
       if (s.kind == KIND_GREEDY) {
         p = (int)i == s.argmax ? 1.0f : 0.0f;
       } else if (s.kind == KIND_DIST && k >= kKeyFloor && comp_of(k, i) >= s.thr) {
-        p = (float)(weight_of((double)float_of_key(k), (double)s.M, (double)s.tau) / s.Z);
+        p = (float)(weight_fast((double)float_of_key(k), (double)s.M, sitau) / s.Z);
       }
       a.out_probs[ob + i] = p;
     }
