@@ -134,6 +134,42 @@ def test_sample_configs(ssb, name):
     check_sample(inp, tok, lp, fl, name)
 
 
+def test_sample_penalised_heads(ssb):
+    """bf16 rows whose head tokens are penalised and biased, so their final
+    values leave the bf16 grid and sit next to the top-k, top-p, min-p and
+    draw boundaries; several Philox positions per row."""
+    rng = np.random.default_rng(97)
+    B, V = 48, 1 << 15
+    xf = rng.normal(0.0, 2.0, (B, V))
+    hist, bids, bvals = [], [], []
+    for r in range(B):
+        heads = rng.choice(V, 24, replace=False)
+        xf[r, heads] += rng.uniform(4.0, 10.0, 24)
+        hist.append(np.concatenate([np.repeat(heads, rng.integers(1, 4, 24)), rng.integers(0, V, 100)]).astype(np.int32))
+        bids.append(rng.choice(heads, 8, replace=False).astype(np.int32))
+        bvals.append(rng.uniform(-2.0, 2.0, 8).astype(np.float32))
+    x = W.bf16_bits_from_f32(xf.astype(np.float32))
+    pen = W.MODE_REP | W.MODE_FREQ | W.MODE_PRES | W.MODE_BIAS
+    hoff = np.concatenate([[0], np.cumsum([len(h) for h in hist])]).astype(np.int32)
+    boff = np.concatenate([[0], np.cumsum([len(v) for v in bids])]).astype(np.int32)
+    min_p = np.where(np.arange(B) % 2 == 0, 0.0, rng.uniform(0.01, 0.3, B)).astype(np.float32)
+    inp = W.custom_rows(x, dtype=W.BF16, k_max=512,
+                        mode=np.full(B, W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP | W.MODE_MINP | pen, np.uint32),
+                        temperature=rng.uniform(0.5, 1.5, B).astype(np.float32),
+                        top_k=rng.integers(2, 301, B).astype(np.int32),
+                        top_p=rng.uniform(0.3, 0.99, B).astype(np.float32), min_p=min_p,
+                        rep=rng.uniform(1.05, 1.5, B).astype(np.float32),
+                        freq=rng.uniform(0.0, 0.7, B).astype(np.float32),
+                        pres=rng.uniform(0.0, 0.7, B).astype(np.float32),
+                        hist_offsets=hoff, hist_ids=np.concatenate(hist),
+                        bias_offsets=boff, bias_ids=np.concatenate(bids), bias_vals=np.concatenate(bvals))
+    for pos in range(3):
+        inp["position"] = np.full(B, pos, np.int64)
+        say(f"[penalised-heads] sample B={B} V={V} position={pos}")
+        tok, lp, fl = run_sample(ssb, inp)
+        check_sample(inp, tok, lp, fl, f"penalised-heads-{pos}")
+
+
 def test_sample_kept_distribution_outputs(ssb):
     inp = W.config1(B=16)
     say("[cfg1-B16] sample with k_out=64")
