@@ -161,7 +161,9 @@ def traffic_from(fetch_dir, write_dir, out_path, workload):
     print(json.dumps(out[workload]))
 
 
-def cpu_baseline(inp, reps):
+def cpu_baseline(inp, min_seconds, min_reps=4):
+    """The oracle on the host: whole batches of the same workload (positions
+    varied) until at least `min_seconds` of wall time have passed."""
     import oracle
     nthreads = os.cpu_count() or 1
     omp = os.environ.get("OMP_NUM_THREADS")
@@ -169,10 +171,12 @@ def cpu_baseline(inp, reps):
         nthreads = min(nthreads, int(omp))
     oracle.sample(inp, nthreads=nthreads)  # load + warm
     t0 = time.perf_counter()
-    for r in range(reps):
+    reps = 0
+    while reps < min_reps or time.perf_counter() - t0 < min_seconds:
         inp2 = dict(inp)
-        inp2["position"] = inp["position"] + r
+        inp2["position"] = inp["position"] + reps
         oracle.sample(inp2, nthreads=nthreads)
+        reps += 1
     dt = time.perf_counter() - t0
     rows = reps * inp["B"]
     return dict(value=rows / dt, unit="rows/s", cores=nthreads, kind="oracle",
@@ -319,7 +323,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=32)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-verify", action="store_true", help="skip the secondary verification measurement")
-    ap.add_argument("--cpu-reps", type=int, default=8)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="wall time of the oracle baseline sample")
     ap.add_argument("--traffic-from", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT"),
                     help="write per-launch HBM bytes from two rocprofv3 --pmc runs, then exit")
     args = ap.parse_args()
@@ -383,7 +387,7 @@ def main():
     if not args.no_verify:
         res["verify"] = bench_verify(args, torch, ssb, W)
     if not args.no_cpu:
-        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_reps)
+        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
     print(json.dumps(res), flush=True)
 
 
