@@ -46,7 +46,7 @@
 
 namespace ss {
 
-constexpr int kPBLog = 18;                  // patched-id bitmap: 2^18 bits
+constexpr int kPBLog = 17;                  // patched-id bitmap: 2^17 bits
 constexpr int kPB = 1 << kPBLog;
 constexpr int kUE = 2048;                    // elements per unit (one wavefront)
 constexpr int kMaxU = SS_MAX_V / kUE;        // units per row at most (512)
@@ -598,8 +598,6 @@ struct MSmem {
   int32_t hk[kH];   // patched id (or -1)
   uint32_t hc[kH];  // occurrence count | has-bias bit 31
   uint32_t hf[kH];  // final key
-  uint16_t claim[kH];  // slots claimed by distinct ids, in claim order
-  uint32_t nclaim;
   union {
     uint32_t gtab[kGT];  // candidate slot -> group offset in the row's regions (gather)
     struct {             // radix histograms (selection and the epilogue, after the gather)
@@ -1306,11 +1304,8 @@ __device__ __forceinline__ uint32_t slow_visit(const KArgs& a, const Ctx& c, con
   }
   // 3. patched final values
   if (pmode == 1) {
-    const uint32_t ncl = S.nclaim;
-    for (uint32_t j = tid; j < ncl; j += kBlock) {
-      const uint32_t sl = S.claim[j];
-      if (S.hf[sl] >= kKeyFloor) vop_apply(o, S.hf[sl], (uint32_t)S.hk[sl], acc, off);
-    }
+    for (int sl = tid; sl < kH; sl += kBlock)
+      if (S.hk[sl] >= 0 && S.hf[sl] >= kKeyFloor) vop_apply(o, S.hf[sl], (uint32_t)S.hk[sl], acc, off);
   } else if (pmode == 2) {
     for (int s = tid; s < kGH; s += kBlock) {
       const uint64_t t = pg.tag[s];
@@ -1565,18 +1560,17 @@ __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MS
   // patched final values at or above tmax go first
   uint32_t base = 0u;
   if (patch) {
+    // occupied slots of the patch table, in slot order
     uint32_t cnt = 0u;
-    const uint32_t ncl = S.nclaim;
-    for (uint32_t j = tid; j < ncl; j += kBlock) {
-      const uint32_t k = S.hf[S.claim[j]];
-      cnt += (k >= tmax && k >= kKeyFloor) ? 1u : 0u;
+    for (int sl = tid; sl < kH; sl += kBlock) {
+      const uint32_t k = S.hf[sl];
+      cnt += (S.hk[sl] >= 0 && k >= tmax && k >= kKeyFloor) ? 1u : 0u;
     }
     uint32_t tot;
     uint32_t off = block_excl_scan(cnt, S.r32, tot);
-    for (uint32_t j = tid; j < ncl; j += kBlock) {
-      const uint32_t sl = S.claim[j];
+    for (int sl = tid; sl < kH; sl += kBlock) {
       const uint32_t k = S.hf[sl];
-      if (k >= tmax && k >= kKeyFloor) {
+      if (S.hk[sl] >= 0 && k >= tmax && k >= kKeyFloor) {
         if (off < pcap) pool[off] = make_uint2(k, (uint32_t)S.hk[sl]);
         ++off;
       }
@@ -2031,7 +2025,6 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
     }
     const int pwords = pexact ? (a.V + 31) >> 5 : kPB / 32;
     for (int s = tid; s < (pwords + 3) >> 2; s += kBlock) reinterpret_cast<uint4*>(S.pbits)[s] = make_uint4(0u, 0u, 0u, 0u);
-    if (tid == 0) S.nclaim = 0u;
   }
   // 1. unit records: largest threshold, row maximum, candidate offsets
   uint32_t hi = 0u, tmax = 0u, ovf = 0u;
@@ -2085,7 +2078,6 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
       for (int p = 0; p < kProbe; ++p) {
         const int old = atomicCAS(&S.hk[s], -1, id);
         if (old == -1 || old == id) {
-          if (old == -1) S.claim[atomicAdd(&S.nclaim, 1u)] = (uint16_t)s;
           if (addc) atomicAdd(&S.hc[s], addc);
           if (bias) {
             const uint32_t prev = atomicOr(&S.hc[s], 0x80000000u);
@@ -2107,16 +2099,15 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
     __syncthreads();
     if (S.flagsw == 0u) {
       pmode = 1;
-      const uint32_t ncl = S.nclaim;
 #pragma unroll 1
-      for (uint32_t j0 = 0; j0 < ncl; j0 += 4 * kBlock) {
+      for (int j0 = 0; j0 < kH; j0 += 4 * kBlock) {  // every slot of the patch table
         int id[4], sl[4];
         uint32_t bits[4], mw[4];
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
-          const uint32_t j = j0 + tid + m * kBlock;
-          sl[m] = j < ncl ? (int)S.claim[j] : -1;
-          id[m] = sl[m] >= 0 ? S.hk[sl[m]] : -1;
+          const int j = j0 + tid + m * kBlock;
+          sl[m] = j;
+          id[m] = S.hk[j];
           bits[m] = 0u;
           mw[m] = 0xFFFFFFFFu;
           // unconditional loads (element 0 stands in for an empty slot), so
@@ -2317,13 +2308,14 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
     }
     if (OP == OP_PROCESS && a.patched && tid == 0) a.npatched[row] = 0u;
     if (OP == OP_PROCESS && pmode == 1) {
-      // (id, final key) list for the materialising pass
-      const uint32_t ncl = S.nclaim;
-      for (uint32_t j = tid; j < ncl; j += kBlock) {
-        const uint32_t sl = S.claim[j];
-        a.patched[(size_t)row * kGH + j] = make_uint2((uint32_t)S.hk[sl], S.hf[sl]);
-      }
-      if (tid == 0) a.npatched[row] = ncl;
+      // (id, final key) list for the materialising pass, in slot order
+      uint32_t cnt = 0u;
+      for (int sl = tid; sl < kH; sl += kBlock) cnt += S.hk[sl] >= 0 ? 1u : 0u;
+      uint32_t tot;
+      uint32_t off = block_excl_scan(cnt, S.r32, tot);
+      for (int sl = tid; sl < kH; sl += kBlock)
+        if (S.hk[sl] >= 0) a.patched[(size_t)row * kGH + off++] = make_uint2((uint32_t)S.hk[sl], S.hf[sl]);
+      if (tid == 0) a.npatched[row] = tot;
     } else if (OP == OP_PROCESS && pmode == 2) {
       uint32_t cnt = 0u;
       for (int s = tid; s < kGH; s += kBlock) cnt += (uint32_t)(pg.tag[s] >> 32) == pg.gen ? 1u : 0u;

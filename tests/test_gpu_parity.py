@@ -170,6 +170,39 @@ def test_sample_penalised_heads(ssb):
         check_sample(inp, tok, lp, fl, f"penalised-heads-{pos}")
 
 
+def test_sample_large_vocab_patched(ssb):
+    """V = 2^18 bf16 with penalties and bias: the patched-id bitmap is hashed
+    above 2^17 ids, so pooled raw copies are checked against the hash table."""
+    rng = np.random.default_rng(2718)
+    B, V = 8, 1 << 18
+    xf = rng.normal(0.0, 2.0, (B, V))
+    hist, bids, bvals = [], [], []
+    for r in range(B):
+        heads = rng.choice(V, 16, replace=False)
+        xf[r, heads] += rng.uniform(6.0, 12.0, 16)
+        hist.append(np.concatenate([heads[:8], rng.integers(0, V, 600)]).astype(np.int32))
+        bids.append(rng.choice(V, 12, replace=False).astype(np.int32))
+        bvals.append(rng.uniform(-3.0, 3.0, 12).astype(np.float32))
+    x = W.bf16_bits_from_f32(xf.astype(np.float32))
+    pen = W.MODE_REP | W.MODE_FREQ | W.MODE_PRES | W.MODE_BIAS
+    mode = np.array([W.MODE_GREEDY | pen if r % 4 == 0 else W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP | pen
+                     for r in range(B)], np.uint32)
+    inp = W.custom_rows(x, dtype=W.BF16, k_max=256, mode=mode,
+                        temperature=rng.uniform(0.6, 1.4, B).astype(np.float32),
+                        top_k=rng.integers(2, 257, B).astype(np.int32),
+                        top_p=rng.uniform(0.5, 0.95, B).astype(np.float32),
+                        rep=rng.uniform(1.1, 1.4, B).astype(np.float32),
+                        freq=rng.uniform(0.0, 0.5, B).astype(np.float32),
+                        pres=rng.uniform(0.0, 0.5, B).astype(np.float32),
+                        hist_offsets=np.concatenate([[0], np.cumsum([len(h) for h in hist])]).astype(np.int32),
+                        hist_ids=np.concatenate(hist),
+                        bias_offsets=np.concatenate([[0], np.cumsum([len(v) for v in bids])]).astype(np.int32),
+                        bias_ids=np.concatenate(bids), bias_vals=np.concatenate(bvals))
+    say(f"[large-vocab-patched] sample B={B} V={V}")
+    tok, lp, fl = run_sample(ssb, inp)
+    check_sample(inp, tok, lp, fl, "large-vocab-patched")
+
+
 def test_sample_kept_distribution_outputs(ssb):
     inp = W.config1(B=16)
     say("[cfg1-B16] sample with k_out=64")
