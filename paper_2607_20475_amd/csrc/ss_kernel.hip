@@ -1254,19 +1254,23 @@ __device__ __forceinline__ uint32_t slow_visit(const KArgs& a, const Ctx& c, con
   for (uint32_t f0 = 0; f0 < NG; f0 += kBlock * 4) {
     uint4 g[4];
     bool ok[4];
+    size_t go[4];
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
       const uint32_t fi = f0 + (uint32_t)(tid + m * kBlock);
       ok[m] = false;
-      g[m] = make_uint4(0u, 0u, 0u, 0u);
+      go[m] = 0;
       if (fi < NG) {
         const int u = unit_of_group<DT>(S, U, fi);
         if (!((S.rmask[u >> 5] >> (u & 31)) & 1u)) {
           ok[m] = true;
-          g[m] = rc[(size_t)u * a.cap + (fi - S.uoff[u])];
+          go[m] = (size_t)u * a.cap + (fi - S.uoff[u]);
         }
       }
     }
+    // unconditional loads (group 0 stands in), all in flight together
+#pragma unroll
+    for (int m = 0; m < 4; ++m) g[m] = rc[go[m]];
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
       if (!ok[m]) continue;
@@ -1280,26 +1284,72 @@ __device__ __forceinline__ uint32_t slow_visit(const KArgs& a, const Ctx& c, con
       }
     }
   }
-  // 2. every element of the re-read units
+  // 2. every element of the re-read units: each thread's VW consecutive
+  // elements of a unit in one 16-byte load, kRU units in flight together
   if (nre > 0) {
     const int W = (a.V + 31) >> 5;
-    for (int u = 0; u < U; ++u) {
-      if (!((S.rmask[u >> 5] >> (u & 31)) & 1u)) continue;
-      const int lo = u * kUE;
-      for (int l0 = tid * VW; l0 < kUE; l0 += kBlock * VW) {
-        uint32_t mwd = 0xFFFFFFFFu;
-        if (c.mask) {
-          const int wi = (lo + l0) >> 5;
-          mwd = wi < W ? (c.mask[wi] >> ((lo + l0) & 31)) : 0u;
+    constexpr int kRU = 8;
+    auto next_unit = [&](int from) {  // first re-read unit >= from, or U
+      for (int u = from; u < U; ++u)
+        if ((S.rmask[u >> 5] >> (u & 31)) & 1u) return u;
+      return U;
+    };
+    constexpr int NCH = kUE / (kBlock * VW);  // 16-byte chunks per thread and unit
+    for (int ch = 0; ch < NCH; ++ch) {
+    const int l0 = (ch * kBlock + tid) * VW;
+    for (int u0 = next_unit(0); u0 < U;) {
+      int uj[kRU];
+      uj[0] = u0;
+#pragma unroll
+      for (int j = 1; j < kRU; ++j) uj[j] = uj[j - 1] < U ? next_unit(uj[j - 1] + 1) : U;
+      u0 = uj[kRU - 1] < U ? next_unit(uj[kRU - 1] + 1) : U;
+      uint4 r[kRU];
+      uint32_t mw[kRU];
+#pragma unroll
+      for (int j = 0; j < kRU; ++j) {
+        r[j] = make_uint4(0u, 0u, 0u, 0u);
+        mw[j] = 0xFFFFFFFFu;
+        const int lo = uj[j] * kUE;
+        if (uj[j] < U && l0 < kUE) {
+          if (a.vec_ok && lo + kUE <= a.V) {
+            r[j] = *reinterpret_cast<const uint4*>(c.xrow + (size_t)(lo + l0) * DTT<DT>::ES);
+          } else {
+            uint32_t w4[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int e = 0; e < VW; ++e) {
+              const int i = lo + l0 + e;
+              if (i < a.V) {
+                const uint32_t bits = load_elem_bits<DT>(c.xrow, i);
+                if constexpr (DT == SS_F32) w4[e] = bits;
+                else w4[e >> 1] |= (bits >> 16) << (16 * (e & 1));
+              }
+            }
+            r[j] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+          }
+          if (c.mask) {
+            const int wi = (lo + l0) >> 5;
+            mw[j] = wi < W ? (c.mask[wi] >> ((lo + l0) & 31)) : 0u;
+          }
         }
+      }
+#pragma unroll
+      for (int j = 0; j < kRU; ++j) {
+        if (uj[j] >= U) continue;
+        const int lo = uj[j] * kUE;
+        const uint32_t w4[4] = {r[j].x, r[j].y, r[j].z, r[j].w};
+#pragma unroll
         for (int e = 0; e < VW; ++e) {
           const int i = lo + l0 + e;
-          if (i >= a.V) break;
-          uint32_t k = fold_nan(key_raw(load_elem_bits<DT>(c.xrow, i)));
-          if (!((mwd >> e) & 1u)) k = 0u;
+          if (l0 >= kUE || i >= a.V) break;
+          uint32_t bits;
+          if constexpr (DT == SS_F32) bits = w4[e];
+          else bits = ((w4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu) << 16;
+          uint32_t k = fold_nan(key_raw(bits));
+          if (!((mw[j] >> e) & 1u)) k = 0u;
           if (k >= kKeyFloor && !is_patched<DT>(c, S, pmode, pg, i)) vop_apply(o, k, (uint32_t)i, acc, off);
         }
       }
+    }
     }
   }
   // 3. patched final values
