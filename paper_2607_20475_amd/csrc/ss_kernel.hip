@@ -1756,10 +1756,15 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
   if (lt > 0.0 || nfin > 64) return false;
   const double tau = (double)c.tau;
   const double itau = 1.0 / tau;
-  uint32_t* cnt = S.hist[0];     // grid elements per bin (bin = key16 - lo16)
-  uint32_t* abv = S.hist[1];     // per position: T elements before it
-  uint64_t* mbf = S.mhist;       // per position: T mass before it
-  for (int i = tid; i < kRBins; i += kBlock) cnt[i] = 0u;
+  uint32_t* cnt = S.hist[0];            // grid elements per bin (bin = key16 - lo16)
+  uint32_t* minix = S.hist[0] + kRBins;  // lowest index of each bin's grid elements
+  uint32_t* abv = S.hist[1];            // per position: T elements before it
+  uint64_t* mbf = S.mhist;              // per position: T mass before it
+  static_assert(2 * kRBins <= (kHCopies * kHStride + 3) / 4 * 4, "bin tables fit one histogram row");
+  for (int i = tid; i < kRBins; i += kBlock) {
+    cnt[i] = 0u;
+    minix[i] = 0xFFFFFFFFu;
+  }
   if (tid == 0) {
     S.bc[2] = 0u;           // last position holding elements of S
     S.bc[4] = 0xFFFFFFFFu;  // top-p crossing position
@@ -1770,14 +1775,17 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
   lds_barrier();
   uint32_t kmx = 0u;
   for (int i0 = tid; i0 < C; i0 += 4 * kBlock) {
-    uint32_t kk[4];
+    uint2 ee[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) kk[u] = pool[i0 + u * kBlock < C ? i0 + u * kBlock : 0].x;
+    for (int u = 0; u < 4; ++u) ee[u] = pool[i0 + u * kBlock < C ? i0 + u * kBlock : 0];
 #pragma unroll
     for (int u = 0; u < 4; ++u)
       if (i0 + u * kBlock < C) {
-        if ((kk[u] & 0xFFFFu) == 0u) atomicAdd(&cnt[(kk[u] >> 16) - lo16], 1u);
-        kmx = max(kmx, kk[u]);
+        if ((ee[u].x & 0xFFFFu) == 0u) {
+          atomicAdd(&cnt[(ee[u].x >> 16) - lo16], 1u);
+          atomicMin(&minix[(ee[u].x >> 16) - lo16], ee[u].y);
+        }
+        kmx = max(kmx, ee[u].x);
       }
   }
   kmx = wave_max(kmx);
@@ -1997,6 +2005,7 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
   const uint32_t jlim = (endn != 0u && D == endp) ? endn : n_at(D);
   const uint64_t bd = mbf[D];
   const uint32_t cd = cnt[bin_of(D)];
+  const uint32_t dmin = minix[bin_of(D)];
   uint64_t md;
   int dix;
   uint32_t dgj;
@@ -2020,7 +2029,9 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
     const uint32_t Kd = grid_key(D);
     Kdraw = Kd;
     const uint32_t j = dgj;
-    if (j == 1u || j == cd) {
+    if (j == 1u) {
+      idx = dmin;
+    } else if (j == cd) {
       uint32_t r = j == 1u ? 0xFFFFFFFFu : 0u;
       for (int i = tid; i < C; i += kBlock) {
         const uint2 e = pool[i];
