@@ -2631,7 +2631,7 @@ __global__ __launch_bounds__(kBlock) void ss_merge_kernel(KArgs a) {
   __syncthreads();
   // The streaming kernel placed row r's units on XCD floor(8 r / rows) when
   // its grid splits evenly over the 8 XCDs; the same remap here runs the
-  // row's merge on that XCD, whose L2 still holds the row's candidates.
+  // row's merge on that XCD as well.
   int row = blockIdx.x;
   const int nunits = a.rows * a.U;
   if ((a.rows & 7) == 0 && (nunits & 31) == 0) row = (row & 7) * (a.rows >> 3) + (row >> 3);
