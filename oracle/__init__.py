@@ -40,9 +40,14 @@ class _Params(C.Structure):
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            _build()
-        _lib = C.CDLL(LIB_PATH)
+        # SSREF_LIB: a library built from a modified copy of ssref.c (the
+        # planted-mistake tests load one to check that the pins catch it)
+        path = os.environ.get("SSREF_LIB")
+        if not path:
+            if not os.path.exists(LIB_PATH):
+                _build()
+            path = LIB_PATH
+        _lib = C.CDLL(path)
         _lib.ssref_uniform.restype = C.c_double
         _lib.ssref_uniform.argtypes = [C.c_uint64, C.c_uint32, C.c_int64, C.c_int]
     return _lib

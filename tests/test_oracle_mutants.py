@@ -1,0 +1,46 @@
+"""Planted mistakes: each case compiles a copy of the oracle's C source with
+one plausible error and checks that the pins named for it fail.  This shows
+the pins constrain the oracle, not only that the oracle agrees with itself.
+CPU only; each case is a gcc build plus one pytest subprocess."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "ssref.c")
+
+# (name, text in ssref.c, replacement, pins expected to catch it)
+MUTANTS = [
+    ("draw_takes_ge", "    if (cum > target) { pick = r; break; }", "    if (cum >= target) { pick = r; break; }",
+     "test_draw_golden"),
+    ("min_p_threshold_shifted", "      if (l >= lt) cnt = r + 1; else break;",
+     "      if (l >= lt + 0.05) cnt = r + 1; else break;", "test_min_p_keeps_tokens"),
+    ("top_p_unnormalised", "    double thr = (double)top_p * Zk;", "    double thr = (double)top_p;",
+     "test_top_p_is_minimal_prefix"),
+    ("repetition_penalty_flipped", "v = (v > 0.0f) ? v / rep : v * rep;", "v = (v > 0.0f) ? v * rep : v / rep;",
+     "test_prologue_golden"),
+    ("frequency_term_dropped", "float t = freq * (float)c[i]; v = v - t;", "float t = freq * (float)c[i]; (void)t;",
+     "test_prologue_golden"),
+    ("philox_key_schedule", "    k0 += 0x9E3779B9u;", "    k0 += 0x9E3779B7u;", "test_philox_published_vectors"),
+    ("ties_take_higher_index", "  return (p->i < q->i) ? -1 : (p->i > q->i);", "  return (p->i > q->i) ? -1 : (p->i < q->i);",
+     "test_topk_matches_lexsort or test_greedy_ties_take_lowest_index"),
+]
+
+
+@pytest.mark.parametrize("name,old,new,pins", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(tmp_path, name, old, new, pins):
+    src = open(SRC).read()
+    assert src.count(old) == 1, name
+    mut = tmp_path / "ssref_mut.c"
+    mut.write_text(src.replace(old, new))
+    so = tmp_path / "libssref_mut.so"
+    subprocess.run(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp", "-shared", "-fPIC", "-o", str(so),
+                    str(mut), "-lm"], check=True)
+    env = dict(os.environ, SSREF_LIB=str(so))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py"), "-k", pins],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert "failed" in r.stdout or "passed" in r.stdout, r.stdout[-2000:]  # the selected pins ran
+    assert r.returncode == 1, f"{name}: the pins ({pins}) did not catch the planted mistake\n{r.stdout[-2000:]}"
