@@ -50,7 +50,17 @@ def lib():
         _lib = C.CDLL(path)
         _lib.ssref_uniform.restype = C.c_double
         _lib.ssref_uniform.argtypes = [C.c_uint64, C.c_uint32, C.c_int64, C.c_int]
+        _lib.ssref_near.restype = C.c_double
     return _lib
+
+
+def near():
+    """Width of the near-boundary band inside which a comparison may go either way."""
+    return float(lib().ssref_near())
+
+
+def adm_max():
+    return int(lib().ssref_adm_max())
 
 
 def _ptr(a):
@@ -124,8 +134,15 @@ def uniform(seed, request, position, word):
 
 
 def sample(inp, nthreads=0):
-    """Singular-mode sampling.  Returns dict(token, logprob, flags, margin, n_kept)."""
+    """Singular-mode sampling.
+
+    Returns dict(token, logprob, flags, margin, n_kept, adm_token [B, A],
+    adm_logprob [B, A], n_adm): the oracle's own outcome and every admissible
+    (token, log-probability) outcome when comparisons within ``near()`` of
+    their boundary may go either way (entry 0 is the oracle's own, -1 pads).
+    """
     B, V = int(inp["B"]), int(inp["V"])
+    A = adm_max()
     x = _x(inp)
     bd = _Bundle(inp)
     tok = np.empty(B, np.int32)
@@ -133,22 +150,31 @@ def sample(inp, nthreads=0):
     fl = np.empty(B, np.int32)
     mg = np.empty(B, np.float64)
     nk = np.empty(B, np.int32)
+    at = np.empty((B, A), np.int32)
+    al = np.empty((B, A), np.float32)
+    na = np.empty(B, np.int32)
     lib().ssref_sample(_ptr(x), C.c_int(_dtype_code(inp)), C.c_int64(V), C.byref(bd.p),
-                       _ptr(tok), _ptr(lp), _ptr(fl), _ptr(mg), _ptr(nk), C.c_int(nthreads))
-    return dict(token=tok, logprob=lp, flags=fl, margin=mg, n_kept=nk)
+                       _ptr(tok), _ptr(lp), _ptr(fl), _ptr(mg), _ptr(nk), _ptr(at), _ptr(al), _ptr(na),
+                       C.c_int(nthreads))
+    return dict(token=tok, logprob=lp, flags=fl, margin=mg, n_kept=nk, adm_token=at, adm_logprob=al, n_adm=na)
 
 
-def process_logits(inp, nthreads=0):
-    """Processed logits y [B,V] (float32) and final probabilities P [B,V] (float64)."""
+def process_logits(inp, nthreads=0, force_ns=None):
+    """Processed logits y [B,V] (float32) and final probabilities P [B,V] (float64).
+
+    Also returns ns_range [B, 2], the admissible kept-set sizes.  ``force_ns``
+    ([B] int) replaces a row's kept-set size by another admissible one."""
     B, V = int(inp["B"]), int(inp["V"])
     x = _x(inp)
     bd = _Bundle(inp)
     y = np.empty((B, V), np.float32)
     P = np.empty((B, V), np.float64)
     fl = np.empty(B, np.int32)
+    rng = np.empty((B, 2), np.int32)
+    fns = None if force_ns is None else np.ascontiguousarray(force_ns, dtype=np.int32)
     lib().ssref_process_logits(_ptr(x), C.c_int(_dtype_code(inp)), C.c_int64(V), C.byref(bd.p),
-                               _ptr(y), _ptr(P), _ptr(fl), C.c_int(nthreads))
-    return dict(y=y, P=P, flags=fl)
+                               _ptr(y), _ptr(P), _ptr(fl), _ptr(rng), _ptr(fns), C.c_int(nthreads))
+    return dict(y=y, P=P, flags=fl, ns_range=rng)
 
 
 def topk(inp, nthreads=0):
@@ -164,8 +190,14 @@ def topk(inp, nthreads=0):
 
 
 def verify(inp, nthreads=0):
-    """Multistep verification.  Returns dict(tokens [B,L+1], n_acc [B], flags, margin)."""
+    """Multistep verification.
+
+    Returns dict(tokens [B,L+1], n_acc [B], flags, margin, adm_tokens [B,A,L+1],
+    adm_nacc [B,A], n_adm): the oracle's own outcome and every admissible
+    outcome when comparisons within ``near()`` of their boundary may go either
+    way (entry 0 is the oracle's own)."""
     B, V, L = int(inp["B"]), int(inp["V"]), int(inp["L"])
+    A = adm_max()
     x = _x(inp)
     q = np.ascontiguousarray(inp["draft_probs"], dtype=np.float32)
     d = np.ascontiguousarray(inp["draft_tokens"], dtype=np.int32)
@@ -174,17 +206,21 @@ def verify(inp, nthreads=0):
     na = np.empty(B, np.int32)
     fl = np.empty(B, np.int32)
     mg = np.empty(B, np.float64)
+    aseq = np.empty((B, A, L + 1), np.int32)
+    anacc = np.empty((B, A), np.int32)
+    nadm = np.empty(B, np.int32)
     lib().ssref_verify(_ptr(x), C.c_int(_dtype_code(inp)), C.c_int64(V), _ptr(q), C.c_int64(V),
                        _ptr(d), C.c_int(L), C.byref(bd.p), _ptr(tok), _ptr(na), _ptr(fl), _ptr(mg),
-                       C.c_int(nthreads))
-    return dict(tokens=tok, n_acc=na, flags=fl, margin=mg)
+                       _ptr(aseq), _ptr(anacc), _ptr(nadm), C.c_int(nthreads))
+    return dict(tokens=tok, n_acc=na, flags=fl, margin=mg, adm_tokens=aseq, adm_nacc=anacc, n_adm=nadm)
 
 
 def row_distribution(y, mode, temperature=1.0, top_k=0, top_p=1.0, min_p=0.0, k_cap=None):
     """Truncated distribution of one processed row ``y`` (float32).
 
     Returns dict(order, P (canonical order, length n_s), n_valid, n_k, n_p, n_m,
-    n_s, greedy, flags, M, tau, Z_k, Z_s, margin_p, margin_m).
+    n_s, greedy, flags, ns_lo, ns_hi (admissible kept-set sizes), M, tau, Z_k,
+    Z_s, margin_p, margin_m).
     """
     y = np.ascontiguousarray(y, dtype=np.float32)
     V = y.size
@@ -192,7 +228,7 @@ def row_distribution(y, mode, temperature=1.0, top_k=0, top_p=1.0, min_p=0.0, k_
         k_cap = max(V, 1)
     order = np.empty(max(V, 1), np.int32)
     P = np.empty(max(k_cap, 1), np.float64)
-    cnt = np.empty(7, np.int32)
+    cnt = np.empty(9, np.int32)
     sums = np.empty(6, np.float64)
     nv = lib().ssref_row_distribution(
         _ptr(y), C.c_int(V), C.c_uint32(mode), C.c_float(temperature), C.c_int32(top_k),
@@ -200,6 +236,7 @@ def row_distribution(y, mode, temperature=1.0, top_k=0, top_p=1.0, min_p=0.0, k_
     ns = int(cnt[4])
     return dict(order=order[:nv].copy(), P=P[:ns].copy(), n_valid=int(cnt[0]), n_k=int(cnt[1]),
                 n_p=int(cnt[2]), n_m=int(cnt[3]), n_s=ns, greedy=int(cnt[5]), flags=int(cnt[6]),
+                ns_lo=int(cnt[7]), ns_hi=int(cnt[8]),
                 M=float(sums[0]), tau=float(sums[1]), Z_k=float(sums[2]), Z_s=float(sums[3]),
                 margin_p=float(sums[4]), margin_m=float(sums[5]))
 
@@ -229,3 +266,17 @@ def draw(w, u):
     """Inverse-CDF pick over weights ``w`` for uniform ``u``."""
     w = np.ascontiguousarray(w, dtype=np.float64)
     return int(lib().ssref_draw(_ptr(w), C.c_int(w.size), C.c_double(u)))
+
+
+def draw_ex(w, u):
+    """Inverse-CDF pick with its boundary distance and admissible ranks.
+
+    Returns (pick, margin relative to sum(w), admissible ranks, own pick first)."""
+    w = np.ascontiguousarray(w, dtype=np.float64)
+    A = adm_max()
+    mg = C.c_double()
+    adm = np.empty(A, np.int32)
+    na = C.c_int32()
+    pick = lib().ssref_draw_ex(_ptr(w), C.c_int(w.size), C.c_double(u), C.byref(mg), _ptr(adm), C.c_int(A),
+                               C.byref(na))
+    return int(pick), float(mg.value), [int(v) for v in adm[:na.value]]

@@ -185,8 +185,17 @@ typedef struct {
   double M, tau, Z_k, Z_s;
   double margin_p; /* relative distance of the top-p comparisons to p*Z_k  */
   double margin_m; /* distance of the min-p comparisons to ln(theta)       */
+  int ns_lo, ns_hi; /* admissible kept-set sizes (see ssref_near below)     */
   int flags;
 } dist_t;
+
+/* Near-boundary band.  A data-dependent comparison whose two sides differ by
+ * less than this (relative to the row's normaliser for masses, absolute in
+ * the logit domain for min-p) may go either way in a float32 / fixed-point
+ * implementation; the oracle then admits both outcomes.  Every other
+ * comparison must come out exactly as here. */
+#define SSREF_NEAR 1e-6
+double ssref_near(void) { return SSREF_NEAR; }
 
 static double weight_of(double yr, double M, double tau) {
   if (yr == M) return 1.0;               /* also covers y = M = +inf */
@@ -204,7 +213,12 @@ static void row_distribution(const float *y, const int32_t *order, int n_valid, 
   if (n_valid == 0) { d->flags |= RF_EMPTY; return; }
   d->greedy = (mode & R_GREEDY) || ((mode & R_TEMP) && temperature <= 0.0f);
   d->M = (double)y[order[0]];
-  if (d->greedy) { d->n_k = d->n_p = d->n_m = d->n_s = 1; d->Z_k = d->Z_s = 1.0; w[0] = 1.0; return; }
+  if (d->greedy) {
+    d->n_k = d->n_p = d->n_m = d->n_s = d->ns_lo = d->ns_hi = 1;
+    d->Z_k = d->Z_s = 1.0;
+    w[0] = 1.0;
+    return;
+  }
   d->tau = (mode & R_TEMP) ? (double)temperature : 1.0;
 
   /* Top-k: the k highest logits.  Bounded by the candidate capacity k_cap
@@ -226,33 +240,58 @@ static void row_distribution(const float *y, const int32_t *order, int n_valid, 
   /* Top-p on the top-k renormalised distribution: keep rank r while the mass
    * strictly before it is below p (minimal prefix with mass >= p). */
   d->n_p = d->n_k;
+  int p_lo = d->n_k, p_hi = d->n_k;
   if ((mode & R_TOPP) && top_p < 1.0f) {
     double thr = (double)top_p * Zk;
     double excl = 0.0;
-    int cnt = 0;
+    int cnt = 0, stopped = 0;
+    p_lo = -1;
+    p_hi = -1;
     for (int r = 0; r < d->n_k; ++r) {
       double m = fabs(excl - thr) / Zk;
+      int keep = excl < thr, near = m < SSREF_NEAR;
       if (m < d->margin_p) d->margin_p = m;
-      if (excl < thr) cnt = r + 1; else break;
+      /* admissible cut: the first rank that may stop, the first that must */
+      if (p_lo < 0 && (!keep || near)) p_lo = r;
+      if (p_hi < 0 && !keep && !near) p_hi = r;
+      if (!stopped) {
+        if (keep) cnt = r + 1; else stopped = 1;
+      }
+      if (stopped && p_hi >= 0) break;
       excl += w[r];
     }
+    if (p_lo < 0) p_lo = d->n_k;
+    if (p_hi < 0) p_hi = d->n_k;
     if (cnt < 1) cnt = 1;
+    if (p_lo < 1) p_lo = 1;
+    if (p_hi < 1) p_hi = 1;
     d->n_p = cnt;
   }
 
   /* Min-p in the logit domain: keep r when (y_r - M)/tau >= ln(theta);
    * rank 0 is always kept. */
   d->n_m = d->n_k;
+  int m_lo = d->n_k, m_hi = d->n_k;
   if ((mode & R_MINP) && min_p > 0.0f) {
     double lt = log((double)min_p);
-    int cnt = 1;
+    int cnt = 1, stopped = 0;
+    m_lo = -1;
+    m_hi = -1;
     for (int r = 1; r < d->n_k; ++r) {
       double yr = (double)y[order[r]];
       double l = (yr == d->M) ? 0.0 : (yr - d->M) / d->tau;
       double m = fabs(l - lt);
+      int keep = l >= lt, near = m < SSREF_NEAR;
       if (m < d->margin_m) d->margin_m = m;
-      if (l >= lt) cnt = r + 1; else break;
+      if (m_lo < 0 && (!keep || near)) m_lo = r;
+      if (m_hi < 0 && !keep && !near) m_hi = r;
+      if (!stopped) {
+        if (keep) cnt = r + 1; else stopped = 1;
+      }
+      if (stopped && m_hi >= 0) break;
     }
+    if (m_lo < 0) m_lo = d->n_k;
+    if (m_hi < 0) m_hi = d->n_k;
     d->n_m = cnt;
   }
 
@@ -260,6 +299,11 @@ static void row_distribution(const float *y, const int32_t *order, int n_valid, 
   if (d->n_p < ns) ns = d->n_p;
   if (d->n_m < ns) ns = d->n_m;
   d->n_s = ns;
+  /* every min(n_k, a, b) with a, b in the admissible top-p / min-p ranges */
+  d->ns_lo = d->n_k < p_lo ? d->n_k : p_lo;
+  if (m_lo < d->ns_lo) d->ns_lo = m_lo;
+  d->ns_hi = d->n_k < p_hi ? d->n_k : p_hi;
+  if (m_hi < d->ns_hi) d->ns_hi = m_hi;
   double Zs = 0.0;
   for (int r = 0; r < ns; ++r) Zs += w[r];
   d->Z_s = Zs;
@@ -281,6 +325,35 @@ static int draw_index(const double *w, int n, double Z, double u, double *margin
     *margin = (Z > 0.0) ? m / Z : 0.0;
   }
   return pick;
+}
+
+/* Ranks an inverse-CDF draw over w[0..n) may return when a prefix sum within
+ * `band` of the target u*Z may compare either way: rank r is admissible when
+ * "sum_{s<r} w_s <= target" and "sum_{s<=r} w_s > target" may both hold
+ * (the last rank takes every overshoot).  The draw's own pick comes first in
+ * out[]; returns the count (at most max). */
+static int draw_admissible(const double *w, int n, double Z, double u, double band, int *out, int max) {
+  if (n <= 0 || max <= 0) return 0;
+  const int pick = draw_index(w, n, Z, u, NULL);
+  const double target = u * Z;
+  int cnt = 0;
+  out[cnt++] = pick;
+  double prev = 0.0, cum = 0.0;
+  for (int r = 0; r < n && cnt < max; ++r) {
+    prev = cum;
+    cum += w[r];
+    int before = prev <= target || fabs(prev - target) < band;
+    int after = cum > target || fabs(cum - target) < band || r == n - 1;
+    if (!before) break;
+    if (after && r != pick) out[cnt++] = r;
+  }
+  return cnt;
+}
+
+static double prefix_sum(const double *w, int n) {
+  double z = 0.0;
+  for (int r = 0; r < n; ++r) z += w[r];
+  return z;
 }
 
 /* ------------------------------------------------------------------------- */
@@ -336,11 +409,21 @@ static void process_one(const void *x, int dtype, int64_t row_off, const ssref_p
 /* Batched entry points (OpenMP over rows; rows are independent).              */
 /* ------------------------------------------------------------------------- */
 
-/* Singular-mode sampling.  margin[b]: smallest relative distance of any
- * data-dependent comparison (draw, top-p, min-p) to its boundary. */
+/* Singular-mode sampling.
+ *   margin[b]   smallest relative distance of any data-dependent comparison
+ *               (draw, top-p, min-p) to its boundary;
+ *   adm_tok / adm_lp [B, SSREF_ADM]: the admissible outcomes -- every
+ *               (token, log-probability) the row can produce when each
+ *               comparison within SSREF_NEAR of its boundary may go either
+ *               way; entry 0 is the oracle's own outcome, -1 pads;
+ *   n_adm[b]    number of admissible outcomes (1 unless a comparison is near). */
+#define SSREF_ADM 16
+int ssref_adm_max(void) { return SSREF_ADM; }
+
 int ssref_sample(const void *x, int dtype, int64_t ld, const ssref_params *p,
                  int32_t *out_token, float *out_logprob, int32_t *flags,
-                 double *margin, int32_t *n_kept, int nthreads) {
+                 double *margin, int32_t *n_kept, int32_t *adm_tok, float *adm_lp,
+                 int32_t *n_adm, int nthreads) {
   int B = p->B, V = p->V;
 #ifdef _OPENMP
   if (nthreads > 0) omp_set_num_threads(nthreads);
@@ -359,6 +442,9 @@ int ssref_sample(const void *x, int dtype, int64_t ld, const ssref_params *p,
     double mg = INFINITY;
     int tok = -1;
     float lp = 0.0f;
+    int32_t at[SSREF_ADM];
+    float al[SSREF_ADM];
+    int na = 0;
     if (nv > 0) {
       if (d.greedy) {
         tok = order[0];
@@ -371,13 +457,40 @@ int ssref_sample(const void *x, int dtype, int64_t ld, const ssref_params *p,
         mg = md;
         if (d.margin_p < mg) mg = d.margin_p;
         if (d.margin_m < mg) mg = d.margin_m;
+        /* admissible outcomes: the own kept-set size first, then the others */
+        at[na] = tok;
+        al[na] = lp;
+        ++na;
+        for (int pass = 0; pass < 2; ++pass) {
+          for (int ns = d.ns_lo; ns <= d.ns_hi && na < SSREF_ADM; ++ns) {
+            if ((pass == 0) != (ns == d.n_s)) continue;
+            double Z = prefix_sum(w, ns);
+            int ranks[SSREF_ADM];
+            int nr = draw_admissible(w, ns, Z, u, SSREF_NEAR * Z, ranks, SSREF_ADM);
+            for (int j = 0; j < nr && na < SSREF_ADM; ++j) {
+              int32_t t = order[ranks[j]];
+              float l = (float)log(w[ranks[j]] / Z);
+              int dup = 0;
+              for (int e = 0; e < na; ++e) dup |= (at[e] == t && al[e] == l);
+              if (!dup) { at[na] = t; al[na] = l; ++na; }
+            }
+          }
+        }
       }
     }
+    if (na == 0) { at[0] = tok; al[0] = lp; na = 1; }
     out_token[b] = tok;
     if (out_logprob) out_logprob[b] = lp;
     if (flags) flags[b] = d.flags;
     if (margin) margin[b] = mg;
     if (n_kept) n_kept[b] = d.n_s;
+    if (adm_tok) {
+      for (int e = 0; e < SSREF_ADM; ++e) {
+        adm_tok[(int64_t)b * SSREF_ADM + e] = e < na ? at[e] : -1;
+        if (adm_lp) adm_lp[(int64_t)b * SSREF_ADM + e] = e < na ? al[e] : 0.0f;
+      }
+    }
+    if (n_adm) n_adm[b] = na;
     free(y); free(order); free(w);
   }
   return 0;
@@ -385,9 +498,14 @@ int ssref_sample(const void *x, int dtype, int64_t ld, const ssref_params *p,
 
 /* Materialised processed logits y [B,V] (float32, pre-temperature) and the
  * final truncated distribution P [B,V] (double; zero outside the kept set,
- * one-hot at the argmax for greedy rows). */
+ * one-hot at the argmax for greedy rows).
+ *   ns_range [B,2] or NULL: admissible kept-set sizes (lowest, highest);
+ *   force_ns [B] or NULL:   a kept-set size to use instead of the oracle's own
+ *                           when it lies in the admissible range (values
+ *                           outside it are ignored). */
 int ssref_process_logits(const void *x, int dtype, int64_t ld, const ssref_params *p,
-                         float *out_y, double *out_p, int32_t *flags, int nthreads) {
+                         float *out_y, double *out_p, int32_t *flags, int32_t *ns_range,
+                         const int32_t *force_ns, int nthreads) {
   int B = p->B, V = p->V;
 #ifdef _OPENMP
   if (nthreads > 0) omp_set_num_threads(nthreads);
@@ -403,13 +521,23 @@ int ssref_process_logits(const void *x, int dtype, int64_t ld, const ssref_param
     row_distribution(y, order, nv, effective_mode(p, b), pf(p->temperature, b, 1.0f),
                      p->top_k ? p->top_k[b] : 0, pf(p->top_p, b, 1.0f), pf(p->min_p, b, 0.0f),
                      p->k_cap, w, &d);
+    int ns = d.n_s;
+    double Z = d.Z_s;
+    if (force_ns && !d.greedy && nv > 0 && force_ns[b] >= d.ns_lo && force_ns[b] <= d.ns_hi) {
+      ns = force_ns[b];
+      Z = prefix_sum(w, ns);
+    }
     if (out_p) {
       double *P = out_p + (int64_t)b * V;
       for (int i = 0; i < V; ++i) P[i] = 0.0;
       if (nv > 0) {
         if (d.greedy) P[order[0]] = 1.0;
-        else for (int r = 0; r < d.n_s; ++r) P[order[r]] = w[r] / d.Z_s;
+        else for (int r = 0; r < ns; ++r) P[order[r]] = w[r] / Z;
       }
+    }
+    if (ns_range) {
+      ns_range[2 * (int64_t)b] = d.ns_lo;
+      ns_range[2 * (int64_t)b + 1] = d.ns_hi;
     }
     if (flags) flags[b] = d.flags;
     if (!out_y) free(y);
@@ -452,101 +580,199 @@ int ssref_topk(const void *x, int dtype, int B, int V, int64_t ld, const int32_t
  * penalty history is the request history plus accepted drafts d_1..d_l.
  * Draft ids outside [0, V) end the draft (q = 0 there: the position then
  * samples from the target distribution).  Outputs out_tokens [B, L+1]
- * (-1 padded) and n_acc [B]. */
+ * (-1 padded) and n_acc [B].
+ *
+ * Admissible outcomes: every (out_tokens, n_acc) the request can produce
+ * when each comparison within SSREF_NEAR of its boundary (top-p, min-p,
+ * acceptance u*q(d) <= P(d), the draws; masses relative to the row's
+ * normaliser, the residual draw absolute in probability units) may go either
+ * way.  adm_seq [B, SSREF_ADM, L+1] and adm_nacc [B, SSREF_ADM] hold them,
+ * entry 0 being the oracle's own outcome; n_adm[b] counts them. */
+typedef struct {
+  int ready, nv;
+  dist_t d;
+  float *y;
+  int32_t *order;
+  double *w;
+} vrow_t;
+
+typedef struct {
+  const void *x;
+  int dtype;
+  int64_t ld_row;
+  const float *q;
+  int64_t ld_q;
+  const int32_t *dr;  /* this request's drafts [L] */
+  int L, b, V;
+  const ssref_params *p;
+  uint32_t mode;
+  vrow_t *rows;       /* [L+1], computed when first reached */
+  double *res;
+  int32_t *seq;       /* [SSREF_ADM, L+1] */
+  int32_t *nacc;      /* [SSREF_ADM] */
+  int nseq;
+  int fl;
+  double mg;
+} vctx_t;
+
+static vrow_t *vrow_get(vctx_t *c, int l) {
+  vrow_t *r = &c->rows[l - 1];
+  if (r->ready) return r;
+  int64_t row = (int64_t)c->b * (c->L + 1) + (l - 1);
+  process_one(c->x, c->dtype, row * c->ld_row, c->p, c->b, c->dr, l - 1, row, r->y);
+  r->nv = ssref_order(r->y, c->V, r->order);
+  row_distribution(r->y, r->order, r->nv, c->mode, pf(c->p->temperature, c->b, 1.0f),
+                   c->p->top_k ? c->p->top_k[c->b] : 0, pf(c->p->top_p, c->b, 1.0f),
+                   pf(c->p->min_p, c->b, 0.0f), c->p->k_cap, r->w, &r->d);
+  c->fl |= r->d.flags;
+  if (!r->d.greedy) {
+    if (r->d.margin_p < c->mg) c->mg = r->d.margin_p;
+    if (r->d.margin_m < c->mg) c->mg = r->d.margin_m;
+  }
+  r->ready = 1;
+  return r;
+}
+
+/* records the outcome "drafts 1..l-1 accepted, `emit` at position l" */
+static void vterminal(vctx_t *c, int l, int32_t emit) {
+  int L = c->L;
+  if (c->nseq >= SSREF_ADM) return;
+  int32_t *s = c->seq + (int64_t)c->nseq * (L + 1);
+  for (int j = 0; j <= L; ++j) s[j] = -1;
+  for (int j = 0; j < l - 1; ++j) s[j] = c->dr[j];
+  s[l - 1] = emit;
+  for (int e = 0; e < c->nseq; ++e) {
+    if (c->nacc[e] != l - 1) continue;
+    if (memcmp(c->seq + (int64_t)e * (L + 1), s, sizeof(int32_t) * (size_t)(L + 1)) == 0) return;
+  }
+  c->nacc[c->nseq] = l - 1;
+  c->nseq++;
+}
+
+/* draws at position l over the first ns weights (own pick first) */
+static void vdraw(vctx_t *c, int l, const vrow_t *r, const double *w, int ns, double total, double band, double u) {
+  int ranks[SSREF_ADM];
+  int nr = draw_admissible(w, ns, total, u, band, ranks, SSREF_ADM);
+  for (int j = 0; j < nr; ++j) vterminal(c, l, r->order[ranks[j]]);
+}
+
+static void vexplore(vctx_t *c, int l) {
+  vrow_t *r = vrow_get(c, l);
+  const int L = c->L, b = c->b;
+  const int64_t pos = c->p->position[b] + (l - 1);
+  const int has_draft = (l <= L) && c->dr[l - 1] >= 0 && c->dr[l - 1] < c->V;
+  if (r->nv == 0) {  /* empty target row: rejected, no correction token */
+    vterminal(c, l, -1);
+    return;
+  }
+  if (r->d.greedy) {
+    if (has_draft && c->dr[l - 1] == r->order[0]) vexplore(c, l + 1);
+    else vterminal(c, l, r->order[0]);
+    return;
+  }
+  const double u0 = ssref_uniform(c->p->seed[b], (uint32_t)b, pos, 0);
+  if (!has_draft) {
+    double md;
+    (void)draw_index(r->w, r->d.n_s, r->d.Z_s, u0, &md);
+    if (md < c->mg) c->mg = md;
+    for (int pass = 0; pass < 2; ++pass)
+      for (int ns = r->d.ns_lo; ns <= r->d.ns_hi; ++ns) {
+        if ((pass == 0) != (ns == r->d.n_s)) continue;
+        double Z = prefix_sum(r->w, ns);
+        vdraw(c, l, r, r->w, ns, Z, SSREF_NEAR * Z, u0);
+      }
+    return;
+  }
+  const int dl = c->dr[l - 1];
+  const float *qrow = c->q + (int64_t)b * L * c->ld_q + (int64_t)(l - 1) * c->ld_q;
+  const double qd = (double)qrow[dl];
+  const double a = ssref_uniform(c->p->seed[b], (uint32_t)b, pos, 1);
+  const double lhs = a * qd;
+  int rd = -1;  /* rank of the draft token in the canonical order (top-k range) */
+  for (int k = 0; k < r->d.n_k; ++k)
+    if (r->order[k] == dl) { rd = k; break; }
+  int accept_done = 0;
+  for (int pass = 0; pass < 2; ++pass) {
+    for (int ns = r->d.ns_lo; ns <= r->d.ns_hi; ++ns) {
+      if ((pass == 0) != (ns == r->d.n_s)) continue;
+      double Z = prefix_sum(r->w, ns);
+      double Pd = (rd >= 0 && rd < ns) ? r->w[rd] / Z : 0.0;
+      int acc = Pd > 0.0 && lhs <= Pd;
+      int near = 0;
+      if (Pd > 0.0) {
+        double den = Pd > qd ? Pd : qd;
+        double m = fabs(lhs - Pd) / den;
+        if (m < c->mg) c->mg = m;
+        near = m < SSREF_NEAR;
+      }
+      for (int branch = 0; branch < 2; ++branch) {
+        int take_accept = (branch == 0) ? acc : !acc;
+        if (branch == 1 && !near) break;  /* the other branch only near the boundary */
+        if (take_accept) {
+          if (!accept_done) { accept_done = 1; vexplore(c, l + 1); }
+          continue;
+        }
+        /* residual max(0, P - q) over the kept set, canonical order */
+        double R = 0.0;
+        for (int k = 0; k < ns; ++k) {
+          double P = r->w[k] / Z;
+          double v = P - (double)qrow[r->order[k]];
+          c->res[k] = v > 0.0 ? v : 0.0;
+          R += c->res[k];
+        }
+        double md;
+        if (R > 0.0) {
+          (void)draw_index(c->res, ns, R, u0, &md);
+          if (ns == r->d.n_s && md < c->mg) c->mg = md;
+          vdraw(c, l, r, c->res, ns, R, SSREF_NEAR, u0);
+        }
+        if (R < SSREF_NEAR) vdraw(c, l, r, r->w, ns, Z, SSREF_NEAR * Z, u0);
+      }
+    }
+  }
+}
+
 int ssref_verify(const void *x, int dtype, int64_t ld_row, const float *draft_probs,
                  int64_t ld_q, const int32_t *draft_tokens, int L, const ssref_params *p,
-                 int32_t *out_tokens, int32_t *n_acc, int32_t *flags, double *margin, int nthreads) {
+                 int32_t *out_tokens, int32_t *n_acc, int32_t *flags, double *margin,
+                 int32_t *adm_seq, int32_t *adm_nacc, int32_t *n_adm, int nthreads) {
   int B = p->B, V = p->V;
 #ifdef _OPENMP
   if (nthreads > 0) omp_set_num_threads(nthreads);
 #pragma omp parallel for schedule(dynamic, 1)
 #endif
   for (int b = 0; b < B; ++b) {
-    float *y = (float *)malloc(sizeof(float) * (size_t)V);
-    int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)V);
     int cap = p->k_cap > 0 ? p->k_cap : 1;
-    double *w = (double *)malloc(sizeof(double) * (size_t)cap + 8);
-    double *res = (double *)malloc(sizeof(double) * (size_t)cap + 8);
-    const int32_t *d = draft_tokens + (int64_t)b * L;
-    uint32_t mode = effective_mode(p, b);
-    int fl = 0;
-    double mg = INFINITY;
-    int acc = 0;
-    for (int l = 0; l <= L; ++l) out_tokens[(int64_t)b * (L + 1) + l] = -1;
-
-    for (int l = 1; l <= L + 1; ++l) {
-      int64_t row = (int64_t)b * (L + 1) + (l - 1);
-      process_one(x, dtype, row * ld_row, p, b, d, l - 1, row, y);
-      int nv = ssref_order(y, V, order);
-      dist_t ds;
-      row_distribution(y, order, nv, mode, pf(p->temperature, b, 1.0f), p->top_k ? p->top_k[b] : 0,
-                       pf(p->top_p, b, 1.0f), pf(p->min_p, b, 0.0f), p->k_cap, w, &ds);
-      fl |= ds.flags;
-      if (!ds.greedy) {
-        if (ds.margin_p < mg) mg = ds.margin_p;
-        if (ds.margin_m < mg) mg = ds.margin_m;
-      }
-      int64_t pos = p->position[b] + (l - 1);
-      int has_draft = (l <= L) && d[l - 1] >= 0 && d[l - 1] < V;
-      int emit = -1;
-      int accepted = 0;
-      if (nv == 0) {
-        /* empty target row: rejected, no correction token */
-      } else if (ds.greedy) {
-        if (has_draft && d[l - 1] == order[0]) accepted = 1;
-        else emit = order[0];
-      } else if (!has_draft) {
-        double md;
-        int r = draw_index(w, ds.n_s, ds.Z_s, ssref_uniform(p->seed[b], (uint32_t)b, pos, 0), &md);
-        if (md < mg) mg = md;
-        emit = order[r];
-      } else {
-        int dl = d[l - 1];
-        double Pd = 0.0;
-        for (int r = 0; r < ds.n_s; ++r)
-          if (order[r] == dl) { Pd = w[r] / ds.Z_s; break; }
-        double qd = (double)draft_probs[(int64_t)b * L * ld_q + (int64_t)(l - 1) * ld_q + dl];
-        double a = ssref_uniform(p->seed[b], (uint32_t)b, pos, 1);
-        double lhs = a * qd;
-        if (Pd > 0.0) {
-          double den = (Pd > qd) ? Pd : qd;
-          double m = fabs(lhs - Pd) / den;
-          if (m < mg) mg = m;
-        }
-        if (Pd > 0.0 && lhs <= Pd) {
-          accepted = 1;
-        } else {
-          /* residual max(0, P - q) over the kept set, in canonical order */
-          double R = 0.0;
-          for (int r = 0; r < ds.n_s; ++r) {
-            double P = w[r] / ds.Z_s;
-            double qv = (double)draft_probs[(int64_t)b * L * ld_q + (int64_t)(l - 1) * ld_q + order[r]];
-            double v = P - qv;
-            res[r] = v > 0.0 ? v : 0.0;
-            R += res[r];
-          }
-          double u = ssref_uniform(p->seed[b], (uint32_t)b, pos, 0);
-          double md;
-          int r;
-          if (R > 0.0) r = draw_index(res, ds.n_s, R, u, &md);
-          else r = draw_index(w, ds.n_s, ds.Z_s, u, &md);
-          if (md < mg) mg = md;
-          emit = order[r];
-        }
-      }
-      if (accepted) {
-        out_tokens[(int64_t)b * (L + 1) + (l - 1)] = d[l - 1];
-        acc = l;
-        continue;
-      }
-      out_tokens[(int64_t)b * (L + 1) + (l - 1)] = emit;
-      break;
+    vctx_t c;
+    memset(&c, 0, sizeof(c));
+    c.x = x; c.dtype = dtype; c.ld_row = ld_row; c.q = draft_probs; c.ld_q = ld_q;
+    c.dr = draft_tokens + (int64_t)b * L; c.L = L; c.b = b; c.V = V; c.p = p;
+    c.mode = effective_mode(p, b);
+    c.mg = INFINITY;
+    c.rows = (vrow_t *)calloc((size_t)(L + 1), sizeof(vrow_t));
+    for (int l = 0; l <= L; ++l) {
+      c.rows[l].y = (float *)malloc(sizeof(float) * (size_t)V);
+      c.rows[l].order = (int32_t *)malloc(sizeof(int32_t) * (size_t)V);
+      c.rows[l].w = (double *)malloc(sizeof(double) * (size_t)cap + 8);
     }
-    if (acc > L) acc = L;
-    n_acc[b] = acc;
-    if (flags) flags[b] = fl;
-    if (margin) margin[b] = mg;
-    free(y); free(order); free(w); free(res);
+    c.res = (double *)malloc(sizeof(double) * (size_t)cap + 8);
+    c.seq = (int32_t *)malloc(sizeof(int32_t) * (size_t)SSREF_ADM * (size_t)(L + 1));
+    c.nacc = (int32_t *)malloc(sizeof(int32_t) * SSREF_ADM);
+    vexplore(&c, 1);
+    for (int l = 0; l <= L; ++l) out_tokens[(int64_t)b * (L + 1) + l] = c.seq[l];
+    n_acc[b] = c.nacc[0];
+    if (flags) flags[b] = c.fl;
+    if (margin) margin[b] = c.mg;
+    if (adm_seq) {
+      for (int e = 0; e < SSREF_ADM; ++e)
+        for (int l = 0; l <= L; ++l)
+          adm_seq[((int64_t)b * SSREF_ADM + e) * (L + 1) + l] = e < c.nseq ? c.seq[(int64_t)e * (L + 1) + l] : -1;
+    }
+    if (adm_nacc)
+      for (int e = 0; e < SSREF_ADM; ++e) adm_nacc[(int64_t)b * SSREF_ADM + e] = e < c.nseq ? c.nacc[e] : -1;
+    if (n_adm) n_adm[b] = c.nseq;
+    for (int l = 0; l <= L; ++l) { free(c.rows[l].y); free(c.rows[l].order); free(c.rows[l].w); }
+    free(c.rows); free(c.res); free(c.seq); free(c.nacc);
   }
   return 0;
 }
@@ -555,7 +781,7 @@ int ssref_verify(const void *x, int dtype, int64_t ld_row, const float *draft_pr
  * P[0..n_s) (normalised, canonical order) and the counts/normalisers. */
 int ssref_row_distribution(const float *y, int V, uint32_t mode, float temperature, int32_t top_k,
                            float top_p, float min_p, int k_cap, int32_t *order, double *P,
-                           int32_t *counts /* n_valid,n_k,n_p,n_m,n_s,greedy,flags */,
+                           int32_t *counts /* n_valid,n_k,n_p,n_m,n_s,greedy,flags,ns_lo,ns_hi */,
                            double *sums /* M, tau, Z_k, Z_s, margin_p, margin_m */) {
   int nv = ssref_order(y, V, order);
   double *w = (double *)malloc(sizeof(double) * (size_t)(k_cap > 0 ? k_cap : 1) + 8);
@@ -564,6 +790,7 @@ int ssref_row_distribution(const float *y, int V, uint32_t mode, float temperatu
   for (int r = 0; r < d.n_s; ++r) P[r] = w[r] / d.Z_s;
   counts[0] = d.n_valid; counts[1] = d.n_k; counts[2] = d.n_p; counts[3] = d.n_m;
   counts[4] = d.n_s; counts[5] = d.greedy; counts[6] = d.flags;
+  counts[7] = d.ns_lo; counts[8] = d.ns_hi;
   sums[0] = d.M; sums[1] = d.tau; sums[2] = d.Z_k; sums[3] = d.Z_s;
   sums[4] = d.margin_p; sums[5] = d.margin_m;
   free(w);
@@ -575,4 +802,17 @@ int ssref_draw(const double *w, int n, double u) {
   double Z = 0.0;
   for (int r = 0; r < n; ++r) Z += w[r];
   return draw_index(w, n, Z, u, NULL);
+}
+
+/* The same draw with its boundary distance (relative to sum w) and its
+ * admissible ranks (band SSREF_NEAR relative to sum w; own pick first). */
+int ssref_draw_ex(const double *w, int n, double u, double *margin, int32_t *adm, int max, int32_t *n_adm) {
+  double Z = prefix_sum(w, n);
+  int pick = draw_index(w, n, Z, u, margin);
+  int ranks[SSREF_ADM];
+  if (max > SSREF_ADM) max = SSREF_ADM;
+  int nr = draw_admissible(w, n, Z, u, SSREF_NEAR * Z, ranks, max);
+  for (int j = 0; j < nr; ++j) adm[j] = ranks[j];
+  *n_adm = nr;
+  return pick;
 }

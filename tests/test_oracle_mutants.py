@@ -15,8 +15,8 @@ SRC = os.path.join(ROOT, "oracle", "ssref.c")
 MUTANTS = [
     ("draw_takes_ge", "    if (cum > target) { pick = r; break; }", "    if (cum >= target) { pick = r; break; }",
      "test_draw_golden"),
-    ("min_p_threshold_shifted", "      if (l >= lt) cnt = r + 1; else break;",
-     "      if (l >= lt + 0.05) cnt = r + 1; else break;", "test_min_p_keeps_tokens"),
+    ("min_p_threshold_shifted", "int keep = l >= lt, near = m < SSREF_NEAR;",
+     "int keep = l >= lt + 0.05, near = m < SSREF_NEAR;", "test_min_p_keeps_tokens"),
     ("top_p_unnormalised", "    double thr = (double)top_p * Zk;", "    double thr = (double)top_p;",
      "test_top_p_is_minimal_prefix"),
     ("repetition_penalty_flipped", "v = (v > 0.0f) ? v / rep : v * rep;", "v = (v > 0.0f) ? v * rep : v / rep;",
@@ -26,6 +26,20 @@ MUTANTS = [
     ("philox_key_schedule", "    k0 += 0x9E3779B9u;", "    k0 += 0x9E3779B7u;", "test_philox_published_vectors"),
     ("ties_take_higher_index", "  return (p->i < q->i) ? -1 : (p->i > q->i);", "  return (p->i > q->i) ? -1 : (p->i < q->i);",
      "test_topk_matches_lexsort or test_greedy_ties_take_lowest_index"),
+    # near-boundary band (admissible outcomes) and the Philox counter layout
+    ("top_p_band_always_open", "int keep = excl < thr, near = m < SSREF_NEAR;", "int keep = excl < thr, near = 1;",
+     "test_top_p_boundary_distance or test_sample_admits_both"),
+    ("min_p_band_too_wide", "int keep = l >= lt, near = m < SSREF_NEAR;", "int keep = l >= lt, near = m < 1e-2;",
+     "test_min_p_boundary_distance"),
+    ("draw_band_closed", "    int before = prev <= target || fabs(prev - target) < band;",
+     "    int before = prev <= target;", "test_draw_boundary_distance"),
+    ("draw_margin_always_zero", "    *margin = (Z > 0.0) ? m / Z : 0.0;", "    *margin = 0.0;",
+     "test_draw_boundary_distance"),
+    ("acceptance_band_closed", "        near = m < SSREF_NEAR;", "        near = 0;",
+     "test_verify_admits_accept_and_reject"),
+    ("uniform_counter_words_swapped", "  uint32_t ctr[4] = {request, (uint32_t)((uint64_t)position & 0xFFFFFFFFu),",
+     "  uint32_t ctr[4] = {(uint32_t)((uint64_t)position & 0xFFFFFFFFu), request,",
+     "test_uniform_counter_words"),
 ]
 
 

@@ -51,6 +51,26 @@ def test_uniform_layout_uses_counter_request_position():
     assert len(set(us)) == len(us)
 
 
+@pytest.mark.parametrize("seed,req,position", [
+    (0x0123456789ABCDEF, 5, (1 << 33) + 7),
+    (1234, 63, 1),
+    (0xFFFFFFFF00000001, 1, 0x7FFFFFFFFFFFFFFF),
+])
+def test_uniform_counter_words_are_request_then_position(seed, req, position):
+    """The uniform of (seed, request, position, word) is word `word` of the
+    published Philox4x32-10 block at counter (request, position lo, position
+    hi, 0) under key (seed lo, seed hi) (reading R14), mapped as (w + 1/2) 2^-32.
+    Non-zero request and a position above 2^32 make every counter word matter,
+    so a swapped or shifted word fails here."""
+    ctr = [req, position & 0xFFFFFFFF, position >> 32, 0]
+    key = [seed & 0xFFFFFFFF, seed >> 32]
+    out = oracle.philox4x32_10(ctr, key)
+    for word in range(4):
+        assert oracle.uniform(seed, req, position, word) == (out[word] + 0.5) / 2.0**32
+    swapped = oracle.philox4x32_10([ctr[1], ctr[0], ctr[2], 0], key)
+    assert swapped != out
+
+
 # --------------------------------------------------------------------------
 # Prologue: hand-computed values from the paper's equations
 # --------------------------------------------------------------------------
@@ -406,3 +426,89 @@ def test_truncation_golden(case):
     assert d["n_s"] == case["n_s"]
     if "order" in case:
         assert list(d["order"][: d["n_s"]]) == case["order"]
+
+
+# --------------------------------------------------------------------------
+# Near-boundary band (reading R21): admissible outcomes
+# --------------------------------------------------------------------------
+BND = _load("boundary_cases.json")
+
+
+def test_near_band_width():
+    assert oracle.near() == BND["near"] == 1e-6
+
+
+@pytest.mark.parametrize("case", BND["draw"], ids=lambda c: c["why"][:40])
+def test_draw_boundary_distance_and_admissible_ranks(case):
+    pick, margin, adm = oracle.draw_ex(case["w"], case["u"])
+    assert pick == case["pick"]
+    assert margin == pytest.approx(case["margin"], rel=1e-6)
+    assert adm == case["admissible"]
+
+
+@pytest.mark.parametrize("case", BND["top_p"], ids=lambda c: "p=%.9f" % c["top_p"])
+def test_top_p_boundary_distance_and_admissible_sizes(case):
+    d = oracle.row_distribution(np.array(case["y"], np.float32), W.MODE_TOPP, top_p=case["top_p"])
+    assert d["margin_p"] == pytest.approx(case["margin"], rel=1e-9)
+    assert d["n_s"] == case["n_s"]
+    assert [d["ns_lo"], d["ns_hi"]] == case["ns_range"]
+
+
+@pytest.mark.parametrize("case", BND["min_p"], ids=lambda c: "theta=%.9f" % c["min_p"])
+def test_min_p_boundary_distance_and_admissible_sizes(case):
+    d = oracle.row_distribution(np.array(case["y"], np.float32), W.MODE_MINP, min_p=case["min_p"])
+    assert d["margin_m"] == pytest.approx(case["margin"], rel=1e-9)
+    assert d["n_s"] == case["n_s"]
+    assert [d["ns_lo"], d["ns_hi"]] == case["ns_range"]
+
+
+def _two_token_sample(y, mode, **kw):
+    x = np.array([y], np.float32)
+    return oracle.sample(W.custom_rows(x, W.F32, k_max=2, mode=[mode], **kw))
+
+
+def test_sample_admits_both_kept_sets_at_a_top_p_boundary():
+    """Two equal logits with top-p a hair above 1/2: the kept set is {0, 1}
+    or {0} depending on a comparison 1.2e-7 from its boundary, so token 1 (log
+    1/2) and token 0 (log 1) are both admissible; far from it, one outcome."""
+    near = _two_token_sample([0.0, 0.0], W.MODE_TOPP, top_p=[np.float32(0.5 + 1e-7)], position=[3])
+    outs = set(zip(near["adm_token"][0, :near["n_adm"][0]].tolist(),
+                   np.round(near["adm_logprob"][0, :near["n_adm"][0]], 6).tolist()))
+    assert (0, 0.0) in outs
+    assert near["n_adm"][0] >= 2
+    assert (near["token"][0], round(float(near["logprob"][0]), 6)) == \
+        (near["adm_token"][0, 0], round(float(near["adm_logprob"][0, 0]), 6))
+    far = _two_token_sample([0.0, 0.0], W.MODE_TOPP, top_p=[np.float32(0.75)], position=[3])
+    assert far["n_adm"][0] == 1
+
+
+def _accept_case(delta, seed=None):
+    """B = 1, L = 1, V = 2, equal target logits (P = 1/2 each), draft token 0
+    with q(0) = (1/2)(1 + delta) / a, a the acceptance uniform: a q(0) - P(0)
+    is (1/2) delta, a relative distance of delta a / (1 + delta)."""
+    for s in range(1, 200):
+        a = oracle.uniform(s, 0, 0, 1)
+        if a > 0.6:
+            break
+    q0 = np.float32(0.5 * (1.0 + delta) / a)
+    q = np.array([[[q0, np.float32(1.0) - q0]]], np.float32)
+    t = np.zeros((1, 2, 2), np.float32)
+    inp = W.custom_rows(t.reshape(2, 2), W.F32, k_max=2, mode=[0, 0], position=[0, 0])
+    for k in ("mode", "temperature", "top_k", "top_p", "min_p", "rep", "freq", "pres", "seed", "position"):
+        inp[k] = inp[k][:1]
+    inp["seed"] = np.array([s], np.uint64)
+    inp.update(x=t, B=1, L=1, draft_probs=q, draft_tokens=np.array([[0]], np.int32))
+    return oracle.verify(inp), a
+
+
+def test_verify_admits_accept_and_reject_at_the_acceptance_boundary():
+    out, a = _accept_case(3e-7)
+    seqs = {(tuple(out["adm_tokens"][0, e]), int(out["adm_nacc"][0, e])) for e in range(out["n_adm"][0])}
+    # u q(0) exceeds P(0) by a relative 1.8e-7: rejected, the residual puts all
+    # its mass on token 1; accepted is admissible too (then a bonus token)
+    assert out["n_acc"][0] == 0 and out["tokens"][0].tolist() == [1, -1]
+    assert ((1, -1), 0) in seqs
+    assert any(n == 1 and t[0] == 0 for t, n in seqs)
+    assert out["n_adm"][0] >= 2
+    far, _ = _accept_case(1e-4)
+    assert far["n_adm"][0] == 1 and far["tokens"][0].tolist() == [1, -1]
