@@ -26,11 +26,17 @@
  *   - Launch shapes depend only on (B, V, L, k_max, dtype): every call can be
  *     captured in a HIP graph.  Per-call values (seed, position, params) are
  *     read from device memory.
- *   - The workspace must be zero-filled before its first use (ss_workspace_init,
- *     or a zeroed allocation); every call leaves it zeroed again.  Calls that
+ *   - The workspace needs no initialisation: every call writes what it reads
+ *     (its contents between calls are unspecified), so one workspace of the
+ *     largest size may serve calls of any operation and shape.  Calls that
  *     share one workspace must not overlap in time.
- *   - Probabilities are computed in double; processed logits in float32 (one
- *     correctly rounded operation per prologue step).
+ *   - Processed logits are float32 (one correctly rounded operation per
+ *     prologue step).  Each kept token's weight exp((y - M)/tau) has its
+ *     exponent formed in double and the exponential taken in float32 (about
+ *     1 ulp, relative error below 2e-7; exponents below about -87 give float32
+ *     subnormals and below about -104 zero, i.e. weights under 1e-38 of the
+ *     row maximum's).  Weights are summed exactly as 2^-50 fixed-point
+ *     integers; probabilities, cuts and draws are then taken in double.
  */
 #ifndef SS_H_
 #define SS_H_
@@ -130,7 +136,8 @@ typedef struct ss_params {
  * SS_OP_VERIFY only; dtype is SS_F32 or SS_BF16.  Returns 0 for invalid sizes. */
 size_t ss_workspace_bytes(int op, int B, int V, int L, int k_max, int dtype);
 
-/* Zero-fills a workspace with a kernel on `stream` (no memset node). */
+/* Zero-fills a workspace with a kernel on `stream` (no memset node).  Not
+ * required before use; kept for callers that want deterministic contents. */
 ss_status ss_workspace_init(void *ws, size_t ws_bytes, void *stream);
 
 /*
@@ -191,18 +198,6 @@ ss_status ss_verify(const void *target_logits, int dtype, int64_t ld_row, const 
 ss_status ss_process_logits(const void *logits, int dtype, int64_t ld, const ss_params *p, int k_max,
                             float *out_logits, float *out_probs, int32_t *flags, void *ws,
                             size_t ws_bytes, void *stream);
-
-/*
- * Profiling hook.  When all three handles are non-NULL hipEvent_t values, every
- * later call records `before_stream` on its stream immediately before its
- * streaming kernel, `before_merge` between the streaming kernel and the row
- * merge kernel, and `after_merge` immediately after the merge kernel, so
- * hipEventElapsedTime of consecutive pairs gives each kernel's duration.
- * Three NULLs disable it; a mix of NULL and non-NULL is SS_ERR_INVALID_ARG.
- * The handles stay owned by the caller and must outlive their use.
- * Process-wide, not thread-safe, and not meant for use under graph capture.
- */
-ss_status ss_set_kernel_events(void *before_stream, void *before_merge, void *after_merge);
 
 const char *ss_status_string(ss_status s);
 

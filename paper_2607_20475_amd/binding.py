@@ -65,8 +65,6 @@ def lib():
                                 vp, vp, sz, vp]
         L.ss_process_logits.restype = i32
         L.ss_process_logits.argtypes = [vp, C.c_int, i64, C.POINTER(_Params), C.c_int, vp, vp, vp, vp, sz, vp]
-        L.ss_set_kernel_events.restype = i32
-        L.ss_set_kernel_events.argtypes = [vp, vp, vp]
         L.ss_status_string.restype = C.c_char_p
         L.ss_status_string.argtypes = [i32]
         _lib = L
@@ -239,14 +237,6 @@ def process_logits(logits, params, k_max, out_logits=None, out_probs=None, flags
     _check(lib().ss_process_logits(_ptr(logits), dt, logits.stride(0), C.byref(p), k_max, _ptr(out_logits),
                                    _ptr(out_probs), _ptr(flags), _ptr(ws), ws.numel(), _stream()))
     return out_logits, out_probs, flags
-
-
-def set_kernel_events(before_stream=None, before_merge=None, after_merge=None):
-    """Profiling hook: record three torch.cuda.Event (already recorded once, so
-    their HIP handles exist) around every later call's streaming and merge
-    kernels; no arguments disables it."""
-    ev = [None if e is None else C.c_void_p(e.cuda_event) for e in (before_stream, before_merge, after_merge)]
-    _check(lib().ss_set_kernel_events(*ev))
 
 
 def logits_tensor(d, device="cuda"):

@@ -1,0 +1,14 @@
+// ss_stream.hip -- the streaming kernel for both logit element types.
+#include "ss_impl.hpp"
+#include "ss_launch.hpp"
+
+namespace ss {
+
+template <int DT>
+void launch_stream(const KArgs& k, dim3 grid, dim3 block, hipStream_t st) {
+  hipLaunchKernelGGL(ss_stream_kernel<DT>, grid, block, 0, st, k);
+}
+template void launch_stream<SS_F32>(const KArgs&, dim3, dim3, hipStream_t);
+template void launch_stream<SS_BF16>(const KArgs&, dim3, dim3, hipStream_t);
+
+}  // namespace ss
