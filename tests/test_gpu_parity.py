@@ -1,9 +1,11 @@
 """GPU parity: the HIP path (through the C ABI) against the CPU oracle.
 
 Bars: top-k values/indices, greedy ids, processed logits and verification ids
-are bit-exact; probabilities and log-probabilities agree to 1e-5 relative;
-sampled ids are exact except where the oracle reports a data-dependent
-comparison within 1e-6 of its boundary (counted and printed).
+are bit-exact; probabilities and log-probabilities agree to 1e-5 relative.
+Where a data-dependent comparison (top-p, min-p, the draw, the acceptance
+test) lies within 1e-6 of its boundary the oracle lists every outcome the row
+admits (each such comparison taken both ways); the GPU's outcome must be one
+of them, and those rows are counted.  Counts are printed at the end of the run.
 """
 import sys
 
@@ -17,12 +19,21 @@ from gen import workloads as W
 pytestmark = pytest.mark.gpu
 
 EMPTY, FALLBACK, OUT_TRUNC, KCAP = 1, 2, 4, 8
-NEAR = 1e-6
 
 
 def say(*a):
     print(*a, flush=True)
     sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _counts(parity_counts):
+    global COUNTS
+    COUNTS = parity_counts
+    yield
+
+
+COUNTS = None
 
 
 @pytest.fixture(scope="module")
@@ -46,16 +57,30 @@ def run_sample(ssb, inp, k_out=0):
     return [_np(o) for o in out]
 
 
-def check_sample(inp, tok, lp, fl, label):
+def _admissible(ref, tok, lp):
+    """Per row: the GPU's (token, log-prob) is one of the oracle's admissible outcomes."""
+    A = ref["adm_token"].shape[1]
+    valid = np.arange(A)[None, :] < ref["n_adm"][:, None]
+    al = ref["adm_logprob"].astype(np.float64)
+    lp_ok = np.abs(lp.astype(np.float64)[:, None] - al) <= 1e-5 * np.abs(al) + 1e-6
+    return (valid & (ref["adm_token"] == tok[:, None]) & lp_ok).any(axis=1)
+
+
+def check_sample(inp, tok, lp, fl, label, counts=None):
     ref = oracle.sample(inp)
-    mism = tok != ref["token"]
-    near = mism & (ref["margin"] < NEAR)
-    bad = np.nonzero(mism & ~near)[0]
-    assert bad.size == 0, (label, bad[:10], tok[bad[:10]], ref["token"][bad[:10]], ref["margin"][bad[:10]])
-    same = ~mism
-    np.testing.assert_allclose(lp[same], ref["logprob"][same], rtol=1e-5, atol=1e-6)
+    ok = _admissible(ref, tok, lp)
+    bad = np.nonzero(~ok)[0]
+    assert bad.size == 0, (label, bad[:10], tok[bad[:10]], lp[bad[:10]], ref["token"][bad[:10]],
+                           ref["logprob"][bad[:10]], ref["n_adm"][bad[:10]])
     assert np.array_equal(fl & (EMPTY | KCAP), ref["flags"] & (EMPTY | KCAP)), label
-    say(f"[{label}] rows={tok.size} near-boundary={int(near.sum())} fallback={int(((fl & FALLBACK) > 0).sum())}")
+    near = int((ref["n_adm"] > 1).sum())
+    alt = int((tok != ref["token"]).sum())
+    fb = int(((fl & FALLBACK) > 0).sum())
+    counts = counts or COUNTS
+    if counts is not None:
+        counts.add(label, tok.size, near, alt, fb)
+    say(f"[{label}] rows={tok.size} near-boundary rows={near} (outcome other than the oracle's own: {alt}) "
+        f"fallback={fb}")
     return ref
 
 
@@ -327,6 +352,95 @@ def test_sample_edge_cases(ssb, kind):
     check_sample(inp, tok, lp, fl, kind)
 
 
+def _patched_rows(V, n_distinct, B=4, seed=31, dtype=None):
+    """Rows whose penalty history holds n_distinct[b] distinct ids (including
+    the row's boosted heads, so penalties move the top tokens)."""
+    rng = np.random.default_rng(seed)
+    xf = rng.normal(0.0, 2.0, (B, V))
+    hist, bids, bvals = [], [], []
+    for r in range(B):
+        heads = rng.choice(V, 16, replace=False)
+        xf[r, heads] += rng.uniform(6.0, 12.0, 16)
+        ids = np.unique(np.concatenate([heads, rng.choice(V, n_distinct[r], replace=False)]))[:n_distinct[r]]
+        ids = np.concatenate([ids, heads[:8], ids[:100]])  # some ids repeat
+        hist.append(rng.permutation(ids).astype(np.int32))
+        bids.append(np.concatenate([heads[8:12], heads[8:10], rng.choice(V, 10, replace=False)]).astype(np.int32))
+        bvals.append(rng.uniform(-3.0, 3.0, 16).astype(np.float32))
+    x = W.bf16_bits_from_f32(xf.astype(np.float32))
+    pen = W.MODE_REP | W.MODE_FREQ | W.MODE_PRES | W.MODE_BIAS
+    mode = np.array([W.MODE_GREEDY | pen if r == 0 else W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP | W.MODE_MINP | pen
+                     for r in range(B)], np.uint32)
+    return W.custom_rows(x, dtype=W.BF16, k_max=256, mode=mode,
+                         temperature=rng.uniform(0.6, 1.4, B).astype(np.float32),
+                         top_k=rng.integers(20, 257, B).astype(np.int32),
+                         top_p=rng.uniform(0.5, 0.95, B).astype(np.float32),
+                         min_p=rng.uniform(0.0, 0.05, B).astype(np.float32),
+                         rep=rng.uniform(1.1, 1.4, B).astype(np.float32),
+                         freq=rng.uniform(0.0, 0.5, B).astype(np.float32),
+                         pres=rng.uniform(0.0, 0.5, B).astype(np.float32),
+                         hist_offsets=np.concatenate([[0], np.cumsum([len(h) for h in hist])]).astype(np.int32),
+                         hist_ids=np.concatenate(hist),
+                         bias_offsets=np.concatenate([[0], np.cumsum([len(v) for v in bids])]).astype(np.int32),
+                         bias_ids=np.concatenate(bids), bias_vals=np.concatenate(bvals),
+                         position=np.arange(B))
+
+
+def test_sample_patch_table_modes(ssb):
+    """Histories of 20 000 distinct ids overflow both patch tables (the merge
+    then looks every id up in the lists); 5 000 overflow only the LDS table
+    (the row's table in the workspace); 1 000 fit the LDS table."""
+    inp = _patched_rows(1 << 17, [20000, 20000, 5000, 1000])
+    say("[patch-modes] sample B=4 V=131072 distinct history ids 20000/20000/5000/1000")
+    tok, lp, fl = run_sample(ssb, inp)
+    check_sample(inp, tok, lp, fl, "patch-modes")
+
+
+def test_workspace_contents_do_not_matter(ssb):
+    """A workspace sized for a larger call and filled with arbitrary bytes
+    serves the global-patch-table case: nothing is read before it is written."""
+    inp = _edge_inputs("long_history")
+    n = ssb.workspace_bytes(ssb.OP_SAMPLE, 64, 1 << 17, 0, 1024, ssb.BF16)
+    assert n >= ssb.workspace_bytes(ssb.OP_SAMPLE, inp["B"], inp["V"], 0, inp["k_max"], ssb.BF16)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(3)
+    ws = torch.randint(0, 256, (n,), dtype=torch.uint8, device="cuda", generator=g)
+    big = W.config1()
+    say("[ws-reuse] cfg1 then long_history on one workspace of random bytes")
+    ssb.sample(ssb.logits_tensor(big), ssb.Params.from_arrays(big), big["k_max"], ws=ws)
+    x = ssb.logits_tensor(inp)
+    prm = ssb.Params.from_arrays(inp)
+    for rep in range(2):
+        tok, lp, fl = [_np(t) for t in ssb.sample(x, prm, inp["k_max"], ws=ws)]
+        torch.cuda.synchronize()
+        check_sample(inp, tok, lp, fl, f"ws-reuse-{rep}")
+        ws.random_(0, 256, generator=g)
+
+
+@pytest.mark.parametrize("kind", ["f32_zeros_2e18", "bf16_ties_2e17"])
+def test_flat_rows_full_size(ssb, kind):
+    """The paper's correctness inputs (all zero; U(128.6, 128.7), all 129.0
+    in bf16) at full vocabulary size: every unit overflows its candidate
+    region and the exact slow path resolves the ties by index."""
+    rng = np.random.default_rng(13)
+    B = 4
+    if kind == "f32_zeros_2e18":
+        V, dt = 1 << 18, W.F32
+        x = np.zeros((B, V), np.float32)
+    else:
+        V, dt = 1 << 17, W.BF16
+        x = W.bf16_bits_from_f32(rng.uniform(128.6, 128.7, (B, V)).astype(np.float32))
+    k = np.array([4096, 1024, 1, 3000], np.int32)
+    inp = W.custom_rows(x, dt, k_max=4096, top_k=k)
+    check_topk(ssb, inp, f"topk-flat-{kind}")
+    stoch = W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP
+    smp = W.custom_rows(x, dt, k_max=1024, mode=np.full(B, stoch), top_k=np.array([1024, 1000, 64, 1024]),
+                        top_p=np.array([0.9, 1.0, 0.5, 0.999]), temperature=np.full(B, 0.8), position=np.arange(B))
+    say(f"[flat-{kind}] sample B={B} V={V}")
+    tok, lp, fl = run_sample(ssb, smp)
+    ref = check_sample(smp, tok, lp, fl, f"flat-{kind}")
+    assert (fl & FALLBACK).all()
+
+
 # --------------------------------------------------------------------------
 # Materialised pipeline
 # --------------------------------------------------------------------------
@@ -342,12 +456,25 @@ def test_process_logits(ssb, name):
     torch.cuda.synchronize()
     y, P = _np(y), _np(P)
     ref = oracle.process_logits(inp)
-    smp = oracle.sample(inp)
     assert np.array_equal(y.view(np.uint32), ref["y"].view(np.uint32)), name
-    rows = smp["margin"] >= NEAR
-    err = np.abs(P[rows].astype(np.float64) - ref["P"][rows])
-    assert np.all(err <= 1e-5 * ref["P"][rows] + 1e-38), (name, err.max())
-    say(f"[{name}] ok, near-boundary rows skipped for P: {int((~rows).sum())}")
+    lo, hi = ref["ns_range"][:, 0], ref["ns_range"][:, 1]
+
+    def close(Pr):
+        err = np.abs(P.astype(np.float64) - Pr)
+        return np.all(err <= 1e-5 * Pr + 1e-38, axis=1)
+
+    ok = close(ref["P"])
+    # rows whose kept-set size depends on a comparison within 1e-6 of its
+    # boundary: the GPU's P must equal the oracle's for one admissible size
+    for j in range(int((hi - lo).max()) + 1 if hi.size else 0):
+        alt = oracle.process_logits(inp, force_ns=np.minimum(lo + j, hi))
+        ok |= close(alt["P"])
+    bad = np.nonzero(~ok)[0]
+    assert bad.size == 0, (name, bad[:5])
+    near = int((hi > lo).sum())
+    if COUNTS is not None:
+        COUNTS.add(f"process-{name}", inp["B"], near, 0, int(((_np(fl) & FALLBACK) > 0).sum()))
+    say(f"[{name}] ok, rows with several admissible kept sets: {near}")
 
 
 # --------------------------------------------------------------------------
@@ -365,12 +492,19 @@ def run_verify(ssb, inp):
 
 def check_verify(inp, out, nacc, fl, label):
     ref = oracle.verify(inp)
-    mism = ~(out == ref["tokens"]).all(axis=1) | (nacc != ref["n_acc"])
-    near = mism & (ref["margin"] < NEAR)
-    bad = np.nonzero(mism & ~near)[0]
-    assert bad.size == 0, (label, bad[:5], out[bad[:5]], ref["tokens"][bad[:5]])
+    A = ref["adm_nacc"].shape[1]
+    valid = np.arange(A)[None, :] < ref["n_adm"][:, None]
+    same = (ref["adm_tokens"] == out[:, None, :]).all(axis=2) & (ref["adm_nacc"] == nacc[:, None]) & valid
+    ok = same.any(axis=1)
+    bad = np.nonzero(~ok)[0]
+    assert bad.size == 0, (label, bad[:5], out[bad[:5]], nacc[bad[:5]], ref["tokens"][bad[:5]], ref["n_adm"][bad[:5]])
     assert np.array_equal(fl & (EMPTY | KCAP), ref["flags"] & (EMPTY | KCAP)), label
-    say(f"[{label}] requests={nacc.size} mean accepted={nacc.mean():.2f} near-boundary={int(near.sum())}")
+    near = int((ref["n_adm"] > 1).sum())
+    alt = int((~((out == ref["tokens"]).all(axis=1) & (nacc == ref["n_acc"]))).sum())
+    if COUNTS is not None:
+        COUNTS.add(label, nacc.size, near, alt, int(((fl & FALLBACK) > 0).sum()))
+    say(f"[{label}] requests={nacc.size} mean accepted={nacc.mean():.2f} near-boundary requests={near} "
+        f"(outcome other than the oracle's own: {alt})")
 
 
 def test_verify_config4(ssb):
@@ -408,6 +542,53 @@ def test_verify_edge_cases(ssb):
     say("[verify-edge] B=12 L=3 V=5000")
     out, nacc, fl = run_verify(ssb, inp)
     check_verify(inp, out, nacc, fl, "verify-edge")
+
+
+def test_verify_grammar(ssb):
+    """Verification with an allow bitmask per target row (B (L+1) rows): draft
+    tokens outside a row's allowed set have P(d) = 0 and are always rejected."""
+    rng = np.random.default_rng(57)
+    B, L, V = 8, 3, 1 << 15
+    t = rng.normal(0.0, 2.0, (B, L + 1, V))
+    for b in range(B):
+        for l in range(L + 1):
+            t[b, l, rng.choice(V, 12, replace=False)] += rng.uniform(6.0, 12.0, 12)
+    z = t[:, :L] + rng.normal(0.0, 1.0, (B, L, V))
+    q64 = np.exp(z - z.max(axis=2, keepdims=True))
+    q64 /= q64.sum(axis=2, keepdims=True)
+    q = q64.astype(np.float32)
+    d = np.stack([[rng.choice(V, p=q64[b, l]) for l in range(L)] for b in range(B)]).astype(np.int32)
+    mask = np.zeros((B * (L + 1), V // 32), np.uint32)
+    for r in range(B * (L + 1)):
+        allow = rng.choice(V, V // 4, replace=False)
+        b, l = divmod(r, L + 1)
+        allow = np.concatenate([allow, [int(np.argmax(t[b, l]))]]) if (b + l) % 2 == 0 else allow
+        if l < L and b % 3 == 0:
+            allow = np.concatenate([allow, [d[b, l]]])
+        for i in allow:
+            mask[r, i >> 5] |= np.uint32(1 << (int(i) & 31))
+    mode = np.full(B, W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP | W.MODE_GRAMMAR | W.MODE_REP)
+    mode[1] = W.MODE_GREEDY | W.MODE_GRAMMAR
+    hist = [rng.integers(0, V, 64).astype(np.int32) for _ in range(B)]
+    off = np.zeros(B + 1, np.int32)
+    off[1:] = np.cumsum([len(h) for h in hist])
+    xb = W.bf16_bits_from_f32(t.astype(np.float32))
+    inp = W.custom_rows(xb.reshape(B * (L + 1), V), W.BF16, k_max=256, mode=np.zeros(B * (L + 1)))
+    for k in ("mode", "temperature", "top_k", "top_p", "min_p", "rep", "freq", "pres", "seed", "position"):
+        inp[k] = inp[k][:B]
+    inp["mode"] = mode.astype(np.uint32)
+    inp["temperature"] = np.full(B, 0.9, np.float32)
+    inp["top_k"] = np.full(B, 200, np.int32)
+    inp["top_p"] = np.full(B, 0.95, np.float32)
+    inp["rep"] = np.full(B, 1.3, np.float32)
+    inp["position"] = np.arange(B, dtype=np.int64) * 7
+    inp["hist_offsets"], inp["hist_ids"] = off, np.concatenate(hist)
+    inp["bias_offsets"] = np.zeros(B + 1, np.int32)
+    inp["bitmask"] = mask
+    inp.update(x=xb, B=B, L=L, draft_probs=q, draft_tokens=d)
+    say(f"[verify-grammar] B={B} L={L} V={V}")
+    out, nacc, fl = run_verify(ssb, inp)
+    check_verify(inp, out, nacc, fl, "verify-grammar")
 
 
 # --------------------------------------------------------------------------
