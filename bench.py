@@ -1,33 +1,43 @@
 """Benchmark of the fused sampling hot path on one MI355X.
 
-Default workload: the heterogeneous singular batch -- B=64 requests,
+Headline workload: the heterogeneous singular batch -- B=64 requests,
 V=131072 bf16 logits, half greedy, half stochastic with per-request
 temperature / top-k / top-p / min-p, repetition / frequency / presence
-penalties over a 512-token history and a 16-entry sparse logit bias.
-One step = one ss_sample call (streaming kernel + row merge kernel) on one batch.
+penalties over a 512-token history and a 16-entry sparse logit bias.  One
+step = one ss_sample call (streaming kernel + row merge kernel) on one batch.
 
-Timing: the K steps are captured in HIP graphs over R rotated logit buffers
-(R x 16.8 MB > 2 x the 256 MB Infinity Cache, so every step reads HBM) and
-replayed between two events after warm-up; value = rows / s over the timed
-region.  Each kernel's own duration is then measured over a second timed
-region of eager steps on the same stream and buffers: the library records
-three HIP events per step (before the streaming kernel, between the two
-kernels, after the merge kernel; ss_set_kernel_events), with no host sync
-inside the loop.  The roofline object describes the kernel with the larger
-average duration, its algorithmic bytes per launch over that duration
-against 8 TB/s; both kernels' figures are listed under "kernels".
+The other four workloads are timed the same way and reported under
+"configs": the tiny B=4 V=32768 fp32 sampling case (launch bound), the
+standalone top-k stress (B=256, V=2^18 fp32, k up to 4096), grammar-constrained
+sampling (B=128, V=2^17 bf16, 5 % allow bitmask) and multistep verification
+(B=64, L=4, V=2^17 bf16 target, fp32 draft).
+
+Timing: every workload's steps are captured in HIP graphs over R rotated input
+buffers, R x (bytes per step) >= 2 x the 256 MB Infinity Cache, so no step
+finds its logits in the cache; the graphs are replayed between two HIP events
+on the stream the kernels run on.  The headline times exactly --steps steps
+after --warmup eager steps.  Achieved bandwidth = algorithmic bytes of one
+call (every logit once, the bitmask, per-request parameters, history and bias
+lists, sparse draft-probability gathers, outputs) / measured time per call;
+frac = that / 8 TB/s.  The roofline object describes the headline call (its
+two kernels back to back); the split between the kernels and the HBM traffic
+come from the committed rocprofv3 summaries under profiles/ and are attached
+only while the kernel sources they were taken from are unchanged.  A plain
+streaming read of the same bytes (a measurement kernel outside the sampler
+library) gives the practical ceiling.
 
 Counter mode (--traffic-from FETCH_DIR WRITE_DIR OUT): reads two rocprofv3
 --pmc runs of this script (FETCH_SIZE, then WRITE_SIZE) and writes the HBM
-bytes per launch of both kernels, each counter scaled by what it reads for
-the 16 MiB device copies this script makes, with the kernel-source hash the
-counters belong to.
+bytes per launch of every sampler kernel, each counter scaled by what it reads
+for the plain read of a known byte count this script makes.
 
 Prints one JSON line.
 """
 from __future__ import annotations
 
 import argparse
+import ctypes as C
+import glob
 import hashlib
 import json
 import os
@@ -43,84 +53,80 @@ METRIC = ("µs per batch + rows/sec for fused sample/verify at V=2^17; "
           "achieved HBM GB/s vs peak")
 HBM_PEAK_GBS = 8000.0
 MALL_BYTES = 256 << 20
+CONFIGS = ("cfg0", "cfg1", "cfg2", "cfg3", "cfg4")
+WORKLOAD = {
+    "cfg0": "tiny singular batch: fused sample B=4 V=32768 fp32, per-row temperature {0,0.7,1.0,1.3}, "
+            "top-k 50, top-p 0.9",
+    "cfg1": "heterogeneous singular batch: fused sample B=64 V=131072 bf16, mixed greedy/stochastic, "
+            "penalties, history 512, sparse bias 16",
+    "cfg2": "standalone top-k stress: B=256 V=262144 fp32, half low-entropy / half flat rows, "
+            "k in {1,50,1024,4096}",
+    "cfg3": "grammar-constrained fused sample: B=128 V=131072 bf16, 5% allow bitmask, penalties, bias",
+    "cfg4": "multistep verification: B=64 L=4 V=131072 bf16 target, fp32 draft",
+}
+READ_PROBE_BYTES = 64 << 20  # the plain read whose counters scale FETCH_SIZE
 
 
-def _params_bytes(inp):
-    n = 0
-    for k in ("mode", "temperature", "top_k", "top_p", "min_p", "rep", "freq", "pres", "seed", "position",
-              "hist_offsets", "hist_ids", "bias_offsets", "bias_ids", "bias_vals", "bitmask"):
-        a = inp.get(k)
-        if a is not None:
-            n += np.asarray(a).nbytes
-    return n
+def _nbytes(a):
+    return 0 if a is None else int(np.asarray(a).nbytes)
 
 
-def algorithmic_bytes(inp, out_bytes_per_row=12):
-    """Bytes one pass must move: logits once, sparse lists, params, outputs."""
-    logits = np.asarray(inp["x"]).nbytes
-    return logits, logits + _params_bytes(inp) + out_bytes_per_row * inp["B"]
-
-
-def stream_alg_bytes(inp):
-    """Streaming kernel: every logit once, the bitmask, and the per-row words
-    it reads (mode, top_k, temperature)."""
-    b = np.asarray(inp["x"]).nbytes + 12 * inp["B"]
-    if inp.get("bitmask") is not None:
-        b += np.asarray(inp["bitmask"]).nbytes
-    return b
-
-
-def merge_alg_bytes(inp, out_bytes_per_row=12):
-    """Row merge kernel: per row the candidate set at the method's minimum
-    (k (key, index) pairs of 8 B for a stochastic row, one for a greedy row),
-    the history and bias lists with one logit gather per listed id, the
-    per-request parameters, and the outputs."""
-    B = inp["B"]
-    esz = 2 if inp["dtype"] == "bf16" else 4
-    mode = np.asarray(inp["mode"])
-    tk = np.asarray(inp["top_k"])
-    temp = np.asarray(inp["temperature"])
-    kmax = inp["k_max"]
-    cand = 0
-    for b in range(B):
-        greedy = (mode[b] & 0x040) or ((mode[b] & 0x020) and temp[b] <= 0)
-        if greedy:
-            cand += 8
-        else:
-            k = int(tk[b]) if (mode[b] & 0x080) and tk[b] >= 1 else kmax
-            cand += 8 * min(k, kmax)
-    nh = int(np.asarray(inp["hist_offsets"])[-1]) if inp.get("hist_offsets") is not None else 0
-    nb = int(np.asarray(inp["bias_offsets"])[-1]) if inp.get("bias_offsets") is not None else 0
-    lists = nh * (4 + esz) + nb * (8 + esz) + 8 * (B + 1)
-    return cand + lists + 48 * B + out_bytes_per_row * B
+def algorithmic_bytes(name, inp):
+    """Bytes one call must move at the method's minimum: every logit once, the
+    grammar bitmask, the per-request parameters (48 B per request), history
+    and bias CSR lists, the draft-probability gathers of verification
+    (q at the kept set and the draft token: at most k_max + 1 floats per draft
+    position) and the outputs."""
+    B = int(inp["B"])
+    if name == "cfg2":
+        k = np.minimum(np.asarray(inp["top_k"]), inp["k_max"])
+        return _nbytes(inp["x"]) + _nbytes(inp["top_k"]) + 8 * int(k.sum())
+    b = _nbytes(inp["x"]) + 48 * B + _nbytes(inp.get("bitmask"))
+    for k in ("hist_offsets", "hist_ids", "bias_offsets", "bias_ids", "bias_vals"):
+        b += _nbytes(inp.get(k))
+    if name == "cfg4":
+        L = int(inp["L"])
+        return b + _nbytes(inp["draft_tokens"]) + B * L * (inp["k_max"] + 1) * 4 + B * (L + 2) * 4
+    return b + 12 * B  # token, log-probability, flags
 
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for p in ("paper_2607_20475_amd/csrc/ss_kernel.hip", "paper_2607_20475_amd/csrc/ss_device.hpp"):
-        with open(os.path.join(ROOT, p), "rb") as f:
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2607_20475_amd", "csrc", "ss_*"))):
+        with open(p, "rb") as f:
+            h.update(os.path.basename(p).encode())
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def load_traffic(workload, kernel):
-    """HBM bytes per launch of one kernel from the committed rocprofv3 counter
-    summary, or None when the kernel source changed since it was taken."""
-    p = os.path.join(ROOT, "profiles", "traffic.json")
+def load_profile(name):
+    """Committed per-kernel figures of one workload (rocprofv3 kernel-trace
+    averages and counter traffic), or None when the kernel sources changed."""
+    p = os.path.join(ROOT, "profiles", "kernels.json")
     if not os.path.exists(p):
         return None
     with open(p) as f:
         d = json.load(f)
-    e = d.get(workload, {}).get(kernel)
+    e = d.get(name)
     if not e or e.get("kernel_hash") != kernel_source_hash():
         return None
-    return e.get("bytes_per_launch")
+    return e
 
 
-def traffic_from(fetch_dir, write_dir, out_path, workload):
-    """Per-launch HBM bytes of both kernels from two rocprofv3 --pmc runs."""
+# ---------------------------------------------------------------------------
+# rocprofv3 summaries -> profiles/kernels.json
+# ---------------------------------------------------------------------------
+def _kernel_key(n):
+    for k in ("ss_stream_kernel", "ss_merge_kernel", "ss_assemble_kernel", "ss_materialize_kernel",
+              "bench_read_kernel", "bench_write_kernel"):
+        if k in n:
+            return n[:n.index("(")] if "(" in n else n
+    return None
+
+
+def traffic_from(fetch_dir, write_dir, out_path, name):
+    """Per-launch HBM bytes of every sampler kernel from two rocprofv3 --pmc runs."""
     import csv
-    import glob
 
     def per_kernel(d, counter):
         f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
@@ -131,48 +137,74 @@ def traffic_from(fetch_dir, write_dir, out_path, workload):
             for r in csv.DictReader(fh):
                 if r["Counter_Name"] != counter:
                     continue
-                n = r["Kernel_Name"]
-                key = ("stream" if "ss_stream_kernel" in n else "merge" if "ss_merge_kernel" in n
-                       else "copy" if "copyBuffer" in n and int(r["Grid_Size"]) > 0 else None)
-                if key is None:
+                k = _kernel_key(r["Kernel_Name"])
+                if k is None:
                     continue
-                acc.setdefault(key, []).append(float(r["Counter_Value"]) * 1024.0)
+                acc.setdefault(k, []).append(float(r["Counter_Value"]) * 1024.0)
         return acc
 
     fe, wr = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
-    copy_bytes = 16 << 20  # the bench's logit-buffer clones: 64 x 131072 bf16
-    # the largest copies are the 16 MiB clones (smaller ones are parameter uploads)
-    cf = sorted(fe["copy"])[-1] / copy_bytes
-    cw = sorted(wr["copy"])[-1] / copy_bytes
+    rk = [k for k in fe if "bench_read_kernel" in k][0]
+    wk = [k for k in wr if "bench_write_kernel" in k][0]
+    cf = float(np.median(fe[rk])) / READ_PROBE_BYTES  # FETCH_SIZE bytes per byte read
+    cw = float(np.median(wr[wk])) / READ_PROBE_BYTES  # WRITE_SIZE bytes per byte written
     out = {}
     if os.path.exists(out_path):
         with open(out_path) as fh:
             out = json.load(fh)
-    ent = {}
-    for k in ("stream", "merge"):
+    ent = out.get(name, {})
+    traffic = {}
+    for k in fe:
+        if k in (rk, wk):
+            continue
         f = float(np.mean(fe[k])) / cf
-        w = float(np.mean(wr[k])) / cw
-        ent[k] = dict(bytes_per_launch=f + w, fetch_bytes=f, write_bytes=w, launches=len(fe[k]),
-                      kernel_hash=kernel_source_hash())
-    ent["copy_scale"] = dict(fetch=cf, write=cw, copy_bytes=copy_bytes)
-    out[workload] = ent
+        w = float(np.mean(wr.get(k, [0.0]))) / cw
+        traffic[k] = dict(bytes_per_launch=f + w, fetch_bytes=f, write_bytes=w, launches=len(fe[k]))
+    ent["traffic"] = traffic
+    ent["fetch_scale"] = cf
+    ent["write_scale"] = cw
+    ent["kernel_hash"] = kernel_source_hash()
+    out[name] = ent
     with open(out_path, "w") as fh:
-        json.dump(out, fh, indent=1)
-    print(json.dumps(out[workload]))
+        json.dump(out, fh, indent=1, sort_keys=True)
+    print(json.dumps(ent))
 
 
-def cpu_baseline(inp, min_seconds, min_reps=4):
+def stats_from(stats_csv, out_path, name):
+    """Per-kernel average durations from a rocprofv3 --stats kernel_stats.csv."""
+    import csv
+    out = {}
+    if os.path.exists(out_path):
+        with open(out_path) as fh:
+            out = json.load(fh)
+    ent = out.get(name, {})
+    ks = {}
+    with open(stats_csv) as fh:
+        for r in csv.DictReader(fh):
+            k = _kernel_key(r["Name"])
+            if k is None:
+                continue
+            ks[k] = dict(calls=int(r["Calls"]), avg_us=float(r["AverageNs"]) / 1000.0,
+                         min_us=float(r["MinNs"]) / 1000.0, max_us=float(r["MaxNs"]) / 1000.0)
+    ent["kernels"] = ks
+    ent["kernel_hash"] = kernel_source_hash()
+    out[name] = ent
+    with open(out_path, "w") as fh:
+        json.dump(out, fh, indent=1, sort_keys=True)
+    print(json.dumps(ent))
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle on the host
+# ---------------------------------------------------------------------------
+def cpu_baseline(inp, seconds, nthreads, min_reps=2):
     """The oracle on the host: whole batches of the same workload (positions
-    varied) until at least `min_seconds` of wall time have passed."""
+    varied) until `seconds` of wall time have passed."""
     import oracle
-    nthreads = os.cpu_count() or 1
-    omp = os.environ.get("OMP_NUM_THREADS")
-    if omp and omp.isdigit():
-        nthreads = min(nthreads, int(omp))
     oracle.sample(inp, nthreads=nthreads)  # load + warm
     t0 = time.perf_counter()
     reps = 0
-    while reps < min_reps or time.perf_counter() - t0 < min_seconds:
+    while reps < min_reps or time.perf_counter() - t0 < seconds:
         inp2 = dict(inp)
         inp2["position"] = inp["position"] + reps
         oracle.sample(inp2, nthreads=nthreads)
@@ -180,155 +212,200 @@ def cpu_baseline(inp, min_seconds, min_reps=4):
     dt = time.perf_counter() - t0
     rows = reps * inp["B"]
     return dict(value=rows / dt, unit="rows/s", cores=nthreads, kind="oracle",
-                sample=f"{reps} batches x {inp['B']} rows of the same workload (positions varied), "
-                       f"{dt:.2f} s wall on {nthreads} threads")
+                sample=f"{reps} batches x {inp['B']} rows of the headline workload (positions varied), "
+                       f"{dt:.2f} s wall on {nthreads} thread(s)")
 
 
-def bench_sample(args, torch, ssb, W):
-    inp = W.config1()
-    B, V, kmax = inp["B"], inp["V"], inp["k_max"]
-    dev = "cuda"
-    x0 = ssb.logits_tensor(inp, dev)
-    buf_bytes = x0.numel() * x0.element_size()
-    R = max(2, -(-2 * MALL_BYTES // buf_bytes))
-    xs = [x0] + [x0.clone() for _ in range(R - 1)]
-    prm = ssb.Params.from_arrays(inp, dev)
-    ws = ssb.workspace(ssb.OP_SAMPLE, B, V, 0, kmax, ssb.BF16, dev)
-    tok = torch.empty(B, dtype=torch.int32, device=dev)
-    lp = torch.empty(B, dtype=torch.float32, device=dev)
-    fl = torch.empty(B, dtype=torch.int32, device=dev)
+# ---------------------------------------------------------------------------
+# GPU timing
+# ---------------------------------------------------------------------------
+class Runner:
+    """Rotated inputs and a step function for one workload."""
 
-    def step(i):
-        ssb.sample(xs[i % R], prm, kmax, out_token=tok, out_logprob=lp, flags=fl, ws=ws)
+    def __init__(self, name, torch, ssb, W, dev="cuda"):
+        self.name = name
+        self.inp = inp = W.make_config(name)
+        self.B = inp["B"]
+        t = torch
+        x0 = ssb.logits_tensor(inp, dev)
+        per_step = x0.numel() * x0.element_size() + _nbytes(inp.get("bitmask"))
+        self.R = max(2, -(-2 * MALL_BYTES // per_step))
+        self.xs = [x0] + [x0.clone() for _ in range(self.R - 1)]
+        self.rows_per_step = inp["B"]
+        if name == "cfg2":
+            k = t.from_numpy(np.ascontiguousarray(inp["top_k"], np.int32)).to(dev)
+            ws = ssb.workspace(ssb.OP_TOPK, inp["B"], inp["V"], 0, inp["k_max"], ssb.F32, dev)
+            ov = t.empty(inp["B"], inp["k_max"], dtype=t.float32, device=dev)
+            oi = t.empty(inp["B"], inp["k_max"], dtype=t.int32, device=dev)
+            fl = t.empty(inp["B"], dtype=t.int32, device=dev)
 
-    for i in range(args.warmup):
-        step(i)
+            def step(i):
+                ssb.topk(self.xs[i % self.R], k, inp["k_max"], out_val=ov, out_idx=oi, flags=fl, ws=ws)
+        elif name == "cfg4":
+            L = inp["L"]
+            q = t.from_numpy(np.ascontiguousarray(inp["draft_probs"], np.float32)).to(dev)
+            d = t.from_numpy(np.ascontiguousarray(inp["draft_tokens"], np.int32)).to(dev)
+            prm = ssb.Params.from_arrays(inp, dev)
+            ws = ssb.workspace(ssb.OP_VERIFY, inp["B"], inp["V"], L, inp["k_max"], ssb.BF16, dev)
+            out = t.empty(inp["B"], L + 1, dtype=t.int32, device=dev)
+            na = t.empty(inp["B"], dtype=t.int32, device=dev)
+            fl = t.empty(inp["B"], dtype=t.int32, device=dev)
+            self.rows_per_step = inp["B"] * (L + 1)
+
+            def step(i):
+                ssb.verify(self.xs[i % self.R], q, d, prm, inp["k_max"], out_tokens=out, out_nacc=na, flags=fl,
+                           ws=ws)
+        else:
+            prm = ssb.Params.from_arrays(inp, dev)
+            if inp.get("bitmask") is not None:
+                # the bitmask rotates with the logits (a new grammar state per step)
+                self.masks = [prm.bitmask] + [prm.bitmask.clone() for _ in range(self.R - 1)]
+            dt = ssb.BF16 if inp["dtype"] == "bf16" else ssb.F32
+            ws = ssb.workspace(ssb.OP_SAMPLE, inp["B"], inp["V"], 0, inp["k_max"], dt, dev)
+            tok = t.empty(inp["B"], dtype=t.int32, device=dev)
+            lp = t.empty(inp["B"], dtype=t.float32, device=dev)
+            fl = t.empty(inp["B"], dtype=t.int32, device=dev)
+
+            def step(i):
+                if inp.get("bitmask") is not None:
+                    prm.bitmask = self.masks[i % self.R]
+                ssb.sample(self.xs[i % self.R], prm, inp["k_max"], out_token=tok, out_logprob=lp, flags=fl, ws=ws)
+        self.step = step
+        self.flags = fl
+
+    def time(self, torch, steps, warmup):
+        """Mean µs per step over exactly `steps` graph-replayed steps."""
+        for i in range(warmup):
+            self.step(i)
+        torch.cuda.synchronize()
+        R = self.R
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for i in range(R):
+                self.step(i)
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        g_full = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_full):
+            for i in range(R):
+                self.step(i)
+        n_full, rem = divmod(steps, R)
+        g_rem = None
+        if rem:
+            g_rem = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_rem):
+                for i in range(rem):
+                    self.step(i)
+        g_full.replay()  # the last buffers of the cycle are the ones left in the cache
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n_full):
+            g_full.replay()
+        if g_rem is not None:
+            g_rem.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return 1000.0 * e0.elapsed_time(e1) / steps
+
+
+def _probe_lib():
+    lib = C.CDLL(os.path.join(ROOT, "paper_2607_20475_amd", "libss_bench.so"))
+    lib.bench_read.restype = C.c_int
+    lib.bench_read.argtypes = [C.c_void_p, C.c_size_t, C.c_int, C.c_uint32, C.c_void_p, C.c_void_p]
+    lib.bench_write.restype = C.c_int
+    lib.bench_write.argtypes = [C.c_void_p, C.c_size_t, C.c_int, C.c_uint32, C.c_void_p]
+    return lib
+
+
+def counter_probes(torch, nbytes):
+    """One plain read and one plain write of `nbytes` each (counter scales)."""
+    lib = _probe_lib()
+    buf = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+    sink = torch.zeros(256, dtype=torch.int32, device="cuda")
+    st = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if lib.bench_write(C.c_void_p(buf.data_ptr()), nbytes, 1024, 3, st) != 0:
+        raise RuntimeError("bench_write failed")
+    if lib.bench_read(C.c_void_p(buf.data_ptr()), nbytes, 1024, 0xDEADBEEF, C.c_void_p(sink.data_ptr()), st) != 0:
+        raise RuntimeError("bench_read failed")
     torch.cuda.synchronize()
 
-    # graphs of G steps cycling through the buffers
-    G = min(R, args.steps)
-    s = torch.cuda.Stream()
-    s.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(s):
-        for i in range(G):
-            step(i)
-    torch.cuda.current_stream().wait_stream(s)
-    torch.cuda.synchronize()
-    g_full = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g_full):
-        for i in range(G):
-            step(i)
-    rem = args.steps % G
-    g_rem = None
-    if rem:
-        g_rem = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g_rem):
-            for i in range(rem):
-                step(i)
-    n_full = args.steps // G
-    for _ in range(2):
-        g_full.replay()
-    torch.cuda.synchronize()
 
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(n_full):
-        g_full.replay()
-    if g_rem is not None:
-        g_rem.replay()
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1)
-    ms_per_step = ms / args.steps
+def read_ceiling(torch, nbytes, reps=50):
+    """GB/s of a plain streaming read of `nbytes` from rotated buffers."""
+    lib = _probe_lib()
+    nbytes = (nbytes + 15) & ~15
+    R = max(2, -(-2 * MALL_BYTES // nbytes))
+    bufs = [torch.ones(nbytes // 4, dtype=torch.int32, device="cuda") for _ in range(R)]
+    sink = torch.zeros(256, dtype=torch.int32, device="cuda")
+    blocks = min(8192, max(256, nbytes // (16 * 256 * 4)))
 
-    # per-kernel durations: three events per step recorded by the library
-    n_k = min(args.steps, 256)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_k)]
-    for e3 in evs:
-        for e in e3:
-            e.record()  # creates the HIP event handles
-    torch.cuda.synchronize()
-    try:
-        for i in range(n_k):
-            ssb.set_kernel_events(*evs[i])
-            step(i)
-    finally:
-        ssb.set_kernel_events()
-    torch.cuda.synchronize()
-    stream_ms = [e[0].elapsed_time(e[1]) for e in evs]
-    merge_ms = [e[1].elapsed_time(e[2]) for e in evs]
-    kernel_us = {"stream": 1000.0 * float(np.mean(stream_ms)), "merge": 1000.0 * float(np.mean(merge_ms)),
-                 "stream_median": 1000.0 * float(np.median(stream_ms)),
-                 "merge_median": 1000.0 * float(np.median(merge_ms)), "launches": n_k}
-    return inp, ms_per_step, kernel_us, R, fl
+    def go(i):
+        st = C.c_void_p(torch.cuda.current_stream().cuda_stream)  # the capture stream inside a graph
+        rc = lib.bench_read(C.c_void_p(bufs[i % R].data_ptr()), nbytes, blocks, 0xDEADBEEF,
+                            C.c_void_p(sink.data_ptr()), st)
+        if rc != 0:
+            raise RuntimeError("bench_read failed")
 
-
-def bench_verify(args, torch, ssb, W):
-    inp = W.config4()
-    B, L, V, kmax = inp["B"], inp["L"], inp["V"], inp["k_max"]
-    dev = "cuda"
-    x0 = ssb.logits_tensor(inp, dev)
-    q = torch.from_numpy(np.ascontiguousarray(inp["draft_probs"])).to(dev)
-    d = torch.from_numpy(np.ascontiguousarray(inp["draft_tokens"])).to(dev)
-    R = max(2, -(-2 * MALL_BYTES // (x0.numel() * x0.element_size())))
-    xs = [x0] + [x0.clone() for _ in range(R - 1)]
-    prm = ssb.Params.from_arrays(inp, dev)
-    ws = ssb.workspace(ssb.OP_VERIFY, B, V, L, kmax, ssb.BF16, dev)
-    out = torch.empty(B, L + 1, dtype=torch.int32, device=dev)
-    na = torch.empty(B, dtype=torch.int32, device=dev)
-    fl = torch.empty(B, dtype=torch.int32, device=dev)
-
-    def step(i):
-        ssb.verify(xs[i % R], q, d, prm, kmax, out_tokens=out, out_nacc=na, flags=fl, ws=ws)
-
-    for i in range(max(4, args.warmup // 4)):
-        step(i)
-    torch.cuda.synchronize()
-    s = torch.cuda.Stream()
-    s.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(s):
-        for i in range(R):
-            step(i)
-    torch.cuda.current_stream().wait_stream(s)
+    for i in range(2 * R):
+        go(i)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
         for i in range(R):
-            step(i)
+            go(i)
     g.replay()
     torch.cuda.synchronize()
-    reps = max(1, args.steps // (4 * R))
+    n = max(1, reps // R)
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record()
-    for _ in range(reps):
+    for _ in range(n):
         g.replay()
     e1.record()
     torch.cuda.synchronize()
-    us = 1000.0 * e0.elapsed_time(e1) / (reps * R)
-    logits = x0.numel() * x0.element_size()
-    gathers = B * L * (kmax + 1) * 4  # upper bound of q gathered on the kept sets
-    alg = logits + _params_bytes(inp) + d.numel() * 4 + B * (L + 2) * 4 + gathers
-    return dict(workload="multistep verification B=64 L=4 V=131072 bf16 target, fp32 draft",
-                us_per_batch=us, requests_per_s=B / (us * 1e-6), rows_per_s=B * (L + 1) / (us * 1e-6),
-                alg_bytes=alg, GBps=alg / (us * 1e-6) / 1e9, steps=reps * R)
+    us = 1000.0 * e0.elapsed_time(e1) / (n * R)
+    return dict(bytes=nbytes, us=us, GBps=nbytes / (us * 1e-6) / 1e9, frac=nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS)
+
+
+def config_entry(name, run, us):
+    alg = algorithmic_bytes(name, run.inp)
+    gbps = alg / (us * 1e-6) / 1e9
+    fb = int(((run.flags.cpu().numpy() & 2) > 0).sum())
+    e = dict(workload=WORKLOAD[name], us_per_batch=us, rows_per_s=run.rows_per_step / (us * 1e-6),
+             alg_bytes=alg, GBps=gbps, frac=gbps / HBM_PEAK_GBS, rotated_buffers=run.R, fallback_rows=fb)
+    if name == "cfg4":
+        e["requests_per_s"] = run.B / (us * 1e-6)
+    prof = load_profile(name)
+    if prof:
+        e["profile"] = prof
+    return e
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=1024)
-    ap.add_argument("--warmup", type=int, default=32)
+    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--config", default="all", choices=("all",) + CONFIGS,
+                    help="time one workload only (profiling runs); 'all' times the five")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
-    ap.add_argument("--no-verify", action="store_true", help="skip the secondary verification measurement")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="wall time of the oracle baseline sample")
-    ap.add_argument("--traffic-from", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT"),
+    ap.add_argument("--read-probe", action="store_true",
+                    help="also make one plain read and one plain write of a known byte count (counter scales "
+                         "for --traffic-from)")
+    ap.add_argument("--traffic-from", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "OUT", "CONFIG"),
                     help="write per-launch HBM bytes from two rocprofv3 --pmc runs, then exit")
+    ap.add_argument("--stats-from", nargs=3, metavar=("KERNEL_STATS_CSV", "OUT", "CONFIG"),
+                    help="write per-kernel average durations from a rocprofv3 --stats run, then exit")
     args = ap.parse_args()
     if args.traffic_from:
-        traffic_from(*args.traffic_from, workload="cfg1_sample")
+        traffic_from(*args.traffic_from)
+        return
+    if args.stats_from:
+        stats_from(*args.stats_from)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py: this build runs on one GPU only; --gpus must be 1 "
@@ -341,53 +418,63 @@ def main():
     from paper_2607_20475_amd import binding as ssb
     ssb.lib()
 
-    inp, ms_per_step, kernel_us, R, fl = bench_sample(args, torch, ssb, W)
-    B = inp["B"]
-    logits_b, path_b = algorithmic_bytes(inp)
-    us = ms_per_step * 1000.0
-    fallback_rows = int(((fl.cpu().numpy() & ssb.FLAG_FALLBACK) > 0).sum())
-    names = {"stream": "ss_stream_kernel<bf16>", "merge": "ss_merge_kernel<bf16, sample>"}
-    alg = {"stream": stream_alg_bytes(inp), "merge": merge_alg_bytes(inp)}
-    kern = {}
-    for k in ("stream", "merge"):
-        a = alg[k] / (kernel_us[k] * 1e-6) / 1e9
-        kern[k] = {"kernel": names[k], "us": kernel_us[k], "us_median": kernel_us[k + "_median"],
-                   "alg_bytes_per_launch": alg[k], "achieved": a, "frac": a / HBM_PEAK_GBS,
-                   "traffic": load_traffic("cfg1_sample", k)}
-    dom = max(("stream", "merge"), key=lambda k: kernel_us[k])
-    d = kern[dom]
+    names = CONFIGS if args.config == "all" else (args.config,)
+    head = "cfg1" if "cfg1" in names else names[0]
+    entries = {}
+    for name in names:
+        run = Runner(name, torch, ssb, W)
+        if name == head:
+            us = run.time(torch, args.steps, args.warmup)
+        else:
+            us = run.time(torch, max(run.R, 64), 4)
+        entries[name] = config_entry(name, run, us)
+        entries[name]["steps"] = args.steps if name == head else max(run.R, 64)
+        print(f"bench: {name} {us:.2f} us per batch", file=sys.stderr, flush=True)
+        del run
+        torch.cuda.empty_cache()
+    if args.read_probe:
+        counter_probes(torch, READ_PROBE_BYTES)
 
+    h = entries[head]
+    inp = W.make_config(head)
+    us = h["us_per_batch"]
+    prof = h.get("profile") or {}
+    split = prof.get("kernels")
+    traffic = None
+    if prof.get("traffic"):
+        traffic = sum(v["bytes_per_launch"] for k, v in prof["traffic"].items() if "ss_" in k)
     res = {
         "metric": METRIC,
-        "value": B / (ms_per_step * 1e-3),
+        "value": h["rows_per_s"],
         "unit": "rows/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": us / 1000.0,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": inp["dtype"],
         "data": "synthetic",
-        "config": {"workload": "heterogeneous singular batch: fused sample B=64 V=131072 bf16, "
-                               "mixed greedy/stochastic, penalties, history 512, sparse bias 16",
-                   "B": B, "V": inp["V"], "k_max": inp["k_max"], "rotated_buffers": R},
+        "config": {"workload": WORKLOAD[head], "B": inp["B"], "V": inp["V"], "k_max": inp["k_max"],
+                   "rotated_buffers": h["rotated_buffers"]},
         "us_per_batch": us,
-        "path_GBps": path_b / (us * 1e-6) / 1e9,
-        "path_frac": path_b / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
-        "path_alg_bytes": path_b,
-        "fallback_rows": fallback_rows,
-        "roofline": {"bound": "hbm", "kernel": d["kernel"], "achieved": d["achieved"], "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": d["frac"], "traffic": d["traffic"],
-                     "alg_bytes_per_launch": d["alg_bytes_per_launch"], "kernel_us": d["us"],
-                     "launches_timed": kernel_us["launches"]},
-        "kernels": kern,
+        "roofline": {"bound": "hbm", "kernel": "ss_sample call: ss_stream_kernel + ss_merge_kernel (back to back)",
+                     "achieved": h["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": h["frac"],
+                     "traffic": traffic, "alg_bytes_per_launch": h["alg_bytes"], "us_per_launch": us,
+                     "launches_timed": args.steps, "kernel_split_us": split},
+        "fallback_rows": h["fallback_rows"],
+        "configs": {k: v for k, v in entries.items() if k != head},
     }
-    if not args.no_verify:
-        res["verify"] = bench_verify(args, torch, ssb, W)
-    if not args.no_cpu:
-        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+    if head in ("cfg1", "cfg2"):
+        res["read_ceiling"] = read_ceiling(torch, h["alg_bytes"])
+    if not args.no_cpu and head != "cfg2" and head != "cfg4":
+        nthreads = os.cpu_count() or 1
+        omp = os.environ.get("OMP_NUM_THREADS")
+        if omp and omp.isdigit():
+            nthreads = min(nthreads, int(omp))
+        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds, nthreads)
+        res["cpu_baseline_1thread"] = cpu_baseline(inp, args.cpu_seconds / 2, 1)
     print(json.dumps(res), flush=True)
 
 
