@@ -199,6 +199,22 @@ ss_status ss_process_logits(const void *logits, int dtype, int64_t ld, const ss_
                             float *out_logits, float *out_probs, int32_t *flags, void *ws,
                             size_t ws_bytes, void *stream);
 
+/*
+ * ss_sample with no workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops and harnesses
+ * that forbid allocation).  The workspace is an SS_NOALLOC_BYTES array in the
+ * library's device memory, one copy per GPU, held until the process ends;
+ * this call allocates and frees nothing.  Arguments and results are those of
+ * ss_sample.  SS_ERR_WORKSPACE when ss_workspace_bytes(SS_OP_SAMPLE, B, V, 0,
+ * k_max, dtype) exceeds SS_NOALLOC_BYTES (B = 64, V = 2^17, k_max = 1024
+ * fits).  Every call on one GPU uses that GPU's single array: calls that
+ * overlap in time on one GPU (other streams, other threads) race.
+ */
+#define SS_NOALLOC_BYTES (32u << 20)
+ss_status ss_sample_noalloc(const void *logits, int dtype, int64_t ld, const ss_params *p, int k_max,
+                            int32_t *out_token, float *out_logprob, int32_t *out_idx, float *out_prob,
+                            int k_out, int32_t *flags, void *stream);
+
 const char *ss_status_string(ss_status s);
 
 #ifdef __cplusplus

@@ -60,6 +60,10 @@ def lib():
         L.ss_sample.restype = i32
         L.ss_sample.argtypes = [vp, C.c_int, i64, C.POINTER(_Params), C.c_int, vp, vp, vp, vp, C.c_int, vp,
                                 vp, sz, vp]
+        if hasattr(L, "ss_sample_noalloc"):
+            L.ss_sample_noalloc.restype = i32
+            L.ss_sample_noalloc.argtypes = [vp, C.c_int, i64, C.POINTER(_Params), C.c_int, vp, vp, vp, vp, C.c_int,
+                                            vp, vp]
         L.ss_verify.restype = i32
         L.ss_verify.argtypes = [vp, C.c_int, i64, vp, i64, vp, C.c_int, C.POINTER(_Params), C.c_int, vp, vp,
                                 vp, vp, sz, vp]
@@ -195,6 +199,17 @@ def sample(logits, params, k_max, k_out=0, out_token=None, out_logprob=None, out
                            ws.numel(), _stream()))
     if k_out > 0:
         return out_token, out_logprob, flags, out_idx, out_prob
+    return out_token, out_logprob, flags
+
+
+def sample_noalloc(logits, params, k_max, out_token, out_logprob, flags, k_out=0, out_idx=None, out_prob=None):
+    """ss_sample_noalloc: sampling into caller-provided outputs with the
+    library's own per-GPU workspace (nothing is allocated by this call)."""
+    B, V = logits.shape
+    p = params.struct()
+    _check(lib().ss_sample_noalloc(_ptr(logits), _dtype_code(logits), logits.stride(0), C.byref(p), k_max,
+                                   _ptr(out_token), _ptr(out_logprob), _ptr(out_idx), _ptr(out_prob), k_out,
+                                   _ptr(flags), _stream()))
     return out_token, out_logprob, flags
 
 

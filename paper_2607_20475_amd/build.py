@@ -41,6 +41,7 @@ def units() -> list[tuple[str, str, list[str]]]:
         ("ss_api", "ss_api.hip", []),
         ("ss_stream", "ss_stream.hip", []),
         ("ss_aux", "ss_aux.hip", []),
+        ("ss_noalloc", "ss_noalloc.hip", []),
     ]
     for dn, dv in _DT.items():
         for on, ov in _OP.items():
