@@ -1200,6 +1200,136 @@ __device__ __forceinline__ int unit_of_group(const MSmem& S, int U, uint32_t f) 
   return lo;
 }
 
+// ---------------------------------------------------------------------------
+// One batch of candidate groups held in registers: kGS groups, kGPer per
+// thread (slot tid + kBlock m), with their group offsets (~0u: no group).
+constexpr int kGPer = kGS / kBlock;
+struct GBatch {
+  uint32_t go[kGPer];
+  uint4 g[kGPer];
+};
+
+// Slot -> group offset table of the row's candidate regions (TPU threads per
+// unit), when the row's groups fit it.
+__device__ __forceinline__ void gather_table(const KArgs& a, MSmem& S, int U, uint32_t NG) {
+  if (NG > (uint32_t)kGT) return;
+  const int tid = threadIdx.x;
+  const int TPU = U >= kBlock ? 1 : kBlock / U;
+  for (int x = tid; x < U * TPU; x += kBlock) {
+    const int u = x / TPU, sub = x - u * TPU;
+    const uint32_t o = S.uoff[u], n = S.uoff[u + 1] - o;
+    for (uint32_t j = (uint32_t)sub; j < n; j += (uint32_t)TPU) S.gtab[o + j] = (uint32_t)u * a.cap + j;
+  }
+  lds_barrier();
+}
+
+// Issues the loads of the batch starting at group f0 (every load in flight,
+// nothing waits for them here).
+template <int DT>
+__device__ __forceinline__ void gather_issue(const KArgs& a, const MSmem& S, int row, int U, uint32_t NG, uint32_t f0,
+                                             GBatch& gb) {
+  const int tid = threadIdx.x;
+  const uint4* rc = a.cand + (size_t)row * U * a.cap;
+  const uint32_t nb = f0 < NG ? min((uint32_t)kGS, NG - f0) : 0u;
+  const bool table = NG <= (uint32_t)kGT;
+#pragma unroll
+  for (int m = 0; m < kGPer; ++m) {
+    const uint32_t q = (uint32_t)(tid + m * kBlock);
+    gb.go[m] = 0xFFFFFFFFu;
+    if (q < nb) {
+      if (table) {
+        gb.go[m] = S.gtab[f0 + q];
+      } else {
+        const int u = unit_of_group<DT>(S, U, f0 + q);
+        gb.go[m] = (uint32_t)u * a.cap + (f0 + q - S.uoff[u]);
+      }
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < kGPer; ++m) gb.g[m] = rc[gb.go[m] == 0xFFFFFFFFu ? 0u : gb.go[m]];
+}
+
+// ---------------------------------------------------------------------------
+// Greedy rows whose emitted maxima are all patched ids with final values
+// below the raw maximum (a repetition penalty on the top token): the
+// processed maximum then lies below every unit threshold that the pool
+// covers.  Each unit emitted the groups holding its maximum, so the best
+// unpatched emitted element B bounds every unit whose maximum is at most B;
+// only the units whose maximum exceeds B (their maximum is patched) are
+// re-read whole.  Returns the composite of the processed maximum over the
+// unpatched raw values and the patched finals (LDS patch table, when `patch`).
+// Units that overflowed their candidate regions are marked for re-reading
+// already, and are re-read as well.
+// ---------------------------------------------------------------------------
+template <int DT>
+__device__ __forceinline__ uint64_t greedy_refill(const KArgs& a, const Ctx& c, MSmem& S, uint32_t NG, bool patch) {
+  constexpr int GE = DTT<DT>::GE, VW = DTT<DT>::VW;
+  const int tid = threadIdx.x;
+  const int U = a.U;
+  const bool exact = c.pexact;
+  auto key_of = [](const uint4& gq, int e) -> uint32_t {
+    if constexpr (DT == SS_BF16) return (((e < 2 ? gq.y : gq.z) >> (16 * (e & 1))) & 0xFFFFu) << 16;
+    else return e ? gq.z : gq.y;
+  };
+  uint64_t best = 0ull;
+  // 1. the best unpatched element among the emitted groups (the slot table
+  // is rebuilt: the fast path may not have run)
+  gather_table(a, S, U, NG);
+  for (uint32_t f0 = 0; f0 < NG; f0 += (uint32_t)kGS) {
+    GBatch gb;
+    gather_issue<DT>(a, S, c.row, U, NG, f0, gb);
+#pragma unroll
+    for (int m = 0; m < kGPer; ++m) {
+      if (gb.go[m] == 0xFFFFFFFFu) continue;
+#pragma unroll
+      for (int e = 0; e < GE; ++e) {
+        const uint32_t k = key_of(gb.g[m], e), i = gb.g[m].x + (uint32_t)e;
+        if (k >= kKeyFloor && !(patch && lds_patched(S, (int)i, exact))) best = max(best, comp_of(k, i));
+      }
+    }
+  }
+  best = block_max(best, S.r64);
+  const uint32_t kb = comp_key(best);
+  // 2. units whose maximum exceeds B
+  for (int u = tid; u < U; u += kBlock) {
+    const uint32_t t = a.rec[(size_t)c.row * U + u].x;
+    if (t != kNoEmit && t > kb) atomicOr(&S.rmask[u >> 5], 1u << (u & 31));
+  }
+  lds_barrier();
+  // 3. every element of those units (grammar mask applied, NaN invalid)
+  const int W = (a.V + 31) >> 5;
+  constexpr int NCH = kUE / (kBlock * VW);
+  for (int w = 0; w < (U + 31) >> 5; ++w) {
+    uint32_t mk = S.rmask[w];
+    while (mk) {
+      const int u = w * 32 + __builtin_ctz(mk);
+      mk &= mk - 1u;
+      const int lo = u * kUE;
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        const int l0 = lo + (ch * kBlock + tid) * VW;
+        uint32_t mw = 0xFFFFFFFFu;
+        if (c.mask && l0 < a.V) mw = ((l0 >> 5) < W ? c.mask[l0 >> 5] : 0u) >> (l0 & 31);
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+          const int i = l0 + e;
+          if (i >= a.V) break;
+          uint32_t k = fold_nan(key_raw(load_elem_bits<DT>(c.xrow, i)));
+          if (!((mw >> e) & 1u)) k = 0u;
+          if (k >= kKeyFloor && !(patch && lds_patched(S, i, exact))) best = max(best, comp_of(k, (uint32_t)i));
+        }
+      }
+    }
+  }
+  // 4. the patched finals
+  for (int sl = tid; patch && sl < kH; sl += kBlock) {
+    const int id = S.hk[sl];
+    const uint32_t k = S.hf[sl];
+    if (id >= 0 && k >= kKeyFloor) best = max(best, comp_of(k, (uint32_t)id));
+  }
+  return block_max(best, S.r64);
+}
+
 enum { VOP_COUNT = 0, VOP_HKEY, VOP_COUNT_EQ, VOP_LIST_EQ, VOP_HIDX, VOP_COUNT_SEL, VOP_COLLECT };
 struct VOp {
   int op;
@@ -1504,6 +1634,14 @@ __device__ __forceinline__ int slow_select(const KArgs& a, const Ctx& c, MSmem& 
   const int row = c.row;
   uint32_t tk = 0u, ti = 0u;
   int nT = 0;
+  if (want == 1 && pmode <= 1) {  // greedy rows: only the units that can hold the maximum are re-read
+    const uint64_t mc = greedy_refill<DT>(a, c, S, NG, pmode == 1);
+    if (tid == 0) pool[0] = make_uint2(comp_key(mc), comp_idx(mc));
+    lds_barrier();
+    *tk_out = comp_key(mc);
+    *ti_out = comp_idx(mc);
+    return mc != 0ull ? 1 : 0;
+  }
   VOp o = {};
   o.op = VOP_COUNT;
   uint32_t nv = slow_visit<DT>(a, c, S, NG, 0, pmode, pg, o, nullptr);
@@ -1541,55 +1679,6 @@ __device__ __forceinline__ int slow_select(const KArgs& a, const Ctx& c, MSmem& 
   *tk_out = tk;
   *ti_out = ti;
   return nT;
-}
-
-// ---------------------------------------------------------------------------
-// One batch of candidate groups held in registers: kGS groups, kGPer per
-// thread (slot tid + kBlock m), with their group offsets (~0u: no group).
-constexpr int kGPer = kGS / kBlock;
-struct GBatch {
-  uint32_t go[kGPer];
-  uint4 g[kGPer];
-};
-
-// Slot -> group offset table of the row's candidate regions (TPU threads per
-// unit), when the row's groups fit it.
-__device__ __forceinline__ void gather_table(const KArgs& a, MSmem& S, int U, uint32_t NG) {
-  if (NG > (uint32_t)kGT) return;
-  const int tid = threadIdx.x;
-  const int TPU = U >= kBlock ? 1 : kBlock / U;
-  for (int x = tid; x < U * TPU; x += kBlock) {
-    const int u = x / TPU, sub = x - u * TPU;
-    const uint32_t o = S.uoff[u], n = S.uoff[u + 1] - o;
-    for (uint32_t j = (uint32_t)sub; j < n; j += (uint32_t)TPU) S.gtab[o + j] = (uint32_t)u * a.cap + j;
-  }
-  lds_barrier();
-}
-
-// Issues the loads of the batch starting at group f0 (every load in flight,
-// nothing waits for them here).
-template <int DT>
-__device__ __forceinline__ void gather_issue(const KArgs& a, const MSmem& S, int row, int U, uint32_t NG, uint32_t f0,
-                                             GBatch& gb) {
-  const int tid = threadIdx.x;
-  const uint4* rc = a.cand + (size_t)row * U * a.cap;
-  const uint32_t nb = f0 < NG ? min((uint32_t)kGS, NG - f0) : 0u;
-  const bool table = NG <= (uint32_t)kGT;
-#pragma unroll
-  for (int m = 0; m < kGPer; ++m) {
-    const uint32_t q = (uint32_t)(tid + m * kBlock);
-    gb.go[m] = 0xFFFFFFFFu;
-    if (q < nb) {
-      if (table) {
-        gb.go[m] = S.gtab[f0 + q];
-      } else {
-        const int u = unit_of_group<DT>(S, U, f0 + q);
-        gb.go[m] = (uint32_t)u * a.cap + (f0 + q - S.uoff[u]);
-      }
-    }
-  }
-#pragma unroll
-  for (int m = 0; m < kGPer; ++m) gb.g[m] = rc[gb.go[m] == 0xFFFFFFFFu ? 0u : gb.go[m]];
 }
 
 // Fast-path pool: every candidate element at or above tmax (raw copies of
@@ -1760,11 +1849,13 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
   uint32_t* cnt = S.hist[0];            // grid elements per bin (bin = key16 - lo16)
   uint32_t* minix = S.hist[0] + kRBins;  // lowest index of each bin's grid elements
   uint32_t* abv = S.hist[1];            // per position: T elements before it
+  uint32_t* ocnt = S.hist[1] + kRBins;  // off-grid (patched) values of each bin
   uint64_t* mbf = S.mhist;              // per position: T mass before it
   static_assert(2 * kRBins <= (kHCopies * kHStride + 3) / 4 * 4, "bin tables fit one histogram row");
   for (int i = tid; i < kRBins; i += kBlock) {
     cnt[i] = 0u;
     minix[i] = 0xFFFFFFFFu;
+    ocnt[i] = 0u;
   }
   if (tid == 0) {
     S.bc[2] = 0u;           // last position holding elements of S
@@ -1785,6 +1876,8 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
         if ((ee[u].x & 0xFFFFu) == 0u) {
           atomicAdd(&cnt[(ee[u].x >> 16) - lo16], 1u);
           atomicMin(&minix[(ee[u].x >> 16) - lo16], ee[u].y);
+        } else {
+          atomicAdd(&ocnt[(ee[u].x >> 16) - lo16], 1u);
         }
         kmx = max(kmx, ee[u].x);
       }
@@ -1880,7 +1973,7 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
     const uint32_t cg = bn >= 0 ? cnt[bn] : 0u;
     uint32_t co = 0u;
     uint64_t mo = 0ull;
-    if (bn >= 0) {
+    if (bn >= 0 && ocnt[bn] != 0u) {
       for (int f = 0; f < nfin; ++f) {  // the few off-grid values of this bin
         const uint32_t k = pool[f].x;
         if (off_in(k, pos)) {
@@ -1920,27 +2013,28 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
   const uint64_t b0 = block_excl_scan(mm[0] + mm[1], S.r64, Zk);
   const uint64_t bb[2] = {b0, b0 + mm[0]};
   const double Xp = (double)c.top_p * (double)Zk;
-  bool hit_p = false, hit_q = false;
+  // positions grow with the lane, so a wavefront's first hit is its lowest
+  // hitting lane's; one atomic per wavefront
+  uint32_t fp = 0xFFFFFFFFu, fq = 0xFFFFFFFFu;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
+  for (int h = 1; h >= 0; --h) {
     const int pos = 2 * tid + h;
     abv[pos] = aa[h];
     mbf[pos] = bb[h];
-    if (topp && !hit_p && nn[h] > 0u && (double)(bb[h] + mm[h]) >= Xp) {
-      atomicMin(&S.bc[4], (uint32_t)pos);  // top-p: first position whose inclusive mass reaches p Z_k
-      hit_p = true;
-    }
-    if (!hit_q && nn[h] > 0u && drop[h]) {
-      atomicMin(&S.bc[5], (uint32_t)pos);  // min-p: first position whose grid value is dropped
-      hit_q = true;
-    }
+    // top-p: first position whose inclusive mass reaches p Z_k
+    if (topp && nn[h] > 0u && (double)(bb[h] + mm[h]) >= Xp) fp = (uint32_t)pos;
+    // min-p: first position whose grid value is dropped
+    if (nn[h] > 0u && drop[h]) fq = (uint32_t)pos;
+  }
+  {
+    const uint64_t bp = __ballot(fp != 0xFFFFFFFFu), bq = __ballot(fq != 0xFFFFFFFFu);
+    if (bp != 0ull && lane() == (int)__builtin_ctzll(bp)) atomicMin(&S.bc[4], fp);
+    if (bq != 0ull && lane() == (int)__builtin_ctzll(bq)) atomicMin(&S.bc[5], fq);
   }
   lds_barrier();
   auto n_at = [&](int pos) -> uint32_t {
     const uint32_t ab = abv[pos];
-    uint32_t co = 0u;
-    for (int f = 0; f < nfin; ++f) co += off_in(pool[f].x, pos) ? 1u : 0u;
-    return ab >= want ? 0u : min(cnt[bin_of(pos)] + co, want - ab);
+    return ab >= want ? 0u : min(cnt[bin_of(pos)] + ocnt[bin_of(pos)], want - ab);
   };
   // kept set S: the shorter of the two prefixes; its end (a bound on the
   // positions, and when S ends inside a position the elements of S in it)
@@ -1986,18 +2080,20 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
   // draw: first element of S whose inclusive mass exceeds u Z_S; and the last
   // position holding elements of S
   const double Xd = uniform01(c.seed, (uint32_t)b, c.pos, 0) * (double)Zs;
-  bool hit_d = false;
+  uint32_t fd = 0xFFFFFFFFu, ld = 0xFFFFFFFFu;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
+  for (int h = 1; h >= 0; --h) {
     const int pos = 2 * tid + h;
     if (nn[h] > 0u && pos <= endp) {
-      atomicMax(&S.bc[2], (uint32_t)pos);
+      if (ld == 0xFFFFFFFFu) ld = (uint32_t)pos;
       const uint64_t mS = (endn != 0u && pos == endp) ? Zs - bb[h] : mm[h];  // S's part of the end position
-      if (!hit_d && (double)(bb[h] + mS) > Xd) {
-        atomicMin(&S.bc[6], (uint32_t)pos);
-        hit_d = true;
-      }
+      if ((double)(bb[h] + mS) > Xd) fd = (uint32_t)pos;
     }
+  }
+  {
+    const uint64_t bd = __ballot(fd != 0xFFFFFFFFu), bl = __ballot(ld != 0xFFFFFFFFu);
+    if (bd != 0ull && lane() == (int)__builtin_ctzll(bd)) atomicMin(&S.bc[6], fd);
+    if (bl != 0ull && lane() == 63 - (int)__builtin_clzll(bl)) atomicMax(&S.bc[2], ld);
   }
   lds_barrier();
   const int last = (int)S.bc[2];

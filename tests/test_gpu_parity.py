@@ -195,6 +195,48 @@ def test_sample_penalised_heads(ssb):
         check_sample(inp, tok, lp, fl, f"penalised-heads-{pos}")
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_greedy_patched_maxima(ssb, dtype):
+    """Greedy rows whose largest raw logits are penalised below other values:
+    the units holding them are re-read (the other units' candidates bound the
+    maximum).  Rows mix one penalised head, many penalised heads spread over
+    the units, a grammar mask, rows with no lists (tied maxima, so the units
+    overflow their candidate regions) and rows where every head is penalised."""
+    rng = np.random.default_rng(4242 if dtype == "bf16" else 4243)
+    B, V = 32, 1 << 17
+    xf = rng.normal(0.0, 1.0, (B, V))
+    hist, mask = [], np.full((B, (V + 31) // 32), 0xFFFFFFFF, np.uint32)
+    mode = np.full(B, W.MODE_GREEDY | W.MODE_REP | W.MODE_FREQ, np.uint32)
+    for r in range(B):
+        kind = r % 4
+        nheads = (1, 40, 6, 0)[kind]
+        heads = rng.choice(V, max(nheads, 1), replace=False)
+        if kind == 3:  # no lists: tied maxima in every unit
+            xf[r, rng.choice(V, 8000, replace=False)] = 6.0
+            mode[r] = W.MODE_GREEDY
+            hist.append(np.zeros(0, np.int32))
+            continue
+        xf[r, heads] += rng.uniform(6.0, 9.0, heads.size)
+        h = np.repeat(heads, 2)
+        if r % 8 == 2:  # one penalised head stays above the rest
+            h = h[2:]
+        hist.append(np.concatenate([h, rng.integers(0, V, 64)]).astype(np.int32))
+        if kind == 2:  # grammar: deny a third of the words
+            mask[r, rng.choice(mask.shape[1], mask.shape[1] // 3, replace=False)] = 0
+            mode[r] |= W.MODE_GRAMMAR
+    x = xf.astype(np.float32)
+    if dtype == "bf16":
+        x = W.bf16_bits_from_f32(x)
+    hoff = np.concatenate([[0], np.cumsum([len(h) for h in hist])]).astype(np.int32)
+    inp = W.custom_rows(x, dtype=W.BF16 if dtype == "bf16" else W.F32, k_max=64, mode=mode,
+                        rep=np.full(B, 4.0, np.float32), freq=np.full(B, 0.5, np.float32),
+                        hist_offsets=hoff, hist_ids=np.concatenate(hist), bitmask=mask)
+    say(f"[greedy-patched-{dtype}] sample B={B} V={V}")
+    tok, lp, fl = run_sample(ssb, inp)
+    ref = check_sample(inp, tok, lp, fl, f"greedy-patched-{dtype}")
+    assert np.array_equal(tok, ref["token"]), f"greedy-patched-{dtype}"
+
+
 def test_sample_large_vocab_patched(ssb):
     """V = 2^18 bf16 with penalties and bias: the patched-id bitmap is hashed
     above 2^17 ids, so pooled raw copies are checked against the hash table."""
