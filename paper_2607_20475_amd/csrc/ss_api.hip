@@ -11,7 +11,7 @@ namespace ss {
 struct Layout {
   int U, cap, pcap, rows, smem;
   size_t off_rec, off_cand, off_res, off_patch, off_npatch, off_gtag, off_gcnt, off_gfin,
-      total;
+      off_pstat, off_ptab, total;
 };
 
 static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -48,6 +48,11 @@ static bool make_layout(int op, int B, int V, int L, int k_max, int dtype, Layou
   o = align256(o + ghr * kGH * 4);
   lay->off_gfin = o;
   o = align256(o + ghr * kGH * 4);
+  // patch tables built by the streaming launch: status word and 2 kH words per row
+  lay->off_pstat = o;
+  o = align256(o + ghr * 4);
+  lay->off_ptab = o;
+  o = align256(o + ghr * 2 * kH * 4);
   lay->total = o;
   lay->U = U;
   lay->cap = cap;
@@ -146,6 +151,10 @@ static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStr
   k.gtag = reinterpret_cast<uint64_t*>(w + lay.off_gtag);
   k.gcnt = reinterpret_cast<uint32_t*>(w + lay.off_gcnt);
   k.gfin = reinterpret_cast<uint32_t*>(w + lay.off_gfin);
+  k.pstat = reinterpret_cast<int32_t*>(w + lay.off_pstat);
+  k.ptab = reinterpret_cast<uint32_t*>(w + lay.off_ptab);
+  // patch-table workgroups (a multiple of 8, so the stream's XCD remap holds)
+  k.patch_wgs = k.op == OP_TOPK ? 0 : (lay.rows + 7) & ~7;
   const int di = dtype == SS_BF16 ? 1 : 0;
   if (!smem_configured[di][k.op]) {
     // the largest dynamic LDS any call can ask for
@@ -154,11 +163,13 @@ static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStr
     smem_configured[di][k.op] = true;
   }
   const int nunits = lay.rows * lay.U;
-  const dim3 grid((unsigned)((nunits + kWaves - 1) / kWaves)), rgrid((unsigned)lay.rows), block(kBlock);
+  const dim3 grid((unsigned)(k.patch_wgs + (nunits + kWaves - 1) / kWaves)), rgrid((unsigned)lay.rows),
+      block(kBlock);
+  const int psmem = k.patch_wgs ? (int)sizeof(PSmem) : 0;
   if (dtype == SS_BF16)
-    launch_stream<SS_BF16>(k, grid, block, st);
+    launch_stream<SS_BF16>(k, grid, block, psmem, st);
   else
-    launch_stream<SS_F32>(k, grid, block, st);
+    launch_stream<SS_F32>(k, grid, block, psmem, st);
   launch_merge_any(k, dtype, rgrid, block, lay.smem, st);
   if (k.op == OP_VERIFY) launch_assemble(k, dim3((unsigned)((k.B + kBlock - 1) / kBlock)), block, st);
   if (materialize) {

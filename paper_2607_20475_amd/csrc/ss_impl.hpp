@@ -128,6 +128,9 @@ struct KArgs {
   uint32_t* gcnt;      // occurrence count | has-bias bit 31
   uint32_t* gfin;      // final key
   uint32_t* npatched;  // process: per row count
+  int32_t* pstat;      // per row: 0 no lists, 1 patch table in ptab, 2 more ids than the table holds
+  uint32_t* ptab;      // per row 2 kH words: slot ids (-1 empty), then final keys
+  int patch_wgs;       // patch-table workgroups at the front of the streaming grid
 };
 
 // ---------------------------------------------------------------------------
@@ -2164,15 +2167,20 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   const int U = a.U;
   const uint32_t cap = (uint32_t)a.cap;
 
-  // history ids (first 4 * kBlock) are loaded up front, next to the records
-  int hid0[4];
+  // the row's patch table (written by the streaming launch) is loaded up
+  // front, next to the records
+  const bool lists = (c.nhist + c.nextra + c.nbias) > 0;
+  const int pst = lists ? a.pstat[row] : 0;
+  constexpr int kTQ = kH / 4 / kBlock;  // 16-byte words per thread and table half
+  uint4 tid4[kTQ], tfin4[kTQ];
+  if (lists) {
+    const uint4* tsrc = reinterpret_cast<const uint4*>(a.ptab + (size_t)row * 2 * kH);
 #pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    const int h = tid + m * kBlock;
-    hid0[m] = h < c.nhist ? c.hist[h] : -1;
+    for (int m = 0; m < kTQ; ++m) {
+      tid4[m] = tsrc[tid + m * kBlock];
+      tfin4[m] = tsrc[kH / 4 + tid + m * kBlock];
+    }
   }
-  const int bid0 = tid < c.nbias ? c.bias_ids[tid] : -1;
-  const float bval0 = tid < c.nbias ? c.bias_vals[tid] : 0.0f;
   // the patch tables are cleared while the records load (the barriers of
   // the record scan order the clearing before the inserts)
   const bool pexact = a.V <= kPB;
@@ -2214,7 +2222,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   int want = c.k_eff;
 
   // 2. patched ids: counts, ordered bias sums, final keys
-  const bool patch = !empty && want > 0 && (c.nhist + c.nextra + c.nbias) > 0;
+  const bool patch = !empty && want > 0 && lists;
   int pmode = 0;
   PatchG pg;
   pg.tag = a.gtag + (size_t)row * kGH;
@@ -2224,81 +2232,30 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   const int Wm = (a.V + 31) >> 5;
   uint32_t hfmax = 0u;  // largest patched final key (LDS mode)
   if (patch) {
-    const bool exact = pexact;
-    // bias entries record their value in hf[] (the final key is written
-    // later); a second entry for the same id sets the "duplicate" bit and the
-    // finals then sum that id's entries in list order
-    auto ins = [&](int id, uint32_t addc, bool bias, float bval) {
-      if (id < 0 || id >= a.V) return;
-      const uint32_t hb2 = pbit(id, exact);
-      atomicOr(&S.pbits[hb2 >> 5], 1u << (hb2 & 31));
-      uint32_t s = hslot(id);
-      for (int p = 0; p < kProbe; ++p) {
-        const int old = atomicCAS(&S.hk[s], -1, id);
-        if (old == -1 || old == id) {
-          if (addc) atomicAdd(&S.hc[s], addc);
-          if (bias) {
-            const uint32_t prev = atomicOr(&S.hc[s], 0x80000000u);
-            if (prev & 0x80000000u) atomicOr(&S.hc[s], 0x40000000u);
-            else S.hf[s] = __float_as_uint(bval);
-          }
-          return;
-        }
-        s = (s + 1) & (kH - 1);
-      }
-      S.flagsw = 1u;
-    };
-#pragma unroll
-    for (int m = 0; m < 4; ++m) ins(hid0[m], 1u, false, 0.0f);
-    for (int h = tid + 4 * kBlock; h < c.nhist; h += kBlock) ins(c.hist[h], 1u, false, 0.0f);  // long histories
-    for (int h = tid; h < c.nextra; h += kBlock) ins(c.extra[h], 1u, false, 0.0f);
-    ins(bid0, 0u, true, bval0);
-    for (int e = tid + kBlock; e < c.nbias; e += kBlock) ins(c.bias_ids[e], 0u, true, c.bias_vals[e]);
-    __syncthreads();
-    if (S.flagsw == 0u) {
+    if (pst == 1) {
       pmode = 1;
-#pragma unroll 1
-      for (int j0 = 0; j0 < kH; j0 += 4 * kBlock) {  // every slot of the patch table
-        int id[4], sl[4];
-        uint32_t bits[4], mw[4];
+      // the table's slots as written (the hash layout is the merge's own):
+      // ids and final keys, then the patched-id bitmap and the largest final
 #pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          const int j = j0 + tid + m * kBlock;
-          sl[m] = j;
-          id[m] = S.hk[j];
-          bits[m] = 0u;
-          mw[m] = 0xFFFFFFFFu;
-          // unconditional loads (element 0 stands in for an empty slot), so
-          // that all of them are in flight together
-          const int ld_id = id[m] >= 0 ? id[m] : 0;
-          bits[m] = load_elem_bits<DT>(c.xrow, ld_id);
-          if (c.mask) mw[m] = (ld_id >> 5) < Wm ? c.mask[ld_id >> 5] : 0u;
-        }
+      for (int m = 0; m < kTQ; ++m) {
+        reinterpret_cast<uint4*>(S.hk)[tid + m * kBlock] = tid4[m];
+        reinterpret_cast<uint4*>(S.hf)[tid + m * kBlock] = tfin4[m];
+      }
 #pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          if (id[m] < 0) continue;
-          const int s = sl[m];
-          const uint32_t hcv = S.hc[s];
-          const bool hb = (hcv >> 31) != 0u;
-          float bsum = 0.0f;
-          if (hb) {
-            if (hcv & 0x40000000u) {  // duplicate bias ids: list order
-              for (int e = 0; e < c.nbias; ++e)
-                if (c.bias_ids[e] == id[m]) bsum = bsum + c.bias_vals[e];
-            } else {
-              bsum = 0.0f + __uint_as_float(S.hf[s]);
-            }
-          }
-          uint32_t k = 0u;
-          if ((mw[m] >> (id[m] & 31)) & 1u)
-            k = fold_nan(penalised_key(bits[m], c.mode, c.rep, c.freq, c.pres, (int)(hcv & 0x3FFFFFFFu), hb, bsum));
-          S.hf[s] = k;
-          hfmax = max(hfmax, k);
+      for (int m = 0; m < kTQ; ++m) {
+        const int ids[4] = {(int)tid4[m].x, (int)tid4[m].y, (int)tid4[m].z, (int)tid4[m].w};
+        const uint32_t fk[4] = {tfin4[m].x, tfin4[m].y, tfin4[m].z, tfin4[m].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (ids[q] < 0) continue;
+          const uint32_t hb2 = pbit(ids[q], pexact);
+          atomicOr(&S.pbits[hb2 >> 5], 1u << (hb2 & 31));
+          hfmax = max(hfmax, fk[q]);
         }
       }
-      hfmax = block_max(hfmax, S.r32);
+      hfmax = block_max(hfmax, S.r32);  // its barriers publish the table and the bitmap
     } else {
-      // more distinct ids than the LDS table holds: the row's table in global
+      // more distinct ids than the LDS table holds (status 2): the row's table in global
       // memory, cleared first (its contents before the call are unspecified)
       for (int sl = tid; sl < kGH / 2; sl += kBlock) reinterpret_cast<uint4*>(pg.tag)[sl] = make_uint4(0u, 0u, 0u, 0u);
       pg.gen = 1u;
@@ -2700,14 +2657,134 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
 }
 
 // ===========================================================================
+// Patch tables (workgroups of the streaming launch)
+// ===========================================================================
+struct PSmem {
+  int32_t hk[kH];   // listed id (or -1)
+  uint32_t hc[kH];  // occurrence count | has-bias bit 31 | duplicate-bias bit 30
+  uint32_t hf[kH];  // bias value, then the final key
+  uint32_t flagsw;  // nonzero: more distinct ids than kH slots
+  uint32_t pad[3];
+};
+
+// Builds a row's patch table: the history, draft and bias ids are counted and
+// summed in an LDS hash table (bias entries of one id summed in list order),
+// each listed id's raw logit is gathered and its final key computed by the
+// Appendix C.1 prologue (Alg. 8 order; grammar-masked ids get the invalid
+// key).  The table goes to the workspace slot for slot, with the row's
+// status: 0 no lists, 1 table written, 2 more distinct ids than the table
+// holds (the merge then builds a table in global memory itself).  It needs
+// the logits and the lists only, so it runs beside the row stream.
+template <int DT>
+__device__ __forceinline__ void patch_row(const KArgs& a, int row, PSmem& P) {
+  const int tid = threadIdx.x;
+  const Ctx c = make_ctx<DT>(a, row);
+  const int ne = c.nhist + c.nextra + c.nbias;
+  if (ne == 0) {
+    if (tid == 0) a.pstat[row] = 0;
+    return;
+  }
+  int hid0[4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const int h = tid + m * kBlock;
+    hid0[m] = h < c.nhist ? c.hist[h] : -1;
+  }
+  const int bid0 = tid < c.nbias ? c.bias_ids[tid] : -1;
+  const float bval0 = tid < c.nbias ? c.bias_vals[tid] : 0.0f;
+  for (int sl = tid; sl < kH / 4; sl += kBlock) {
+    reinterpret_cast<int4*>(P.hk)[sl] = make_int4(-1, -1, -1, -1);
+    reinterpret_cast<uint4*>(P.hc)[sl] = make_uint4(0u, 0u, 0u, 0u);
+  }
+  if (tid == 0) P.flagsw = 0u;
+  lds_barrier();
+  // a second bias entry for one id sets the "duplicate" bit; the finals then
+  // sum that id's entries in list order
+  auto ins = [&](int id, uint32_t addc, bool bias, float bval) {
+    if (id < 0 || id >= a.V) return;
+    uint32_t sl = hslot(id);
+    for (int p = 0; p < kProbe; ++p) {
+      const int old = atomicCAS(&P.hk[sl], -1, id);
+      if (old == -1 || old == id) {
+        if (addc) atomicAdd(&P.hc[sl], addc);
+        if (bias) {
+          const uint32_t prev = atomicOr(&P.hc[sl], 0x80000000u);
+          if (prev & 0x80000000u) atomicOr(&P.hc[sl], 0x40000000u);
+          else P.hf[sl] = __float_as_uint(bval);
+        }
+        return;
+      }
+      sl = (sl + 1) & (kH - 1);
+    }
+    P.flagsw = 1u;
+  };
+#pragma unroll
+  for (int m = 0; m < 4; ++m) ins(hid0[m], 1u, false, 0.0f);
+  for (int h = tid + 4 * kBlock; h < c.nhist; h += kBlock) ins(c.hist[h], 1u, false, 0.0f);  // long histories
+  for (int h = tid; h < c.nextra; h += kBlock) ins(c.extra[h], 1u, false, 0.0f);
+  ins(bid0, 0u, true, bval0);
+  for (int e = tid + kBlock; e < c.nbias; e += kBlock) ins(c.bias_ids[e], 0u, true, c.bias_vals[e]);
+  lds_barrier();
+  if (P.flagsw != 0u) {
+    if (tid == 0) a.pstat[row] = 2;
+    return;
+  }
+  // final keys: every slot's raw logit (and grammar word) is loaded before
+  // any is used
+  constexpr int kSl = kH / kBlock;
+  const int Wm = (a.V + 31) >> 5;
+  int id[kSl];
+  uint32_t bits[kSl], mw[kSl];
+#pragma unroll
+  for (int m = 0; m < kSl; ++m) {
+    id[m] = P.hk[tid + m * kBlock];
+    const int ld = id[m] >= 0 ? id[m] : 0;  // element 0 stands in for an empty slot
+    bits[m] = load_elem_bits<DT>(c.xrow, ld);
+    mw[m] = c.mask ? ((ld >> 5) < Wm ? c.mask[ld >> 5] : 0u) : 0xFFFFFFFFu;
+  }
+  uint32_t* dst = a.ptab + (size_t)row * 2 * kH;
+#pragma unroll
+  for (int m = 0; m < kSl; ++m) {
+    const int sl = tid + m * kBlock;
+    uint32_t k = 0u;
+    if (id[m] >= 0) {
+      const uint32_t hcv = P.hc[sl];
+      const bool hb = (hcv >> 31) != 0u;
+      float bsum = 0.0f;
+      if (hb) {
+        if (hcv & 0x40000000u) {  // duplicate bias ids: list order
+          for (int e = 0; e < c.nbias; ++e)
+            if (c.bias_ids[e] == id[m]) bsum = bsum + c.bias_vals[e];
+        } else {
+          bsum = 0.0f + __uint_as_float(P.hf[sl]);
+        }
+      }
+      if ((mw[m] >> (id[m] & 31)) & 1u)
+        k = fold_nan(penalised_key(bits[m], c.mode, c.rep, c.freq, c.pres, (int)(hcv & 0x3FFFFFFFu), hb, bsum));
+    }
+    dst[sl] = (uint32_t)id[m];
+    dst[kH + sl] = k;
+  }
+  if (tid == 0) a.pstat[row] = 1;
+}
+
+// ===========================================================================
 // Kernels
 // ===========================================================================
 // Streaming kernel: one unit per wavefront, no LDS, no barrier.  Workgroups
 // are remapped so that consecutive units (one row) share an XCD and its L2.
+// For the operations that apply penalties and bias, the first workgroups of
+// the grid build the rows' patch tables (dynamic LDS) beside the stream.
 template <int DT>
 __global__ __launch_bounds__(kBlock) void ss_stream_kernel(KArgs a) {
   int bid = blockIdx.x;
-  const int nb = gridDim.x;
+  if (bid < a.patch_wgs) {  // patch-table workgroups (a multiple of 8) come first
+    extern __shared__ __align__(16) unsigned char psmem[];
+    if (bid < a.rows) patch_row<DT>(a, bid, *reinterpret_cast<PSmem*>(psmem));
+    return;
+  }
+  bid -= a.patch_wgs;
+  const int nb = gridDim.x - a.patch_wgs;
   if (bid < (nb & ~7)) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
   const int gu = __builtin_amdgcn_readfirstlane(bid * kWaves + wave());
   if (gu < a.rows * a.U) scan_unit<DT>(a, gu);

@@ -8,7 +8,7 @@ namespace ss {
 struct KArgs;
 
 template <int DT>
-void launch_stream(const KArgs& k, dim3 grid, dim3 block, hipStream_t st);
+void launch_stream(const KArgs& k, dim3 grid, dim3 block, int smem, hipStream_t st);
 template <int DT, int OP>
 void launch_merge(const KArgs& k, dim3 grid, dim3 block, int smem, hipStream_t st);
 template <int DT, int OP>
@@ -30,8 +30,8 @@ SS_EXTERN_MERGE(1, 1)
 SS_EXTERN_MERGE(1, 2)
 SS_EXTERN_MERGE(1, 3)
 #undef SS_EXTERN_MERGE
-extern template void launch_stream<0>(const KArgs&, dim3, dim3, hipStream_t);
-extern template void launch_stream<1>(const KArgs&, dim3, dim3, hipStream_t);
+extern template void launch_stream<0>(const KArgs&, dim3, dim3, int, hipStream_t);
+extern template void launch_stream<1>(const KArgs&, dim3, dim3, int, hipStream_t);
 extern template void launch_materialize<0>(const KArgs&, dim3, dim3, hipStream_t);
 extern template void launch_materialize<1>(const KArgs&, dim3, dim3, hipStream_t);
 

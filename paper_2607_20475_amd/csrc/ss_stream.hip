@@ -5,10 +5,10 @@
 namespace ss {
 
 template <int DT>
-void launch_stream(const KArgs& k, dim3 grid, dim3 block, hipStream_t st) {
-  hipLaunchKernelGGL(ss_stream_kernel<DT>, grid, block, 0, st, k);
+void launch_stream(const KArgs& k, dim3 grid, dim3 block, int smem, hipStream_t st) {
+  hipLaunchKernelGGL(ss_stream_kernel<DT>, grid, block, smem, st, k);
 }
-template void launch_stream<SS_F32>(const KArgs&, dim3, dim3, hipStream_t);
-template void launch_stream<SS_BF16>(const KArgs&, dim3, dim3, hipStream_t);
+template void launch_stream<SS_F32>(const KArgs&, dim3, dim3, int, hipStream_t);
+template void launch_stream<SS_BF16>(const KArgs&, dim3, dim3, int, hipStream_t);
 
 }  // namespace ss
