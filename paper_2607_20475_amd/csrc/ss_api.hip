@@ -158,7 +158,7 @@ static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStr
   const int di = dtype == SS_BF16 ? 1 : 0;
   if (!smem_configured[di][k.op]) {
     // the largest dynamic LDS any call can ask for
-    const int maxb = kSmemFixed + 8 * (2 * SS_MAX_K + 512);
+    const int maxb = kSmemFixed + 8 * (((2 * SS_MAX_K + 128 + 255) & ~255) + kBlock);
     if (merge_smem_any(dtype, k.op, maxb) != hipSuccess) return SS_ERR_HIP;
     smem_configured[di][k.op] = true;
   }

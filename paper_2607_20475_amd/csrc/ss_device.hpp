@@ -1,15 +1,15 @@
 // ss_device.hpp -- device primitives for the gfx950 sampler kernels.
 //
 // Order-preserving keys, Philox4x32-10, wave64 / workgroup reductions and
-// scans, and an LDS bitonic sort.  Workgroups are kBlock = 256 threads
-// (four 64-lane wavefronts).
+// scans, and an LDS bitonic sort.  Workgroups are kBlock = 512 threads
+// (eight 64-lane wavefronts, two per SIMD).
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace ss {
 
-constexpr int kBlock = 256;
+constexpr int kBlock = 512;
 constexpr int kWaves = kBlock / 64;
 
 // ---------------------------------------------------------------------------

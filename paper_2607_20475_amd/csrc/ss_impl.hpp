@@ -60,7 +60,6 @@ constexpr int kHCopies = 2;                  // privatised radix histograms
 constexpr int kRB = 9;                       // widest radix digit (bits)
 constexpr int kRBins = 1 << kRB;
 constexpr int kHStride = kRBins + 1;
-constexpr int kTS = SS_MAX_K / kBlock;       // selected elements per thread (16)
 constexpr int kGT = 4096;                    // gather table entries (LDS)
 constexpr int kGS = 2048;                    // candidate groups staged in LDS per batch
 constexpr uint32_t kNoEmit = 0xFFFFFFFFu;    // threshold of a unit that emits nothing
@@ -599,7 +598,6 @@ struct MSmem {
   uint32_t x32[3][kWaves];
   uint32_t pbits[kPB / 32];  // bit pbit(id) set for every patched id
   int32_t hk[kH];   // patched id (or -1)
-  uint32_t hc[kH];  // occurrence count | has-bias bit 31
   uint32_t hf[kH];  // final key
   union {
     uint32_t gtab[kGT];  // candidate slot -> group offset in the row's regions (gather)
@@ -618,7 +616,7 @@ static_assert(sizeof(uint32_t) * 2 * ((kHCopies * kHStride + 3) & ~3) + 4 * 2 * 
 constexpr int kSmemFixed = (int)((sizeof(MSmem) + 15) & ~(size_t)15);
 // the largest merge footprint (sampling ops at k_max = SS_MAX_K: pcap + kBlock
 // <= 2 SS_MAX_K + 512 entries) fits gfx950's 160 KiB of LDS
-static_assert(kSmemFixed + 8 * (2 * SS_MAX_K + 512) <= 160 * 1024, "merge LDS too large");
+static_assert(kSmemFixed + 8 * (((2 * SS_MAX_K + 128 + 255) & ~255) + kBlock) <= 160 * 1024, "merge LDS too large");
 
 __device__ __forceinline__ uint32_t hslot(int id) { return ((uint32_t)id * 2654435761u) >> 21; }  // 11 bits
 static_assert(kH == 2048, "hslot assumes 2048 slots");
@@ -1301,7 +1299,7 @@ __device__ __forceinline__ uint64_t greedy_refill(const KArgs& a, const Ctx& c, 
   lds_barrier();
   // 3. every element of those units (grammar mask applied, NaN invalid)
   const int W = (a.V + 31) >> 5;
-  constexpr int NCH = kUE / (kBlock * VW);
+  constexpr int NCH = (kUE + kBlock * VW - 1) / (kBlock * VW);  // 16-byte chunks per thread and unit
   for (int w = 0; w < (U + 31) >> 5; ++w) {
     uint32_t mk = S.rmask[w];
     while (mk) {
@@ -1310,6 +1308,7 @@ __device__ __forceinline__ uint64_t greedy_refill(const KArgs& a, const Ctx& c, 
       const int lo = u * kUE;
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch) {
+        if ((ch * kBlock + tid) * VW >= kUE) break;
         const int l0 = lo + (ch * kBlock + tid) * VW;
         uint32_t mw = 0xFFFFFFFFu;
         if (c.mask && l0 < a.V) mw = ((l0 >> 5) < W ? c.mask[l0 >> 5] : 0u) >> (l0 & 31);
@@ -1428,7 +1427,7 @@ __device__ __forceinline__ uint32_t slow_visit(const KArgs& a, const Ctx& c, con
         if ((S.rmask[u >> 5] >> (u & 31)) & 1u) return u;
       return U;
     };
-    constexpr int NCH = kUE / (kBlock * VW);  // 16-byte chunks per thread and unit
+    constexpr int NCH = (kUE + kBlock * VW - 1) / (kBlock * VW);  // 16-byte chunks per thread and unit
     for (int ch = 0; ch < NCH; ++ch) {
     const int l0 = (ch * kBlock + tid) * VW;
     for (int u0 = next_unit(0); u0 < U;) {
@@ -1890,7 +1889,7 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
   lds_barrier();
   // positions in canonical order: position p holds bin top - p, its off-grid
   // values first (they exceed its grid key), then its grid elements; thread t
-  // holds positions 2t and 2t + 1
+  // holds positions PP t .. PP t + PP - 1 (PP = kRBins / kBlock)
   const uint32_t Kmax = S.bc[7];
   const uint32_t top = (Kmax >> 16) - lo16;
   const double M = (double)float_of_key(Kmax);
@@ -1966,12 +1965,14 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
     *mass_out = cum;
     return j;
   };
-  uint32_t ct[2], nn[2], fg[2];
-  uint64_t mm[2], wg[2];
-  bool drop[2];
+  constexpr int PP = kRBins / kBlock;  // positions per thread
+  static_assert(PP >= 1 && PP * kBlock == kRBins, "every key bin has one position");
+  uint32_t ct[PP], nn[PP], fg[PP];
+  uint64_t mm[PP], wg[PP];
+  bool drop[PP];
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int pos = 2 * tid + h;
+  for (int h = 0; h < PP; ++h) {
+    const int pos = PP * tid + h;
     const int bn = bin_of(pos);
     const uint32_t cg = bn >= 0 ? cnt[bn] : 0u;
     uint32_t co = 0u;
@@ -1992,13 +1993,18 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
     drop[h] = minp && bn >= 0 && dropped(grid_key(pos));
   }
   uint32_t tot;
-  const uint32_t a0 = block_excl_scan(ct[0] + ct[1], S.r32, tot);
-  const uint32_t aa[2] = {a0, a0 + ct[0]};
+  uint32_t ctt = 0u;
+#pragma unroll
+  for (int h = 0; h < PP; ++h) ctt += ct[h];
+  const uint32_t a0 = block_excl_scan(ctt, S.r32, tot);
+  uint32_t aa[PP];
+#pragma unroll
+  for (int h = 0; h < PP; ++h) aa[h] = h == 0 ? a0 : aa[h - 1] + ct[h - 1];
   // T: every element of the positions above the top-k boundary, the first
   // `want` minus those above at the boundary, nothing below
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int pos = 2 * tid + h;
+  for (int h = 0; h < PP; ++h) {
+    const int pos = PP * tid + h;
     nn[h] = aa[h] >= want ? 0u : min(ct[h], want - aa[h]);
     if (fg[h] == 0u || nn[h] == ct[h]) {
       mm[h] = fg[h] == 0u ? (uint64_t)nn[h] * wg[h] : mm[h] + (uint64_t)(ct[h] - fg[h]) * wg[h];
@@ -2013,15 +2019,20 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
     }
   }
   uint64_t Zk;
-  const uint64_t b0 = block_excl_scan(mm[0] + mm[1], S.r64, Zk);
-  const uint64_t bb[2] = {b0, b0 + mm[0]};
+  uint64_t mmt = 0ull;
+#pragma unroll
+  for (int h = 0; h < PP; ++h) mmt += mm[h];
+  const uint64_t b0 = block_excl_scan(mmt, S.r64, Zk);
+  uint64_t bb[PP];
+#pragma unroll
+  for (int h = 0; h < PP; ++h) bb[h] = h == 0 ? b0 : bb[h - 1] + mm[h - 1];
   const double Xp = (double)c.top_p * (double)Zk;
   // positions grow with the lane, so a wavefront's first hit is its lowest
   // hitting lane's; one atomic per wavefront
   uint32_t fp = 0xFFFFFFFFu, fq = 0xFFFFFFFFu;
 #pragma unroll
-  for (int h = 1; h >= 0; --h) {
-    const int pos = 2 * tid + h;
+  for (int h = PP - 1; h >= 0; --h) {
+    const int pos = PP * tid + h;
     abv[pos] = aa[h];
     mbf[pos] = bb[h];
     // top-p: first position whose inclusive mass reaches p Z_k
@@ -2085,8 +2096,8 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
   const double Xd = uniform01(c.seed, (uint32_t)b, c.pos, 0) * (double)Zs;
   uint32_t fd = 0xFFFFFFFFu, ld = 0xFFFFFFFFu;
 #pragma unroll
-  for (int h = 1; h >= 0; --h) {
-    const int pos = 2 * tid + h;
+  for (int h = PP - 1; h >= 0; --h) {
+    const int pos = PP * tid + h;
     if (nn[h] > 0u && pos <= endp) {
       if (ld == 0xFFFFFFFFu) ld = (uint32_t)pos;
       const uint64_t mS = (endn != 0u && pos == endp) ? Zs - bb[h] : mm[h];  // S's part of the end position
@@ -2181,14 +2192,10 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
       tfin4[m] = tsrc[kH / 4 + tid + m * kBlock];
     }
   }
-  // the patch tables are cleared while the records load (the barriers of
-  // the record scan order the clearing before the inserts)
+  // the patched-id bitmap is cleared while the records load (the barriers of
+  // the record scan order the clearing before the table's ids are set)
   const bool pexact = a.V <= kPB;
   if ((c.nhist + c.nextra + c.nbias) > 0) {
-    for (int s = tid; s < kH / 4; s += kBlock) {
-      reinterpret_cast<int4*>(S.hk)[s] = make_int4(-1, -1, -1, -1);
-      reinterpret_cast<uint4*>(S.hc)[s] = make_uint4(0u, 0u, 0u, 0u);
-    }
     const int pwords = pexact ? (a.V + 31) >> 5 : kPB / 32;
     for (int s = tid; s < (pwords + 3) >> 2; s += kBlock) reinterpret_cast<uint4*>(S.pbits)[s] = make_uint4(0u, 0u, 0u, 0u);
   }
