@@ -163,13 +163,13 @@ static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStr
     smem_configured[di][k.op] = true;
   }
   const int nunits = lay.rows * lay.U;
-  const dim3 grid((unsigned)(k.patch_wgs + (nunits + kWaves - 1) / kWaves)), rgrid((unsigned)lay.rows),
-      block(kBlock);
+  const dim3 grid((unsigned)(k.patch_wgs + (nunits + kSWaves - 1) / kSWaves)), sblock(kSBlock),
+      rgrid((unsigned)lay.rows), block(kBlock);
   const int psmem = k.patch_wgs ? (int)sizeof(PSmem) : 0;
   if (dtype == SS_BF16)
-    launch_stream<SS_BF16>(k, grid, block, psmem, st);
+    launch_stream<SS_BF16>(k, grid, sblock, psmem, st);
   else
-    launch_stream<SS_F32>(k, grid, block, psmem, st);
+    launch_stream<SS_F32>(k, grid, sblock, psmem, st);
   launch_merge_any(k, dtype, rgrid, block, lay.smem, st);
   if (k.op == OP_VERIFY) launch_assemble(k, dim3((unsigned)((k.B + kBlock - 1) / kBlock)), block, st);
   if (materialize) {

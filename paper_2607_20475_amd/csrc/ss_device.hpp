@@ -11,6 +11,10 @@ namespace ss {
 
 constexpr int kBlock = 512;
 constexpr int kWaves = kBlock / 64;
+// the streaming launch (one unit per wavefront, plus the patch-table
+// workgroups) keeps 256-thread workgroups
+constexpr int kSBlock = 256;
+constexpr int kSWaves = kSBlock / 64;
 
 // ---------------------------------------------------------------------------
 // Order-preserving 32-bit key of a float32 bit pattern.

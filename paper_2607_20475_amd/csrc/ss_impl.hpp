@@ -2694,12 +2694,12 @@ __device__ __forceinline__ void patch_row(const KArgs& a, int row, PSmem& P) {
   int hid0[4];
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
-    const int h = tid + m * kBlock;
+    const int h = tid + m * kSBlock;
     hid0[m] = h < c.nhist ? c.hist[h] : -1;
   }
   const int bid0 = tid < c.nbias ? c.bias_ids[tid] : -1;
   const float bval0 = tid < c.nbias ? c.bias_vals[tid] : 0.0f;
-  for (int sl = tid; sl < kH / 4; sl += kBlock) {
+  for (int sl = tid; sl < kH / 4; sl += kSBlock) {
     reinterpret_cast<int4*>(P.hk)[sl] = make_int4(-1, -1, -1, -1);
     reinterpret_cast<uint4*>(P.hc)[sl] = make_uint4(0u, 0u, 0u, 0u);
   }
@@ -2727,10 +2727,10 @@ __device__ __forceinline__ void patch_row(const KArgs& a, int row, PSmem& P) {
   };
 #pragma unroll
   for (int m = 0; m < 4; ++m) ins(hid0[m], 1u, false, 0.0f);
-  for (int h = tid + 4 * kBlock; h < c.nhist; h += kBlock) ins(c.hist[h], 1u, false, 0.0f);  // long histories
-  for (int h = tid; h < c.nextra; h += kBlock) ins(c.extra[h], 1u, false, 0.0f);
+  for (int h = tid + 4 * kSBlock; h < c.nhist; h += kSBlock) ins(c.hist[h], 1u, false, 0.0f);  // long histories
+  for (int h = tid; h < c.nextra; h += kSBlock) ins(c.extra[h], 1u, false, 0.0f);
   ins(bid0, 0u, true, bval0);
-  for (int e = tid + kBlock; e < c.nbias; e += kBlock) ins(c.bias_ids[e], 0u, true, c.bias_vals[e]);
+  for (int e = tid + kSBlock; e < c.nbias; e += kSBlock) ins(c.bias_ids[e], 0u, true, c.bias_vals[e]);
   lds_barrier();
   if (P.flagsw != 0u) {
     if (tid == 0) a.pstat[row] = 2;
@@ -2738,13 +2738,13 @@ __device__ __forceinline__ void patch_row(const KArgs& a, int row, PSmem& P) {
   }
   // final keys: every slot's raw logit (and grammar word) is loaded before
   // any is used
-  constexpr int kSl = kH / kBlock;
+  constexpr int kSl = kH / kSBlock;
   const int Wm = (a.V + 31) >> 5;
   int id[kSl];
   uint32_t bits[kSl], mw[kSl];
 #pragma unroll
   for (int m = 0; m < kSl; ++m) {
-    id[m] = P.hk[tid + m * kBlock];
+    id[m] = P.hk[tid + m * kSBlock];
     const int ld = id[m] >= 0 ? id[m] : 0;  // element 0 stands in for an empty slot
     bits[m] = load_elem_bits<DT>(c.xrow, ld);
     mw[m] = c.mask ? ((ld >> 5) < Wm ? c.mask[ld >> 5] : 0u) : 0xFFFFFFFFu;
@@ -2752,7 +2752,7 @@ __device__ __forceinline__ void patch_row(const KArgs& a, int row, PSmem& P) {
   uint32_t* dst = a.ptab + (size_t)row * 2 * kH;
 #pragma unroll
   for (int m = 0; m < kSl; ++m) {
-    const int sl = tid + m * kBlock;
+    const int sl = tid + m * kSBlock;
     uint32_t k = 0u;
     if (id[m] >= 0) {
       const uint32_t hcv = P.hc[sl];
@@ -2783,7 +2783,7 @@ __device__ __forceinline__ void patch_row(const KArgs& a, int row, PSmem& P) {
 // For the operations that apply penalties and bias, the first workgroups of
 // the grid build the rows' patch tables (dynamic LDS) beside the stream.
 template <int DT>
-__global__ __launch_bounds__(kBlock) void ss_stream_kernel(KArgs a) {
+__global__ __launch_bounds__(kSBlock) void ss_stream_kernel(KArgs a) {
   int bid = blockIdx.x;
   if (bid < a.patch_wgs) {  // patch-table workgroups (a multiple of 8) come first
     extern __shared__ __align__(16) unsigned char psmem[];
@@ -2793,7 +2793,7 @@ __global__ __launch_bounds__(kBlock) void ss_stream_kernel(KArgs a) {
   bid -= a.patch_wgs;
   const int nb = gridDim.x - a.patch_wgs;
   if (bid < (nb & ~7)) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
-  const int gu = __builtin_amdgcn_readfirstlane(bid * kWaves + wave());
+  const int gu = __builtin_amdgcn_readfirstlane(bid * kSWaves + wave());
   if (gu < a.rows * a.U) scan_unit<DT>(a, gu);
 }
 
