@@ -61,7 +61,7 @@ constexpr int kRB = 9;                       // widest radix digit (bits)
 constexpr int kRBins = 1 << kRB;
 constexpr int kHStride = kRBins + 1;
 constexpr int kGT = 4096;                    // gather table entries (LDS)
-constexpr int kGS = 2048;                    // candidate groups staged in LDS per batch
+constexpr int kGS = 2048;                    // candidate groups held in registers per batch
 constexpr uint32_t kNoEmit = 0xFFFFFFFFu;    // threshold of a unit that emits nothing
 constexpr double kFix = 1125899906842624.0;  // 2^50: fixed-point scale of probability mass
 
@@ -1684,42 +1684,21 @@ __device__ __forceinline__ int slow_select(const KArgs& a, const Ctx& c, MSmem& 
 }
 
 // Fast-path pool: every candidate element at or above tmax (raw copies of
-// patched ids dropped) plus the patched final values at or above it, in a
-// deterministic order (batches of groups held in registers, block-scan
-// offsets).
+// patched ids dropped) behind the nfin patched final values at or above it
+// already at pool[0, nfin), in a deterministic order (batches of groups held
+// in registers, block-scan offsets).  The caller issued the first batch
+// (`cur`) right after the unit records, so its loads overlap the patch
+// tables' copy.
 // Returns the element count (elements beyond a.pcap are counted, not stored).
 template <int DT>
 __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MSmem& S, uint32_t NG, bool patch,
-                                                uint32_t tmax, uint2* pool, uint32_t& nvalid_out, uint32_t& nfin_out) {
+                                                uint32_t tmax, uint2* pool, uint32_t& nvalid_out, uint32_t nfin,
+                                                GBatch& cur) {
   constexpr int GE = DTT<DT>::GE;
   const int tid = threadIdx.x;
   const int U = a.U;
   const uint32_t pcap = (uint32_t)a.pcap;
-  // the first batch's loads are in flight during the patched-finals pass
-  gather_table(a, S, U, NG);
-  GBatch cur;
-  gather_issue<DT>(a, S, c.row, U, NG, 0u, cur);
-  // patched final values at or above tmax go first
-  uint32_t base = 0u;
-  if (patch) {
-    // occupied slots of the patch table, in slot order
-    uint32_t cnt = 0u;
-    for (int sl = tid; sl < kH; sl += kBlock) {
-      const uint32_t k = S.hf[sl];
-      cnt += (S.hk[sl] >= 0 && k >= tmax && k >= kKeyFloor) ? 1u : 0u;
-    }
-    uint32_t tot;
-    uint32_t off = block_excl_scan(cnt, S.r32, tot);
-    for (int sl = tid; sl < kH; sl += kBlock) {
-      const uint32_t k = S.hf[sl];
-      if (S.hk[sl] >= 0 && k >= tmax && k >= kKeyFloor) {
-        if (off < pcap) pool[off] = make_uint2(k, (uint32_t)S.hk[sl]);
-        ++off;
-      }
-    }
-    base = tot;
-  }
-  nfin_out = base;  // pool[0, base): the patched final values
+  uint32_t base = nfin;
   auto key_of = [](const uint4& gq, int e) -> uint32_t {
     if constexpr (DT == SS_BF16) return (((e < 2 ? gq.y : gq.z) >> (16 * (e & 1))) & 0xFFFFu) << 16;
     else return e ? gq.z : gq.y;
@@ -2227,6 +2206,13 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   int flags = c.kcap ? SS_FLAG_KCAP : 0;
   const bool empty = hi < kKeyFloor;
   int want = c.k_eff;
+  // the first batch of candidate groups is in flight from here on
+  const bool fast = !empty && want > 0 && ovf == 0u;
+  GBatch cur;
+  if (fast) {
+    gather_table(a, S, U, NG);
+    gather_issue<DT>(a, S, row, U, NG, 0u, cur);
+  }
 
   // 2. patched ids: counts, ordered bias sums, final keys
   const bool patch = !empty && want > 0 && lists;
@@ -2238,6 +2224,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   pg.gen = 0u;
   const int Wm = (a.V + 31) >> 5;
   uint32_t hfmax = 0u;  // largest patched final key (LDS mode)
+  uint32_t nfin0 = 0u;  // patched finals at the front of the fast-path pool
   if (patch) {
     if (pst == 1) {
       pmode = 1;
@@ -2261,6 +2248,29 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
         }
       }
       hfmax = block_max(hfmax, S.r32);  // its barriers publish the table and the bitmap
+      if (fast) {  // finals at or above tmax open the fast-path pool, in slot order
+        uint32_t cnt = 0u;
+#pragma unroll
+        for (int m = 0; m < kTQ; ++m) {
+          const int ids[4] = {(int)tid4[m].x, (int)tid4[m].y, (int)tid4[m].z, (int)tid4[m].w};
+          const uint32_t fk[4] = {tfin4[m].x, tfin4[m].y, tfin4[m].z, tfin4[m].w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) cnt += (ids[q] >= 0 && fk[q] >= tmax && fk[q] >= kKeyFloor) ? 1u : 0u;
+        }
+        uint32_t off = block_excl_scan(cnt, S.r32, nfin0);
+#pragma unroll
+        for (int m = 0; m < kTQ; ++m) {
+          const int ids[4] = {(int)tid4[m].x, (int)tid4[m].y, (int)tid4[m].z, (int)tid4[m].w};
+          const uint32_t fk[4] = {tfin4[m].x, tfin4[m].y, tfin4[m].z, tfin4[m].w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if (ids[q] >= 0 && fk[q] >= tmax && fk[q] >= kKeyFloor) {
+              if (off < (uint32_t)a.pcap) pool[off] = make_uint2(fk[q], (uint32_t)ids[q]);
+              ++off;
+            }
+          }
+        }
+      }
     } else {
       // more distinct ids than the LDS table holds (status 2): the row's table in global
       // memory, cleared first (its contents before the call are unspecified)
@@ -2326,7 +2336,8 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
     uint32_t C = 0u;
     uint32_t Cv = 0u;  // valid pool elements (C less the invalidated raw copies)
     if (!slow) {
-      C = gather_pool<DT>(a, c, S, NG, pmode == 1, tmax, pool, Cv, nfin);
+      nfin = nfin0;
+      C = gather_pool<DT>(a, c, S, NG, pmode == 1, tmax, pool, Cv, nfin, cur);
       if ((int)C > a.pcap || (int)Cv < want) slow = true;
       phi = max(hi, hfmax);  // every pool key lies in [tmax, phi]
     }
