@@ -210,7 +210,7 @@ ss_status ss_process_logits(const void *logits, int dtype, int64_t ld, const ss_
  * fits).  Every call on one GPU uses that GPU's single array: calls that
  * overlap in time on one GPU (other streams, other threads) race.
  */
-#define SS_NOALLOC_BYTES (32u << 20)
+#define SS_NOALLOC_BYTES (48u << 20)
 ss_status ss_sample_noalloc(const void *logits, int dtype, int64_t ld, const ss_params *p, int k_max,
                             int32_t *out_token, float *out_logprob, int32_t *out_idx, float *out_prob,
                             int k_out, int32_t *flags, void *stream);

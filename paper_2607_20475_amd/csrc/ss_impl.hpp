@@ -11,25 +11,30 @@
 // invalid), finds a unit threshold t -- the largest 16-bit key prefix such
 // that at least q group maxima of the unit reach it, q being the unit's share
 // of the row's top-k plus a statistical margin -- and writes every group of
-// consecutive elements whose maximum reaches t to the unit's candidate region.
-// This is the paper's bounded candidate set of the two-stage scheme (Section
-// 3.2), chosen per unit by ballots instead of a per-tile sort.  Nothing here
-// depends on the request's penalty history or logit bias: those touch at most
-// a few hundred ids per row and are applied in the merge, so the streaming
-// pass has no barrier, no LDS and no per-row list traffic.
+// consecutive elements whose maximum reaches t to the unit's candidate region
+// (when ties at t overflow the region, the lowest-index tie groups, and the
+// unit's threshold becomes the composite (t, last kept index)).  This is the
+// paper's bounded candidate set of the two-stage scheme (Section 3.2), chosen
+// per unit by ballots instead of a per-tile sort.  The unit stream does not
+// depend on the request's penalty history or logit bias: those touch at most
+// a few hundred ids per row, and extra workgroups at the front of the same
+// launch build each row's patch table: the listed ids' counts and ordered
+// bias sums in an LDS hash, their raw logits gathered and put through the
+// Appendix C.1 prologue (repetition, frequency, presence penalty, bias; Alg. 8
+// order).
 //
 // Merge kernel, one workgroup per row:
-//   1. builds a hash table of the row's penalised / biased ids (LDS; a
-//      generation-tagged table in the workspace when the lists hold more
-//      distinct ids than LDS does) with occurrence counts and ordered bias
-//      sums, gathers their raw logits and applies the Appendix C.1 prologue
-//      (repetition, frequency, presence penalty, bias; Alg. 8 order);
+//   1. loads the unit records and the row's patch table (a generation-tagged
+//      table in the workspace is built here instead when the lists hold more
+//      distinct ids than the table does);
 //   2. gathers the candidate groups, drops the raw copies of patched ids and
-//      keeps the elements at or above the largest unit threshold tmax, plus
-//      the patched final values at or above it.  If at least k of them reach
-//      tmax they provably contain the row's exact top-k; otherwise (candidate
-//      overflow, skewed or heavily tied rows, patched top tokens) an exact
-//      slow path re-reads the units that could hide a top-k element;
+//      keeps the elements whose composite (key, lower index first) is at or
+//      above the largest unit threshold tc, plus the patched final values at
+//      or above it.  If at least k of them reach tc they provably contain the
+//      row's exact top-k; otherwise (candidate overflow, skewed rows, patched
+//      top tokens) an exact slow path re-reads the units that could hide a
+//      top-k element (greedy rows: only the units whose threshold exceeds the
+//      best unpatched candidate);
 //   3. selects the exact top-k (radix select, ties -> lower index) and runs
 //      the Alg. 11 epilogue: temperature weights, min-p, top-p and the token
 //      draw.  Top-p and the draw are "first element in canonical order whose
@@ -304,7 +309,15 @@ __host__ __device__ inline int unit_cap(int k_cap, int U, int dt) {
   const int gpu = groups_per_unit(dt);
   const int q = quota(k_cap, U);
   if (thr_groups(q, dt == SS_BF16 ? 8 : 16) == 0) return gpu;
-  const int c = 2 * q + 64;
+  // room for twice the quota, and, when less than a whole unit, for k_cap
+  // elements of one unit: a row tied at its maximum then finds its top-k
+  // among the lowest-index tie groups of its first unit (the tie cut keeps
+  // them)
+  const int ge = dt == SS_BF16 ? 4 : 2;
+  const int kg = (k_cap + ge - 1) / ge;
+  int c = 2 * q + 64;
+  if (kg < gpu && c < kg) c = kg;
+  if ((c & 63) == 0) c += 4;  // regions not a multiple of 1 KB apart: their heads spread over the memory channels
   return c < gpu ? c : gpu;
 }
 
@@ -392,7 +405,56 @@ __device__ __forceinline__ uint32_t thr_f32(const uint32_t (&kk)[32], uint32_t q
   return thr_search<G>(gm, q, 16);
 }
 
+// Ties at a unit threshold t can put more groups at or above t than the
+// unit's candidate region holds.  Then every group whose maximum exceeds t is
+// kept (when those alone fit) together with the lowest-index groups whose
+// maximum equals t, up to the capacity: the unit still holds every element
+// whose composite (key, lower index first) is at or above (t, cut), where
+// cut is the last element index of the last kept tie group.  gm[g] is group
+// g's maximum key; group g of a lane starts at element (g / 2 * 64 + lane) VW
+// + (g % 2) GE of the unit, so index order is (g / 2, lane, g % 2).  Returns
+// false (a true overflow) when the groups above t alone exceed the capacity.
+template <int NG, int VW, int GE>
+__device__ __forceinline__ bool tie_trim(const uint32_t (&gm)[NG], uint32_t t, uint32_t cap, uint32_t& gmask,
+                                         uint32_t& cut_rel) {
+  const int ln = lane();
+  uint32_t gtm = 0u, eqm = 0u;
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    gtm |= (gm[g] > t ? 1u : 0u) << g;
+    eqm |= (gm[g] == t ? 1u : 0u) << g;
+  }
+  uint32_t ngt;
+  (void)wave_excl_small((uint32_t)__popc(gtm), ngt);
+  if (ngt > cap) return false;
+  const uint32_t rem = cap - ngt;
+  uint32_t keep = 0u, base = 0u, last = 0u;
+#pragma unroll
+  for (int c = 0; c < NG / 2; ++c) {
+    const uint32_t e2 = (eqm >> (2 * c)) & 3u;
+    uint32_t tc;
+    uint32_t r = base + wave_excl_small((uint32_t)__popc(e2), tc);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if ((e2 >> h) & 1u) {
+        if (r < rem) {
+          keep |= 1u << (2 * c + h);
+          last = max(last, (uint32_t)((c * 64 + ln) * VW + h * GE + GE - 1));
+        }
+        ++r;
+      }
+    }
+    base += tc;
+  }
+  gmask = gtm | keep;
+  cut_rel = wave_max_u32(last);
+  return true;
+}
+
 // Streams unit `gu` (wave-uniform) and writes its record and candidate groups.
+// The record is (threshold key, groups written or the count that overflowed,
+// unit maximum key, last index of the tie cut or ~0u when every group at or
+// above the threshold was written).
 template <int DT>
 __device__ __forceinline__ void scan_unit(const KArgs& a, int gu) {
   constexpr int VW = DTT<DT>::VW, NLD = DTT<DT>::NLD, ES = DTT<DT>::ES, GPL = DTT<DT>::GPL;
@@ -455,7 +517,7 @@ __device__ __forceinline__ void scan_unit(const KArgs& a, int gu) {
   // 3. keys, unit maximum, threshold, emission
   uint4* region = a.cand + (size_t)gu * (size_t)a.cap;
   const uint32_t cap = (uint32_t)a.cap;
-  uint32_t t, wm, total;
+  uint32_t t, wm, total, cut = 0xFFFFFFFFu;
   if constexpr (DT == SS_BF16) {
     uint32_t kd[16];
 #pragma unroll
@@ -505,10 +567,20 @@ __device__ __forceinline__ void scan_unit(const KArgs& a, int gu) {
       else t16 = 0x0081u;
       t16 = max(t16, 0x0081u);
     }
-    uint32_t gmask = 0u;
+    uint32_t gmask = 0u, gm[8];
 #pragma unroll
-    for (int g = 0; g < 8; ++g) gmask |= (hmax16(pkmax16(kd[2 * g], kd[2 * g + 1])) >= t16) ? (1u << g) : 0u;
-    const uint32_t off = wave_excl_small((uint32_t)__popc(gmask), total);
+    for (int g = 0; g < 8; ++g) {
+      gm[g] = hmax16(pkmax16(kd[2 * g], kd[2 * g + 1]));
+      gmask |= (gm[g] >= t16) ? (1u << g) : 0u;
+    }
+    uint32_t off = wave_excl_small((uint32_t)__popc(gmask), total);
+    if (total > cap && t16 < 0x10000u) {
+      uint32_t cr;
+      if (tie_trim<8, 8, 4>(gm, t16, cap, gmask, cr)) {
+        cut = (uint32_t)lo + cr;
+        off = wave_excl_small((uint32_t)__popc(gmask), total);
+      }
+    }
 #pragma unroll
     for (int g = 0; g < 8; ++g) {
       if ((gmask >> g) & 1u) {
@@ -564,12 +636,20 @@ __device__ __forceinline__ void scan_unit(const KArgs& a, int gu) {
       else t = kKeyFloor;
       t = max(t, kKeyFloor);
     }
-    uint32_t gmask = 0u;
-    if (t != kNoEmit) {
+    uint32_t gmask = 0u, gm[16];
 #pragma unroll
-      for (int g = 0; g < 16; ++g) gmask |= (max(kk[2 * g], kk[2 * g + 1]) >= t) ? (1u << g) : 0u;
+    for (int g = 0; g < 16; ++g) {
+      gm[g] = max(kk[2 * g], kk[2 * g + 1]);
+      gmask |= (t != kNoEmit && gm[g] >= t) ? (1u << g) : 0u;
     }
-    const uint32_t off = wave_excl_small((uint32_t)__popc(gmask), total);
+    uint32_t off = wave_excl_small((uint32_t)__popc(gmask), total);
+    if (total > cap && t != kNoEmit) {
+      uint32_t cr;
+      if (tie_trim<16, 4, 2>(gm, t, cap, gmask, cr)) {
+        cut = (uint32_t)lo + cr;
+        off = wave_excl_small((uint32_t)__popc(gmask), total);
+      }
+    }
 #pragma unroll
     for (int g = 0; g < 16; ++g) {
       if ((gmask >> g) & 1u) {
@@ -579,7 +659,7 @@ __device__ __forceinline__ void scan_unit(const KArgs& a, int gu) {
       }
     }
   }
-  if (ln == 0) a.rec[gu] = make_uint4(t, total, wm, 0u);
+  if (ln == 0) a.rec[gu] = make_uint4(t, total, wm, cut);
 }
 
 // ===========================================================================
@@ -622,6 +702,25 @@ __device__ __forceinline__ uint32_t hslot(int id) { return ((uint32_t)id * 26544
 static_assert(kH == 2048, "hslot assumes 2048 slots");
 
 // Several workgroup reductions sharing one pair of barriers.
+// (max of a 64-bit value and of two 32-bit values)
+__device__ __forceinline__ void block_max64_2(uint64_t& w64, uint32_t& x, uint32_t& y, MSmem& S) {
+  w64 = wave_max(w64);
+  x = wave_max(x);
+  y = wave_max(y);
+  if (lane() == 0) {
+    S.x64[0][wave()] = w64;
+    S.x32[0][wave()] = x;
+    S.x32[1][wave()] = y;
+  }
+  lds_barrier();
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    w64 = max(w64, S.x64[0][w]);
+    x = max(x, S.x32[0][w]);
+    y = max(y, S.x32[1][w]);
+  }
+  lds_barrier();
+}
 __device__ __forceinline__ void block_max3(uint32_t& x, uint32_t& y, uint32_t& z, MSmem& S) {
   x = wave_max(x);
   y = wave_max(y);
@@ -1254,10 +1353,10 @@ __device__ __forceinline__ void gather_issue(const KArgs& a, const MSmem& S, int
 // Greedy rows whose emitted maxima are all patched ids with final values
 // below the raw maximum (a repetition penalty on the top token): the
 // processed maximum then lies below every unit threshold that the pool
-// covers.  Each unit emitted the groups holding its maximum, so the best
-// unpatched emitted element B bounds every unit whose maximum is at most B;
-// only the units whose maximum exceeds B (their maximum is patched) are
-// re-read whole.  Returns the composite of the processed maximum over the
+// covers.  Each unit emitted every element at or above its threshold (a
+// composite when ties were cut by index), so the best unpatched emitted
+// element B bounds every unit whose threshold is at most B; only the units
+// whose threshold exceeds B (their maximum is patched) are re-read whole.  Returns the composite of the processed maximum over the
 // unpatched raw values and the patched finals (LDS patch table, when `patch`).
 // Units that overflowed their candidate regions are marked for re-reading
 // already, and are re-read as well.
@@ -1290,11 +1389,10 @@ __device__ __forceinline__ uint64_t greedy_refill(const KArgs& a, const Ctx& c, 
     }
   }
   best = block_max(best, S.r64);
-  const uint32_t kb = comp_key(best);
   // 2. units whose maximum exceeds B
   for (int u = tid; u < U; u += kBlock) {
-    const uint32_t t = a.rec[(size_t)c.row * U + u].x;
-    if (t != kNoEmit && t > kb) atomicOr(&S.rmask[u >> 5], 1u << (u & 31));
+    const uint4 r4 = a.rec[(size_t)c.row * U + u];
+    if (r4.x != kNoEmit && comp_of(r4.x, r4.w) > best) atomicOr(&S.rmask[u >> 5], 1u << (u & 31));
   }
   lds_barrier();
   // 3. every element of those units (grammar mask applied, NaN invalid)
@@ -1648,14 +1746,12 @@ __device__ __forceinline__ int slow_select(const KArgs& a, const Ctx& c, MSmem& 
   o.op = VOP_COUNT;
   uint32_t nv = slow_visit<DT>(a, c, S, NG, 0, pmode, pg, o, nullptr);
   nv = block_sum(nv, S.r32);
-  uint32_t v0 = kKeyFloor;
-  if (nv >= (uint32_t)want) {
-    uint32_t i0;
-    slow_radix<DT>(a, c, S, NG, 0, pmode, pg, (uint32_t)want, nv, &v0, &i0);
-  }
+  uint32_t v0 = kKeyFloor, i0 = 0xFFFFFFFFu;
+  if (nv >= (uint32_t)want) slow_radix<DT>(a, c, S, NG, 0, pmode, pg, (uint32_t)want, nv, &v0, &i0);
+  // units whose threshold (ties cut by index) lies above the want-th candidate
   for (int u = tid; u < U; u += kBlock) {
-    const uint32_t tu = a.rec[(size_t)row * U + u].x;
-    if (tu != kNoEmit && tu > v0) atomicOr(&S.rmask[u >> 5], 1u << (u & 31));
+    const uint4 r4 = a.rec[(size_t)row * U + u];
+    if (r4.x != kNoEmit && comp_of(r4.x, r4.w) > comp_of(v0, i0)) atomicOr(&S.rmask[u >> 5], 1u << (u & 31));
   }
   lds_barrier();
   int nre = 0;
@@ -1683,7 +1779,8 @@ __device__ __forceinline__ int slow_select(const KArgs& a, const Ctx& c, MSmem& 
   return nT;
 }
 
-// Fast-path pool: every candidate element at or above tmax (raw copies of
+// Fast-path pool: every candidate element whose composite is at or above tc
+// (the largest unit threshold, ties cut by index; raw copies of
 // patched ids dropped) behind the nfin patched final values at or above it
 // already at pool[0, nfin), in a deterministic order (batches of groups held
 // in registers, block-scan offsets).  The caller issued the first batch
@@ -1692,12 +1789,13 @@ __device__ __forceinline__ int slow_select(const KArgs& a, const Ctx& c, MSmem& 
 // Returns the element count (elements beyond a.pcap are counted, not stored).
 template <int DT>
 __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MSmem& S, uint32_t NG, bool patch,
-                                                uint32_t tmax, uint2* pool, uint32_t& nvalid_out, uint32_t nfin,
+                                                uint64_t tc, uint2* pool, uint32_t& nvalid_out, uint32_t nfin,
                                                 GBatch& cur) {
   constexpr int GE = DTT<DT>::GE;
   const int tid = threadIdx.x;
   const int U = a.U;
   const uint32_t pcap = (uint32_t)a.pcap;
+  const uint32_t tck = comp_key(tc), tcut = comp_idx(tc);  // tc = (key, last index of its tie cut)
   uint32_t base = nfin;
   auto key_of = [](const uint4& gq, int e) -> uint32_t {
     if constexpr (DT == SS_BF16) return (((e < 2 ? gq.y : gq.z) >> (16 * (e & 1))) & 0xFFFFu) << 16;
@@ -1721,8 +1819,8 @@ __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MS
       pw[m] = 0u;
       if (patch && exact) pw[m] = S.pbits[go[m] == 0xFFFFFFFFu ? 0u : min(g[m].x >> 5, pwmax)];
     }
-    // selection: key >= tmax, valid, and not the raw copy of a patched id
-    // (its final value is in the pool already when it is >= tmax)
+    // selection: composite (key, index) >= tc, valid, and not the raw copy of
+    // a patched id (its final value is in the pool already when it is >= tc)
     uint32_t sel = 0u;
 #pragma unroll
     for (int m = 0; m < kPer; ++m) {
@@ -1730,7 +1828,8 @@ __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MS
 #pragma unroll
       for (int e = 0; e < GE; ++e) {
         const uint32_t k = key_of(g[m], e);
-        sel |= ((gv && k >= tmax && k >= kKeyFloor) ? 1u : 0u) << (m * GE + e);
+        const bool at = k > tck || (k == tck && g[m].x + (uint32_t)e <= tcut);  // composite >= tc
+        sel |= ((gv && at && k >= kKeyFloor) ? 1u : 0u) << (m * GE + e);
       }
     }
     if (patch) {
@@ -2179,7 +2278,8 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
     for (int s = tid; s < (pwords + 3) >> 2; s += kBlock) reinterpret_cast<uint4*>(S.pbits)[s] = make_uint4(0u, 0u, 0u, 0u);
   }
   // 1. unit records: largest threshold, row maximum, candidate offsets
-  uint32_t hi = 0u, tmax = 0u, ovf = 0u;
+  uint32_t hi = 0u, ovf = 0u;
+  uint64_t tc = 0ull;  // largest unit threshold as a composite (key, cut index)
   uint32_t NG = 0u;
   for (int h = 0; h * kBlock < U; ++h) {
     const int u = tid + h * kBlock;
@@ -2187,7 +2287,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
     if (u < U) {
       const uint4 r4 = a.rec[(size_t)row * U + u];
       hi = max(hi, r4.z);
-      if (r4.x != kNoEmit) tmax = max(tmax, r4.x);
+      if (r4.x != kNoEmit) tc = max(tc, comp_of(r4.x, r4.w));
       if (r4.y > cap) {  // partial candidate list: the unit is re-read by the slow path
         ovf = 1u;
         atomicOr(&S.rmask[u >> 5], 1u << (u & 31));
@@ -2201,7 +2301,8 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   }
   if (tid == 0) S.uoff[U] = NG;
   if (tid == 0) S.flagsw = 0u;
-  block_max3(hi, tmax, ovf, S);
+  block_max64_2(tc, hi, ovf, S);
+  const uint32_t tmax = comp_key(tc);  // every element at or above tc has a key >= tmax
 
   int flags = c.kcap ? SS_FLAG_KCAP : 0;
   const bool empty = hi < kKeyFloor;
@@ -2255,7 +2356,8 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
           const int ids[4] = {(int)tid4[m].x, (int)tid4[m].y, (int)tid4[m].z, (int)tid4[m].w};
           const uint32_t fk[4] = {tfin4[m].x, tfin4[m].y, tfin4[m].z, tfin4[m].w};
 #pragma unroll
-          for (int q = 0; q < 4; ++q) cnt += (ids[q] >= 0 && fk[q] >= tmax && fk[q] >= kKeyFloor) ? 1u : 0u;
+          for (int q = 0; q < 4; ++q)
+            cnt += (ids[q] >= 0 && comp_of(fk[q], (uint32_t)ids[q]) >= tc && fk[q] >= kKeyFloor) ? 1u : 0u;
         }
         uint32_t off = block_excl_scan(cnt, S.r32, nfin0);
 #pragma unroll
@@ -2264,7 +2366,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
           const uint32_t fk[4] = {tfin4[m].x, tfin4[m].y, tfin4[m].z, tfin4[m].w};
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            if (ids[q] >= 0 && fk[q] >= tmax && fk[q] >= kKeyFloor) {
+            if (ids[q] >= 0 && comp_of(fk[q], (uint32_t)ids[q]) >= tc && fk[q] >= kKeyFloor) {
               if (off < (uint32_t)a.pcap) pool[off] = make_uint2(fk[q], (uint32_t)ids[q]);
               ++off;
             }
@@ -2323,7 +2425,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
     }
   }
 
-  // 3. candidate pool: elements >= tmax (fast path)
+  // 3. candidate pool: elements whose composite is >= tc (fast path)
   int nT = 0;
   uint32_t tk = 0u, ti = 0u;
   bool slow = ovf != 0u;
@@ -2337,7 +2439,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
     uint32_t Cv = 0u;  // valid pool elements (C less the invalidated raw copies)
     if (!slow) {
       nfin = nfin0;
-      C = gather_pool<DT>(a, c, S, NG, pmode == 1, tmax, pool, Cv, nfin, cur);
+      C = gather_pool<DT>(a, c, S, NG, pmode == 1, tc, pool, Cv, nfin, cur);
       if ((int)C > a.pcap || (int)Cv < want) slow = true;
       phi = max(hi, hfmax);  // every pool key lies in [tmax, phi]
     }

@@ -461,8 +461,10 @@ def test_workspace_contents_do_not_matter(ssb):
 @pytest.mark.parametrize("kind", ["f32_zeros_2e18", "bf16_ties_2e17"])
 def test_flat_rows_full_size(ssb, kind):
     """The paper's correctness inputs (all zero; U(128.6, 128.7), all 129.0
-    in bf16) at full vocabulary size: every unit overflows its candidate
-    region and the exact slow path resolves the ties by index."""
+    in bf16) at full vocabulary size: every unit's ties overflow its candidate
+    region, so each keeps its lowest-index tie groups.  Sampling (k_max 1024)
+    finds its top-k in the first unit's groups without the slow path; top-k
+    rows beyond one unit's capacity take the exact slow path."""
     rng = np.random.default_rng(13)
     B = 4
     if kind == "f32_zeros_2e18":
@@ -480,7 +482,23 @@ def test_flat_rows_full_size(ssb, kind):
     say(f"[flat-{kind}] sample B={B} V={V}")
     tok, lp, fl = run_sample(ssb, smp)
     ref = check_sample(smp, tok, lp, fl, f"flat-{kind}")
-    assert (fl & FALLBACK).all()
+    assert not (fl & FALLBACK).any(), fl
+
+
+def test_tied_rows_headline_params(ssb):
+    """B=64 rows of one tied bf16 value (V=2^17) with the headline workload's
+    per-request parameters (mixed greedy and stochastic, k up to 900,
+    penalties over a 512-id history, bias): the tie cut keeps every row off
+    the slow path and the results match the oracle."""
+    inp = W.config1()
+    inp["x"] = np.full_like(inp["x"], W.bf16_bits_from_f32(np.array([0.5], np.float32))[0])
+    # k <= 900: the first unit's 1024 tie elements, less the listed ids among
+    # them (a few), cover every row's top-k
+    inp["top_k"] = np.minimum(inp["top_k"], 900).astype(np.int32)
+    say("[tied-headline] sample B=64 V=131072 bf16, one tied value")
+    tok, lp, fl = run_sample(ssb, inp)
+    check_sample(inp, tok, lp, fl, "tied-headline")
+    assert not (fl & FALLBACK).any(), np.nonzero(fl & FALLBACK)[0]
 
 
 # --------------------------------------------------------------------------

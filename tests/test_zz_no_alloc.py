@@ -59,7 +59,7 @@ def test_noalloc_matches_workspace_entry_point(ssb):
 def test_noalloc_rejects_sizes_beyond_its_array(ssb):
     inp = W.config1(B=8)
     n = ssb.workspace_bytes(ssb.OP_SAMPLE, 4096, 1 << 17, 0, 1024, ssb.BF16)
-    assert n > (32 << 20)
+    assert n > (48 << 20)
     x = torch.zeros(4096, 1 << 17, dtype=torch.bfloat16, device="cuda")
     prm = ssb.Params(4096, 1 << 17, mode=torch.zeros(4096, dtype=torch.int32, device="cuda"))
     o = [torch.empty(4096, dtype=torch.int32, device="cuda"), torch.empty(4096, device="cuda"),
