@@ -54,6 +54,9 @@ METRIC = ("µs per batch + rows/sec for fused sample/verify at V=2^17; "
 HBM_PEAK_GBS = 8000.0
 MALL_BYTES = 256 << 20
 CONFIGS = ("cfg0", "cfg1", "cfg2", "cfg3", "cfg4")
+# a stress line beside the five workloads: the headline batch with every
+# logit of a row equal (the paper's tied correctness inputs at full size)
+EXTRA = ("cfg1_tied",)
 WORKLOAD = {
     "cfg0": "tiny singular batch: fused sample B=4 V=32768 fp32, per-row temperature {0,0.7,1.0,1.3}, "
             "top-k 50, top-p 0.9",
@@ -63,7 +66,18 @@ WORKLOAD = {
             "k in {1,50,1024,4096}",
     "cfg3": "grammar-constrained fused sample: B=128 V=131072 bf16, 5% allow bitmask, penalties, bias",
     "cfg4": "multistep verification: B=64 L=4 V=131072 bf16 target, fp32 draft",
+    "cfg1_tied": "tied rows: the heterogeneous singular batch (B=64 V=131072 bf16, same parameters) with every "
+                 "logit 0.5",
 }
+
+
+def make_input(name, W):
+    """The named workload's seeded synthetic input."""
+    if name == "cfg1_tied":
+        inp = W.make_config("cfg1")
+        inp["x"] = np.full_like(inp["x"], W.bf16_bits_from_f32(np.array([0.5], np.float32))[0])
+        return inp
+    return W.make_config(name)
 READ_PROBE_BYTES = 64 << 20  # the plain read whose counters scale FETCH_SIZE
 
 
@@ -224,7 +238,7 @@ class Runner:
 
     def __init__(self, name, torch, ssb, W, dev="cuda"):
         self.name = name
-        self.inp = inp = W.make_config(name)
+        self.inp = inp = make_input(name, W)
         self.B = inp["B"]
         t = torch
         x0 = ssb.logits_tensor(inp, dev)
@@ -389,7 +403,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=256)
     ap.add_argument("--warmup", type=int, default=16)
-    ap.add_argument("--config", default="all", choices=("all",) + CONFIGS,
+    ap.add_argument("--config", default="all", choices=("all",) + CONFIGS + EXTRA,
                     help="time one workload only (profiling runs); 'all' times the five")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="wall time of the oracle baseline sample")
@@ -418,7 +432,7 @@ def main():
     from paper_2607_20475_amd import binding as ssb
     ssb.lib()
 
-    names = CONFIGS if args.config == "all" else (args.config,)
+    names = CONFIGS + EXTRA if args.config == "all" else (args.config,)
     head = "cfg1" if "cfg1" in names else names[0]
     entries = {}
     for name in names:
@@ -436,7 +450,7 @@ def main():
         counter_probes(torch, READ_PROBE_BYTES)
 
     h = entries[head]
-    inp = W.make_config(head)
+    inp = make_input(head, W)
     us = h["us_per_batch"]
     prof = h.get("profile") or {}
     split = prof.get("kernels")
