@@ -476,11 +476,15 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "ss_sample call: ss_stream_kernel + ss_merge_kernel (back to back)",
                      "achieved": h["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": h["frac"],
                      "traffic": traffic, "alg_bytes_per_launch": h["alg_bytes"], "us_per_launch": us,
-                     "launches_timed": args.steps, "kernel_split_us": split},
+                     "launches_timed": args.steps, "kernel_split_us": split,
+                     "note": "the method's bound is HBM (every logit read once); of the call's two kernels the "
+                             "row merge (one workgroup per row, a dependent chain of LDS and VALU steps) is "
+                             "latency-bound and the longer one; the streaming kernel takes about twice the plain "
+                             "read of the same bytes (read_ceiling)"},
         "fallback_rows": h["fallback_rows"],
         "configs": {k: v for k, v in entries.items() if k != head},
     }
-    if head in ("cfg1", "cfg2"):
+    if head in ("cfg1", "cfg2") and not args.read_probe:  # counter runs keep the probe the only plain read
         res["read_ceiling"] = read_ceiling(torch, h["alg_bytes"])
     if not args.no_cpu and head != "cfg2" and head != "cfg4":
         nthreads = os.cpu_count() or 1
