@@ -189,6 +189,21 @@ def topk(inp, nthreads=0):
     return val, idx
 
 
+def logprobs(inp, n_lp, nthreads=0):
+    """Top-k log-probabilities of the rows with indicator bit 0x400: indices
+    [B, n_lp] int32 (canonical order of the processed logits, -1 padded) and
+    log-probabilities [B, n_lp] float32 under the untruncated softmax(y / tau)
+    of the row (-inf padded)."""
+    B, V = int(inp["B"]), int(inp["V"])
+    x = _x(inp)
+    bd = _Bundle(inp)
+    idx = np.empty((B, n_lp), np.int32)
+    lp = np.empty((B, n_lp), np.float32)
+    lib().ssref_logprobs(_ptr(x), C.c_int(_dtype_code(inp)), C.c_int64(V), C.byref(bd.p), C.c_int(n_lp),
+                         _ptr(idx), _ptr(lp), C.c_int(nthreads))
+    return idx, lp
+
+
 def verify(inp, nthreads=0):
     """Multistep verification.
 

@@ -22,7 +22,10 @@
  *     uniform from Philox4x32-10 keyed by (seed, request, position);
  *   - speculative verification (Section 3.1 "Speculative Verification",
  *     Appendix C.4): accept when u*q(d) <= p(d), else resample from
- *     normalize(max(0, p - q)); a bonus token after full acceptance.
+ *     normalize(max(0, p - q)); a bonus token after full acceptance;
+ *   - top-k log-probabilities (indicator bit 0x400 of the bit-level encoding
+ *     table, Section 3.5): the leading tokens of the canonical order with
+ *     their log-probabilities under the untruncated distribution of the row.
  *
  * Probabilities, sums and every decision taken on them are in double
  * precision.  Readings of points the paper leaves open are listed in the
@@ -40,7 +43,7 @@
 enum {
   R_GRAMMAR = 0x001, R_REP = 0x002, R_FREQ = 0x004, R_PRES = 0x008,
   R_BIAS = 0x010, R_TEMP = 0x020, R_GREEDY = 0x040, R_TOPK = 0x080,
-  R_TOPP = 0x100, R_MINP = 0x200
+  R_TOPP = 0x100, R_MINP = 0x200, R_LOGPROBS = 0x400
 };
 /* Per-row result flags. */
 enum { RF_EMPTY = 1, RF_KCAP = 8 };
@@ -569,6 +572,52 @@ int ssref_topk(const void *x, int dtype, int B, int V, int64_t ld, const int32_t
     for (int r = 0; r < k_max; ++r) {
       out_val[(int64_t)b * k_max + r] = (r < kb) ? y[order[r]] : -INFINITY;
       out_idx[(int64_t)b * k_max + r] = (r < kb) ? order[r] : -1;
+    }
+    free(y); free(order);
+  }
+  return 0;
+}
+
+/* Top-k log-probabilities (indicator bit 0x400, Section 3.5; the log-
+ * probability output of Alg. 11).  For a row with the bit: the first
+ * min(n_lp, n_valid) tokens of the canonical order of the processed logits y
+ * (value descending, lower index first) and their log-probabilities under the
+ * untruncated distribution softmax(y / tau) over every valid token:
+ *   lp_i = (y_i - M) / tau - ln sum_j exp((y_j - M) / tau),   M = max_j y_j,
+ * tau the row's temperature when its bit is on, tau > 0 and the row is not
+ * greedy, else 1 (a greedy row reports the untempered distribution).  Top-k,
+ * top-p and min-p do not apply.  Rows without the bit, and entries beyond the
+ * valid tokens, hold (-1, -inf). */
+int ssref_logprobs(const void *x, int dtype, int64_t ld, const ssref_params *p, int n_lp,
+                   int32_t *out_idx, float *out_lp, int nthreads) {
+  int B = p->B, V = p->V;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+#endif
+  for (int b = 0; b < B; ++b) {
+    int32_t *oi = out_idx + (int64_t)b * n_lp;
+    float *ol = out_lp + (int64_t)b * n_lp;
+    for (int r = 0; r < n_lp; ++r) { oi[r] = -1; ol[r] = -INFINITY; }
+    uint32_t mode = p->mode ? p->mode[b] : 0u;
+    if (!(mode & R_LOGPROBS)) continue;
+    float *y = (float *)malloc(sizeof(float) * (size_t)V);
+    int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)V);
+    process_one(x, dtype, (int64_t)b * ld, p, b, NULL, 0, b, y);
+    int nv = ssref_order(y, V, order);
+    if (nv > 0) {
+      uint32_t em = effective_mode(p, b);
+      double tau = 1.0;
+      if ((em & R_TEMP) && !(em & R_GREEDY) && p->temperature[b] > 0.0f) tau = (double)p->temperature[b];
+      double M = (double)y[order[0]];
+      double Z = 0.0;
+      for (int r = 0; r < nv; ++r) Z += exp(((double)y[order[r]] - M) / tau);
+      double lz = log(Z);
+      int n = n_lp < nv ? n_lp : nv;
+      for (int r = 0; r < n; ++r) {
+        oi[r] = order[r];
+        ol[r] = (float)(((double)y[order[r]] - M) / tau - lz);
+      }
     }
     free(y); free(order);
   }

@@ -37,6 +37,13 @@ MUTANTS = [
      "test_draw_boundary_distance"),
     ("acceptance_band_closed", "        near = m < SSREF_NEAR;", "        near = 0;",
      "test_verify_admits_accept_and_reject"),
+    ("logprob_normaliser_over_listed_tokens", "      for (int r = 0; r < nv; ++r) Z += exp(((double)y[order[r]] - M) / tau);",
+     "      for (int r = 0; r < (n_lp < nv ? n_lp : nv); ++r) Z += exp(((double)y[order[r]] - M) / tau);",
+     "test_logprobs_match_scipy_log_softmax"),
+    ("logprob_temperature_ignored",
+     "      if ((em & R_TEMP) && !(em & R_GREEDY) && p->temperature[b] > 0.0f) tau = (double)p->temperature[b];",
+     "      if ((em & R_TEMP) && !(em & R_GREEDY) && p->temperature[b] > 0.0f) tau = 1.0;",
+     "test_logprobs_temperature_scales_differences"),
     ("uniform_counter_words_swapped", "  uint32_t ctr[4] = {request, (uint32_t)((uint64_t)position & 0xFFFFFFFFu),",
      "  uint32_t ctr[4] = {(uint32_t)((uint64_t)position & 0xFFFFFFFFu), request,",
      "test_uniform_counter_words"),

@@ -512,3 +512,105 @@ def test_verify_admits_accept_and_reject_at_the_acceptance_boundary():
     assert out["n_adm"][0] >= 2
     far, _ = _accept_case(1e-4)
     assert far["n_adm"][0] == 1 and far["tokens"][0].tolist() == [1, -1]
+
+
+# --------------------------------------------------------------------------
+# Top-k log-probabilities (indicator bit 0x400)
+# --------------------------------------------------------------------------
+def _lp_rows(rng, B, V, tau, mask=False):
+    x = rng.normal(0.0, 2.0, (B, V)).astype(np.float32)
+    x[:, : V // 8] = np.round(x[:, : V // 8])  # exact ties among the leaders
+    mode = np.full(B, W.MODE_LOGPROBS | W.MODE_TEMP | W.MODE_REP | W.MODE_BIAS, np.uint32)
+    hist = [rng.integers(0, V, 12).astype(np.int32) for _ in range(B)]
+    bids = [rng.choice(V, 3, replace=False).astype(np.int32) for _ in range(B)]
+    extra = {}
+    if mask:
+        m = np.full((B, (V + 31) // 32), 0xFFFFFFFF, np.uint32)
+        m[:, 0] = 0x0000FFFF  # ids 16..31 denied
+        extra = dict(bitmask=m)
+        mode |= np.uint32(W.MODE_GRAMMAR)
+    return W.custom_rows(x, W.F32, k_max=V, mode=mode, temperature=np.asarray(tau, np.float32),
+                         rep=np.full(B, 1.3, np.float32),
+                         hist_offsets=np.arange(0, 12 * B + 1, 12, dtype=np.int32), hist_ids=np.concatenate(hist),
+                         bias_offsets=np.arange(0, 3 * B + 1, 3, dtype=np.int32), bias_ids=np.concatenate(bids),
+                         bias_vals=rng.uniform(-3, 3, 3 * B).astype(np.float32), **extra)
+
+
+def test_logprobs_two_token_closed_form():
+    """Two logits 0 and ln 3: probabilities 1/4 and 3/4."""
+    y1 = np.float32(np.log(3.0))
+    inp = W.custom_rows(np.array([[0.0, y1]], np.float32), W.F32, k_max=2, mode=np.array([W.MODE_LOGPROBS]))
+    idx, lp = oracle.logprobs(inp, 2)
+    assert idx.tolist() == [[1, 0]]
+    z = 1.0 + math.exp(float(y1))
+    assert lp[0, 0] == pytest.approx(float(y1) - math.log(z), abs=1e-7)
+    assert lp[0, 1] == pytest.approx(-math.log(z), abs=1e-7)
+
+
+@pytest.mark.parametrize("mask", [False, True])
+def test_logprobs_match_scipy_log_softmax(mask):
+    """The leading n_lp tokens and their log-probabilities equal scipy's
+    log_softmax of the processed logits at the row's temperature, the
+    normaliser running over every valid token (masked ids excluded)."""
+    rng = np.random.default_rng(77)
+    B, V, n = 6, 200, 17
+    tau = rng.uniform(0.4, 2.0, B)
+    inp = _lp_rows(rng, B, V, tau, mask)
+    idx, lp = oracle.logprobs(inp, n)
+    y = oracle.process_logits(inp)["y"].astype(np.float64)
+    for b in range(B):
+        valid = np.isfinite(y[b])
+        ls = np.full(V, -np.inf)
+        ls[valid] = special.log_softmax(y[b][valid] / float(np.float32(tau[b])))
+        order = np.lexsort((np.arange(V), -y[b]))
+        order = order[valid[order]]
+        assert idx[b].tolist() == order[:n].tolist()
+        np.testing.assert_allclose(lp[b], ls[order[:n]], rtol=1e-6, atol=1e-6)
+
+
+def test_logprobs_full_list_sums_to_one():
+    rng = np.random.default_rng(78)
+    B, V = 4, 96
+    inp = _lp_rows(rng, B, V, rng.uniform(0.5, 1.5, B), mask=True)
+    idx, lp = oracle.logprobs(inp, V)
+    for b in range(B):
+        k = idx[b] >= 0
+        assert np.exp(lp[b][k].astype(np.float64)).sum() == pytest.approx(1.0, abs=1e-5)
+        assert (~k).sum() == 16  # the denied ids pad the tail
+
+
+def test_logprobs_temperature_scales_differences():
+    """lp_i - lp_j = (y_i - y_j) / tau for any two listed tokens."""
+    rng = np.random.default_rng(79)
+    B, V, n = 3, 128, 10
+    tau = np.array([0.5, 1.0, 1.7])
+    inp = _lp_rows(rng, B, V, tau)
+    idx, lp = oracle.logprobs(inp, n)
+    y = oracle.process_logits(inp)["y"].astype(np.float64)
+    for b in range(B):
+        t = float(np.float32(tau[b]))
+        d_lp = lp[b, 0] - lp[b, 1:]
+        d_y = (y[b, idx[b, 0]] - y[b, idx[b, 1:]]) / t
+        np.testing.assert_allclose(d_lp, d_y, atol=2e-6)
+
+
+def test_logprobs_rows_without_the_bit_greedy_and_empty():
+    """Rows without bit 0x400 and fully masked rows are padded; a greedy row
+    (or one with the temperature bit off) reports tau = 1 log-probabilities."""
+    rng = np.random.default_rng(80)
+    V = 64
+    x = rng.normal(0, 1, (4, V)).astype(np.float32)
+    mask = np.full((4, 2), 0xFFFFFFFF, np.uint32)
+    mask[3] = 0
+    mode = np.array([0, W.MODE_LOGPROBS | W.MODE_GREEDY | W.MODE_TEMP, W.MODE_LOGPROBS,
+                     W.MODE_LOGPROBS | W.MODE_GRAMMAR], np.uint32)
+    inp = W.custom_rows(x, W.F32, k_max=V, mode=mode, temperature=np.array([1.0, 0.3, 0.3, 1.0], np.float32),
+                        bitmask=mask)
+    idx, lp = oracle.logprobs(inp, 5)
+    assert (idx[0] == -1).all() and np.isneginf(lp[0]).all()
+    assert (idx[3] == -1).all() and np.isneginf(lp[3]).all()
+    for b in (1, 2):
+        ls = special.log_softmax(x[b].astype(np.float64))
+        order = np.lexsort((np.arange(V), -x[b]))[:5]
+        assert idx[b].tolist() == order.tolist()
+        np.testing.assert_allclose(lp[b], ls[order], atol=1e-6)
