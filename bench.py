@@ -56,7 +56,8 @@ MALL_BYTES = 256 << 20
 CONFIGS = ("cfg0", "cfg1", "cfg2", "cfg3", "cfg4")
 # a stress line beside the five workloads: the headline batch with every
 # logit of a row equal (the paper's tied correctness inputs at full size)
-EXTRA = ("cfg1_tied",)
+EXTRA = ("cfg1_tied", "cfg1_logprobs")
+LOGPROBS_N = 20  # log-probabilities per request on the log-probability line
 WORKLOAD = {
     "cfg0": "tiny singular batch: fused sample B=4 V=32768 fp32, per-row temperature {0,0.7,1.0,1.3}, "
             "top-k 50, top-p 0.9",
@@ -68,11 +69,17 @@ WORKLOAD = {
     "cfg4": "multistep verification: B=64 L=4 V=131072 bf16 target, fp32 draft",
     "cfg1_tied": "tied rows: the heterogeneous singular batch (B=64 V=131072 bf16, same parameters) with every "
                  "logit 0.5",
+    "cfg1_logprobs": "top-20 log-probabilities (ss_logprobs) of the heterogeneous singular batch (B=64 V=131072 "
+                     "bf16, penalties, bias), every request with bit 0x400",
 }
 
 
 def make_input(name, W):
     """The named workload's seeded synthetic input."""
+    if name == "cfg1_logprobs":
+        inp = W.make_config("cfg1")
+        inp["mode"] = inp["mode"] | np.uint32(W.MODE_LOGPROBS)
+        return inp
     if name == "cfg1_tied":
         inp = W.make_config("cfg1")
         inp["x"] = np.full_like(inp["x"], W.bf16_bits_from_f32(np.array([0.5], np.float32))[0])
@@ -98,6 +105,8 @@ def algorithmic_bytes(name, inp):
     b = _nbytes(inp["x"]) + 48 * B + _nbytes(inp.get("bitmask"))
     for k in ("hist_offsets", "hist_ids", "bias_offsets", "bias_ids", "bias_vals"):
         b += _nbytes(inp.get(k))
+    if name == "cfg1_logprobs":
+        return b + B * (LOGPROBS_N * 8 + 4)  # (index, log-probability) pairs and flags
     if name == "cfg4":
         L = int(inp["L"])
         return b + _nbytes(inp["draft_tokens"]) + B * L * (inp["k_max"] + 1) * 4 + B * (L + 2) * 4
@@ -255,6 +264,15 @@ class Runner:
 
             def step(i):
                 ssb.topk(self.xs[i % self.R], k, inp["k_max"], out_val=ov, out_idx=oi, flags=fl, ws=ws)
+        elif name == "cfg1_logprobs":
+            prm = ssb.Params.from_arrays(inp, dev)
+            ws = ssb.workspace(ssb.OP_LOGPROBS, inp["B"], inp["V"], 0, LOGPROBS_N, ssb.BF16, dev)
+            oi = t.empty(inp["B"], LOGPROBS_N, dtype=t.int32, device=dev)
+            ol = t.empty(inp["B"], LOGPROBS_N, dtype=t.float32, device=dev)
+            fl = t.empty(inp["B"], dtype=t.int32, device=dev)
+
+            def step(i):
+                ssb.logprobs(self.xs[i % self.R], prm, LOGPROBS_N, out_idx=oi, out_lp=ol, flags=fl, ws=ws)
         elif name == "cfg4":
             L = inp["L"]
             q = t.from_numpy(np.ascontiguousarray(inp["draft_probs"], np.float32)).to(dev)

@@ -10,6 +10,8 @@
  *                      from normalize(max(0, p - q)); bonus token on full acceptance
  *   ss_topk            exact top-k (value, index) per row (Section 3.4)
  *   ss_process_logits  materialised processed logits and final probabilities
+ *   ss_logprobs        top-k log-probabilities under the full-row distribution
+ *                      (indicator bit 0x400, Section 3.5)
  *
  * Conventions (all functions):
  *   - Every array argument is a DEVICE pointer owned by the caller, except
@@ -70,7 +72,7 @@ typedef int32_t ss_status;
 #define SS_TOPK 0x080u     /* top-k filtering                                    */
 #define SS_TOPP 0x100u     /* top-p filtering                                    */
 #define SS_MINP 0x200u     /* min-p filtering                                    */
-#define SS_LOGPROBS 0x400u /* top-k log-probabilities (accepted, not produced)   */
+#define SS_LOGPROBS 0x400u /* top-k log-probabilities (ss_logprobs)              */
 
 /* Per-row result flags (int32 flags[rows]). */
 #define SS_FLAG_EMPTY 1      /* every token masked: token -1                       */
@@ -83,6 +85,7 @@ typedef int32_t ss_status;
 #define SS_OP_SAMPLE 1
 #define SS_OP_VERIFY 2
 #define SS_OP_PROCESS 3
+#define SS_OP_LOGPROBS 4
 
 /* Limits. */
 #define SS_MAX_K 4096      /* k_max upper bound                                    */
@@ -198,6 +201,30 @@ ss_status ss_verify(const void *target_logits, int dtype, int64_t ld_row, const 
 ss_status ss_process_logits(const void *logits, int dtype, int64_t ld, const ss_params *p, int k_max,
                             float *out_logits, float *out_probs, int32_t *flags, void *ws,
                             size_t ws_bytes, void *stream);
+
+/*
+ * Top-k log-probabilities (indicator bit SS_LOGPROBS = 0x400 of the
+ * bit-level encoding table, Section 3.5; the log-probability output of
+ * Alg. 11).  For every request whose mode has the bit: the n_lp leading
+ * tokens of the canonical order of its processed logits y (the Appendix C.1
+ * prologue: grammar mask, penalties, bias; value descending, lower index
+ * first) and their log-probabilities under the untruncated distribution
+ * softmax(y / tau) over all valid tokens of the row:
+ *     lp_i = (y_i - M) / tau - ln sum_j exp((y_j - M) / tau),   M = max_j y_j,
+ * tau being the request's temperature when SS_TEMP is set, tau > 0 and the
+ * request is not greedy, else 1.  Top-k, top-p and min-p do not apply.
+ *   logits    [B, ld] of `dtype`.
+ *   n_lp      1..SS_MAX_K entries per request.
+ *   out_idx   int32[B, n_lp], out_lp float[B, n_lp]: padded with (-1, -inf)
+ *             beyond the valid tokens and for requests without the bit.
+ *   flags     int32[B] or NULL.
+ *   ws        ss_workspace_bytes(SS_OP_LOGPROBS, B, V, 0, n_lp, dtype) bytes.
+ * The normaliser's terms are float32 exponentials summed in double
+ * (relative error below about 2e-7).
+ */
+ss_status ss_logprobs(const void *logits, int dtype, int64_t ld, const ss_params *p, int n_lp,
+                      int32_t *out_idx, float *out_lp, int32_t *flags, void *ws, size_t ws_bytes,
+                      void *stream);
 
 /*
  * ss_sample with no workspace argument, for callers that cannot allocate

@@ -21,7 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libss.so")
 GRAMMAR, REP, FREQ, PRES, BIAS, TEMP = 0x001, 0x002, 0x004, 0x008, 0x010, 0x020
 GREEDY, TOPK, TOPP, MINP, LOGPROBS = 0x040, 0x080, 0x100, 0x200, 0x400
 FLAG_EMPTY, FLAG_FALLBACK, FLAG_OUT_TRUNC, FLAG_KCAP = 1, 2, 4, 8
-OP_TOPK, OP_SAMPLE, OP_VERIFY, OP_PROCESS = 0, 1, 2, 3
+OP_TOPK, OP_SAMPLE, OP_VERIFY, OP_PROCESS, OP_LOGPROBS = 0, 1, 2, 3, 4
 F32, BF16 = 0, 1
 
 _lib = None
@@ -67,6 +67,9 @@ def lib():
         L.ss_verify.restype = i32
         L.ss_verify.argtypes = [vp, C.c_int, i64, vp, i64, vp, C.c_int, C.POINTER(_Params), C.c_int, vp, vp,
                                 vp, vp, sz, vp]
+        if hasattr(L, "ss_logprobs"):
+            L.ss_logprobs.restype = i32
+            L.ss_logprobs.argtypes = [vp, C.c_int, i64, C.POINTER(_Params), C.c_int, vp, vp, vp, vp, sz, vp]
         L.ss_process_logits.restype = i32
         L.ss_process_logits.argtypes = [vp, C.c_int, i64, C.POINTER(_Params), C.c_int, vp, vp, vp, vp, sz, vp]
         L.ss_status_string.restype = C.c_char_p
@@ -173,6 +176,22 @@ def topk(x, k, k_max, out_val=None, out_idx=None, flags=None, ws=None):
     _check(lib().ss_topk(_ptr(x), dt, B, V, x.stride(0), _ptr(k), k_max, _ptr(out_val), _ptr(out_idx),
                          _ptr(flags), _ptr(ws), ws.numel(), _stream()))
     return out_val, out_idx
+
+
+def logprobs(logits, params, n_lp, out_idx=None, out_lp=None, flags=None, ws=None):
+    """Top-k log-probabilities (rows whose mode has bit 0x400): indices and
+    log-probabilities [B, n_lp] under the full-row distribution."""
+    B, V = logits.shape
+    dt = _dtype_code(logits)
+    ws = _ws(ws, OP_LOGPROBS, B, V, 0, n_lp, dt, logits.device)
+    if out_idx is None:
+        out_idx = torch.empty(B, n_lp, dtype=torch.int32, device=logits.device)
+    if out_lp is None:
+        out_lp = torch.empty(B, n_lp, dtype=torch.float32, device=logits.device)
+    p = params.struct()
+    _check(lib().ss_logprobs(_ptr(logits), dt, logits.stride(0), C.byref(p), n_lp, _ptr(out_idx), _ptr(out_lp),
+                             _ptr(flags), _ptr(ws), ws.numel(), _stream()))
+    return out_idx, out_lp
 
 
 def sample(logits, params, k_max, k_out=0, out_token=None, out_logprob=None, out_idx=None, out_prob=None,

@@ -11,7 +11,7 @@ namespace ss {
 struct Layout {
   int U, cap, pcap, rows, smem;
   size_t off_rec, off_cand, off_res, off_patch, off_npatch, off_gtag, off_gcnt, off_gfin,
-      off_pstat, off_ptab, total;
+      off_pstat, off_ptab, off_usum, total;
 };
 
 static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -19,7 +19,7 @@ static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 static bool make_layout(int op, int B, int V, int L, int k_max, int dtype, Layout* lay) {
   if (B <= 0 || V <= 0 || V > SS_MAX_V || k_max < 1 || k_max > SS_MAX_K) return false;
   if (op == OP_VERIFY && (L < 1 || L > SS_MAX_L)) return false;
-  if (op < OP_TOPK || op > OP_PROCESS) return false;
+  if (op < OP_TOPK || op > OP_LOGPROBS) return false;
   const int rows = op == OP_VERIFY ? B * (L + 1) : B;
   const int U = (V + kUE - 1) / kUE;
   const int cap = unit_cap(k_max, U, dtype);
@@ -53,6 +53,9 @@ static bool make_layout(int op, int B, int V, int L, int k_max, int dtype, Layou
   o = align256(o + ghr * 4);
   lay->off_ptab = o;
   o = align256(o + ghr * 2 * kH * 4);
+  // log-probabilities: every unit's share of its row's normaliser
+  lay->off_usum = o;
+  if (op == OP_LOGPROBS) o = align256(o + (size_t)rows * U * 8);
   lay->total = o;
   lay->U = U;
   lay->cap = cap;
@@ -63,7 +66,8 @@ static bool make_layout(int op, int B, int V, int L, int k_max, int dtype, Layou
 }
 
 static uint32_t feature_mask(const ss_params* p) {
-  uint32_t f = SS_GREEDY | SS_GRAMMAR | SS_REP | SS_FREQ | SS_PRES | SS_BIAS | SS_TEMP | SS_TOPK | SS_TOPP | SS_MINP;
+  uint32_t f = SS_GREEDY | SS_GRAMMAR | SS_REP | SS_FREQ | SS_PRES | SS_BIAS | SS_TEMP | SS_TOPK | SS_TOPP | SS_MINP |
+               SS_LOGPROBS;
   if (!p->temperature) f &= ~SS_TEMP;
   if (!p->top_k) f &= ~SS_TOPK;
   if (!p->top_p) f &= ~SS_TOPP;
@@ -106,6 +110,7 @@ static void launch_merge_any(const KArgs& k, int dtype, dim3 grid, dim3 block, i
       case OP_TOPK: launch_merge<SS_BF16, OP_TOPK>(k, grid, block, smem, st); break;
       case OP_SAMPLE: launch_merge<SS_BF16, OP_SAMPLE>(k, grid, block, smem, st); break;
       case OP_VERIFY: launch_merge<SS_BF16, OP_VERIFY>(k, grid, block, smem, st); break;
+      case OP_LOGPROBS: launch_merge<SS_BF16, OP_LOGPROBS>(k, grid, block, smem, st); break;
       default: launch_merge<SS_BF16, OP_PROCESS>(k, grid, block, smem, st); break;
     }
   } else {
@@ -113,6 +118,7 @@ static void launch_merge_any(const KArgs& k, int dtype, dim3 grid, dim3 block, i
       case OP_TOPK: launch_merge<SS_F32, OP_TOPK>(k, grid, block, smem, st); break;
       case OP_SAMPLE: launch_merge<SS_F32, OP_SAMPLE>(k, grid, block, smem, st); break;
       case OP_VERIFY: launch_merge<SS_F32, OP_VERIFY>(k, grid, block, smem, st); break;
+      case OP_LOGPROBS: launch_merge<SS_F32, OP_LOGPROBS>(k, grid, block, smem, st); break;
       default: launch_merge<SS_F32, OP_PROCESS>(k, grid, block, smem, st); break;
     }
   }
@@ -124,6 +130,7 @@ static hipError_t merge_smem_any(int dtype, int op, int bytes) {
       case OP_TOPK: return merge_smem_limit<SS_BF16, OP_TOPK>(bytes);
       case OP_SAMPLE: return merge_smem_limit<SS_BF16, OP_SAMPLE>(bytes);
       case OP_VERIFY: return merge_smem_limit<SS_BF16, OP_VERIFY>(bytes);
+      case OP_LOGPROBS: return merge_smem_limit<SS_BF16, OP_LOGPROBS>(bytes);
       default: return merge_smem_limit<SS_BF16, OP_PROCESS>(bytes);
     }
   }
@@ -131,11 +138,12 @@ static hipError_t merge_smem_any(int dtype, int op, int bytes) {
     case OP_TOPK: return merge_smem_limit<SS_F32, OP_TOPK>(bytes);
     case OP_SAMPLE: return merge_smem_limit<SS_F32, OP_SAMPLE>(bytes);
     case OP_VERIFY: return merge_smem_limit<SS_F32, OP_VERIFY>(bytes);
+    case OP_LOGPROBS: return merge_smem_limit<SS_F32, OP_LOGPROBS>(bytes);
     default: return merge_smem_limit<SS_F32, OP_PROCESS>(bytes);
   }
 }
 
-static bool smem_configured[2][4];
+static bool smem_configured[2][5];
 
 static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStream_t st, bool materialize) {
   unsigned char* w = reinterpret_cast<unsigned char*>(ws);
@@ -153,6 +161,7 @@ static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStr
   k.gfin = reinterpret_cast<uint32_t*>(w + lay.off_gfin);
   k.pstat = reinterpret_cast<int32_t*>(w + lay.off_pstat);
   k.ptab = reinterpret_cast<uint32_t*>(w + lay.off_ptab);
+  k.usum = k.op == OP_LOGPROBS ? reinterpret_cast<double*>(w + lay.off_usum) : nullptr;
   // patch-table workgroups (a multiple of 8, so the stream's XCD remap holds)
   k.patch_wgs = k.op == OP_TOPK ? 0 : (lay.rows + 7) & ~7;
   const int di = dtype == SS_BF16 ? 1 : 0;
@@ -166,10 +175,11 @@ static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStr
   const dim3 grid((unsigned)(k.patch_wgs + (nunits + kSWaves - 1) / kSWaves)), sblock(kSBlock),
       rgrid((unsigned)lay.rows), block(kBlock);
   const int psmem = k.patch_wgs ? (int)sizeof(PSmem) : 0;
+  const bool lp = k.op == OP_LOGPROBS;
   if (dtype == SS_BF16)
-    launch_stream<SS_BF16>(k, grid, sblock, psmem, st);
+    lp ? launch_stream<SS_BF16, true>(k, grid, sblock, psmem, st) : launch_stream<SS_BF16, false>(k, grid, sblock, psmem, st);
   else
-    launch_stream<SS_F32>(k, grid, sblock, psmem, st);
+    lp ? launch_stream<SS_F32, true>(k, grid, sblock, psmem, st) : launch_stream<SS_F32, false>(k, grid, sblock, psmem, st);
   launch_merge_any(k, dtype, rgrid, block, lay.smem, st);
   if (k.op == OP_VERIFY) launch_assemble(k, dim3((unsigned)((k.B + kBlock - 1) / kBlock)), block, st);
   if (materialize) {
@@ -235,6 +245,31 @@ ss_status ss_topk(const void* x, int dtype, int B, int V, int64_t ld, const int3
   a.top_k = k;
   a.out_val = out_val;
   a.out_idx = out_idx;
+  a.flags = flags;
+  return launch(a, dtype, lay, ws, (hipStream_t)stream, false);
+}
+
+ss_status ss_logprobs(const void* logits, int dtype, int64_t ld, const ss_params* p, int n_lp, int32_t* out_idx,
+                      float* out_lp, int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+  if (!logits || !p || !out_idx || !out_lp || !ws || (dtype != SS_F32 && dtype != SS_BF16)) return SS_ERR_INVALID_ARG;
+  const int B = p->B, V = p->V;
+  if (ld < V || !params_ok(p, B, V)) return SS_ERR_INVALID_ARG;
+  Layout lay;
+  if (!make_layout(OP_LOGPROBS, B, V, 0, n_lp, dtype, &lay)) return SS_ERR_INVALID_ARG;
+  if (ws_bytes < lay.total || !aligned16(ws)) return SS_ERR_WORKSPACE;
+  KArgs a = {};
+  a.x = logits;
+  a.ld = ld;
+  a.op = OP_LOGPROBS;
+  a.B = B;
+  a.rows = B;
+  a.V = V;
+  a.L = 0;
+  a.k_cap = n_lp;
+  a.vec_ok = aligned16(logits) && ((ld * esize(dtype)) % 16 == 0);
+  fill_params(a, p);
+  a.out_idx = out_idx;
+  a.out_val = out_lp;
   a.flags = flags;
   return launch(a, dtype, lay, ws, (hipStream_t)stream, false);
 }

@@ -70,7 +70,8 @@ constexpr int kGS = 2048;                    // candidate groups held in registe
 constexpr uint32_t kNoEmit = 0xFFFFFFFFu;    // threshold of a unit that emits nothing
 constexpr double kFix = 1125899906842624.0;  // 2^50: fixed-point scale of probability mass
 
-enum { OP_TOPK = SS_OP_TOPK, OP_SAMPLE = SS_OP_SAMPLE, OP_VERIFY = SS_OP_VERIFY, OP_PROCESS = SS_OP_PROCESS };
+enum { OP_TOPK = SS_OP_TOPK, OP_SAMPLE = SS_OP_SAMPLE, OP_VERIFY = SS_OP_VERIFY, OP_PROCESS = SS_OP_PROCESS,
+       OP_LOGPROBS = SS_OP_LOGPROBS };
 enum { KIND_EMPTY = 0, KIND_GREEDY = 1, KIND_DIST = 2 };
 
 struct RowSummary {
@@ -135,6 +136,7 @@ struct KArgs {
   int32_t* pstat;      // per row: 0 no lists, 1 patch table in ptab, 2 more ids than the table holds
   uint32_t* ptab;      // per row 2 kH words: slot ids (-1 empty), then final keys
   int patch_wgs;       // patch-table workgroups at the front of the streaming grid
+  double* usum;        // log-probabilities: per unit, sum of exp((x - unit max) / tau) over its valid logits
 };
 
 // ---------------------------------------------------------------------------
@@ -273,6 +275,9 @@ __device__ __forceinline__ Ctx make_ctx(const KArgs& a, int row) {
     c.greedy = false;
     int k = a.top_k ? a.top_k[b] : a.k_cap;
     c.k_eff = k < 0 ? 0 : (k > a.k_cap ? a.k_cap : k);
+  } else if (a.op == OP_LOGPROBS) {  // the leading k_cap tokens of rows with the bit
+    c.greedy = false;
+    c.k_eff = (m & SS_LOGPROBS) ? a.k_cap : 0;
   } else {
     c.greedy = (m & SS_GREEDY) || ((m & SS_TEMP) && c.tau <= 0.0f);
     const int64_t kreq = ((m & SS_TOPK) && a.top_k[b] >= 1) ? (int64_t)a.top_k[b] : (int64_t)INT_MAX;
@@ -451,11 +456,22 @@ __device__ __forceinline__ bool tie_trim(const uint32_t (&gm)[NG], uint32_t t, u
   return true;
 }
 
+// Temperature of a row's log-probabilities: its own when the temperature bit
+// is on, tau > 0 and the row is not greedy, else 1.
+__device__ __forceinline__ float lp_tau(const KArgs& a, uint32_t mode, int b) {
+  if ((mode & SS_TEMP) && !(mode & SS_GREEDY) && a.temperature[b] > 0.0f) return a.temperature[b];
+  return 1.0f;
+}
+// One term of a unit's normaliser sum, exp((v - mu) / tau) in float32 from
+// the float32 reciprocal itau; the merge recomputes it bit for bit for the
+// raw copies of patched ids.
+__device__ __forceinline__ float lp_term(float v, float mu, float itau) { return expf((v - mu) * itau); }
+
 // Streams unit `gu` (wave-uniform) and writes its record and candidate groups.
 // The record is (threshold key, groups written or the count that overflowed,
 // unit maximum key, last index of the tie cut or ~0u when every group at or
 // above the threshold was written).
-template <int DT>
+template <int DT, bool LP>
 __device__ __forceinline__ void scan_unit(const KArgs& a, int gu) {
   constexpr int VW = DTT<DT>::VW, NLD = DTT<DT>::NLD, ES = DTT<DT>::ES, GPL = DTT<DT>::GPL;
   const int ln = lane();
@@ -509,6 +525,8 @@ __device__ __forceinline__ void scan_unit(const KArgs& a, int gu) {
   if (a.op == OP_TOPK) {
     const int k = a.top_k ? a.top_k[b] : a.k_cap;
     k_eff = k < 0 ? 0 : min(k, a.k_cap);
+  } else if (a.op == OP_LOGPROBS) {
+    k_eff = (mode & SS_LOGPROBS) ? a.k_cap : 0;
   } else {
     const bool greedy = (mode & SS_GREEDY) || ((mode & SS_TEMP) && a.temperature[b] <= 0.0f);
     k_eff = greedy ? 1 : (((mode & SS_TOPK) && a.top_k[b] >= 1) ? min(a.top_k[b], a.k_cap) : a.k_cap);
@@ -550,6 +568,24 @@ __device__ __forceinline__ void scan_unit(const KArgs& a, int gu) {
 #pragma unroll
       for (int j = 1; j < 16; ++j) lm = pkmax16(lm, kd[j]);
       wm16 = wave_max_u32(hmax16(lm));
+    }
+    if constexpr (LP) {  // the unit's share of the full-row normaliser
+      if (mode & SS_LOGPROBS) {
+        double sl = 0.0;
+        if (wm16 >= 0x0081u) {
+          const float mu = float_of_key(wm16 << 16), itau = 1.0f / lp_tau(a, mode, b);
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              const uint32_t k16 = (kd[j] >> (16 * h)) & 0xFFFFu;
+              if (k16 >= 0x0081u) sl += (double)lp_term(float_of_key(k16 << 16), mu, itau);
+            }
+          }
+        }
+        sl = wave_sum(sl);
+        if (ln == 0) a.usum[gu] = sl;
+      }
     }
     uint32_t t16;
     if (k_eff <= 0) {
@@ -619,6 +655,19 @@ __device__ __forceinline__ void scan_unit(const KArgs& a, int gu) {
 #pragma unroll
       for (int j = 1; j < 32; ++j) lm = max(lm, kk[j]);
       wm = wave_max_u32(lm);
+    }
+    if constexpr (LP) {  // the unit's share of the full-row normaliser
+      if (mode & SS_LOGPROBS) {
+        double sl = 0.0;
+        if (wm >= kKeyFloor) {
+          const float mu = float_of_key(wm), itau = 1.0f / lp_tau(a, mode, b);
+#pragma unroll
+          for (int j = 0; j < 32; ++j)
+            if (kk[j] >= kKeyFloor) sl += (double)lp_term(float_of_key(kk[j]), mu, itau);
+        }
+        sl = wave_sum(sl);
+        if (ln == 0) a.usum[gu] = sl;
+      }
     }
     if (k_eff <= 0) {
       t = kNoEmit;
@@ -2523,6 +2572,66 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
     }
     if (a.flags && tid == 0) a.flags[b] = flags & SS_FLAG_FALLBACK;
     return;
+  } else if constexpr (OP == OP_LOGPROBS) {
+    // the leading tokens in canonical order, then the full-row normaliser:
+    // the units' sums (taken by the streaming kernel relative to each unit's
+    // raw maximum) rescaled to the row maximum M, each patched id's raw term
+    // replaced by its final value's
+    const int n_sel = none ? 0 : nT;
+    if (n_sel > 0) {
+      uint64_t* sel = reinterpret_cast<uint64_t*>(pool);
+      const int N = next_pow2(n_sel);
+      for (int i = tid; i < N; i += kBlock) sel[i] = i < n_sel ? comp_of(pool[i].x, pool[i].y) : 0ull;
+      lds_barrier();
+      lds_sort_desc(sel, N);
+    }
+    const float tauf = lp_tau(a, c.mode, b), itau = 1.0f / tauf;
+    const double tau = (double)tauf;
+    const double M = n_sel > 0 ? (double)float_of_key(comp_key(Mcomp)) : 0.0;
+    double z = 0.0;
+    if (n_sel > 0) {
+      const int Wm = (a.V + 31) >> 5;
+      auto allowed = [&](int id) { return !c.mask || ((((id >> 5) < Wm ? c.mask[id >> 5] : 0u) >> (id & 31)) & 1u); };
+      if (pmode <= 1) {
+        for (int u = tid; u < U; u += kBlock) {
+          const uint32_t wmu = a.rec[(size_t)row * U + u].z;
+          if (wmu >= kKeyFloor) z += exp(((double)float_of_key(wmu) - M) / tau) * a.usum[(size_t)row * U + u];
+        }
+        for (int sl = tid; pmode == 1 && sl < kH; sl += kBlock) {
+          const int id = S.hk[sl];
+          if (id < 0) continue;
+          uint32_t kr = fold_nan(key_raw(load_elem_bits<DT>(c.xrow, id)));  // as the unit sum counted it
+          if (!allowed(id)) kr = 0u;
+          if (kr >= kKeyFloor) {
+            const float mu = float_of_key(a.rec[(size_t)row * U + id / kUE].z);
+            z -= exp(((double)mu - M) / tau) * (double)lp_term(float_of_key(kr), mu, itau);
+          }
+          if (S.hf[sl] >= kKeyFloor) z += exp(((double)float_of_key(S.hf[sl]) - M) / tau);
+        }
+      } else {  // lists beyond the LDS table: every element's processed value
+        for (int i = tid; i < a.V; i += kBlock) {
+          uint32_t k = fold_nan(key_raw(load_elem_bits<DT>(c.xrow, i)));
+          if (!allowed(i)) k = 0u;
+          if (is_patched<DT>(c, S, pmode, pg, i)) k = pmode == 2 ? pg.fin[gfind(pg, i)] : lin_final<DT>(a, c, i);
+          if (k >= kKeyFloor) z += exp(((double)float_of_key(k) - M) / tau);
+        }
+      }
+    }
+    z = block_sum(z, S.rd);
+    const double lz = n_sel > 0 ? log(z) : 0.0;
+    const uint64_t* sel = reinterpret_cast<const uint64_t*>(pool);
+    for (int r = tid; r < a.k_cap; r += kBlock) {
+      const size_t o = (size_t)b * a.k_cap + r;
+      if (r < n_sel) {
+        a.out_idx[o] = (int32_t)comp_idx(sel[r]);
+        a.out_val[o] = (float)(((double)float_of_key(comp_key(sel[r])) - M) / tau - lz);
+      } else {
+        a.out_idx[o] = -1;
+        a.out_val[o] = -__builtin_inff();
+      }
+    }
+    if (a.flags && tid == 0) a.flags[b] = (c.mode & SS_LOGPROBS) ? flags & (SS_FLAG_FALLBACK | SS_FLAG_EMPTY) : 0;
+    return;
   } else {
     int token = -1;
     float logprob = 0.0f;
@@ -2895,7 +3004,7 @@ __device__ __forceinline__ void patch_row(const KArgs& a, int row, PSmem& P) {
 // are remapped so that consecutive units (one row) share an XCD and its L2.
 // For the operations that apply penalties and bias, the first workgroups of
 // the grid build the rows' patch tables (dynamic LDS) beside the stream.
-template <int DT>
+template <int DT, bool LP>
 __global__ __launch_bounds__(kSBlock) void ss_stream_kernel(KArgs a) {
   int bid = blockIdx.x;
   if (bid < a.patch_wgs) {  // patch-table workgroups (a multiple of 8) come first
@@ -2907,7 +3016,7 @@ __global__ __launch_bounds__(kSBlock) void ss_stream_kernel(KArgs a) {
   const int nb = gridDim.x - a.patch_wgs;
   if (bid < (nb & ~7)) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
   const int gu = __builtin_amdgcn_readfirstlane(bid * kSWaves + wave());
-  if (gu < a.rows * a.U) scan_unit<DT>(a, gu);
+  if (gu < a.rows * a.U) scan_unit<DT, LP>(a, gu);
 }
 
 // Merge kernel: one workgroup per row (the launch boundary orders the

@@ -7,7 +7,7 @@ namespace ss {
 
 struct KArgs;
 
-template <int DT>
+template <int DT, bool LP>
 void launch_stream(const KArgs& k, dim3 grid, dim3 block, int smem, hipStream_t st);
 template <int DT, int OP>
 void launch_merge(const KArgs& k, dim3 grid, dim3 block, int smem, hipStream_t st);
@@ -25,13 +25,17 @@ SS_EXTERN_MERGE(0, 0)
 SS_EXTERN_MERGE(0, 1)
 SS_EXTERN_MERGE(0, 2)
 SS_EXTERN_MERGE(0, 3)
+SS_EXTERN_MERGE(0, 4)
 SS_EXTERN_MERGE(1, 0)
 SS_EXTERN_MERGE(1, 1)
 SS_EXTERN_MERGE(1, 2)
 SS_EXTERN_MERGE(1, 3)
+SS_EXTERN_MERGE(1, 4)
 #undef SS_EXTERN_MERGE
-extern template void launch_stream<0>(const KArgs&, dim3, dim3, int, hipStream_t);
-extern template void launch_stream<1>(const KArgs&, dim3, dim3, int, hipStream_t);
+extern template void launch_stream<0, false>(const KArgs&, dim3, dim3, int, hipStream_t);
+extern template void launch_stream<1, false>(const KArgs&, dim3, dim3, int, hipStream_t);
+extern template void launch_stream<0, true>(const KArgs&, dim3, dim3, int, hipStream_t);
+extern template void launch_stream<1, true>(const KArgs&, dim3, dim3, int, hipStream_t);
 extern template void launch_materialize<0>(const KArgs&, dim3, dim3, hipStream_t);
 extern template void launch_materialize<1>(const KArgs&, dim3, dim3, hipStream_t);
 

@@ -53,6 +53,23 @@ def test_workspace_sizes(lib):
     assert b.workspace_bytes(b.OP_TOPK, 256, 1 << 18, 0, 4096, b.F32) < 256 * (1 << 18) * 4 // 2
 
 
+def test_logprobs_arguments_are_checked_before_launch(lib):
+    from paper_2607_20475_amd import binding as b
+    fake = C.c_void_p(0x10000)  # never dereferenced: validation fails first
+    p = b._Params(B=4, V=100)
+    mode = (C.c_uint32 * 4)()
+    p.mode = C.cast(mode, C.c_void_p)
+    bad = -1  # SS_ERR_INVALID_ARG
+    assert lib.ss_logprobs(None, 0, 100, C.byref(p), 10, fake, fake, None, fake, 1 << 20, None) == bad
+    assert lib.ss_logprobs(fake, 0, 100, C.byref(p), 0, fake, fake, None, fake, 1 << 20, None) == bad
+    assert lib.ss_logprobs(fake, 0, 100, C.byref(p), 4097, fake, fake, None, fake, 1 << 20, None) == bad
+    assert lib.ss_logprobs(fake, 0, 99, C.byref(p), 10, fake, fake, None, fake, 1 << 20, None) == bad
+    assert lib.ss_logprobs(fake, 0, 100, C.byref(p), 10, None, fake, None, fake, 1 << 20, None) == bad
+    n = b.workspace_bytes(b.OP_LOGPROBS, 4, 100, 0, 10, b.F32)
+    assert n > b.workspace_bytes(b.OP_SAMPLE, 4, 100, 0, 10, b.F32)
+    assert lib.ss_logprobs(fake, 0, 100, C.byref(p), 10, fake, fake, None, fake, n - 256, None) == -3  # SS_ERR_WORKSPACE
+
+
 def test_invalid_arguments_are_rejected_before_launch(lib):
     from paper_2607_20475_amd import binding as b
     fake = C.c_void_p(0x10000)  # never dereferenced: validation fails first

@@ -502,6 +502,69 @@ def test_tied_rows_headline_params(ssb):
 
 
 # --------------------------------------------------------------------------
+# Top-k log-probabilities
+# --------------------------------------------------------------------------
+def check_logprobs(ssb, inp, n_lp, label):
+    x = ssb.logits_tensor(inp)
+    prm = ssb.Params.from_arrays(inp)
+    fl = torch.zeros(inp["B"], dtype=torch.int32, device="cuda")
+    say(f"[{label}] logprobs B={inp['B']} V={inp['V']} n_lp={n_lp} dtype={inp['dtype']}")
+    idx, lp = ssb.logprobs(x, prm, n_lp, flags=fl)
+    torch.cuda.synchronize()
+    ri, rl = oracle.logprobs(inp, n_lp)
+    gi, gl = _np(idx), _np(lp)
+    bad = np.nonzero(~(gi == ri).all(axis=1))[0]
+    assert bad.size == 0, (label, bad[:5], gi[bad[:1]], ri[bad[:1]])
+    fin = ri >= 0
+    assert np.isneginf(gl[~fin]).all(), label
+    # float32 exponentials summed in double: the normaliser's relative error is
+    # a few 1e-7, so each log-probability is within 1e-5 (absolute, or
+    # relative for magnitudes above 1)
+    err = np.abs(gl[fin].astype(np.float64) - rl[fin]) / np.maximum(1.0, np.abs(rl[fin]))
+    assert err.max(initial=0.0) <= 1e-5, (label, float(err.max()))
+    fb = int(((_np(fl) & FALLBACK) > 0).sum())
+    say(f"[{label}] ok, max error {err.max(initial=0.0):.2e}, fallback rows={fb}")
+
+
+@pytest.mark.parametrize("name", ["cfg1", "cfg3", "cfg0"])
+def test_logprobs_configs(ssb, name):
+    """The workloads' rows (penalties, bias, grammar, temperatures, greedy
+    rows) with the log-probability bit on every other row."""
+    inp = W.make_config(name)
+    inp["mode"] = inp["mode"] | np.where(np.arange(inp["B"]) % 2 == 1, W.MODE_LOGPROBS, 0).astype(np.uint32)
+    inp["mode"][0] |= np.uint32(W.MODE_LOGPROBS)  # a greedy row too (cfg1/cfg3)
+    for n in (1, 20, 700):
+        check_logprobs(ssb, inp, n, f"logprobs-{name}-{n}")
+
+
+def test_logprobs_edge_cases(ssb):
+    """Tied rows, a fully masked row, NaN and -inf, long histories (the
+    merge's global patch table), and a vocabulary that is not a multiple of a
+    unit."""
+    rng = np.random.default_rng(91)
+    B, V = 6, 40000
+    x = rng.normal(0, 3, (B, V)).astype(np.float32)
+    x[0] = 1.5
+    x[2, ::7] = np.nan
+    x[3, :100] = -np.inf
+    mask = np.full((B, (V + 31) // 32), 0xFFFFFFFF, np.uint32)
+    mask[1] = 0
+    hist = [rng.integers(0, V, 20).astype(np.int32) for _ in range(B)]
+    hist[4] = rng.integers(0, V, 5000).astype(np.int32)  # more distinct ids than the LDS table
+    pen = W.MODE_LOGPROBS | W.MODE_REP | W.MODE_FREQ | W.MODE_TEMP | W.MODE_GRAMMAR
+    inp = W.custom_rows(x, W.F32, k_max=64, mode=np.full(B, pen, np.uint32),
+                        temperature=rng.uniform(0.5, 2.0, B).astype(np.float32), rep=np.full(B, 1.2, np.float32),
+                        freq=np.full(B, 0.3, np.float32), bitmask=mask,
+                        hist_offsets=np.concatenate([[0], np.cumsum([len(h) for h in hist])]).astype(np.int32),
+                        hist_ids=np.concatenate(hist))
+    check_logprobs(ssb, inp, 50, "logprobs-edges-f32")
+    inp_b = dict(inp)
+    inp_b["x"] = W.bf16_bits_from_f32(x)
+    inp_b["dtype"] = W.BF16
+    check_logprobs(ssb, inp_b, 50, "logprobs-edges-bf16")
+
+
+# --------------------------------------------------------------------------
 # Materialised pipeline
 # --------------------------------------------------------------------------
 @pytest.mark.parametrize("name", ["cfg0", "cfg1", "long_history", "dense_patch", "nan_empty", "grammar_few"])
