@@ -16,6 +16,9 @@ oracle and the HIP binding accept:
   seed           uint64 ``[B]``;  position  int64 ``[B]``
   k_max          candidate bound (int)
   draft_probs    float32 ``[B, L, V]`` and draft_tokens int32 ``[B, L]`` (verification)
+  draft_idx, draft_q  int32 / float32 ``[B, L, kq]``: sparse draft distributions
+                 (the (id, probability) list a draft step emits over its kept
+                 set, padded with (-1, 0)); they replace ``draft_probs``
 
 Logits follow the paper's evaluation regime (concentrated next-token
 distributions, Section 3.3) with the shapes of the five evaluated
@@ -217,9 +220,51 @@ def config4(B: int = 64, L: int = 4) -> dict:
                 draft_probs=q, draft_tokens=d, **p)
 
 
+def sparse_drafts(noisy: np.ndarray, kq: int, top_p: float, rng_d) -> tuple:
+    """Sparse draft lists from draft logits ``noisy`` [B, L, V] (float64): per
+    position the kq leading ids (value descending, lower index first), cut to
+    the shortest prefix whose softmax mass reaches top_p, renormalised, as
+    float32 (id, q) pairs padded with (-1, 0); and one draft token drawn from
+    each list.  Input preparation standing in for a draft model's sampler."""
+    B, L, V = noisy.shape
+    idx = np.full((B, L, kq), -1, np.int32)
+    qv = np.zeros((B, L, kq), np.float32)
+    d = np.empty((B, L), np.int32)
+    for b in range(B):
+        for l in range(L):
+            row = noisy[b, l]
+            top = np.argpartition(-row, kq - 1)[:kq]
+            top = top[np.lexsort((top, -row[top]))]
+            w = np.exp(row[top] - row[top[0]])
+            c = np.cumsum(w)
+            n = min(int(np.searchsorted(c, top_p * c[-1], side="left")) + 1, kq)
+            q = w[:n] / c[n - 1]
+            idx[b, l, :n] = top[:n]
+            qv[b, l, :n] = q.astype(np.float32)
+            cq = np.cumsum(q)
+            d[b, l] = int(top[min(int(np.searchsorted(cq, rng_d.random() * cq[-1], side="right")), n - 1)])
+    return idx, qv, d
+
+
+def config4_sparse(B: int = 64, L: int = 4, kq: int = 64) -> dict:
+    """Verification against sparse draft lists: the target and parameters of
+    config4, each draft position carrying at most kq (id, q) pairs (the draft
+    distribution of config4 cut to its kq leading ids and top-p 0.95)."""
+    rng = np.random.default_rng(1000 * 4 + 7)
+    V = 1 << 17
+    xf = _head_logits(rng, B * (L + 1), V, heads=16)
+    x = bf16_bits_from_f32(xf).reshape(B, L + 1, V)
+    p = _hetero_params(rng, B, V)
+    tgt = f32_from_bf16_bits(x[:, :L, :]).astype(np.float64)
+    noisy = tgt + rng.normal(0.0, 1.0, size=tgt.shape)
+    idx, qv, d = sparse_drafts(noisy, kq, 0.95, np.random.default_rng(1000 * 4 + 9))
+    return dict(name="cfg4_sparse", x=x, dtype=BF16, B=B, V=V, L=L, k_max=1024,
+                draft_idx=idx, draft_q=qv, draft_tokens=d, **p)
+
+
 def make_config(name: str, **kw) -> dict:
     return {"cfg0": config0, "cfg1": config1, "cfg2": config2,
-            "cfg3": config3, "cfg4": config4}[name](**kw)
+            "cfg3": config3, "cfg4": config4, "cfg4_sparse": config4_sparse}[name](**kw)
 
 
 def custom_rows(x, dtype: str = F32, k_max: int = 64, L: int = 0, **params) -> dict:

@@ -205,7 +205,8 @@ def logprobs(inp, n_lp, nthreads=0):
 
 
 def verify(inp, nthreads=0):
-    """Multistep verification.
+    """Multistep verification, against dense ``draft_probs`` [B, L, V] or, when
+    the input holds ``draft_idx`` / ``draft_q`` [B, L, kq], sparse draft lists.
 
     Returns dict(tokens [B,L+1], n_acc [B], flags, margin, adm_tokens [B,A,L+1],
     adm_nacc [B,A], n_adm): the oracle's own outcome and every admissible
@@ -214,7 +215,13 @@ def verify(inp, nthreads=0):
     B, V, L = int(inp["B"]), int(inp["V"]), int(inp["L"])
     A = adm_max()
     x = _x(inp)
-    q = np.ascontiguousarray(inp["draft_probs"], dtype=np.float32)
+    sparse = inp.get("draft_idx") is not None
+    if sparse:
+        qi = np.ascontiguousarray(inp["draft_idx"], dtype=np.int32)
+        qv = np.ascontiguousarray(inp["draft_q"], dtype=np.float32)
+        assert qi.shape == qv.shape and qi.shape[:2] == (B, L)
+    else:
+        q = np.ascontiguousarray(inp["draft_probs"], dtype=np.float32)
     d = np.ascontiguousarray(inp["draft_tokens"], dtype=np.int32)
     bd = _Bundle(inp)
     tok = np.empty((B, L + 1), np.int32)
@@ -224,9 +231,14 @@ def verify(inp, nthreads=0):
     aseq = np.empty((B, A, L + 1), np.int32)
     anacc = np.empty((B, A), np.int32)
     nadm = np.empty(B, np.int32)
-    lib().ssref_verify(_ptr(x), C.c_int(_dtype_code(inp)), C.c_int64(V), _ptr(q), C.c_int64(V),
-                       _ptr(d), C.c_int(L), C.byref(bd.p), _ptr(tok), _ptr(na), _ptr(fl), _ptr(mg),
-                       _ptr(aseq), _ptr(anacc), _ptr(nadm), C.c_int(nthreads))
+    outs = (_ptr(tok), _ptr(na), _ptr(fl), _ptr(mg), _ptr(aseq), _ptr(anacc), _ptr(nadm), C.c_int(nthreads))
+    if sparse:
+        rc = lib().ssref_verify_sparse(_ptr(x), C.c_int(_dtype_code(inp)), C.c_int64(V), _ptr(qi), _ptr(qv),
+                                       C.c_int(qi.shape[2]), _ptr(d), C.c_int(L), C.byref(bd.p), *outs)
+        assert rc == 0
+    else:
+        lib().ssref_verify(_ptr(x), C.c_int(_dtype_code(inp)), C.c_int64(V), _ptr(q), C.c_int64(V),
+                           _ptr(d), C.c_int(L), C.byref(bd.p), *outs)
     return dict(tokens=tok, n_acc=na, flags=fl, margin=mg, adm_tokens=aseq, adm_nacc=anacc, n_adm=nadm)
 
 

@@ -22,7 +22,10 @@
  *     uniform from Philox4x32-10 keyed by (seed, request, position);
  *   - speculative verification (Section 3.1 "Speculative Verification",
  *     Appendix C.4): accept when u*q(d) <= p(d), else resample from
- *     normalize(max(0, p - q)); a bonus token after full acceptance;
+ *     normalize(max(0, p - q)); a bonus token after full acceptance; the
+ *     draft distribution q either dense over the vocabulary or sparse, as the
+ *     (id, probability) list a singular-mode draft step emits over its
+ *     candidate set (Section 3.2), every unlisted id having q = 0;
  *   - top-k log-probabilities (indicator bit 0x400 of the bit-level encoding
  *     table, Section 3.5): the leading tokens of the canonical order with
  *     their log-probabilities under the untruncated distribution of the row.
@@ -649,8 +652,11 @@ typedef struct {
   const void *x;
   int dtype;
   int64_t ld_row;
-  const float *q;
+  const float *q;     /* dense q [B, L, ld_q], or NULL when sparse */
   int64_t ld_q;
+  const int32_t *qi;  /* sparse q: ids [B, L, kq] */
+  const float *qv;    /*           probabilities [B, L, kq] */
+  int kq;
   const int32_t *dr;  /* this request's drafts [L] */
   int L, b, V;
   const ssref_params *p;
@@ -663,6 +669,18 @@ typedef struct {
   int fl;
   double mg;
 } vctx_t;
+
+/* Draft probability q_l(id) at draft position l (1-based).  Sparse lists: the
+ * sum, in double and in list order, of the entries naming id (ids outside
+ * [0, V) are padding); an unlisted id has q = 0. */
+static double qget(const vctx_t *c, int l, int id) {
+  if (c->kq <= 0) return (double)c->q[(int64_t)c->b * c->L * c->ld_q + (int64_t)(l - 1) * c->ld_q + id];
+  const int64_t o = ((int64_t)c->b * c->L + (l - 1)) * c->kq;
+  double s = 0.0;
+  for (int i = 0; i < c->kq; ++i)
+    if (c->qi[o + i] == id) s += (double)c->qv[o + i];
+  return s;
+}
 
 static vrow_t *vrow_get(vctx_t *c, int l) {
   vrow_t *r = &c->rows[l - 1];
@@ -733,8 +751,7 @@ static void vexplore(vctx_t *c, int l) {
     return;
   }
   const int dl = c->dr[l - 1];
-  const float *qrow = c->q + (int64_t)b * L * c->ld_q + (int64_t)(l - 1) * c->ld_q;
-  const double qd = (double)qrow[dl];
+  const double qd = qget(c, l, dl);
   const double a = ssref_uniform(c->p->seed[b], (uint32_t)b, pos, 1);
   const double lhs = a * qd;
   int rd = -1;  /* rank of the draft token in the canonical order (top-k range) */
@@ -765,7 +782,7 @@ static void vexplore(vctx_t *c, int l) {
         double R = 0.0;
         for (int k = 0; k < ns; ++k) {
           double P = r->w[k] / Z;
-          double v = P - (double)qrow[r->order[k]];
+          double v = P - qget(c, l, r->order[k]);
           c->res[k] = v > 0.0 ? v : 0.0;
           R += c->res[k];
         }
@@ -781,10 +798,10 @@ static void vexplore(vctx_t *c, int l) {
   }
 }
 
-int ssref_verify(const void *x, int dtype, int64_t ld_row, const float *draft_probs,
-                 int64_t ld_q, const int32_t *draft_tokens, int L, const ssref_params *p,
-                 int32_t *out_tokens, int32_t *n_acc, int32_t *flags, double *margin,
-                 int32_t *adm_seq, int32_t *adm_nacc, int32_t *n_adm, int nthreads) {
+static int verify_all(const void *x, int dtype, int64_t ld_row, const float *draft_probs, int64_t ld_q,
+                      const int32_t *q_idx, const float *q_val, int kq, const int32_t *draft_tokens, int L,
+                      const ssref_params *p, int32_t *out_tokens, int32_t *n_acc, int32_t *flags,
+                      double *margin, int32_t *adm_seq, int32_t *adm_nacc, int32_t *n_adm, int nthreads) {
   int B = p->B, V = p->V;
 #ifdef _OPENMP
   if (nthreads > 0) omp_set_num_threads(nthreads);
@@ -795,6 +812,7 @@ int ssref_verify(const void *x, int dtype, int64_t ld_row, const float *draft_pr
     vctx_t c;
     memset(&c, 0, sizeof(c));
     c.x = x; c.dtype = dtype; c.ld_row = ld_row; c.q = draft_probs; c.ld_q = ld_q;
+    c.qi = q_idx; c.qv = q_val; c.kq = kq;
     c.dr = draft_tokens + (int64_t)b * L; c.L = L; c.b = b; c.V = V; c.p = p;
     c.mode = effective_mode(p, b);
     c.mg = INFINITY;
@@ -824,6 +842,26 @@ int ssref_verify(const void *x, int dtype, int64_t ld_row, const float *draft_pr
     free(c.rows); free(c.res); free(c.seq); free(c.nacc);
   }
   return 0;
+}
+
+/* Verification against a dense draft distribution q [B, L, ld_q]. */
+int ssref_verify(const void *x, int dtype, int64_t ld_row, const float *draft_probs,
+                 int64_t ld_q, const int32_t *draft_tokens, int L, const ssref_params *p,
+                 int32_t *out_tokens, int32_t *n_acc, int32_t *flags, double *margin,
+                 int32_t *adm_seq, int32_t *adm_nacc, int32_t *n_adm, int nthreads) {
+  return verify_all(x, dtype, ld_row, draft_probs, ld_q, NULL, NULL, 0, draft_tokens, L, p, out_tokens,
+                    n_acc, flags, margin, adm_seq, adm_nacc, n_adm, nthreads);
+}
+
+/* Verification against sparse draft distributions: kq (id, probability)
+ * entries per draft position, [B, L, kq] each (qget gives their meaning). */
+int ssref_verify_sparse(const void *x, int dtype, int64_t ld_row, const int32_t *q_idx, const float *q_val,
+                        int kq, const int32_t *draft_tokens, int L, const ssref_params *p,
+                        int32_t *out_tokens, int32_t *n_acc, int32_t *flags, double *margin,
+                        int32_t *adm_seq, int32_t *adm_nacc, int32_t *n_adm, int nthreads) {
+  if (kq < 1) return -1;
+  return verify_all(x, dtype, ld_row, NULL, 0, q_idx, q_val, kq, draft_tokens, L, p, out_tokens, n_acc,
+                    flags, margin, adm_seq, adm_nacc, n_adm, nthreads);
 }
 
 /* One row's truncated distribution, for pin tests: fills order[0..n_valid),

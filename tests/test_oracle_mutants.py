@@ -44,6 +44,10 @@ MUTANTS = [
      "      if ((em & R_TEMP) && !(em & R_GREEDY) && p->temperature[b] > 0.0f) tau = (double)p->temperature[b];",
      "      if ((em & R_TEMP) && !(em & R_GREEDY) && p->temperature[b] > 0.0f) tau = 1.0;",
      "test_logprobs_temperature_scales_differences"),
+    ("sparse_q_last_entry_wins", "    if (c->qi[o + i] == id) s += (double)c->qv[o + i];",
+     "    if (c->qi[o + i] == id) s = (double)c->qv[o + i];", "test_verify_sparse_first_token"),
+    ("sparse_q_first_position_list", "  const int64_t o = ((int64_t)c->b * c->L + (l - 1)) * c->kq;",
+     "  const int64_t o = ((int64_t)c->b * c->L) * c->kq;", "test_verify_sparse_lists_are_per_position"),
     ("uniform_counter_words_swapped", "  uint32_t ctr[4] = {request, (uint32_t)((uint64_t)position & 0xFFFFFFFFu),",
      "  uint32_t ctr[4] = {(uint32_t)((uint64_t)position & 0xFFFFFFFFu), request,",
      "test_uniform_counter_words"),

@@ -404,6 +404,124 @@ def test_verify_special_cases():
     assert np.all(o["n_acc"] == 0) and np.all(o["tokens"][:, 0] == am)
 
 
+def _sparse(inp, idx, qv):
+    """Replaces the dense draft distribution of ``inp`` by sparse lists."""
+    inp = dict(inp)
+    inp.pop("draft_probs")
+    inp["draft_idx"] = np.ascontiguousarray(idx, np.int32)
+    inp["draft_q"] = np.ascontiguousarray(qv, np.float32)
+    return inp
+
+
+def test_verify_sparse_first_token_follows_target_chi_square():
+    # q supported on 4 of 8 ids, listed with a duplicated id (two entries whose
+    # sum is its probability), padding and an out-of-range id: the first output
+    # token still follows the target exactly (the guarantee of speculative
+    # sampling holds for any q the draft was drawn from), and one draft is
+    # accepted with probability sum_x min(p(x), q(x)).
+    V, B, L = 8, 40000, 1
+    rng = np.random.default_rng(27)
+    t = rng.normal(0, 1, V).astype(np.float32)
+    support = np.array([5, 1, 6, 2])
+    qs = np.array([0.4375, 0.25, 0.1875, 0.125])  # exact in float32
+    qd = np.zeros(V)
+    qd[support] = qs
+    d = rng.choice(V, size=(B, L), p=qd)
+    idx = np.array([5, 1, -1, 6, 2, 1, V, 9999], np.int32)
+    val = np.array([0.4375, 0.125, 0.5, 0.1875, 0.125, 0.125, 0.3, 0.2], np.float32)
+    x = np.tile(t, (B, L + 1, 1))
+    inp = _verify_inputs(x, np.zeros((B, L, V)), d, np.full(B, W.MODE_TEMP), L, temperature=np.full(B, 0.8),
+                         position=np.arange(B) * 3)
+    out = oracle.verify(_sparse(inp, np.tile(idx, (B, L, 1)), np.tile(val, (B, L, 1))))
+    first = out["tokens"][:, 0]
+    assert np.all(first >= 0)
+    p = special.softmax(t.astype(np.float64) / np.float32(0.8))
+    ok, pv = _chi2_ok(np.bincount(first, minlength=V).astype(float), p)
+    assert ok, pv
+    acc = float(np.mean(out["n_acc"] == 1))
+    want = float(np.minimum(p, qd).sum())
+    assert abs(acc - want) < 4 * math.sqrt(want * (1 - want) / B)
+
+
+def test_verify_sparse_lists_are_per_position():
+    # two draft positions with different targets and different sparse lists:
+    # conditioned on the first draft being accepted, the second output token
+    # follows the second target, which needs the second position's own list
+    V, B, L = 6, 60000, 2
+    rng = np.random.default_rng(35)
+    t = rng.normal(0, 0.8, (L + 1, V)).astype(np.float32)
+    lists = [(np.array([0, 3, 4]), np.array([0.5, 0.375, 0.125])),
+             (np.array([2, 5, 1]), np.array([0.625, 0.25, 0.125]))]
+    idx = np.full((B, L, 3), -1, np.int32)
+    val = np.zeros((B, L, 3), np.float32)
+    d = np.empty((B, L), np.int64)
+    for l, (ii, qq) in enumerate(lists):
+        idx[:, l] = ii
+        val[:, l] = qq
+        d[:, l] = rng.choice(ii, size=B, p=qq)
+    x = np.tile(t, (B, 1, 1))
+    inp = _verify_inputs(x, np.zeros((B, L, V)), d, np.full(B, W.MODE_TEMP), L, temperature=np.full(B, 1.0),
+                         position=np.arange(B) * 5)
+    out = oracle.verify(_sparse(inp, idx, val))
+    tok = out["tokens"]
+    sel = out["n_acc"] >= 1
+    assert sel.sum() > 5000
+    p2 = special.softmax(t[1].astype(np.float64))
+    ok, pv = _chi2_ok(np.bincount(tok[sel, 1], minlength=V).astype(float), p2)
+    assert ok, pv
+
+
+def test_verify_sparse_matches_dense_scatter():
+    # lists without repeated ids give the outcome (tokens, accepted counts and
+    # admissible sets) of the dense q they scatter to
+    V, L, B = 64, 3, 48
+    rng = np.random.default_rng(12)
+    t = rng.normal(0, 1.5, (B, L + 1, V)).astype(np.float32)
+    kq = 12
+    idx = np.full((B, L, kq), -1, np.int32)
+    val = np.zeros((B, L, kq), np.float32)
+    dense = np.zeros((B, L, V), np.float32)
+    d = np.empty((B, L), np.int64)
+    for b in range(B):
+        for l in range(L):
+            n = int(rng.integers(1, kq + 1))
+            ii = rng.choice(V, size=n, replace=False)
+            qq = rng.dirichlet(np.ones(n)).astype(np.float32)
+            idx[b, l, :n], val[b, l, :n] = ii, qq
+            dense[b, l, ii] = qq
+            d[b, l] = ii[0] if b % 3 else int(rng.integers(0, V))  # some drafts outside the list
+    mode = np.where(np.arange(B) % 4 == 0, W.MODE_GREEDY, W.MODE_TEMP | W.MODE_TOPP)
+    inp = _verify_inputs(t, dense, d, mode, L, temperature=np.full(B, 0.9), top_p=np.full(B, 0.9),
+                         position=np.arange(B) * 11)
+    a = oracle.verify(inp)
+    s_ = oracle.verify(_sparse(inp, idx, val))
+    for k in ("tokens", "n_acc", "adm_tokens", "adm_nacc", "n_adm", "flags"):
+        assert np.array_equal(a[k], s_[k]), k
+
+
+def test_verify_sparse_unlisted_draft_is_accepted():
+    # an unlisted draft id has q = 0: accepted whenever the target gives it
+    # positive probability, rejected (and resampled from p) when it does not
+    V, L, B = 16, 2, 256
+    rng = np.random.default_rng(8)
+    t = rng.normal(0, 1, V).astype(np.float32)
+    x = np.tile(t, (B, L + 1, 1))
+    order = np.argsort(-t, kind="stable")
+    idx = np.tile(np.array([order[0], -1], np.int32), (B, L, 1))
+    val = np.tile(np.array([1.0, 0.0], np.float32), (B, L, 1))
+    d = np.tile(order[1:1 + L], (B, 1))
+    inp = _verify_inputs(x, np.zeros((B, L, V)), d, np.full(B, W.MODE_TEMP), L, position=np.arange(B))
+    o = oracle.verify(_sparse(inp, idx, val))
+    assert np.all(o["n_acc"] == L) and np.all(o["tokens"][:, :L] == d)
+    # top-k 2 excludes order[2]: P(d) = 0, rejected; resampling max(0, P - q)
+    # leaves only order[1] (order[0] has q = 1 >= P)
+    d2 = np.tile(order[2], (B, L))
+    inp = _verify_inputs(x, np.zeros((B, L, V)), d2, np.full(B, W.MODE_TEMP | W.MODE_TOPK), L,
+                         top_k=np.full(B, 2), position=np.arange(B))
+    o = oracle.verify(_sparse(inp, idx, val))
+    assert np.all(o["n_acc"] == 0) and np.all(o["tokens"][:, 0] == order[1])
+
+
 def test_process_logits_distribution_sums_to_one():
     inp = W.config0()
     out = oracle.process_logits(inp)
