@@ -56,7 +56,7 @@ MALL_BYTES = 256 << 20
 CONFIGS = ("cfg0", "cfg1", "cfg2", "cfg3", "cfg4")
 # a stress line beside the five workloads: the headline batch with every
 # logit of a row equal (the paper's tied correctness inputs at full size)
-EXTRA = ("cfg1_tied", "cfg1_logprobs")
+EXTRA = ("cfg1_tied", "cfg1_logprobs", "cfg4_sparse")
 LOGPROBS_N = 20  # log-probabilities per request on the log-probability line
 WORKLOAD = {
     "cfg0": "tiny singular batch: fused sample B=4 V=32768 fp32, per-row temperature {0,0.7,1.0,1.3}, "
@@ -71,6 +71,8 @@ WORKLOAD = {
                  "logit 0.5",
     "cfg1_logprobs": "top-20 log-probabilities (ss_logprobs) of the heterogeneous singular batch (B=64 V=131072 "
                      "bf16, penalties, bias), every request with bit 0x400",
+    "cfg4_sparse": "multistep verification against sparse draft lists (ss_verify_sparse): B=64 L=4 V=131072 "
+                   "bf16 target, at most 64 (id, q) pairs per draft position",
 }
 
 
@@ -110,6 +112,10 @@ def algorithmic_bytes(name, inp):
     if name == "cfg4":
         L = int(inp["L"])
         return b + _nbytes(inp["draft_tokens"]) + B * L * (inp["k_max"] + 1) * 4 + B * (L + 2) * 4
+    if name == "cfg4_sparse":  # the sparse lists are read whole
+        L = int(inp["L"])
+        return (b + _nbytes(inp["draft_tokens"]) + _nbytes(inp["draft_idx"]) + _nbytes(inp["draft_q"])
+                + B * (L + 2) * 4)
     return b + 12 * B  # token, log-probability, flags
 
 
@@ -273,6 +279,21 @@ class Runner:
 
             def step(i):
                 ssb.logprobs(self.xs[i % self.R], prm, LOGPROBS_N, out_idx=oi, out_lp=ol, flags=fl, ws=ws)
+        elif name == "cfg4_sparse":
+            L = inp["L"]
+            qi = t.from_numpy(np.ascontiguousarray(inp["draft_idx"], np.int32)).to(dev)
+            qv = t.from_numpy(np.ascontiguousarray(inp["draft_q"], np.float32)).to(dev)
+            d = t.from_numpy(np.ascontiguousarray(inp["draft_tokens"], np.int32)).to(dev)
+            prm = ssb.Params.from_arrays(inp, dev)
+            ws = ssb.workspace(ssb.OP_VERIFY, inp["B"], inp["V"], L, inp["k_max"], ssb.BF16, dev)
+            out = t.empty(inp["B"], L + 1, dtype=t.int32, device=dev)
+            na = t.empty(inp["B"], dtype=t.int32, device=dev)
+            fl = t.empty(inp["B"], dtype=t.int32, device=dev)
+            self.rows_per_step = inp["B"] * (L + 1)
+
+            def step(i):
+                ssb.verify_sparse(self.xs[i % self.R], qi, qv, d, prm, inp["k_max"], out_tokens=out, out_nacc=na,
+                                  flags=fl, ws=ws)
         elif name == "cfg4":
             L = inp["L"]
             q = t.from_numpy(np.ascontiguousarray(inp["draft_probs"], np.float32)).to(dev)
@@ -408,7 +429,7 @@ def config_entry(name, run, us):
     fb = int(((run.flags.cpu().numpy() & 2) > 0).sum())
     e = dict(workload=WORKLOAD[name], us_per_batch=us, rows_per_s=run.rows_per_step / (us * 1e-6),
              alg_bytes=alg, GBps=gbps, frac=gbps / HBM_PEAK_GBS, rotated_buffers=run.R, fallback_rows=fb)
-    if name == "cfg4":
+    if name in ("cfg4", "cfg4_sparse"):
         e["requests_per_s"] = run.B / (us * 1e-6)
     prof = load_profile(name)
     if prof:
@@ -504,7 +525,7 @@ def main():
     }
     if head in ("cfg1", "cfg2") and not args.read_probe:  # counter runs keep the probe the only plain read
         res["read_ceiling"] = read_ceiling(torch, h["alg_bytes"])
-    if not args.no_cpu and head != "cfg2" and head != "cfg4":
+    if not args.no_cpu and head not in ("cfg2", "cfg4", "cfg4_sparse"):
         nthreads = os.cpu_count() or 1
         omp = os.environ.get("OMP_NUM_THREADS")
         if omp and omp.isdigit():

@@ -8,6 +8,9 @@
  *   ss_verify          multistep speculative verification (Section 3.1,
  *                      Appendix C.4): accept when u*q(d) <= p(d), else resample
  *                      from normalize(max(0, p - q)); bonus token on full acceptance
+ *   ss_verify_sparse   the same against sparse draft distributions: the
+ *                      (id, probability) lists a singular-mode draft step
+ *                      emits over its candidate set (Section 3.2)
  *   ss_topk            exact top-k (value, index) per row (Section 3.4)
  *   ss_process_logits  materialised processed logits and final probabilities
  *   ss_logprobs        top-k log-probabilities under the full-row distribution
@@ -190,6 +193,23 @@ ss_status ss_verify(const void *target_logits, int dtype, int64_t ld_row, const 
                     int64_t ld_q, const int32_t *draft_tokens, int L, const ss_params *p, int k_max,
                     int32_t *out_tokens, int32_t *out_num_accepted, int32_t *flags, void *ws,
                     size_t ws_bytes, void *stream);
+
+/*
+ * Multistep speculative verification against sparse draft distributions
+ * (Section 3.1 with the draft probabilities a singular-mode draft step emits
+ * over its candidate set, Section 3.2): position l of request b lists kq
+ * (id, probability) entries, e.g. the out_idx / out_prob rows of ss_sample.
+ * q_l(j) is the sum of the entries naming j; unlisted ids have q = 0, and ids
+ * outside [0, V) (the padding -1 among them) are ignored.  Everything else,
+ * results included, is as for ss_verify.
+ *   draft_idx   int32[B, L, kq], draft_q float[B, L, kq] (used as given).
+ *   kq          1..SS_MAX_K entries per draft position.
+ *   ws          ss_workspace_bytes(SS_OP_VERIFY, B, V, L, k_max, dtype) bytes.
+ */
+ss_status ss_verify_sparse(const void *target_logits, int dtype, int64_t ld_row, const int32_t *draft_idx,
+                           const float *draft_q, int kq, const int32_t *draft_tokens, int L,
+                           const ss_params *p, int k_max, int32_t *out_tokens, int32_t *out_num_accepted,
+                           int32_t *flags, void *ws, size_t ws_bytes, void *stream);
 
 /*
  * Materialised pipeline (unfused reference path).

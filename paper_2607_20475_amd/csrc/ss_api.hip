@@ -304,14 +304,16 @@ ss_status ss_sample(const void* logits, int dtype, int64_t ld, const ss_params* 
   return launch(a, dtype, lay, ws, (hipStream_t)stream, false);
 }
 
-ss_status ss_verify(const void* target_logits, int dtype, int64_t ld_row, const float* draft_probs, int64_t ld_q,
-                    const int32_t* draft_tokens, int L, const ss_params* p, int k_max, int32_t* out_tokens,
-                    int32_t* out_num_accepted, int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
-  if (!target_logits || !p || !draft_probs || !draft_tokens || !out_tokens || !out_num_accepted || !ws)
-    return SS_ERR_INVALID_ARG;
+static ss_status verify_any(const void* target_logits, int dtype, int64_t ld_row, const float* draft_probs,
+                            int64_t ld_q, const int32_t* q_idx, const float* q_val, int kq,
+                            const int32_t* draft_tokens, int L, const ss_params* p, int k_max, int32_t* out_tokens,
+                            int32_t* out_num_accepted, int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+  if (!target_logits || !p || !draft_tokens || !out_tokens || !out_num_accepted || !ws) return SS_ERR_INVALID_ARG;
   if (dtype != SS_F32 && dtype != SS_BF16) return SS_ERR_INVALID_ARG;
   const int B = p->B, V = p->V;
-  if (ld_row < V || ld_q < V || !params_ok(p, B, V)) return SS_ERR_INVALID_ARG;
+  if (ld_row < V || !params_ok(p, B, V)) return SS_ERR_INVALID_ARG;
+  if (kq == 0 && (!draft_probs || ld_q < V)) return SS_ERR_INVALID_ARG;
+  if (kq != 0 && (!q_idx || !q_val || kq < 1 || kq > SS_MAX_K)) return SS_ERR_INVALID_ARG;
   if (!p->seed || !p->position) return SS_ERR_INVALID_ARG;
   Layout lay;
   if (!make_layout(OP_VERIFY, B, V, L, k_max, dtype, &lay)) return SS_ERR_INVALID_ARG;
@@ -328,13 +330,32 @@ ss_status ss_verify(const void* target_logits, int dtype, int64_t ld_row, const 
   a.k_out = 0;
   a.vec_ok = aligned16(target_logits) && ((ld_row * esize(dtype)) % 16 == 0);
   fill_params(a, p);
-  a.draft_probs = draft_probs;
-  a.ld_q = ld_q;
+  a.draft_probs = kq == 0 ? draft_probs : nullptr;
+  a.ld_q = kq == 0 ? ld_q : 0;
+  a.dq_idx = q_idx;
+  a.dq_val = q_val;
+  a.kq = kq;
   a.draft_tokens = draft_tokens;
   a.out_tokens = out_tokens;
   a.out_nacc = out_num_accepted;
   a.flags = flags;
   return launch(a, dtype, lay, ws, (hipStream_t)stream, false);
+}
+
+ss_status ss_verify(const void* target_logits, int dtype, int64_t ld_row, const float* draft_probs, int64_t ld_q,
+                    const int32_t* draft_tokens, int L, const ss_params* p, int k_max, int32_t* out_tokens,
+                    int32_t* out_num_accepted, int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+  return verify_any(target_logits, dtype, ld_row, draft_probs, ld_q, nullptr, nullptr, 0, draft_tokens, L, p,
+                    k_max, out_tokens, out_num_accepted, flags, ws, ws_bytes, stream);
+}
+
+ss_status ss_verify_sparse(const void* target_logits, int dtype, int64_t ld_row, const int32_t* draft_idx,
+                           const float* draft_q, int kq, const int32_t* draft_tokens, int L, const ss_params* p,
+                           int k_max, int32_t* out_tokens, int32_t* out_num_accepted, int32_t* flags, void* ws,
+                           size_t ws_bytes, void* stream) {
+  if (kq < 1 || kq > SS_MAX_K || !draft_idx || !draft_q) return SS_ERR_INVALID_ARG;
+  return verify_any(target_logits, dtype, ld_row, nullptr, 0, draft_idx, draft_q, kq, draft_tokens, L, p, k_max,
+                    out_tokens, out_num_accepted, flags, ws, ws_bytes, stream);
 }
 
 ss_status ss_process_logits(const void* logits, int dtype, int64_t ld, const ss_params* p, int k_max,

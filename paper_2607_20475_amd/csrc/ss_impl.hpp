@@ -67,6 +67,7 @@ constexpr int kRBins = 1 << kRB;
 constexpr int kHStride = kRBins + 1;
 constexpr int kGT = 4096;                    // gather table entries (LDS)
 constexpr int kGS = 2048;                    // candidate groups held in registers per batch
+constexpr int kQScan = 256;                  // sparse draft lists up to this length are scanned, longer ones sorted
 constexpr uint32_t kNoEmit = 0xFFFFFFFFu;    // threshold of a unit that emits nothing
 constexpr double kFix = 1125899906842624.0;  // 2^50: fixed-point scale of probability mass
 
@@ -111,8 +112,11 @@ struct KArgs {
   int64_t mask_ld;
   const uint64_t* seed;
   const int64_t* position;
-  const float* draft_probs;
+  const float* draft_probs;  // dense q [B, L, ld_q] (NULL when sparse)
   int64_t ld_q;
+  const int32_t* dq_idx;     // sparse q: ids [B, L, kq]
+  const float* dq_val;       //           probabilities [B, L, kq]
+  int kq;                    // entries per draft position (0: dense q)
   const int32_t* draft_tokens;
   int32_t* out_token;
   float* out_logprob;
@@ -746,6 +750,15 @@ constexpr int kSmemFixed = (int)((sizeof(MSmem) + 15) & ~(size_t)15);
 // the largest merge footprint (sampling ops at k_max = SS_MAX_K: pcap + kBlock
 // <= 2 SS_MAX_K + 512 entries) fits gfx950's 160 KiB of LDS
 static_assert(kSmemFixed + 8 * (((2 * SS_MAX_K + 128 + 255) & ~255) + kBlock) <= 160 * 1024, "merge LDS too large");
+// The verification epilogue keeps a sorted copy of a sparse draft list (one
+// 64-bit entry per listed id) over the patch bitmap and table, which are dead
+// once the candidate pool holds the final keys.
+static_assert(offsetof(MSmem, hk) == offsetof(MSmem, pbits) + sizeof(uint32_t) * (kPB / 32) &&
+                  offsetof(MSmem, hf) == offsetof(MSmem, hk) + sizeof(int32_t) * kH &&
+                  offsetof(MSmem, pbits) % 8 == 0 &&
+                  sizeof(uint32_t) * (kPB / 32 + 2 * kH) >= sizeof(uint64_t) * SS_MAX_K,
+              "sparse draft list view");
+__device__ __forceinline__ uint64_t* qlist_view(MSmem& S) { return reinterpret_cast<uint64_t*>(S.pbits); }
 
 __device__ __forceinline__ uint32_t hslot(int id) { return ((uint32_t)id * 2654435761u) >> 21; }  // 11 bits
 static_assert(kH == 2048, "hslot assumes 2048 slots");
@@ -2808,7 +2821,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
           }
         } else {
           // verification of draft token dtok against this row's distribution
-          const float* qrow = a.draft_probs + ((size_t)b * a.L + c.ell) * (size_t)a.ld_q;
+          const float* qrow = a.draft_probs ? a.draft_probs + ((size_t)b * a.L + c.ell) * (size_t)a.ld_q : nullptr;
           double pd_local = 0.0;
           for (int m = 0; m < MT; ++m) {
             const int i = tid + m * kBlock;
@@ -2816,27 +2829,84 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
               pd_local = weight_fast((double)float_of_key(pool[i].x), M, itau) / Zsd;
           }
           const double Pd = block_max(pd_local, S.rd);
-          const double qd = (double)qrow[dtok];
+          // sparse q: the entries naming an id summed, an unlisted id at 0
+          const bool sparse = a.kq > 0;
+          const size_t qo = ((size_t)b * a.L + c.ell) * (size_t)a.kq;
+          uint64_t* ql = qlist_view(S);
+          int NQ = 0;
+          double qd;
+          if (sparse) {
+            // the list into LDS as (id << 32 | q bits), ids outside [0, V)
+            // as 0xFFFFFFFF, padded to a power of two when it will be sorted
+            NQ = a.kq <= kQScan ? a.kq : next_pow2(a.kq);
+            double qs = 0.0;
+            for (int i = tid; i < NQ; i += kBlock) {
+              uint64_t e = ~0ull;
+              if (i < a.kq) {
+                const int id = a.dq_idx[qo + i];
+                const float v = a.dq_val[qo + i];
+                if (id == dtok) qs += (double)v;
+                if (id >= 0 && id < a.V) e = ((uint64_t)(uint32_t)id << 32) | __float_as_uint(v);
+              }
+              ql[i] = e;
+            }
+            qd = block_sum(qs, S.rd);  // its barriers publish the list
+          } else {
+            qd = (double)qrow[dtok];
+          }
           const double u1 = uniform01(seed, (uint32_t)b, pos, 1);
           accept = (Pd > 0.0 && u1 * qd <= Pd) ? 1 : 0;
+          // a long list is sorted (ids descending, padding first) for binary
+          // search; a short one is scanned in list order, every lane reading
+          // the same entry
+          const bool qsorted = sparse && !accept && a.kq > kQScan;
+          if (qsorted) lds_sort_desc(ql, NQ);
+          auto q_of = [&](uint32_t id) -> double {
+            if (!sparse) return (double)qrow[id];
+            double s = 0.0;
+            if (!qsorted) {
+#pragma unroll 8
+              for (int j = 0; j < NQ; ++j) {
+                const uint64_t e = ql[j];
+                if ((uint32_t)(e >> 32) == id) s += (double)__uint_as_float((uint32_t)e);
+              }
+              return s;
+            }
+            int lo = 0, hi = NQ;  // first entry whose id is at most `id`
+            while (lo < hi) {
+              const int mid = (lo + hi) >> 1;
+              if ((uint32_t)(ql[mid] >> 32) > id) lo = mid + 1;
+              else hi = mid;
+            }
+            for (; lo < NQ && (uint32_t)(ql[lo] >> 32) == id; ++lo) s += (double)__uint_as_float((uint32_t)ql[lo]);
+            return s;
+          };
           if (!accept) {
-            // residual max(0, P - q) over the kept set, canonical order
-            auto resid = [&](int i) -> uint64_t {
-              const double P = weight_fast((double)float_of_key(pool[i].x), M, itau) / Zsd;
-              const double v = P - (double)qrow[pool[i].y];
-              return v > 0.0 ? (uint64_t)__double2ll_rn(v * kFix) : 0ull;
-            };
+            // residual max(0, P - q) over the kept set, canonical order, in
+            // place of the kept weights (restored when the residual is empty)
             uint64_t rl = 0ull;
-            for (int m = 0; m < MT; ++m)
-              if ((inS >> m) & 1u) rl += resid(tid + m * kBlock);
-            const uint64_t Rt = block_sum(rl, S.r64);
+            for (int m = 0; m < MT; ++m) {
+              if ((inS >> m) & 1u) {
+                const int i = tid + m * kBlock;
+                const double P = weight_fast((double)float_of_key(pool[i].x), M, itau) / Zsd;
+                const double v = P - q_of(pool[i].y);
+                const uint64_t r = v > 0.0 ? (uint64_t)__double2ll_rn(v * kFix) : 0ull;
+                Wl[i] = r;
+                rl += r;
+              }
+            }
+            const uint64_t Rt = block_sum(rl, S.r64);  // its barriers publish the residuals
             uint64_t e;
             if (Rt > 0ull) {
-              for (int m = 0; m < MT; ++m)
-                if ((inS >> m) & 1u) Wl[tid + m * kBlock] = resid(tid + m * kBlock);
-              lds_barrier();
               e = draw((double)Rt);
             } else {
+              for (int m = 0; m < MT; ++m) {
+                if ((inS >> m) & 1u) {
+                  const int i = tid + m * kBlock;
+                  Wl[i] = (uint64_t)__double2ll_rn(weight_fast((double)float_of_key(pool[i].x), M, itau) * kFix);
+                }
+              }
+              lds_barrier();
               e = draw((double)Zs);
             }
             token = (int)comp_idx(e);

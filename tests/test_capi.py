@@ -70,6 +70,29 @@ def test_logprobs_arguments_are_checked_before_launch(lib):
     assert lib.ss_logprobs(fake, 0, 100, C.byref(p), 10, fake, fake, None, fake, n - 256, None) == -3  # SS_ERR_WORKSPACE
 
 
+def test_verify_sparse_arguments_are_checked_before_launch(lib):
+    from paper_2607_20475_amd import binding as b
+    fake = C.c_void_p(0x10000)  # never dereferenced: validation fails first
+    p = b._Params(B=4, V=100)
+    mode = (C.c_uint32 * 4)()
+    p.mode = C.cast(mode, C.c_void_p)
+    p.seed = fake
+    p.position = fake
+    bad = -1  # SS_ERR_INVALID_ARG
+
+    def call(x=fake, idx=fake, q=fake, kq=8, L=2, ws_bytes=1 << 24):
+        return lib.ss_verify_sparse(x, 0, 100, idx, q, kq, fake, L, C.byref(p), 16, fake, fake, None, fake,
+                                    ws_bytes, None)
+    assert call(kq=0) == bad
+    assert call(kq=4097) == bad
+    assert call(idx=None) == bad
+    assert call(q=None) == bad
+    assert call(x=None) == bad
+    assert call(L=0) == bad
+    n = b.workspace_bytes(b.OP_VERIFY, 4, 100, 2, 16, b.F32)
+    assert call(ws_bytes=n - 256) == -3  # SS_ERR_WORKSPACE: every argument passed its check
+
+
 def test_invalid_arguments_are_rejected_before_launch(lib):
     from paper_2607_20475_amd import binding as b
     fake = C.c_void_p(0x10000)  # never dereferenced: validation fails first

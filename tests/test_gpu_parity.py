@@ -714,6 +714,100 @@ def test_verify_grammar(ssb):
     check_verify(inp, out, nacc, fl, "verify-grammar")
 
 
+def run_verify_sparse(ssb, inp):
+    x = ssb.logits_tensor(inp)
+    qi = torch.from_numpy(np.ascontiguousarray(inp["draft_idx"], np.int32)).cuda()
+    qv = torch.from_numpy(np.ascontiguousarray(inp["draft_q"], np.float32)).cuda()
+    d = torch.from_numpy(np.ascontiguousarray(inp["draft_tokens"], np.int32)).cuda()
+    prm = ssb.Params.from_arrays(inp)
+    out, nacc, fl = ssb.verify_sparse(x, qi, qv, d, prm, inp["k_max"])
+    torch.cuda.synchronize()
+    return _np(out), _np(nacc), _np(fl)
+
+
+def test_verify_sparse_config4(ssb):
+    inp = W.config4_sparse()
+    say("[cfg4_sparse] verify B=64 L=4 V=131072 kq=64")
+    out, nacc, fl = run_verify_sparse(ssb, inp)
+    check_verify(inp, out, nacc, fl, "cfg4_sparse")
+
+
+def _sparse_edge_input(rng, B, L, V, kq, dtype, k_max):
+    """Target rows with a few heads, sparse lists holding duplicates, padding
+    (-1), out-of-range ids and unlisted drafts; greedy, end-of-draft and
+    penalised requests mixed in."""
+    t = rng.normal(0.0, 1.5, (B, L + 1, V))
+    for b in range(B):
+        for l in range(L + 1):
+            t[b, l, rng.choice(V, 24, replace=False)] += rng.uniform(3.0, 8.0, 24)
+    idx = np.full((B, L, kq), -1, np.int32)
+    val = np.zeros((B, L, kq), np.float32)
+    d = np.empty((B, L), np.int32)
+    for b in range(B):
+        for l in range(L):
+            n = int(rng.integers(1, kq + 1))
+            heads = np.argsort(-t[b, l], kind="stable")[: min(n, 32)]
+            ids = np.concatenate([heads, rng.choice(V, n - heads.size)]) if n > heads.size else heads
+            q = rng.dirichlet(np.ones(n)).astype(np.float32)
+            idx[b, l, :n], val[b, l, :n] = ids, q
+            if n >= 4:
+                idx[b, l, n - 1] = ids[0]          # a repeated id: its entries add up
+                idx[b, l, n - 2] = V + 3           # out of range: ignored
+            d[b, l] = ids[int(rng.integers(0, n))] if b % 4 else int(rng.integers(0, V))  # some unlisted drafts
+    d[1, -1] = -1                                   # end of draft
+    mode = np.full(B, W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP | W.MODE_REP)
+    mode[2] = W.MODE_GREEDY
+    mode[5 % B] = W.MODE_TEMP | W.MODE_MINP
+    tt = t.astype(np.float32)
+    x = tt if dtype == W.F32 else W.bf16_bits_from_f32(tt)
+    inp = W.custom_rows(x.reshape(B * (L + 1), V), dtype, k_max=k_max, mode=np.zeros(B * (L + 1)))
+    for k in ("mode", "temperature", "top_k", "top_p", "min_p", "rep", "freq", "pres", "seed", "position"):
+        inp[k] = inp[k][:B]
+    inp["mode"] = mode.astype(np.uint32)
+    inp["temperature"] = np.full(B, 0.9, np.float32)
+    inp["top_k"] = np.full(B, k_max, np.int32)
+    inp["top_p"] = np.full(B, 0.97, np.float32)
+    inp["min_p"] = np.full(B, 0.01, np.float32)
+    inp["rep"] = np.full(B, 1.2, np.float32)
+    inp["position"] = np.arange(B, dtype=np.int64) * 13
+    hist = [rng.integers(0, V, 40).astype(np.int32) for _ in range(B)]
+    off = np.zeros(B + 1, np.int32)
+    off[1:] = np.cumsum([len(h) for h in hist])
+    inp["hist_offsets"], inp["hist_ids"] = off, np.concatenate(hist)
+    inp["bias_offsets"] = np.zeros(B + 1, np.int32)
+    inp.update(x=x, B=B, L=L, draft_idx=idx, draft_q=val, draft_tokens=d)
+    return inp
+
+
+@pytest.mark.parametrize("dtype,kq,V,k_max", [(W.F32, 1, 3000, 64), (W.F32, 40, 5000, 256),
+                                             (W.BF16, 700, 1 << 15, 1024), (W.BF16, 4096, 1 << 16, 2048)],
+                         ids=["f32-kq1", "f32-kq40", "bf16-kq700", "bf16-kq4096"])
+def test_verify_sparse_edge_cases(ssb, dtype, kq, V, k_max):
+    rng = np.random.default_rng(60 + kq)
+    B, L = 10, 3
+    inp = _sparse_edge_input(rng, B, L, V, kq, dtype, k_max)
+    label = f"verify-sparse-{dtype}-kq{kq}"
+    say(f"[{label}] B={B} L={L} V={V} k_max={k_max}")
+    out, nacc, fl = run_verify_sparse(ssb, inp)
+    check_verify(inp, out, nacc, fl, label)
+
+
+def test_verify_sparse_equals_dense_scatter(ssb):
+    # repeat-free lists: the sparse call gives the dense call's outputs for
+    # the q they scatter to (same kernels, only the q lookup differs)
+    inp = W.config4_sparse(B=16)
+    V = inp["V"]
+    dense = np.zeros(inp["draft_idx"].shape[:2] + (V,), np.float32)
+    for b in range(dense.shape[0]):
+        for l in range(dense.shape[1]):
+            m = inp["draft_idx"][b, l] >= 0
+            dense[b, l, inp["draft_idx"][b, l, m]] = inp["draft_q"][b, l, m]
+    sp = run_verify_sparse(ssb, inp)
+    dn = run_verify(ssb, dict(inp, draft_probs=dense))
+    for a_, b_ in zip(sp, dn):
+        assert np.array_equal(a_, b_)
+
+
 # --------------------------------------------------------------------------
 # Graph capture and determinism
 # --------------------------------------------------------------------------
