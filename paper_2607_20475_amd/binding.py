@@ -60,6 +60,10 @@ def lib():
         L.ss_sample.restype = i32
         L.ss_sample.argtypes = [vp, C.c_int, i64, C.POINTER(_Params), C.c_int, vp, vp, vp, vp, C.c_int, vp,
                                 vp, sz, vp]
+        if hasattr(L, "ss_sample_gumbel"):
+            L.ss_sample_gumbel.restype = i32
+            L.ss_sample_gumbel.argtypes = [vp, C.c_int, i64, C.POINTER(_Params), C.c_int, vp, i64, vp, vp, vp, vp,
+                                           C.c_int, vp, vp, sz, vp]
         if hasattr(L, "ss_sample_noalloc"):
             L.ss_sample_noalloc.restype = i32
             L.ss_sample_noalloc.argtypes = [vp, C.c_int, i64, C.POINTER(_Params), C.c_int, vp, vp, vp, vp, C.c_int,
@@ -67,6 +71,10 @@ def lib():
         L.ss_verify.restype = i32
         L.ss_verify.argtypes = [vp, C.c_int, i64, vp, i64, vp, C.c_int, C.POINTER(_Params), C.c_int, vp, vp,
                                 vp, vp, sz, vp]
+        if hasattr(L, "ss_verify_sparse"):
+            L.ss_verify_sparse.restype = i32
+            L.ss_verify_sparse.argtypes = [vp, C.c_int, i64, vp, vp, C.c_int, vp, C.c_int, C.POINTER(_Params),
+                                           C.c_int, vp, vp, vp, vp, sz, vp]
         if hasattr(L, "ss_logprobs"):
             L.ss_logprobs.restype = i32
             L.ss_logprobs.argtypes = [vp, C.c_int, i64, C.POINTER(_Params), C.c_int, vp, vp, vp, vp, sz, vp]
@@ -221,6 +229,37 @@ def sample(logits, params, k_max, k_out=0, out_token=None, out_logprob=None, out
     return out_token, out_logprob, flags
 
 
+def sample_gumbel(logits, params, k_max, noise, k_out=0, out_token=None, out_logprob=None, out_idx=None,
+                  out_prob=None, flags=None, ws=None):
+    """ss_sample_gumbel: sampling with the Gumbel-max draw; noise float32 [B, >= V]
+    holds g = ln z (z ~ Exp(1)) per token.  Returns as ``sample``."""
+    B, V = logits.shape
+    dt = _dtype_code(logits)
+    dev = logits.device
+    if noise.dtype != torch.float32 or noise.dim() != 2 or noise.shape[0] != B or noise.shape[1] < V \
+            or noise.stride(1) != 1:
+        raise SSError("noise must be float32 [B, >= V] with unit column stride")
+    ws = _ws(ws, OP_SAMPLE, B, V, 0, k_max, dt, dev)
+    if out_token is None:
+        out_token = torch.empty(B, dtype=torch.int32, device=dev)
+    if out_logprob is None:
+        out_logprob = torch.empty(B, dtype=torch.float32, device=dev)
+    if flags is None:
+        flags = torch.empty(B, dtype=torch.int32, device=dev)
+    if k_out > 0:
+        if out_idx is None:
+            out_idx = torch.empty(B, k_out, dtype=torch.int32, device=dev)
+        if out_prob is None:
+            out_prob = torch.empty(B, k_out, dtype=torch.float32, device=dev)
+    p = params.struct()
+    _check(lib().ss_sample_gumbel(_ptr(logits), dt, logits.stride(0), C.byref(p), k_max, _ptr(noise), noise.stride(0),
+                                  _ptr(out_token), _ptr(out_logprob), _ptr(out_idx), _ptr(out_prob), k_out,
+                                  _ptr(flags), _ptr(ws), ws.numel(), _stream()))
+    if k_out > 0:
+        return out_token, out_logprob, flags, out_idx, out_prob
+    return out_token, out_logprob, flags
+
+
 def sample_noalloc(logits, params, k_max, out_token, out_logprob, flags, k_out=0, out_idx=None, out_prob=None):
     """ss_sample_noalloc: sampling into caller-provided outputs with the
     library's own per-GPU workspace (nothing is allocated by this call)."""
@@ -252,6 +291,34 @@ def verify(target_logits, draft_probs, draft_tokens, params, k_max, out_tokens=N
     _check(lib().ss_verify(_ptr(target_logits), dt, target_logits.stride(1), _ptr(draft_probs),
                            draft_probs.stride(1), _ptr(draft_tokens), L, C.byref(p), k_max, _ptr(out_tokens),
                            _ptr(out_nacc), _ptr(flags), _ptr(ws), ws.numel(), _stream()))
+    return out_tokens, out_nacc, flags
+
+
+def verify_sparse(target_logits, draft_idx, draft_q, draft_tokens, params, k_max, out_tokens=None, out_nacc=None,
+                  flags=None, ws=None):
+    """target_logits [B, L+1, V]; draft_idx int32 / draft_q float32 [B, L, kq]
+    (sparse draft lists); draft_tokens [B, L] int32."""
+    B, L1, V = target_logits.shape
+    L = L1 - 1
+    kq = draft_idx.shape[-1]
+    dt = _dtype_code(target_logits)
+    dev = target_logits.device
+    ws = _ws(ws, OP_VERIFY, B, V, L, k_max, dt, dev)
+    if out_tokens is None:
+        out_tokens = torch.empty(B, L + 1, dtype=torch.int32, device=dev)
+    if out_nacc is None:
+        out_nacc = torch.empty(B, dtype=torch.int32, device=dev)
+    if flags is None:
+        flags = torch.empty(B, dtype=torch.int32, device=dev)
+    if target_logits.stride(0) != L1 * target_logits.stride(1):
+        raise SSError("target rows must be evenly strided")
+    for t, dtype in ((draft_idx, torch.int32), (draft_q, torch.float32)):
+        if t.shape != (B, L, kq) or t.dtype != dtype or not t.is_contiguous():
+            raise SSError("draft lists must be contiguous [B, L, kq] int32 ids and float32 probabilities")
+    p = params.struct()
+    _check(lib().ss_verify_sparse(_ptr(target_logits), dt, target_logits.stride(1), _ptr(draft_idx), _ptr(draft_q),
+                                  kq, _ptr(draft_tokens), L, C.byref(p), k_max, _ptr(out_tokens), _ptr(out_nacc),
+                                  _ptr(flags), _ptr(ws), ws.numel(), _stream()))
     return out_tokens, out_nacc, flags
 
 
