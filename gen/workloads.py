@@ -262,6 +262,13 @@ def config4_sparse(B: int = 64, L: int = 4, kq: int = 64) -> dict:
                 draft_idx=idx, draft_q=qv, draft_tokens=d, **p)
 
 
+def gumbel_noise(B: int, V: int, seed: int) -> np.ndarray:
+    """Pre-drawn noise for the Gumbel-max draw: g = ln z, z ~ Exp(1), float32
+    ``[B, V]`` (one value per token; the draw subtracts it at the kept ids)."""
+    rng = np.random.default_rng(seed)
+    return np.log(rng.standard_exponential(size=(B, V), dtype=np.float32))
+
+
 def make_config(name: str, **kw) -> dict:
     return {"cfg0": config0, "cfg1": config1, "cfg2": config2,
             "cfg3": config3, "cfg4": config4, "cfg4_sparse": config4_sparse}[name](**kw)

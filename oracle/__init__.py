@@ -159,6 +159,30 @@ def sample(inp, nthreads=0):
     return dict(token=tok, logprob=lp, flags=fl, margin=mg, n_kept=nk, adm_token=at, adm_logprob=al, n_adm=na)
 
 
+def sample_gumbel(inp, noise, nthreads=0):
+    """Singular-mode sampling with the Gumbel-max draw: ``noise`` float32
+    [B, V] holds g = ln z (z ~ Exp(1)) per token.  Returns the keys of
+    ``sample`` except ``margin`` (the pick has no tolerance band of its own;
+    the admissible outcomes cover the kept-set boundaries)."""
+    B, V = int(inp["B"]), int(inp["V"])
+    A = adm_max()
+    x = _x(inp)
+    g = np.ascontiguousarray(noise, dtype=np.float32)
+    assert g.shape == (B, V)
+    bd = _Bundle(inp)
+    tok = np.empty(B, np.int32)
+    lp = np.empty(B, np.float32)
+    fl = np.empty(B, np.int32)
+    nk = np.empty(B, np.int32)
+    at = np.empty((B, A), np.int32)
+    al = np.empty((B, A), np.float32)
+    na = np.empty(B, np.int32)
+    lib().ssref_sample_gumbel(_ptr(x), C.c_int(_dtype_code(inp)), C.c_int64(V), C.byref(bd.p), _ptr(g),
+                              C.c_int64(V), _ptr(tok), _ptr(lp), _ptr(fl), _ptr(nk), _ptr(at), _ptr(al),
+                              _ptr(na), C.c_int(nthreads))
+    return dict(token=tok, logprob=lp, flags=fl, n_kept=nk, adm_token=at, adm_logprob=al, n_adm=na)
+
+
 def process_logits(inp, nthreads=0, force_ns=None):
     """Processed logits y [B,V] (float32) and final probabilities P [B,V] (float64).
 

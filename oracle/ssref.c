@@ -19,7 +19,10 @@
  *     distribution, then min-p in the logit domain, eq. "min_p_trick",
  *     Appendix C.2), temperature entering only the probabilities;
  *   - categorical selection by inverse CDF over the kept prefix, with a
- *     uniform from Philox4x32-10 keyed by (seed, request, position);
+ *     uniform from Philox4x32-10 keyed by (seed, request, position); or by
+ *     Gumbel-max over the kept set with caller-drawn noise g = ln z,
+ *     z ~ Exp(1) (Appendix C.3; the Stage-2 selection subtracts g at the kept
+ *     ids);
  *   - speculative verification (Section 3.1 "Speculative Verification",
  *     Appendix C.4): accept when u*q(d) <= p(d), else resample from
  *     normalize(max(0, p - q)); a bonus token after full acceptance; the
@@ -489,6 +492,82 @@ int ssref_sample(const void *x, int dtype, int64_t ld, const ssref_params *p,
     if (out_logprob) out_logprob[b] = lp;
     if (flags) flags[b] = d.flags;
     if (margin) margin[b] = mg;
+    if (n_kept) n_kept[b] = d.n_s;
+    if (adm_tok) {
+      for (int e = 0; e < SSREF_ADM; ++e) {
+        adm_tok[(int64_t)b * SSREF_ADM + e] = e < na ? at[e] : -1;
+        if (adm_lp) adm_lp[(int64_t)b * SSREF_ADM + e] = e < na ? al[e] : 0.0f;
+      }
+    }
+    if (n_adm) n_adm[b] = na;
+    free(y); free(order); free(w);
+  }
+  return 0;
+}
+
+/* Gumbel-max selection over the kept prefix (Appendix C.3): the rank whose
+ * score (y - M)/tau - g[id] is largest, the lower token id on equal scores.
+ * The score is formed in double exactly in this order (y == M gives 0). */
+static int gumbel_pick(const float *y, const int32_t *order, int ns, double M, double tau, const float *g) {
+  int best = -1;
+  double bs = 0.0;
+  for (int r = 0; r < ns; ++r) {
+    double yr = (double)y[order[r]];
+    double sc = ((yr == M) ? 0.0 : (yr - M) / tau) - (double)g[order[r]];
+    if (best < 0 || sc > bs || (sc == bs && order[r] < order[best])) { best = r; bs = sc; }
+  }
+  return best;
+}
+
+/* Sampling with the Gumbel-max draw: as ssref_sample, the token chosen by
+ * gumbel_pick with noise g [B, ld_g] (read at the kept ids only).  The
+ * admissible outcomes are the picks over every admissible kept-set size. */
+int ssref_sample_gumbel(const void *x, int dtype, int64_t ld, const ssref_params *p, const float *g,
+                        int64_t ld_g, int32_t *out_token, float *out_logprob, int32_t *flags,
+                        int32_t *n_kept, int32_t *adm_tok, float *adm_lp, int32_t *n_adm, int nthreads) {
+  int B = p->B, V = p->V;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+#endif
+  for (int b = 0; b < B; ++b) {
+    float *y = (float *)malloc(sizeof(float) * (size_t)V);
+    int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)V);
+    double *w = (double *)malloc(sizeof(double) * (size_t)(p->k_cap > 0 ? p->k_cap : 1) + 8);
+    process_one(x, dtype, (int64_t)b * ld, p, b, NULL, 0, b, y);
+    int nv = ssref_order(y, V, order);
+    uint32_t mode = effective_mode(p, b);
+    dist_t d;
+    row_distribution(y, order, nv, mode, pf(p->temperature, b, 1.0f), p->top_k ? p->top_k[b] : 0,
+                     pf(p->top_p, b, 1.0f), pf(p->min_p, b, 0.0f), p->k_cap, w, &d);
+    int tok = -1;
+    float lp = 0.0f;
+    int32_t at[SSREF_ADM];
+    float al[SSREF_ADM];
+    int na = 0;
+    if (nv > 0) {
+      if (d.greedy) {
+        tok = order[0];
+      } else {
+        const float *gr = g + (int64_t)b * ld_g;
+        for (int pass = 0; pass < 2; ++pass) {
+          for (int ns = d.ns_lo; ns <= d.ns_hi && na < SSREF_ADM; ++ns) {
+            if ((pass == 0) != (ns == d.n_s)) continue;
+            int r = gumbel_pick(y, order, ns, d.M, d.tau, gr);
+            int32_t t = order[r];
+            float l = (float)log(w[r] / prefix_sum(w, ns));
+            if (pass == 0) { tok = t; lp = l; }
+            int dup = 0;
+            for (int e = 0; e < na; ++e) dup |= (at[e] == t && al[e] == l);
+            if (!dup) { at[na] = t; al[na] = l; ++na; }
+          }
+        }
+      }
+    }
+    if (na == 0) { at[0] = tok; al[0] = lp; na = 1; }
+    out_token[b] = tok;
+    if (out_logprob) out_logprob[b] = lp;
+    if (flags) flags[b] = d.flags;
     if (n_kept) n_kept[b] = d.n_s;
     if (adm_tok) {
       for (int e = 0; e < SSREF_ADM; ++e) {

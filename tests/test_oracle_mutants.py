@@ -48,6 +48,12 @@ MUTANTS = [
      "    if (c->qi[o + i] == id) s = (double)c->qv[o + i];", "test_verify_sparse_first_token"),
     ("sparse_q_first_position_list", "  const int64_t o = ((int64_t)c->b * c->L + (l - 1)) * c->kq;",
      "  const int64_t o = ((int64_t)c->b * c->L) * c->kq;", "test_verify_sparse_lists_are_per_position"),
+    ("gumbel_noise_added", "    double sc = ((yr == M) ? 0.0 : (yr - M) / tau) - (double)g[order[r]];",
+     "    double sc = ((yr == M) ? 0.0 : (yr - M) / tau) + (double)g[order[r]];", "test_gumbel_draw"),
+    ("gumbel_temperature_dropped", "    double sc = ((yr == M) ? 0.0 : (yr - M) / tau) - (double)g[order[r]];",
+     "    double sc = ((yr == M) ? 0.0 : (yr - M)) - (double)g[order[r]];", "test_gumbel_draw"),
+    ("gumbel_noise_by_rank", "    double sc = ((yr == M) ? 0.0 : (yr - M) / tau) - (double)g[order[r]];",
+     "    double sc = ((yr == M) ? 0.0 : (yr - M) / tau) - (double)g[r];", "test_gumbel_draw"),
     ("uniform_counter_words_swapped", "  uint32_t ctr[4] = {request, (uint32_t)((uint64_t)position & 0xFFFFFFFFu),",
      "  uint32_t ctr[4] = {(uint32_t)((uint64_t)position & 0xFFFFFFFFu), request,",
      "test_uniform_counter_words"),

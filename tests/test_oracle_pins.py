@@ -299,6 +299,70 @@ def test_sampling_distribution_chi_square():
 
 
 # --------------------------------------------------------------------------
+# Gumbel-max draw (Appendix C.3)
+# --------------------------------------------------------------------------
+def test_gumbel_draw_follows_truncated_distribution_chi_square():
+    # with g = ln z, z ~ Exp(1) fresh per row, the Gumbel-max pick over the kept
+    # set is distributed as the truncated distribution P (the reparameterisation)
+    V, B = 12, 40000
+    rng = np.random.default_rng(17)
+    y = rng.normal(0, 1, V).astype(np.float32)
+    mode = W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP
+    inp = W.custom_rows(np.tile(y, (B, 1)), W.F32, k_max=V, mode=np.full(B, mode), temperature=np.full(B, 0.7),
+                        top_k=np.full(B, 9), top_p=np.full(B, 0.95))
+    g = np.log(rng.exponential(size=(B, V))).astype(np.float32)
+    tok = oracle.sample_gumbel(inp, g)["token"]
+    d = oracle.row_distribution(y, mode, temperature=0.7, top_k=9, top_p=0.95, k_cap=V)
+    probs = np.zeros(V)
+    probs[d["order"][: d["n_s"]]] = d["P"]
+    counts = np.bincount(tok, minlength=V).astype(np.float64)
+    assert counts[probs == 0].sum() == 0
+    ok, pv = _chi2_ok(counts[probs > 0], probs[probs > 0])
+    assert ok, pv
+
+
+def test_gumbel_draw_hand_cases():
+    # two tokens y = (1, 0): the pick is token 0 iff (0 - g0) > (-1/tau - g1)
+    tau = np.float32(0.5)
+    y = np.array([[1.0, 0.0]], np.float32)
+    inp = W.custom_rows(y, W.F32, k_max=2, mode=np.array([W.MODE_TEMP]), temperature=np.array([tau]))
+    for g0, g1, want in ((0.0, 0.0, 0), (1.9, 0.0, 0), (2.1, 0.0, 1), (0.0, -2.1, 1), (-3.0, -4.9, 0),
+                         (-3.0, -5.1, 1)):
+        g = np.array([[g0, g1]], np.float32)
+        assert int(oracle.sample_gumbel(inp, g)["token"][0]) == want, (g0, g1)
+    # equal scores: the lower token id
+    y2 = np.array([[0.0, 1.0, 0.0]], np.float32)
+    inp2 = W.custom_rows(y2, W.F32, k_max=3, mode=np.array([0]))
+    o = oracle.sample_gumbel(inp2, np.array([[0.0, 1.0, 0.0]], np.float32))
+    assert int(o["token"][0]) == 0
+    # zero noise is the argmax (greedy as z = 1), with its truncated log-probability
+    yr = np.random.default_rng(3).normal(0, 1, (4, 50)).astype(np.float32)
+    inp3 = W.custom_rows(yr, W.F32, k_max=50, mode=np.full(4, W.MODE_TEMP | W.MODE_TOPK),
+                         temperature=np.full(4, 1.3), top_k=np.full(4, 5))
+    o = oracle.sample_gumbel(inp3, np.zeros((4, 50), np.float32))
+    assert np.array_equal(o["token"], np.argmax(yr, axis=1))
+    sp = special.softmax(np.sort(yr.astype(np.float64), axis=1)[:, ::-1][:, :5] / np.float32(1.3), axis=1)
+    assert np.allclose(o["logprob"], np.log(sp[:, 0]), rtol=1e-6)
+
+
+def test_gumbel_draw_never_leaves_the_kept_set():
+    # a token outside the top-k with a very large perturbation is still excluded
+    V, B = 40, 64
+    rng = np.random.default_rng(5)
+    y = rng.normal(0, 1, (B, V)).astype(np.float32)
+    g = np.log(rng.exponential(size=(B, V))).astype(np.float32)
+    order = np.argsort(-y, axis=1, kind="stable")
+    for b in range(B):
+        g[b, order[b, 6:]] = -1e6  # score +1e6 outside the top 6
+    inp = W.custom_rows(y, W.F32, k_max=V, mode=np.full(B, W.MODE_TOPK), top_k=np.full(B, 6))
+    tok = oracle.sample_gumbel(inp, g)["token"]
+    assert all(tok[b] in order[b, :6] for b in range(B))
+    # greedy rows ignore the noise
+    inp = W.custom_rows(y, W.F32, k_max=V, mode=np.full(B, W.MODE_GREEDY))
+    assert np.array_equal(oracle.sample_gumbel(inp, g)["token"], np.argmax(y, axis=1))
+
+
+# --------------------------------------------------------------------------
 # Speculative verification
 # --------------------------------------------------------------------------
 def _verify_inputs(x_rows, q, d, mode, L, **params):
