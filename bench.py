@@ -56,8 +56,9 @@ MALL_BYTES = 256 << 20
 CONFIGS = ("cfg0", "cfg1", "cfg2", "cfg3", "cfg4")
 # a stress line beside the five workloads: the headline batch with every
 # logit of a row equal (the paper's tied correctness inputs at full size)
-EXTRA = ("cfg1_tied", "cfg1_logprobs", "cfg4_sparse")
+EXTRA = ("cfg1_tied", "cfg1_logprobs", "cfg4_sparse", "cfg1_gumbel")
 LOGPROBS_N = 20  # log-probabilities per request on the log-probability line
+MODE_TOPK = 0x080  # the top-k indicator bit (bit-level encoding table, Section 3.5)
 WORKLOAD = {
     "cfg0": "tiny singular batch: fused sample B=4 V=32768 fp32, per-row temperature {0,0.7,1.0,1.3}, "
             "top-k 50, top-p 0.9",
@@ -71,6 +72,8 @@ WORKLOAD = {
                  "logit 0.5",
     "cfg1_logprobs": "top-20 log-probabilities (ss_logprobs) of the heterogeneous singular batch (B=64 V=131072 "
                      "bf16, penalties, bias), every request with bit 0x400",
+    "cfg1_gumbel": "the heterogeneous singular batch (B=64 V=131072 bf16) sampled with the Gumbel-max draw "
+                   "(ss_sample_gumbel, noise [B, V] fp32 read at the kept ids)",
     "cfg4_sparse": "multistep verification against sparse draft lists (ss_verify_sparse): B=64 L=4 V=131072 "
                    "bf16 target, at most 64 (id, q) pairs per draft position",
 }
@@ -78,6 +81,8 @@ WORKLOAD = {
 
 def make_input(name, W):
     """The named workload's seeded synthetic input."""
+    if name == "cfg1_gumbel":
+        return W.make_config("cfg1")
     if name == "cfg1_logprobs":
         inp = W.make_config("cfg1")
         inp["mode"] = inp["mode"] | np.uint32(W.MODE_LOGPROBS)
@@ -109,6 +114,10 @@ def algorithmic_bytes(name, inp):
         b += _nbytes(inp.get(k))
     if name == "cfg1_logprobs":
         return b + B * (LOGPROBS_N * 8 + 4)  # (index, log-probability) pairs and flags
+    if name == "cfg1_gumbel":  # plus the noise at the kept ids (at most k_max per row)
+        topk_on = (np.asarray(inp["mode"]) & MODE_TOPK) != 0
+        k = np.where(topk_on, np.clip(np.asarray(inp["top_k"]), 0, inp["k_max"]), inp["k_max"])
+        return b + 4 * int(k.sum()) + 12 * B
     if name == "cfg4":
         L = int(inp["L"])
         return b + _nbytes(inp["draft_tokens"]) + B * L * (inp["k_max"] + 1) * 4 + B * (L + 2) * 4
@@ -270,6 +279,17 @@ class Runner:
 
             def step(i):
                 ssb.topk(self.xs[i % self.R], k, inp["k_max"], out_val=ov, out_idx=oi, flags=fl, ws=ws)
+        elif name == "cfg1_gumbel":
+            prm = ssb.Params.from_arrays(inp, dev)
+            g = t.from_numpy(W.gumbel_noise(inp["B"], inp["V"], 1001)).to(dev)
+            ws = ssb.workspace(ssb.OP_SAMPLE, inp["B"], inp["V"], 0, inp["k_max"], ssb.BF16, dev)
+            tok = t.empty(inp["B"], dtype=t.int32, device=dev)
+            lp = t.empty(inp["B"], dtype=t.float32, device=dev)
+            fl = t.empty(inp["B"], dtype=t.int32, device=dev)
+
+            def step(i):
+                ssb.sample_gumbel(self.xs[i % self.R], prm, inp["k_max"], g, out_token=tok, out_logprob=lp,
+                                  flags=fl, ws=ws)
         elif name == "cfg1_logprobs":
             prm = ssb.Params.from_arrays(inp, dev)
             ws = ssb.workspace(ssb.OP_LOGPROBS, inp["B"], inp["V"], 0, LOGPROBS_N, ssb.BF16, dev)

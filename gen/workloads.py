@@ -266,7 +266,7 @@ def gumbel_noise(B: int, V: int, seed: int) -> np.ndarray:
     """Pre-drawn noise for the Gumbel-max draw: g = ln z, z ~ Exp(1), float32
     ``[B, V]`` (one value per token; the draw subtracts it at the kept ids)."""
     rng = np.random.default_rng(seed)
-    return np.log(rng.standard_exponential(size=(B, V), dtype=np.float32))
+    return np.log(rng.standard_exponential(size=(B, V))).astype(np.float32)
 
 
 def make_config(name: str, **kw) -> dict:

@@ -5,6 +5,8 @@
  *   ss_sample          singular-mode sampling: prologue (Appendix C.1), top-k /
  *                      top-p / min-p truncation in Alg. 11 order (Appendix C.2),
  *                      greedy or stochastic selection (Section 3.5, Appendix C.3)
+ *   ss_sample_gumbel   the same with the Gumbel-max draw over the kept set and
+ *                      caller-drawn noise (Appendix C.3; the Stage-2 selection)
  *   ss_verify          multistep speculative verification (Section 3.1,
  *                      Appendix C.4): accept when u*q(d) <= p(d), else resample
  *                      from normalize(max(0, p - q)); bonus token on full acceptance
@@ -175,6 +177,24 @@ ss_status ss_topk(const void *x, int dtype, int B, int V, int64_t ld, const int3
 ss_status ss_sample(const void *logits, int dtype, int64_t ld, const ss_params *p, int k_max,
                     int32_t *out_token, float *out_logprob, int32_t *out_idx, float *out_prob,
                     int k_out, int32_t *flags, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Singular-mode sampling with the Gumbel-max draw (Appendix C.3: the argmax
+ * of the perturbed logits is distributed as the categorical; the Stage-2
+ * selection takes pre-drawn noise).  Everything is as for ss_sample except the
+ * draw: a stochastic request's token is the kept id i with the largest
+ *     (y_i - M) / tau - g_i        (in double; 0 - g_i for y_i = M),
+ * the lower id on equal scores, where g = ln z, z ~ Exp(1), is drawn by the
+ * caller (so results are reproducible and calls capture in graphs without an
+ * RNG state).  Greedy requests ignore the noise; out_logprob is ln P(token)
+ * under the truncated distribution, as for ss_sample.
+ *   noise     float[B, ld_noise] (ld_noise >= V), g per token; read at the
+ *             kept ids only.  NaN noise is outside the contract.
+ */
+ss_status ss_sample_gumbel(const void *logits, int dtype, int64_t ld, const ss_params *p, int k_max,
+                           const float *noise, int64_t ld_noise, int32_t *out_token, float *out_logprob,
+                           int32_t *out_idx, float *out_prob, int k_out, int32_t *flags, void *ws,
+                           size_t ws_bytes, void *stream);
 
 /*
  * Multistep speculative verification.

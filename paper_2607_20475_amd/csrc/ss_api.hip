@@ -274,13 +274,15 @@ ss_status ss_logprobs(const void* logits, int dtype, int64_t ld, const ss_params
   return launch(a, dtype, lay, ws, (hipStream_t)stream, false);
 }
 
-ss_status ss_sample(const void* logits, int dtype, int64_t ld, const ss_params* p, int k_max, int32_t* out_token,
-                    float* out_logprob, int32_t* out_idx, float* out_prob, int k_out, int32_t* flags, void* ws,
-                    size_t ws_bytes, void* stream) {
+static ss_status sample_any(const void* logits, int dtype, int64_t ld, const ss_params* p, int k_max,
+                            const float* noise, int64_t ld_noise, int32_t* out_token, float* out_logprob,
+                            int32_t* out_idx, float* out_prob, int k_out, int32_t* flags, void* ws, size_t ws_bytes,
+                            void* stream) {
   if (!logits || !p || !out_token || !ws || (dtype != SS_F32 && dtype != SS_BF16)) return SS_ERR_INVALID_ARG;
   if (k_out < 0 || (k_out > 0 && (!out_idx || !out_prob))) return SS_ERR_INVALID_ARG;
   const int B = p->B, V = p->V;
   if (ld < V || !params_ok(p, B, V)) return SS_ERR_INVALID_ARG;
+  if (noise && ld_noise < V) return SS_ERR_INVALID_ARG;
   Layout lay;
   if (!make_layout(OP_SAMPLE, B, V, 0, k_max, dtype, &lay)) return SS_ERR_INVALID_ARG;
   if (ws_bytes < lay.total || !aligned16(ws)) return SS_ERR_WORKSPACE;
@@ -296,12 +298,30 @@ ss_status ss_sample(const void* logits, int dtype, int64_t ld, const ss_params* 
   a.k_out = k_out;
   a.vec_ok = aligned16(logits) && ((ld * esize(dtype)) % 16 == 0);
   fill_params(a, p);
+  a.gum = noise;
+  a.ld_g = noise ? ld_noise : 0;
   a.out_token = out_token;
   a.out_logprob = out_logprob;
   a.out_idx = k_out > 0 ? out_idx : nullptr;
   a.out_prob = k_out > 0 ? out_prob : nullptr;
   a.flags = flags;
   return launch(a, dtype, lay, ws, (hipStream_t)stream, false);
+}
+
+ss_status ss_sample(const void* logits, int dtype, int64_t ld, const ss_params* p, int k_max, int32_t* out_token,
+                    float* out_logprob, int32_t* out_idx, float* out_prob, int k_out, int32_t* flags, void* ws,
+                    size_t ws_bytes, void* stream) {
+  return sample_any(logits, dtype, ld, p, k_max, nullptr, 0, out_token, out_logprob, out_idx, out_prob, k_out, flags,
+                    ws, ws_bytes, stream);
+}
+
+ss_status ss_sample_gumbel(const void* logits, int dtype, int64_t ld, const ss_params* p, int k_max,
+                           const float* noise, int64_t ld_noise, int32_t* out_token, float* out_logprob,
+                           int32_t* out_idx, float* out_prob, int k_out, int32_t* flags, void* ws, size_t ws_bytes,
+                           void* stream) {
+  if (!noise) return SS_ERR_INVALID_ARG;
+  return sample_any(logits, dtype, ld, p, k_max, noise, ld_noise, out_token, out_logprob, out_idx, out_prob, k_out,
+                    flags, ws, ws_bytes, stream);
 }
 
 static ss_status verify_any(const void* target_logits, int dtype, int64_t ld_row, const float* draft_probs,

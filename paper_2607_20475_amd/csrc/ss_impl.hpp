@@ -117,6 +117,8 @@ struct KArgs {
   const int32_t* dq_idx;     // sparse q: ids [B, L, kq]
   const float* dq_val;       //           probabilities [B, L, kq]
   int kq;                    // entries per draft position (0: dense q)
+  const float* gum;          // sampling with the Gumbel-max draw: g = ln z per token [B, ld_g] (else NULL)
+  int64_t ld_g;
   const int32_t* draft_tokens;
   int32_t* out_token;
   float* out_logprob;
@@ -2526,7 +2528,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
         }
       };
       if constexpr (OP == OP_SAMPLE && DT == SS_BF16) {
-        if (!a.out_idx && (phi >> 16) - (tmax >> 16) < (uint32_t)kRBins)
+        if (!a.out_idx && !a.gum && (phi >> 16) - (tmax >> 16) < (uint32_t)kRBins)
           binned = sample_binned(c, S, pool, (int)C, (int)nfin, (uint32_t)want, tmax >> 16, a.V, b, btoken, blogprob);
       }
       if (binned) {
@@ -2784,7 +2786,31 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
         }
       } else {
         if (OP == OP_SAMPLE || !has_draft) {
-          const uint64_t e = draw((double)Zs);
+          uint64_t e;
+          if (OP == OP_SAMPLE && a.gum) {
+            // Gumbel-max over the kept set (Appendix C.3): the largest
+            // (y - M)/tau - g[id] in double, the lower id on equal scores
+            const float* grow = a.gum + (size_t)b * (size_t)a.ld_g;
+            double bs = -__builtin_inf();
+            uint64_t bk = 0ull;  // (~id << 32) | key of this thread's best
+            for (int m = 0; m < MT; ++m) {
+              if ((inS >> m) & 1u) {
+                const int i = tid + m * kBlock;
+                const double y = (double)float_of_key(pool[i].x);
+                const double sc = (y == M ? 0.0 : (y - M) / tau) - (double)grow[pool[i].y];
+                const uint64_t k2 = ((uint64_t)(~pool[i].y) << 32) | pool[i].x;
+                if (sc > bs || (sc == bs && k2 > bk)) {
+                  bs = sc;
+                  bk = k2;
+                }
+              }
+            }
+            const double top = block_max(bs, S.rd);
+            const uint64_t win = block_max<uint64_t>(bs == top ? bk : (uint64_t)0, S.r64);
+            e = comp_of((uint32_t)win, ~(uint32_t)(win >> 32));
+          } else {
+            e = draw((double)Zs);
+          }
           token = (int)comp_idx(e);
           const double w = weight_fast((double)float_of_key(comp_key(e)), M, itau);
           logprob = (float)log(w / Zsd);

@@ -93,6 +93,23 @@ def test_verify_sparse_arguments_are_checked_before_launch(lib):
     assert call(ws_bytes=n - 256) == -3  # SS_ERR_WORKSPACE: every argument passed its check
 
 
+def test_sample_gumbel_arguments_are_checked_before_launch(lib):
+    from paper_2607_20475_amd import binding as b
+    fake = C.c_void_p(0x10000)  # never dereferenced: validation fails first
+    p = b._Params(B=4, V=100)
+    mode = (C.c_uint32 * 4)()
+    p.mode = C.cast(mode, C.c_void_p)
+
+    def call(noise=fake, ld_noise=100, ws_bytes=1 << 24, k_max=10):
+        return lib.ss_sample_gumbel(fake, 0, 100, C.byref(p), k_max, noise, ld_noise, fake, None, None, None, 0,
+                                    None, fake, ws_bytes, None)
+    assert call(noise=None) == -1
+    assert call(ld_noise=99) == -1
+    assert call(k_max=0) == -1
+    n = b.workspace_bytes(b.OP_SAMPLE, 4, 100, 0, 10, b.F32)
+    assert call(ws_bytes=n - 256) == -3  # SS_ERR_WORKSPACE: every argument passed its check
+
+
 def test_invalid_arguments_are_rejected_before_launch(lib):
     from paper_2607_20475_amd import binding as b
     fake = C.c_void_p(0x10000)  # never dereferenced: validation fails first

@@ -287,6 +287,63 @@ def test_sample_kept_distribution_outputs(ssb):
         assert np.all(idx[b, m:] == -1)
 
 
+def check_sample_gumbel(ssb, inp, noise, label, k_out=0):
+    x = ssb.logits_tensor(inp)
+    prm = ssb.Params.from_arrays(inp)
+    g = torch.from_numpy(np.ascontiguousarray(noise, np.float32)).cuda()
+    r = ssb.sample_gumbel(x, prm, inp["k_max"], g, k_out=k_out)
+    torch.cuda.synchronize()
+    tok, lp, fl = _np(r[0]), _np(r[1]), _np(r[2])
+    ref = oracle.sample_gumbel(inp, noise)
+    ok = _admissible(ref, tok, lp)
+    bad = np.nonzero(~ok)[0]
+    assert bad.size == 0, (label, bad[:10], tok[bad[:10]], lp[bad[:10]], ref["token"][bad[:10]],
+                           ref["logprob"][bad[:10]], ref["n_adm"][bad[:10]])
+    assert np.array_equal(fl & (EMPTY | KCAP), ref["flags"] & (EMPTY | KCAP)), label
+    near = int((ref["n_adm"] > 1).sum())
+    alt = int((tok != ref["token"]).sum())
+    fb = int(((fl & FALLBACK) > 0).sum())
+    if COUNTS is not None:
+        COUNTS.add(label, tok.size, near, alt, fb)
+    say(f"[{label}] rows={tok.size} near-boundary rows={near} (outcome other than the oracle's own: {alt}) "
+        f"fallback={fb}")
+    return r
+
+
+@pytest.mark.parametrize("name", ["cfg0", "cfg1", "cfg3"])
+def test_sample_gumbel_configs(ssb, name):
+    inp = W.make_config(name)
+    say(f"[{name}-gumbel] sample B={inp['B']} V={inp['V']} dtype={inp['dtype']}")
+    check_sample_gumbel(ssb, inp, W.gumbel_noise(inp["B"], inp["V"], 500 + len(name)), f"{name}-gumbel")
+
+
+def test_sample_gumbel_edge_cases(ssb):
+    # zero noise (the argmax of the kept set), equal scores (lower id), heavy
+    # noise outside the kept set, tied and masked rows, a k_out list beside
+    rng = np.random.default_rng(88)
+    B, V = 12, 3000
+    x = rng.normal(0, 1, (B, V)).astype(np.float32)
+    x[3] = 0.0                               # every logit tied
+    x[4, ::2] = -np.inf                      # half masked
+    x[5, 7] = np.nan
+    noise = np.log(rng.exponential(size=(B, V))).astype(np.float32)
+    noise[0] = 0.0                           # zero noise: the argmax
+    order = np.argsort(-x[1], kind="stable")
+    noise[1, order[20:]] = -1e30             # huge scores outside the kept set
+    noise[2] = 0.0
+    x[2, :4] = np.array([1.0, 2.0, 1.0, 2.0], np.float32)
+    x[2, 4:] = -5.0
+    # tau 0.5: scores (1 - 2)/0.5 + 1 = -1 (id 0) and 0 - 1 = -1 (id 1) tie: the lower id
+    noise[2, :4] = np.array([-1.0, 1.0, 5.0, 5.0], np.float32)
+    mode = np.full(B, W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP | W.MODE_MINP, np.uint32)
+    mode[6] = W.MODE_GREEDY
+    mode[7] = W.MODE_TEMP                    # no truncation: the k_max bound
+    inp = W.custom_rows(x, W.F32, k_max=256, mode=mode, temperature=np.full(B, 0.5), top_k=np.full(B, 20),
+                        top_p=np.full(B, 0.97), min_p=np.full(B, 0.001), position=np.arange(B))
+    r = check_sample_gumbel(ssb, inp, noise, "gumbel-edge", k_out=32)
+    assert int(_np(r[0])[2]) == 0
+
+
 def _edge_inputs(kind):
     rng = np.random.default_rng(77)
     B = 8
