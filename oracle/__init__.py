@@ -230,7 +230,9 @@ def logprobs(inp, n_lp, nthreads=0):
 
 def verify(inp, nthreads=0):
     """Multistep verification, against dense ``draft_probs`` [B, L, V] or, when
-    the input holds ``draft_idx`` / ``draft_q`` [B, L, kq], sparse draft lists.
+    the input holds ``draft_idx`` / ``draft_q`` [B, L, kq], sparse draft lists;
+    with ``row_map`` [B, L+1] the logits ``x`` are [B, Lt, V] target rows of a
+    draft tree and path position l reads row ``row_map[b, l]``.
 
     Returns dict(tokens [B,L+1], n_acc [B], flags, margin, adm_tokens [B,A,L+1],
     adm_nacc [B,A], n_adm): the oracle's own outcome and every admissible
@@ -256,7 +258,16 @@ def verify(inp, nthreads=0):
     anacc = np.empty((B, A), np.int32)
     nadm = np.empty(B, np.int32)
     outs = (_ptr(tok), _ptr(na), _ptr(fl), _ptr(mg), _ptr(aseq), _ptr(anacc), _ptr(nadm), C.c_int(nthreads))
-    if sparse:
+    if inp.get("row_map") is not None:
+        assert sparse, "tree paths take sparse draft lists"
+        rm = np.ascontiguousarray(inp["row_map"], dtype=np.int32)
+        Lt = int(np.asarray(inp["x"]).shape[1])
+        assert rm.shape == (B, L + 1)
+        rc = lib().ssref_verify_tree(_ptr(x), C.c_int(_dtype_code(inp)), C.c_int64(V), C.c_int(Lt), _ptr(rm),
+                                     _ptr(qi), _ptr(qv), C.c_int(qi.shape[2]), _ptr(d), C.c_int(L),
+                                     C.byref(bd.p), *outs)
+        assert rc == 0
+    elif sparse:
         rc = lib().ssref_verify_sparse(_ptr(x), C.c_int(_dtype_code(inp)), C.c_int64(V), _ptr(qi), _ptr(qv),
                                        C.c_int(qi.shape[2]), _ptr(d), C.c_int(L), C.byref(bd.p), *outs)
         assert rc == 0

@@ -28,7 +28,10 @@
  *     normalize(max(0, p - q)); a bonus token after full acceptance; the
  *     draft distribution q either dense over the vocabulary or sparse, as the
  *     (id, probability) list a singular-mode draft step emits over its
- *     candidate set (Section 3.2), every unlisted id having q = 0;
+ *     candidate set (Section 3.2), every unlisted id having q = 0; and, for
+ *     one path through a draft tree, a map from the path's positions to the
+ *     target rows computed for the tree (the draft-to-target mapping of
+ *     Appendix C.4);
  *   - top-k log-probabilities (indicator bit 0x400 of the bit-level encoding
  *     table, Section 3.5): the leading tokens of the canonical order with
  *     their log-probabilities under the untruncated distribution of the row.
@@ -736,6 +739,8 @@ typedef struct {
   const int32_t *qi;  /* sparse q: ids [B, L, kq] */
   const float *qv;    /*           probabilities [B, L, kq] */
   int kq;
+  const int32_t *rmap; /* path position -> target row of the request [B, L+1], or NULL */
+  int Lt;              /* target rows per request (L+1 without a map) */
   const int32_t *dr;  /* this request's drafts [L] */
   int L, b, V;
   const ssref_params *p;
@@ -764,8 +769,19 @@ static double qget(const vctx_t *c, int l, int id) {
 static vrow_t *vrow_get(vctx_t *c, int l) {
   vrow_t *r = &c->rows[l - 1];
   if (r->ready) return r;
-  int64_t row = (int64_t)c->b * (c->L + 1) + (l - 1);
-  process_one(c->x, c->dtype, row * c->ld_row, c->p, c->b, c->dr, l - 1, row, r->y);
+  int64_t row = (int64_t)c->b * (c->L + 1) + (l - 1);  /* path row: its grammar mask row */
+  int64_t src = (int64_t)c->b * c->Lt + (l - 1);
+  int dead = 0;
+  if (c->rmap) {
+    int32_t t = c->rmap[row];
+    if (t >= 0 && t < c->Lt) src = (int64_t)c->b * c->Lt + t;
+    else dead = 1;
+  }
+  if (dead) {  /* a map entry outside [0, Lt): every token of the row is masked */
+    for (int v = 0; v < c->V; ++v) r->y[v] = -INFINITY;
+  } else {
+    process_one(c->x, c->dtype, src * c->ld_row, c->p, c->b, c->dr, l - 1, row, r->y);
+  }
   r->nv = ssref_order(r->y, c->V, r->order);
   row_distribution(r->y, r->order, r->nv, c->mode, pf(c->p->temperature, c->b, 1.0f),
                    c->p->top_k ? c->p->top_k[c->b] : 0, pf(c->p->top_p, c->b, 1.0f),
@@ -877,10 +893,11 @@ static void vexplore(vctx_t *c, int l) {
   }
 }
 
-static int verify_all(const void *x, int dtype, int64_t ld_row, const float *draft_probs, int64_t ld_q,
-                      const int32_t *q_idx, const float *q_val, int kq, const int32_t *draft_tokens, int L,
-                      const ssref_params *p, int32_t *out_tokens, int32_t *n_acc, int32_t *flags,
-                      double *margin, int32_t *adm_seq, int32_t *adm_nacc, int32_t *n_adm, int nthreads) {
+static int verify_all(const void *x, int dtype, int64_t ld_row, int Lt, const int32_t *row_map,
+                      const float *draft_probs, int64_t ld_q, const int32_t *q_idx, const float *q_val, int kq,
+                      const int32_t *draft_tokens, int L, const ssref_params *p, int32_t *out_tokens,
+                      int32_t *n_acc, int32_t *flags, double *margin, int32_t *adm_seq, int32_t *adm_nacc,
+                      int32_t *n_adm, int nthreads) {
   int B = p->B, V = p->V;
 #ifdef _OPENMP
   if (nthreads > 0) omp_set_num_threads(nthreads);
@@ -892,6 +909,7 @@ static int verify_all(const void *x, int dtype, int64_t ld_row, const float *dra
     memset(&c, 0, sizeof(c));
     c.x = x; c.dtype = dtype; c.ld_row = ld_row; c.q = draft_probs; c.ld_q = ld_q;
     c.qi = q_idx; c.qv = q_val; c.kq = kq;
+    c.rmap = row_map; c.Lt = Lt;
     c.dr = draft_tokens + (int64_t)b * L; c.L = L; c.b = b; c.V = V; c.p = p;
     c.mode = effective_mode(p, b);
     c.mg = INFINITY;
@@ -928,8 +946,8 @@ int ssref_verify(const void *x, int dtype, int64_t ld_row, const float *draft_pr
                  int64_t ld_q, const int32_t *draft_tokens, int L, const ssref_params *p,
                  int32_t *out_tokens, int32_t *n_acc, int32_t *flags, double *margin,
                  int32_t *adm_seq, int32_t *adm_nacc, int32_t *n_adm, int nthreads) {
-  return verify_all(x, dtype, ld_row, draft_probs, ld_q, NULL, NULL, 0, draft_tokens, L, p, out_tokens,
-                    n_acc, flags, margin, adm_seq, adm_nacc, n_adm, nthreads);
+  return verify_all(x, dtype, ld_row, L + 1, NULL, draft_probs, ld_q, NULL, NULL, 0, draft_tokens, L, p,
+                    out_tokens, n_acc, flags, margin, adm_seq, adm_nacc, n_adm, nthreads);
 }
 
 /* Verification against sparse draft distributions: kq (id, probability)
@@ -939,8 +957,23 @@ int ssref_verify_sparse(const void *x, int dtype, int64_t ld_row, const int32_t 
                         int32_t *out_tokens, int32_t *n_acc, int32_t *flags, double *margin,
                         int32_t *adm_seq, int32_t *adm_nacc, int32_t *n_adm, int nthreads) {
   if (kq < 1) return -1;
-  return verify_all(x, dtype, ld_row, NULL, 0, q_idx, q_val, kq, draft_tokens, L, p, out_tokens, n_acc,
-                    flags, margin, adm_seq, adm_nacc, n_adm, nthreads);
+  return verify_all(x, dtype, ld_row, L + 1, NULL, NULL, 0, q_idx, q_val, kq, draft_tokens, L, p, out_tokens,
+                    n_acc, flags, margin, adm_seq, adm_nacc, n_adm, nthreads);
+}
+
+/* Verification of one path through a draft tree (draft-to-target mapping,
+ * Appendix C.4): the target computed Lt rows per request (x [B, Lt, ld_row]);
+ * path position l (0-based; l = L is the bonus position) is verified against
+ * target row row_map[b, l], an entry outside [0, Lt) giving a row with every
+ * token masked.  Draft lists are sparse (as ssref_verify_sparse); the
+ * penalty history and the grammar rows follow the path. */
+int ssref_verify_tree(const void *x, int dtype, int64_t ld_row, int Lt, const int32_t *row_map,
+                      const int32_t *q_idx, const float *q_val, int kq, const int32_t *draft_tokens, int L,
+                      const ssref_params *p, int32_t *out_tokens, int32_t *n_acc, int32_t *flags,
+                      double *margin, int32_t *adm_seq, int32_t *adm_nacc, int32_t *n_adm, int nthreads) {
+  if (kq < 1 || Lt < 1 || !row_map) return -1;
+  return verify_all(x, dtype, ld_row, Lt, row_map, NULL, 0, q_idx, q_val, kq, draft_tokens, L, p, out_tokens,
+                    n_acc, flags, margin, adm_seq, adm_nacc, n_adm, nthreads);
 }
 
 /* One row's truncated distribution, for pin tests: fills order[0..n_valid),

@@ -54,6 +54,10 @@ MUTANTS = [
      "    double sc = ((yr == M) ? 0.0 : (yr - M)) - (double)g[order[r]];", "test_gumbel_draw"),
     ("gumbel_noise_by_rank", "    double sc = ((yr == M) ? 0.0 : (yr - M) / tau) - (double)g[order[r]];",
      "    double sc = ((yr == M) ? 0.0 : (yr - M) / tau) - (double)g[r];", "test_gumbel_draw"),
+    ("tree_map_ignored", "    if (t >= 0 && t < c->Lt) src = (int64_t)c->b * c->Lt + t;",
+     "    if (t >= 0 && t < c->Lt) src = (int64_t)c->b * c->Lt + (l - 1);", "test_verify_tree_rows_are_selected"),
+    ("tree_request_stride_of_the_path", "    if (t >= 0 && t < c->Lt) src = (int64_t)c->b * c->Lt + t;",
+     "    if (t >= 0 && t < c->Lt) src = (int64_t)c->b * (c->L + 1) + t;", "test_verify_tree_rows_are_selected"),
     ("uniform_counter_words_swapped", "  uint32_t ctr[4] = {request, (uint32_t)((uint64_t)position & 0xFFFFFFFFu),",
      "  uint32_t ctr[4] = {(uint32_t)((uint64_t)position & 0xFFFFFFFFu), request,",
      "test_uniform_counter_words"),

@@ -586,6 +586,85 @@ def test_verify_sparse_unlisted_draft_is_accepted():
     assert np.all(o["n_acc"] == 0) and np.all(o["tokens"][:, 0] == order[1])
 
 
+def _tree_case(seed, B=24, L=3, V=48, kq=10):
+    """A path verification input (sparse lists, penalties, grammar rows per
+    path position) and the same path hidden in a larger tree of target rows."""
+    rng = np.random.default_rng(seed)
+    t = rng.normal(0, 1.5, (B, L + 1, V)).astype(np.float32)
+    idx = np.full((B, L, kq), -1, np.int32)
+    val = np.zeros((B, L, kq), np.float32)
+    d = np.empty((B, L), np.int64)
+    for b in range(B):
+        for l in range(L):
+            n = int(rng.integers(1, kq + 1))
+            ii = rng.choice(V, size=n, replace=False)
+            idx[b, l, :n], val[b, l, :n] = ii, rng.dirichlet(np.ones(n)).astype(np.float32)
+            d[b, l] = ii[0]
+    mode = np.where(np.arange(B) % 5 == 0, W.MODE_GREEDY | W.MODE_REP | W.MODE_GRAMMAR,
+                    W.MODE_TEMP | W.MODE_TOPP | W.MODE_REP | W.MODE_GRAMMAR)
+    hist = np.zeros(B + 1, np.int32)
+    inp = _verify_inputs(t, np.zeros((B, L, V)), d, mode, L, temperature=np.full(B, 0.9),
+                         top_p=np.full(B, 0.9), rep=np.full(B, 1.4), position=np.arange(B) * 7,
+                         hist_offsets=hist)
+    mask = np.zeros((B * (L + 1), (V + 31) // 32), np.uint32)
+    for r in range(B * (L + 1)):
+        for i in rng.choice(V, V // 2, replace=False):
+            mask[r, i >> 5] |= np.uint32(1 << (int(i) & 31))
+        for i in idx.reshape(B, L * kq)[r // (L + 1)]:  # keep most listed drafts allowed
+            if i >= 0 and rng.random() < 0.8:
+                mask[r, i >> 5] |= np.uint32(1 << (int(i) & 31))
+    inp["bitmask"] = mask
+    inp["mode"] = mode.astype(np.uint32)
+    inp = _sparse(inp, idx, val)
+    # the tree: Lt = 2 (L + 1) + 1 rows per request, the path's rows at random
+    # places, the others distractors
+    Lt = 2 * (L + 1) + 1
+    tree = rng.normal(0, 1.5, (B, Lt, V)).astype(np.float32)
+    rmap = np.stack([rng.choice(Lt, L + 1, replace=False) for _ in range(B)]).astype(np.int32)
+    for b in range(B):
+        tree[b, rmap[b]] = t[b]
+    tinp = dict(inp, x=tree, row_map=rmap)
+    return inp, tinp
+
+
+def test_verify_tree_rows_are_selected_by_the_map():
+    # a path hidden among distractor rows gives the outcomes of the path alone
+    for seed in (1, 2):
+        inp, tinp = _tree_case(seed)
+        a, t_ = oracle.verify(inp), oracle.verify(tinp)
+        for k in ("tokens", "n_acc", "adm_tokens", "adm_nacc", "n_adm", "flags"):
+            assert np.array_equal(a[k], t_[k]), (seed, k)
+        assert a["n_acc"].max() >= 1  # some paths go past the first position
+
+
+def test_verify_tree_identity_map_is_the_path():
+    inp, _ = _tree_case(3)
+    L = int(inp["L"])
+    a = oracle.verify(inp)
+    b = oracle.verify(dict(inp, row_map=np.tile(np.arange(L + 1, dtype=np.int32), (inp["B"], 1))))
+    for k in ("tokens", "n_acc", "adm_tokens", "n_adm"):
+        assert np.array_equal(a[k], b[k]), k
+
+
+def test_verify_tree_entry_outside_the_tree_masks_its_row():
+    # greedy requests whose first draft is the argmax of their first row: an
+    # entry outside [0, Lt) at position 0 rejects at once with no correction;
+    # at position 1 it accepts the first draft, then emits nothing
+    V, L, B = 16, 2, 4
+    rng = np.random.default_rng(9)
+    t = rng.normal(0, 1, (B, L + 1, V)).astype(np.float32)
+    d = np.stack([[int(np.argmax(t[b, 0])), int(np.argmax(t[b, 1]))] for b in range(B)])
+    inp = _verify_inputs(t, np.zeros((B, L, V)), d, np.full(B, W.MODE_GREEDY), L)
+    inp = _sparse(inp, np.full((B, L, 1), -1, np.int32), np.zeros((B, L, 1), np.float32))
+    rmap = np.tile(np.arange(L + 1, dtype=np.int32), (B, 1))
+    rmap[0, 0], rmap[1, 0], rmap[2, 1], rmap[3, 1] = -1, L + 1, L + 1, -5
+    o = oracle.verify(dict(inp, row_map=rmap))
+    assert list(o["n_acc"]) == [0, 0, 1, 1]
+    assert np.all(o["tokens"][:2] == -1)
+    assert np.array_equal(o["tokens"][2:, 0], d[2:, 0]) and np.all(o["tokens"][2:, 1:] == -1)
+    assert np.all(o["flags"] & 1)  # SS_FLAG_EMPTY
+
+
 def test_process_logits_distribution_sums_to_one():
     inp = W.config0()
     out = oracle.process_logits(inp)
