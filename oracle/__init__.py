@@ -159,6 +159,27 @@ def sample(inp, nthreads=0):
     return dict(token=tok, logprob=lp, flags=fl, margin=mg, n_kept=nk, adm_token=at, adm_logprob=al, n_adm=na)
 
 
+def sample_full(inp, nthreads=0):
+    """Sampling with full-row truncation for requests without a top-k cut
+    (top-p / min-p over the whole row when the kept set fits ``k_max``, else
+    the bounded result flagged KCAP).  Returns the keys of ``sample`` except
+    ``margin``."""
+    B, V = int(inp["B"]), int(inp["V"])
+    A = adm_max()
+    x = _x(inp)
+    bd = _Bundle(inp)
+    tok = np.empty(B, np.int32)
+    lp = np.empty(B, np.float32)
+    fl = np.empty(B, np.int32)
+    nk = np.empty(B, np.int32)
+    at = np.empty((B, A), np.int32)
+    al = np.empty((B, A), np.float32)
+    na = np.empty(B, np.int32)
+    lib().ssref_sample_full(_ptr(x), C.c_int(_dtype_code(inp)), C.c_int64(V), C.byref(bd.p), _ptr(tok), _ptr(lp),
+                            _ptr(fl), _ptr(nk), _ptr(at), _ptr(al), _ptr(na), C.c_int(nthreads))
+    return dict(token=tok, logprob=lp, flags=fl, n_kept=nk, adm_token=at, adm_logprob=al, n_adm=na)
+
+
 def sample_gumbel(inp, noise, nthreads=0):
     """Singular-mode sampling with the Gumbel-max draw: ``noise`` float32
     [B, V] holds g = ln z (z ~ Exp(1)) per token.  Returns the keys of

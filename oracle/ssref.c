@@ -17,7 +17,11 @@
  *     index win ties);
  *   - truncation in Alg. 11 order (top-k, then top-p on the top-k-renormalised
  *     distribution, then min-p in the logit domain, eq. "min_p_trick",
- *     Appendix C.2), temperature entering only the probabilities;
+ *     Appendix C.2), temperature entering only the probabilities; requests
+ *     without a top-k cut either bounded to the k_cap leading tokens
+ *     (Section 3.3's bounded candidate set) or, in the full-row form, with
+ *     top-p over the whole row's distribution (Appendix C.2) whenever the
+ *     kept set fits the bound;
  *   - categorical selection by inverse CDF over the kept prefix, with a
  *     uniform from Philox4x32-10 keyed by (seed, request, position); or by
  *     Gumbel-max over the kept set with caller-drawn noise g = ln z,
@@ -580,6 +584,106 @@ int ssref_sample_gumbel(const void *x, int dtype, int64_t ld, const ssref_params
     }
     if (n_adm) n_adm[b] = na;
     free(y); free(order); free(w);
+  }
+  return 0;
+}
+
+/* Sampling with full-row truncation for requests without a top-k cut (top-k
+ * bit off or k <= 0; not greedy): top-p and min-p over every valid token of
+ * the row (the Appendix C.2 definitions), used when the kept set fits the
+ * candidate bound, i.e. when it holds fewer than k_cap tokens or every valid
+ * token; otherwise the bounded result of ssref_sample with RF_KCAP.  Other
+ * requests are sampled exactly as by ssref_sample.  Outputs as ssref_sample;
+ * the admissible outcomes cover both sides of the fit test when a kept-set
+ * size within the band changes it. */
+static int full_fits(int ns, int n_valid, int k_cap) { return ns < k_cap || n_valid <= k_cap; }
+
+/* adds the admissible draws over w[0..ns) to the outcome list (no duplicates) */
+static void add_draws(const double *w, int ns, const int32_t *order, double u, int32_t *at, float *al, int *na) {
+  double Z = prefix_sum(w, ns);
+  int ranks[SSREF_ADM];
+  int nr = draw_admissible(w, ns, Z, u, SSREF_NEAR * Z, ranks, SSREF_ADM);
+  for (int j = 0; j < nr && *na < SSREF_ADM; ++j) {
+    int32_t t = order[ranks[j]];
+    float l = (float)log(w[ranks[j]] / Z);
+    int dup = 0;
+    for (int e = 0; e < *na; ++e) dup |= (at[e] == t && al[e] == l);
+    if (!dup) { at[*na] = t; al[*na] = l; ++*na; }
+  }
+}
+
+int ssref_sample_full(const void *x, int dtype, int64_t ld, const ssref_params *p, int32_t *out_token,
+                      float *out_logprob, int32_t *flags, int32_t *n_kept, int32_t *adm_tok, float *adm_lp,
+                      int32_t *n_adm, int nthreads) {
+  int B = p->B, V = p->V;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+#endif
+  for (int b = 0; b < B; ++b) {
+    float *y = (float *)malloc(sizeof(float) * (size_t)V);
+    int32_t *order = (int32_t *)malloc(sizeof(int32_t) * (size_t)V);
+    double *wf = (double *)malloc(sizeof(double) * (size_t)V + 8);
+    double *wb = (double *)malloc(sizeof(double) * (size_t)(p->k_cap > 0 ? p->k_cap : 1) + 8);
+    process_one(x, dtype, (int64_t)b * ld, p, b, NULL, 0, b, y);
+    int nv = ssref_order(y, V, order);
+    uint32_t mode = effective_mode(p, b);
+    const float tmp = pf(p->temperature, b, 1.0f), tp = pf(p->top_p, b, 1.0f), mp = pf(p->min_p, b, 0.0f);
+    const int32_t tk = p->top_k ? p->top_k[b] : 0;
+    const int cap = p->k_cap;
+    dist_t db, df;
+    row_distribution(y, order, nv, mode, tmp, tk, tp, mp, cap, wb, &db);
+    const int full = nv > 0 && !db.greedy && !((mode & R_TOPK) && tk >= 1);
+    if (full) row_distribution(y, order, nv, mode, tmp, tk, tp, mp, nv, wf, &df);
+    int tok = -1, ns_own = db.n_s, fl = db.flags;
+    float lp = 0.0f;
+    int32_t at[SSREF_ADM];
+    float al[SSREF_ADM];
+    int na = 0;
+    if (nv > 0 && db.greedy) {
+      tok = order[0];
+    } else if (nv > 0) {
+      const double u = ssref_uniform(p->seed[b], (uint32_t)b, p->position[b], 0);
+      const int own_full = full && full_fits(df.n_s, nv, cap);
+      const double *wo = own_full ? wf : wb;
+      const int no = own_full ? df.n_s : db.n_s;
+      const double Zo = prefix_sum(wo, no);
+      const int r = draw_index(wo, no, Zo, u, NULL);
+      tok = order[r];
+      lp = (float)log(wo[r] / Zo);
+      ns_own = no;
+      if (full) fl = (df.flags & ~RF_KCAP) | (own_full ? 0 : RF_KCAP);
+      at[na] = tok; al[na] = lp; ++na;
+      /* every admissible kept-set size (the own one first): a full-row size
+       * that fits gives its own draws, one that does not gives the bounded
+       * distribution's */
+      const dist_t *d0 = full ? &df : &db;
+      for (int pass = 0; pass < 2; ++pass) {
+        for (int m = d0->ns_lo; m <= d0->ns_hi; ++m) {
+          if ((pass == 0) != (m == d0->n_s)) continue;
+          if (full && full_fits(m, nv, cap)) {
+            add_draws(wf, m, order, u, at, al, &na);
+          } else {
+            for (int q = 0; q < 2; ++q)
+              for (int nb = db.ns_lo; nb <= db.ns_hi; ++nb)
+                if ((q == 0) == (nb == db.n_s)) add_draws(wb, nb, order, u, at, al, &na);
+          }
+        }
+      }
+    }
+    out_token[b] = tok;
+    if (out_logprob) out_logprob[b] = lp;
+    if (flags) flags[b] = fl;
+    if (n_kept) n_kept[b] = ns_own;
+    if (na == 0) { at[0] = tok; al[0] = lp; na = 1; }
+    if (adm_tok) {
+      for (int e = 0; e < SSREF_ADM; ++e) {
+        adm_tok[(int64_t)b * SSREF_ADM + e] = e < na ? at[e] : -1;
+        if (adm_lp) adm_lp[(int64_t)b * SSREF_ADM + e] = e < na ? al[e] : 0.0f;
+      }
+    }
+    if (n_adm) n_adm[b] = na;
+    free(y); free(order); free(wf); free(wb);
   }
   return 0;
 }

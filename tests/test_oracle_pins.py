@@ -299,6 +299,101 @@ def test_sampling_distribution_chi_square():
 
 
 # --------------------------------------------------------------------------
+# Full-row truncation for requests without a top-k cut (Appendix C.2)
+# --------------------------------------------------------------------------
+def _full_rows(y, k_max, mode, **params):
+    B = y.shape[0]
+    return W.custom_rows(y, W.F32, k_max=k_max, mode=np.full(B, mode), position=np.arange(B) * 3, **params)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_full_row_top_p_uses_the_whole_row(seed):
+    # a head plus a long tail: the top-p cut over the whole row (scipy softmax
+    # over every token) lies inside k_max but differs from the cut over the
+    # k_max leading tokens; the kept set and the drawn token's probability
+    # follow the whole-row rule
+    rng = np.random.default_rng(300 + seed)
+    V, k_max, B, p, tau = 600, 64, 16, 0.8, np.float32(0.9)
+    y = rng.normal(0, 0.3, (B, V)).astype(np.float32)
+    y[:, rng.choice(V, 12, replace=False)] += rng.uniform(5.0, 6.0, 12).astype(np.float32)
+    mode = W.MODE_TEMP | W.MODE_TOPP
+    inp = _full_rows(y, k_max, mode, temperature=np.full(B, tau), top_p=np.full(B, p))
+    o = oracle.sample_full(inp)
+    ob = oracle.sample(inp)
+    differ = 0
+    for b in range(B):
+        order, sp = _softmax_sorted(y[b], tau)
+        n = int(np.searchsorted(np.cumsum(sp), p) + 1)
+        assert n < k_max
+        assert o["n_kept"][b] == n
+        kept = sp[:n] / sp[:n].sum()
+        r = int(np.nonzero(order == o["token"][b])[0][0])
+        assert r < n and abs(float(o["logprob"][b]) - math.log(kept[r])) < 1e-6
+        assert (o["flags"][b] & 8) == 0  # not bounded
+        differ += int(o["n_kept"][b] != ob["n_kept"][b])
+    assert differ > 0
+
+
+def test_full_row_overflow_falls_back_to_the_bounded_result():
+    # a flat row keeps ~90 % of 500 tokens under top-p 0.9: more than k_max,
+    # so the result is ssref_sample's (top-p over the k_max leading tokens) with
+    # the KCAP flag; the same at a kept set of exactly k_max tokens
+    V, k_max, B = 500, 64, 6
+    y = np.zeros((B, V), np.float32)
+    inp = _full_rows(y, k_max, W.MODE_TOPP, top_p=np.full(B, 0.9))
+    o, ob = oracle.sample_full(inp), oracle.sample(inp)
+    assert np.array_equal(o["token"], ob["token"]) and np.array_equal(o["n_kept"], ob["n_kept"])
+    assert np.all(o["flags"] & 8)
+    # min-p keeping exactly k_max tokens of a row longer than k_max: overflow
+    y2 = np.full((B, V), -10.0, np.float32)
+    y2[:, :k_max] = 0.0
+    inp2 = _full_rows(y2, k_max, W.MODE_MINP, min_p=np.full(B, 0.5))
+    o2 = oracle.sample_full(inp2)
+    assert np.all(o2["flags"] & 8) and np.all(o2["n_kept"] == k_max)
+    # one token fewer fits: the whole-row result without the flag
+    y3 = y2.copy()
+    y3[:, k_max - 1] = -10.0
+    o3 = oracle.sample_full(_full_rows(y3, k_max, W.MODE_MINP, min_p=np.full(B, 0.5)))
+    assert np.all((o3["flags"] & 8) == 0) and np.all(o3["n_kept"] == k_max - 1)
+    # a row with no more valid tokens than k_max always fits
+    o4 = oracle.sample_full(_full_rows(np.zeros((B, 50), np.float32), k_max, W.MODE_TEMP))
+    assert np.all((o4["flags"] & 8) == 0) and np.all(o4["n_kept"] == 50)
+
+
+def test_full_row_leaves_other_requests_alone():
+    # top-k requests (k <= k_max and k > k_max) and greedy ones are sampled as by ssref_sample
+    rng = np.random.default_rng(12)
+    V, B = 300, 12
+    y = rng.normal(0, 1, (B, V)).astype(np.float32)
+    mode = np.full(B, W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP, np.uint32)
+    mode[::4] = W.MODE_GREEDY
+    inp = W.custom_rows(y, W.F32, k_max=64, mode=mode, temperature=np.full(B, 0.8),
+                        top_k=np.where(np.arange(B) % 3 == 0, 200, 20), top_p=np.full(B, 0.95),
+                        position=np.arange(B))
+    o, ob = oracle.sample_full(inp), oracle.sample(inp)
+    for k in ("token", "logprob", "flags", "n_kept"):
+        assert np.array_equal(o[k], ob[k]), k
+
+
+def test_full_row_draws_follow_the_whole_row_distribution_chi_square():
+    V, B, p = 40, 40000, 0.9
+    rng = np.random.default_rng(23)
+    yv = rng.normal(0, 1.2, V).astype(np.float32)
+    inp = W.custom_rows(np.tile(yv, (B, 1)), W.F32, k_max=32, mode=np.full(B, W.MODE_TOPP),
+                        top_p=np.full(B, p), position=np.arange(B))
+    o = oracle.sample_full(inp)
+    order, sp = _softmax_sorted(yv, np.float32(1.0))
+    n = int(np.searchsorted(np.cumsum(sp), p) + 1)
+    assert n < 32 and np.all(o["n_kept"] == n)
+    probs = np.zeros(V)
+    probs[order[:n]] = sp[:n] / sp[:n].sum()
+    counts = np.bincount(o["token"], minlength=V).astype(np.float64)
+    assert counts[probs == 0].sum() == 0
+    ok, pv = _chi2_ok(counts[probs > 0], probs[probs > 0])
+    assert ok, pv
+
+
+# --------------------------------------------------------------------------
 # Gumbel-max draw (Appendix C.3)
 # --------------------------------------------------------------------------
 def test_gumbel_draw_follows_truncated_distribution_chi_square():
