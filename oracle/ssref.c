@@ -591,12 +591,13 @@ int ssref_sample_gumbel(const void *x, int dtype, int64_t ld, const ssref_params
 /* Sampling with full-row truncation for requests without a top-k cut (top-k
  * bit off or k <= 0; not greedy): top-p and min-p over every valid token of
  * the row (the Appendix C.2 definitions), used when the kept set fits the
- * candidate bound, i.e. when it holds fewer than k_cap tokens or every valid
- * token; otherwise the bounded result of ssref_sample with RF_KCAP.  Other
+ * candidate bound, i.e. holds fewer than k_cap tokens; otherwise the bounded
+ * result of ssref_sample with RF_KCAP (the same tokens when the row has at
+ * most k_cap valid tokens: the bounded set is then the whole row).  Other
  * requests are sampled exactly as by ssref_sample.  Outputs as ssref_sample;
  * the admissible outcomes cover both sides of the fit test when a kept-set
  * size within the band changes it. */
-static int full_fits(int ns, int n_valid, int k_cap) { return ns < k_cap || n_valid <= k_cap; }
+static int full_fits(int ns, int k_cap) { return ns < k_cap; }
 
 /* adds the admissible draws over w[0..ns) to the outcome list (no duplicates) */
 static void add_draws(const double *w, int ns, const int32_t *order, double u, int32_t *at, float *al, int *na) {
@@ -644,7 +645,7 @@ int ssref_sample_full(const void *x, int dtype, int64_t ld, const ssref_params *
       tok = order[0];
     } else if (nv > 0) {
       const double u = ssref_uniform(p->seed[b], (uint32_t)b, p->position[b], 0);
-      const int own_full = full && full_fits(df.n_s, nv, cap);
+      const int own_full = full && full_fits(df.n_s, cap);
       const double *wo = own_full ? wf : wb;
       const int no = own_full ? df.n_s : db.n_s;
       const double Zo = prefix_sum(wo, no);
@@ -661,7 +662,7 @@ int ssref_sample_full(const void *x, int dtype, int64_t ld, const ssref_params *
       for (int pass = 0; pass < 2; ++pass) {
         for (int m = d0->ns_lo; m <= d0->ns_hi; ++m) {
           if ((pass == 0) != (m == d0->n_s)) continue;
-          if (full && full_fits(m, nv, cap)) {
+          if (full && full_fits(m, cap)) {
             add_draws(wf, m, order, u, at, al, &na);
           } else {
             for (int q = 0; q < 2; ++q)

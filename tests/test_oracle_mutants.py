@@ -61,8 +61,8 @@ MUTANTS = [
     ("full_row_uses_bounded_normaliser", "    if (full) row_distribution(y, order, nv, mode, tmp, tk, tp, mp, nv, wf, &df);",
      "    if (full) row_distribution(y, order, nv, mode, tmp, tk, tp, mp, cap, wf, &df);",
      "test_full_row_top_p_uses_the_whole_row"),
-    ("full_row_fit_test_inclusive", "static int full_fits(int ns, int n_valid, int k_cap) { return ns < k_cap || n_valid <= k_cap; }",
-     "static int full_fits(int ns, int n_valid, int k_cap) { return ns <= k_cap || n_valid <= k_cap; }",
+    ("full_row_fit_test_inclusive", "static int full_fits(int ns, int k_cap) { return ns < k_cap; }",
+     "static int full_fits(int ns, int k_cap) { return ns <= k_cap; }",
      "test_full_row_overflow_falls_back"),
     ("uniform_counter_words_swapped", "  uint32_t ctr[4] = {request, (uint32_t)((uint64_t)position & 0xFFFFFFFFu),",
      "  uint32_t ctr[4] = {(uint32_t)((uint64_t)position & 0xFFFFFFFFu), request,",

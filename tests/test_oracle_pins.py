@@ -355,9 +355,12 @@ def test_full_row_overflow_falls_back_to_the_bounded_result():
     y3[:, k_max - 1] = -10.0
     o3 = oracle.sample_full(_full_rows(y3, k_max, W.MODE_MINP, min_p=np.full(B, 0.5)))
     assert np.all((o3["flags"] & 8) == 0) and np.all(o3["n_kept"] == k_max - 1)
-    # a row with no more valid tokens than k_max always fits
+    # a row with fewer valid tokens than k_max always fits; one with exactly
+    # k_max keeps them all too, with the flag (its bounded set is the row)
     o4 = oracle.sample_full(_full_rows(np.zeros((B, 50), np.float32), k_max, W.MODE_TEMP))
     assert np.all((o4["flags"] & 8) == 0) and np.all(o4["n_kept"] == 50)
+    o5 = oracle.sample_full(_full_rows(np.zeros((B, k_max), np.float32), k_max, W.MODE_TEMP))
+    assert np.all(o5["flags"] & 8) and np.all(o5["n_kept"] == k_max)
 
 
 def test_full_row_leaves_other_requests_alone():
