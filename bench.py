@@ -56,7 +56,7 @@ MALL_BYTES = 256 << 20
 CONFIGS = ("cfg0", "cfg1", "cfg2", "cfg3", "cfg4")
 # a stress line beside the five workloads: the headline batch with every
 # logit of a row equal (the paper's tied correctness inputs at full size)
-EXTRA = ("cfg1_tied", "cfg1_logprobs", "cfg4_sparse", "cfg1_gumbel")
+EXTRA = ("cfg1_tied", "cfg1_logprobs", "cfg4_sparse", "cfg4_tree", "cfg1_gumbel")
 LOGPROBS_N = 20  # log-probabilities per request on the log-probability line
 MODE_TOPK = 0x080  # the top-k indicator bit (bit-level encoding table, Section 3.5)
 WORKLOAD = {
@@ -74,6 +74,8 @@ WORKLOAD = {
                      "bf16, penalties, bias), every request with bit 0x400",
     "cfg1_gumbel": "the heterogeneous singular batch (B=64 V=131072 bf16) sampled with the Gumbel-max draw "
                    "(ss_sample_gumbel, noise [B, V] fp32 read at the kept ids)",
+    "cfg4_tree": "tree-path verification (ss_verify_tree): the sparse-list verification batch (B=64 L=4 V=131072 "
+                 "bf16) with each request's 5 path rows among 9 target rows of a draft tree",
     "cfg4_sparse": "multistep verification against sparse draft lists (ss_verify_sparse): B=64 L=4 V=131072 "
                    "bf16 target, at most 64 (id, q) pairs per draft position",
 }
@@ -83,6 +85,8 @@ def make_input(name, W):
     """The named workload's seeded synthetic input."""
     if name == "cfg1_gumbel":
         return W.make_config("cfg1")
+    if name == "cfg4_tree":
+        return W.tree_from_path(W.make_config("cfg4_sparse"), 9, 4242)
     if name == "cfg1_logprobs":
         inp = W.make_config("cfg1")
         inp["mode"] = inp["mode"] | np.uint32(W.MODE_LOGPROBS)
@@ -121,8 +125,11 @@ def algorithmic_bytes(name, inp):
     if name == "cfg4":
         L = int(inp["L"])
         return b + _nbytes(inp["draft_tokens"]) + B * L * (inp["k_max"] + 1) * 4 + B * (L + 2) * 4
-    if name == "cfg4_sparse":  # the sparse lists are read whole
+    if name in ("cfg4_sparse", "cfg4_tree"):  # the sparse lists are read whole
         L = int(inp["L"])
+        if name == "cfg4_tree":  # only the path's rows of the tree are read, plus the map
+            xb = _nbytes(inp["x"])
+            b += _nbytes(inp["row_map"]) - xb + xb * (L + 1) // np.asarray(inp["x"]).shape[1]
         return (b + _nbytes(inp["draft_tokens"]) + _nbytes(inp["draft_idx"]) + _nbytes(inp["draft_q"])
                 + B * (L + 2) * 4)
     return b + 12 * B  # token, log-probability, flags
@@ -299,6 +306,22 @@ class Runner:
 
             def step(i):
                 ssb.logprobs(self.xs[i % self.R], prm, LOGPROBS_N, out_idx=oi, out_lp=ol, flags=fl, ws=ws)
+        elif name == "cfg4_tree":
+            L = inp["L"]
+            rm = t.from_numpy(np.ascontiguousarray(inp["row_map"], np.int32)).to(dev)
+            qi = t.from_numpy(np.ascontiguousarray(inp["draft_idx"], np.int32)).to(dev)
+            qv = t.from_numpy(np.ascontiguousarray(inp["draft_q"], np.float32)).to(dev)
+            d = t.from_numpy(np.ascontiguousarray(inp["draft_tokens"], np.int32)).to(dev)
+            prm = ssb.Params.from_arrays(inp, dev)
+            ws = ssb.workspace(ssb.OP_VERIFY, inp["B"], inp["V"], L, inp["k_max"], ssb.BF16, dev)
+            out = t.empty(inp["B"], L + 1, dtype=t.int32, device=dev)
+            na = t.empty(inp["B"], dtype=t.int32, device=dev)
+            fl = t.empty(inp["B"], dtype=t.int32, device=dev)
+            self.rows_per_step = inp["B"] * (L + 1)
+
+            def step(i):
+                ssb.verify_tree(self.xs[i % self.R], rm, qi, qv, d, prm, inp["k_max"], out_tokens=out, out_nacc=na,
+                                flags=fl, ws=ws)
         elif name == "cfg4_sparse":
             L = inp["L"]
             qi = t.from_numpy(np.ascontiguousarray(inp["draft_idx"], np.int32)).to(dev)
@@ -449,7 +472,7 @@ def config_entry(name, run, us):
     fb = int(((run.flags.cpu().numpy() & 2) > 0).sum())
     e = dict(workload=WORKLOAD[name], us_per_batch=us, rows_per_s=run.rows_per_step / (us * 1e-6),
              alg_bytes=alg, GBps=gbps, frac=gbps / HBM_PEAK_GBS, rotated_buffers=run.R, fallback_rows=fb)
-    if name in ("cfg4", "cfg4_sparse"):
+    if name in ("cfg4", "cfg4_sparse", "cfg4_tree"):
         e["requests_per_s"] = run.B / (us * 1e-6)
     prof = load_profile(name)
     if prof:
@@ -545,7 +568,7 @@ def main():
     }
     if head in ("cfg1", "cfg2") and not args.read_probe:  # counter runs keep the probe the only plain read
         res["read_ceiling"] = read_ceiling(torch, h["alg_bytes"])
-    if not args.no_cpu and head not in ("cfg2", "cfg4", "cfg4_sparse"):
+    if not args.no_cpu and head not in ("cfg2", "cfg4", "cfg4_sparse", "cfg4_tree"):
         nthreads = os.cpu_count() or 1
         omp = os.environ.get("OMP_NUM_THREADS")
         if omp and omp.isdigit():

@@ -9,7 +9,8 @@ from .workloads import (  # noqa: F401
     MODE_GREEDY, MODE_TOPK, MODE_TOPP, MODE_MINP, MODE_LOGPROBS,
     F32, BF16,
     bf16_bits_from_f32, f32_from_bf16_bits,
-    config0, config1, config2, config3, config4, config4_sparse, sparse_drafts, gumbel_noise, make_config,
+    config0, config1, config2, config3, config4, config4_sparse, sparse_drafts, gumbel_noise, tree_from_path,
+    make_config,
     CONFIG_NAMES,
     custom_rows, empty_params,
 )

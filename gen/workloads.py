@@ -262,6 +262,25 @@ def config4_sparse(B: int = 64, L: int = 4, kq: int = 64) -> dict:
                 draft_idx=idx, draft_q=qv, draft_tokens=d, **p)
 
 
+def tree_from_path(inp: dict, Lt: int, seed: int) -> dict:
+    """A draft tree holding a verification input's path: ``x`` becomes
+    ``[B, Lt, V]`` with the path's L+1 target rows at distinct random rows of
+    each request and N(0, 2) distractor rows elsewhere; ``row_map`` [B, L+1]
+    names the path's rows.  Everything else is the path input's."""
+    x = np.asarray(inp["x"])
+    B, L1, V = x.shape
+    assert Lt >= L1
+    rng = np.random.default_rng(seed)
+    noise = rng.normal(0.0, 2.0, size=(B, Lt, V)).astype(np.float32)
+    tree = bf16_bits_from_f32(noise) if inp["dtype"] == BF16 else noise
+    rmap = np.stack([rng.choice(Lt, L1, replace=False) for _ in range(B)]).astype(np.int32)
+    for b in range(B):
+        tree[b, rmap[b]] = x[b]
+    out = dict(inp, x=tree, row_map=rmap)
+    out["name"] = str(inp.get("name", "custom")) + "_tree"
+    return out
+
+
 def gumbel_noise(B: int, V: int, seed: int) -> np.ndarray:
     """Pre-drawn noise for the Gumbel-max draw: g = ln z, z ~ Exp(1), float32
     ``[B, V]`` (one value per token; the draw subtracts it at the kept ids)."""

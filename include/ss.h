@@ -13,6 +13,8 @@
  *   ss_verify_sparse   the same against sparse draft distributions: the
  *                      (id, probability) lists a singular-mode draft step
  *                      emits over its candidate set (Section 3.2)
+ *   ss_verify_tree     one path through a draft tree, its positions mapped to
+ *                      the target rows of the tree (Appendix C.4)
  *   ss_topk            exact top-k (value, index) per row (Section 3.4)
  *   ss_process_logits  materialised processed logits and final probabilities
  *   ss_logprobs        top-k log-probabilities under the full-row distribution
@@ -230,6 +232,27 @@ ss_status ss_verify_sparse(const void *target_logits, int dtype, int64_t ld_row,
                            const float *draft_q, int kq, const int32_t *draft_tokens, int L,
                            const ss_params *p, int k_max, int32_t *out_tokens, int32_t *out_num_accepted,
                            int32_t *flags, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Verification of one path through a draft tree (the draft-to-target mapping
+ * of Appendix C.4, as tree speculation needs): the target evaluated Lt rows
+ * per request for the tree's nodes, and path position l (0-based, l = L being
+ * the bonus / correction position after L acceptances) is verified against
+ * target row row_map[b, l].  A map entry outside [0, Lt) gives a target row
+ * with every token masked (SS_FLAG_EMPTY: the path ends there with no
+ * correction token).  Draft lists are sparse, as for ss_verify_sparse.  The
+ * penalty history, the grammar rows (bitmask rows B*(L+1), one per path
+ * position), the uniforms and the outputs follow the path, as for ss_verify.
+ *   target_logits  [B, Lt, V] rows of `dtype`, row stride ld_row (request b's
+ *                  row t at (b*Lt + t) * ld_row).
+ *   Lt             target rows per request, >= 1.
+ *   row_map        int32[B, L+1].
+ *   ws             ss_workspace_bytes(SS_OP_VERIFY, B, V, L, k_max, dtype) bytes.
+ */
+ss_status ss_verify_tree(const void *target_logits, int dtype, int64_t ld_row, int Lt, const int32_t *row_map,
+                         const int32_t *draft_idx, const float *draft_q, int kq, const int32_t *draft_tokens,
+                         int L, const ss_params *p, int k_max, int32_t *out_tokens, int32_t *out_num_accepted,
+                         int32_t *flags, void *ws, size_t ws_bytes, void *stream);
 
 /*
  * Materialised pipeline (unfused reference path).

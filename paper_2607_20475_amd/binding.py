@@ -71,6 +71,10 @@ def lib():
         L.ss_verify.restype = i32
         L.ss_verify.argtypes = [vp, C.c_int, i64, vp, i64, vp, C.c_int, C.POINTER(_Params), C.c_int, vp, vp,
                                 vp, vp, sz, vp]
+        if hasattr(L, "ss_verify_tree"):
+            L.ss_verify_tree.restype = i32
+            L.ss_verify_tree.argtypes = [vp, C.c_int, i64, C.c_int, vp, vp, vp, C.c_int, vp, C.c_int,
+                                         C.POINTER(_Params), C.c_int, vp, vp, vp, vp, sz, vp]
         if hasattr(L, "ss_verify_sparse"):
             L.ss_verify_sparse.restype = i32
             L.ss_verify_sparse.argtypes = [vp, C.c_int, i64, vp, vp, C.c_int, vp, C.c_int, C.POINTER(_Params),
@@ -319,6 +323,37 @@ def verify_sparse(target_logits, draft_idx, draft_q, draft_tokens, params, k_max
     _check(lib().ss_verify_sparse(_ptr(target_logits), dt, target_logits.stride(1), _ptr(draft_idx), _ptr(draft_q),
                                   kq, _ptr(draft_tokens), L, C.byref(p), k_max, _ptr(out_tokens), _ptr(out_nacc),
                                   _ptr(flags), _ptr(ws), ws.numel(), _stream()))
+    return out_tokens, out_nacc, flags
+
+
+def verify_tree(target_logits, row_map, draft_idx, draft_q, draft_tokens, params, k_max, out_tokens=None,
+                out_nacc=None, flags=None, ws=None):
+    """target_logits [B, Lt, V] (a draft tree's target rows); row_map int32
+    [B, L+1] (path position -> row); draft_idx int32 / draft_q float32
+    [B, L, kq]; draft_tokens [B, L] int32."""
+    B, Lt, V = target_logits.shape
+    L = row_map.shape[1] - 1
+    kq = draft_idx.shape[-1]
+    dt = _dtype_code(target_logits)
+    dev = target_logits.device
+    ws = _ws(ws, OP_VERIFY, B, V, L, k_max, dt, dev)
+    if out_tokens is None:
+        out_tokens = torch.empty(B, L + 1, dtype=torch.int32, device=dev)
+    if out_nacc is None:
+        out_nacc = torch.empty(B, dtype=torch.int32, device=dev)
+    if flags is None:
+        flags = torch.empty(B, dtype=torch.int32, device=dev)
+    if target_logits.stride(0) != Lt * target_logits.stride(1):
+        raise SSError("target rows must be evenly strided")
+    if row_map.shape != (B, L + 1) or row_map.dtype != torch.int32 or not row_map.is_contiguous():
+        raise SSError("row_map must be contiguous int32 [B, L+1]")
+    for t, dtype in ((draft_idx, torch.int32), (draft_q, torch.float32)):
+        if t.shape != (B, L, kq) or t.dtype != dtype or not t.is_contiguous():
+            raise SSError("draft lists must be contiguous [B, L, kq] int32 ids and float32 probabilities")
+    p = params.struct()
+    _check(lib().ss_verify_tree(_ptr(target_logits), dt, target_logits.stride(1), Lt, _ptr(row_map), _ptr(draft_idx),
+                                _ptr(draft_q), kq, _ptr(draft_tokens), L, C.byref(p), k_max, _ptr(out_tokens),
+                                _ptr(out_nacc), _ptr(flags), _ptr(ws), ws.numel(), _stream()))
     return out_tokens, out_nacc, flags
 
 

@@ -324,8 +324,8 @@ ss_status ss_sample_gumbel(const void* logits, int dtype, int64_t ld, const ss_p
                     flags, ws, ws_bytes, stream);
 }
 
-static ss_status verify_any(const void* target_logits, int dtype, int64_t ld_row, const float* draft_probs,
-                            int64_t ld_q, const int32_t* q_idx, const float* q_val, int kq,
+static ss_status verify_any(const void* target_logits, int dtype, int64_t ld_row, int Lt, const int32_t* row_map,
+                            const float* draft_probs, int64_t ld_q, const int32_t* q_idx, const float* q_val, int kq,
                             const int32_t* draft_tokens, int L, const ss_params* p, int k_max, int32_t* out_tokens,
                             int32_t* out_num_accepted, int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
   if (!target_logits || !p || !draft_tokens || !out_tokens || !out_num_accepted || !ws) return SS_ERR_INVALID_ARG;
@@ -334,6 +334,7 @@ static ss_status verify_any(const void* target_logits, int dtype, int64_t ld_row
   if (ld_row < V || !params_ok(p, B, V)) return SS_ERR_INVALID_ARG;
   if (kq == 0 && (!draft_probs || ld_q < V)) return SS_ERR_INVALID_ARG;
   if (kq != 0 && (!q_idx || !q_val || kq < 1 || kq > SS_MAX_K)) return SS_ERR_INVALID_ARG;
+  if (row_map && Lt < 1) return SS_ERR_INVALID_ARG;
   if (!p->seed || !p->position) return SS_ERR_INVALID_ARG;
   Layout lay;
   if (!make_layout(OP_VERIFY, B, V, L, k_max, dtype, &lay)) return SS_ERR_INVALID_ARG;
@@ -355,6 +356,8 @@ static ss_status verify_any(const void* target_logits, int dtype, int64_t ld_row
   a.dq_idx = q_idx;
   a.dq_val = q_val;
   a.kq = kq;
+  a.rmap = row_map;
+  a.Lt = row_map ? Lt : L + 1;
   a.draft_tokens = draft_tokens;
   a.out_tokens = out_tokens;
   a.out_nacc = out_num_accepted;
@@ -365,8 +368,8 @@ static ss_status verify_any(const void* target_logits, int dtype, int64_t ld_row
 ss_status ss_verify(const void* target_logits, int dtype, int64_t ld_row, const float* draft_probs, int64_t ld_q,
                     const int32_t* draft_tokens, int L, const ss_params* p, int k_max, int32_t* out_tokens,
                     int32_t* out_num_accepted, int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
-  return verify_any(target_logits, dtype, ld_row, draft_probs, ld_q, nullptr, nullptr, 0, draft_tokens, L, p,
-                    k_max, out_tokens, out_num_accepted, flags, ws, ws_bytes, stream);
+  return verify_any(target_logits, dtype, ld_row, L + 1, nullptr, draft_probs, ld_q, nullptr, nullptr, 0,
+                    draft_tokens, L, p, k_max, out_tokens, out_num_accepted, flags, ws, ws_bytes, stream);
 }
 
 ss_status ss_verify_sparse(const void* target_logits, int dtype, int64_t ld_row, const int32_t* draft_idx,
@@ -374,8 +377,17 @@ ss_status ss_verify_sparse(const void* target_logits, int dtype, int64_t ld_row,
                            int k_max, int32_t* out_tokens, int32_t* out_num_accepted, int32_t* flags, void* ws,
                            size_t ws_bytes, void* stream) {
   if (kq < 1 || kq > SS_MAX_K || !draft_idx || !draft_q) return SS_ERR_INVALID_ARG;
-  return verify_any(target_logits, dtype, ld_row, nullptr, 0, draft_idx, draft_q, kq, draft_tokens, L, p, k_max,
-                    out_tokens, out_num_accepted, flags, ws, ws_bytes, stream);
+  return verify_any(target_logits, dtype, ld_row, L + 1, nullptr, nullptr, 0, draft_idx, draft_q, kq, draft_tokens,
+                    L, p, k_max, out_tokens, out_num_accepted, flags, ws, ws_bytes, stream);
+}
+
+ss_status ss_verify_tree(const void* target_logits, int dtype, int64_t ld_row, int Lt, const int32_t* row_map,
+                         const int32_t* draft_idx, const float* draft_q, int kq, const int32_t* draft_tokens, int L,
+                         const ss_params* p, int k_max, int32_t* out_tokens, int32_t* out_num_accepted,
+                         int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+  if (!row_map || Lt < 1 || kq < 1 || kq > SS_MAX_K || !draft_idx || !draft_q) return SS_ERR_INVALID_ARG;
+  return verify_any(target_logits, dtype, ld_row, Lt, row_map, nullptr, 0, draft_idx, draft_q, kq, draft_tokens, L,
+                    p, k_max, out_tokens, out_num_accepted, flags, ws, ws_bytes, stream);
 }
 
 ss_status ss_process_logits(const void* logits, int dtype, int64_t ld, const ss_params* p, int k_max,

@@ -119,6 +119,8 @@ struct KArgs {
   int kq;                    // entries per draft position (0: dense q)
   const float* gum;          // sampling with the Gumbel-max draw: g = ln z per token [B, ld_g] (else NULL)
   int64_t ld_g;
+  const int32_t* rmap;       // verification of a tree path: path position -> target row [B, L+1] (else NULL)
+  int Lt;                    // target rows per request (L+1 without a map)
   const int32_t* draft_tokens;
   int32_t* out_token;
   float* out_logprob;
@@ -229,6 +231,20 @@ struct Ctx {
   int k_eff;
 };
 
+// Allow bits of a target row that a tree path maps outside the tree: none
+// (zero-initialised device memory, never written).
+static __device__ uint32_t g_none_allowed[SS_MAX_V / 32];
+
+// Logits row read for verification row `row` (request b, path position
+// row mod (L+1)): through the path's row map when there is one; -1 when the
+// map points outside the request's Lt target rows.
+__device__ __forceinline__ int64_t source_row(const KArgs& a, int row) {
+  if (!a.rmap) return row;
+  const int b = row / (a.L + 1);
+  const int t = a.rmap[row];
+  return (t >= 0 && t < a.Lt) ? (int64_t)b * a.Lt + t : -1;
+}
+
 template <int DT>
 __device__ __forceinline__ Ctx make_ctx(const KArgs& a, int row) {
   Ctx c;
@@ -243,7 +259,8 @@ __device__ __forceinline__ Ctx make_ctx(const KArgs& a, int row) {
   const int b = c.req;
   const uint32_t m = (a.op == OP_TOPK ? SS_TOPK : (a.mode ? a.mode[b] : 0u)) & a.feat;
   c.mode = m;
-  c.xrow = reinterpret_cast<const unsigned char*>(a.x) + (size_t)row * (size_t)a.ld * DTT<DT>::ES;
+  const int64_t srow = a.op == OP_VERIFY ? source_row(a, row) : row;
+  c.xrow = reinterpret_cast<const unsigned char*>(a.x) + (size_t)(srow < 0 ? 0 : srow) * (size_t)a.ld * DTT<DT>::ES;
   c.hist = nullptr;
   c.nhist = 0;
   c.extra = nullptr;
@@ -265,6 +282,7 @@ __device__ __forceinline__ Ctx make_ctx(const KArgs& a, int row) {
     c.nbias = a.bias_off[b + 1] - a.bias_off[b];
   }
   c.mask = (m & SS_GRAMMAR) ? a.bitmask + (size_t)row * (size_t)a.mask_ld : nullptr;
+  if (srow < 0) c.mask = g_none_allowed;  // every token masked
   c.rep = (m & SS_REP) ? a.rep[b] : 1.0f;
   c.freq = (m & SS_FREQ) ? a.freq[b] : 0.0f;
   c.pres = (m & SS_PRES) ? a.pres[b] : 0.0f;
@@ -484,11 +502,13 @@ __device__ __forceinline__ void scan_unit(const KArgs& a, int gu) {
   const int row = gu / a.U;
   const int u = gu - row * a.U;
   const int lo = u * kUE;
-  const int n = min(kUE, a.V - lo);
+  const int64_t srow = a.op == OP_VERIFY ? source_row(a, row) : row;
+  const int n = srow < 0 ? 0 : min(kUE, a.V - lo);  // a row outside the tree reads nothing
   const int b = a.op == OP_VERIFY ? row / (a.L + 1) : row;
   const uint32_t mode = (a.op == OP_TOPK ? SS_TOPK : (a.mode ? a.mode[b] : 0u)) & a.feat;
   const uint32_t* mask = (mode & SS_GRAMMAR) ? a.bitmask + (size_t)row * (size_t)a.mask_ld : nullptr;
-  const unsigned char* xrow = reinterpret_cast<const unsigned char*>(a.x) + (size_t)row * (size_t)a.ld * ES;
+  const unsigned char* xrow =
+      reinterpret_cast<const unsigned char*>(a.x) + (size_t)(srow < 0 ? 0 : srow) * (size_t)a.ld * ES;
 
   // 1. loads: the unit's chunks, then the grammar words that cover them
   uint4 r[NLD];

@@ -110,6 +110,25 @@ def test_sample_gumbel_arguments_are_checked_before_launch(lib):
     assert call(ws_bytes=n - 256) == -3  # SS_ERR_WORKSPACE: every argument passed its check
 
 
+def test_verify_tree_arguments_are_checked_before_launch(lib):
+    from paper_2607_20475_amd import binding as b
+    fake = C.c_void_p(0x10000)  # never dereferenced: validation fails first
+    p = b._Params(B=4, V=100)
+    mode = (C.c_uint32 * 4)()
+    p.mode = C.cast(mode, C.c_void_p)
+    p.seed = fake
+    p.position = fake
+
+    def call(Lt=7, rmap=fake, kq=8, ws_bytes=1 << 24):
+        return lib.ss_verify_tree(fake, 0, 100, Lt, rmap, fake, fake, kq, fake, 2, C.byref(p), 16, fake, fake,
+                                  None, fake, ws_bytes, None)
+    assert call(Lt=0) == -1
+    assert call(rmap=None) == -1
+    assert call(kq=0) == -1
+    n = b.workspace_bytes(b.OP_VERIFY, 4, 100, 2, 16, b.F32)
+    assert call(ws_bytes=n - 256) == -3
+
+
 def test_invalid_arguments_are_rejected_before_launch(lib):
     from paper_2607_20475_amd import binding as b
     fake = C.c_void_p(0x10000)  # never dereferenced: validation fails first

@@ -865,6 +865,55 @@ def test_verify_sparse_equals_dense_scatter(ssb):
         assert np.array_equal(a_, b_)
 
 
+def run_verify_tree(ssb, inp):
+    x = ssb.logits_tensor(inp)
+    rm = torch.from_numpy(np.ascontiguousarray(inp["row_map"], np.int32)).cuda()
+    qi = torch.from_numpy(np.ascontiguousarray(inp["draft_idx"], np.int32)).cuda()
+    qv = torch.from_numpy(np.ascontiguousarray(inp["draft_q"], np.float32)).cuda()
+    d = torch.from_numpy(np.ascontiguousarray(inp["draft_tokens"], np.int32)).cuda()
+    prm = ssb.Params.from_arrays(inp)
+    out, nacc, fl = ssb.verify_tree(x, rm, qi, qv, d, prm, inp["k_max"])
+    torch.cuda.synchronize()
+    return _np(out), _np(nacc), _np(fl)
+
+
+def test_verify_tree_config4(ssb):
+    # the sparse-list verification workload's paths hidden in trees of 9 rows
+    inp = W.tree_from_path(W.config4_sparse(), 9, 4242)
+    say("[cfg4_tree] verify B=64 L=4 Lt=9 V=131072 kq=64")
+    out, nacc, fl = run_verify_tree(ssb, inp)
+    check_verify(inp, out, nacc, fl, "cfg4_tree")
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_verify_tree_edge_cases(ssb, dtype):
+    # penalties, grammar rows along the path, greedy rows, map entries outside
+    # the tree at the first and at later positions, repeated rows in one map
+    rng = np.random.default_rng(71)
+    B, L, V, kq = 10, 3, 1 << 14, 48
+    path = _sparse_edge_input(rng, B, L, V, kq, dtype, 512)
+    mask = np.zeros((B * (L + 1), V // 32), np.uint32)
+    for r in range(B * (L + 1)):
+        b, l = divmod(r, L + 1)
+        allow = rng.choice(V, V // 3, replace=False)
+        if l < L:
+            allow = np.concatenate([allow, path["draft_idx"][b, l][path["draft_idx"][b, l] >= 0]])
+        ok = allow[(allow >= 0) & (allow < V)]
+        np.bitwise_or.at(mask[r], ok >> 5, (np.uint32(1) << (ok & 31).astype(np.uint32)))
+    path["bitmask"] = mask
+    path["mode"] = path["mode"] | np.uint32(W.MODE_GRAMMAR)
+    inp = W.tree_from_path(path, 2 * (L + 1), 99)
+    rm = inp["row_map"]
+    rm[0, 0] = -1                # outside the tree at the first position
+    rm[1, 2] = 2 * (L + 1)       # ... at a later one
+    rm[4, 1] = rm[4, 0]          # the same row twice
+    label = f"verify-tree-{dtype}"
+    say(f"[{label}] B={B} L={L} Lt={2 * (L + 1)} V={V}")
+    out, nacc, fl = run_verify_tree(ssb, inp)
+    check_verify(inp, out, nacc, fl, label)
+    assert nacc[0] == 0 and np.all(out[0] == -1) and (fl[0] & EMPTY)
+
+
 # --------------------------------------------------------------------------
 # Graph capture and determinism
 # --------------------------------------------------------------------------
