@@ -56,7 +56,7 @@ MALL_BYTES = 256 << 20
 CONFIGS = ("cfg0", "cfg1", "cfg2", "cfg3", "cfg4")
 # a stress line beside the five workloads: the headline batch with every
 # logit of a row equal (the paper's tied correctness inputs at full size)
-EXTRA = ("cfg1_tied", "cfg1_logprobs", "cfg4_sparse", "cfg4_tree", "cfg1_gumbel")
+EXTRA = ("cfg1_tied", "cfg1_logprobs", "cfg4_sparse", "cfg4_tree", "cfg1_gumbel", "cfg1_nucleus")
 LOGPROBS_N = 20  # log-probabilities per request on the log-probability line
 MODE_TOPK = 0x080  # the top-k indicator bit (bit-level encoding table, Section 3.5)
 WORKLOAD = {
@@ -72,6 +72,8 @@ WORKLOAD = {
                  "logit 0.5",
     "cfg1_logprobs": "top-20 log-probabilities (ss_logprobs) of the heterogeneous singular batch (B=64 V=131072 "
                      "bf16, penalties, bias), every request with bit 0x400",
+    "cfg1_nucleus": "full-row truncation (ss_sample_full): the heterogeneous singular batch (B=64 V=131072 bf16) "
+                    "with the top-k bit cleared on every stochastic request (top-p / min-p over the whole row)",
     "cfg1_gumbel": "the heterogeneous singular batch (B=64 V=131072 bf16) sampled with the Gumbel-max draw "
                    "(ss_sample_gumbel, noise [B, V] fp32 read at the kept ids)",
     "cfg4_tree": "tree-path verification (ss_verify_tree): the sparse-list verification batch (B=64 L=4 V=131072 "
@@ -85,6 +87,11 @@ def make_input(name, W):
     """The named workload's seeded synthetic input."""
     if name == "cfg1_gumbel":
         return W.make_config("cfg1")
+    if name == "cfg1_nucleus":
+        inp = W.make_config("cfg1")
+        greedy = (inp["mode"] & W.MODE_GREEDY) != 0
+        inp["mode"] = np.where(greedy, inp["mode"], inp["mode"] & ~np.uint32(W.MODE_TOPK)).astype(np.uint32)
+        return inp
     if name == "cfg4_tree":
         return W.tree_from_path(W.make_config("cfg4_sparse"), 9, 4242)
     if name == "cfg1_logprobs":
@@ -286,6 +293,16 @@ class Runner:
 
             def step(i):
                 ssb.topk(self.xs[i % self.R], k, inp["k_max"], out_val=ov, out_idx=oi, flags=fl, ws=ws)
+        elif name == "cfg1_nucleus":
+            prm = ssb.Params.from_arrays(inp, dev)
+            ws = ssb.workspace(ssb.OP_SAMPLE, inp["B"], inp["V"], 0, inp["k_max"], ssb.BF16, dev)
+            tok = t.empty(inp["B"], dtype=t.int32, device=dev)
+            lp = t.empty(inp["B"], dtype=t.float32, device=dev)
+            fl = t.empty(inp["B"], dtype=t.int32, device=dev)
+
+            def step(i):
+                ssb.sample_full(self.xs[i % self.R], prm, inp["k_max"], out_token=tok, out_logprob=lp, flags=fl,
+                                ws=ws)
         elif name == "cfg1_gumbel":
             prm = ssb.Params.from_arrays(inp, dev)
             g = t.from_numpy(W.gumbel_noise(inp["B"], inp["V"], 1001)).to(dev)

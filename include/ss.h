@@ -5,6 +5,8 @@
  *   ss_sample          singular-mode sampling: prologue (Appendix C.1), top-k /
  *                      top-p / min-p truncation in Alg. 11 order (Appendix C.2),
  *                      greedy or stochastic selection (Section 3.5, Appendix C.3)
+ *   ss_sample_full     the same with top-p / min-p over the whole row for
+ *                      requests without a top-k cut (Appendix C.2)
  *   ss_sample_gumbel   the same with the Gumbel-max draw over the kept set and
  *                      caller-drawn noise (Appendix C.3; the Stage-2 selection)
  *   ss_verify          multistep speculative verification (Section 3.1,
@@ -179,6 +181,22 @@ ss_status ss_topk(const void *x, int dtype, int B, int V, int64_t ld, const int3
 ss_status ss_sample(const void *logits, int dtype, int64_t ld, const ss_params *p, int k_max,
                     int32_t *out_token, float *out_logprob, int32_t *out_idx, float *out_prob,
                     int k_out, int32_t *flags, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Singular-mode sampling with full-row truncation (Appendix C.2 defines top-p
+ * and min-p over the whole vocabulary; ss_sample bounds requests without a
+ * top-k cut to their k_max leading tokens, the bounded regime of Section
+ * 3.3).  For a stochastic request whose top-k bit is off (or k <= 0), top-p
+ * takes its boundary against the normaliser of every valid token of the row
+ * (computed in the same pass over the logits) and min-p is as ever; that
+ * result is returned when the kept set holds fewer than k_max tokens.  A
+ * longer kept set gives ss_sample's bounded result with SS_FLAG_KCAP.  Other
+ * requests, arguments and outputs are as for ss_sample (workspace
+ * ss_workspace_bytes(SS_OP_SAMPLE, ...)).
+ */
+ss_status ss_sample_full(const void *logits, int dtype, int64_t ld, const ss_params *p, int k_max,
+                         int32_t *out_token, float *out_logprob, int32_t *out_idx, float *out_prob, int k_out,
+                         int32_t *flags, void *ws, size_t ws_bytes, void *stream);
 
 /*
  * Singular-mode sampling with the Gumbel-max draw (Appendix C.3: the argmax

@@ -60,6 +60,10 @@ def lib():
         L.ss_sample.restype = i32
         L.ss_sample.argtypes = [vp, C.c_int, i64, C.POINTER(_Params), C.c_int, vp, vp, vp, vp, C.c_int, vp,
                                 vp, sz, vp]
+        if hasattr(L, "ss_sample_full"):
+            L.ss_sample_full.restype = i32
+            L.ss_sample_full.argtypes = [vp, C.c_int, i64, C.POINTER(_Params), C.c_int, vp, vp, vp, vp, C.c_int,
+                                         vp, vp, sz, vp]
         if hasattr(L, "ss_sample_gumbel"):
             L.ss_sample_gumbel.restype = i32
             L.ss_sample_gumbel.argtypes = [vp, C.c_int, i64, C.POINTER(_Params), C.c_int, vp, i64, vp, vp, vp, vp,
@@ -228,6 +232,34 @@ def sample(logits, params, k_max, k_out=0, out_token=None, out_logprob=None, out
     _check(lib().ss_sample(_ptr(logits), dt, logits.stride(0), C.byref(p), k_max, _ptr(out_token),
                            _ptr(out_logprob), _ptr(out_idx), _ptr(out_prob), k_out, _ptr(flags), _ptr(ws),
                            ws.numel(), _stream()))
+    if k_out > 0:
+        return out_token, out_logprob, flags, out_idx, out_prob
+    return out_token, out_logprob, flags
+
+
+def sample_full(logits, params, k_max, k_out=0, out_token=None, out_logprob=None, out_idx=None, out_prob=None,
+                flags=None, ws=None):
+    """ss_sample_full: sampling with full-row top-p / min-p for requests
+    without a top-k cut.  Returns as ``sample``."""
+    B, V = logits.shape
+    dt = _dtype_code(logits)
+    dev = logits.device
+    ws = _ws(ws, OP_SAMPLE, B, V, 0, k_max, dt, dev)
+    if out_token is None:
+        out_token = torch.empty(B, dtype=torch.int32, device=dev)
+    if out_logprob is None:
+        out_logprob = torch.empty(B, dtype=torch.float32, device=dev)
+    if flags is None:
+        flags = torch.empty(B, dtype=torch.int32, device=dev)
+    if k_out > 0:
+        if out_idx is None:
+            out_idx = torch.empty(B, k_out, dtype=torch.int32, device=dev)
+        if out_prob is None:
+            out_prob = torch.empty(B, k_out, dtype=torch.float32, device=dev)
+    p = params.struct()
+    _check(lib().ss_sample_full(_ptr(logits), dt, logits.stride(0), C.byref(p), k_max, _ptr(out_token),
+                                _ptr(out_logprob), _ptr(out_idx), _ptr(out_prob), k_out, _ptr(flags), _ptr(ws),
+                                ws.numel(), _stream()))
     if k_out > 0:
         return out_token, out_logprob, flags, out_idx, out_prob
     return out_token, out_logprob, flags

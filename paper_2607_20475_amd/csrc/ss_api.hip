@@ -53,9 +53,9 @@ static bool make_layout(int op, int B, int V, int L, int k_max, int dtype, Layou
   o = align256(o + ghr * 4);
   lay->off_ptab = o;
   o = align256(o + ghr * 2 * kH * 4);
-  // log-probabilities: every unit's share of its row's normaliser
+  // log-probabilities and full-row sampling: every unit's share of its row's normaliser
   lay->off_usum = o;
-  if (op == OP_LOGPROBS) o = align256(o + (size_t)rows * U * 8);
+  if (op == OP_LOGPROBS || op == OP_SAMPLE) o = align256(o + (size_t)rows * U * 8);
   lay->total = o;
   lay->U = U;
   lay->cap = cap;
@@ -161,7 +161,7 @@ static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStr
   k.gfin = reinterpret_cast<uint32_t*>(w + lay.off_gfin);
   k.pstat = reinterpret_cast<int32_t*>(w + lay.off_pstat);
   k.ptab = reinterpret_cast<uint32_t*>(w + lay.off_ptab);
-  k.usum = k.op == OP_LOGPROBS ? reinterpret_cast<double*>(w + lay.off_usum) : nullptr;
+  k.usum = (k.op == OP_LOGPROBS || k.full) ? reinterpret_cast<double*>(w + lay.off_usum) : nullptr;
   // patch-table workgroups (a multiple of 8, so the stream's XCD remap holds)
   k.patch_wgs = k.op == OP_TOPK ? 0 : (lay.rows + 7) & ~7;
   const int di = dtype == SS_BF16 ? 1 : 0;
@@ -175,7 +175,7 @@ static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStr
   const dim3 grid((unsigned)(k.patch_wgs + (nunits + kSWaves - 1) / kSWaves)), sblock(kSBlock),
       rgrid((unsigned)lay.rows), block(kBlock);
   const int psmem = k.patch_wgs ? (int)sizeof(PSmem) : 0;
-  const bool lp = k.op == OP_LOGPROBS;
+  const bool lp = k.op == OP_LOGPROBS || k.full;  // units add their normaliser shares
   if (dtype == SS_BF16)
     lp ? launch_stream<SS_BF16, true>(k, grid, sblock, psmem, st) : launch_stream<SS_BF16, false>(k, grid, sblock, psmem, st);
   else
@@ -274,7 +274,7 @@ ss_status ss_logprobs(const void* logits, int dtype, int64_t ld, const ss_params
   return launch(a, dtype, lay, ws, (hipStream_t)stream, false);
 }
 
-static ss_status sample_any(const void* logits, int dtype, int64_t ld, const ss_params* p, int k_max,
+static ss_status sample_any(const void* logits, int dtype, int64_t ld, const ss_params* p, int k_max, int full,
                             const float* noise, int64_t ld_noise, int32_t* out_token, float* out_logprob,
                             int32_t* out_idx, float* out_prob, int k_out, int32_t* flags, void* ws, size_t ws_bytes,
                             void* stream) {
@@ -300,6 +300,7 @@ static ss_status sample_any(const void* logits, int dtype, int64_t ld, const ss_
   fill_params(a, p);
   a.gum = noise;
   a.ld_g = noise ? ld_noise : 0;
+  a.full = full;
   a.out_token = out_token;
   a.out_logprob = out_logprob;
   a.out_idx = k_out > 0 ? out_idx : nullptr;
@@ -311,8 +312,15 @@ static ss_status sample_any(const void* logits, int dtype, int64_t ld, const ss_
 ss_status ss_sample(const void* logits, int dtype, int64_t ld, const ss_params* p, int k_max, int32_t* out_token,
                     float* out_logprob, int32_t* out_idx, float* out_prob, int k_out, int32_t* flags, void* ws,
                     size_t ws_bytes, void* stream) {
-  return sample_any(logits, dtype, ld, p, k_max, nullptr, 0, out_token, out_logprob, out_idx, out_prob, k_out, flags,
-                    ws, ws_bytes, stream);
+  return sample_any(logits, dtype, ld, p, k_max, 0, nullptr, 0, out_token, out_logprob, out_idx, out_prob, k_out,
+                    flags, ws, ws_bytes, stream);
+}
+
+ss_status ss_sample_full(const void* logits, int dtype, int64_t ld, const ss_params* p, int k_max,
+                         int32_t* out_token, float* out_logprob, int32_t* out_idx, float* out_prob, int k_out,
+                         int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+  return sample_any(logits, dtype, ld, p, k_max, 1, nullptr, 0, out_token, out_logprob, out_idx, out_prob, k_out,
+                    flags, ws, ws_bytes, stream);
 }
 
 ss_status ss_sample_gumbel(const void* logits, int dtype, int64_t ld, const ss_params* p, int k_max,
@@ -320,8 +328,8 @@ ss_status ss_sample_gumbel(const void* logits, int dtype, int64_t ld, const ss_p
                            int32_t* out_idx, float* out_prob, int k_out, int32_t* flags, void* ws, size_t ws_bytes,
                            void* stream) {
   if (!noise) return SS_ERR_INVALID_ARG;
-  return sample_any(logits, dtype, ld, p, k_max, noise, ld_noise, out_token, out_logprob, out_idx, out_prob, k_out,
-                    flags, ws, ws_bytes, stream);
+  return sample_any(logits, dtype, ld, p, k_max, 0, noise, ld_noise, out_token, out_logprob, out_idx, out_prob,
+                    k_out, flags, ws, ws_bytes, stream);
 }
 
 static ss_status verify_any(const void* target_logits, int dtype, int64_t ld_row, int Lt, const int32_t* row_map,

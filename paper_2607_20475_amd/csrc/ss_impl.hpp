@@ -121,6 +121,7 @@ struct KArgs {
   int64_t ld_g;
   const int32_t* rmap;       // verification of a tree path: path position -> target row [B, L+1] (else NULL)
   int Lt;                    // target rows per request (L+1 without a map)
+  int full;                  // sampling: full-row top-p / min-p for requests without a top-k cut
   const int32_t* draft_tokens;
   int32_t* out_token;
   float* out_logprob;
@@ -228,6 +229,7 @@ struct Ctx {
   bool greedy;
   bool kcap;
   bool pexact;              // the patched-id bitmap is exact (V <= kPB)
+  bool full_row;            // truncation over the whole row (sampling with a.full, no top-k cut)
   int k_eff;
 };
 
@@ -294,6 +296,7 @@ __device__ __forceinline__ Ctx make_ctx(const KArgs& a, int row) {
   c.dtok = -1;
   if (a.op == OP_VERIFY && c.ell < a.L) c.dtok = a.draft_tokens[(size_t)b * a.L + c.ell];
   c.kcap = false;
+  c.full_row = false;
   c.pexact = a.V <= kPB;
   if (a.op == OP_TOPK) {
     c.greedy = false;
@@ -307,6 +310,7 @@ __device__ __forceinline__ Ctx make_ctx(const KArgs& a, int row) {
     const int64_t kreq = ((m & SS_TOPK) && a.top_k[b] >= 1) ? (int64_t)a.top_k[b] : (int64_t)INT_MAX;
     c.k_eff = kreq < a.k_cap ? (int)kreq : a.k_cap;
     c.kcap = !c.greedy && kreq > a.k_cap;
+    c.full_row = a.full && !c.greedy && !((m & SS_TOPK) && a.top_k[b] >= 1);
     if (c.greedy) c.k_eff = 1;
   }
   return c;
@@ -490,6 +494,15 @@ __device__ __forceinline__ float lp_tau(const KArgs& a, uint32_t mode, int b) {
 // the float32 reciprocal itau; the merge recomputes it bit for bit for the
 // raw copies of patched ids.
 __device__ __forceinline__ float lp_term(float v, float mu, float itau) { return expf((v - mu) * itau); }
+// Rows whose units add their share of the full-row normaliser: requests with
+// the log-probability bit, or, in full-row sampling, stochastic requests
+// without a top-k cut.
+__device__ __forceinline__ bool usum_row(const KArgs& a, uint32_t mode, int b) {
+  if (a.op == OP_LOGPROBS) return (mode & SS_LOGPROBS) != 0u;
+  if (!a.full) return false;
+  const bool greedy = (mode & SS_GREEDY) || ((mode & SS_TEMP) && a.temperature[b] <= 0.0f);
+  return !greedy && !((mode & SS_TOPK) && a.top_k[b] >= 1);
+}
 
 // Streams unit `gu` (wave-uniform) and writes its record and candidate groups.
 // The record is (threshold key, groups written or the count that overflowed,
@@ -596,7 +609,7 @@ __device__ __forceinline__ void scan_unit(const KArgs& a, int gu) {
       wm16 = wave_max_u32(hmax16(lm));
     }
     if constexpr (LP) {  // the unit's share of the full-row normaliser
-      if (mode & SS_LOGPROBS) {
+      if (usum_row(a, mode, b)) {
         double sl = 0.0;
         if (wm16 >= 0x0081u) {
           const float mu = float_of_key(wm16 << 16), itau = 1.0f / lp_tau(a, mode, b);
@@ -683,7 +696,7 @@ __device__ __forceinline__ void scan_unit(const KArgs& a, int gu) {
       wm = wave_max_u32(lm);
     }
     if constexpr (LP) {  // the unit's share of the full-row normaliser
-      if (mode & SS_LOGPROBS) {
+      if (usum_row(a, mode, b)) {
         double sl = 0.0;
         if (wm >= kKeyFloor) {
           const float mu = float_of_key(wm), itau = 1.0f / lp_tau(a, mode, b);
@@ -2331,6 +2344,48 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
 // ---------------------------------------------------------------------------
 // Row merge: the whole workgroup, after the row's last unit was written.
 // ---------------------------------------------------------------------------
+// This thread's share of the full-row normaliser sum_j exp((y_j - M) / tau)
+// over the row's valid processed logits: the units' sums (taken by the
+// streaming kernel relative to each unit's raw maximum) rescaled to M, each
+// patched id's raw term (recomputed bit for bit) replaced by its final
+// value's; rows whose lists exceed the LDS table recompute every element.
+// The caller sums the shares over the workgroup.
+template <int DT>
+__device__ __forceinline__ double row_norm_part(const KArgs& a, const Ctx& c, const MSmem& S, int row, int pmode,
+                                                const PatchG& pg, double M, float tauf) {
+  const int U = a.U, tid = threadIdx.x;
+  const float itau = 1.0f / tauf;
+  const double tau = (double)tauf;
+  const int Wm = (a.V + 31) >> 5;
+  auto allowed = [&](int id) { return !c.mask || ((((id >> 5) < Wm ? c.mask[id >> 5] : 0u) >> (id & 31)) & 1u); };
+  double z = 0.0;
+  if (pmode <= 1) {
+    for (int u = tid; u < U; u += kBlock) {
+      const uint32_t wmu = a.rec[(size_t)row * U + u].z;
+      if (wmu >= kKeyFloor) z += exp(((double)float_of_key(wmu) - M) / tau) * a.usum[(size_t)row * U + u];
+    }
+    for (int sl = tid; pmode == 1 && sl < kH; sl += kBlock) {
+      const int id = S.hk[sl];
+      if (id < 0) continue;
+      uint32_t kr = fold_nan(key_raw(load_elem_bits<DT>(c.xrow, id)));  // as the unit sum counted it
+      if (!allowed(id)) kr = 0u;
+      if (kr >= kKeyFloor) {
+        const float mu = float_of_key(a.rec[(size_t)row * U + id / kUE].z);
+        z -= exp(((double)mu - M) / tau) * (double)lp_term(float_of_key(kr), mu, itau);
+      }
+      if (S.hf[sl] >= kKeyFloor) z += exp(((double)float_of_key(S.hf[sl]) - M) / tau);
+    }
+  } else {  // lists beyond the LDS table: every element's processed value
+    for (int i = tid; i < a.V; i += kBlock) {
+      uint32_t k = fold_nan(key_raw(load_elem_bits<DT>(c.xrow, i)));
+      if (!allowed(i)) k = 0u;
+      if (is_patched<DT>(c, S, pmode, pg, i)) k = pmode == 2 ? pg.fin[gfind(pg, i)] : lin_final<DT>(a, c, i);
+      if (k >= kKeyFloor) z += exp(((double)float_of_key(k) - M) / tau);
+    }
+  }
+  return z;
+}
+
 template <int DT, int OP>
 __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uint2* pool) {
   constexpr int GE = DTT<DT>::GE;
@@ -2548,7 +2603,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
         }
       };
       if constexpr (OP == OP_SAMPLE && DT == SS_BF16) {
-        if (!a.out_idx && !a.gum && (phi >> 16) - (tmax >> 16) < (uint32_t)kRBins)
+        if (!a.out_idx && !a.gum && !c.full_row && (phi >> 16) - (tmax >> 16) < (uint32_t)kRBins)
           binned = sample_binned(c, S, pool, (int)C, (int)nfin, (uint32_t)want, tmax >> 16, a.V, b, btoken, blogprob);
       }
       if (binned) {
@@ -2620,38 +2675,10 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
       lds_barrier();
       lds_sort_desc(sel, N);
     }
-    const float tauf = lp_tau(a, c.mode, b), itau = 1.0f / tauf;
+    const float tauf = lp_tau(a, c.mode, b);
     const double tau = (double)tauf;
     const double M = n_sel > 0 ? (double)float_of_key(comp_key(Mcomp)) : 0.0;
-    double z = 0.0;
-    if (n_sel > 0) {
-      const int Wm = (a.V + 31) >> 5;
-      auto allowed = [&](int id) { return !c.mask || ((((id >> 5) < Wm ? c.mask[id >> 5] : 0u) >> (id & 31)) & 1u); };
-      if (pmode <= 1) {
-        for (int u = tid; u < U; u += kBlock) {
-          const uint32_t wmu = a.rec[(size_t)row * U + u].z;
-          if (wmu >= kKeyFloor) z += exp(((double)float_of_key(wmu) - M) / tau) * a.usum[(size_t)row * U + u];
-        }
-        for (int sl = tid; pmode == 1 && sl < kH; sl += kBlock) {
-          const int id = S.hk[sl];
-          if (id < 0) continue;
-          uint32_t kr = fold_nan(key_raw(load_elem_bits<DT>(c.xrow, id)));  // as the unit sum counted it
-          if (!allowed(id)) kr = 0u;
-          if (kr >= kKeyFloor) {
-            const float mu = float_of_key(a.rec[(size_t)row * U + id / kUE].z);
-            z -= exp(((double)mu - M) / tau) * (double)lp_term(float_of_key(kr), mu, itau);
-          }
-          if (S.hf[sl] >= kKeyFloor) z += exp(((double)float_of_key(S.hf[sl]) - M) / tau);
-        }
-      } else {  // lists beyond the LDS table: every element's processed value
-        for (int i = tid; i < a.V; i += kBlock) {
-          uint32_t k = fold_nan(key_raw(load_elem_bits<DT>(c.xrow, i)));
-          if (!allowed(i)) k = 0u;
-          if (is_patched<DT>(c, S, pmode, pg, i)) k = pmode == 2 ? pg.fin[gfind(pg, i)] : lin_final<DT>(a, c, i);
-          if (k >= kKeyFloor) z += exp(((double)float_of_key(k) - M) / tau);
-        }
-      }
-    }
+    double z = n_sel > 0 ? row_norm_part<DT>(a, c, S, row, pmode, pg, M, tauf) : 0.0;
     z = block_sum(z, S.rd);
     const double lz = n_sel > 0 ? log(z) : 0.0;
     const uint64_t* sel = reinterpret_cast<const uint64_t*>(pool);
@@ -2761,29 +2788,50 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
         }
       }
       const uint64_t Zk = block_sum(zl, S.r64);  // its barriers publish Wl
-      // top-p boundary: first element whose running mass reaches p * Z_k
-      uint64_t ep = 0ull;
-      if (topp)
-        ep = cross_find(S, pool, Wl, nT, inT, (double)c.top_p * (double)Zk, false, kmin, comp_key(Mcomp), a.V);
-      // kept set S = T, min-p survivors, canonical prefix up to ep
+      // kept set S = T, min-p survivors, canonical prefix up to the top-p
+      // boundary ep (the first element whose running mass reaches p * Z).
+      // Full-row truncation (Appendix C.2) takes Z over the whole row; its
+      // result stands when the kept set holds fewer than k_max tokens, else
+      // the bounded one (Z over T) is taken with KCAP.
+      double zthr = (double)Zk;
+      bool full_try = OP == OP_SAMPLE && c.full_row;
+      if (full_try)
+        zthr = kFix * block_sum(row_norm_part<DT>(a, c, S, row, pmode, pg, M, lp_tau(a, c.mode, b)), S.rd);
       uint32_t inS = 0u;
       uint64_t zs = 0ull, lastc = ~0ull;
       uint32_t ns = 0u;
       uint32_t smin = 0xFFFFFFFFu;
-      for (int m = 0; m < MT; ++m) {
-        const int i = tid + m * kBlock;
-        if ((keepm >> m) & 1u) {
-          const uint64_t cm = comp_of(pool[i].x, pool[i].y);
-          if (ep == 0ull || cm >= ep) {
-            inS |= 1u << m;
-            zs += Wl[i];
-            ++ns;
-            lastc = min(lastc, cm);
-            smin = min(smin, pool[i].x);
+      for (;;) {
+        uint64_t ep = 0ull;
+        if (topp) ep = cross_find(S, pool, Wl, nT, inT, (double)c.top_p * zthr, false, kmin, comp_key(Mcomp), a.V);
+        inS = 0u;
+        zs = 0ull;
+        lastc = ~0ull;
+        ns = 0u;
+        smin = 0xFFFFFFFFu;
+        for (int m = 0; m < MT; ++m) {
+          const int i = tid + m * kBlock;
+          if ((keepm >> m) & 1u) {
+            const uint64_t cm = comp_of(pool[i].x, pool[i].y);
+            if (ep == 0ull || cm >= ep) {
+              inS |= 1u << m;
+              zs += Wl[i];
+              ++ns;
+              lastc = min(lastc, cm);
+              smin = min(smin, pool[i].x);
+            }
           }
         }
+        block_sum_min2(zs, lastc, ns, smin, S);
+        if (!full_try) break;
+        full_try = false;
+        if (ns < (uint32_t)a.k_cap) {
+          flags &= ~SS_FLAG_KCAP;
+          break;
+        }
+        flags |= SS_FLAG_KCAP;
+        zthr = (double)Zk;
       }
-      block_sum_min2(zs, lastc, ns, smin, S);
       const uint64_t Zs = zs;
       const uint32_t n_s = ns;
       const uint64_t last = lastc;

@@ -287,6 +287,92 @@ def test_sample_kept_distribution_outputs(ssb):
         assert np.all(idx[b, m:] == -1)
 
 
+def check_sample_full(ssb, inp, label, k_out=0):
+    x = ssb.logits_tensor(inp)
+    prm = ssb.Params.from_arrays(inp)
+    r = ssb.sample_full(x, prm, inp["k_max"], k_out=k_out)
+    torch.cuda.synchronize()
+    tok, lp, fl = _np(r[0]), _np(r[1]), _np(r[2])
+    ref = oracle.sample_full(inp)
+    ok = _admissible(ref, tok, lp)
+    bad = np.nonzero(~ok)[0]
+    assert bad.size == 0, (label, bad[:10], tok[bad[:10]], lp[bad[:10]], ref["token"][bad[:10]],
+                           ref["logprob"][bad[:10]], ref["n_adm"][bad[:10]])
+    # the fit test may go either way only where a kept-set boundary is near
+    sure = ref["n_adm"] == 1
+    assert np.array_equal((fl & (EMPTY | KCAP))[sure], (ref["flags"] & (EMPTY | KCAP))[sure]), label
+    near = int((ref["n_adm"] > 1).sum())
+    alt = int((tok != ref["token"]).sum())
+    fb = int(((fl & FALLBACK) > 0).sum())
+    over = int(((ref["flags"] & KCAP) > 0).sum())
+    if COUNTS is not None:
+        COUNTS.add(label, tok.size, near, alt, fb)
+    say(f"[{label}] rows={tok.size} near-boundary rows={near} (outcome other than the oracle's own: {alt}) "
+        f"fallback={fb} bounded (KCAP)={over}")
+    return ref
+
+
+def nucleus_rows(inp):
+    """The input with the top-k bit cleared on every stochastic request."""
+    inp = dict(inp)
+    greedy = (inp["mode"] & W.MODE_GREEDY) != 0
+    inp["mode"] = np.where(greedy, inp["mode"], inp["mode"] & ~np.uint32(W.MODE_TOPK)).astype(np.uint32)
+    return inp
+
+
+@pytest.mark.parametrize("name", ["cfg0", "cfg1", "cfg3"])
+def test_sample_full_configs(ssb, name):
+    inp = nucleus_rows(W.make_config(name))
+    say(f"[{name}-full] sample B={inp['B']} V={inp['V']} dtype={inp['dtype']}")
+    ref = check_sample_full(ssb, inp, f"{name}-full")
+    stoch = (inp["mode"] & W.MODE_GREEDY) == 0
+    assert ((ref["flags"][stoch] & KCAP) == 0).any()  # some requests take the full-row result
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_sample_full_edge_cases(ssb, dtype):
+    # long tails (the whole-row cut differs from the bounded one), flat rows
+    # (overflow), min-p keeping exactly k_max and one fewer, short valid sets,
+    # masked and NaN entries, penalised and biased heads, a long history that
+    # overflows the LDS patch table, and top-k requests beside
+    rng = np.random.default_rng(123)
+    B, V, k_max = 16, 20000, 128
+    x = rng.normal(0, 0.3, (B, V)).astype(np.float32)
+    for b in range(B):
+        x[b, rng.choice(V, 10, replace=False)] += rng.uniform(5.0, 6.5, 10).astype(np.float32)
+    x[2] = 0.0                                        # flat: overflow
+    x[3] = -20.0
+    x[3, :k_max] = 0.0                                # min-p keeps exactly k_max: overflow
+    x[4] = -20.0
+    x[4, : k_max - 1] = 0.0                           # ... k_max - 1: fits
+    x[5, 40:] = -np.inf                               # 40 valid tokens
+    x[6, ::3] = np.nan
+    mode = np.full(B, W.MODE_TEMP | W.MODE_TOPP | W.MODE_MINP | W.MODE_REP | W.MODE_BIAS, np.uint32)
+    mode[3] = mode[4] = W.MODE_MINP
+    mode[7] = W.MODE_TEMP | W.MODE_TOPK | W.MODE_TOPP
+    mode[8] = W.MODE_GREEDY
+    top_p = np.full(B, 0.9, np.float32)
+    top_p[9] = 0.999
+    min_p = np.full(B, 0.001, np.float32)
+    min_p[3] = min_p[4] = 0.5
+    hist = [rng.integers(0, V, 64).astype(np.int32) for _ in range(B)]
+    hist[10] = rng.choice(V, 3000, replace=False).astype(np.int32)  # beyond the LDS table
+    off = np.zeros(B + 1, np.int32)
+    off[1:] = np.cumsum([len(h) for h in hist])
+    bids = [rng.choice(V, 8, replace=False).astype(np.int32) for _ in range(B)]
+    boff = np.arange(B + 1, dtype=np.int32) * 8
+    xx = x if dtype == W.F32 else W.bf16_bits_from_f32(x)
+    inp = W.custom_rows(xx, dtype, k_max=k_max, mode=mode, temperature=np.full(B, 0.8), top_k=np.full(B, 50),
+                        top_p=top_p, min_p=min_p, rep=np.full(B, 1.3), position=np.arange(B) * 5)
+    inp["hist_offsets"], inp["hist_ids"] = off, np.concatenate(hist)
+    inp["bias_offsets"], inp["bias_ids"] = boff, np.concatenate(bids)
+    inp["bias_vals"] = rng.uniform(-3, 3, B * 8).astype(np.float32)
+    label = f"full-edge-{dtype}"
+    say(f"[{label}] B={B} V={V} k_max={k_max}")
+    ref = check_sample_full(ssb, inp, label, k_out=16)
+    assert ref["flags"][2] & KCAP and ref["flags"][3] & KCAP and not ref["flags"][4] & KCAP
+
+
 def check_sample_gumbel(ssb, inp, noise, label, k_out=0):
     x = ssb.logits_tensor(inp)
     prm = ssb.Params.from_arrays(inp)
