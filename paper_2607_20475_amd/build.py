@@ -32,7 +32,7 @@ HIPCC_FLAGS = [
 ]
 
 _DT = {"f32": 0, "bf16": 1}
-_OP = {"topk": 0, "sample": 1, "verify": 2, "process": 3, "logprobs": 4}
+_OP = {"topk": 0, "sample": 1, "verify": 2, "process": 3, "logprobs": 4, "sample_x": 5}
 
 
 def units() -> list[tuple[str, str, list[str]]]:

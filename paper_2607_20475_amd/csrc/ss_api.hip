@@ -104,21 +104,27 @@ static void fill_params(KArgs& k, const ss_params* p) {
 
 static int esize(int dtype) { return dtype == SS_BF16 ? 2 : 4; }
 
+// The merge instantiation of a call: sampling with full-row truncation or the
+// Gumbel-max draw has its own, so plain sampling carries neither extension.
+static int merge_op(const KArgs& k) { return (k.op == OP_SAMPLE && (k.full || k.gum)) ? (int)OP_SAMPLE_X : k.op; }
+
 static void launch_merge_any(const KArgs& k, int dtype, dim3 grid, dim3 block, int smem, hipStream_t st) {
   if (dtype == SS_BF16) {
-    switch (k.op) {
+    switch (merge_op(k)) {
       case OP_TOPK: launch_merge<SS_BF16, OP_TOPK>(k, grid, block, smem, st); break;
       case OP_SAMPLE: launch_merge<SS_BF16, OP_SAMPLE>(k, grid, block, smem, st); break;
       case OP_VERIFY: launch_merge<SS_BF16, OP_VERIFY>(k, grid, block, smem, st); break;
       case OP_LOGPROBS: launch_merge<SS_BF16, OP_LOGPROBS>(k, grid, block, smem, st); break;
+      case OP_SAMPLE_X: launch_merge<SS_BF16, OP_SAMPLE_X>(k, grid, block, smem, st); break;
       default: launch_merge<SS_BF16, OP_PROCESS>(k, grid, block, smem, st); break;
     }
   } else {
-    switch (k.op) {
+    switch (merge_op(k)) {
       case OP_TOPK: launch_merge<SS_F32, OP_TOPK>(k, grid, block, smem, st); break;
       case OP_SAMPLE: launch_merge<SS_F32, OP_SAMPLE>(k, grid, block, smem, st); break;
       case OP_VERIFY: launch_merge<SS_F32, OP_VERIFY>(k, grid, block, smem, st); break;
       case OP_LOGPROBS: launch_merge<SS_F32, OP_LOGPROBS>(k, grid, block, smem, st); break;
+      case OP_SAMPLE_X: launch_merge<SS_F32, OP_SAMPLE_X>(k, grid, block, smem, st); break;
       default: launch_merge<SS_F32, OP_PROCESS>(k, grid, block, smem, st); break;
     }
   }
@@ -131,6 +137,7 @@ static hipError_t merge_smem_any(int dtype, int op, int bytes) {
       case OP_SAMPLE: return merge_smem_limit<SS_BF16, OP_SAMPLE>(bytes);
       case OP_VERIFY: return merge_smem_limit<SS_BF16, OP_VERIFY>(bytes);
       case OP_LOGPROBS: return merge_smem_limit<SS_BF16, OP_LOGPROBS>(bytes);
+      case OP_SAMPLE_X: return merge_smem_limit<SS_BF16, OP_SAMPLE_X>(bytes);
       default: return merge_smem_limit<SS_BF16, OP_PROCESS>(bytes);
     }
   }
@@ -139,11 +146,12 @@ static hipError_t merge_smem_any(int dtype, int op, int bytes) {
     case OP_SAMPLE: return merge_smem_limit<SS_F32, OP_SAMPLE>(bytes);
     case OP_VERIFY: return merge_smem_limit<SS_F32, OP_VERIFY>(bytes);
     case OP_LOGPROBS: return merge_smem_limit<SS_F32, OP_LOGPROBS>(bytes);
+    case OP_SAMPLE_X: return merge_smem_limit<SS_F32, OP_SAMPLE_X>(bytes);
     default: return merge_smem_limit<SS_F32, OP_PROCESS>(bytes);
   }
 }
 
-static bool smem_configured[2][5];
+static bool smem_configured[2][6];
 
 static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStream_t st, bool materialize) {
   unsigned char* w = reinterpret_cast<unsigned char*>(ws);
@@ -165,11 +173,12 @@ static ss_status launch(KArgs& k, int dtype, const Layout& lay, void* ws, hipStr
   // patch-table workgroups (a multiple of 8, so the stream's XCD remap holds)
   k.patch_wgs = k.op == OP_TOPK ? 0 : (lay.rows + 7) & ~7;
   const int di = dtype == SS_BF16 ? 1 : 0;
-  if (!smem_configured[di][k.op]) {
+  const int mop = merge_op(k);
+  if (!smem_configured[di][mop]) {
     // the largest dynamic LDS any call can ask for
     const int maxb = kSmemFixed + 8 * (((2 * SS_MAX_K + 128 + 255) & ~255) + kBlock);
-    if (merge_smem_any(dtype, k.op, maxb) != hipSuccess) return SS_ERR_HIP;
-    smem_configured[di][k.op] = true;
+    if (merge_smem_any(dtype, mop, maxb) != hipSuccess) return SS_ERR_HIP;
+    smem_configured[di][mop] = true;
   }
   const int nunits = lay.rows * lay.U;
   const dim3 grid((unsigned)(k.patch_wgs + (nunits + kSWaves - 1) / kSWaves)), sblock(kSBlock),

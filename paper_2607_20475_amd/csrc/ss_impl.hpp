@@ -72,7 +72,10 @@ constexpr uint32_t kNoEmit = 0xFFFFFFFFu;    // threshold of a unit that emits n
 constexpr double kFix = 1125899906842624.0;  // 2^50: fixed-point scale of probability mass
 
 enum { OP_TOPK = SS_OP_TOPK, OP_SAMPLE = SS_OP_SAMPLE, OP_VERIFY = SS_OP_VERIFY, OP_PROCESS = SS_OP_PROCESS,
-       OP_LOGPROBS = SS_OP_LOGPROBS };
+       OP_LOGPROBS = SS_OP_LOGPROBS,
+       OP_SAMPLE_X = 5 };  // merge only: sampling with full-row truncation or the Gumbel-max draw
+// the merge instantiations that sample (the plain one carries neither extension)
+constexpr bool sampling_op(int op) { return op == OP_SAMPLE || op == OP_SAMPLE_X; }
 enum { KIND_EMPTY = 0, KIND_GREEDY = 1, KIND_DIST = 2 };
 
 struct RowSummary {
@@ -2602,8 +2605,9 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
             if (i0 + u * kBlock < (int)C) f(e[u].x, e[u].y);
         }
       };
-      if constexpr (OP == OP_SAMPLE && DT == SS_BF16) {
-        if (!a.out_idx && !a.gum && !c.full_row && (phi >> 16) - (tmax >> 16) < (uint32_t)kRBins)
+      if constexpr (sampling_op(OP) && DT == SS_BF16) {
+        const bool ext = OP == OP_SAMPLE_X && (a.gum || c.full_row);  // these draw element-wise
+        if (!a.out_idx && !ext && (phi >> 16) - (tmax >> 16) < (uint32_t)kRBins)
           binned = sample_binned(c, S, pool, (int)C, (int)nfin, (uint32_t)want, tmax >> 16, a.V, b, btoken, blogprob);
       }
       if (binned) {
@@ -2746,7 +2750,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
           a.summ[row] = s;
         }
       }
-      if constexpr (OP == OP_SAMPLE) {
+      if constexpr (sampling_op(OP)) {
         if (a.out_idx) {
           for (int r = tid; r < a.k_out; r += kBlock) {
             a.out_idx[(size_t)b * a.k_out + r] = r == 0 ? argmax : -1;
@@ -2794,7 +2798,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
       // result stands when the kept set holds fewer than k_max tokens, else
       // the bounded one (Z over T) is taken with KCAP.
       double zthr = (double)Zk;
-      bool full_try = OP == OP_SAMPLE && c.full_row;
+      bool full_try = OP == OP_SAMPLE_X && c.full_row;
       if (full_try)
         zthr = kFix * block_sum(row_norm_part<DT>(a, c, S, row, pmode, pg, M, lp_tau(a, c.mode, b)), S.rd);
       uint32_t inS = 0u;
@@ -2853,9 +2857,9 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
           a.summ[row] = s;
         }
       } else {
-        if (OP == OP_SAMPLE || !has_draft) {
+        if (sampling_op(OP) || !has_draft) {
           uint64_t e;
-          if (OP == OP_SAMPLE && a.gum) {
+          if (OP == OP_SAMPLE_X && a.gum) {
             // Gumbel-max over the kept set (Appendix C.3): the largest
             // (y - M)/tau - g[id] in double, the lower id on equal scores
             const float* grow = a.gum + (size_t)b * (size_t)a.ld_g;
@@ -2882,7 +2886,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
           token = (int)comp_idx(e);
           const double w = weight_fast((double)float_of_key(comp_key(e)), M, itau);
           logprob = (float)log(w / Zsd);
-          if constexpr (OP == OP_SAMPLE) {
+          if constexpr (sampling_op(OP)) {
             if (a.out_idx) {
               // kept list in canonical order: compact S to the front, sort
               uint64_t* srt = reinterpret_cast<uint64_t*>(pool);
@@ -3022,7 +3026,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
       }
       if (a.flags && tid == 0) a.flags[b] = flags;
       return;
-    } else if constexpr (OP == OP_SAMPLE) {
+    } else if constexpr (sampling_op(OP)) {
       if (tid == 0) {
         a.out_token[b] = token;
         if (a.out_logprob) a.out_logprob[b] = logprob;

@@ -26,11 +26,13 @@ SS_EXTERN_MERGE(0, 1)
 SS_EXTERN_MERGE(0, 2)
 SS_EXTERN_MERGE(0, 3)
 SS_EXTERN_MERGE(0, 4)
+SS_EXTERN_MERGE(0, 5)
 SS_EXTERN_MERGE(1, 0)
 SS_EXTERN_MERGE(1, 1)
 SS_EXTERN_MERGE(1, 2)
 SS_EXTERN_MERGE(1, 3)
 SS_EXTERN_MERGE(1, 4)
+SS_EXTERN_MERGE(1, 5)
 #undef SS_EXTERN_MERGE
 extern template void launch_stream<0, false>(const KArgs&, dim3, dim3, int, hipStream_t);
 extern template void launch_stream<1, false>(const KArgs&, dim3, dim3, int, hipStream_t);
