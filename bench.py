@@ -521,7 +521,7 @@ def main():
         stats_from(*args.stats_from)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: this build runs on one GPU only; --gpus must be 1 "
+        print("bench.py: the benchmark runs on one GPU only; --gpus must be 1 "
               "(rows are independent, so a multi-GPU run would shard the batch with no communication)",
               file=sys.stderr)
         sys.exit(2)
