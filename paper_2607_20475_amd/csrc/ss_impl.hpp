@@ -3177,7 +3177,11 @@ __global__ __launch_bounds__(kSBlock) void ss_stream_kernel(KArgs a) {
   int bid = blockIdx.x;
   if (bid < a.patch_wgs) {  // patch-table workgroups (a multiple of 8) come first
     extern __shared__ __align__(16) unsigned char psmem[];
-    if (bid < a.rows) patch_row<DT>(a, bid, *reinterpret_cast<PSmem*>(psmem));
+    // on the XCD that streams the row (below), so the gathers of its listed
+    // ids and its units' loads share that XCD's L2
+    int row = bid;
+    if ((a.rows & 7) == 0 && ((a.rows * a.U) & 31) == 0) row = (bid & 7) * (a.rows >> 3) + (bid >> 3);
+    if (row < a.rows) patch_row<DT>(a, row, *reinterpret_cast<PSmem*>(psmem));
     return;
   }
   bid -= a.patch_wgs;
