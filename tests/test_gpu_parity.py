@@ -1043,6 +1043,71 @@ def test_graph_replay_matches_eager(ssb):
     check_sample(inp2, _np(tok), _np(lp), _np(fl), "graph-pos+1")
 
 
+@pytest.mark.parametrize("entry", ["sample_full", "sample_gumbel", "verify_sparse", "verify_tree"])
+def test_graph_replay_of_the_extended_entry_points(ssb, entry):
+    """Each extended entry point captured in a HIP graph: every replay (with
+    eager calls between replays) gives the eager result."""
+    if entry.startswith("sample"):
+        inp = nucleus_rows(W.config1(B=16)) if entry == "sample_full" else W.config1(B=16)
+        x = ssb.logits_tensor(inp)
+        prm = ssb.Params.from_arrays(inp)
+        ws = ssb.workspace(ssb.OP_SAMPLE, inp["B"], inp["V"], 0, inp["k_max"], ssb.BF16)
+        outs = [torch.empty(inp["B"], dtype=dt, device="cuda") for dt in (torch.int32, torch.float32, torch.int32)]
+        g_noise = torch.from_numpy(W.gumbel_noise(inp["B"], inp["V"], 77)).cuda()
+
+        def call(o):
+            if entry == "sample_full":
+                ssb.sample_full(x, prm, inp["k_max"], out_token=o[0], out_logprob=o[1], flags=o[2], ws=ws)
+            else:
+                ssb.sample_gumbel(x, prm, inp["k_max"], g_noise, out_token=o[0], out_logprob=o[1], flags=o[2], ws=ws)
+    else:
+        inp = W.config4_sparse(B=8)
+        if entry == "verify_tree":
+            inp = W.tree_from_path(inp, 7, 5)
+        x = ssb.logits_tensor(inp)
+        qi = torch.from_numpy(np.ascontiguousarray(inp["draft_idx"], np.int32)).cuda()
+        qv = torch.from_numpy(np.ascontiguousarray(inp["draft_q"], np.float32)).cuda()
+        d = torch.from_numpy(np.ascontiguousarray(inp["draft_tokens"], np.int32)).cuda()
+        prm = ssb.Params.from_arrays(inp)
+        L = inp["L"]
+        ws = ssb.workspace(ssb.OP_VERIFY, inp["B"], inp["V"], L, inp["k_max"], ssb.BF16)
+        outs = [torch.empty(inp["B"], L + 1, dtype=torch.int32, device="cuda"),
+                torch.empty(inp["B"], dtype=torch.int32, device="cuda"),
+                torch.empty(inp["B"], dtype=torch.int32, device="cuda")]
+        rm = torch.from_numpy(np.ascontiguousarray(inp.get("row_map", np.zeros((1, 1))), np.int32)).cuda()
+
+        def call(o):
+            if entry == "verify_tree":
+                ssb.verify_tree(x, rm, qi, qv, d, prm, inp["k_max"], out_tokens=o[0], out_nacc=o[1], flags=o[2], ws=ws)
+            else:
+                ssb.verify_sparse(x, qi, qv, d, prm, inp["k_max"], out_tokens=o[0], out_nacc=o[1], flags=o[2], ws=ws)
+    say(f"[graph-{entry}] eager reference")
+    call(outs)
+    torch.cuda.synchronize()
+    ref = [_np(o).copy() for o in outs]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        call(outs)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    say(f"[graph-{entry}] capture")
+    with torch.cuda.graph(g):
+        call(outs)
+    scratch = [torch.empty_like(o) for o in outs]
+    for rep in range(3):
+        for o in outs:
+            o.fill_(-7)
+        say(f"[graph-{entry}] replay {rep}")
+        g.replay()
+        torch.cuda.synchronize()
+        for a_, r_ in zip(outs, ref):
+            assert np.array_equal(_np(a_), r_), (entry, rep)
+        call(scratch)  # eager work between replays
+        torch.cuda.synchronize()
+
+
 def test_repeat_calls_are_bitwise_identical(ssb):
     inp = W.config3(B=32)
     say("[determinism] cfg3 B=32 x3")
