@@ -369,8 +369,30 @@ def test_sample_full_edge_cases(ssb, dtype):
     inp["bias_vals"] = rng.uniform(-3, 3, B * 8).astype(np.float32)
     label = f"full-edge-{dtype}"
     say(f"[{label}] B={B} V={V} k_max={k_max}")
+    x_t = ssb.logits_tensor(inp)
+    r = ssb.sample_full(x_t, ssb.Params.from_arrays(inp), k_max, k_out=16)
+    torch.cuda.synchronize()
+    gidx, gprob = _np(r[3]), _np(r[4])
     ref = check_sample_full(ssb, inp, label, k_out=16)
     assert ref["flags"][2] & KCAP and ref["flags"][3] & KCAP and not ref["flags"][4] & KCAP
+    # the kept list of rows that fit: the n_kept leading tokens of the processed
+    # row (canonical order) with their probabilities over the kept set
+    y = oracle.process_logits(inp)["y"]
+    tau = np.float32(0.8)
+    for b in range(B):
+        stoch = (mode[b] & W.MODE_GREEDY) == 0
+        if not stoch or ref["n_adm"][b] != 1 or (ref["flags"][b] & KCAP) or (mode[b] & W.MODE_TOPK):
+            continue
+        yb = y[b].astype(np.float64)
+        order = np.lexsort((np.arange(V), -yb))
+        n = int(ref["n_kept"][b])
+        t_b = float(tau) if mode[b] & W.MODE_TEMP else 1.0
+        w = np.exp((yb[order[:n]] - yb[order[0]]) / t_b)
+        P = w / w.sum()
+        m = min(n, 16)
+        assert np.array_equal(gidx[b, :m], order[:m]), b
+        np.testing.assert_allclose(gprob[b, :m], P[:m], rtol=1e-5, atol=1e-30)
+        assert np.all(gidx[b, m:] == -1)
 
 
 def check_sample_gumbel(ssb, inp, noise, label, k_out=0):
