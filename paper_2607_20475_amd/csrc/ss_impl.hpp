@@ -67,6 +67,7 @@ constexpr int kRBins = 1 << kRB;
 constexpr int kHStride = kRBins + 1;
 constexpr int kGT = 4096;                    // gather table entries (LDS)
 constexpr int kGS = 2048;                    // candidate groups held in registers per batch
+constexpr int kEBins = 1024;                 // key bins of the sampling epilogue
 constexpr int kQScan = 256;                  // sparse draft lists up to this length are scanned, longer ones sorted
 constexpr uint32_t kNoEmit = 0xFFFFFFFFu;    // threshold of a unit that emits nothing
 constexpr double kFix = 1125899906842624.0;  // 2^50: fixed-point scale of probability mass
@@ -797,6 +798,9 @@ static_assert(offsetof(MSmem, hk) == offsetof(MSmem, pbits) + sizeof(uint32_t) *
                   sizeof(uint32_t) * (kPB / 32 + 2 * kH) >= sizeof(uint64_t) * SS_MAX_K,
               "sparse draft list view");
 __device__ __forceinline__ uint64_t* qlist_view(MSmem& S) { return reinterpret_cast<uint64_t*>(S.pbits); }
+// The key-bin sampling epilogue keeps four word tables of kEBins bins over the
+// patch bitmap and its mass table over the patch table's ids (dead there too).
+static_assert(4 * kEBins <= kPB / 32 && 2 * kEBins <= kH, "key-bin tables over the patch tables");
 
 __device__ __forceinline__ uint32_t hslot(int id) { return ((uint32_t)id * 2654435761u) >> 21; }  // 11 bits
 static_assert(kH == 2048, "hslot assumes 2048 slots");
@@ -2003,7 +2007,8 @@ __device__ __forceinline__ uint32_t compact_pool(MSmem& S, uint2* pool, int n, P
 
 // ---------------------------------------------------------------------------
 // Sampling epilogue on key bins, for bf16 rows whose pool keys span fewer than
-// kRBins consecutive 16-bit key values (Alg. 11 order, Appendix C.2-C.3).
+// NB consecutive 16-bit key values (Alg. 11 order, Appendix C.2-C.3); rows
+// spanning up to 512 keys take the one-bin-per-thread instantiation.
 // Raw bf16 values lie on the 16-bit key grid, and elements with one key share
 // one weight, so the top-k boundary, Z_k, the top-p and min-p cuts, Z_S and
 // the drawn key follow from per-key counts in canonical order (keys
@@ -2017,8 +2022,10 @@ __device__ __forceinline__ uint32_t compact_pool(MSmem& S, uint2* pool, int n, P
 // min-p would cut inside the maximum's own key or more than 64 patched
 // finals are pooled: the element-wise epilogue then handles the row.
 // ---------------------------------------------------------------------------
+template <int NB>  // key bins: 512 or kEBins
 __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint2* pool, int C, int nfin,
                                               uint32_t want, uint32_t lo16, int V, int b, int& token, float& logprob) {
+  static_assert(NB <= kEBins, "bin tables sized for kEBins");
   const int tid = threadIdx.x;
   const bool minp = (c.mode & SS_MINP) && c.min_p > 0.0f;
   const bool topp = (c.mode & SS_TOPP) && c.top_p < 1.0f;
@@ -2026,13 +2033,13 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
   if (lt > 0.0 || nfin > 64) return false;
   const double tau = (double)c.tau;
   const double itau = 1.0 / tau;
-  uint32_t* cnt = S.hist[0];            // grid elements per bin (bin = key16 - lo16)
-  uint32_t* minix = S.hist[0] + kRBins;  // lowest index of each bin's grid elements
-  uint32_t* abv = S.hist[1];            // per position: T elements before it
-  uint32_t* ocnt = S.hist[1] + kRBins;  // off-grid (patched) values of each bin
-  uint64_t* mbf = S.mhist;              // per position: T mass before it
-  static_assert(2 * kRBins <= (kHCopies * kHStride + 3) / 4 * 4, "bin tables fit one histogram row");
-  for (int i = tid; i < kRBins; i += kBlock) {
+  // the pool holds the patched finals by now: the patch tables' memory is free
+  uint32_t* cnt = S.pbits;                                  // grid elements per bin (bin = key16 - lo16)
+  uint32_t* minix = S.pbits + kEBins;                       // lowest index of each bin's grid elements
+  uint32_t* abv = S.pbits + 2 * kEBins;                     // per position: T elements before it
+  uint32_t* ocnt = S.pbits + 3 * kEBins;                    // off-grid (patched) values of each bin
+  uint64_t* mbf = reinterpret_cast<uint64_t*>(S.hk);        // per position: T mass before it
+  for (int i = tid; i < NB; i += kBlock) {
     cnt[i] = 0u;
     minix[i] = 0xFFFFFFFFu;
     ocnt[i] = 0u;
@@ -2067,7 +2074,7 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
   lds_barrier();
   // positions in canonical order: position p holds bin top - p, its off-grid
   // values first (they exceed its grid key), then its grid elements; thread t
-  // holds positions PP t .. PP t + PP - 1 (PP = kRBins / kBlock)
+  // holds positions PP t .. PP t + PP - 1 (PP = NB / kBlock)
   const uint32_t Kmax = S.bc[7];
   const uint32_t top = (Kmax >> 16) - lo16;
   const double M = (double)float_of_key(Kmax);
@@ -2143,8 +2150,8 @@ __device__ __forceinline__ bool sample_binned(const Ctx& c, MSmem& S, const uint
     *mass_out = cum;
     return j;
   };
-  constexpr int PP = kRBins / kBlock;  // positions per thread
-  static_assert(PP >= 1 && PP * kBlock == kRBins, "every key bin has one position");
+  constexpr int PP = NB / kBlock;  // positions per thread
+  static_assert(PP >= 1 && PP * kBlock == NB, "every key bin has one position");
   uint32_t ct[PP], nn[PP], fg[PP];
   uint64_t mm[PP], wg[PP];
   bool drop[PP];
@@ -2607,8 +2614,13 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
       };
       if constexpr (sampling_op(OP) && DT == SS_BF16) {
         const bool ext = OP == OP_SAMPLE_X && (a.gum || c.full_row);  // these draw element-wise
-        if (!a.out_idx && !ext && (phi >> 16) - (tmax >> 16) < (uint32_t)kRBins)
-          binned = sample_binned(c, S, pool, (int)C, (int)nfin, (uint32_t)want, tmax >> 16, a.V, b, btoken, blogprob);
+        const uint32_t span = (phi >> 16) - (tmax >> 16);  // key values the pool spans
+        if (!a.out_idx && !ext && span < (uint32_t)kBlock)
+          binned = sample_binned<kBlock>(c, S, pool, (int)C, (int)nfin, (uint32_t)want, tmax >> 16, a.V, b, btoken,
+                                         blogprob);
+        else if (!a.out_idx && !ext && span < (uint32_t)kEBins)
+          binned = sample_binned<kEBins>(c, S, pool, (int)C, (int)nfin, (uint32_t)want, tmax >> 16, a.V, b, btoken,
+                                         blogprob);
       }
       if (binned) {
         nT = want;  // T is not materialised on this path
