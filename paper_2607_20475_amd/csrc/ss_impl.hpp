@@ -1405,13 +1405,23 @@ __device__ __forceinline__ int unit_of_group(const MSmem& S, int U, uint32_t f) 
 }
 
 // ---------------------------------------------------------------------------
-// One batch of candidate groups held in registers: kGS groups, kGPer per
-// thread (slot tid + kBlock m), with their group offsets (~0u: no group).
+// One batch of candidate groups held in registers: PER per thread (slot
+// tid + kBlock m), with their group offsets (~0u: no group).
 constexpr int kGPer = kGS / kBlock;
-struct GBatch {
-  uint32_t go[kGPer];
-  uint4 g[kGPer];
+template <int PER>
+struct GBatchT {
+  uint32_t go[PER];
+  uint4 g[PER];
 };
+using GBatch = GBatchT<kGPer>;
+// Groups per thread of a merge's candidate batches: six where one workgroup
+// per CU suffices and large-k rows then fit one batch (bf16 sampling, fp32
+// top-k), four where two workgroups must share a CU (verification, 64 + 1
+// rows per CU) or where six measured slower.
+template <int DT, int OP>
+constexpr int gather_per() {
+  return ((DT == SS_BF16 && sampling_op(OP)) || (DT == SS_F32 && OP == OP_TOPK)) ? 6 : kGPer;
+}
 
 // Slot -> group offset table of the row's candidate regions (TPU threads per
 // unit), when the row's groups fit it.
@@ -1429,15 +1439,15 @@ __device__ __forceinline__ void gather_table(const KArgs& a, MSmem& S, int U, ui
 
 // Issues the loads of the batch starting at group f0 (every load in flight,
 // nothing waits for them here).
-template <int DT>
+template <int DT, int PER>
 __device__ __forceinline__ void gather_issue(const KArgs& a, const MSmem& S, int row, int U, uint32_t NG, uint32_t f0,
-                                             GBatch& gb) {
+                                             GBatchT<PER>& gb) {
   const int tid = threadIdx.x;
   const uint4* rc = a.cand + (size_t)row * U * a.cap;
-  const uint32_t nb = f0 < NG ? min((uint32_t)kGS, NG - f0) : 0u;
+  const uint32_t nb = f0 < NG ? min((uint32_t)(PER * kBlock), NG - f0) : 0u;
   const bool table = NG <= (uint32_t)kGT;
 #pragma unroll
-  for (int m = 0; m < kGPer; ++m) {
+  for (int m = 0; m < PER; ++m) {
     const uint32_t q = (uint32_t)(tid + m * kBlock);
     gb.go[m] = 0xFFFFFFFFu;
     if (q < nb) {
@@ -1450,7 +1460,7 @@ __device__ __forceinline__ void gather_issue(const KArgs& a, const MSmem& S, int
     }
   }
 #pragma unroll
-  for (int m = 0; m < kGPer; ++m) gb.g[m] = rc[gb.go[m] == 0xFFFFFFFFu ? 0u : gb.go[m]];
+  for (int m = 0; m < PER; ++m) gb.g[m] = rc[gb.go[m] == 0xFFFFFFFFu ? 0u : gb.go[m]];
 }
 
 // ---------------------------------------------------------------------------
@@ -1891,10 +1901,10 @@ __device__ __forceinline__ int slow_select(const KArgs& a, const Ctx& c, MSmem& 
 // (`cur`) right after the unit records, so its loads overlap the patch
 // tables' copy.
 // Returns the element count (elements beyond a.pcap are counted, not stored).
-template <int DT>
+template <int DT, int PER>
 __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MSmem& S, uint32_t NG, bool patch,
                                                 uint64_t tc, uint2* pool, uint32_t& nvalid_out, uint32_t nfin,
-                                                GBatch& cur) {
+                                                GBatchT<PER>& cur) {
   constexpr int GE = DTT<DT>::GE;
   const int tid = threadIdx.x;
   const int U = a.U;
@@ -1908,12 +1918,13 @@ __device__ __forceinline__ uint32_t gather_pool(const KArgs& a, const Ctx& c, MS
   // Groups start at multiples of GE, so a group's ids share one bitmap word.
   const bool exact = a.V <= kPB;
   const uint32_t pwmax = (uint32_t)((a.V + 31) >> 5) - 1u;
-  constexpr int kPer = kGPer;
+  constexpr int kPer = PER;
+  constexpr uint32_t kBatch = (uint32_t)(PER * kBlock);
   static_assert(kPer * GE <= 32, "selection mask is 32 bits");
-  // batch f0 is processed while the loads of batch f0 + kGS are in flight
-  for (uint32_t f0 = 0; f0 < NG; f0 += (uint32_t)kGS) {
-    GBatch nxt;
-    if (f0 + (uint32_t)kGS < NG) gather_issue<DT>(a, S, c.row, U, NG, f0 + (uint32_t)kGS, nxt);
+  // batch f0 is processed while the loads of batch f0 + kBatch are in flight
+  for (uint32_t f0 = 0; f0 < NG; f0 += kBatch) {
+    GBatchT<PER> nxt;
+    if (f0 + kBatch < NG) gather_issue<DT>(a, S, c.row, U, NG, f0 + kBatch, nxt);
     const uint32_t(&go)[kPer] = cur.go;
     const uint4(&g)[kPer] = cur.g;
     // patched-id bitmap words (all reads issued before any is used)
@@ -2458,7 +2469,7 @@ __device__ __forceinline__ void merge_row(const KArgs& a, int row, MSmem& S, uin
   int want = c.k_eff;
   // the first batch of candidate groups is in flight from here on
   const bool fast = !empty && want > 0 && ovf == 0u;
-  GBatch cur;
+  GBatchT<gather_per<DT, OP>()> cur;
   if (fast) {
     gather_table(a, S, U, NG);
     gather_issue<DT>(a, S, row, U, NG, 0u, cur);
